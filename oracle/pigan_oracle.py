@@ -1,0 +1,399 @@
+"""Plain fp64 CPU oracle of the PI-GAN training step (arXiv 1910.13444).
+
+TEST INFRASTRUCTURE.  Only the tests, the package smoke check and the
+benchmark's CPU-baseline leg may import this module.  It shares no code with
+the HIP path and imports nothing from it.
+
+What is computed (all in float64, NumPy only, no blocking or fusion beyond what
+the definitions state):
+
+* Generator networks G(x, z) for Y = log k and for the head u: a tanh MLP on the
+  narrow input [x_1..x_d, z_1..z_nz] (one location plus the noise vector,
+  Sec. III.C "Single Node optimizations"), L tanh layers of width W, then a
+  linear scalar output.
+* Exact spatial jets (value, d/dx_i, d^2/dx_i^2) of the generator, carried
+  forward layer by layer by the chain rule.  The paper obtains the source term
+  f by applying the differential operator to the generator with automatic
+  differentiation (Sec. III.B.1, "Baseline Architecture"); the jets are the
+  exact derivatives that operation produces.
+* The Darcy residual r = -div(exp(Y) grad u) - f, from the Darcy equation
+  (Eq. 1) with the lognormal conductivity k = exp(Y) (Eq. 2), expanded as
+  -exp(Y) (grad Y . grad u + lap u) - f.
+* Sensor snapshots [Y at the Y sensors | u at the u sensors] per noise sample
+  and the discriminator, a tanh MLP on the whole snapshot (Sec. III.C).
+* WGAN critic losses per subdomain group, weighted by the subdomain weight
+  (Sec. III.B.1): L_D = w (mean D(fake) - mean D(real)),
+  L_adv = -w mean D(fake), L_pde = w lambda mean r^2, L_G = L_adv + L_pde.
+* Exact weight gradients of L_D (discriminator) and L_G (both generators) by
+  an explicit reverse pass.  Losses are means, so the step is additive over
+  sample chunks, the same identity the paper uses to fold subdomain losses into
+  its data-parallel gradient sum (Sec. III.D.1).
+
+Parameter packing (float32 master copy in, float64 internally):
+[W1 (W x in_dim, row-major), b1, W2 (W x W), b2, ..., W_L, b_L, w_out (W), b_out].
+
+Pins: see tests/test_oracle_*.py (closed forms, finite differences of the jets
+and of every weight gradient, torch.autograd in float64, invariants).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+F64 = np.float64
+
+
+# ----------------------------------------------------------------------------
+# parameter packing
+# ----------------------------------------------------------------------------
+
+def unpack(params, in_dim: int, L: int, W: int):
+    """Split a packed parameter vector into ([(W_l, b_l)], w_out, b_out)."""
+    p = np.asarray(params, dtype=F64).reshape(-1)
+    layers = []
+    off = 0
+    fan = in_dim
+    for _ in range(L):
+        Wl = p[off:off + W * fan].reshape(W, fan)
+        off += W * fan
+        bl = p[off:off + W]
+        off += W
+        layers.append((Wl, bl))
+        fan = W
+    w_out = p[off:off + W]
+    off += W
+    b_out = float(p[off])
+    off += 1
+    if off != p.size:
+        raise ValueError(f"parameter vector has {p.size} entries, shape needs {off}")
+    return layers, w_out, b_out
+
+
+def pack(layer_grads, gw_out, gb_out) -> np.ndarray:
+    parts = []
+    for gW, gb in layer_grads:
+        parts.append(np.asarray(gW, F64).reshape(-1))
+        parts.append(np.asarray(gb, F64).reshape(-1))
+    parts.append(np.asarray(gw_out, F64).reshape(-1))
+    parts.append(np.array([gb_out], F64))
+    return np.concatenate(parts)
+
+
+# ----------------------------------------------------------------------------
+# tanh and its derivatives with respect to the pre-activation a
+# ----------------------------------------------------------------------------
+
+def _tanh_derivs(a):
+    t = np.tanh(a)
+    s = 1.0 - t * t                  # dt/da
+    sp = -2.0 * t * s                # d2t/da2
+    spp = 2.0 * s * (3.0 * t * t - 1.0)   # d3t/da3
+    return t, s, sp, spp
+
+
+# ----------------------------------------------------------------------------
+# generator: forward jets and reverse pass
+# ----------------------------------------------------------------------------
+
+def gen_forward(params, shape, d: int, X, Z, order: int, keep: bool = False):
+    """Evaluate a generator and its spatial jets at rows (X[n], Z[n]).
+
+    X: [N, d] locations, Z: [N, n_z] noise (one row per evaluation point).
+    order 0: value only; 1: value and d/dx_i; 2: also d^2/dx_i^2 (pure second
+    derivatives only: the Laplacian needs no mixed terms).
+    Returns dict(y=[N], dy=[d, N] or None, ddy=[d, N] or None, cache).
+    """
+    in_dim, L, W = shape
+    layers, w_out, b_out = unpack(params, in_dim, L, W)
+    X = np.asarray(X, F64)
+    Z = np.asarray(Z, F64)
+    N = X.shape[0]
+    W1, b1 = layers[0]
+    # layer 1 on the concatenated input [x ; z]
+    a = X @ W1[:, :d].T + Z @ W1[:, d:].T + b1
+    # d a / d x_i is column i of W1; the second derivative of a is zero
+    da = [np.broadcast_to(W1[:, i], (N, W)).copy() for i in range(d)] if order >= 1 else []
+    dda = [np.zeros((N, W)) for _ in range(d)] if order >= 2 else []
+    cache = []
+    h = dh = ddh = None
+    for l in range(L):
+        if l > 0:
+            Wl, bl = layers[l]
+            a = h @ Wl.T + bl                      # bias enters the value only
+            da = [g @ Wl.T for g in dh]
+            dda = [g @ Wl.T for g in ddh]
+        t, s, sp, _ = _tanh_derivs(a)
+        if keep:
+            cache.append((a, da, dda, (h, dh, ddh)))
+        h = t
+        dh = [s * g for g in da]
+        ddh = [s * g2 + sp * g1 * g1 for g1, g2 in zip(da, dda)]
+    y = h @ w_out + b_out
+    out = dict(y=y,
+               dy=np.stack([g @ w_out for g in dh]) if order >= 1 else None,
+               ddy=np.stack([g @ w_out for g in ddh]) if order >= 2 else None)
+    if keep:
+        out["cache"] = cache
+        out["top"] = (h, dh, ddh)
+    return out
+
+
+def gen_backward(params, shape, d: int, X, Z, fwd, g_y, g_dy=None, g_ddy=None) -> np.ndarray:
+    """Reverse pass of gen_forward (keep=True) for output cotangents.
+
+    g_y: [N]; g_dy, g_ddy: [d, N] or None.  Returns the packed gradient (fp64).
+    """
+    in_dim, L, W = shape
+    layers, w_out, b_out = unpack(params, in_dim, L, W)
+    X = np.asarray(X, F64)
+    Z = np.asarray(Z, F64)
+    N = X.shape[0]
+    hL, dhL, ddhL = fwd["top"]
+    order = 0 if not dhL else (1 if not ddhL else 2)
+    g_y = np.asarray(g_y, F64)
+    g_dy = [np.asarray(g_dy[i], F64) for i in range(d)] if order >= 1 else []
+    g_ddy = [np.asarray(g_ddy[i], F64) for i in range(d)] if order >= 2 else []
+    # output layer y = w_out . h (+ b_out on the value only)
+    gw_out = hL.T @ g_y
+    for i in range(len(g_dy)):
+        gw_out = gw_out + dhL[i].T @ g_dy[i]
+    for i in range(len(g_ddy)):
+        gw_out = gw_out + ddhL[i].T @ g_ddy[i]
+    gb_out = g_y.sum()
+    gh = np.outer(g_y, w_out)
+    gdh = [np.outer(g, w_out) for g in g_dy]
+    gddh = [np.outer(g, w_out) for g in g_ddy]
+    grads = [None] * L
+    for l in reversed(range(L)):
+        a, da, dda, prev = fwd["cache"][l]
+        t, s, sp, spp = _tanh_derivs(a)
+        # h = t(a); h'_i = s a'_i; h''_i = s a''_i + s' a'_i^2
+        ga = s * gh
+        for i in range(len(gdh)):
+            ga = ga + sp * da[i] * gdh[i]
+        for i in range(len(gddh)):
+            ga = ga + (sp * dda[i] + spp * da[i] * da[i]) * gddh[i]
+        gda = []
+        for i in range(len(gdh)):
+            g = s * gdh[i]
+            if gddh:
+                g = g + 2.0 * sp * da[i] * gddh[i]
+            gda.append(g)
+        gdda = [s * g for g in gddh]
+        if l > 0:
+            Wl, _ = layers[l]
+            h, dh, ddh = prev
+            gW = ga.T @ h
+            for i in range(len(gda)):
+                gW = gW + gda[i].T @ dh[i]
+            for i in range(len(gdda)):
+                gW = gW + gdda[i].T @ ddh[i]
+            grads[l] = (gW, ga.sum(axis=0))
+            gh = ga @ Wl
+            gdh = [g @ Wl for g in gda]
+            gddh = [g @ Wl for g in gdda]
+        else:
+            gW1 = np.zeros((W, in_dim))
+            gW1[:, :d] = ga.T @ X
+            gW1[:, d:] = ga.T @ Z
+            for i in range(len(gda)):
+                gW1[:, i] += gda[i].sum(axis=0)   # a'_i = W1[:, i] for every row
+            grads[0] = (gW1, ga.sum(axis=0))
+    return pack(grads, gw_out, gb_out)
+
+
+# ----------------------------------------------------------------------------
+# plain tanh MLP (discriminator)
+# ----------------------------------------------------------------------------
+
+def mlp_forward(params, shape, V, keep: bool = False):
+    """D(v) = w_out . h_L + b_out with h_l = tanh(W_l h_{l-1} + b_l), h_0 = v."""
+    in_dim, L, W = shape
+    layers, w_out, b_out = unpack(params, in_dim, L, W)
+    h = np.asarray(V, F64)
+    hs = [h]
+    for Wl, bl in layers:
+        h = np.tanh(h @ Wl.T + bl)
+        hs.append(h)
+    y = h @ w_out + b_out
+    return (y, hs) if keep else y
+
+
+def mlp_backward(params, shape, hs, g_y, want_input_grad: bool = False):
+    in_dim, L, W = shape
+    layers, w_out, b_out = unpack(params, in_dim, L, W)
+    g_y = np.asarray(g_y, F64)
+    gw_out = hs[-1].T @ g_y
+    gb_out = g_y.sum()
+    gh = np.outer(g_y, w_out)
+    grads = [None] * L
+    for l in reversed(range(L)):
+        t = hs[l + 1]
+        ga = (1.0 - t * t) * gh
+        grads[l] = (ga.T @ hs[l], ga.sum(axis=0))
+        gh = ga @ layers[l][0]
+    g = pack(grads, gw_out, gb_out)
+    return (g, gh) if want_input_grad else g
+
+
+# ----------------------------------------------------------------------------
+# Darcy residual (Eq. 1 with k = exp(Y), Eq. 2)
+# ----------------------------------------------------------------------------
+
+def darcy_residual(Y, dY, dU, ddU, f):
+    """r = -div(exp(Y) grad u) - f = -exp(Y) (sum_i dY_i dU_i + sum_i ddU_i) - f."""
+    Y = np.asarray(Y, F64)
+    flux_div = (np.asarray(dY, F64) * np.asarray(dU, F64)).sum(axis=0) + np.asarray(ddU, F64).sum(axis=0)
+    return -np.exp(Y) * flux_div - np.asarray(f, F64)
+
+
+# ----------------------------------------------------------------------------
+# row builders: sensors are shared by all samples, collocation points are per
+# sample; every row carries its sample's noise vector
+# ----------------------------------------------------------------------------
+
+def sensor_rows(xs, z):
+    """Rows (s, j) for s in samples, j in sensors: X [S*n, d], Z [S*n, n_z]."""
+    xs = np.asarray(xs, F64)
+    z = np.asarray(z, F64)
+    S, n = z.shape[0], xs.shape[0]
+    return np.tile(xs, (S, 1)), np.repeat(z, n, axis=0)
+
+
+def colloc_rows(xc, z):
+    """Rows (s, p): xc [S, P, d] per sample, or [P, d] shared by every sample."""
+    xc = np.asarray(xc, F64)
+    z = np.asarray(z, F64)
+    S = z.shape[0]
+    if xc.ndim == 2:
+        xc = np.broadcast_to(xc, (S,) + xc.shape)
+    P = xc.shape[1]
+    return xc.reshape(S * P, -1), np.repeat(z, P, axis=0)
+
+
+def gen_jets(params, shape, d, z, x, order):
+    """Jets [1 + order*d, S, P] (value, d/dx_i, d^2/dx_i^2) at points x of each sample."""
+    X, Z = colloc_rows(x, z)
+    S = np.asarray(z).shape[0]
+    out = gen_forward(params, shape, d, X, Z, order)
+    P = X.shape[0] // S
+    comps = [out["y"][None]]
+    if order >= 1:
+        comps.append(out["dy"])
+    if order >= 2:
+        comps.append(out["ddy"])
+    return np.concatenate(comps, axis=0).reshape(-1, S, P)
+
+
+def snapshots(pY, pU, shape, d, xsY, xsU, z):
+    """Sensor snapshots [S, n_sY + n_sU] = [Y at Y sensors | u at u sensors]."""
+    S = np.asarray(z).shape[0]
+    XY, ZY = sensor_rows(xsY, z)
+    XU, ZU = sensor_rows(xsU, z)
+    yY = gen_forward(pY, shape, d, XY, ZY, 0)["y"].reshape(S, -1)
+    yU = gen_forward(pU, shape, d, XU, ZU, 0)["y"].reshape(S, -1)
+    return np.concatenate([yY, yU], axis=1)
+
+
+# ----------------------------------------------------------------------------
+# the training step
+# ----------------------------------------------------------------------------
+
+def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
+                     w=1.0, lambda_pde=1.0, chunk_S=None):
+    """One subdomain group's losses and gradients.
+
+    Returns dict(L_D, L_adv, L_pde, gY, gU, gD) with gradients of
+    L_D (discriminator weights) and of L_G = L_adv + L_pde (generator weights).
+    ``f`` is an [S, P] array.  Samples are processed in chunks of ``chunk_S``
+    (all at once by default); the result does not depend on the chunking.
+    """
+    z = np.asarray(z, F64)
+    xc = np.asarray(xc, F64)
+    f = np.asarray(f, F64)
+    real = np.asarray(real, F64)
+    S, P = xc.shape[0], xc.shape[1]
+    B = real.shape[0]
+    nY = np.asarray(xsY).shape[0]
+    chunk_S = S if not chunk_S else chunk_S
+
+    gY = np.zeros(np.asarray(pY).size)
+    gU = np.zeros(np.asarray(pU).size)
+    gD = np.zeros(np.asarray(pD).size)
+    sum_DF = 0.0
+    sum_r2 = 0.0
+
+    # real snapshots: dL_D/dD(real_b) = -w/B
+    DR, hsR = mlp_forward(pD, dshape, real, keep=True)
+    gD += mlp_backward(pD, dshape, hsR, np.full(B, -w / B))
+    sum_DR = DR.sum()
+
+    for s0 in range(0, S, chunk_S):
+        sl = slice(s0, min(S, s0 + chunk_S))
+        zc = z[sl]
+        Sc = zc.shape[0]
+        # --- generators at the sensors (value only) -> fake snapshots
+        XY, ZY = sensor_rows(xsY, zc)
+        XU, ZU = sensor_rows(xsU, zc)
+        fY_s = gen_forward(pY, gshape, d, XY, ZY, 0, keep=True)
+        fU_s = gen_forward(pU, gshape, d, XU, ZU, 0, keep=True)
+        F = np.concatenate([fY_s["y"].reshape(Sc, -1), fU_s["y"].reshape(Sc, -1)], axis=1)
+        # --- generators at the collocation points with jets
+        XC, ZC = colloc_rows(xc[sl], zc)
+        jY = gen_forward(pY, gshape, d, XC, ZC, 1, keep=True)
+        jU = gen_forward(pU, gshape, d, XC, ZC, 2, keep=True)
+        fc = f[sl].reshape(-1)
+        r = darcy_residual(jY["y"], jY["dy"], jU["dy"], jU["ddy"], fc)
+        sum_r2 += float((r * r).sum())
+        # --- discriminator on the fake snapshots: dL_D/dD(F_s) = w/S
+        DF, hsF = mlp_forward(pD, dshape, F, keep=True)
+        sum_DF += float(DF.sum())
+        gDc, gF = mlp_backward(pD, dshape, hsF, np.full(Sc, w / S), want_input_grad=True)
+        gD += gDc
+        # L_adv = -w mean D(F): its snapshot cotangent is the negated L_D one
+        gF = -gF
+        # --- residual cotangents: dL_pde/dr = 2 w lambda r / (S P)
+        q = 2.0 * w * lambda_pde * r / (S * P)
+        eY = np.exp(jY["y"])
+        g_Yval = q * (r + fc)                       # dr/dY = -exp(Y)(...) = r + f
+        g_Ydy = np.stack([-q * eY * jU["dy"][i] for i in range(d)])
+        g_Udy = np.stack([-q * eY * jY["dy"][i] for i in range(d)])
+        g_Uddy = np.stack([-q * eY for _ in range(d)])
+        g_Uval = np.zeros_like(r)                   # u itself does not enter r
+        # --- reverse passes through both generators
+        gY += gen_backward(pY, gshape, d, XY, ZY, fY_s, gF[:, :nY].reshape(-1))
+        gU += gen_backward(pU, gshape, d, XU, ZU, fU_s, gF[:, nY:].reshape(-1))
+        gY += gen_backward(pY, gshape, d, XC, ZC, jY, g_Yval, g_Ydy)
+        gU += gen_backward(pU, gshape, d, XC, ZC, jU, g_Uval, g_Udy, g_Uddy)
+
+    L_D = w * (sum_DF / S - sum_DR / B)
+    L_adv = -w * sum_DF / S
+    L_pde = w * lambda_pde * sum_r2 / (S * P)
+    return dict(L_D=L_D, L_adv=L_adv, L_pde=L_pde, gY=gY, gU=gU, gD=gD)
+
+
+def train_step(wl, inp, real, lambda_pde=None, chunk_S=None):
+    """All groups of a workload.  ``inp`` is an inputs.StepInputs-like object,
+    ``real`` the real snapshots [G, B_r, n_in].  Returns dict of stacked arrays:
+    loss [G, 3] (L_D, L_adv, L_pde), gY [G, nY], gU [G, nU], gD [G, nD]."""
+    lam = wl.lambda_pde if lambda_pde is None else lambda_pde
+    gshape = (wl.d + wl.n_z, wl.L, wl.W)
+    dshape = (wl.n_sY + wl.n_sU, wl.L_D, wl.W_D)
+    G = inp.z.shape[0]
+    S, P = inp.xc.shape[1], inp.xc.shape[2]
+    outs = []
+    for g in range(G):
+        f = inp.f[g] if inp.f is not None else np.full((S, P), inp.f_const)
+        outs.append(train_step_group(gshape, dshape, wl.d, inp.pY[g], inp.pU[g], inp.pD[g],
+                                     inp.z[g], inp.xc[g], inp.xsY[g], inp.xsU[g], f, real[g],
+                                     w=float(inp.w_group[g]), lambda_pde=lam, chunk_S=chunk_S))
+    return dict(loss=np.array([[o["L_D"], o["L_adv"], o["L_pde"]] for o in outs]),
+                gY=np.stack([o["gY"] for o in outs]),
+                gU=np.stack([o["gU"] for o in outs]),
+                gD=np.stack([o["gD"] for o in outs]))
+
+
+def real_snapshots(wl, inp):
+    """Teacher snapshots [G, B_r, n_in] from the teacher weights and noise z'."""
+    gshape = (wl.d + wl.n_z, wl.L, wl.W)
+    return np.stack([snapshots(inp.tY[g], inp.tU[g], gshape, wl.d, inp.xsY[g], inp.xsU[g],
+                               inp.z_teach[g]) for g in range(inp.z.shape[0])])

@@ -1,0 +1,96 @@
+"""Workload shapes for the PI-GAN training step.
+
+Each workload fixes the two generator MLPs (log-conductivity Y and head u), the
+discriminator MLP, the number of noise samples S, collocation points per sample
+P, the Y/u sensor counts and the number of independent subdomain groups G.
+
+The shapes follow the paper's problem statement: the generator takes one
+spatial location plus the noise vector as a narrow input and the sensors of a
+realisation become rows of a larger batch (Sec. III.C, "Single Node
+optimizations"); the discriminator sees a whole sensor snapshot as one input
+(same section); subdomains each own a discriminator and their loss terms are
+weighted by 1/(levels * subdomains in the level) (Sec. III.B.1).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, replace
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    dtype: str          # storage / MFMA operand type: "fp32", "bf16" or "fp16"
+    G: int              # independent subdomain groups
+    d: int              # spatial dimensions
+    n_z: int            # noise dimension
+    L: int              # generator hidden tanh layers
+    W: int              # generator width
+    S: int              # noise samples per step
+    P: int              # collocation points per sample
+    n_sY: int           # log-conductivity sensors
+    n_sU: int           # head sensors
+    L_D: int            # discriminator hidden tanh layers
+    W_D: int            # discriminator width
+    B_r: int            # real snapshots per step
+    f_const: float      # source term used when no f array is given
+    lambda_pde: float = 1.0
+    seed: int = 1910
+
+    @property
+    def n_in(self) -> int:
+        return self.n_sY + self.n_sU
+
+    @property
+    def in_dim(self) -> int:
+        return self.d + self.n_z
+
+    @property
+    def c_Y(self) -> int:
+        return 1 + self.d
+
+    @property
+    def c_U(self) -> int:
+        return 1 + 2 * self.d
+
+    @property
+    def w_group(self) -> float:
+        # one level of G subdomains: weight 1/(levels * subdomains)
+        return 1.0 / self.G
+
+    def gen_shape(self) -> tuple[int, int, int]:
+        return (self.in_dim, self.L, self.W)
+
+    def disc_shape(self) -> tuple[int, int, int]:
+        return (self.n_in, self.L_D, self.W_D)
+
+    def with_(self, **kw) -> "Workload":
+        return replace(self, **kw)
+
+
+def n_params(in_dim: int, L: int, W: int) -> int:
+    """Parameter count of a tanh MLP packed as
+    [W1 (W x in_dim, row-major), b1, W2 (W x W), b2, ..., W_L, b_L, w_out (W), b_out]."""
+    return W * in_dim + W + (L - 1) * (W * W + W) + W + 1
+
+
+C1 = Workload("darcy1d_toy_fp32", "fp32", G=1, d=1, n_z=4, L=3, W=32, S=64, P=32,
+              n_sY=8, n_sU=8, L_D=2, W_D=32, B_r=64, f_const=1.0, seed=1911)
+C2 = Workload("darcy2d_w128_bf16", "bf16", G=1, d=2, n_z=20, L=4, W=128, S=256, P=1024,
+              n_sY=200, n_sU=200, L_D=3, W_D=256, B_r=256, f_const=0.0, seed=1912)
+C3 = Workload("darcy2d_sd1000_w512_bf16", "bf16", G=1, d=2, n_z=64, L=6, W=512, S=512, P=4096,
+              n_sY=1000, n_sU=1000, L_D=4, W_D=1024, B_r=512, f_const=0.0, seed=1913)
+C4 = Workload("subdomains16_w256_bf16", "bf16", G=16, d=2, n_z=32, L=4, W=256, S=128, P=1024,
+              n_sY=125, n_sU=125, L_D=3, W_D=512, B_r=128, f_const=0.0, seed=1914)
+C5 = Workload("bigstep_w1024_disc2048_bf16", "bf16", G=1, d=2, n_z=128, L=6, W=1024, S=1024,
+              P=2048, n_sY=4096, n_sU=4096, L_D=5, W_D=2048, B_r=1024, f_const=0.0, seed=1915)
+C5H = C5.with_(name="bigstep_w1024_disc2048_fp16", dtype="fp16")
+
+WORKLOADS = {w.name: w for w in (C1, C2, C3, C4, C5, C5H)}
+ALIASES = {"c1": C1, "c2": C2, "c3": C3, "c4": C4, "c5": C5, "c5h": C5H}
+
+
+def get(name: str) -> Workload:
+    key = name.lower()
+    if key in ALIASES:
+        return ALIASES[key]
+    return WORKLOADS[name]
