@@ -1,0 +1,209 @@
+/*
+ * pigan.h — C ABI of the MI355X PI-GAN training-step library (libpigan.so).
+ *
+ * The library evaluates the physics-informed GAN of arXiv 1910.13444 on one
+ * AMD MI355X (gfx950): tanh-MLP generators for the log-conductivity Y = log k
+ * and the hydraulic head u, both taking one location x plus the noise vector z
+ * as a narrow input (Sec. III.C, "Single Node optimizations"); first and second
+ * spatial derivatives carried through every layer so that the Darcy residual
+ * -div(exp(Y) grad u) - f can be formed (Eq. 1 with k = exp(Y), Eq. 2;
+ * the paper induces this f-network by automatic differentiation,
+ * Sec. III.B.1); a tanh-MLP discriminator on whole sensor snapshots
+ * (Sec. III.C); WGAN critic losses weighted per subdomain (Sec. III.B.1);
+ * and fp32 gradients of every weight with half-precision activations
+ * (Sec. III.C, mixed precision).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every pointer argument is a DEVICE pointer owned by the caller unless
+ *    stated otherwise.  The library never allocates device memory, never frees
+ *    caller memory and keeps no state between calls besides a thread-local
+ *    error string (and, when enabled, the profiling record).
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Calls enqueue work
+ *    on it and return; outputs are valid after the caller synchronises it.
+ *  - Argument checks run on the host before anything is enqueued; a non-OK
+ *    status means nothing was launched (except PIGAN_EDEVICE, which reports a
+ *    HIP launch/runtime error).  pigan_last_error() describes the failure.
+ *  - MLP parameters are fp32, packed per group as
+ *      [W1 (width x in_dim, row-major), b1, W2 (width x width), b2, ...,
+ *       W_L, b_L, w_out (width), b_out]
+ *    and groups are stacked contiguously: params[g * n_params + i].
+ *  - Generator input order is [x_1..x_d, z_1..z_nz] (in_dim = d + n_z).
+ *  - The arithmetic type (pigan_dtype) selects the storage and matrix-core
+ *    operand type of the hidden layers; accumulation, the first generator
+ *    layer, tanh and its derivatives, the residual, losses and gradients are
+ *    always fp32.
+ *  - Results are deterministic run to run (fixed-order reductions, no float
+ *    atomics).
+ */
+#ifndef PIGAN_H
+#define PIGAN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PIGAN_OK = 0,
+  PIGAN_EINVAL = 1,      /* null pointer, non-positive size, inconsistent shapes */
+  PIGAN_ENOTSUP = 2,     /* valid request the library does not implement */
+  PIGAN_EWORKSPACE = 3,  /* workspace missing or smaller than required */
+  PIGAN_EDEVICE = 4      /* HIP launch or runtime error */
+} pigan_status;
+
+typedef enum {
+  PIGAN_FP32 = 0,        /* fp32 storage, fp32 matrix cores */
+  PIGAN_BF16 = 1,        /* bf16 storage (round-to-nearest-even), fp32 accumulate */
+  PIGAN_FP16 = 2         /* fp16 storage (round-to-nearest-even), fp32 accumulate */
+} pigan_dtype;
+
+/* Shape of one tanh MLP: n_hidden tanh layers of `width` units on `in_dim`
+ * inputs, then a linear scalar output.  `n_groups` independent copies
+ * (subdomains) share the shape.  width must be a multiple of 32 and at most
+ * 4096; n_hidden >= 1; in_dim >= 1. */
+typedef struct {
+  int32_t n_groups;
+  int32_t in_dim;
+  int32_t n_hidden;
+  int32_t width;
+} pigan_mlp;
+
+/* Number of fp32 parameters of one group of `net` (see packing above). */
+int64_t pigan_mlp_n_params(const pigan_mlp* net);
+
+/*
+ * pigan_gen_forward — generator values and spatial jets (Sec. III.B.1: the
+ * generator represents log k and u from a location and a noise vector; the
+ * differential operator is applied to it analytically).
+ *
+ *   net    : generator shape; net->in_dim must equal d + n_z.
+ *   params : [G, n_params] fp32.
+ *   d      : spatial dimensions, 1..3.
+ *   z      : [G, S, n_z] fp32 noise vectors.
+ *   x      : [G, S, P, d] fp32 locations, or [G, P, d] when x_shared != 0
+ *            (the same P locations for every sample).
+ *   order  : 0 value only; 1 adds d/dx_i; 2 adds d^2/dx_i^2 (no mixed terms).
+ *   jet    : [G, 1 + order*d, S, P] fp32 output, components in the order
+ *            value, d/dx_1..d/dx_d, d^2/dx_1^2..d^2/dx_d^2.
+ *   ws     : device workspace of at least pigan_gen_forward_workspace() bytes,
+ *            256-byte aligned.
+ */
+size_t pigan_gen_forward_workspace(const pigan_mlp* net, int32_t d, int32_t S, int32_t P,
+                                   int32_t order, pigan_dtype dt);
+pigan_status pigan_gen_forward(const pigan_mlp* net, const float* params, int32_t d,
+                               const float* z, const float* x, int32_t x_shared,
+                               int32_t S, int32_t P, int32_t order, pigan_dtype dt,
+                               float* jet, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * pigan_pde_residual — Darcy residual r = -div(exp(Y) grad u) - f
+ * = -exp(Y) (sum_i dY/dx_i du/dx_i + sum_i d^2u/dx_i^2) - f  (Eq. 1, Eq. 2).
+ * The sign convention puts the operator on the left with a minus sign, so
+ * f here is the negative of the paper's right-hand side (the paper's data use
+ * f = 0).
+ *
+ *   jetY : [G, 1 + d, M] fp32 (value, d/dx_i) — layout of pigan_gen_forward
+ *          with order 1 and M = S*P.
+ *   jetU : [G, 1 + 2d, M] fp32 (value unused, d/dx_i, d^2/dx_i^2).
+ *   f    : [G, M] fp32, or NULL to use the constant f_const everywhere.
+ *   r    : [G, M] fp32 output.
+ */
+pigan_status pigan_pde_residual(int32_t d, int32_t G, int64_t M, const float* jetY,
+                                const float* jetU, const float* f, float f_const, float* r,
+                                void* stream);
+
+/*
+ * pigan_disc_forward — discriminator scores D(v) = w_out . h_L + b_out,
+ * h_l = tanh(W_l h_{l-1} + b_l), h_0 = v, one whole snapshot per row
+ * (Sec. III.C: the discriminator receives all sensors of its subdomain as a
+ * single input).
+ *
+ *   snap  : [G, B, in_dim] fp32 snapshots.
+ *   score : [G, B] fp32 output.
+ */
+size_t pigan_disc_forward_workspace(const pigan_mlp* net, int32_t B, pigan_dtype dt);
+pigan_status pigan_disc_forward(const pigan_mlp* net, const float* params, const float* snap,
+                                int32_t B, pigan_dtype dt, float* score, void* ws,
+                                size_t ws_bytes, void* stream);
+
+/*
+ * One training step of the PI-GAN (Sec. III.B.1 and Sec. III.C).
+ *
+ * Per group g with weight w_g (the paper weights a subdomain's critic by
+ * 1/(levels * subdomains in its level)):
+ *   fake snapshot F_s = [Y(xsY_j, z_s)]_j || [u(xsU_j, z_s)]_j,  s < S
+ *   r_{s,p}         = -exp(Y)(grad Y . grad u + lap u) - f  at (xc_{s,p}, z_s)
+ *   L_D   = w_g (mean_s D(F_s) - mean_b D(real_b))
+ *   L_adv = -w_g mean_s D(F_s)
+ *   L_pde = w_g lambda_pde mean_{s,p} r^2
+ * Outputs: gD = dL_D/d(disc params), gY = d(L_adv + L_pde)/d(Y params),
+ * gU = d(L_adv + L_pde)/d(u params).  Gradients are OVERWRITTEN (not
+ * accumulated).  The step is exactly additive over noise samples, so the
+ * library processes samples in chunks of chunk_S (0 = the largest chunk whose
+ * workspace stays within 64 GiB); the result does not depend on the chunking
+ * up to fp32 summation order.
+ */
+typedef struct {
+  pigan_mlp genY, genU, disc;  /* equal n_groups; genY/genU in_dim = d + n_z;
+                                  disc in_dim = n_sY + n_sU */
+  int32_t d, n_z;              /* d in 1..3 */
+  int32_t S, P;                /* noise samples, collocation points per sample */
+  int32_t n_sY, n_sU;          /* Y and u sensors per group (>= 1 each) */
+  int32_t B_r;                 /* real snapshots per group */
+  int32_t chunk_S;             /* samples per chunk, 0 = automatic */
+  pigan_dtype dt;
+  float lambda_pde;            /* weight of the residual penalty (>= 0) */
+  float lambda_gp;             /* gradient-penalty weight: must be 0 (not implemented) */
+  float loss_scale;            /* static loss scale (> 0; 1 unless fp16) */
+} pigan_step_desc;
+
+size_t pigan_workspace_bytes(const pigan_step_desc* s);
+
+/*
+ *   pY, pU, pD : [G, n_params] fp32 master weights.
+ *   z   : [G, S, n_z]; xc : [G, S, P, d] collocation points (per sample);
+ *   xsY : [G, n_sY, d], xsU : [G, n_sU, d] sensor locations (shared by all
+ *         samples); f : [G, S, P] or NULL (then f_const);
+ *   real: [G, B_r, n_sY + n_sU] real snapshots; w_group : [G] or NULL (= 1).
+ *   gY, gU, gD : [G, n_params] fp32 outputs.
+ *   loss : [G, 3] fp32 output (L_D, L_adv, L_pde).
+ *   nonfinite : one device int32, set to 1 when any gradient or loss is not
+ *               finite (the caller's loss-scaling logic skips such a step),
+ *               else 0.
+ */
+pigan_status pigan_train_step_grads(const pigan_step_desc* s, const float* pY, const float* pU,
+                                    const float* pD, const float* z, const float* xc,
+                                    const float* xsY, const float* xsU, const float* f,
+                                    float f_const, const float* real, const float* w_group,
+                                    float* gY, float* gU, float* gD, float* loss,
+                                    int32_t* nonfinite, void* ws, size_t ws_bytes, void* stream);
+
+/* Thread-local description of the last non-OK status ("" if none). */
+const char* pigan_last_error(void);
+
+/*
+ * Kernel timing (instrumentation, not part of the method).  While enabled,
+ * every library kernel launch is bracketed by HIP events recorded on the
+ * caller's stream, and its algorithmic work is recorded with it.
+ * pigan_profile_read() must be called after the caller has synchronised the
+ * stream; it aggregates per kernel family and resets the record.
+ */
+typedef struct {
+  char name[48];          /* kernel family, e.g. "gemm_fwd" */
+  int64_t launches;
+  double total_ms;        /* sum of event-measured durations */
+  double flops;           /* algorithmic matrix FLOPs of all launches (2*M*N*K) */
+  double bytes;           /* algorithmic HBM bytes of all launches */
+} pigan_kernel_stat;
+
+pigan_status pigan_profile_enable(int32_t on);
+pigan_status pigan_profile_read(pigan_kernel_stat* out, int32_t max_entries, int32_t* n_entries);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PIGAN_H */

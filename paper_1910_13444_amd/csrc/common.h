@@ -1,0 +1,135 @@
+// Internal declarations shared by the HIP kernels and the host orchestration
+// of libpigan.so.  gfx950 (CDNA4) only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "pigan.h"
+
+namespace pigan {
+
+typedef __bf16 bf16;
+typedef _Float16 f16;
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+// ---------------------------------------------------------------------------
+// Element traits.  A matrix-core "chunk" covers 16 values of the contraction
+// index: every lane holds 8 consecutive values of its row (16 bytes in bf16 /
+// fp16, 32 bytes in fp32).  The same (lane, element) -> k assignment is used
+// for both operands, so any k order inside a chunk is consistent.
+// ---------------------------------------------------------------------------
+template <class T> struct Elem;
+
+template <> struct Elem<float> {
+  typedef f32x8 frag;
+  static __device__ __forceinline__ float to_f(float v) { return v; }
+  static __device__ __forceinline__ float from_f(float v) { return v; }
+  static __device__ __forceinline__ void mma(f32x16& acc, const frag& a, const frag& b) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[q], b[q], acc, 0, 0, 0);
+  }
+};
+
+template <> struct Elem<bf16> {
+  typedef bf16x8 frag;
+  static __device__ __forceinline__ float to_f(bf16 v) { return (float)v; }
+  static __device__ __forceinline__ bf16 from_f(float v) { return (bf16)v; }
+  static __device__ __forceinline__ void mma(f32x16& acc, const frag& a, const frag& b) {
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+  }
+};
+
+template <> struct Elem<f16> {
+  typedef f16x8 frag;
+  static __device__ __forceinline__ float to_f(f16 v) { return (float)v; }
+  static __device__ __forceinline__ f16 from_f(float v) { return (f16)v; }
+  static __device__ __forceinline__ void mma(f32x16& acc, const frag& a, const frag& b) {
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, acc, 0, 0, 0);
+  }
+};
+
+// ---------------------------------------------------------------------------
+// tanh and its derivatives with respect to the pre-activation a:
+//   t = tanh(a), s = dt/da = 1 - t^2, s' = -2 t s, s'' = 2 s (3 t^2 - 1).
+// With e = exp(-2|a|) and m = e - 1 (= expm1(-2|a|)):
+//   |t| = -m / (2 + m),  s = 4 e / (1 + e)^2.
+// s is formed from e directly, so it keeps full relative accuracy for
+// saturated units where 1 - t^2 would cancel; for |a| < 1/8 the factor m is
+// taken from its Taylor series (8 terms, truncation below 1e-9 relative) so
+// that t keeps full relative accuracy near zero.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void tanh_ts(float a, float& t, float& s) {
+  const float x = -2.0f * fabsf(a);
+  const float e = expf(x);
+  // expm1(x) = x (1 + x/2 (1 + x/3 (1 + x/4 (... (1 + x/8)))))
+  float p = 1.0f + x * (1.0f / 8.0f);
+  p = 1.0f + x * (1.0f / 7.0f) * p;
+  p = 1.0f + x * (1.0f / 6.0f) * p;
+  p = 1.0f + x * (1.0f / 5.0f) * p;
+  p = 1.0f + x * (1.0f / 4.0f) * p;
+  p = 1.0f + x * (1.0f / 3.0f) * p;
+  p = 1.0f + x * 0.5f * p;
+  const float m = (x > -0.25f) ? x * p : e - 1.0f;
+  const float ta = -m * __builtin_amdgcn_rcpf(2.0f + m);
+  t = copysignf(ta, a);
+  const float den = 1.0f + e;
+  s = 4.0f * e * __builtin_amdgcn_rcpf(den * den);
+}
+
+// ---------------------------------------------------------------------------
+// Launch descriptors (host side builds them, kernels read them by value).
+// Row layout of one network's activations for a chunk of samples:
+//   rows [0, n_sen)                       sensor points (value stream only)
+//   rows [n_sen + k*n_col, n_sen+(k+1)*n_col)  collocation stream k
+// with stream order value, d/dx_1..d/dx_d, d^2/dx_1^2..d^2/dx_d^2.  The value
+// rows are therefore contiguous: [0, n_sen + n_col).
+// ---------------------------------------------------------------------------
+struct Seg {
+  int64_t n_points;   // points in the segment
+  int64_t row0;       // row of stream 0, point 0
+  int64_t plane;      // row distance between streams of one point
+};
+
+enum EpiMode { EPI_FWD = 0, EPI_BWD = 1, EPI_DF = 2 };
+
+template <class T> struct NtArgs {
+  const T* X;  int64_t x_g;  int64_t ldx;  // A operand rows (activations)
+  const T* Wm; int64_t w_g;  int64_t ldw;  // B operand rows: [N x K] row-major
+  const float* bias; int64_t b_g;         // EPI_FWD: bias on stream 0 (may be null)
+  T* out_a;  T* out_h; int64_t o_g; int64_t ldo;  // EPI_FWD: pre-activation / activation
+  const T* aprev;                          // EPI_BWD: saved pre-activation of the layer below
+  T* out_da;                               // EPI_BWD: its pre-activation cotangent
+  float* seedY; float* seedU; int64_t sY_g; int64_t sU_g;  // EPI_DF outputs
+  int32_t nY; int32_t nU; float df_sign;
+  Seg seg;
+  int32_t N, K;
+};
+
+// per-kernel-family profiling hooks (host)
+void prof_begin(hipStream_t st, const char* name, double flops, double bytes);
+void prof_end(hipStream_t st);
+
+// ---------------------------------------------------------------------------
+// Host launchers (defined in the .hip files)
+// ---------------------------------------------------------------------------
+template <class T>
+hipError_t launch_gemm_nt(int epi, int nd1, int nd2, const NtArgs<T>& a, int G, hipStream_t st);
+
+template <class T>
+hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int64_t h_g, int64_t ldh,
+                          int64_t R, int64_t n_value, int N, int J, float* partial, float* pdb,
+                          int n_split, int64_t rows_per_split, int G, hipStream_t st);
+
+hipError_t launch_reduce_dw(const float* partial, const float* pdb, int n_split, int N, int Jpad,
+                            int J, float* gW, float* gb, int64_t g_g, int accumulate, float scale,
+                            int32_t* nonfinite, int G, hipStream_t st);
+
+void dw_split_plan(int64_t R, int N, int J, int elem_bytes, int G, int* n_split, int64_t* rows_per_split);
+
+}  // namespace pigan

@@ -1,0 +1,960 @@
+// Host side of libpigan.so: argument checks, workspace planning, the chunked
+// orchestration of one PI-GAN training step and the C entry points declared
+// in include/pigan.h.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "common.h"
+#include "pointwise.h"
+
+namespace pigan {
+
+// ---------------------------------------------------------------------------
+// errors
+// ---------------------------------------------------------------------------
+static thread_local std::string g_err;
+
+static pigan_status fail(pigan_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define HIP_TRY(expr)                                                                       \
+  do {                                                                                      \
+    hipError_t e_ = (expr);                                                                 \
+    if (e_ != hipSuccess) return fail(PIGAN_EDEVICE, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+// ---------------------------------------------------------------------------
+// kernel timing record (enabled by pigan_profile_enable)
+// ---------------------------------------------------------------------------
+struct ProfRec {
+  std::string name;
+  hipEvent_t a, b;
+  double flops, bytes;
+};
+static std::mutex g_pm;
+static bool g_prof = false;
+static std::vector<ProfRec> g_recs;
+static std::vector<hipEvent_t> g_pool;
+
+static hipEvent_t pool_get() {
+  if (!g_pool.empty()) {
+    hipEvent_t e = g_pool.back();
+    g_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+void prof_begin(hipStream_t st, const char* name, double flops, double bytes) {
+  std::lock_guard<std::mutex> lk(g_pm);
+  if (!g_prof) return;
+  ProfRec r{name, pool_get(), pool_get(), flops, bytes};
+  if (r.a) (void)hipEventRecord(r.a, st);
+  g_recs.push_back(r);
+}
+
+void prof_end(hipStream_t st) {
+  std::lock_guard<std::mutex> lk(g_pm);
+  if (!g_prof || g_recs.empty()) return;
+  if (g_recs.back().b) (void)hipEventRecord(g_recs.back().b, st);
+}
+
+struct ProfScope {
+  hipStream_t st;
+  ProfScope(hipStream_t s, const char* name, double flops, double bytes) : st(s) {
+    prof_begin(s, name, flops, bytes);
+  }
+  ~ProfScope() { prof_end(st); }
+};
+
+// ---------------------------------------------------------------------------
+// shapes and workspace carving
+// ---------------------------------------------------------------------------
+static inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+struct Carver {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    off = (size_t)round_up((int64_t)off, 256);
+    const size_t o = off;
+    off += bytes;
+    return o;
+  }
+};
+
+static size_t esize(pigan_dtype dt) { return dt == PIGAN_FP32 ? 4 : 2; }
+
+struct MlpOff {  // offsets (in floats) of one group's packed parameters
+  int in_dim, L, W;
+  int64_t n;
+  std::vector<int64_t> w, b;
+  int64_t wout;
+  void init(int in_dim_, int L_, int W_) {
+    in_dim = in_dim_;
+    L = L_;
+    W = W_;
+    w.assign(L + 1, 0);
+    b.assign(L + 1, 0);
+    int64_t off = 0;
+    int fan = in_dim;
+    for (int l = 1; l <= L; ++l) {
+      w[l] = off;
+      off += (int64_t)W * fan;
+      b[l] = off;
+      off += W;
+      fan = W;
+    }
+    wout = off;
+    n = off + W + 1;
+  }
+};
+
+static bool width_ok(int W) {
+  if (W < 32 || W > 4096 || W % 32) return false;
+  return W <= 256 ? (256 % W == 0) : (W % 256 == 0);
+}
+
+static pigan_status check_mlp(const pigan_mlp* m, const char* what) {
+  if (!m) return fail(PIGAN_EINVAL, "%s: null shape", what);
+  if (m->n_groups < 1 || m->n_groups > 65535) return fail(PIGAN_EINVAL, "%s: n_groups=%d out of [1,65535]", what, m->n_groups);
+  if (m->in_dim < 1) return fail(PIGAN_EINVAL, "%s: in_dim=%d must be >= 1", what, m->in_dim);
+  if (m->n_hidden < 1) return fail(PIGAN_EINVAL, "%s: n_hidden=%d must be >= 1", what, m->n_hidden);
+  if (m->width < 1) return fail(PIGAN_EINVAL, "%s: width=%d must be >= 1", what, m->width);
+  if (!width_ok(m->width))
+    return fail(PIGAN_ENOTSUP, "%s: width=%d unsupported (multiple of 32 dividing 256, or multiple of 256 up to 4096)",
+                what, m->width);
+  return PIGAN_OK;
+}
+
+static pigan_status check_dtype(pigan_dtype dt) {
+  if (dt != PIGAN_FP32 && dt != PIGAN_BF16 && dt != PIGAN_FP16) return fail(PIGAN_EINVAL, "unknown dtype %d", (int)dt);
+  return PIGAN_OK;
+}
+
+// points per block of the output-layer reverse pass
+static int64_t ob_ppb(int64_t n_points) {
+  int64_t p = (n_points + 511) / 512;
+  return p < 8 ? 8 : p;
+}
+
+// ---------------------------------------------------------------------------
+// training-step plan
+// ---------------------------------------------------------------------------
+struct NetBuf {
+  MlpOff off;
+  int nd1 = 0, nd2 = 0, n_s = 0;
+  int64_t n_sen = 0, n_col = 0;
+  int64_t R = 0;     // planned rows per group (group stride of every activation buffer)
+  int64_t rows = 0;  // rows used by the current chunk (<= R)
+  std::vector<size_t> A, H;  // index 1..L
+  size_t dA[2] = {0, 0};
+  size_t jet = 0, gbar = 0, zp = 0, wc = 0, wcT = 0, fb = 0, ob = 0;
+  int64_t ob_slots = 0;
+  int64_t ppb_sen = 8, ppb_col = 8;
+};
+
+struct DiscBuf {
+  MlpOff off;
+  int Kp = 0;
+  int64_t Bmax = 0;
+  std::vector<size_t> A, H;
+  size_t X0 = 0, dA[2] = {0, 0}, score = 0, seed = 0, w1 = 0, w1T = 0, wc = 0, wcT = 0, ob = 0;
+  int64_t ob_slots = 0, ppb = 8;
+};
+
+struct StepPlan {
+  int G = 1, Sc = 1;
+  size_t es = 4;
+  NetBuf Y, U;
+  DiscBuf D;
+  size_t dwp = 0, dwdb = 0, rpart = 0, acc = 0;
+  int64_t dwp_floats = 0, dwdb_floats = 0;
+  int rblocks = 0;
+  size_t total = 0;
+};
+
+static void plan_net(Carver& cv, NetBuf& nb, const pigan_mlp& m, int d, int nd2, int n_s, int Sc, int P, size_t es,
+                     int G) {
+  nb.off.init(m.in_dim, m.n_hidden, m.width);
+  nb.nd1 = d;
+  nb.nd2 = nd2;
+  nb.n_s = n_s;
+  nb.n_sen = (int64_t)Sc * n_s;
+  nb.n_col = (int64_t)Sc * P;
+  const int C = 1 + nb.nd1 + nb.nd2;
+  nb.R = nb.n_sen + C * nb.n_col;
+  nb.rows = nb.R;
+  const int L = m.n_hidden, W = m.width;
+  const size_t act = (size_t)nb.R * W * es * G;
+  nb.A.assign(L + 1, 0);
+  nb.H.assign(L + 1, 0);
+  for (int l = 1; l <= L; ++l) {
+    nb.A[l] = cv.take(act);
+    nb.H[l] = cv.take(act);
+  }
+  nb.dA[0] = cv.take(act);
+  nb.dA[1] = cv.take(act);
+  nb.jet = cv.take((size_t)nb.R * 4 * G);
+  nb.gbar = cv.take((size_t)nb.R * 4 * G);
+  nb.zp = cv.take((size_t)Sc * W * 4 * G);
+  const size_t wsz = (size_t)std::max(L - 1, 1) * W * W * es * G;
+  nb.wc = cv.take(wsz);
+  nb.wcT = cv.take(wsz);
+  nb.fb = cv.take((size_t)Sc * 7 * W * 4 * G);
+  nb.ppb_sen = ob_ppb(nb.n_sen);
+  nb.ppb_col = ob_ppb(nb.n_col);
+  nb.ob_slots = out_bwd_blocks(nb.n_sen, (int)nb.ppb_sen) + out_bwd_blocks(nb.n_col, (int)nb.ppb_col);
+  nb.ob = cv.take((size_t)nb.ob_slots * (W + 1) * 4 * G);
+}
+
+static void plan_step(const pigan_step_desc* s, int Sc, StepPlan& pl) {
+  Carver cv;
+  pl.G = s->genY.n_groups;
+  pl.Sc = Sc;
+  pl.es = esize(s->dt);
+  const int G = pl.G;
+  plan_net(cv, pl.Y, s->genY, s->d, 0, s->n_sY, Sc, s->P, pl.es, G);
+  plan_net(cv, pl.U, s->genU, s->d, s->d, s->n_sU, Sc, s->P, pl.es, G);
+  DiscBuf& D = pl.D;
+  D.off.init(s->disc.in_dim, s->disc.n_hidden, s->disc.width);
+  const int WD = s->disc.width, LD = s->disc.n_hidden;
+  D.Kp = (int)round_up(s->disc.in_dim, 32);
+  D.Bmax = (int64_t)Sc + s->B_r;
+  D.X0 = cv.take((size_t)D.Bmax * D.Kp * pl.es * G);
+  D.A.assign(LD + 1, 0);
+  D.H.assign(LD + 1, 0);
+  const size_t act = (size_t)D.Bmax * WD * pl.es * G;
+  for (int l = 1; l <= LD; ++l) {
+    D.A[l] = cv.take(act);
+    D.H[l] = cv.take(act);
+  }
+  D.dA[0] = cv.take(act);
+  D.dA[1] = cv.take(act);
+  D.score = cv.take((size_t)D.Bmax * 4 * G);
+  D.seed = cv.take((size_t)D.Bmax * 4 * G);
+  D.w1 = cv.take((size_t)WD * D.Kp * pl.es * G);
+  D.w1T = cv.take((size_t)WD * D.Kp * pl.es * G);
+  const size_t wsz = (size_t)std::max(LD - 1, 1) * WD * WD * pl.es * G;
+  D.wc = cv.take(wsz);
+  D.wcT = cv.take(wsz);
+  D.ppb = ob_ppb(D.Bmax);
+  D.ob_slots = out_bwd_blocks(D.Bmax, (int)D.ppb);
+  D.ob = cv.take((size_t)D.ob_slots * (WD + 1) * 4 * G);
+  // split-K partials: the largest of all weight-gradient launches
+  int64_t mx = 0, mxb = 0;
+  auto consider = [&](int64_t R, int N, int J) {
+    int ns;
+    int64_t rps;
+    dw_split_plan(R, N, J, (int)pl.es, G, &ns, &rps);
+    mx = std::max(mx, (int64_t)ns * N * J);
+    mxb = std::max(mxb, (int64_t)ns * N);
+  };
+  if (s->genY.n_hidden > 1) consider(pl.Y.R, s->genY.width, s->genY.width);
+  if (s->genU.n_hidden > 1) consider(pl.U.R, s->genU.width, s->genU.width);
+  consider(D.Bmax, WD, D.Kp);
+  if (LD > 1) consider(D.Bmax, WD, WD);
+  pl.dwp_floats = mx;
+  pl.dwdb_floats = mxb;
+  pl.dwp = cv.take((size_t)mx * 4 * G);
+  pl.dwdb = cv.take((size_t)mxb * 4 * G);
+  pl.rblocks = residual_blocks((int64_t)Sc * s->P);
+  pl.rpart = cv.take((size_t)pl.rblocks * 8 * G);
+  pl.acc = cv.take((size_t)4 * 8 * G);
+  pl.total = round_up((int64_t)cv.off, 256);
+}
+
+static const size_t kAutoCap = (size_t)64 << 30;
+
+static int choose_chunk(const pigan_step_desc* s) {
+  if (s->chunk_S > 0) return std::min(s->chunk_S, s->S);
+  int Sc = s->S;
+  StepPlan pl;
+  while (true) {
+    plan_step(s, Sc, pl);
+    if (pl.total <= kAutoCap || Sc == 1) return Sc;
+    Sc = (Sc + 1) / 2;
+  }
+}
+
+static pigan_status check_step(const pigan_step_desc* s) {
+  if (!s) return fail(PIGAN_EINVAL, "null step descriptor");
+  pigan_status st;
+  if ((st = check_mlp(&s->genY, "genY")) != PIGAN_OK) return st;
+  if ((st = check_mlp(&s->genU, "genU")) != PIGAN_OK) return st;
+  if ((st = check_mlp(&s->disc, "disc")) != PIGAN_OK) return st;
+  if ((st = check_dtype(s->dt)) != PIGAN_OK) return st;
+  if (s->genU.n_groups != s->genY.n_groups || s->disc.n_groups != s->genY.n_groups)
+    return fail(PIGAN_EINVAL, "n_groups differ between networks");
+  if (s->d < 1 || s->d > 3) return fail(PIGAN_EINVAL, "d=%d must be 1, 2 or 3", s->d);
+  if (s->n_z < 1) return fail(PIGAN_EINVAL, "n_z=%d must be >= 1", s->n_z);
+  if (s->genY.in_dim != s->d + s->n_z || s->genU.in_dim != s->d + s->n_z)
+    return fail(PIGAN_EINVAL, "generator in_dim must equal d + n_z = %d", s->d + s->n_z);
+  if (s->S < 1 || s->P < 1) return fail(PIGAN_EINVAL, "S=%d and P=%d must be >= 1", s->S, s->P);
+  if (s->n_sY < 1 || s->n_sU < 1) return fail(PIGAN_EINVAL, "n_sY=%d and n_sU=%d must be >= 1", s->n_sY, s->n_sU);
+  if (s->disc.in_dim != s->n_sY + s->n_sU)
+    return fail(PIGAN_EINVAL, "disc in_dim=%d must equal n_sY + n_sU = %d", s->disc.in_dim, s->n_sY + s->n_sU);
+  if (s->B_r < 1) return fail(PIGAN_EINVAL, "B_r=%d must be >= 1", s->B_r);
+  if (s->chunk_S < 0) return fail(PIGAN_EINVAL, "chunk_S=%d must be >= 0", s->chunk_S);
+  if (!(s->lambda_pde >= 0.0f) || !__builtin_isfinite(s->lambda_pde))
+    return fail(PIGAN_EINVAL, "lambda_pde must be finite and >= 0");
+  if (s->lambda_gp != 0.0f) return fail(PIGAN_ENOTSUP, "lambda_gp != 0: gradient penalty not implemented");
+  if (!(s->loss_scale > 0.0f) || !__builtin_isfinite(s->loss_scale))
+    return fail(PIGAN_EINVAL, "loss_scale must be finite and > 0");
+  return PIGAN_OK;
+}
+
+// ---------------------------------------------------------------------------
+// building blocks
+// ---------------------------------------------------------------------------
+template <class T> static T* tp(void* ws, size_t off) { return (T*)((char*)ws + off); }
+
+template <class T>
+static pigan_status gemm_nt(int epi, int nd1, int nd2, const NtArgs<T>& a, int G, hipStream_t st, const char* name) {
+  const int C = 1 + nd1 + nd2;
+  const double M = (double)C * a.seg.n_points;
+  const double flops = 2.0 * M * a.N * a.K * G;
+  const double es = sizeof(T);
+  double bytes = (M * a.K + (double)a.N * a.K) * es * G;
+  if (epi == EPI_FWD) bytes += M * a.N * es * G * (a.out_a ? 2 : 1);
+  else if (epi == EPI_BWD) bytes += 2.0 * M * a.N * es * G;
+  else bytes += M * a.N * 4.0 * G;
+  ProfScope ps(st, name, flops, bytes);
+  HIP_TRY(launch_gemm_nt<T>(epi, nd1, nd2, a, G, st));
+  return PIGAN_OK;
+}
+
+template <class T>
+static pigan_status weight_grad(const T* dA, int64_t a_g, int64_t lda, const T* H, int64_t h_g, int64_t ldh,
+                                int64_t R, int64_t n_value, int N, int Jp, int J, float* gW, float* gb, int64_t g_g,
+                                int accumulate, float scale, int32_t* nonfinite, float* part, float* pdb, int G,
+                                hipStream_t st) {
+  int ns;
+  int64_t rps;
+  dw_split_plan(R, N, Jp, (int)sizeof(T), G, &ns, &rps);
+  {
+    ProfScope ps(st, "gemm_dw", 2.0 * R * N * Jp * G, ((double)R * (N + Jp) * sizeof(T) + 4.0 * ns * N * Jp) * G);
+    HIP_TRY(launch_gemm_dw<T>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, Jp, part, pdb, ns, rps, G, st));
+  }
+  {
+    ProfScope ps(st, "reduce_dw", 0.0, 4.0 * ((double)ns + 1.0) * N * Jp * G);
+    HIP_TRY(launch_reduce_dw(part, pdb, ns, N, Jp, J, gW, gb, g_g, accumulate, scale, nonfinite, G, st));
+  }
+  return PIGAN_OK;
+}
+
+// Forward of one generator over a chunk: sensor rows then collocation rows.
+template <class T>
+static pigan_status gen_chunk_fwd(void* ws, const NetBuf& nb, const float* params, const float* xs, int64_t xs_g,
+                                  const float* xc, int64_t xc_g, const float* z, int64_t z_g, int d, int n_z, int Sc,
+                                  int P, int G, hipStream_t st) {
+  const int W = nb.off.W, L = nb.off.L;
+  const int64_t pg = nb.off.n;
+  const int64_t actg = nb.R * W;  // per-group element stride of activations
+  {
+    ProfScope ps(st, "zproj", 2.0 * Sc * W * n_z * G, 0.0);
+    HIP_TRY(launch_zproj(params, pg, nb.off.in_dim, d, W, z, z_g, n_z, Sc, tp<float>(ws, nb.zp), (int64_t)Sc * W, G,
+                         st));
+  }
+  FirstArgs<T> fa{};
+  fa.p1 = params; fa.p_g = pg; fa.in_dim = nb.off.in_dim; fa.d = d; fa.W = W;
+  fa.zp = tp<float>(ws, nb.zp); fa.zp_g = (int64_t)Sc * W;
+  fa.out_a = tp<T>(ws, nb.A[1]); fa.out_h = tp<T>(ws, nb.H[1]); fa.o_g = actg; fa.ldo = W;
+  // sensors: shared locations, value stream only
+  fa.x = xs; fa.x_g = xs_g; fa.x_shared = 1; fa.Pn = nb.n_s;
+  fa.seg = Seg{nb.n_sen, 0, 0};
+  {
+    ProfScope ps(st, "first_fwd", 2.0 * nb.n_sen * W * d * G, (double)nb.n_sen * W * 2 * sizeof(T) * G);
+    HIP_TRY(launch_first_fwd<T>(0, 0, fa, G, st));
+  }
+  fa.x = xc; fa.x_g = xc_g; fa.x_shared = 0; fa.Pn = P;
+  fa.seg = Seg{nb.n_col, nb.n_sen, nb.n_col};
+  {
+    const int C = 1 + nb.nd1 + nb.nd2;
+    ProfScope ps(st, "first_fwd", 2.0 * nb.n_col * W * d * G, (double)nb.n_col * C * W * 2 * sizeof(T) * G);
+    HIP_TRY(launch_first_fwd<T>(nb.nd1, nb.nd2, fa, G, st));
+  }
+  for (int l = 2; l <= L; ++l) {
+    NtArgs<T> a{};
+    a.X = tp<T>(ws, nb.H[l - 1]); a.x_g = actg; a.ldx = W;
+    a.Wm = tp<T>(ws, nb.wc) + (size_t)(l - 2) * W * W; a.w_g = (int64_t)std::max(L - 1, 1) * W * W; a.ldw = W;
+    a.bias = params + nb.off.b[l]; a.b_g = pg;
+    a.out_a = tp<T>(ws, nb.A[l]); a.out_h = tp<T>(ws, nb.H[l]); a.o_g = actg; a.ldo = W;
+    a.N = W; a.K = W;
+    a.seg = Seg{nb.n_sen, 0, 0};
+    pigan_status s1 = gemm_nt<T>(EPI_FWD, 0, 0, a, G, st, "gemm_fwd");
+    if (s1 != PIGAN_OK) return s1;
+    a.seg = Seg{nb.n_col, nb.n_sen, nb.n_col};
+    s1 = gemm_nt<T>(EPI_FWD, nb.nd1, nb.nd2, a, G, st, "gemm_fwd");
+    if (s1 != PIGAN_OK) return s1;
+  }
+  {
+    ProfScope ps(st, "out_fwd", 2.0 * nb.rows * W * G, (double)nb.rows * W * sizeof(T) * G);
+    HIP_TRY(launch_out_fwd<T>(tp<T>(ws, nb.H[L]), actg, W, nb.rows, nb.n_sen + nb.n_col, W, params + nb.off.wout, pg,
+                              tp<float>(ws, nb.jet), nb.R, G, st));
+  }
+  return PIGAN_OK;
+}
+
+// Reverse pass of one generator over a chunk (cotangents of the outputs are
+// in nb.gbar).  Gradients go to grad (accumulated when accumulate != 0).
+template <class T>
+static pigan_status gen_chunk_bwd(void* ws, const StepPlan& pl, const NetBuf& nb, const float* params,
+                                  const float* xs, int64_t xs_g, const float* xc, int64_t xc_g, const float* z,
+                                  int64_t z_g, int d, int n_z, int Sc, int P, float* grad, int accumulate, float scale,
+                                  int32_t* nonfinite, int G, hipStream_t st) {
+  const int W = nb.off.W, L = nb.off.L;
+  const int64_t pg = nb.off.n;
+  const int64_t actg = nb.R * W;
+  OutBwdArgs<T> ob{};
+  ob.A = tp<T>(ws, nb.A[L]); ob.dA = tp<T>(ws, nb.dA[0]); ob.o_g = actg; ob.ldo = W;
+  ob.gbar = tp<float>(ws, nb.gbar); ob.gb_g = nb.R;
+  ob.wout = params + nb.off.wout; ob.w_g = pg;
+  const int blk_sen = out_bwd_blocks(nb.n_sen, (int)nb.ppb_sen);
+  const int n_slots = blk_sen + out_bwd_blocks(nb.n_col, (int)nb.ppb_col);
+  ob.W = W; ob.part = tp<float>(ws, nb.ob); ob.n_slots = n_slots;
+  ob.ppb = nb.ppb_sen; ob.slot0 = 0; ob.seg = Seg{nb.n_sen, 0, 0};
+  {
+    ProfScope ps(st, "out_bwd", 0.0, (double)nb.rows * W * 2 * sizeof(T) * G);
+    HIP_TRY(launch_out_bwd<T>(0, 0, ob, G, st));
+    ob.ppb = nb.ppb_col; ob.slot0 = blk_sen; ob.seg = Seg{nb.n_col, nb.n_sen, nb.n_col};
+    HIP_TRY(launch_out_bwd<T>(nb.nd1, nb.nd2, ob, G, st));
+    HIP_TRY(launch_reduce_slots(tp<float>(ws, nb.ob), n_slots, W, grad + nb.off.wout, pg, accumulate, scale,
+                                nonfinite, G, st));
+  }
+  int cur = 0;
+  for (int l = L; l >= 2; --l) {
+    pigan_status s1 = weight_grad<T>(tp<T>(ws, nb.dA[cur]), actg, W, tp<T>(ws, nb.H[l - 1]), actg, W, nb.rows,
+                                     nb.n_sen + nb.n_col, W, W, W, grad + nb.off.w[l], grad + nb.off.b[l], pg,
+                                     accumulate, scale, nonfinite, tp<float>(ws, pl.dwp), tp<float>(ws, pl.dwdb), G, st);
+    if (s1 != PIGAN_OK) return s1;
+    NtArgs<T> a{};
+    a.X = tp<T>(ws, nb.dA[cur]); a.x_g = actg; a.ldx = W;
+    a.Wm = tp<T>(ws, nb.wcT) + (size_t)(l - 2) * W * W; a.w_g = (int64_t)std::max(L - 1, 1) * W * W; a.ldw = W;
+    a.aprev = tp<T>(ws, nb.A[l - 1]); a.out_da = tp<T>(ws, nb.dA[1 - cur]); a.o_g = actg; a.ldo = W;
+    a.N = W; a.K = W;
+    a.seg = Seg{nb.n_sen, 0, 0};
+    s1 = gemm_nt<T>(EPI_BWD, 0, 0, a, G, st, "gemm_bwd");
+    if (s1 != PIGAN_OK) return s1;
+    a.seg = Seg{nb.n_col, nb.n_sen, nb.n_col};
+    s1 = gemm_nt<T>(EPI_BWD, nb.nd1, nb.nd2, a, G, st, "gemm_bwd");
+    if (s1 != PIGAN_OK) return s1;
+    cur = 1 - cur;
+  }
+  FirstBwdArgs<T> fb{};
+  fb.dA = tp<T>(ws, nb.dA[cur]); fb.a_g = actg; fb.lda = W;
+  fb.n_sen = nb.n_sen; fb.n_col = nb.n_col; fb.n_s = nb.n_s; fb.P = P; fb.S = Sc; fb.W = W; fb.d = d; fb.nd1 = nb.nd1;
+  fb.xs = xs; fb.xs_g = xs_g; fb.xc = xc; fb.xc_g = xc_g; fb.part = tp<float>(ws, nb.fb);
+  {
+    ProfScope ps(st, "first_bwd", 0.0, (double)(nb.n_sen + (1 + nb.nd1) * nb.n_col) * W * sizeof(T) * G);
+    HIP_TRY(launch_first_bwd<T>(fb, G, st));
+    HIP_TRY(launch_first_wgrad(tp<float>(ws, nb.fb), Sc, W, d, nb.nd1, nb.off.in_dim, z, z_g, n_z, grad, pg,
+                               accumulate, scale, nonfinite, G, st));
+  }
+  return PIGAN_OK;
+}
+
+template <class T>
+static pigan_status cast_gen_weights(void* ws, const NetBuf& nb, const float* params, int G, hipStream_t st) {
+  const int W = nb.off.W, L = nb.off.L;
+  const int64_t dg = (int64_t)std::max(L - 1, 1) * W * W;
+  for (int l = 2; l <= L; ++l)
+    HIP_TRY(launch_cast<T>(params + nb.off.w[l], nb.off.n, W, W, W, tp<T>(ws, nb.wc) + (size_t)(l - 2) * W * W,
+                           tp<T>(ws, nb.wcT) + (size_t)(l - 2) * W * W, dg, G, st));
+  return PIGAN_OK;
+}
+
+template <class T>
+static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const float* pY, const float* pU,
+                             const float* pD, const float* z, const float* xc, const float* xsY, const float* xsU,
+                             const float* f, float f_const, const float* real, const float* w_group, float* gY,
+                             float* gU, float* gD, float* loss, int32_t* nonfinite, void* ws, hipStream_t st) {
+  const int G = pl.G, d = s->d, n_z = s->n_z, P = s->P, S = s->S;
+  const float ls = s->loss_scale;
+  const float inv = 1.0f / ls;
+  const DiscBuf& D = pl.D;
+  const int WD = s->disc.width, LD = s->disc.n_hidden, n_in = s->disc.in_dim;
+  double* acc = tp<double>(ws, pl.acc);
+  pigan_status r;
+
+  {
+    ProfScope ps(st, "misc", 0.0, 0.0);
+    HIP_TRY(launch_zero(acc, 4 * G, nonfinite, st));
+    if ((r = cast_gen_weights<T>(ws, pl.Y, pY, G, st)) != PIGAN_OK) return r;
+    if ((r = cast_gen_weights<T>(ws, pl.U, pU, G, st)) != PIGAN_OK) return r;
+    const int64_t dg1 = (int64_t)WD * D.Kp;
+    HIP_TRY(launch_cast<T>(pD + D.off.w[1], D.off.n, WD, n_in, D.Kp, tp<T>(ws, D.w1), tp<T>(ws, D.w1T), dg1, G, st));
+    const int64_t dgl = (int64_t)std::max(LD - 1, 1) * WD * WD;
+    for (int l = 2; l <= LD; ++l)
+      HIP_TRY(launch_cast<T>(pD + D.off.w[l], D.off.n, WD, WD, WD, tp<T>(ws, D.wc) + (size_t)(l - 2) * WD * WD,
+                             tp<T>(ws, D.wcT) + (size_t)(l - 2) * WD * WD, dgl, G, st));
+  }
+
+  const int64_t xs_gY = (int64_t)s->n_sY * d, xs_gU = (int64_t)s->n_sU * d;
+  const int64_t xc_g = (int64_t)S * P * d, z_g = (int64_t)S * n_z;
+  for (int s0 = 0, ci = 0; s0 < S; s0 += pl.Sc, ++ci) {
+    const int Sc = std::min(pl.Sc, S - s0);
+    const int accum = ci > 0;
+    const float* zc = z + (int64_t)s0 * n_z;
+    const float* xcc = xc + (int64_t)s0 * P * d;
+    // chunk-local views: the plan is laid out for pl.Sc samples; a shorter
+    // last chunk uses the same buffers with its own row counts
+    NetBuf Yc = pl.Y, Uc = pl.U;
+    for (NetBuf* nb : {&Yc, &Uc}) {
+      nb->n_sen = (int64_t)Sc * nb->n_s;
+      nb->n_col = (int64_t)Sc * P;
+      nb->rows = nb->n_sen + (1 + nb->nd1 + nb->nd2) * nb->n_col;
+    }
+    // generator forward passes
+    if ((r = gen_chunk_fwd<T>(ws, Yc, pY, xsY, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, G, st)) != PIGAN_OK) return r;
+    if ((r = gen_chunk_fwd<T>(ws, Uc, pU, xsU, xs_gU, xcc, xc_g, zc, z_g, d, n_z, Sc, P, G, st)) != PIGAN_OK) return r;
+    // residual and its cotangents
+    {
+      ResidArgs ra{};
+      ra.jY = tp<float>(ws, Yc.jet); ra.jy_g = Yc.R; ra.offY = Yc.n_sen;
+      ra.jU = tp<float>(ws, Uc.jet); ra.ju_g = Uc.R; ra.offU = Uc.n_sen;
+      ra.plane = Yc.n_col; ra.M = (int64_t)Sc * P; ra.d = d;
+      ra.f = f ? f + (int64_t)s0 * P : nullptr; ra.f_g = (int64_t)S * P; ra.f_const = f_const;
+      ra.gY = tp<float>(ws, Yc.gbar); ra.gU = tp<float>(ws, Uc.gbar);
+      ra.w_group = w_group; ra.qscale = (float)(2.0 * s->lambda_pde * ls / ((double)S * P));
+      ra.part = tp<double>(ws, pl.rpart);
+      ProfScope ps(st, "residual", 0.0, (double)ra.M * (3 * d + 2) * 4.0 * 2 * G);
+      HIP_TRY(launch_residual(ra, G, st));
+      HIP_TRY(launch_sum_partials(tp<double>(ws, pl.rpart), residual_blocks(ra.M), acc, 4, 2, G, st));
+    }
+    // discriminator forward on fake (and, in the first chunk, real) snapshots
+    const int n_real = ci == 0 ? s->B_r : 0;
+    const int B = Sc + n_real;
+    const int64_t dact = D.Bmax * WD;
+    {
+      ProfScope ps(st, "misc", 0.0, 0.0);
+      HIP_TRY(launch_snap_fill<T>(tp<float>(ws, Yc.jet), Yc.R, tp<float>(ws, Uc.jet), Uc.R, s->n_sY, s->n_sU, Sc, real,
+                                  (int64_t)s->B_r * n_in, n_real, n_in, tp<T>(ws, D.X0), D.Bmax * D.Kp, D.Kp, G, st));
+    }
+    for (int l = 1; l <= LD; ++l) {
+      NtArgs<T> a{};
+      if (l == 1) {
+        a.X = tp<T>(ws, D.X0); a.x_g = D.Bmax * D.Kp; a.ldx = D.Kp;
+        a.Wm = tp<T>(ws, D.w1); a.w_g = (int64_t)WD * D.Kp; a.ldw = D.Kp; a.K = D.Kp;
+      } else {
+        a.X = tp<T>(ws, D.H[l - 1]); a.x_g = dact; a.ldx = WD;
+        a.Wm = tp<T>(ws, D.wc) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD;
+        a.ldw = WD; a.K = WD;
+      }
+      a.bias = pD + D.off.b[l]; a.b_g = D.off.n;
+      a.out_a = tp<T>(ws, D.A[l]); a.out_h = tp<T>(ws, D.H[l]); a.o_g = dact; a.ldo = WD;
+      a.N = WD;
+      a.seg = Seg{B, 0, 0};
+      if ((r = gemm_nt<T>(EPI_FWD, 0, 0, a, G, st, "disc_fwd")) != PIGAN_OK) return r;
+    }
+    {
+      ProfScope ps(st, "out_fwd", 2.0 * B * WD * G, (double)B * WD * sizeof(T) * G);
+      HIP_TRY(launch_out_fwd<T>(tp<T>(ws, D.H[LD]), dact, WD, B, B, WD, pD + D.off.wout, D.off.n,
+                                tp<float>(ws, D.score), D.Bmax, G, st));
+      HIP_TRY(launch_disc_seed(tp<float>(ws, D.score), D.Bmax, Sc, n_real, S, s->B_r, w_group, ls,
+                               tp<float>(ws, D.seed), acc, 4, G, st));
+    }
+    // discriminator reverse pass
+    {
+      OutBwdArgs<T> ob{};
+      ob.A = tp<T>(ws, D.A[LD]); ob.dA = tp<T>(ws, D.dA[0]); ob.o_g = dact; ob.ldo = WD;
+      ob.gbar = tp<float>(ws, D.seed); ob.gb_g = D.Bmax;
+      ob.wout = pD + D.off.wout; ob.w_g = D.off.n;
+      ob.W = WD; ob.ppb = D.ppb; ob.part = tp<float>(ws, D.ob); ob.n_slots = out_bwd_blocks(B, (int)D.ppb);
+      ob.slot0 = 0; ob.seg = Seg{B, 0, 0};
+      ProfScope ps(st, "out_bwd", 0.0, (double)B * WD * 2 * sizeof(T) * G);
+      HIP_TRY(launch_out_bwd<T>(0, 0, ob, G, st));
+      HIP_TRY(launch_reduce_slots(tp<float>(ws, D.ob), ob.n_slots, WD, gD + D.off.wout, D.off.n, accum, inv,
+                                  nonfinite, G, st));
+    }
+    int cur = 0;
+    for (int l = LD; l >= 2; --l) {
+      if ((r = weight_grad<T>(tp<T>(ws, D.dA[cur]), dact, WD, tp<T>(ws, D.H[l - 1]), dact, WD, B, B, WD, WD, WD,
+                              gD + D.off.w[l], gD + D.off.b[l], D.off.n, accum, inv, nonfinite, tp<float>(ws, pl.dwp),
+                              tp<float>(ws, pl.dwdb), G, st)) != PIGAN_OK)
+        return r;
+      NtArgs<T> a{};
+      a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
+      a.Wm = tp<T>(ws, D.wcT) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD; a.ldw = WD;
+      a.aprev = tp<T>(ws, D.A[l - 1]); a.out_da = tp<T>(ws, D.dA[1 - cur]); a.o_g = dact; a.ldo = WD;
+      a.N = WD; a.K = WD; a.seg = Seg{B, 0, 0};
+      if ((r = gemm_nt<T>(EPI_BWD, 0, 0, a, G, st, "disc_bwd")) != PIGAN_OK) return r;
+      cur = 1 - cur;
+    }
+    if ((r = weight_grad<T>(tp<T>(ws, D.dA[cur]), dact, WD, tp<T>(ws, D.X0), D.Bmax * D.Kp, D.Kp, B, B, WD, D.Kp, n_in,
+                            gD + D.off.w[1], gD + D.off.b[1], D.off.n, accum, inv, nonfinite, tp<float>(ws, pl.dwp),
+                            tp<float>(ws, pl.dwdb), G, st)) != PIGAN_OK)
+      return r;
+    {
+      // d(L_adv)/dF = -dL_D/dF for the fake rows -> generator sensor cotangents
+      NtArgs<T> a{};
+      a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
+      a.Wm = tp<T>(ws, D.w1T); a.w_g = (int64_t)WD * D.Kp; a.ldw = WD;
+      a.N = D.Kp; a.K = WD; a.seg = Seg{Sc, 0, 0};
+      a.seedY = tp<float>(ws, Yc.gbar); a.sY_g = Yc.R; a.seedU = tp<float>(ws, Uc.gbar); a.sU_g = Uc.R;
+      a.nY = s->n_sY; a.nU = s->n_sU; a.df_sign = -1.0f;
+      if ((r = gemm_nt<T>(EPI_DF, 0, 0, a, G, st, "disc_bwd")) != PIGAN_OK) return r;
+    }
+    // generator reverse passes
+    if ((r = gen_chunk_bwd<T>(ws, pl, Yc, pY, xsY, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, gY, accum, inv, nonfinite,
+                              G, st)) != PIGAN_OK)
+      return r;
+    if ((r = gen_chunk_bwd<T>(ws, pl, Uc, pU, xsU, xs_gU, xcc, xc_g, zc, z_g, d, n_z, Sc, P, gU, accum, inv, nonfinite,
+                              G, st)) != PIGAN_OK)
+      return r;
+  }
+  {
+    ProfScope ps(st, "misc", 0.0, 0.0);
+    HIP_TRY(launch_losses(acc, 4, w_group, S, s->B_r, (int64_t)S * P, s->lambda_pde, loss, nonfinite, G, st));
+  }
+  return PIGAN_OK;
+}
+
+}  // namespace pigan
+
+using namespace pigan;
+
+// ===========================================================================
+// C entry points
+// ===========================================================================
+extern "C" {
+
+const char* pigan_last_error(void) { return g_err.c_str(); }
+
+int64_t pigan_mlp_n_params(const pigan_mlp* net) {
+  if (!net) return -1;
+  MlpOff o;
+  o.init(net->in_dim, net->n_hidden, net->width);
+  return o.n;
+}
+
+size_t pigan_workspace_bytes(const pigan_step_desc* s) {
+  if (check_step(s) != PIGAN_OK) return 0;
+  StepPlan pl;
+  plan_step(s, choose_chunk(s), pl);
+  return pl.total;
+}
+
+pigan_status pigan_train_step_grads(const pigan_step_desc* s, const float* pY, const float* pU, const float* pD,
+                                    const float* z, const float* xc, const float* xsY, const float* xsU,
+                                    const float* f, float f_const, const float* real, const float* w_group,
+                                    float* gY, float* gU, float* gD, float* loss, int32_t* nonfinite, void* ws,
+                                    size_t ws_bytes, void* stream) {
+  g_err.clear();
+  pigan_status st = check_step(s);
+  if (st != PIGAN_OK) return st;
+  if (!pY || !pU || !pD || !z || !xc || !xsY || !xsU || !real || !gY || !gU || !gD || !loss || !nonfinite)
+    return fail(PIGAN_EINVAL, "null input or output pointer");
+  if (!__builtin_isfinite(f_const)) return fail(PIGAN_EINVAL, "f_const must be finite");
+  StepPlan pl;
+  plan_step(s, choose_chunk(s), pl);
+  if (!ws) return fail(PIGAN_EWORKSPACE, "null workspace (need %zu bytes)", pl.total);
+  if (ws_bytes < pl.total) return fail(PIGAN_EWORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, pl.total);
+  if ((uintptr_t)ws % 256) return fail(PIGAN_EINVAL, "workspace must be 256-byte aligned");
+  hipStream_t hs = (hipStream_t)stream;
+  switch (s->dt) {
+    case PIGAN_FP32:
+      return run_step<float>(s, pl, pY, pU, pD, z, xc, xsY, xsU, f, f_const, real, w_group, gY, gU, gD, loss,
+                             nonfinite, ws, hs);
+    case PIGAN_BF16:
+      return run_step<bf16>(s, pl, pY, pU, pD, z, xc, xsY, xsU, f, f_const, real, w_group, gY, gU, gD, loss,
+                            nonfinite, ws, hs);
+    default:
+      return run_step<f16>(s, pl, pY, pU, pD, z, xc, xsY, xsU, f, f_const, real, w_group, gY, gU, gD, loss,
+                           nonfinite, ws, hs);
+  }
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// generator forward
+// ---------------------------------------------------------------------------
+struct GenFwdPlan {
+  size_t zp, h[2], wc, total;
+  int64_t R;
+};
+
+static GenFwdPlan plan_gen_fwd(const pigan_mlp* net, int d, int S, int P, int order, pigan_dtype dt) {
+  GenFwdPlan p{};
+  Carver cv;
+  const int G = net->n_groups, W = net->width, L = net->n_hidden;
+  const size_t es = esize(dt);
+  const int C = 1 + order * d;
+  p.R = (int64_t)C * S * P;
+  p.zp = cv.take((size_t)S * W * 4 * G);
+  p.h[0] = cv.take((size_t)p.R * W * es * G);
+  p.h[1] = cv.take((size_t)p.R * W * es * G);
+  p.wc = cv.take((size_t)std::max(L - 1, 1) * W * W * es * G);
+  p.total = round_up((int64_t)cv.off, 256);
+  return p;
+}
+
+static pigan_status check_gen_fwd(const pigan_mlp* net, int d, int S, int P, int order, pigan_dtype dt) {
+  pigan_status st = check_mlp(net, "generator");
+  if (st != PIGAN_OK) return st;
+  if ((st = check_dtype(dt)) != PIGAN_OK) return st;
+  if (d < 1 || d > 3) return fail(PIGAN_EINVAL, "d=%d must be 1, 2 or 3", d);
+  if (net->in_dim <= d) return fail(PIGAN_EINVAL, "in_dim=%d must exceed d=%d (n_z >= 1)", net->in_dim, d);
+  if (S < 1 || P < 1) return fail(PIGAN_EINVAL, "S=%d and P=%d must be >= 1", S, P);
+  if (order < 0 || order > 2) return fail(PIGAN_EINVAL, "order=%d must be 0, 1 or 2", order);
+  return PIGAN_OK;
+}
+
+extern "C" {
+
+size_t pigan_gen_forward_workspace(const pigan_mlp* net, int32_t d, int32_t S, int32_t P, int32_t order,
+                                   pigan_dtype dt) {
+  if (check_gen_fwd(net, d, S, P, order, dt) != PIGAN_OK) return 0;
+  return plan_gen_fwd(net, d, S, P, order, dt).total;
+}
+
+}  // extern "C"
+
+template <class T>
+static pigan_status run_gen_fwd(const pigan_mlp* net, const float* params, int d, const float* z, const float* x,
+                                int x_shared, int S, int P, int order, float* jet, void* ws, const GenFwdPlan& p,
+                                hipStream_t st) {
+  const int G = net->n_groups, W = net->width, L = net->n_hidden, in_dim = net->in_dim, n_z = in_dim - d;
+  MlpOff off;
+  off.init(in_dim, L, W);
+  const int nd1 = order >= 1 ? d : 0, nd2 = order >= 2 ? d : 0;
+  const int64_t M = (int64_t)S * P;
+  const int64_t actg = p.R * W;
+  {
+    ProfScope ps(st, "misc", 0.0, 0.0);
+    const int64_t dg = (int64_t)std::max(L - 1, 1) * W * W;
+    for (int l = 2; l <= L; ++l)
+      HIP_TRY(launch_cast<T>(params + off.w[l], off.n, W, W, W, tp<T>(ws, p.wc) + (size_t)(l - 2) * W * W, nullptr,
+                             dg, G, st));
+    HIP_TRY(launch_zproj(params, off.n, in_dim, d, W, z, (int64_t)S * n_z, n_z, S, tp<float>(ws, p.zp),
+                         (int64_t)S * W, G, st));
+  }
+  FirstArgs<T> fa{};
+  fa.p1 = params; fa.p_g = off.n; fa.in_dim = in_dim; fa.d = d; fa.W = W;
+  fa.zp = tp<float>(ws, p.zp); fa.zp_g = (int64_t)S * W;
+  fa.x = x; fa.x_g = x_shared ? (int64_t)P * d : M * d; fa.x_shared = x_shared ? 1 : 0; fa.Pn = P;
+  fa.out_a = nullptr; fa.out_h = tp<T>(ws, p.h[0]); fa.o_g = actg; fa.ldo = W;
+  fa.seg = Seg{M, 0, M};
+  {
+    ProfScope ps(st, "first_fwd", 2.0 * M * W * d * G, (double)M * (1 + nd1 + nd2) * W * sizeof(T) * G);
+    HIP_TRY(launch_first_fwd<T>(nd1, nd2, fa, G, st));
+  }
+  int cur = 0;
+  for (int l = 2; l <= L; ++l) {
+    NtArgs<T> a{};
+    a.X = tp<T>(ws, p.h[cur]); a.x_g = actg; a.ldx = W;
+    a.Wm = tp<T>(ws, p.wc) + (size_t)(l - 2) * W * W; a.w_g = (int64_t)std::max(L - 1, 1) * W * W; a.ldw = W;
+    a.bias = params + off.b[l]; a.b_g = off.n;
+    a.out_a = nullptr; a.out_h = tp<T>(ws, p.h[1 - cur]); a.o_g = actg; a.ldo = W;
+    a.N = W; a.K = W; a.seg = Seg{M, 0, M};
+    pigan_status s1 = gemm_nt<T>(EPI_FWD, nd1, nd2, a, G, st, "gemm_fwd");
+    if (s1 != PIGAN_OK) return s1;
+    cur = 1 - cur;
+  }
+  {
+    ProfScope ps(st, "out_fwd", 2.0 * p.R * W * G, (double)p.R * W * sizeof(T) * G);
+    HIP_TRY(launch_out_fwd<T>(tp<T>(ws, p.h[cur]), actg, W, p.R, M, W, params + off.wout, off.n, jet, p.R, G, st));
+  }
+  return PIGAN_OK;
+}
+
+extern "C" {
+
+pigan_status pigan_gen_forward(const pigan_mlp* net, const float* params, int32_t d, const float* z, const float* x,
+                               int32_t x_shared, int32_t S, int32_t P, int32_t order, pigan_dtype dt, float* jet,
+                               void* ws, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  pigan_status st = check_gen_fwd(net, d, S, P, order, dt);
+  if (st != PIGAN_OK) return st;
+  if (!params || !z || !x || !jet) return fail(PIGAN_EINVAL, "null input or output pointer");
+  GenFwdPlan p = plan_gen_fwd(net, d, S, P, order, dt);
+  if (!ws) return fail(PIGAN_EWORKSPACE, "null workspace (need %zu bytes)", p.total);
+  if (ws_bytes < p.total) return fail(PIGAN_EWORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, p.total);
+  if ((uintptr_t)ws % 256) return fail(PIGAN_EINVAL, "workspace must be 256-byte aligned");
+  hipStream_t hs = (hipStream_t)stream;
+  switch (dt) {
+    case PIGAN_FP32: return run_gen_fwd<float>(net, params, d, z, x, x_shared, S, P, order, jet, ws, p, hs);
+    case PIGAN_BF16: return run_gen_fwd<bf16>(net, params, d, z, x, x_shared, S, P, order, jet, ws, p, hs);
+    default: return run_gen_fwd<f16>(net, params, d, z, x, x_shared, S, P, order, jet, ws, p, hs);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// residual
+// ---------------------------------------------------------------------------
+pigan_status pigan_pde_residual(int32_t d, int32_t G, int64_t M, const float* jetY, const float* jetU,
+                                const float* f, float f_const, float* r, void* stream) {
+  g_err.clear();
+  if (d < 1 || d > 3) return fail(PIGAN_EINVAL, "d=%d must be 1, 2 or 3", d);
+  if (G < 1 || G > 65535) return fail(PIGAN_EINVAL, "G=%d out of [1,65535]", G);
+  if (M < 1) return fail(PIGAN_EINVAL, "M=%lld must be >= 1", (long long)M);
+  if (!jetY || !jetU || !r) return fail(PIGAN_EINVAL, "null input or output pointer");
+  if (!__builtin_isfinite(f_const)) return fail(PIGAN_EINVAL, "f_const must be finite");
+  ResidArgs ra{};
+  ra.jY = jetY; ra.jy_g = (1 + d) * M; ra.offY = 0;
+  ra.jU = jetU; ra.ju_g = (1 + 2 * d) * M; ra.offU = 0;
+  ra.plane = M; ra.M = M; ra.d = d;
+  ra.f = f; ra.f_g = M; ra.f_const = f_const;
+  ra.r = r; ra.r_g = M;
+  hipStream_t hs = (hipStream_t)stream;
+  ProfScope ps(hs, "residual", 0.0, (double)M * (3 * d + 3) * 4.0 * G);
+  HIP_TRY(launch_residual(ra, G, hs));
+  return PIGAN_OK;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// discriminator forward
+// ---------------------------------------------------------------------------
+struct DiscFwdPlan {
+  size_t X0, h[2], w1, wc, total;
+  int Kp;
+};
+
+static DiscFwdPlan plan_disc_fwd(const pigan_mlp* net, int B, pigan_dtype dt) {
+  DiscFwdPlan p{};
+  Carver cv;
+  const int G = net->n_groups, W = net->width, L = net->n_hidden;
+  const size_t es = esize(dt);
+  p.Kp = (int)round_up(net->in_dim, 32);
+  p.X0 = cv.take((size_t)B * p.Kp * es * G);
+  p.h[0] = cv.take((size_t)B * W * es * G);
+  p.h[1] = cv.take((size_t)B * W * es * G);
+  p.w1 = cv.take((size_t)W * p.Kp * es * G);
+  p.wc = cv.take((size_t)std::max(L - 1, 1) * W * W * es * G);
+  p.total = round_up((int64_t)cv.off, 256);
+  return p;
+}
+
+extern "C" {
+
+size_t pigan_disc_forward_workspace(const pigan_mlp* net, int32_t B, pigan_dtype dt) {
+  if (check_mlp(net, "disc") != PIGAN_OK || check_dtype(dt) != PIGAN_OK || B < 1) return 0;
+  return plan_disc_fwd(net, B, dt).total;
+}
+
+}  // extern "C"
+
+template <class T>
+static pigan_status run_disc_fwd(const pigan_mlp* net, const float* params, const float* snap, int B, float* score,
+                                 void* ws, const DiscFwdPlan& p, hipStream_t st) {
+  const int G = net->n_groups, W = net->width, L = net->n_hidden, n_in = net->in_dim;
+  MlpOff off;
+  off.init(n_in, L, W);
+  const int64_t actg = (int64_t)B * W;
+  {
+    ProfScope ps(st, "misc", 0.0, 0.0);
+    HIP_TRY(launch_cast<T>(params + off.w[1], off.n, W, n_in, p.Kp, tp<T>(ws, p.w1), nullptr, (int64_t)W * p.Kp, G,
+                           st));
+    const int64_t dg = (int64_t)std::max(L - 1, 1) * W * W;
+    for (int l = 2; l <= L; ++l)
+      HIP_TRY(launch_cast<T>(params + off.w[l], off.n, W, W, W, tp<T>(ws, p.wc) + (size_t)(l - 2) * W * W, nullptr,
+                             dg, G, st));
+    HIP_TRY(launch_snap_fill<T>(nullptr, 0, nullptr, 0, 0, 0, 0, snap, (int64_t)B * n_in, B, n_in, tp<T>(ws, p.X0),
+                                (int64_t)B * p.Kp, p.Kp, G, st));
+  }
+  // layer l writes h[(l - 1) % 2]
+  for (int l = 1; l <= L; ++l) {
+    NtArgs<T> a{};
+    if (l == 1) {
+      a.X = tp<T>(ws, p.X0); a.x_g = (int64_t)B * p.Kp; a.ldx = p.Kp;
+      a.Wm = tp<T>(ws, p.w1); a.w_g = (int64_t)W * p.Kp; a.ldw = p.Kp; a.K = p.Kp;
+    } else {
+      a.X = tp<T>(ws, p.h[(l - 2) % 2]); a.x_g = actg; a.ldx = W;
+      a.Wm = tp<T>(ws, p.wc) + (size_t)(l - 2) * W * W; a.w_g = (int64_t)std::max(L - 1, 1) * W * W; a.ldw = W;
+      a.K = W;
+    }
+    a.bias = params + off.b[l]; a.b_g = off.n;
+    a.out_a = nullptr; a.out_h = tp<T>(ws, p.h[(l - 1) % 2]); a.o_g = actg; a.ldo = W;
+    a.N = W; a.seg = Seg{B, 0, 0};
+    pigan_status s1 = gemm_nt<T>(EPI_FWD, 0, 0, a, G, st, "disc_fwd");
+    if (s1 != PIGAN_OK) return s1;
+  }
+  const int cur = (L - 1) % 2;
+  {
+    ProfScope ps(st, "out_fwd", 2.0 * B * W * G, (double)B * W * sizeof(T) * G);
+    HIP_TRY(launch_out_fwd<T>(tp<T>(ws, p.h[cur]), actg, W, B, B, W, params + off.wout, off.n, score, B, G, st));
+  }
+  return PIGAN_OK;
+}
+
+extern "C" {
+
+pigan_status pigan_disc_forward(const pigan_mlp* net, const float* params, const float* snap, int32_t B,
+                                pigan_dtype dt, float* score, void* ws, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  pigan_status st = check_mlp(net, "disc");
+  if (st != PIGAN_OK) return st;
+  if ((st = check_dtype(dt)) != PIGAN_OK) return st;
+  if (B < 1) return fail(PIGAN_EINVAL, "B=%d must be >= 1", B);
+  if (!params || !snap || !score) return fail(PIGAN_EINVAL, "null input or output pointer");
+  DiscFwdPlan p = plan_disc_fwd(net, B, dt);
+  if (!ws) return fail(PIGAN_EWORKSPACE, "null workspace (need %zu bytes)", p.total);
+  if (ws_bytes < p.total) return fail(PIGAN_EWORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, p.total);
+  if ((uintptr_t)ws % 256) return fail(PIGAN_EINVAL, "workspace must be 256-byte aligned");
+  hipStream_t hs = (hipStream_t)stream;
+  switch (dt) {
+    case PIGAN_FP32: return run_disc_fwd<float>(net, params, snap, B, score, ws, p, hs);
+    case PIGAN_BF16: return run_disc_fwd<bf16>(net, params, snap, B, score, ws, p, hs);
+    default: return run_disc_fwd<f16>(net, params, snap, B, score, ws, p, hs);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// profiling
+// ---------------------------------------------------------------------------
+pigan_status pigan_profile_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(g_pm);
+  g_prof = on != 0;
+  return PIGAN_OK;
+}
+
+pigan_status pigan_profile_read(pigan_kernel_stat* out, int32_t max_entries, int32_t* n_entries) {
+  g_err.clear();
+  if (!n_entries || (max_entries > 0 && !out)) return fail(PIGAN_EINVAL, "null output");
+  std::lock_guard<std::mutex> lk(g_pm);
+  std::vector<pigan_kernel_stat> agg;
+  for (auto& r : g_recs) {
+    float ms = 0.0f;
+    if (r.a && r.b) {
+      hipError_t e = hipEventElapsedTime(&ms, r.a, r.b);
+      if (e != hipSuccess) ms = 0.0f;
+    }
+    auto it = std::find_if(agg.begin(), agg.end(), [&](const pigan_kernel_stat& k) { return r.name == k.name; });
+    if (it == agg.end()) {
+      pigan_kernel_stat k{};
+      snprintf(k.name, sizeof k.name, "%s", r.name.c_str());
+      agg.push_back(k);
+      it = agg.end() - 1;
+    }
+    it->launches += 1;
+    it->total_ms += ms;
+    it->flops += r.flops;
+    it->bytes += r.bytes;
+    if (r.a) g_pool.push_back(r.a);
+    if (r.b) g_pool.push_back(r.b);
+  }
+  g_recs.clear();
+  const int n = (int)agg.size();
+  for (int i = 0; i < n && i < max_entries; ++i) out[i] = agg[i];
+  *n_entries = n;
+  return PIGAN_OK;
+}
+
+}  // extern "C"

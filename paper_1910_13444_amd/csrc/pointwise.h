@@ -1,0 +1,76 @@
+// Argument blocks and launchers of the memory-bound PI-GAN kernels.
+#pragma once
+#include "common.h"
+
+namespace pigan {
+
+template <class T> struct FirstArgs {
+  const float* p1; int64_t p_g; int in_dim; int d; int W;  // fp32 master W1 (row-major [W][in_dim])
+  const float* zp; int64_t zp_g;                           // per-sample z-projection + b1
+  const float* x; int64_t x_g; int x_shared; int64_t Pn;   // locations; Pn points per sample
+  T* out_a; T* out_h; int64_t o_g; int64_t ldo;
+  Seg seg;
+};
+
+struct ResidArgs {
+  const float* jY; int64_t jy_g; int64_t offY;   // Y jets: value at offY, d/dx_i at offY + (1+i)*plane
+  const float* jU; int64_t ju_g; int64_t offU;   // u jets: d/dx_i at offU+(1+i)*plane, d2 at offU+(1+d+i)*plane
+  int64_t plane; int64_t M; int d;
+  const float* f; int64_t f_g; float f_const;
+  float* r; int64_t r_g;
+  float* gY; float* gU;                          // cotangent vectors (same layout as the jets) or null
+  const float* w_group; float qscale;            // q = qscale * w_g * r
+  double* part;                                  // [G][blocks] partial sums of r^2, or null
+};
+
+template <class T> struct OutBwdArgs {
+  const T* A; T* dA; int64_t o_g; int64_t ldo;   // saved pre-activation of the top layer, its cotangent
+  const float* gbar; int64_t gb_g;               // output cotangents (jet layout)
+  const float* wout; int64_t w_g;                // w_out (W) followed by b_out
+  int W; int64_t ppb;                            // points per block
+  float* part; int n_slots; int slot0;           // [G][n_slots][W+1]
+  Seg seg;
+};
+
+template <class T> struct FirstBwdArgs {
+  const T* dA; int64_t a_g; int64_t lda;
+  int64_t n_sen; int64_t n_col;
+  int n_s; int P; int S; int W; int d; int nd1;
+  const float* xs; int64_t xs_g;                 // sensor locations [n_s][d]
+  const float* xc; int64_t xc_g;                 // collocation points of the chunk [S][P][d]
+  float* part;                                   // [G][S][7][W]
+};
+
+hipError_t launch_zproj(const float* p1, int64_t p_g, int in_dim, int d, int W, const float* z, int64_t z_g,
+                        int n_z, int S, float* zp, int64_t zp_g, int G, hipStream_t st);
+template <class T> hipError_t launch_first_fwd(int nd1, int nd2, const FirstArgs<T>& a, int G, hipStream_t st);
+template <class T>
+hipError_t launch_out_fwd(const T* H, int64_t h_g, int64_t ldh, int64_t R, int64_t n_value, int W,
+                          const float* wout, int64_t w_g, float* y, int64_t y_g, int G, hipStream_t st);
+hipError_t launch_residual(const ResidArgs& a, int G, hipStream_t st);
+int residual_blocks(int64_t M);
+hipError_t launch_sum_partials(const double* part, int nb, double* acc, int acc_stride, int slot, int G,
+                               hipStream_t st);
+template <class T>
+hipError_t launch_snap_fill(const float* yY, int64_t yY_g, const float* yU, int64_t yU_g, int nY, int nU,
+                            int n_fake, const float* real, int64_t real_g, int n_real, int n_in, T* X,
+                            int64_t x_g, int ldx, int G, hipStream_t st);
+hipError_t launch_disc_seed(const float* score, int64_t sc_g, int n_fake, int n_real, int S_total, int B_total,
+                            const float* w_group, float loss_scale, float* seed, double* acc, int acc_stride,
+                            int G, hipStream_t st);
+int out_bwd_blocks(int64_t n_points, int ppb);
+template <class T> hipError_t launch_out_bwd(int nd1, int nd2, const OutBwdArgs<T>& a, int G, hipStream_t st);
+hipError_t launch_reduce_slots(const float* part, int n_slots, int W, float* dst, int64_t d_g, int accumulate,
+                               float scale, int32_t* nonfinite, int G, hipStream_t st);
+template <class T> hipError_t launch_first_bwd(const FirstBwdArgs<T>& a, int G, hipStream_t st);
+hipError_t launch_first_wgrad(const float* part, int S, int W, int d, int nd1, int in_dim, const float* z,
+                              int64_t z_g, int n_z, float* grad, int64_t g_g, int accumulate, float scale,
+                              int32_t* nonfinite, int G, hipStream_t st);
+hipError_t launch_losses(const double* acc, int acc_stride, const float* w_group, int S, int B, int64_t SP,
+                         float lambda_pde, float* loss, int32_t* nonfinite, int G, hipStream_t st);
+hipError_t launch_zero(double* acc, int n, int32_t* flag, hipStream_t st);
+template <class T>
+hipError_t launch_cast(const float* src, int64_t s_g, int N, int K, int Kp, T* dst, T* dstT, int64_t d_g, int G,
+                       hipStream_t st);
+
+}  // namespace pigan

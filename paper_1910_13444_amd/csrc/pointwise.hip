@@ -1,0 +1,624 @@
+// Memory-bound kernels of the PI-GAN step for gfx950: the generator's first
+// layer (z-projection hoisted per sample, derivative seeds are columns of
+// W1), the scalar output layer, the Darcy residual and its cotangents, the
+// output-layer reverse pass, the first-layer weight gradient, discriminator
+// score cotangents, losses, weight casts.  All reductions are fixed-order
+// (partial sums per block, then an ordered sum), never atomics.
+#include "pointwise.h"
+
+namespace pigan {
+
+// ---------------------------------------------------------------------------
+// zp[g][s][n] = b1[n] + sum_j W1[n][d + j] z[g][s][j]      (fp32)
+// ---------------------------------------------------------------------------
+__global__ void k_zproj(const float* __restrict__ p1, int64_t p_g, int in_dim, int d, int W,
+                        const float* __restrict__ z, int64_t z_g, int n_z, int S, float* __restrict__ zp,
+                        int64_t zp_g) {
+  const int g = blockIdx.z;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)S * W) return;
+  const int s = (int)(idx / W), n = (int)(idx % W);
+  const float* Wn = p1 + g * p_g + (int64_t)n * in_dim + d;
+  const float* zs = z + g * z_g + (int64_t)s * n_z;
+  float a = p1[g * p_g + (int64_t)W * in_dim + n];
+  for (int j = 0; j < n_z; ++j) a += Wn[j] * zs[j];
+  zp[g * zp_g + idx] = a;
+}
+
+// ---------------------------------------------------------------------------
+// first layer: a = zp[s] + W1[:, :d] x ; a'_i = W1[:, i] ; a''_i = 0
+// ---------------------------------------------------------------------------
+template <class T, int ND1, int ND2>
+__global__ void k_first_fwd(FirstArgs<T> p) {
+  constexpr int C = 1 + ND1 + ND2;
+  const int g = blockIdx.z;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int W = p.W;
+  if (idx >= p.seg.n_points * W) return;
+  const int64_t pt = idx / W;
+  const int n = (int)(idx % W);
+  const int64_t s = pt / p.Pn;
+  const int64_t xr = p.x_shared ? pt % p.Pn : pt;
+  const float* xv = p.x + g * p.x_g + xr * p.d;
+  const float* Wn = p.p1 + g * p.p_g + (int64_t)n * p.in_dim;
+  float a = p.zp[g * p.zp_g + s * W + n];
+  for (int i = 0; i < p.d; ++i) a += Wn[i] * xv[i];
+  float t, sd;
+  tanh_ts(a, t, sd);
+  const float sp = -2.0f * t * sd;
+  int64_t o[C];
+#pragma unroll
+  for (int k = 0; k < C; ++k) o[k] = g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + n;
+  if (p.out_a) {
+    p.out_a[o[0]] = Elem<T>::from_f(a);
+#pragma unroll
+    for (int i = 0; i < ND1; ++i) p.out_a[o[1 + i]] = Elem<T>::from_f(Wn[i]);
+#pragma unroll
+    for (int i = 0; i < ND2; ++i) p.out_a[o[1 + ND1 + i]] = Elem<T>::from_f(0.0f);
+  }
+  p.out_h[o[0]] = Elem<T>::from_f(t);
+#pragma unroll
+  for (int i = 0; i < ND1; ++i) p.out_h[o[1 + i]] = Elem<T>::from_f(sd * Wn[i]);
+#pragma unroll
+  for (int i = 0; i < ND2; ++i) p.out_h[o[1 + ND1 + i]] = Elem<T>::from_f(sp * Wn[i] * Wn[i]);
+}
+
+// ---------------------------------------------------------------------------
+// scalar output layer: y[row] = w_out . H[row] (+ b_out on value rows)
+// eight lanes per row, 16-byte loads, shuffle reduction
+// ---------------------------------------------------------------------------
+template <class T>
+__global__ void __launch_bounds__(256)
+k_out_fwd(const T* __restrict__ H, int64_t h_g, int64_t ldh, int64_t R, int64_t n_value, int W,
+          const float* __restrict__ wout, int64_t w_g, float* __restrict__ y, int64_t y_g) {
+  constexpr int EPP = 16 / (int)sizeof(T);
+  const int g = blockIdx.z;
+  const int team = threadIdx.x >> 3, e = threadIdx.x & 7;
+  const int64_t row = (int64_t)blockIdx.x * 32 + team;
+  const float* w = wout + g * w_g;
+  float acc = 0.0f;
+  if (row < R) {
+    const T* hr = H + g * h_g + row * ldh;
+    for (int c = e * EPP; c < W; c += 8 * EPP) {
+      uint4 v = *(const uint4*)(hr + c);
+      const T* hv = (const T*)&v;
+#pragma unroll
+      for (int q = 0; q < EPP; ++q) acc += w[c + q] * Elem<T>::to_f(hv[q]);
+    }
+  }
+  acc += __shfl_xor(acc, 1);
+  acc += __shfl_xor(acc, 2);
+  acc += __shfl_xor(acc, 4);
+  if (row < R && e == 0) y[g * y_g + row] = acc + (row < n_value ? w[W] : 0.0f);
+}
+
+// ---------------------------------------------------------------------------
+// Darcy residual r = -exp(Y)(sum_i dY_i dU_i + sum_i ddU_i) - f  and the
+// cotangents of L_pde = w lambda mean r^2 with respect to the jets:
+//   q = 2 w lambda r / (S P);   gY = q (r + f);  g dY_i = -q e^Y dU_i;
+//   g dU_i = -q e^Y dY_i;  g ddU_i = -q e^Y;  g U = 0.
+// Per-block partial sums of r^2 (double) for the loss.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256)
+k_residual(ResidArgs p) {
+  __shared__ double red[256];
+  const int g = blockIdx.z;
+  const int64_t pt = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  double r2 = 0.0;
+  if (pt < p.M) {
+    const float* jy = p.jY + g * p.jy_g + p.offY;
+    const float* ju = p.jU + g * p.ju_g + p.offU;
+    const float Y = jy[pt];
+    const float f = p.f ? p.f[g * p.f_g + pt] : p.f_const;
+    float flux = 0.0f;
+    for (int i = 0; i < p.d; ++i) flux += jy[(1 + i) * p.plane + pt] * ju[(1 + i) * p.plane + pt];
+    for (int i = 0; i < p.d; ++i) flux += ju[(1 + p.d + i) * p.plane + pt];
+    const float eY = expf(Y);
+    const float r = -eY * flux - f;
+    if (p.r) p.r[g * p.r_g + pt] = r;
+    r2 = (double)r * (double)r;
+    if (p.gY) {
+      const float w = p.w_group ? p.w_group[g] : 1.0f;
+      const float q = p.qscale * w * r;
+      float* gy = p.gY + g * p.jy_g + p.offY;
+      float* gu = p.gU + g * p.ju_g + p.offU;
+      gy[pt] = q * (r + f);
+      gu[pt] = 0.0f;
+      for (int i = 0; i < p.d; ++i) {
+        gy[(1 + i) * p.plane + pt] = -q * eY * ju[(1 + i) * p.plane + pt];
+        gu[(1 + i) * p.plane + pt] = -q * eY * jy[(1 + i) * p.plane + pt];
+        gu[(1 + p.d + i) * p.plane + pt] = -q * eY;
+      }
+    }
+  }
+  if (p.part) {
+    red[threadIdx.x] = r2;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+      if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) p.part[(int64_t)g * gridDim.x + blockIdx.x] = red[0];
+  }
+}
+
+// acc[g*stride + slot] += sum_b part[g][b]   (one block per group, fixed order)
+__global__ void __launch_bounds__(256)
+k_sum_partials(const double* __restrict__ part, int nb, double* acc, int acc_stride, int slot) {
+  __shared__ double red[256];
+  const int g = blockIdx.x;
+  double s = 0.0;
+  for (int b = threadIdx.x; b < nb; b += 256) s += part[(int64_t)g * nb + b];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) acc[g * acc_stride + slot] += red[0];
+}
+
+// ---------------------------------------------------------------------------
+// discriminator input rows: fake snapshots [Y sensors | u sensors] from the
+// generator outputs (b < n_fake), then real snapshots; zero padded to ldx.
+// ---------------------------------------------------------------------------
+template <class T>
+__global__ void k_snap_fill(const float* __restrict__ yY, int64_t yY_g, const float* __restrict__ yU,
+                            int64_t yU_g, int nY, int nU, int n_fake, const float* __restrict__ real,
+                            int64_t real_g, int n_real, int n_in, T* __restrict__ X, int64_t x_g, int ldx) {
+  const int g = blockIdx.z;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int B = n_fake + n_real;
+  if (idx >= (int64_t)B * ldx) return;
+  const int b = (int)(idx / ldx), j = (int)(idx % ldx);
+  float v = 0.0f;
+  if (j < n_in) {
+    if (b < n_fake) {
+      v = j < nY ? yY[g * yY_g + (int64_t)b * nY + j] : yU[g * yU_g + (int64_t)b * nU + (j - nY)];
+    } else {
+      v = real[g * real_g + (int64_t)(b - n_fake) * n_in + j];
+    }
+  }
+  X[g * x_g + idx] = Elem<T>::from_f(v);
+}
+
+// ---------------------------------------------------------------------------
+// critic cotangents and score sums (one block per group):
+//   dL_D/dD(fake_s) = w/S,  dL_D/dD(real_b) = -w/B_r   (times the loss scale)
+//   acc[g][0] += sum D(fake), acc[g][1] += sum D(real)
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256)
+k_disc_seed(const float* __restrict__ score, int64_t sc_g, int n_fake, int n_real, int S_total, int B_total,
+            const float* __restrict__ w_group, float loss_scale, float* __restrict__ seed, double* acc,
+            int acc_stride) {
+  __shared__ double red[2][256];
+  const int g = blockIdx.x;
+  const float w = w_group ? w_group[g] : 1.0f;
+  double sf = 0.0, sr = 0.0;
+  for (int b = threadIdx.x; b < n_fake + n_real; b += 256) {
+    const float v = score[g * sc_g + b];
+    if (b < n_fake) {
+      sf += v;
+      seed[g * sc_g + b] = loss_scale * w / (float)S_total;
+    } else {
+      sr += v;
+      seed[g * sc_g + b] = -loss_scale * w / (float)B_total;
+    }
+  }
+  red[0][threadIdx.x] = sf;
+  red[1][threadIdx.x] = sr;
+  __syncthreads();
+  for (int k = 128; k > 0; k >>= 1) {
+    if ((int)threadIdx.x < k) {
+      red[0][threadIdx.x] += red[0][threadIdx.x + k];
+      red[1][threadIdx.x] += red[1][threadIdx.x + k];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    acc[g * acc_stride + 0] += red[0][0];
+    acc[g * acc_stride + 1] += red[1][0];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// output layer reverse pass for one segment of points:
+//   dH_k[pt][n] = gbar_k[pt] w_out[n]  -> carry reverse with the saved A_L
+//   partial dw_out[n] = sum gbar_k h_k (h recomputed from A_L),
+//   partial db_out   = sum over value rows of gbar_0.
+// Threads: TPP = min(W,256) per point, 256/TPP points per pass, W/256 columns
+// per thread when W > 256.
+// ---------------------------------------------------------------------------
+template <class T, int ND1, int ND2>
+__global__ void __launch_bounds__(256)
+k_out_bwd(OutBwdArgs<T> p) {
+  constexpr int C = 1 + ND1 + ND2;
+  constexpr int MAXC = 16;
+  __shared__ float red[256 * 2];
+  const int g = blockIdx.z;
+  const int W = p.W;
+  const int TPP = W < 256 ? W : 256;
+  const int PPP = 256 / TPP;
+  const int NC = W > 256 ? W / 256 : 1;
+  const int lt = threadIdx.x % TPP;
+  const int lp = threadIdx.x / TPP;
+  const int64_t pbeg = (int64_t)blockIdx.x * p.ppb;
+  int64_t pend = pbeg + p.ppb;
+  if (pend > p.seg.n_points) pend = p.seg.n_points;
+  const float* w = p.wout + g * p.w_g;
+  const float* gb = p.gbar + g * p.gb_g;
+  float dw[MAXC];
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) dw[c] = 0.0f;
+  float db = 0.0f;
+  for (int64_t pt = pbeg + lp; pt < pend; pt += PPP) {
+    float gk[C];
+#pragma unroll
+    for (int k = 0; k < C; ++k) gk[k] = gb[p.seg.row0 + k * p.seg.plane + pt];
+    if (lt == 0) db += gk[0];
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+      if (c >= NC) continue;
+      const int n = lt + 256 * c;
+      const float wn = w[n];
+      float ap[C];
+      int64_t o[C];
+#pragma unroll
+      for (int k = 0; k < C; ++k) {
+        o[k] = g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + n;
+        ap[k] = Elem<T>::to_f(p.A[o[k]]);
+      }
+      float t, s;
+      tanh_ts(ap[0], t, s);
+      const float sp = -2.0f * t * s;
+      const float spp = 2.0f * s * (3.0f * t * t - 1.0f);
+      // activations (for dw_out)
+      float hsum = gk[0] * t;
+#pragma unroll
+      for (int i = 0; i < ND1; ++i) hsum += gk[1 + i] * s * ap[1 + i];
+#pragma unroll
+      for (int i = 0; i < ND2; ++i) hsum += gk[1 + ND1 + i] * (s * ap[1 + ND1 + i] + sp * ap[1 + i] * ap[1 + i]);
+      dw[c] += hsum;
+      // carry reverse
+      float ga = s * gk[0] * wn;
+#pragma unroll
+      for (int i = 0; i < ND1; ++i) ga += sp * ap[1 + i] * gk[1 + i] * wn;
+#pragma unroll
+      for (int i = 0; i < ND2; ++i) ga += (sp * ap[1 + ND1 + i] + spp * ap[1 + i] * ap[1 + i]) * gk[1 + ND1 + i] * wn;
+      p.dA[o[0]] = Elem<T>::from_f(ga);
+#pragma unroll
+      for (int i = 0; i < ND1; ++i) {
+        float gd = s * gk[1 + i] * wn;
+        if (i < ND2) gd += 2.0f * sp * ap[1 + i] * gk[1 + ND1 + i] * wn;
+        p.dA[o[1 + i]] = Elem<T>::from_f(gd);
+      }
+#pragma unroll
+      for (int i = 0; i < ND2; ++i) p.dA[o[1 + ND1 + i]] = Elem<T>::from_f(s * gk[1 + ND1 + i] * wn);
+    }
+  }
+  // block reduction over the PPP point lanes, fixed order
+  float* pw = p.part + ((int64_t)g * p.n_slots + p.slot0 + blockIdx.x) * (W + 1);
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    if (c >= NC) continue;
+    red[threadIdx.x] = dw[c];
+    __syncthreads();
+    if (lp == 0) {
+      float s = 0.0f;
+      for (int q = 0; q < PPP; ++q) s += red[q * TPP + lt];
+      pw[lt + 256 * c] = s;
+    }
+    __syncthreads();
+  }
+  red[threadIdx.x] = db;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float s = 0.0f;
+    for (int q = 0; q < PPP; ++q) s += red[q * TPP];
+    pw[W] = s;
+  }
+}
+
+// dst[g][n] (+)= scale * sum_slot part[g][slot][n]  for n <= W (n == W: bias)
+__global__ void __launch_bounds__(256)
+k_reduce_slots(const float* __restrict__ part, int n_slots, int W, float* dst, int64_t d_g, int accumulate,
+               float scale, int32_t* nonfinite) {
+  const int g = blockIdx.z;
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n > W) return;
+  const float* src = part + (int64_t)g * n_slots * (W + 1) + n;
+  float s = 0.0f;
+  for (int q = 0; q < n_slots; ++q) s += src[(int64_t)q * (W + 1)];
+  s *= scale;
+  float* o = dst + g * d_g + n;
+  if (accumulate) s += *o;
+  *o = s;
+  if (!__builtin_isfinite(s)) *nonfinite = 1;
+}
+
+// ---------------------------------------------------------------------------
+// first-layer reverse pass, per sample s and column n:
+//   gs   = sum over value rows of s of dA_1
+//   gx_i = sum over value rows of s of dA_1 * x_i
+//   gd_i = sum over d/dx_i rows of s of dA_1   (a'_i = W1[:, i])
+// part[g][s][q][n] with q = 0 (gs), 1..3 (gx_i), 4..6 (gd_i); unused slots 0
+// ---------------------------------------------------------------------------
+template <class T>
+__global__ void __launch_bounds__(256)
+k_first_bwd(FirstBwdArgs<T> p) {
+  __shared__ float red[256];
+  const int g = blockIdx.z;
+  const int s = blockIdx.x;
+  const int W = p.W;
+  const int TPP = W < 256 ? W : 256;
+  const int PPP = 256 / TPP;
+  const int lt = threadIdx.x % TPP;
+  const int lp = threadIdx.x / TPP;
+  const int n = blockIdx.y * 256 + lt;
+  const int d = p.d;
+  float acc[7];
+#pragma unroll
+  for (int q = 0; q < 7; ++q) acc[q] = 0.0f;
+  const T* A = p.dA + g * p.a_g;
+  if (n < W) {
+    // sensor rows of sample s (value stream only)
+    for (int j = lp; j < p.n_s; j += PPP) {
+      const float v = Elem<T>::to_f(A[((int64_t)s * p.n_s + j) * p.lda + n]);
+      const float* xv = p.xs + g * p.xs_g + (int64_t)j * d;
+      acc[0] += v;
+#pragma unroll
+      for (int i = 0; i < 3; ++i)
+        if (i < d) acc[1 + i] += v * xv[i];
+    }
+    // collocation rows of sample s
+    for (int q = lp; q < p.P; q += PPP) {
+      const int64_t pt = (int64_t)s * p.P + q;
+      const float v = Elem<T>::to_f(A[(p.n_sen + pt) * p.lda + n]);
+      const float* xv = p.xc + g * p.xc_g + pt * d;
+      acc[0] += v;
+#pragma unroll
+      for (int i = 0; i < 3; ++i)
+        if (i < d) acc[1 + i] += v * xv[i];
+#pragma unroll
+      for (int i = 0; i < 3; ++i)
+        if (i < p.nd1) acc[4 + i] += Elem<T>::to_f(A[(p.n_sen + (1 + i) * p.n_col + pt) * p.lda + n]);
+    }
+  }
+  float* out = p.part + (((int64_t)g * p.S + s) * 7) * W;
+#pragma unroll
+  for (int q = 0; q < 7; ++q) {
+    red[threadIdx.x] = acc[q];
+    __syncthreads();
+    if (lp == 0 && n < W) {
+      float v = 0.0f;
+      for (int u = 0; u < PPP; ++u) v += red[u * TPP + lt];
+      out[(int64_t)q * W + n] = v;
+    }
+    __syncthreads();
+  }
+}
+
+// dW1[n][c] and db1[n] from the per-sample partials:
+//   c < d : sum_s gx_c + gd_c ;  c >= d : sum_s gs z_s[c-d] ;  bias: sum_s gs
+__global__ void __launch_bounds__(256)
+k_first_wgrad(const float* __restrict__ part, int S, int W, int d, int nd1, int in_dim,
+              const float* __restrict__ z, int64_t z_g, int n_z, float* grad, int64_t g_g, int accumulate,
+              float scale, int32_t* nonfinite) {
+  const int g = blockIdx.z;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t nW = (int64_t)W * in_dim;
+  if (idx >= nW + W) return;
+  const float* pp = part + (int64_t)g * S * 7 * W;
+  float v = 0.0f;
+  int64_t o;
+  if (idx < nW) {
+    const int n = (int)(idx / in_dim), c = (int)(idx % in_dim);
+    if (c < d) {
+      for (int s = 0; s < S; ++s) {
+        v += pp[((int64_t)s * 7 + 1 + c) * W + n];
+        if (c < nd1) v += pp[((int64_t)s * 7 + 4 + c) * W + n];
+      }
+    } else {
+      const float* zz = z + g * z_g + (c - d);
+      for (int s = 0; s < S; ++s) v += pp[((int64_t)s * 7) * W + n] * zz[(int64_t)s * n_z];
+    }
+    o = idx;
+  } else {
+    const int n = (int)(idx - nW);
+    for (int s = 0; s < S; ++s) v += pp[((int64_t)s * 7) * W + n];
+    o = nW + n;
+  }
+  v *= scale;
+  float* dst = grad + g * g_g + o;
+  if (accumulate) v += *dst;
+  *dst = v;
+  if (!__builtin_isfinite(v)) *nonfinite = 1;
+}
+
+// ---------------------------------------------------------------------------
+// losses from the accumulated sums (double): acc[g] = {sum D(fake),
+// sum D(real), sum r^2}
+// ---------------------------------------------------------------------------
+__global__ void k_losses(const double* __restrict__ acc, int acc_stride, const float* __restrict__ w_group,
+                         int S, int B, int64_t SP, float lambda_pde, float* loss, int32_t* nonfinite, int G) {
+  const int g = blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= G) return;
+  const double w = w_group ? (double)w_group[g] : 1.0;
+  const double* a = acc + g * acc_stride;
+  const double LD = w * (a[0] / S - a[1] / B);
+  const double La = -w * a[0] / S;
+  const double Lp = w * (double)lambda_pde * a[2] / (double)SP;
+  loss[3 * g + 0] = (float)LD;
+  loss[3 * g + 1] = (float)La;
+  loss[3 * g + 2] = (float)Lp;
+  if (!__builtin_isfinite(LD) || !__builtin_isfinite(La) || !__builtin_isfinite(Lp)) *nonfinite = 1;
+}
+
+__global__ void k_zero(double* acc, int n, int32_t* flag) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) acc[i] = 0.0;
+  if (i == 0 && flag) *flag = 0;
+}
+
+// ---------------------------------------------------------------------------
+// weight casts: src fp32 [N][K] -> dst [N][Kp] (zero padded) and optionally
+// dstT [Kp][N]
+// ---------------------------------------------------------------------------
+template <class T>
+__global__ void k_cast(const float* __restrict__ src, int64_t s_g, int N, int K, int Kp, T* __restrict__ dst,
+                       T* __restrict__ dstT, int64_t d_g) {
+  const int g = blockIdx.z;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)N * Kp) return;
+  const int n = (int)(idx / Kp), k = (int)(idx % Kp);
+  const float v = k < K ? src[g * s_g + (int64_t)n * K + k] : 0.0f;
+  const T tv = Elem<T>::from_f(v);
+  if (dst) dst[g * d_g + idx] = tv;
+  if (dstT) dstT[g * d_g + (int64_t)k * N + n] = tv;
+}
+
+// ===========================================================================
+// host launchers
+// ===========================================================================
+static inline unsigned nblk(int64_t n, int b) { return (unsigned)((n + b - 1) / b); }
+
+hipError_t launch_zproj(const float* p1, int64_t p_g, int in_dim, int d, int W, const float* z, int64_t z_g,
+                        int n_z, int S, float* zp, int64_t zp_g, int G, hipStream_t st) {
+  k_zproj<<<dim3(nblk((int64_t)S * W, 256), 1, G), 256, 0, st>>>(p1, p_g, in_dim, d, W, z, z_g, n_z, S, zp, zp_g);
+  return hipGetLastError();
+}
+
+template <class T>
+hipError_t launch_first_fwd(int nd1, int nd2, const FirstArgs<T>& a, int G, hipStream_t st) {
+  if (a.seg.n_points <= 0) return hipSuccess;
+  dim3 grid(nblk(a.seg.n_points * a.W, 256), 1, G);
+  switch (nd1 * 10 + nd2) {
+    case 0: k_first_fwd<T, 0, 0><<<grid, 256, 0, st>>>(a); break;
+    case 10: k_first_fwd<T, 1, 0><<<grid, 256, 0, st>>>(a); break;
+    case 20: k_first_fwd<T, 2, 0><<<grid, 256, 0, st>>>(a); break;
+    case 30: k_first_fwd<T, 3, 0><<<grid, 256, 0, st>>>(a); break;
+    case 11: k_first_fwd<T, 1, 1><<<grid, 256, 0, st>>>(a); break;
+    case 22: k_first_fwd<T, 2, 2><<<grid, 256, 0, st>>>(a); break;
+    case 33: k_first_fwd<T, 3, 3><<<grid, 256, 0, st>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <class T>
+hipError_t launch_out_fwd(const T* H, int64_t h_g, int64_t ldh, int64_t R, int64_t n_value, int W,
+                          const float* wout, int64_t w_g, float* y, int64_t y_g, int G, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  k_out_fwd<T><<<dim3(nblk(R, 32), 1, G), 256, 0, st>>>(H, h_g, ldh, R, n_value, W, wout, w_g, y, y_g);
+  return hipGetLastError();
+}
+
+hipError_t launch_residual(const ResidArgs& a, int G, hipStream_t st) {
+  if (a.M <= 0) return hipSuccess;
+  k_residual<<<dim3(nblk(a.M, 256), 1, G), 256, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+int residual_blocks(int64_t M) { return (int)nblk(M, 256); }
+
+hipError_t launch_sum_partials(const double* part, int nb, double* acc, int acc_stride, int slot, int G,
+                               hipStream_t st) {
+  k_sum_partials<<<G, 256, 0, st>>>(part, nb, acc, acc_stride, slot);
+  return hipGetLastError();
+}
+
+template <class T>
+hipError_t launch_snap_fill(const float* yY, int64_t yY_g, const float* yU, int64_t yU_g, int nY, int nU,
+                            int n_fake, const float* real, int64_t real_g, int n_real, int n_in, T* X,
+                            int64_t x_g, int ldx, int G, hipStream_t st) {
+  const int64_t tot = (int64_t)(n_fake + n_real) * ldx;
+  if (tot <= 0) return hipSuccess;
+  k_snap_fill<T><<<dim3(nblk(tot, 256), 1, G), 256, 0, st>>>(yY, yY_g, yU, yU_g, nY, nU, n_fake, real, real_g,
+                                                             n_real, n_in, X, x_g, ldx);
+  return hipGetLastError();
+}
+
+hipError_t launch_disc_seed(const float* score, int64_t sc_g, int n_fake, int n_real, int S_total, int B_total,
+                            const float* w_group, float loss_scale, float* seed, double* acc, int acc_stride,
+                            int G, hipStream_t st) {
+  k_disc_seed<<<G, 256, 0, st>>>(score, sc_g, n_fake, n_real, S_total, B_total, w_group, loss_scale, seed, acc,
+                                 acc_stride);
+  return hipGetLastError();
+}
+
+int out_bwd_blocks(int64_t n_points, int ppb) { return (int)nblk(n_points, ppb); }
+
+template <class T>
+hipError_t launch_out_bwd(int nd1, int nd2, const OutBwdArgs<T>& a, int G, hipStream_t st) {
+  if (a.seg.n_points <= 0) return hipSuccess;
+  dim3 grid(nblk(a.seg.n_points, a.ppb), 1, G);
+  switch (nd1 * 10 + nd2) {
+    case 0: k_out_bwd<T, 0, 0><<<grid, 256, 0, st>>>(a); break;
+    case 10: k_out_bwd<T, 1, 0><<<grid, 256, 0, st>>>(a); break;
+    case 20: k_out_bwd<T, 2, 0><<<grid, 256, 0, st>>>(a); break;
+    case 30: k_out_bwd<T, 3, 0><<<grid, 256, 0, st>>>(a); break;
+    case 11: k_out_bwd<T, 1, 1><<<grid, 256, 0, st>>>(a); break;
+    case 22: k_out_bwd<T, 2, 2><<<grid, 256, 0, st>>>(a); break;
+    case 33: k_out_bwd<T, 3, 3><<<grid, 256, 0, st>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_slots(const float* part, int n_slots, int W, float* dst, int64_t d_g, int accumulate,
+                               float scale, int32_t* nonfinite, int G, hipStream_t st) {
+  k_reduce_slots<<<dim3(nblk(W + 1, 256), 1, G), 256, 0, st>>>(part, n_slots, W, dst, d_g, accumulate, scale,
+                                                              nonfinite);
+  return hipGetLastError();
+}
+
+template <class T>
+hipError_t launch_first_bwd(const FirstBwdArgs<T>& a, int G, hipStream_t st) {
+  if (a.S <= 0) return hipSuccess;
+  dim3 grid(a.S, nblk(a.W, 256), G);
+  k_first_bwd<T><<<grid, 256, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_first_wgrad(const float* part, int S, int W, int d, int nd1, int in_dim, const float* z,
+                              int64_t z_g, int n_z, float* grad, int64_t g_g, int accumulate, float scale,
+                              int32_t* nonfinite, int G, hipStream_t st) {
+  const int64_t tot = (int64_t)W * in_dim + W;
+  k_first_wgrad<<<dim3(nblk(tot, 256), 1, G), 256, 0, st>>>(part, S, W, d, nd1, in_dim, z, z_g, n_z, grad, g_g,
+                                                             accumulate, scale, nonfinite);
+  return hipGetLastError();
+}
+
+hipError_t launch_losses(const double* acc, int acc_stride, const float* w_group, int S, int B, int64_t SP,
+                         float lambda_pde, float* loss, int32_t* nonfinite, int G, hipStream_t st) {
+  k_losses<<<nblk(G, 64), 64, 0, st>>>(acc, acc_stride, w_group, S, B, SP, lambda_pde, loss, nonfinite, G);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero(double* acc, int n, int32_t* flag, hipStream_t st) {
+  k_zero<<<nblk(n > 1 ? n : 1, 256), 256, 0, st>>>(acc, n, flag);
+  return hipGetLastError();
+}
+
+template <class T>
+hipError_t launch_cast(const float* src, int64_t s_g, int N, int K, int Kp, T* dst, T* dstT, int64_t d_g, int G,
+                       hipStream_t st) {
+  k_cast<T><<<dim3(nblk((int64_t)N * Kp, 256), 1, G), 256, 0, st>>>(src, s_g, N, K, Kp, dst, dstT, d_g);
+  return hipGetLastError();
+}
+
+#define PIGAN_INST(T)                                                                                         \
+  template hipError_t launch_first_fwd<T>(int, int, const FirstArgs<T>&, int, hipStream_t);                  \
+  template hipError_t launch_out_fwd<T>(const T*, int64_t, int64_t, int64_t, int64_t, int, const float*,       \
+                                        int64_t, float*, int64_t, int, hipStream_t);                          \
+  template hipError_t launch_snap_fill<T>(const float*, int64_t, const float*, int64_t, int, int, int,         \
+                                          const float*, int64_t, int, int, T*, int64_t, int, int, hipStream_t); \
+  template hipError_t launch_out_bwd<T>(int, int, const OutBwdArgs<T>&, int, hipStream_t);                    \
+  template hipError_t launch_first_bwd<T>(const FirstBwdArgs<T>&, int, hipStream_t);                          \
+  template hipError_t launch_cast<T>(const float*, int64_t, int, int, int, T*, T*, int64_t, int, hipStream_t);
+PIGAN_INST(float)
+PIGAN_INST(bf16)
+PIGAN_INST(f16)
+#undef PIGAN_INST
+
+}  // namespace pigan

@@ -1,0 +1,81 @@
+"""Helpers of the GPU parity tests: run the HIP path through the C-ABI and
+compare it tensor by tensor with the fp64 oracle."""
+from __future__ import annotations
+
+import numpy as np
+
+TOL = {"fp32": 1e-5, "bf16": 2e-2, "fp16": 2e-2}
+
+
+def rel(a, b) -> float:
+    a = np.asarray(a, np.float64).ravel()
+    b = np.asarray(b, np.float64).ravel()
+    den = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / den) if den > 0 else float(np.linalg.norm(a))
+
+
+def param_slices(in_dim, L, W):
+    """(name, slice) of every weight tensor in the packed parameter vector."""
+    out = []
+    off = 0
+    fan = in_dim
+    for l in range(1, L + 1):
+        out.append((f"W{l}", slice(off, off + W * fan)))
+        off += W * fan
+        out.append((f"b{l}", slice(off, off + W)))
+        off += W
+        fan = W
+    out.append(("w_out", slice(off, off + W)))
+    out.append(("b_out", slice(off + W, off + W + 1)))
+    return out
+
+
+def grad_errors(g_gpu, g_ref, shape, prefix):
+    errs = {}
+    G = g_ref.shape[0]
+    for name, sl in param_slices(*shape):
+        if name == "b_out" and shape is not None:
+            # a single scalar per group: compare all groups together
+            errs[f"{prefix}.{name}"] = rel(g_gpu[:, sl], g_ref[:, sl])
+            continue
+        errs[f"{prefix}.{name}"] = max(rel(g_gpu[g, sl], g_ref[g, sl]) for g in range(G))
+    return errs
+
+
+def check(errs: dict, tol: float, label: str = ""):
+    bad = {k: v for k, v in errs.items() if not (v <= tol)}
+    worst = sorted(errs.items(), key=lambda kv: -kv[1])[:6]
+    msg = f"{label} tol={tol:g} worst: " + ", ".join(f"{k}={v:.3g}" for k, v in worst)
+    print(msg)
+    assert not bad, msg
+
+
+def to_dev(a, dev="cuda"):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+
+
+def run_step_gpu(wl, inp, real, chunk_S=0, dtype=None, loss_scale=1.0, lambda_pde=None):
+    """One training step through pigan_train_step_grads; returns numpy outputs."""
+    import torch
+    from paper_1910_13444_amd import pigan
+    S = inp.z.shape[1]
+    desc = pigan.step_desc(wl, S=S, B_r=real.shape[1], chunk_S=chunk_S, dtype=dtype, loss_scale=loss_scale,
+                           lambda_pde=lambda_pde)
+    step = pigan.TrainStep(desc)
+    o = step(to_dev(inp.pY), to_dev(inp.pU), to_dev(inp.pD), to_dev(inp.z), to_dev(inp.xc), to_dev(inp.xsY),
+             to_dev(inp.xsU), to_dev(real), f=None if inp.f is None else to_dev(inp.f), f_const=inp.f_const,
+             w_group=to_dev(inp.w_group))
+    torch.cuda.synchronize()
+    return dict(gY=o.gY.cpu().numpy(), gU=o.gU.cpu().numpy(), gD=o.gD.cpu().numpy(), loss=o.loss.cpu().numpy(),
+                nonfinite=int(o.nonfinite.cpu().item()))
+
+
+def step_errors(wl, out, ref):
+    errs = {}
+    errs.update(grad_errors(out["gY"], ref["gY"], wl.gen_shape(), "gY"))
+    errs.update(grad_errors(out["gU"], ref["gU"], wl.gen_shape(), "gU"))
+    errs.update(grad_errors(out["gD"], ref["gD"], wl.disc_shape(), "gD"))
+    for i, k in enumerate(("L_D", "L_adv", "L_pde")):
+        errs[k] = rel(out["loss"][:, i], ref["loss"][:, i])
+    return errs

@@ -1,0 +1,114 @@
+"""The C-ABI library loads, exports every symbol include/pigan.h declares, and
+rejects invalid arguments on the host before touching the device (these calls
+return before any HIP call, so they run without a GPU)."""
+import ctypes as C
+import os
+
+import pytest
+
+from paper_1910_13444_amd import configs, pigan
+
+pytestmark = pytest.mark.skipif(not os.path.exists(pigan.LIB_PATH), reason="libpigan.so not built")
+
+FAKE = C.c_void_p(4096)   # never dereferenced: every case below fails validation first
+
+
+def test_exports_every_declared_symbol():
+    L = pigan.lib()
+    names = pigan.declared_symbols()
+    assert "pigan_train_step_grads" in names and len(names) >= 11
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_n_params_matches_packing():
+    L = pigan.lib()
+    for wl in (configs.C1, configs.C2, configs.C5):
+        m = pigan.Mlp(1, wl.in_dim, wl.L, wl.W)
+        assert L.pigan_mlp_n_params(C.byref(m)) == configs.n_params(wl.in_dim, wl.L, wl.W)
+
+
+def _step(desc, ws_bytes, ptr=FAKE, f=None, wg=None):
+    L = pigan.lib()
+    args = [ptr] * 8
+    args[7] = f        # f may be null
+    return L.pigan_train_step_grads(C.byref(desc), *args[:7], f, 0.0, ptr, wg, ptr, ptr, ptr, ptr, ptr, ptr,
+                                    ws_bytes, None)
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("d", 0, pigan.EINVAL), ("d", 4, pigan.EINVAL), ("n_z", 0, pigan.EINVAL), ("S", 0, pigan.EINVAL),
+    ("P", -1, pigan.EINVAL), ("n_sY", 0, pigan.EINVAL), ("B_r", 0, pigan.EINVAL), ("chunk_S", -2, pigan.EINVAL),
+    ("lambda_gp", 0.5, pigan.ENOTSUP), ("loss_scale", 0.0, pigan.EINVAL), ("lambda_pde", -1.0, pigan.EINVAL),
+    ("dt", 7, pigan.EINVAL),
+])
+def test_step_rejects_bad_descriptor(field, value, status):
+    d = pigan.step_desc(configs.C1)
+    setattr(d, field, value)
+    assert _step(d, 1 << 40) == status
+    assert pigan.lib().pigan_last_error()
+    assert pigan.workspace_bytes(d) == 0
+
+
+def test_step_rejects_inconsistent_shapes():
+    d = pigan.step_desc(configs.C1)
+    d.genY.in_dim += 1
+    assert _step(d, 1 << 40) == pigan.EINVAL
+    d = pigan.step_desc(configs.C1)
+    d.disc.in_dim += 1
+    assert _step(d, 1 << 40) == pigan.EINVAL
+    d = pigan.step_desc(configs.C1)
+    d.genU.n_groups = 2
+    assert _step(d, 1 << 40) == pigan.EINVAL
+    d = pigan.step_desc(configs.C1)
+    d.genY.width = 48           # not a supported width
+    assert _step(d, 1 << 40) == pigan.ENOTSUP
+
+
+def test_step_rejects_null_and_small_workspace():
+    d = pigan.step_desc(configs.C1)
+    need = pigan.workspace_bytes(d)
+    assert need > 0
+    assert _step(d, need, ptr=None) == pigan.EINVAL           # null inputs
+    L = pigan.lib()
+    args = [FAKE] * 7
+    st = L.pigan_train_step_grads(C.byref(d), *args, None, 0.0, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                  need, None)
+    assert st == pigan.EWORKSPACE                               # null workspace
+    assert _step(d, need - 1) == pigan.EWORKSPACE
+    # misaligned workspace
+    st = L.pigan_train_step_grads(C.byref(d), *args, None, 0.0, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                  C.c_void_p(4096 + 16), need, None)
+    assert st == pigan.EINVAL
+
+
+def test_workspace_grows_with_chunk():
+    d = pigan.step_desc(configs.C2)
+    full = pigan.workspace_bytes(d)
+    d.chunk_S = 32
+    part = pigan.workspace_bytes(d)
+    assert 0 < part < full
+
+
+def test_auto_chunk_keeps_large_steps_bounded():
+    for wl in (configs.C3, configs.C5):
+        assert 0 < pigan.workspace_bytes(pigan.step_desc(wl)) <= (64 << 30)
+
+
+def test_gen_forward_and_disc_forward_validation():
+    L = pigan.lib()
+    net = pigan.Mlp(1, 6, 2, 32)
+    assert L.pigan_gen_forward_workspace(C.byref(net), 2, 4, 8, 2, 1) > 0
+    assert L.pigan_gen_forward_workspace(C.byref(net), 2, 4, 8, 3, 1) == 0   # order 3
+    st = L.pigan_gen_forward(C.byref(net), FAKE, 7, FAKE, FAKE, 0, 4, 8, 1, 1, FAKE, FAKE, 1 << 30, None)
+    assert st == pigan.EINVAL                                                 # in_dim <= d
+    st = L.pigan_gen_forward(C.byref(net), FAKE, 2, FAKE, FAKE, 0, 4, 8, 1, 1, FAKE, FAKE, 16, None)
+    assert st == pigan.EWORKSPACE
+    dnet = pigan.Mlp(1, 250, 3, 64)
+    assert L.pigan_disc_forward_workspace(C.byref(dnet), 16, 0) > 0
+    st = L.pigan_disc_forward(C.byref(dnet), FAKE, FAKE, 0, 0, FAKE, FAKE, 1 << 30, None)
+    assert st == pigan.EINVAL
+    st = L.pigan_pde_residual(0, 1, 10, FAKE, FAKE, None, 0.0, FAKE, None)
+    assert st == pigan.EINVAL
+    st = L.pigan_pde_residual(2, 1, 10, None, FAKE, None, 0.0, FAKE, None)
+    assert st == pigan.EINVAL
