@@ -1,0 +1,199 @@
+"""Benchmark of the PI-GAN training step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2]
+
+A step is one call of pigan_train_step_grads: both generators' jets at every
+(collocation point x noise sample) pair and at the sensors, the Darcy
+residual, the discriminator on fake and real snapshots, and every weight
+gradient.  Inputs are seeded synthetic data resident in HBM before the timed
+region starts.  Prints ONE JSON line on stdout; diagnostics go to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"bf16": 2516.6, "fp16": 2516.6, "fp32": 157.3}
+PEAK_GBS = 8000.0
+METRIC = "PI-GAN train-step TFLOP/s (bf16 MFMA) + collocation points/s, 1 MI355X"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def device_inputs(wl, dev):
+    import numpy as np
+    import torch
+
+    from paper_1910_13444_amd import pigan
+    from paper_1910_13444_amd.inputs import make_inputs
+
+    inp = make_inputs(wl)
+
+    def t(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+
+    d = dict(pY=t(inp.pY), pU=t(inp.pU), pD=t(inp.pD), z=t(inp.z), xc=t(inp.xc), xsY=t(inp.xsY),
+             xsU=t(inp.xsU), w_group=t(inp.w_group))
+    # real snapshots: the seeded teacher generators at the sensors, on the device
+    shape = wl.gen_shape()
+    zt = t(inp.z_teach)
+    yY = pigan.gen_forward(t(inp.tY), shape, wl.d, zt, d["xsY"], 0, dtype="fp32", x_shared=True)
+    yU = pigan.gen_forward(t(inp.tU), shape, wl.d, zt, d["xsU"], 0, dtype="fp32", x_shared=True)
+    d["real"] = torch.cat([yY[:, 0], yU[:, 0]], dim=-1).contiguous()
+    torch.cuda.synchronize()
+    return d, inp
+
+
+def run_steps(step, d, wl, k):
+    for _ in range(k):
+        step(d["pY"], d["pU"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["real"], f=None,
+             f_const=wl.f_const, w_group=d["w_group"])
+
+
+def cpu_baseline(wl, budget_s: float = 15.0):
+    """The fp64 oracle on a bounded sample of the same workload (S' noise
+    samples, all collocation points and sensors), scaled to TFLOP/s."""
+    import numpy as np
+
+    import oracle
+    from paper_1910_13444_amd import flops
+    from paper_1910_13444_amd.inputs import make_inputs
+
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+
+    def timed(S):
+        w2 = wl.with_(S=S, B_r=min(wl.B_r, S))
+        inp = make_inputs(w2)
+        real = np.random.default_rng(0).standard_normal((w2.G, w2.B_r, w2.n_in)).astype(np.float32)
+        t0 = time.perf_counter()
+        oracle.train_step(w2, inp, real)
+        return w2, time.perf_counter() - t0
+
+    w2, t2 = timed(min(2, wl.S))
+    S = int(max(1, min(wl.S, round(budget_s / max(t2, 1e-3) * w2.S))))
+    if S != w2.S:
+        w2, t2 = timed(S)
+    f = flops.step_flops(w2, S=w2.S, B_r=w2.B_r)
+    return {"value": f / t2 / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{w2.S} of {wl.S} noise samples (B_r={w2.B_r}), all {wl.P} collocation points "
+                      f"and all sensors per sample, fp64 NumPy, {t2:.2f} s",
+            "collocation_points_per_s": w2.G * w2.S * wl.P / t2}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c2")
+    ap.add_argument("--chunk-S", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true")
+    a = ap.parse_args()
+
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print(f"bench.py measures one GPU only: the PI-GAN step is built and timed on a single MI355X "
+              f"(requested --gpus {a.gpus}); multi-GPU runs are not part of this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_1910_13444_amd import configs, flops, pigan
+
+    wl = configs.get(a.workload)
+    dev = torch.device("cuda:0")
+    pigan.lib()
+    log(f"bench: workload {wl.name} dtype {wl.dtype} S={wl.S} P={wl.P} W={wl.W} L={wl.L}")
+    d, inp = device_inputs(wl, dev)
+    step = pigan.TrainStep(pigan.step_desc(wl, chunk_S=a.chunk_S), device=dev)
+    log(f"bench: workspace {step.ws_bytes / 2**30:.2f} GiB; warmup {a.warmup}")
+    run_steps(step, d, wl, a.warmup)
+    torch.cuda.synchronize()
+    nf = int(step.out.nonfinite.item())
+
+    # timed region
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    ev0.record()
+    run_steps(step, d, wl, a.steps)
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms = ev0.elapsed_time(ev1) / a.steps
+    log(f"bench: {a.steps} steps, {ms:.3f} ms/step (wall {wall * 1e3 / a.steps:.3f} ms/step)")
+
+    F = flops.step_flops(wl)
+    pts = flops.collocation_points(wl)
+    tflops = F / (ms * 1e-3) / 1e12
+
+    # per-kernel timing: the same steps again with HIP events around every launch
+    roof = None
+    kernels = None
+    if not a.no_profile:
+        pigan.profile_enable(True)
+        run_steps(step, d, wl, a.steps)
+        torch.cuda.synchronize()
+        stats = pigan.profile_read()
+        pigan.profile_enable(False)
+        tot = sum(s["total_ms"] for s in stats)
+        kernels = {s["name"]: {"launches_per_step": s["launches"] / a.steps,
+                               "ms_per_step": s["total_ms"] / a.steps,
+                               "share": s["total_ms"] / tot if tot else 0.0} for s in stats}
+        dom = max(stats, key=lambda s: s["total_ms"])
+        avg_ms = dom["total_ms"] / dom["launches"]
+        fl = dom["flops"] / dom["launches"]
+        by = dom["bytes"] / dom["launches"]
+        ridge = PEAK_TFLOPS[wl.dtype] * 1e12 / (PEAK_GBS * 1e9)
+        if by > 0 and fl / by < ridge:
+            ach = by / (avg_ms * 1e-3) / 1e9
+            roof = {"kernel": dom["name"], "bound": "hbm", "achieved": ach, "peak": PEAK_GBS, "unit": "GB/s",
+                    "frac": ach / PEAK_GBS, "traffic": None, "avg_launch_ms": avg_ms,
+                    "launches_per_step": dom["launches"] / a.steps, "alg_bytes_per_launch": by,
+                    "alg_flops_per_launch": fl}
+        else:
+            ach = fl / (avg_ms * 1e-3) / 1e12
+            pk = PEAK_TFLOPS[wl.dtype]
+            roof = {"kernel": dom["name"], "bound": "mfma", "achieved": ach, "peak": pk, "unit": "TFLOP/s",
+                    "frac": ach / pk, "traffic": None, "avg_launch_ms": avg_ms,
+                    "launches_per_step": dom["launches"] / a.steps, "alg_bytes_per_launch": by,
+                    "alg_flops_per_launch": fl}
+        for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
+            log(f"  {k:12s} {v['ms_per_step']:.4f} ms/step  {100 * v['share']:.1f}%  "
+                f"launches/step {v['launches_per_step']:.0f}")
+
+    cpu = None if a.no_cpu_baseline else cpu_baseline(wl)
+
+    out = {
+        "metric": METRIC, "value": tflops, "unit": "TFLOP/s", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": wl.name, "G": wl.G, "d": wl.d, "n_z": wl.n_z, "gen": f"{wl.L}x{wl.W} tanh",
+                   "disc": f"{wl.L_D}x{wl.W_D} tanh on {wl.n_in}", "S": wl.S, "P": wl.P,
+                   "sensors": [wl.n_sY, wl.n_sU], "B_r": wl.B_r, "chunk_S": a.chunk_S,
+                   "collocation_points_per_step": pts, "alg_flops_per_step": F},
+        "collocation_points_per_s": pts / (ms * 1e-3),
+        "mfma_frac_step": tflops / PEAK_TFLOPS[wl.dtype],
+        "nonfinite": nf,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -34,12 +34,77 @@ Parameter packing (float32 master copy in, float64 internally):
 
 Pins: see tests/test_oracle_*.py (closed forms, finite differences of the jets
 and of every weight gradient, torch.autograd in float64, invariants).
+
+Precision models (optional, off by default).  They do not change what is
+computed; their distance from the exact result measures how strongly each
+output amplifies rounding (its conditioning):
+* prec="bf16" / "fp16": the storage points of a mixed-precision evaluation are
+  rounded to that format -- hidden-layer and discriminator weights, every
+  stored pre-activation, activation and pre-activation cotangent, the
+  discriminator input -- and matrix products accumulate in fp32 (the paper
+  keeps half-precision activations and gradients with single-precision
+  accumulation, Sec. III.C);
+* prec="fp32": every array operation of the oracle runs in fp32.
 """
 from __future__ import annotations
 
 import numpy as np
 
-F64 = np.float64
+F64 = np.float64      # working type of every array; fp32 only inside _working_type
+
+
+def _round_bf16(x):
+    """Round to bfloat16 (round to nearest, ties to even), returned as float64."""
+    f = np.asarray(x, np.float64).astype(np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+class _Num:
+    """Storage rounding q() and matrix product mm() of one precision model."""
+
+    def __init__(self, prec=None):
+        self.prec = prec
+        if prec is None:
+            self.q = lambda x: x
+        elif prec == "fp32":
+            self.q = lambda x: np.asarray(x, np.float64).astype(np.float32).astype(np.float64)
+        elif prec == "bf16":
+            self.q = _round_bf16
+        elif prec == "fp16":
+            self.q = lambda x: np.asarray(x, np.float64).astype(np.float16).astype(np.float64)
+        else:
+            raise ValueError(f"unknown precision model {prec!r}")
+
+    def mm(self, a, b):
+        if self.prec is None:
+            return a @ b
+        return (np.asarray(a, np.float32) @ np.asarray(b, np.float32)).astype(np.float64)
+
+    def colsum(self, a):
+        if self.prec is None:
+            return a.sum(axis=0)
+        return np.asarray(a, np.float32).sum(axis=0).astype(np.float64)
+
+
+EXACT = _Num(None)
+
+
+class _working_type:
+    """Run the oracle's array arithmetic in another floating type."""
+
+    def __init__(self, dt):
+        self.dt = dt
+
+    def __enter__(self):
+        global F64
+        self.saved, F64 = F64, self.dt
+
+    def __exit__(self, *exc):
+        global F64
+        F64 = self.saved
+        return False
 
 
 # ----------------------------------------------------------------------------
@@ -94,7 +159,7 @@ def _tanh_derivs(a):
 # generator: forward jets and reverse pass
 # ----------------------------------------------------------------------------
 
-def gen_forward(params, shape, d: int, X, Z, order: int, keep: bool = False):
+def gen_forward(params, shape, d: int, X, Z, order: int, keep: bool = False, prec=None):
     """Evaluate a generator and its spatial jets at rows (X[n], Z[n]).
 
     X: [N, d] locations, Z: [N, n_z] noise (one row per evaluation point).
@@ -103,6 +168,8 @@ def gen_forward(params, shape, d: int, X, Z, order: int, keep: bool = False):
     Returns dict(y=[N], dy=[d, N] or None, ddy=[d, N] or None, cache).
     """
     in_dim, L, W = shape
+    num = prec if isinstance(prec, _Num) else _Num(prec)
+    q = num.q
     layers, w_out, b_out = unpack(params, in_dim, L, W)
     X = np.asarray(X, F64)
     Z = np.asarray(Z, F64)
@@ -112,21 +179,22 @@ def gen_forward(params, shape, d: int, X, Z, order: int, keep: bool = False):
     a = X @ W1[:, :d].T + Z @ W1[:, d:].T + b1
     # d a / d x_i is column i of W1; the second derivative of a is zero
     da = [np.broadcast_to(W1[:, i], (N, W)).copy() for i in range(d)] if order >= 1 else []
-    dda = [np.zeros((N, W)) for _ in range(d)] if order >= 2 else []
+    dda = [np.zeros((N, W), F64) for _ in range(d)] if order >= 2 else []
     cache = []
     h = dh = ddh = None
     for l in range(L):
         if l > 0:
             Wl, bl = layers[l]
-            a = h @ Wl.T + bl                      # bias enters the value only
-            da = [g @ Wl.T for g in dh]
-            dda = [g @ Wl.T for g in ddh]
+            Wq = q(Wl).T
+            a = num.mm(h, Wq) + bl                  # bias enters the value only
+            da = [num.mm(g, Wq) for g in dh]
+            dda = [num.mm(g, Wq) for g in ddh]
         t, s, sp, _ = _tanh_derivs(a)
         if keep:
-            cache.append((a, da, dda, (h, dh, ddh)))
-        h = t
-        dh = [s * g for g in da]
-        ddh = [s * g2 + sp * g1 * g1 for g1, g2 in zip(da, dda)]
+            cache.append((q(a), [q(g) for g in da], [q(g) for g in dda], (h, dh, ddh)))
+        h = q(t)
+        dh = [q(s * g) for g in da]
+        ddh = [q(s * g2 + sp * g1 * g1) for g1, g2 in zip(da, dda)]
     y = h @ w_out + b_out
     out = dict(y=y,
                dy=np.stack([g @ w_out for g in dh]) if order >= 1 else None,
@@ -137,12 +205,14 @@ def gen_forward(params, shape, d: int, X, Z, order: int, keep: bool = False):
     return out
 
 
-def gen_backward(params, shape, d: int, X, Z, fwd, g_y, g_dy=None, g_ddy=None) -> np.ndarray:
+def gen_backward(params, shape, d: int, X, Z, fwd, g_y, g_dy=None, g_ddy=None, prec=None) -> np.ndarray:
     """Reverse pass of gen_forward (keep=True) for output cotangents.
 
     g_y: [N]; g_dy, g_ddy: [d, N] or None.  Returns the packed gradient (fp64).
     """
     in_dim, L, W = shape
+    num = prec if isinstance(prec, _Num) else _Num(prec)
+    q = num.q
     layers, w_out, b_out = unpack(params, in_dim, L, W)
     X = np.asarray(X, F64)
     Z = np.asarray(Z, F64)
@@ -177,27 +247,29 @@ def gen_backward(params, shape, d: int, X, Z, fwd, g_y, g_dy=None, g_ddy=None) -
             g = s * gdh[i]
             if gddh:
                 g = g + 2.0 * sp * da[i] * gddh[i]
-            gda.append(g)
-        gdda = [s * g for g in gddh]
+            gda.append(q(g))
+        gdda = [q(s * g) for g in gddh]
+        ga = q(ga)
         if l > 0:
             Wl, _ = layers[l]
             h, dh, ddh = prev
-            gW = ga.T @ h
+            gW = num.mm(ga.T, h)
             for i in range(len(gda)):
-                gW = gW + gda[i].T @ dh[i]
+                gW = gW + num.mm(gda[i].T, dh[i])
             for i in range(len(gdda)):
-                gW = gW + gdda[i].T @ ddh[i]
-            grads[l] = (gW, ga.sum(axis=0))
-            gh = ga @ Wl
-            gdh = [g @ Wl for g in gda]
-            gddh = [g @ Wl for g in gdda]
+                gW = gW + num.mm(gdda[i].T, ddh[i])
+            grads[l] = (gW, num.colsum(ga))
+            Wq = q(Wl)
+            gh = num.mm(ga, Wq)
+            gdh = [num.mm(g, Wq) for g in gda]
+            gddh = [num.mm(g, Wq) for g in gdda]
         else:
-            gW1 = np.zeros((W, in_dim))
+            gW1 = np.zeros((W, in_dim), F64)
             gW1[:, :d] = ga.T @ X
             gW1[:, d:] = ga.T @ Z
             for i in range(len(gda)):
-                gW1[:, i] += gda[i].sum(axis=0)   # a'_i = W1[:, i] for every row
-            grads[0] = (gW1, ga.sum(axis=0))
+                gW1[:, i] += num.colsum(gda[i])   # a'_i = W1[:, i] for every row
+            grads[0] = (gW1, num.colsum(ga))
     return pack(grads, gw_out, gb_out)
 
 
@@ -205,32 +277,45 @@ def gen_backward(params, shape, d: int, X, Z, fwd, g_y, g_dy=None, g_ddy=None) -
 # plain tanh MLP (discriminator)
 # ----------------------------------------------------------------------------
 
-def mlp_forward(params, shape, V, keep: bool = False):
-    """D(v) = w_out . h_L + b_out with h_l = tanh(W_l h_{l-1} + b_l), h_0 = v."""
+def mlp_forward(params, shape, V, keep: bool = False, prec=None):
+    """D(v) = w_out . h_L + b_out with h_l = tanh(W_l h_{l-1} + b_l), h_0 = v.
+
+    keep=True also returns the cache (activations h_0..h_L, pre-activations)."""
     in_dim, L, W = shape
+    num = prec if isinstance(prec, _Num) else _Num(prec)
+    q = num.q
     layers, w_out, b_out = unpack(params, in_dim, L, W)
-    h = np.asarray(V, F64)
+    h = q(np.asarray(V, F64))
     hs = [h]
+    pre = []
     for Wl, bl in layers:
-        h = np.tanh(h @ Wl.T + bl)
+        a = num.mm(h, q(Wl).T) + bl
+        pre.append(q(a))
+        h = q(np.tanh(a))
         hs.append(h)
     y = h @ w_out + b_out
-    return (y, hs) if keep else y
+    return (y, dict(h=hs, a=pre)) if keep else y
 
 
-def mlp_backward(params, shape, hs, g_y, want_input_grad: bool = False):
+def mlp_backward(params, shape, cache, g_y, want_input_grad: bool = False, prec=None):
     in_dim, L, W = shape
+    num = prec if isinstance(prec, _Num) else _Num(prec)
+    q = num.q
     layers, w_out, b_out = unpack(params, in_dim, L, W)
+    hs = cache["h"]
     g_y = np.asarray(g_y, F64)
-    gw_out = hs[-1].T @ g_y
+    # in the precision model the activations are re-formed from the stored
+    # (rounded) pre-activations, as a mixed-precision reverse pass does
+    tops = [np.tanh(a) for a in cache["a"]] if num.prec is not None else hs[1:]
+    gw_out = tops[-1].T @ g_y
     gb_out = g_y.sum()
     gh = np.outer(g_y, w_out)
     grads = [None] * L
     for l in reversed(range(L)):
-        t = hs[l + 1]
-        ga = (1.0 - t * t) * gh
-        grads[l] = (ga.T @ hs[l], ga.sum(axis=0))
-        gh = ga @ layers[l][0]
+        t = tops[l]
+        ga = q((1.0 - t * t) * gh)
+        grads[l] = (num.mm(ga.T, hs[l]), num.colsum(ga))
+        gh = num.mm(ga, q(layers[l][0]))
     g = pack(grads, gw_out, gb_out)
     return (g, gh) if want_input_grad else g
 
@@ -299,7 +384,7 @@ def snapshots(pY, pU, shape, d, xsY, xsU, z):
 # ----------------------------------------------------------------------------
 
 def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
-                     w=1.0, lambda_pde=1.0, chunk_S=None):
+                     w=1.0, lambda_pde=1.0, chunk_S=None, prec=None):
     """One subdomain group's losses and gradients.
 
     Returns dict(L_D, L_adv, L_pde, gY, gU, gD) with gradients of
@@ -315,16 +400,21 @@ def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
     B = real.shape[0]
     nY = np.asarray(xsY).shape[0]
     chunk_S = S if not chunk_S else chunk_S
+    if prec == "fp32":
+        with _working_type(np.float32):
+            return train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real, w=w,
+                                    lambda_pde=lambda_pde, chunk_S=chunk_S, prec=None)
+    num = _Num(prec)
 
-    gY = np.zeros(np.asarray(pY).size)
-    gU = np.zeros(np.asarray(pU).size)
-    gD = np.zeros(np.asarray(pD).size)
+    gY = np.zeros(np.asarray(pY).size, F64)
+    gU = np.zeros(np.asarray(pU).size, F64)
+    gD = np.zeros(np.asarray(pD).size, F64)
     sum_DF = 0.0
     sum_r2 = 0.0
 
     # real snapshots: dL_D/dD(real_b) = -w/B
-    DR, hsR = mlp_forward(pD, dshape, real, keep=True)
-    gD += mlp_backward(pD, dshape, hsR, np.full(B, -w / B))
+    DR, hsR = mlp_forward(pD, dshape, real, keep=True, prec=num)
+    gD += mlp_backward(pD, dshape, hsR, np.full(B, -w / B, F64), prec=num)
     sum_DR = DR.sum()
 
     for s0 in range(0, S, chunk_S):
@@ -334,20 +424,20 @@ def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
         # --- generators at the sensors (value only) -> fake snapshots
         XY, ZY = sensor_rows(xsY, zc)
         XU, ZU = sensor_rows(xsU, zc)
-        fY_s = gen_forward(pY, gshape, d, XY, ZY, 0, keep=True)
-        fU_s = gen_forward(pU, gshape, d, XU, ZU, 0, keep=True)
+        fY_s = gen_forward(pY, gshape, d, XY, ZY, 0, keep=True, prec=num)
+        fU_s = gen_forward(pU, gshape, d, XU, ZU, 0, keep=True, prec=num)
         F = np.concatenate([fY_s["y"].reshape(Sc, -1), fU_s["y"].reshape(Sc, -1)], axis=1)
         # --- generators at the collocation points with jets
         XC, ZC = colloc_rows(xc[sl], zc)
-        jY = gen_forward(pY, gshape, d, XC, ZC, 1, keep=True)
-        jU = gen_forward(pU, gshape, d, XC, ZC, 2, keep=True)
+        jY = gen_forward(pY, gshape, d, XC, ZC, 1, keep=True, prec=num)
+        jU = gen_forward(pU, gshape, d, XC, ZC, 2, keep=True, prec=num)
         fc = f[sl].reshape(-1)
         r = darcy_residual(jY["y"], jY["dy"], jU["dy"], jU["ddy"], fc)
         sum_r2 += float((r * r).sum())
         # --- discriminator on the fake snapshots: dL_D/dD(F_s) = w/S
-        DF, hsF = mlp_forward(pD, dshape, F, keep=True)
+        DF, hsF = mlp_forward(pD, dshape, F, keep=True, prec=num)
         sum_DF += float(DF.sum())
-        gDc, gF = mlp_backward(pD, dshape, hsF, np.full(Sc, w / S), want_input_grad=True)
+        gDc, gF = mlp_backward(pD, dshape, hsF, np.full(Sc, w / S, F64), want_input_grad=True, prec=num)
         gD += gDc
         # L_adv = -w mean D(F): its snapshot cotangent is the negated L_D one
         gF = -gF
@@ -360,10 +450,10 @@ def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
         g_Uddy = np.stack([-q * eY for _ in range(d)])
         g_Uval = np.zeros_like(r)                   # u itself does not enter r
         # --- reverse passes through both generators
-        gY += gen_backward(pY, gshape, d, XY, ZY, fY_s, gF[:, :nY].reshape(-1))
-        gU += gen_backward(pU, gshape, d, XU, ZU, fU_s, gF[:, nY:].reshape(-1))
-        gY += gen_backward(pY, gshape, d, XC, ZC, jY, g_Yval, g_Ydy)
-        gU += gen_backward(pU, gshape, d, XC, ZC, jU, g_Uval, g_Udy, g_Uddy)
+        gY += gen_backward(pY, gshape, d, XY, ZY, fY_s, gF[:, :nY].reshape(-1), prec=num)
+        gU += gen_backward(pU, gshape, d, XU, ZU, fU_s, gF[:, nY:].reshape(-1), prec=num)
+        gY += gen_backward(pY, gshape, d, XC, ZC, jY, g_Yval, g_Ydy, prec=num)
+        gU += gen_backward(pU, gshape, d, XC, ZC, jU, g_Uval, g_Udy, g_Uddy, prec=num)
 
     L_D = w * (sum_DF / S - sum_DR / B)
     L_adv = -w * sum_DF / S
@@ -371,7 +461,7 @@ def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
     return dict(L_D=L_D, L_adv=L_adv, L_pde=L_pde, gY=gY, gU=gU, gD=gD)
 
 
-def train_step(wl, inp, real, lambda_pde=None, chunk_S=None):
+def train_step(wl, inp, real, lambda_pde=None, chunk_S=None, prec=None):
     """All groups of a workload.  ``inp`` is an inputs.StepInputs-like object,
     ``real`` the real snapshots [G, B_r, n_in].  Returns dict of stacked arrays:
     loss [G, 3] (L_D, L_adv, L_pde), gY [G, nY], gU [G, nU], gD [G, nD]."""
@@ -385,7 +475,8 @@ def train_step(wl, inp, real, lambda_pde=None, chunk_S=None):
         f = inp.f[g] if inp.f is not None else np.full((S, P), inp.f_const)
         outs.append(train_step_group(gshape, dshape, wl.d, inp.pY[g], inp.pU[g], inp.pD[g],
                                      inp.z[g], inp.xc[g], inp.xsY[g], inp.xsU[g], f, real[g],
-                                     w=float(inp.w_group[g]), lambda_pde=lam, chunk_S=chunk_S))
+                                     w=float(inp.w_group[g]), lambda_pde=lam, chunk_S=chunk_S,
+                                     prec=prec))
     return dict(loss=np.array([[o["L_D"], o["L_adv"], o["L_pde"]] for o in outs]),
                 gY=np.stack([o["gY"] for o in outs]),
                 gU=np.stack([o["gU"] for o in outs]),

@@ -123,12 +123,8 @@ hipError_t launch_gemm_nt(int epi, int nd1, int nd2, const NtArgs<T>& a, int G, 
 
 template <class T>
 hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int64_t h_g, int64_t ldh,
-                          int64_t R, int64_t n_value, int N, int J, float* partial, float* pdb,
+                          int64_t R, int64_t n_value, int N, int J, float* partial, double* pdb,
                           int n_split, int64_t rows_per_split, int G, hipStream_t st);
-
-hipError_t launch_reduce_dw(const float* partial, const float* pdb, int n_split, int N, int Jpad,
-                            int J, float* gW, float* gb, int64_t g_g, int accumulate, float scale,
-                            int32_t* nonfinite, int G, hipStream_t st);
 
 void dw_split_plan(int64_t R, int N, int J, int elem_bytes, int G, int* n_split, int64_t* rows_per_split);
 

@@ -18,7 +18,7 @@
 //            critic term).
 // k_gemm_dw  : dW = sum_rows dA^T H (split over rows, fp32 partials), plus
 //              the bias cotangent sum over the value rows.
-// k_reduce_dw: fixed-order sum of the split partials into the fp32 gradient.
+// The split partials are summed in fp64, in split order, by k_colsum.
 //
 // Tiles: a 64-lane wave owns 32 points x 32*NT columns for every stream; the
 // block is WM x WN waves.  Operands are staged through LDS in 64-byte k-slices
@@ -205,7 +205,7 @@ template <class T, int WM, int WN, int NT>
 __global__ void __launch_bounds__(64 * WM * WN)
 k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restrict__ H, int64_t h_g,
           int64_t ldh, int64_t R, int64_t n_value, int N, int J, float* __restrict__ partial,
-          float* __restrict__ pdb, int n_split, int64_t rows_per_split) {
+          double* __restrict__ pdb, int n_split, int64_t rows_per_split) {
   constexpr int BNn = 32 * NT * WM;
   constexpr int BJ = 32 * NT * WN;
   constexpr int NTH = 64 * WM * WN;
@@ -247,7 +247,7 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
     for (int b = 0; b < NT; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
-  float dbacc = 0.0f;
+  double dbacc = 0.0;
 
   uint4 buf[PPT][RPP];
   auto gload = [&](int64_t k0) {
@@ -318,7 +318,9 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
     if (pdb && tj == 0 && tid < BNn && k0 < rv) {
       const int nr = (int)((rv - k0) < SR ? (rv - k0) : SR);
       const T* colp = (const T*)(lds + tid * LDS_PITCH);
-      for (int u = 0; u < nr; ++u) dbacc += Elem<T>::to_f(colp[u]);
+      float part_sum = 0.0f;
+      for (int u = 0; u < nr; ++u) part_sum += Elem<T>::to_f(colp[u]);
+      dbacc += (double)part_sum;
     }
   }
 
@@ -339,53 +341,6 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
   }
   if (pdb && tj == 0 && tid < BNn && n0 + tid < N)
     pdb[((int64_t)g * n_split + split) * N + n0 + tid] = dbacc;
-}
-
-// Sum the split partials in split order.  Four thread groups take every
-// fourth split for 64 consecutive outputs; the four sums are added in group
-// order.  Output j < Jreal goes to gW[n*Jreal + j]; the bias to gb[n].
-__global__ void __launch_bounds__(256)
-k_reduce_dw(const float* __restrict__ partial, const float* __restrict__ pdb, int n_split, int N, int Jp,
-            int J, float* gW, float* gb, int64_t g_g, int accumulate, float scale, int32_t* nonfinite) {
-  __shared__ float sm[4][64];
-  const int g = blockIdx.z;
-  const int64_t nw = (int64_t)N * Jp;
-  const int64_t base = (int64_t)blockIdx.x * 64;
-  const int lane = threadIdx.x & 63;
-  const int grp = threadIdx.x >> 6;
-  const int64_t idx = base + lane;
-  const bool isb = idx >= nw;
-  const int64_t tot = nw + N;
-  float s = 0.0f;
-  if (idx < tot) {
-    if (!isb) {
-      const float* src = partial + (int64_t)g * n_split * nw + idx;
-      for (int q = grp; q < n_split; q += 4) s += src[(int64_t)q * nw];
-    } else if (pdb) {
-      const float* src = pdb + (int64_t)g * n_split * N + (idx - nw);
-      for (int q = grp; q < n_split; q += 4) s += src[(int64_t)q * N];
-    }
-  }
-  sm[grp][lane] = s;
-  __syncthreads();
-  if (grp == 0 && idx < tot) {
-    float v = ((sm[0][lane] + sm[1][lane]) + sm[2][lane]) + sm[3][lane];
-    v *= scale;
-    if (!isb) {
-      const int n = (int)(idx / Jp), j = (int)(idx % Jp);
-      if (j < J) {
-        float* dst = gW + g * g_g + (int64_t)n * J + j;
-        if (accumulate) v += *dst;
-        *dst = v;
-        if (!__builtin_isfinite(v)) *nonfinite = 1;
-      }
-    } else if (gb && pdb) {
-      float* dst = gb + g * g_g + (idx - nw);
-      if (accumulate) v += *dst;
-      *dst = v;
-      if (!__builtin_isfinite(v)) *nonfinite = 1;
-    }
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -456,7 +411,7 @@ void dw_split_plan(int64_t R, int N, int J, int elem_bytes, int G, int* n_split,
 
 template <class T>
 hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int64_t h_g, int64_t ldh,
-                          int64_t R, int64_t n_value, int N, int J, float* partial, float* pdb,
+                          int64_t R, int64_t n_value, int N, int J, float* partial, double* pdb,
                           int n_split, int64_t rows_per_split, int G, hipStream_t st) {
   if (R <= 0) return hipSuccess;
   if (N >= 128 && J >= 128) {
@@ -475,20 +430,10 @@ hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_dw(const float* partial, const float* pdb, int n_split, int N, int Jp, int J,
-                            float* gW, float* gb, int64_t g_g, int accumulate, float scale,
-                            int32_t* nonfinite, int G, hipStream_t st) {
-  const int64_t tot = (int64_t)N * Jp + N;
-  dim3 grid((unsigned)((tot + 63) / 64), 1, G);
-  k_reduce_dw<<<grid, 256, 0, st>>>(partial, pdb, n_split, N, Jp, J, gW, gb, g_g, accumulate, scale,
-                                    nonfinite);
-  return hipGetLastError();
-}
-
 #define PIGAN_INST(T)                                                                                    \
   template hipError_t launch_gemm_nt<T>(int, int, int, const NtArgs<T>&, int, hipStream_t);              \
   template hipError_t launch_gemm_dw<T>(const T*, int64_t, int64_t, const T*, int64_t, int64_t, int64_t, \
-                                        int64_t, int, int, float*, float*, int, int64_t, int, hipStream_t);
+                                        int64_t, int, int, float*, double*, int, int64_t, int, hipStream_t);
 PIGAN_INST(float)
 PIGAN_INST(bf16)
 PIGAN_INST(f16)

@@ -146,6 +146,12 @@ static pigan_status check_dtype(pigan_dtype dt) {
   return PIGAN_OK;
 }
 
+// row chunks per sample of the first-layer reverse pass: about 1024 blocks
+static int first_bwd_chunks(int S) {
+  int c = (1024 + S - 1) / S;
+  return c < 1 ? 1 : (c > 64 ? 64 : c);
+}
+
 // points per block of the output-layer reverse pass
 static int64_t ob_ppb(int64_t n_points) {
   int64_t p = (n_points + 511) / 512;
@@ -166,6 +172,7 @@ struct NetBuf {
   size_t jet = 0, gbar = 0, zp = 0, wc = 0, wcT = 0, fb = 0, ob = 0;
   int64_t ob_slots = 0;
   int64_t ppb_sen = 8, ppb_col = 8;
+  int nrc = 1;       // row chunks per sample in the first-layer reverse pass
 };
 
 struct DiscBuf {
@@ -215,11 +222,12 @@ static void plan_net(Carver& cv, NetBuf& nb, const pigan_mlp& m, int d, int nd2,
   const size_t wsz = (size_t)std::max(L - 1, 1) * W * W * es * G;
   nb.wc = cv.take(wsz);
   nb.wcT = cv.take(wsz);
-  nb.fb = cv.take((size_t)Sc * 7 * W * 4 * G);
+  nb.nrc = first_bwd_chunks(Sc);
+  nb.fb = cv.take((size_t)Sc * nb.nrc * 7 * W * 4 * G);
   nb.ppb_sen = ob_ppb(nb.n_sen);
   nb.ppb_col = ob_ppb(nb.n_col);
   nb.ob_slots = out_bwd_blocks(nb.n_sen, (int)nb.ppb_sen) + out_bwd_blocks(nb.n_col, (int)nb.ppb_col);
-  nb.ob = cv.take((size_t)nb.ob_slots * (W + 1) * 4 * G);
+  nb.ob = cv.take((size_t)nb.ob_slots * (W + 1) * 8 * G);
 }
 
 static void plan_step(const pigan_step_desc* s, int Sc, StepPlan& pl) {
@@ -254,7 +262,7 @@ static void plan_step(const pigan_step_desc* s, int Sc, StepPlan& pl) {
   D.wcT = cv.take(wsz);
   D.ppb = ob_ppb(D.Bmax);
   D.ob_slots = out_bwd_blocks(D.Bmax, (int)D.ppb);
-  D.ob = cv.take((size_t)D.ob_slots * (WD + 1) * 4 * G);
+  D.ob = cv.take((size_t)D.ob_slots * (WD + 1) * 8 * G);
   // split-K partials: the largest of all weight-gradient launches
   int64_t mx = 0, mxb = 0;
   auto consider = [&](int64_t R, int N, int J) {
@@ -271,7 +279,7 @@ static void plan_step(const pigan_step_desc* s, int Sc, StepPlan& pl) {
   pl.dwp_floats = mx;
   pl.dwdb_floats = mxb;
   pl.dwp = cv.take((size_t)mx * 4 * G);
-  pl.dwdb = cv.take((size_t)mxb * 4 * G);
+  pl.dwdb = cv.take((size_t)mxb * 8 * G);
   pl.rblocks = residual_blocks((int64_t)Sc * s->P);
   pl.rpart = cv.take((size_t)pl.rblocks * 8 * G);
   pl.acc = cv.take((size_t)4 * 8 * G);
@@ -341,7 +349,7 @@ static pigan_status gemm_nt(int epi, int nd1, int nd2, const NtArgs<T>& a, int G
 template <class T>
 static pigan_status weight_grad(const T* dA, int64_t a_g, int64_t lda, const T* H, int64_t h_g, int64_t ldh,
                                 int64_t R, int64_t n_value, int N, int Jp, int J, float* gW, float* gb, int64_t g_g,
-                                int accumulate, float scale, int32_t* nonfinite, float* part, float* pdb, int G,
+                                int accumulate, float scale, int32_t* nonfinite, float* part, double* pdb, int G,
                                 hipStream_t st) {
   int ns;
   int64_t rps;
@@ -352,7 +360,11 @@ static pigan_status weight_grad(const T* dA, int64_t a_g, int64_t lda, const T* 
   }
   {
     ProfScope ps(st, "reduce_dw", 0.0, 4.0 * ((double)ns + 1.0) * N * Jp * G);
-    HIP_TRY(launch_reduce_dw(part, pdb, ns, N, Jp, J, gW, gb, g_g, accumulate, scale, nonfinite, G, st));
+    const int64_t nw = (int64_t)N * Jp;
+    HIP_TRY(launch_colsum<float>(part, (int64_t)ns * nw, ns, nw, nw, Jp, J, gW, g_g, accumulate, scale, nonfinite, G,
+                                 st));
+    HIP_TRY(launch_colsum<double>(pdb, (int64_t)ns * N, ns, N, N, 1, 1, gb, g_g, accumulate, scale, nonfinite, G,
+                                  st));
   }
   return PIGAN_OK;
 }
@@ -426,21 +438,21 @@ static pigan_status gen_chunk_bwd(void* ws, const StepPlan& pl, const NetBuf& nb
   ob.wout = params + nb.off.wout; ob.w_g = pg;
   const int blk_sen = out_bwd_blocks(nb.n_sen, (int)nb.ppb_sen);
   const int n_slots = blk_sen + out_bwd_blocks(nb.n_col, (int)nb.ppb_col);
-  ob.W = W; ob.part = tp<float>(ws, nb.ob); ob.n_slots = n_slots;
+  ob.W = W; ob.part = tp<double>(ws, nb.ob); ob.n_slots = n_slots;
   ob.ppb = nb.ppb_sen; ob.slot0 = 0; ob.seg = Seg{nb.n_sen, 0, 0};
   {
     ProfScope ps(st, "out_bwd", 0.0, (double)nb.rows * W * 2 * sizeof(T) * G);
     HIP_TRY(launch_out_bwd<T>(0, 0, ob, G, st));
     ob.ppb = nb.ppb_col; ob.slot0 = blk_sen; ob.seg = Seg{nb.n_col, nb.n_sen, nb.n_col};
     HIP_TRY(launch_out_bwd<T>(nb.nd1, nb.nd2, ob, G, st));
-    HIP_TRY(launch_reduce_slots(tp<float>(ws, nb.ob), n_slots, W, grad + nb.off.wout, pg, accumulate, scale,
-                                nonfinite, G, st));
+    HIP_TRY(launch_colsum<double>(tp<double>(ws, nb.ob), (int64_t)n_slots * (W + 1), n_slots, W + 1, W + 1, 1, 1,
+                                  grad + nb.off.wout, pg, accumulate, scale, nonfinite, G, st));
   }
   int cur = 0;
   for (int l = L; l >= 2; --l) {
     pigan_status s1 = weight_grad<T>(tp<T>(ws, nb.dA[cur]), actg, W, tp<T>(ws, nb.H[l - 1]), actg, W, nb.rows,
                                      nb.n_sen + nb.n_col, W, W, W, grad + nb.off.w[l], grad + nb.off.b[l], pg,
-                                     accumulate, scale, nonfinite, tp<float>(ws, pl.dwp), tp<float>(ws, pl.dwdb), G, st);
+                                     accumulate, scale, nonfinite, tp<float>(ws, pl.dwp), tp<double>(ws, pl.dwdb), G, st);
     if (s1 != PIGAN_OK) return s1;
     NtArgs<T> a{};
     a.X = tp<T>(ws, nb.dA[cur]); a.x_g = actg; a.ldx = W;
@@ -459,10 +471,11 @@ static pigan_status gen_chunk_bwd(void* ws, const StepPlan& pl, const NetBuf& nb
   fb.dA = tp<T>(ws, nb.dA[cur]); fb.a_g = actg; fb.lda = W;
   fb.n_sen = nb.n_sen; fb.n_col = nb.n_col; fb.n_s = nb.n_s; fb.P = P; fb.S = Sc; fb.W = W; fb.d = d; fb.nd1 = nb.nd1;
   fb.xs = xs; fb.xs_g = xs_g; fb.xc = xc; fb.xc_g = xc_g; fb.part = tp<float>(ws, nb.fb);
+  fb.nrc = nb.nrc;   // planned for the largest chunk: Sc * nrc never exceeds the partial buffer
   {
     ProfScope ps(st, "first_bwd", 0.0, (double)(nb.n_sen + (1 + nb.nd1) * nb.n_col) * W * sizeof(T) * G);
     HIP_TRY(launch_first_bwd<T>(fb, G, st));
-    HIP_TRY(launch_first_wgrad(tp<float>(ws, nb.fb), Sc, W, d, nb.nd1, nb.off.in_dim, z, z_g, n_z, grad, pg,
+    HIP_TRY(launch_first_wgrad(tp<float>(ws, nb.fb), Sc, fb.nrc, W, d, nb.nd1, nb.off.in_dim, z, z_g, n_z, grad, pg,
                                accumulate, scale, nonfinite, G, st));
   }
   return PIGAN_OK;
@@ -574,18 +587,18 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
       ob.A = tp<T>(ws, D.A[LD]); ob.dA = tp<T>(ws, D.dA[0]); ob.o_g = dact; ob.ldo = WD;
       ob.gbar = tp<float>(ws, D.seed); ob.gb_g = D.Bmax;
       ob.wout = pD + D.off.wout; ob.w_g = D.off.n;
-      ob.W = WD; ob.ppb = D.ppb; ob.part = tp<float>(ws, D.ob); ob.n_slots = out_bwd_blocks(B, (int)D.ppb);
+      ob.W = WD; ob.ppb = D.ppb; ob.part = tp<double>(ws, D.ob); ob.n_slots = out_bwd_blocks(B, (int)D.ppb);
       ob.slot0 = 0; ob.seg = Seg{B, 0, 0};
       ProfScope ps(st, "out_bwd", 0.0, (double)B * WD * 2 * sizeof(T) * G);
       HIP_TRY(launch_out_bwd<T>(0, 0, ob, G, st));
-      HIP_TRY(launch_reduce_slots(tp<float>(ws, D.ob), ob.n_slots, WD, gD + D.off.wout, D.off.n, accum, inv,
-                                  nonfinite, G, st));
+      HIP_TRY(launch_colsum<double>(tp<double>(ws, D.ob), (int64_t)ob.n_slots * (WD + 1), ob.n_slots, WD + 1, WD + 1,
+                                    1, 1, gD + D.off.wout, D.off.n, accum, inv, nonfinite, G, st));
     }
     int cur = 0;
     for (int l = LD; l >= 2; --l) {
       if ((r = weight_grad<T>(tp<T>(ws, D.dA[cur]), dact, WD, tp<T>(ws, D.H[l - 1]), dact, WD, B, B, WD, WD, WD,
                               gD + D.off.w[l], gD + D.off.b[l], D.off.n, accum, inv, nonfinite, tp<float>(ws, pl.dwp),
-                              tp<float>(ws, pl.dwdb), G, st)) != PIGAN_OK)
+                              tp<double>(ws, pl.dwdb), G, st)) != PIGAN_OK)
         return r;
       NtArgs<T> a{};
       a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
@@ -597,7 +610,7 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
     }
     if ((r = weight_grad<T>(tp<T>(ws, D.dA[cur]), dact, WD, tp<T>(ws, D.X0), D.Bmax * D.Kp, D.Kp, B, B, WD, D.Kp, n_in,
                             gD + D.off.w[1], gD + D.off.b[1], D.off.n, accum, inv, nonfinite, tp<float>(ws, pl.dwp),
-                            tp<float>(ws, pl.dwdb), G, st)) != PIGAN_OK)
+                            tp<double>(ws, pl.dwdb), G, st)) != PIGAN_OK)
       return r;
     {
       // d(L_adv)/dF = -dL_D/dF for the fake rows -> generator sensor cotangents

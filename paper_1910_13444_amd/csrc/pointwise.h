@@ -28,7 +28,7 @@ template <class T> struct OutBwdArgs {
   const float* gbar; int64_t gb_g;               // output cotangents (jet layout)
   const float* wout; int64_t w_g;                // w_out (W) followed by b_out
   int W; int64_t ppb;                            // points per block
-  float* part; int n_slots; int slot0;           // [G][n_slots][W+1]
+  double* part; int n_slots; int slot0;          // [G][n_slots][W+1] fp64 partials
   Seg seg;
 };
 
@@ -38,7 +38,8 @@ template <class T> struct FirstBwdArgs {
   int n_s; int P; int S; int W; int d; int nd1;
   const float* xs; int64_t xs_g;                 // sensor locations [n_s][d]
   const float* xc; int64_t xc_g;                 // collocation points of the chunk [S][P][d]
-  float* part;                                   // [G][S][7][W]
+  int nrc;                                       // row chunks per sample (blocks per sample)
+  float* part;                                   // [G][S][nrc][7][W]
 };
 
 hipError_t launch_zproj(const float* p1, int64_t p_g, int in_dim, int d, int W, const float* z, int64_t z_g,
@@ -60,10 +61,13 @@ hipError_t launch_disc_seed(const float* score, int64_t sc_g, int n_fake, int n_
                             int G, hipStream_t st);
 int out_bwd_blocks(int64_t n_points, int ppb);
 template <class T> hipError_t launch_out_bwd(int nd1, int nd2, const OutBwdArgs<T>& a, int G, hipStream_t st);
-hipError_t launch_reduce_slots(const float* part, int n_slots, int W, float* dst, int64_t d_g, int accumulate,
-                               float scale, int32_t* nonfinite, int G, hipStream_t st);
+// dst[(col/Jp)*J + col%Jp] (+)= scale * sum_slots part[g][slot][col]  (fp64, fixed order)
+template <class Tin>
+hipError_t launch_colsum(const Tin* part, int64_t p_g, int n_slots, int64_t slot_stride, int64_t ncols, int Jp, int J,
+                         float* dst, int64_t d_g, int accumulate, float scale, int32_t* nonfinite, int G,
+                         hipStream_t st);
 template <class T> hipError_t launch_first_bwd(const FirstBwdArgs<T>& a, int G, hipStream_t st);
-hipError_t launch_first_wgrad(const float* part, int S, int W, int d, int nd1, int in_dim, const float* z,
+hipError_t launch_first_wgrad(const float* part, int S, int nrc, int W, int d, int nd1, int in_dim, const float* z,
                               int64_t z_g, int n_z, float* grad, int64_t g_g, int accumulate, float scale,
                               int32_t* nonfinite, int G, hipStream_t st);
 hipError_t launch_losses(const double* acc, int acc_stride, const float* w_group, int S, int B, int64_t SP,

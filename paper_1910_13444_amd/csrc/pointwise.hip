@@ -26,41 +26,97 @@ __global__ void k_zproj(const float* __restrict__ p1, int64_t p_g, int in_dim, i
 }
 
 // ---------------------------------------------------------------------------
+// 8-wide vector access in the storage type (16 bytes in bf16/fp16, 32 in fp32)
+// ---------------------------------------------------------------------------
+template <class T>
+__device__ __forceinline__ void load8(const T* p, float* v) {
+  if (sizeof(T) == 2) {
+    const uint4 raw = *(const uint4*)p;
+    const T* e = (const T*)&raw;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = Elem<T>::to_f(e[i]);
+  } else {
+    const float4 a = *(const float4*)p, b = *((const float4*)p + 1);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+}
+
+template <class T>
+__device__ __forceinline__ void store8(T* p, const float* v) {
+  if (sizeof(T) == 2) {
+    uint4 raw;
+    T* e = (T*)&raw;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) e[i] = Elem<T>::from_f(v[i]);
+    *(uint4*)p = raw;
+  } else {
+    *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
+    *((float4*)p + 1) = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // first layer: a = zp[s] + W1[:, :d] x ; a'_i = W1[:, i] ; a''_i = 0
+// one thread per (point, 8 columns)
 // ---------------------------------------------------------------------------
 template <class T, int ND1, int ND2>
-__global__ void k_first_fwd(FirstArgs<T> p) {
+__global__ void __launch_bounds__(256)
+k_first_fwd(FirstArgs<T> p) {
   constexpr int C = 1 + ND1 + ND2;
   const int g = blockIdx.z;
+  const int G8 = p.W / 8;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int W = p.W;
-  if (idx >= p.seg.n_points * W) return;
-  const int64_t pt = idx / W;
-  const int n = (int)(idx % W);
+  if (idx >= p.seg.n_points * G8) return;
+  const int64_t pt = idx / G8;
+  const int n0 = (int)(idx % G8) * 8;
   const int64_t s = pt / p.Pn;
   const int64_t xr = p.x_shared ? pt % p.Pn : pt;
   const float* xv = p.x + g * p.x_g + xr * p.d;
-  const float* Wn = p.p1 + g * p.p_g + (int64_t)n * p.in_dim;
-  float a = p.zp[g * p.zp_g + s * W + n];
-  for (int i = 0; i < p.d; ++i) a += Wn[i] * xv[i];
-  float t, sd;
-  tanh_ts(a, t, sd);
-  const float sp = -2.0f * t * sd;
-  int64_t o[C];
+  float x[3] = {0.0f, 0.0f, 0.0f};
 #pragma unroll
-  for (int k = 0; k < C; ++k) o[k] = g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + n;
-  if (p.out_a) {
-    p.out_a[o[0]] = Elem<T>::from_f(a);
+  for (int i = 0; i < 3; ++i)
+    if (i < p.d) x[i] = xv[i];
+  const float* W1 = p.p1 + g * p.p_g + (int64_t)n0 * p.in_dim;
+  float a[8], wc[3][8];
+  load8<float>(p.zp + g * p.zp_g + s * p.W + n0, a);
 #pragma unroll
-    for (int i = 0; i < ND1; ++i) p.out_a[o[1 + i]] = Elem<T>::from_f(Wn[i]);
+  for (int e = 0; e < 8; ++e) {
 #pragma unroll
-    for (int i = 0; i < ND2; ++i) p.out_a[o[1 + ND1 + i]] = Elem<T>::from_f(0.0f);
+    for (int i = 0; i < 3; ++i) {
+      wc[i][e] = i < p.d ? W1[(int64_t)e * p.in_dim + i] : 0.0f;
+      a[e] += wc[i][e] * x[i];
+    }
   }
-  p.out_h[o[0]] = Elem<T>::from_f(t);
+  float h[C][8];
+  float s8[8], sp8[8];
 #pragma unroll
-  for (int i = 0; i < ND1; ++i) p.out_h[o[1 + i]] = Elem<T>::from_f(sd * Wn[i]);
+  for (int e = 0; e < 8; ++e) {
+    float t, sd;
+    tanh_ts(a[e], t, sd);
+    h[0][e] = t;
+    s8[e] = sd;
+    sp8[e] = -2.0f * t * sd;
+  }
 #pragma unroll
-  for (int i = 0; i < ND2; ++i) p.out_h[o[1 + ND1 + i]] = Elem<T>::from_f(sp * Wn[i] * Wn[i]);
+  for (int i = 0; i < ND1; ++i)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h[1 + i][e] = s8[e] * wc[i][e];
+#pragma unroll
+  for (int i = 0; i < ND2; ++i)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h[1 + ND1 + i][e] = sp8[e] * wc[i][e] * wc[i][e];
+  const int64_t base = g * p.o_g + (p.seg.row0 + pt) * p.ldo + n0;
+  const int64_t pl = p.seg.plane * p.ldo;
+  if (p.out_a) {
+    store8<T>(p.out_a + base, a);
+#pragma unroll
+    for (int i = 0; i < ND1; ++i) store8<T>(p.out_a + base + (1 + i) * pl, wc[i]);
+    float z8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < ND2; ++i) store8<T>(p.out_a + base + (1 + ND1 + i) * pl, z8);
+  }
+#pragma unroll
+  for (int k = 0; k < C; ++k) store8<T>(p.out_h + base + k * pl, h[k]);
 }
 
 // ---------------------------------------------------------------------------
@@ -224,22 +280,22 @@ k_disc_seed(const float* __restrict__ score, int64_t sc_g, int n_fake, int n_rea
 // ---------------------------------------------------------------------------
 // output layer reverse pass for one segment of points:
 //   dH_k[pt][n] = gbar_k[pt] w_out[n]  -> carry reverse with the saved A_L
-//   partial dw_out[n] = sum gbar_k h_k (h recomputed from A_L),
+//   partial dw_out[n] = sum gbar_k h_k (h re-formed from A_L),
 //   partial db_out   = sum over value rows of gbar_0.
-// Threads: TPP = min(W,256) per point, 256/TPP points per pass, W/256 columns
-// per thread when W > 256.
+// A thread owns 8 consecutive columns; TPP = W/8 (<= 256) threads per point,
+// 256/TPP points per pass; up to two column groups per thread (W <= 4096).
+// Partials are fp64: part[g][slot][W+1].
 // ---------------------------------------------------------------------------
 template <class T, int ND1, int ND2>
 __global__ void __launch_bounds__(256)
 k_out_bwd(OutBwdArgs<T> p) {
   constexpr int C = 1 + ND1 + ND2;
-  constexpr int MAXC = 16;
-  __shared__ float red[256 * 2];
+  __shared__ double red[256 * 8];
   const int g = blockIdx.z;
   const int W = p.W;
-  const int TPP = W < 256 ? W : 256;
+  const int G8 = W / 8;
+  const int TPP = G8 < 256 ? G8 : 256;
   const int PPP = 256 / TPP;
-  const int NC = W > 256 ? W / 256 : 1;
   const int lt = threadIdx.x % TPP;
   const int lp = threadIdx.x / TPP;
   const int64_t pbeg = (int64_t)blockIdx.x * p.ppb;
@@ -247,192 +303,263 @@ k_out_bwd(OutBwdArgs<T> p) {
   if (pend > p.seg.n_points) pend = p.seg.n_points;
   const float* w = p.wout + g * p.w_g;
   const float* gb = p.gbar + g * p.gb_g;
-  float dw[MAXC];
+  double dw[2][8];
 #pragma unroll
-  for (int c = 0; c < MAXC; ++c) dw[c] = 0.0f;
-  float db = 0.0f;
+  for (int c = 0; c < 2; ++c)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dw[c][e] = 0.0;
+  double db = 0.0;
+  const int64_t pl = p.seg.plane * p.ldo;
   for (int64_t pt = pbeg + lp; pt < pend; pt += PPP) {
     float gk[C];
 #pragma unroll
     for (int k = 0; k < C; ++k) gk[k] = gb[p.seg.row0 + k * p.seg.plane + pt];
     if (lt == 0) db += gk[0];
 #pragma unroll
-    for (int c = 0; c < MAXC; ++c) {
-      if (c >= NC) continue;
-      const int n = lt + 256 * c;
-      const float wn = w[n];
-      float ap[C];
-      int64_t o[C];
+    for (int c = 0; c < 2; ++c) {
+      const int cg = lt + 256 * c;
+      if (cg >= G8) continue;
+      const int n0 = cg * 8;
+      float wn[8];
 #pragma unroll
-      for (int k = 0; k < C; ++k) {
-        o[k] = g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + n;
-        ap[k] = Elem<T>::to_f(p.A[o[k]]);
+      for (int e = 0; e < 8; ++e) wn[e] = w[n0 + e];   // parameter vectors are only 4-byte aligned
+      const int64_t base = g * p.o_g + (p.seg.row0 + pt) * p.ldo + n0;
+      float ap[C][8];
+#pragma unroll
+      for (int k = 0; k < C; ++k) load8<T>(p.A + base + k * pl, ap[k]);
+      float da[C][8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float t, s;
+        tanh_ts(ap[0][e], t, s);
+        const float sp = -2.0f * t * s;
+        const float spp = 2.0f * s * (3.0f * t * t - 1.0f);
+        float hsum = gk[0] * t;
+#pragma unroll
+        for (int i = 0; i < ND1; ++i) hsum += gk[1 + i] * s * ap[1 + i][e];
+#pragma unroll
+        for (int i = 0; i < ND2; ++i)
+          hsum += gk[1 + ND1 + i] * (s * ap[1 + ND1 + i][e] + sp * ap[1 + i][e] * ap[1 + i][e]);
+        dw[c][e] += (double)hsum;
+        float ga = s * gk[0];
+#pragma unroll
+        for (int i = 0; i < ND1; ++i) ga += sp * ap[1 + i][e] * gk[1 + i];
+#pragma unroll
+        for (int i = 0; i < ND2; ++i) ga += (sp * ap[1 + ND1 + i][e] + spp * ap[1 + i][e] * ap[1 + i][e]) * gk[1 + ND1 + i];
+        da[0][e] = ga * wn[e];
+#pragma unroll
+        for (int i = 0; i < ND1; ++i) {
+          float gd = s * gk[1 + i];
+          if (i < ND2) gd += 2.0f * sp * ap[1 + i][e] * gk[1 + ND1 + i];
+          da[1 + i][e] = gd * wn[e];
+        }
+#pragma unroll
+        for (int i = 0; i < ND2; ++i) da[1 + ND1 + i][e] = s * gk[1 + ND1 + i] * wn[e];
       }
-      float t, s;
-      tanh_ts(ap[0], t, s);
-      const float sp = -2.0f * t * s;
-      const float spp = 2.0f * s * (3.0f * t * t - 1.0f);
-      // activations (for dw_out)
-      float hsum = gk[0] * t;
 #pragma unroll
-      for (int i = 0; i < ND1; ++i) hsum += gk[1 + i] * s * ap[1 + i];
-#pragma unroll
-      for (int i = 0; i < ND2; ++i) hsum += gk[1 + ND1 + i] * (s * ap[1 + ND1 + i] + sp * ap[1 + i] * ap[1 + i]);
-      dw[c] += hsum;
-      // carry reverse
-      float ga = s * gk[0] * wn;
-#pragma unroll
-      for (int i = 0; i < ND1; ++i) ga += sp * ap[1 + i] * gk[1 + i] * wn;
-#pragma unroll
-      for (int i = 0; i < ND2; ++i) ga += (sp * ap[1 + ND1 + i] + spp * ap[1 + i] * ap[1 + i]) * gk[1 + ND1 + i] * wn;
-      p.dA[o[0]] = Elem<T>::from_f(ga);
-#pragma unroll
-      for (int i = 0; i < ND1; ++i) {
-        float gd = s * gk[1 + i] * wn;
-        if (i < ND2) gd += 2.0f * sp * ap[1 + i] * gk[1 + ND1 + i] * wn;
-        p.dA[o[1 + i]] = Elem<T>::from_f(gd);
-      }
-#pragma unroll
-      for (int i = 0; i < ND2; ++i) p.dA[o[1 + ND1 + i]] = Elem<T>::from_f(s * gk[1 + ND1 + i] * wn);
+      for (int k = 0; k < C; ++k) store8<T>(p.dA + base + k * pl, da[k]);
     }
   }
-  // block reduction over the PPP point lanes, fixed order
-  float* pw = p.part + ((int64_t)g * p.n_slots + p.slot0 + blockIdx.x) * (W + 1);
+  // block reduction over the PPP point lanes, fixed order, fp64
+  double* pw = p.part + ((int64_t)g * p.n_slots + p.slot0 + blockIdx.x) * (W + 1);
 #pragma unroll
-  for (int c = 0; c < MAXC; ++c) {
-    if (c >= NC) continue;
-    red[threadIdx.x] = dw[c];
+  for (int c = 0; c < 2; ++c) {
+    if (G8 <= 256 * c) continue;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) red[threadIdx.x * 8 + e] = dw[c][e];
     __syncthreads();
-    if (lp == 0) {
-      float s = 0.0f;
-      for (int q = 0; q < PPP; ++q) s += red[q * TPP + lt];
-      pw[lt + 256 * c] = s;
+    const int cg = lt + 256 * c;
+    if (lp == 0 && cg < G8) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        double s = 0.0;
+        for (int q = 0; q < PPP; ++q) s += red[(q * TPP + lt) * 8 + e];
+        pw[cg * 8 + e] = s;
+      }
     }
     __syncthreads();
   }
   red[threadIdx.x] = db;
   __syncthreads();
   if (threadIdx.x == 0) {
-    float s = 0.0f;
+    double s = 0.0;
     for (int q = 0; q < PPP; ++q) s += red[q * TPP];
     pw[W] = s;
   }
 }
 
-// dst[g][n] (+)= scale * sum_slot part[g][slot][n]  for n <= W (n == W: bias)
+// ---------------------------------------------------------------------------
+// dst (+)= scale * sum over slots of part[g][slot][col], fp64, fixed order.
+// 32 columns x 8 slot groups per block; group q sums slots q, q+8, ...; the
+// eight group sums are added in group order.  Column col maps to
+// dst[(col / Jp) * J + col % Jp] and is skipped when col % Jp >= J (padding).
+// ---------------------------------------------------------------------------
+template <class Tin>
 __global__ void __launch_bounds__(256)
-k_reduce_slots(const float* __restrict__ part, int n_slots, int W, float* dst, int64_t d_g, int accumulate,
-               float scale, int32_t* nonfinite) {
+k_colsum(const Tin* __restrict__ part, int64_t p_g, int n_slots, int64_t slot_stride, int64_t ncols, int Jp, int J,
+         float* dst, int64_t d_g, int accumulate, float scale, int32_t* nonfinite) {
+  __shared__ double red[8][32];
   const int g = blockIdx.z;
-  const int n = blockIdx.x * blockDim.x + threadIdx.x;
-  if (n > W) return;
-  const float* src = part + (int64_t)g * n_slots * (W + 1) + n;
-  float s = 0.0f;
-  for (int q = 0; q < n_slots; ++q) s += src[(int64_t)q * (W + 1)];
-  s *= scale;
-  float* o = dst + g * d_g + n;
-  if (accumulate) s += *o;
-  *o = s;
-  if (!__builtin_isfinite(s)) *nonfinite = 1;
+  const int lane = threadIdx.x & 31, grp = threadIdx.x >> 5;
+  const int64_t col = (int64_t)blockIdx.x * 32 + lane;
+  double s = 0.0;
+  if (col < ncols) {
+    const Tin* src = part + g * p_g + col;
+#pragma unroll 8
+    for (int q = grp; q < n_slots; q += 8) s += (double)src[(int64_t)q * slot_stride];
+  }
+  red[grp][lane] = s;
+  __syncthreads();
+  if (grp == 0 && col < ncols) {
+    double v = 0.0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v += red[q][lane];
+    const int64_t n = col / Jp;
+    const int j = (int)(col % Jp);
+    if (j < J) {
+      float* o = dst + g * d_g + n * J + j;
+      float r = (float)(v * (double)scale);
+      if (accumulate) r += *o;
+      *o = r;
+      if (!__builtin_isfinite(r)) *nonfinite = 1;
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
-// first-layer reverse pass, per sample s and column n:
-//   gs   = sum over value rows of s of dA_1
-//   gx_i = sum over value rows of s of dA_1 * x_i
-//   gd_i = sum over d/dx_i rows of s of dA_1   (a'_i = W1[:, i])
-// part[g][s][q][n] with q = 0 (gs), 1..3 (gx_i), 4..6 (gd_i); unused slots 0
+// first-layer reverse pass.  Block (s, rc) covers chunk rc of sample s's
+// sensor rows and collocation points; per column n it sums
+//   q=0   : dA_1 over value rows                       (gs)
+//   q=1..3: dA_1 * x_i over value rows                  (gx_i)
+//   q=4..6: dA_1 over the d/dx_i rows                   (gd_i; a'_i = W1[:, i])
+// into part[g][s][rc][q][n] (fp32; slots beyond d stay zero).
 // ---------------------------------------------------------------------------
 template <class T>
 __global__ void __launch_bounds__(256)
 k_first_bwd(FirstBwdArgs<T> p) {
-  __shared__ float red[256];
+  __shared__ float red[256 * 8];
   const int g = blockIdx.z;
-  const int s = blockIdx.x;
+  const int s = blockIdx.x / p.nrc;
+  const int rc = blockIdx.x % p.nrc;
   const int W = p.W;
-  const int TPP = W < 256 ? W : 256;
+  const int G8 = W / 8;
+  const int TPP = G8 < 256 ? G8 : 256;
   const int PPP = 256 / TPP;
   const int lt = threadIdx.x % TPP;
   const int lp = threadIdx.x / TPP;
-  const int n = blockIdx.y * 256 + lt;
+  const int cg = blockIdx.y * 256 + lt;
+  const bool valid = cg < G8;
+  const int n0 = cg * 8;
   const int d = p.d;
-  float acc[7];
+  float acc[7][8];
 #pragma unroll
-  for (int q = 0; q < 7; ++q) acc[q] = 0.0f;
+  for (int q = 0; q < 7; ++q)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[q][e] = 0.0f;
   const T* A = p.dA + g * p.a_g;
-  if (n < W) {
-    // sensor rows of sample s (value stream only)
-    for (int j = lp; j < p.n_s; j += PPP) {
-      const float v = Elem<T>::to_f(A[((int64_t)s * p.n_s + j) * p.lda + n]);
+  if (valid) {
+    const int j0 = (int)((int64_t)p.n_s * rc / p.nrc), j1 = (int)((int64_t)p.n_s * (rc + 1) / p.nrc);
+    for (int j = j0 + lp; j < j1; j += PPP) {
+      float v[8];
+      load8<T>(A + ((int64_t)s * p.n_s + j) * p.lda + n0, v);
       const float* xv = p.xs + g * p.xs_g + (int64_t)j * d;
-      acc[0] += v;
+      float x[3];
 #pragma unroll
-      for (int i = 0; i < 3; ++i)
-        if (i < d) acc[1 + i] += v * xv[i];
+      for (int i = 0; i < 3; ++i) x[i] = i < d ? xv[i] : 0.0f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        acc[0][e] += v[e];
+#pragma unroll
+        for (int i = 0; i < 3; ++i) acc[1 + i][e] += v[e] * x[i];
+      }
     }
-    // collocation rows of sample s
-    for (int q = lp; q < p.P; q += PPP) {
+    const int q0 = (int)((int64_t)p.P * rc / p.nrc), q1 = (int)((int64_t)p.P * (rc + 1) / p.nrc);
+    for (int q = q0 + lp; q < q1; q += PPP) {
       const int64_t pt = (int64_t)s * p.P + q;
-      const float v = Elem<T>::to_f(A[(p.n_sen + pt) * p.lda + n]);
+      float v[8];
+      load8<T>(A + (p.n_sen + pt) * p.lda + n0, v);
       const float* xv = p.xc + g * p.xc_g + pt * d;
-      acc[0] += v;
+      float x[3];
 #pragma unroll
-      for (int i = 0; i < 3; ++i)
-        if (i < d) acc[1 + i] += v * xv[i];
+      for (int i = 0; i < 3; ++i) x[i] = i < d ? xv[i] : 0.0f;
 #pragma unroll
-      for (int i = 0; i < 3; ++i)
-        if (i < p.nd1) acc[4 + i] += Elem<T>::to_f(A[(p.n_sen + (1 + i) * p.n_col + pt) * p.lda + n]);
+      for (int e = 0; e < 8; ++e) {
+        acc[0][e] += v[e];
+#pragma unroll
+        for (int i = 0; i < 3; ++i) acc[1 + i][e] += v[e] * x[i];
+      }
+#pragma unroll
+      for (int i = 0; i < 3; ++i) {
+        if (i >= p.nd1) continue;
+        float u[8];
+        load8<T>(A + (p.n_sen + (1 + i) * p.n_col + pt) * p.lda + n0, u);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[4 + i][e] += u[e];
+      }
     }
   }
-  float* out = p.part + (((int64_t)g * p.S + s) * 7) * W;
+  float* out = p.part + (((int64_t)g * p.S + s) * p.nrc + rc) * 7 * W;
 #pragma unroll
   for (int q = 0; q < 7; ++q) {
-    red[threadIdx.x] = acc[q];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) red[threadIdx.x * 8 + e] = acc[q][e];
     __syncthreads();
-    if (lp == 0 && n < W) {
-      float v = 0.0f;
-      for (int u = 0; u < PPP; ++u) v += red[u * TPP + lt];
-      out[(int64_t)q * W + n] = v;
+    if (lp == 0 && valid) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float t = 0.0f;
+        for (int u = 0; u < PPP; ++u) t += red[(u * TPP + lt) * 8 + e];
+        v[e] = t;
+      }
+      store8<float>(out + (int64_t)q * W + n0, v);
     }
     __syncthreads();
   }
 }
 
-// dW1[n][c] and db1[n] from the per-sample partials:
-//   c < d : sum_s gx_c + gd_c ;  c >= d : sum_s gs z_s[c-d] ;  bias: sum_s gs
+// dW1[n][c] and db1[n] from the partials (fp64 sums, fixed order):
+//   c < d : sum_{s,rc} gx_c + gd_c ;  c >= d : sum_{s,rc} gs * z_s[c-d] ;
+//   bias (blockIdx.y == in_dim) : sum_{s,rc} gs
 __global__ void __launch_bounds__(256)
-k_first_wgrad(const float* __restrict__ part, int S, int W, int d, int nd1, int in_dim,
+k_first_wgrad(const float* __restrict__ part, int S, int nrc, int W, int d, int nd1, int in_dim,
               const float* __restrict__ z, int64_t z_g, int n_z, float* grad, int64_t g_g, int accumulate,
               float scale, int32_t* nonfinite) {
+  __shared__ double red[8][32];
   const int g = blockIdx.z;
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t nW = (int64_t)W * in_dim;
-  if (idx >= nW + W) return;
-  const float* pp = part + (int64_t)g * S * 7 * W;
-  float v = 0.0f;
-  int64_t o;
-  if (idx < nW) {
-    const int n = (int)(idx / in_dim), c = (int)(idx % in_dim);
-    if (c < d) {
-      for (int s = 0; s < S; ++s) {
-        v += pp[((int64_t)s * 7 + 1 + c) * W + n];
-        if (c < nd1) v += pp[((int64_t)s * 7 + 4 + c) * W + n];
+  const int c = blockIdx.y;
+  const int lane = threadIdx.x & 31, grp = threadIdx.x >> 5;
+  const int n = blockIdx.x * 32 + lane;
+  double acc = 0.0;
+  if (n < W) {
+    const float* pp = part + (int64_t)g * S * nrc * 7 * W + n;
+    for (int s = grp; s < S; s += 8) {
+      float zz = 1.0f;
+      if (c >= d && c < in_dim) zz = z[g * z_g + (int64_t)s * n_z + (c - d)];
+      for (int r = 0; r < nrc; ++r) {
+        const float* b = pp + ((int64_t)s * nrc + r) * 7 * W;
+        if (c < d) {
+          acc += (double)b[(int64_t)(1 + c) * W];
+          if (c < nd1) acc += (double)b[(int64_t)(4 + c) * W];
+        } else {
+          acc += (double)b[0] * (double)zz;
+        }
       }
-    } else {
-      const float* zz = z + g * z_g + (c - d);
-      for (int s = 0; s < S; ++s) v += pp[((int64_t)s * 7) * W + n] * zz[(int64_t)s * n_z];
     }
-    o = idx;
-  } else {
-    const int n = (int)(idx - nW);
-    for (int s = 0; s < S; ++s) v += pp[((int64_t)s * 7) * W + n];
-    o = nW + n;
   }
-  v *= scale;
-  float* dst = grad + g * g_g + o;
-  if (accumulate) v += *dst;
-  *dst = v;
-  if (!__builtin_isfinite(v)) *nonfinite = 1;
+  red[grp][lane] = acc;
+  __syncthreads();
+  if (grp == 0 && n < W) {
+    double v = 0.0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v += red[q][lane];
+    const int64_t o = c < in_dim ? (int64_t)n * in_dim + c : (int64_t)W * in_dim + n;
+    float* dst = grad + g * g_g + o;
+    float r = (float)(v * (double)scale);
+    if (accumulate) r += *dst;
+    *dst = r;
+    if (!__builtin_isfinite(r)) *nonfinite = 1;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -491,7 +618,7 @@ hipError_t launch_zproj(const float* p1, int64_t p_g, int in_dim, int d, int W, 
 template <class T>
 hipError_t launch_first_fwd(int nd1, int nd2, const FirstArgs<T>& a, int G, hipStream_t st) {
   if (a.seg.n_points <= 0) return hipSuccess;
-  dim3 grid(nblk(a.seg.n_points * a.W, 256), 1, G);
+  dim3 grid(nblk(a.seg.n_points * (a.W / 8), 256), 1, G);
   switch (nd1 * 10 + nd2) {
     case 0: k_first_fwd<T, 0, 0><<<grid, 256, 0, st>>>(a); break;
     case 10: k_first_fwd<T, 1, 0><<<grid, 256, 0, st>>>(a); break;
@@ -565,27 +692,33 @@ hipError_t launch_out_bwd(int nd1, int nd2, const OutBwdArgs<T>& a, int G, hipSt
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_slots(const float* part, int n_slots, int W, float* dst, int64_t d_g, int accumulate,
-                               float scale, int32_t* nonfinite, int G, hipStream_t st) {
-  k_reduce_slots<<<dim3(nblk(W + 1, 256), 1, G), 256, 0, st>>>(part, n_slots, W, dst, d_g, accumulate, scale,
-                                                              nonfinite);
+template <class Tin>
+hipError_t launch_colsum(const Tin* part, int64_t p_g, int n_slots, int64_t slot_stride, int64_t ncols, int Jp, int J,
+                         float* dst, int64_t d_g, int accumulate, float scale, int32_t* nonfinite, int G,
+                         hipStream_t st) {
+  if (ncols <= 0) return hipSuccess;
+  k_colsum<Tin><<<dim3(nblk(ncols, 32), 1, G), 256, 0, st>>>(part, p_g, n_slots, slot_stride, ncols, Jp, J, dst, d_g,
+                                                            accumulate, scale, nonfinite);
   return hipGetLastError();
 }
+template hipError_t launch_colsum<float>(const float*, int64_t, int, int64_t, int64_t, int, int, float*, int64_t, int,
+                                         float, int32_t*, int, hipStream_t);
+template hipError_t launch_colsum<double>(const double*, int64_t, int, int64_t, int64_t, int, int, float*, int64_t,
+                                          int, float, int32_t*, int, hipStream_t);
 
 template <class T>
 hipError_t launch_first_bwd(const FirstBwdArgs<T>& a, int G, hipStream_t st) {
   if (a.S <= 0) return hipSuccess;
-  dim3 grid(a.S, nblk(a.W, 256), G);
+  dim3 grid(a.S * a.nrc, nblk(a.W / 8, 256), G);
   k_first_bwd<T><<<grid, 256, 0, st>>>(a);
   return hipGetLastError();
 }
 
-hipError_t launch_first_wgrad(const float* part, int S, int W, int d, int nd1, int in_dim, const float* z,
+hipError_t launch_first_wgrad(const float* part, int S, int nrc, int W, int d, int nd1, int in_dim, const float* z,
                               int64_t z_g, int n_z, float* grad, int64_t g_g, int accumulate, float scale,
                               int32_t* nonfinite, int G, hipStream_t st) {
-  const int64_t tot = (int64_t)W * in_dim + W;
-  k_first_wgrad<<<dim3(nblk(tot, 256), 1, G), 256, 0, st>>>(part, S, W, d, nd1, in_dim, z, z_g, n_z, grad, g_g,
-                                                             accumulate, scale, nonfinite);
+  k_first_wgrad<<<dim3(nblk(W, 32), in_dim + 1, G), 256, 0, st>>>(part, S, nrc, W, d, nd1, in_dim, z, z_g, n_z, grad,
+                                                                  g_g, accumulate, scale, nonfinite);
   return hipGetLastError();
 }
 

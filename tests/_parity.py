@@ -50,6 +50,24 @@ def check(errs: dict, tol: float, label: str = ""):
     assert not bad, msg
 
 
+COND_FACTOR = 3.0
+
+
+def check_conditioned(errs: dict, errs_model: dict, tol: float, label: str = ""):
+    """Per-tensor bar: err <= max(tol, COND_FACTOR * err_model), where err_model
+    is the distance of the oracle's own precision model (same storage format,
+    fp32 accumulation) from the exact result.  A tensor whose value is a sum of
+    nearly cancelling terms amplifies storage rounding; the precision model
+    measures that amplification on the same inputs."""
+    lim = {k: max(tol, COND_FACTOR * errs_model.get(k, 0.0)) for k in errs}
+    bad = {k: (v, lim[k]) for k, v in errs.items() if not (v <= lim[k])}
+    ratio = sorted(((v / lim[k], k) for k, v in errs.items()), reverse=True)[:6]
+    msg = (f"{label} tol={tol:g} worst err/limit: "
+           + ", ".join(f"{k}={errs[k]:.3g}/{lim[k]:.3g}" for _, k in ratio))
+    print(msg)
+    assert not bad, msg
+
+
 def to_dev(a, dev="cuda"):
     import torch
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)

@@ -1,0 +1,102 @@
+"""Parity at the full benchmark size (2-D Darcy, 4x128 generators, S=256 noise
+samples x P=1024 collocation points, 200+200 sensors, 3x256 discriminator,
+bf16), in the launch configuration the benchmark times:
+
+* generator jets at sampled (sample, point) pairs against the oracle;
+* the three losses against the oracle evaluated at full size;
+* gradients through a property that holds at any size: the step is a mean
+  over noise samples, so the full step equals the average of the steps on
+  the two halves of the samples (same real batch)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_1910_13444_amd import configs, pigan
+from paper_1910_13444_amd.inputs import make_inputs
+from _parity import TOL, check, check_conditioned, rel, run_step_gpu, to_dev
+
+pytestmark = pytest.mark.gpu
+
+WL = configs.C2
+
+
+@pytest.fixture(scope="module")
+def full():
+    inp = make_inputs(WL)
+    real = oracle.real_snapshots(WL, inp)
+    return inp, real
+
+
+def test_full_jets_sampled(full):
+    import torch
+    inp, _ = full
+    print("full-size jets, sampled", flush=True)
+    shape = WL.gen_shape()
+    rng = np.random.default_rng(11)
+    ss = rng.integers(0, WL.S, 24)
+    pp = rng.integers(0, WL.P, 24)
+    for name, p, order in (("Y", inp.pY, 1), ("U", inp.pU, 2)):
+        jet = pigan.gen_forward(to_dev(p), shape, WL.d, to_dev(inp.z), to_dev(inp.xc), order, dtype=WL.dtype)
+        torch.cuda.synchronize()
+        got = jet.cpu().numpy()[0][:, ss, pp]                       # [c, 24]
+        X = inp.xc[0][ss, pp]
+        Z = inp.z[0][ss]
+        o = oracle.gen_forward(p[0], shape, WL.d, X, Z, order)
+        ref = [o["y"]] + ([o["dy"][i] for i in range(WL.d)] if order >= 1 else []) + \
+              ([o["ddy"][i] for i in range(WL.d)] if order >= 2 else [])
+        check({f"{name}.c{k}": rel(got[k], ref[k]) for k in range(len(ref))}, TOL[WL.dtype], f"full jets {name}")
+
+
+def _oracle_losses(inp, real, prec=None, with_pde=True, chunk=32):
+    """Losses of the step at full size from the oracle's forward passes."""
+    gs, ds, d = WL.gen_shape(), WL.disc_shape(), WL.d
+    g = 0
+    F = oracle.snapshots(inp.pY[g], inp.pU[g], gs, d, inp.xsY[g], inp.xsU[g], inp.z[g]) if prec is None else None
+    if prec is not None:
+        from oracle.pigan_oracle import sensor_rows, gen_forward
+        S = inp.z.shape[1]
+        XY, ZY = sensor_rows(inp.xsY[g], inp.z[g])
+        XU, ZU = sensor_rows(inp.xsU[g], inp.z[g])
+        F = np.concatenate([gen_forward(inp.pY[g], gs, d, XY, ZY, 0, prec=prec)["y"].reshape(S, -1),
+                            gen_forward(inp.pU[g], gs, d, XU, ZU, 0, prec=prec)["y"].reshape(S, -1)], axis=1)
+    DF = oracle.mlp_forward(inp.pD[g], ds, F, prec=prec)
+    DR = oracle.mlp_forward(inp.pD[g], ds, real[g], prec=prec)
+    w = float(inp.w_group[g])
+    out = {"L_D": w * (DF.mean() - DR.mean()), "L_adv": -w * DF.mean()}
+    if with_pde:
+        r2 = 0.0
+        for s0 in range(0, WL.S, chunk):
+            z = inp.z[g][s0:s0 + chunk]
+            x = inp.xc[g][s0:s0 + chunk]
+            jY = oracle.gen_jets(inp.pY[g], gs, d, z, x, 1)
+            jU = oracle.gen_jets(inp.pU[g], gs, d, z, x, 2)
+            r = oracle.darcy_residual(jY[0], jY[1:1 + d], jU[1:1 + d], jU[1 + d:], WL.f_const)
+            r2 += float((r * r).sum())
+        out["L_pde"] = w * WL.lambda_pde * r2 / (WL.S * WL.P)
+    return out
+
+
+def test_full_losses(full):
+    inp, real = full
+    print("full-size step losses", flush=True)
+    out = run_step_gpu(WL, inp, real)
+    assert out["nonfinite"] == 0
+    ref = _oracle_losses(inp, real)
+    errs = {k: rel(out["loss"][0, i], ref[k]) for i, k in enumerate(("L_D", "L_adv", "L_pde"))}
+    model = _oracle_losses(inp, real, prec=WL.dtype, with_pde=False)
+    merrs = {k: rel(model[k], ref[k]) for k in ("L_D", "L_adv")}
+    check_conditioned(errs, merrs, TOL[WL.dtype], "full losses")
+
+
+def test_full_step_is_mean_of_half_steps(full):
+    inp, real = full
+    print("full-size sample split", flush=True)
+    a = run_step_gpu(WL, inp, real)
+    halves = []
+    for lo, hi in ((0, WL.S // 2), (WL.S // 2, WL.S)):
+        h = make_inputs(WL)
+        h.z = inp.z[:, lo:hi].copy()
+        h.xc = inp.xc[:, lo:hi].copy()
+        halves.append(run_step_gpu(WL, h, real))
+    errs = {k: rel(0.5 * (halves[0][k] + halves[1][k]), a[k]) for k in ("gY", "gU", "gD", "loss")}
+    check(errs, 1e-4, "sample split")
