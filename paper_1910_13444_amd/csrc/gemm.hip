@@ -21,7 +21,8 @@
 // The split partials are summed in fp64, in split order, by k_colsum.
 //
 // Tiles: a 64-lane wave owns 32 points x 32*NT columns for every stream; the
-// block is WM x WN waves.  Operands are staged through LDS in 64-byte k-slices
+// block is WM x WN waves.  The MFMA computes W . X^T so that a lane holds one
+// point and runs of four columns (vector stores, lane-local derivative carry).  Operands are staged through LDS in 64-byte k-slices
 // (80-byte row pitch, conflict-free 16-byte fragment reads) with the next
 // slice prefetched into registers while the current one is multiplied.
 #include "common.h"
@@ -30,20 +31,62 @@ namespace pigan {
 
 static constexpr int LDS_PITCH = 80;
 
+// Workgroups are dispatched round-robin over the 8 XCDs (each with its own
+// L2).  Map hardware block b to a logical tile so that every XCD walks one
+// contiguous range of logical tiles: blocks that share an operand tile run on
+// the same XCD at about the same time.  Bijective for any block count.
+__device__ __forceinline__ int64_t xcd_remap(int64_t b, int64_t nb) {
+  const int64_t q = nb / 8, r = nb % 8;
+  const int64_t x = b % 8, local = b / 8;
+  return x < r ? x * (q + 1) + local : r * (q + 1) + (x - r) * q + local;
+}
+
+// four consecutive elements in the storage type (8 bytes in bf16/fp16, 16 in fp32)
+template <class T>
+__device__ __forceinline__ void store4(T* p, const float* v) {
+  if (sizeof(T) == 2) {
+    uint2 raw;
+    T* e = (T*)&raw;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) e[i] = Elem<T>::from_f(v[i]);
+    *(uint2*)p = raw;
+  } else {
+    *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
+  }
+}
+
+template <class T>
+__device__ __forceinline__ void load4(const T* p, float* v) {
+  if (sizeof(T) == 2) {
+    const uint2 raw = *(const uint2*)p;
+    const T* e = (const T*)&raw;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = Elem<T>::to_f(e[i]);
+  } else {
+    const float4 a = *(const float4*)p;
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  }
+}
+
 template <class T, int ND1, int ND2, int WM, int WN, int NT, int EPI>
-__global__ void __launch_bounds__(64 * WM * WN)
+__global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(ND1 + ND2 >= 6 ? 1 : 2)))
 k_gemm_nt(const NtArgs<T> p) {
   constexpr int C = 1 + ND1 + ND2;
   constexpr int BM = 32 * WM;
   constexpr int BN = 32 * NT * WN;
   constexpr int NTH = 64 * WM * WN;
-  constexpr int KS = 64 / (int)sizeof(T);          // k values per stage
-  constexpr int NCH = 64 / (16 * (int)sizeof(T));  // 16-wide chunks per stage
+  constexpr int ES = (int)sizeof(T);
+  constexpr int KS = 64 / ES;                      // k values per stage
+  constexpr int NCH = 64 / (16 * ES);              // 16-wide chunks per stage
   constexpr int ROWS = C * BM + BN;
+  constexpr int STAGE = ROWS * LDS_PITCH;          // bytes of one operand stage
   constexpr int PIECES = ROWS * 4;
   constexpr int PPT = (PIECES + NTH - 1) / NTH;
+  constexpr int OPITCH = BN * ES + 16;             // epilogue staging pitch (bytes)
+  constexpr int OUTB = BM * OPITCH;
+  constexpr int LDSB = 2 * STAGE > OUTB ? 2 * STAGE : OUTB;
   typedef typename Elem<T>::frag frag;
-  __shared__ __attribute__((aligned(16))) char lds[ROWS * LDS_PITCH];
+  __shared__ __attribute__((aligned(16))) char lds[LDSB];
 
   const int g = blockIdx.z;
   const int tid = threadIdx.x;
@@ -51,31 +94,37 @@ k_gemm_nt(const NtArgs<T> p) {
   const int wave = tid >> 6;
   const int wm = wave % WM;
   const int wn = wave / WM;
-  const int64_t m0 = (int64_t)blockIdx.x * BM;
-  const int n0 = blockIdx.y * BN;
+  // logical tile: column tiles fastest, so the blocks reading one tile of
+  // activations run together on one XCD and share it through its L2
+  const int ntn = (p.N + BN - 1) / BN;
+  const int64_t lt = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t m0 = (lt / ntn) * BM;
+  const int n0 = (int)(lt % ntn) * BN;
   const int64_t npts = p.seg.n_points;
 
   const char* Xb = (const char*)(p.X + g * p.x_g);
   const char* Wb = (const char*)(p.Wm + g * p.w_g);
 
-  int64_t srcoff[PPT];
+  // each thread moves PPT 16-byte pieces of every stage: operand row piece>>2,
+  // 16-byte segment piece&3 of its 64-byte k-slice
+  const char* src[PPT];
   bool valid[PPT];
 #pragma unroll
   for (int i = 0; i < PPT; ++i) {
     const int piece = tid + i * NTH;
     const int row = piece >> 2, sg = piece & 3;
     valid[i] = false;
-    srcoff[i] = 0;
+    src[i] = Xb;
     if (piece < PIECES) {
       if (row < C * BM) {
         const int k = row / BM, pp = row % BM;
         const int64_t pt = m0 + pp;
         valid[i] = pt < npts;
-        srcoff[i] = (p.seg.row0 + k * p.seg.plane + pt) * p.ldx * (int64_t)sizeof(T) + sg * 16;
+        src[i] = Xb + (p.seg.row0 + k * p.seg.plane + pt) * p.ldx * (int64_t)ES + sg * 16;
       } else {
         const int n = n0 + row - C * BM;
         valid[i] = n < p.N;
-        srcoff[i] = (int64_t)n * p.ldw * (int64_t)sizeof(T) + sg * 16;
+        src[i] = Wb + (int64_t)n * p.ldw * (int64_t)ES + sg * 16;
       }
     }
   }
@@ -88,121 +137,202 @@ k_gemm_nt(const NtArgs<T> p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[k][t][r] = 0.0f;
 
-  uint4 buf[PPT];
-  auto gload = [&](int kt) {
+  auto gload = [&](uint4* buf, int kt) {
+#pragma unroll
+    for (int i = 0; i < PPT; ++i)
+      buf[i] = valid[i] ? *(const uint4*)(src[i] + (int64_t)kt * 64) : make_uint4(0u, 0u, 0u, 0u);
+  };
+  auto lstore = [&](const uint4* buf, int stage) {
+    char* base = lds + stage * STAGE;
 #pragma unroll
     for (int i = 0; i < PPT; ++i) {
       const int piece = tid + i * NTH;
-      const int row = piece >> 2;
-      if (valid[i]) {
-        const char* base = row < C * BM ? Xb : Wb;
-        buf[i] = *(const uint4*)(base + srcoff[i] + (int64_t)kt * 64);
-      } else {
-        buf[i] = make_uint4(0u, 0u, 0u, 0u);
+      if (piece < PIECES) *(uint4*)(base + (piece >> 2) * LDS_PITCH + (piece & 3) * 16) = buf[i];
+    }
+  };
+  auto compute = [&](int stage) {
+    const char* base = lds + stage * STAGE;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int koff = c * 32 + (lane >> 5) * (8 * ES);
+      frag bfr[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        bfr[t] = *(const frag*)(base + (C * BM + 32 * (wn * NT + t) + (lane & 31)) * LDS_PITCH + koff);
+#pragma unroll
+      for (int k = 0; k < C; ++k) {
+        const frag afr = *(const frag*)(base + (k * BM + 32 * wm + (lane & 31)) * LDS_PITCH + koff);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) Elem<T>::mma(acc[k][t], bfr[t], afr);   // rows: columns n; cols: points
       }
     }
   };
 
+  // two LDS stages, two register buffers: the global loads of stage kt+2 are
+  // issued before stage kt is multiplied; one barrier per stage
   const int nk = p.K / KS;
-  gload(0);
-  for (int kt = 0; kt < nk; ++kt) {
+  uint4 b0[PPT], b1[PPT];
+  gload(b0, 0);
+  lstore(b0, 0);
+  if (nk > 1) gload(b1, 1);
+  __syncthreads();
+  for (int kt = 0; kt < nk; kt += 2) {
+    if (kt + 2 < nk) gload(b0, kt + 2);
+    compute(0);
+    if (kt + 1 < nk) lstore(b1, 1);
     __syncthreads();
-#pragma unroll
-    for (int i = 0; i < PPT; ++i) {
-      const int piece = tid + i * NTH;
-      if (piece < PIECES) *(uint4*)(lds + (piece >> 2) * LDS_PITCH + (piece & 3) * 16) = buf[i];
-    }
+    if (kt + 1 >= nk) break;
+    if (kt + 3 < nk) gload(b1, kt + 3);
+    compute(1);
+    if (kt + 2 < nk) lstore(b0, 0);
     __syncthreads();
-    if (kt + 1 < nk) gload(kt + 1);
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      const int koff = c * 32 + (lane >> 5) * (8 * (int)sizeof(T));
-      frag bfr[NT];
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-        bfr[t] = *(const frag*)(lds + (C * BM + 32 * (wn * NT + t) + (lane & 31)) * LDS_PITCH + koff);
-#pragma unroll
-      for (int k = 0; k < C; ++k) {
-        const frag afr = *(const frag*)(lds + (k * BM + 32 * wm + (lane & 31)) * LDS_PITCH + koff);
-#pragma unroll
-        for (int t = 0; t < NT; ++t) Elem<T>::mma(acc[k][t], afr, bfr[t]);
-      }
-    }
   }
 
-  // ---- epilogue: lane owns column (lane & 31) and 16 rows of every 32x32 tile
+  // ---- epilogue.  The products were formed as W . X^T, so lane (m = lane & 31)
+  // owns one point and, in register group q (regs 4q..4q+3), four consecutive
+  // columns 8q + 4*(lane >> 5) + 0..3 of every 32x32 tile: all jet streams of a
+  // (point, column) sit in the same lane.  Results are staged through LDS one
+  // stream at a time and leave in full 16-byte row segments.
   const int hh = lane >> 5;
+  const int ml = 32 * wm + (lane & 31);            // point within the block
+  const int64_t pt = m0 + ml;
+  const bool pvalid = pt < npts;
+  auto ncol = [&](int t, int q) { return 32 * (wn * NT + t) + 8 * q + 4 * hh; };   // column within the block
+
+  if (EPI == EPI_DF) {
+    if (pvalid) {
 #pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    const int n = n0 + 32 * (wn * NT + t) + (lane & 31);
-    if (n >= p.N) continue;
-    float bn = 0.0f;
-    if (EPI == EPI_FWD && p.bias) bn = p.bias[g * p.b_g + n];
+      for (int t = 0; t < NT; ++t)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int64_t pt = m0 + 32 * wm + 8 * (r >> 2) + 4 * hh + (r & 3);
-      if (pt >= npts) continue;
-      int64_t o[C];
+        for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int k = 0; k < C; ++k) o[k] = g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + n;
-      if (EPI == EPI_FWD) {
-        const float a0 = acc[0][t][r] + bn;
+          for (int e = 0; e < 4; ++e) {
+            const int n = n0 + ncol(t, q) + e;
+            const float v = p.df_sign * acc[0][t][4 * q + e];
+            if (n < p.nY) p.seedY[g * p.sY_g + pt * p.nY + n] = v;
+            else if (n < p.nY + p.nU) p.seedU[g * p.sU_g + pt * p.nU + (n - p.nY)] = v;
+          }
+    }
+    return;
+  }
+
+  // staging: one [BM x BN] plane at a time through LDS, copied out in full
+  // 16-byte row segments
+  constexpr int CPR = BN * ES / 16;                // 16-byte chunks per staged row
+  constexpr int CHUNKS = BM * CPR;
+  auto stage_out = [&](int k, T* dst) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = acc[k][t][4 * q + e];
+        store4<T>((T*)(lds + ml * OPITCH + ncol(t, q) * ES), v);
+      }
+    __syncthreads();
+#pragma unroll
+    for (int i = tid; i < CHUNKS; i += NTH) {
+      const int row = i / CPR, ch = i % CPR;
+      const int64_t ptr = m0 + row;
+      const int n = n0 + ch * (16 / ES);
+      if (ptr < npts && n < p.N)
+        *(uint4*)(dst + g * p.o_g + (p.seg.row0 + k * p.seg.plane + ptr) * p.ldo + n) =
+            *(const uint4*)(lds + row * OPITCH + ch * 16);
+    }
+    __syncthreads();
+  };
+
+  if (EPI == EPI_FWD) {
+    // pre-activations (bias on the value stream), then activations in place:
+    //   h = t, h'_i = s a'_i, h''_i = s a''_i + s' (a'_i)^2
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int n = n0 + ncol(t, r >> 2) + (r & 3);
+        if (p.bias && n < p.N) acc[0][t][r] += p.bias[g * p.b_g + n];
+      }
+    if (p.out_a) {
+#pragma unroll
+      for (int k = 0; k < C; ++k) stage_out(k, p.out_a);
+    }
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
         float tt, s;
-        tanh_ts(a0, tt, s);
+        tanh_ts(acc[0][t][r], tt, s);
         const float sp = -2.0f * tt * s;
-        if (p.out_a) {
-          p.out_a[o[0]] = Elem<T>::from_f(a0);
 #pragma unroll
-          for (int k = 1; k < C; ++k) p.out_a[o[k]] = Elem<T>::from_f(acc[k][t][r]);
-        }
-        p.out_h[o[0]] = Elem<T>::from_f(tt);
+        for (int i = 0; i < ND2; ++i)
+          acc[1 + ND1 + i][t][r] = s * acc[1 + ND1 + i][t][r] + sp * acc[1 + i][t][r] * acc[1 + i][t][r];
 #pragma unroll
-        for (int i = 0; i < ND1; ++i) p.out_h[o[1 + i]] = Elem<T>::from_f(s * acc[1 + i][t][r]);
+        for (int i = 0; i < ND1; ++i) acc[1 + i][t][r] *= s;
+        acc[0][t][r] = tt;
+      }
 #pragma unroll
-        for (int i = 0; i < ND2; ++i) {
-          const float a1 = acc[1 + i][t][r];
-          p.out_h[o[1 + ND1 + i]] = Elem<T>::from_f(s * acc[1 + ND1 + i][t][r] + sp * a1 * a1);
-        }
-      } else if (EPI == EPI_BWD) {
-        float ap[C];
+    for (int k = 0; k < C; ++k) stage_out(k, p.out_h);
+    return;
+  }
+
+  // reverse carry, in place: acc[k] becomes the cotangent of the saved
+  // pre-activation a_k of the layer below
 #pragma unroll
-        for (int k = 0; k < C; ++k) ap[k] = Elem<T>::to_f(p.aprev[o[k]]);
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int nb = n0 + ncol(t, q);
+      float ap[C][4];
+#pragma unroll
+      for (int k = 0; k < C; ++k) {
+        if (pvalid && nb < p.N) load4<T>(p.aprev + g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + nb, ap[k]);
+        else ap[k][0] = ap[k][1] = ap[k][2] = ap[k][3] = 0.0f;
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 4 * q + e;
         float tt, s;
-        tanh_ts(ap[0], tt, s);
+        tanh_ts(ap[0][e], tt, s);
         const float sp = -2.0f * tt * s;
         const float spp = 2.0f * s * (3.0f * tt * tt - 1.0f);
         float ga = s * acc[0][t][r];
 #pragma unroll
-        for (int i = 0; i < ND1; ++i) ga += sp * ap[1 + i] * acc[1 + i][t][r];
+        for (int i = 0; i < ND1; ++i) ga += sp * ap[1 + i][e] * acc[1 + i][t][r];
 #pragma unroll
         for (int i = 0; i < ND2; ++i)
-          ga += (sp * ap[1 + ND1 + i] + spp * ap[1 + i] * ap[1 + i]) * acc[1 + ND1 + i][t][r];
-        p.out_da[o[0]] = Elem<T>::from_f(ga);
+          ga += (sp * ap[1 + ND1 + i][e] + spp * ap[1 + i][e] * ap[1 + i][e]) * acc[1 + ND1 + i][t][r];
 #pragma unroll
         for (int i = 0; i < ND1; ++i) {
-          float gd = s * acc[1 + i][t][r];
-          if (i < ND2) gd += 2.0f * sp * ap[1 + i] * acc[1 + ND1 + i][t][r];
-          p.out_da[o[1 + i]] = Elem<T>::from_f(gd);
+          float v = s * acc[1 + i][t][r];
+          if (i < ND2) v += 2.0f * sp * ap[1 + i][e] * acc[1 + ND1 + i][t][r];
+          acc[1 + i][t][r] = v;
         }
 #pragma unroll
-        for (int i = 0; i < ND2; ++i) p.out_da[o[1 + ND1 + i]] = Elem<T>::from_f(s * acc[1 + ND1 + i][t][r]);
-      } else {  // EPI_DF: rows are fake snapshots (samples), columns snapshot entries
-        const float v = p.df_sign * acc[0][t][r];
-        if (n < p.nY) p.seedY[g * p.sY_g + pt * p.nY + n] = v;
-        else if (n < p.nY + p.nU) p.seedU[g * p.sU_g + pt * p.nU + (n - p.nY)] = v;
+        for (int i = 0; i < ND2; ++i) acc[1 + ND1 + i][t][r] *= s;
+        acc[0][t][r] = ga;
       }
     }
-  }
+#pragma unroll
+  for (int k = 0; k < C; ++k) stage_out(k, p.out_da);
 }
 
 // ---------------------------------------------------------------------------
 // dW[n][j] = sum_{rows m} dA[m][n] H[m][j]   (contraction over rows)
 // Each block owns a (BNn x BJ) output tile and one contiguous range of rows.
-// Row slices are transposed into LDS ([column][row], 80-byte pitch) so that
-// the fragments (8 consecutive rows of one column) are 16-byte reads.
+// Row slices are transposed into LDS: every operand column is one 64-byte
+// line of SR rows (8 rows per 16-byte fragment), so the fragments are single
+// 16-byte reads.  Line base of column c (bytes): 80 c, plus 64 for columns
+// 16..31 of every 32 (period 2624 bytes).  With lanes running over 16 row
+// pairs x 4 column groups, each transposing write instruction then hits 64
+// distinct banks, and the fragment reads stay conflict-free.
 // ---------------------------------------------------------------------------
+__device__ __forceinline__ int dw_col(int c) {
+  return (c >> 5) * 2624 + (c & 31) * 80 + ((c & 16) ? 64 : 0);
+}
+
 template <class T, int WM, int WN, int NT>
-__global__ void __launch_bounds__(64 * WM * WN)
+__global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2)))
 k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restrict__ H, int64_t h_g,
           int64_t ldh, int64_t R, int64_t n_value, int N, int J, float* __restrict__ partial,
           double* __restrict__ pdb, int n_split, int64_t rows_per_split) {
@@ -212,19 +342,27 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
   constexpr int ES = (int)sizeof(T);
   constexpr int SR = 64 / ES;               // rows per stage
   constexpr int EPP = 16 / ES;              // elements per 16-byte load
-  constexpr int RPP = ES == 2 ? 2 : 1;      // rows per piece (packed LDS writes)
+  constexpr int RPP = ES == 2 ? 2 : 1;      // rows per piece (packed 4-byte LDS writes)
+  constexpr int NRP = SR / RPP;             // row pieces per stage (16)
   constexpr int NCH = 64 / (16 * ES);
-  constexpr int PA = (SR / RPP) * (BNn / EPP);
-  constexpr int PB = (SR / RPP) * (BJ / EPP);
+  constexpr int PA = NRP * (BNn / EPP);
+  constexpr int PB = NRP * (BJ / EPP);
   constexpr int PIECES = PA + PB;
   constexpr int PPT = (PIECES + NTH - 1) / NTH;
+  constexpr int REGA = (BNn / 32) * 2624;   // bytes of the dA part of a stage
+  constexpr int STAGE = REGA + (BJ / 32) * 2624;
   typedef typename Elem<T>::frag frag;
-  __shared__ __attribute__((aligned(16))) char lds[(BNn + BJ) * LDS_PITCH];
+  __shared__ __attribute__((aligned(16))) char lds[2 * STAGE];
 
+  // logical block: output tiles fastest, so the blocks reading one row range
+  // run together on one XCD
   const int tiles_n = (N + BNn - 1) / BNn;
-  const int tn = blockIdx.x % tiles_n;
-  const int tj = blockIdx.x / tiles_n;
-  const int split = blockIdx.y;
+  const int tiles = tiles_n * ((J + BJ - 1) / BJ);
+  const int64_t lb = xcd_remap(blockIdx.x, gridDim.x);
+  const int tile = (int)(lb % tiles);
+  const int tn = tile % tiles_n;
+  const int tj = tile / tiles_n;
+  const int split = (int)(lb / tiles);
   const int g = blockIdx.z;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -236,6 +374,7 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
   const int64_t r0 = (int64_t)split * rows_per_split;
   const int64_t r1 = r0 + rows_per_split < R ? r0 + rows_per_split : R;
   const int64_t rv = r1 < n_value ? r1 : n_value;
+  const int nst = (int)((r1 - r0 + SR - 1) / SR);
 
   const T* A = dA + g * a_g;
   const T* B = H + g * h_g;
@@ -249,65 +388,58 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
   double dbacc = 0.0;
 
-  uint4 buf[PPT][RPP];
-  auto gload = [&](int64_t k0) {
+  // piece q of an operand: row piece q % NRP, column group q / NRP
+  auto gload = [&](uint4 (*buf)[RPP], int64_t k0) {
 #pragma unroll
     for (int i = 0; i < PPT; ++i) {
       const int piece = tid + i * NTH;
       const bool isA = piece < PA;
       const int q = isA ? piece : piece - PA;
-      const int ncg = (isA ? BNn : BJ) / EPP;
-      const int rp = q / ncg, cg = q % ncg;
+      const int rp = q % NRP, cg = q / NRP;
       const int col = (isA ? n0 : j0) + cg * EPP;
       const int lim = isA ? N : J;
 #pragma unroll
       for (int u = 0; u < RPP; ++u) {
         const int64_t row = k0 + rp * RPP + u;
-        if (piece < PIECES && row < r1 && col < lim) {
+        if (piece < PIECES && row < r1 && col < lim)
           buf[i][u] = isA ? *(const uint4*)(A + row * lda + col) : *(const uint4*)(B + row * ldh + col);
-        } else {
+        else
           buf[i][u] = make_uint4(0u, 0u, 0u, 0u);
-        }
       }
     }
   };
-
-  gload(r0);
-  for (int64_t k0 = r0; k0 < r1; k0 += SR) {
-    __syncthreads();
+  auto lstore = [&](const uint4 (*buf)[RPP], int stage) {
 #pragma unroll
     for (int i = 0; i < PPT; ++i) {
       const int piece = tid + i * NTH;
       if (piece >= PIECES) continue;
       const bool isA = piece < PA;
       const int q = isA ? piece : piece - PA;
-      const int ncg = (isA ? BNn : BJ) / EPP;
-      const int rp = q / ncg, cg = q % ncg;
-      char* base = lds + (isA ? 0 : BNn * LDS_PITCH);
+      const int rp = q % NRP, cg = q / NRP;
+      char* base = lds + stage * STAGE + (isA ? 0 : REGA);
       if (ES == 2) {
         const uint16_t* lo = (const uint16_t*)&buf[i][0];
         const uint16_t* hi = (const uint16_t*)&buf[i][RPP - 1];
 #pragma unroll
-        for (int e = 0; e < EPP; ++e) {
-          const uint32_t w = (uint32_t)lo[e] | ((uint32_t)hi[e] << 16);
-          *(uint32_t*)(base + (cg * EPP + e) * LDS_PITCH + rp * 4) = w;
-        }
+        for (int e = 0; e < EPP; ++e)
+          *(uint32_t*)(base + dw_col(cg * EPP + e) + rp * 4) = (uint32_t)lo[e] | ((uint32_t)hi[e] << 16);
       } else {
         const uint32_t* v = (const uint32_t*)&buf[i][0];
 #pragma unroll
-        for (int e = 0; e < EPP; ++e) *(uint32_t*)(base + (cg * EPP + e) * LDS_PITCH + rp * 4) = v[e];
+        for (int e = 0; e < EPP; ++e) *(uint32_t*)(base + dw_col(cg * EPP + e) + rp * 4) = v[e];
       }
     }
-    __syncthreads();
-    if (k0 + SR < r1) gload(k0 + SR);
+  };
+  auto compute = [&](int stage, int64_t k0) {
+    const char* base = lds + stage * STAGE;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       const int koff = c * 32 + (lane >> 5) * (8 * ES);
       frag af[NT], bf[NT];
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        af[t] = *(const frag*)(lds + (32 * (wm * NT + t) + (lane & 31)) * LDS_PITCH + koff);
-        bf[t] = *(const frag*)(lds + (BNn + 32 * (wn * NT + t) + (lane & 31)) * LDS_PITCH + koff);
+        af[t] = *(const frag*)(base + dw_col(32 * (wm * NT + t) + (lane & 31)) + koff);
+        bf[t] = *(const frag*)(base + REGA + dw_col(32 * (wn * NT + t) + (lane & 31)) + koff);
       }
 #pragma unroll
       for (int a = 0; a < NT; ++a)
@@ -317,11 +449,31 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
     // bias cotangent: value rows of this slice, one column per thread
     if (pdb && tj == 0 && tid < BNn && k0 < rv) {
       const int nr = (int)((rv - k0) < SR ? (rv - k0) : SR);
-      const T* colp = (const T*)(lds + tid * LDS_PITCH);
+      const T* colp = (const T*)(base + dw_col(tid));
       float part_sum = 0.0f;
       for (int u = 0; u < nr; ++u) part_sum += Elem<T>::to_f(colp[u]);
       dbacc += (double)part_sum;
     }
+  };
+
+  // two LDS stages, two register buffers, loads issued two stages ahead
+  uint4 b0[PPT][RPP], b1[PPT][RPP];
+  if (nst > 0) {
+    gload(b0, r0);
+    lstore(b0, 0);
+    if (nst > 1) gload(b1, r0 + SR);
+  }
+  __syncthreads();
+  for (int st = 0; st < nst; st += 2) {
+    if (st + 2 < nst) gload(b0, r0 + (int64_t)(st + 2) * SR);
+    compute(0, r0 + (int64_t)st * SR);
+    if (st + 1 < nst) lstore(b1, 1);
+    __syncthreads();
+    if (st + 1 >= nst) break;
+    if (st + 3 < nst) gload(b1, r0 + (int64_t)(st + 3) * SR);
+    compute(1, r0 + (int64_t)(st + 1) * SR);
+    if (st + 2 < nst) lstore(b0, 0);
+    __syncthreads();
   }
 
   const int hh = lane >> 5;
@@ -348,20 +500,23 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
 // ---------------------------------------------------------------------------
 namespace {
 
+// Tile per stream count: a wave owns 32 points x 32*NT columns of every
+// stream; NT = 4 for one stream, 2 for two, 1 beyond (the accumulators stay
+// within the register budget of two waves per SIMD).  Narrow layers (N <= 32) use a
+// 4 x 1 wave block.
 template <class T, int ND1, int ND2, int EPI>
 hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   constexpr int C = 1 + ND1 + ND2;
+  constexpr int NTM = C == 1 ? 4 : (C == 2 ? 2 : 1);
   const int64_t npts = a.seg.n_points;
   if (npts <= 0) return hipSuccess;
   if (a.N <= 32) {
-    dim3 grid((unsigned)((npts + 127) / 128), (unsigned)((a.N + 31) / 32), G);
+    dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 31) / 32)), 1, G);
     k_gemm_nt<T, ND1, ND2, 4, 1, 1, EPI><<<grid, 256, 0, st>>>(a);
-  } else if (a.N <= 64 || C > 5) {
-    dim3 grid((unsigned)((npts + 63) / 64), (unsigned)((a.N + 63) / 64), G);
-    k_gemm_nt<T, ND1, ND2, 2, 2, 1, EPI><<<grid, 256, 0, st>>>(a);
   } else {
-    dim3 grid((unsigned)((npts + 63) / 64), (unsigned)((a.N + 127) / 128), G);
-    k_gemm_nt<T, ND1, ND2, 2, 2, 2, EPI><<<grid, 256, 0, st>>>(a);
+    constexpr int BN = 64 * NTM;
+    dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + BN - 1) / BN)), 1, G);
+    k_gemm_nt<T, ND1, ND2, 2, 2, NTM, EPI><<<grid, 256, 0, st>>>(a);
   }
   return hipGetLastError();
 }
@@ -415,15 +570,15 @@ hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int
                           int n_split, int64_t rows_per_split, int G, hipStream_t st) {
   if (R <= 0) return hipSuccess;
   if (N >= 128 && J >= 128) {
-    dim3 grid((unsigned)(((N + 127) / 128) * ((J + 127) / 128)), n_split, G);
+    dim3 grid((unsigned)(((N + 127) / 128) * ((J + 127) / 128)) * n_split, 1, G);
     k_gemm_dw<T, 2, 2, 2><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
                                                  n_split, rows_per_split);
   } else if (N >= 64 && J >= 64) {
-    dim3 grid((unsigned)(((N + 63) / 64) * ((J + 63) / 64)), n_split, G);
+    dim3 grid((unsigned)(((N + 63) / 64) * ((J + 63) / 64)) * n_split, 1, G);
     k_gemm_dw<T, 2, 2, 1><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
                                                  n_split, rows_per_split);
   } else {
-    dim3 grid((unsigned)(((N + 31) / 32) * ((J + 31) / 32)), n_split, G);
+    dim3 grid((unsigned)(((N + 31) / 32) * ((J + 31) / 32)) * n_split, 1, G);
     k_gemm_dw<T, 1, 1, 1><<<grid, 64, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
                                                 n_split, rows_per_split);
   }
