@@ -68,11 +68,11 @@ __device__ __forceinline__ void load4(const T* p, float* v) {
   }
 }
 
-template <class T, int ND1, int ND2, int WM, int WN, int NT, int EPI>
-__global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(ND1 + ND2 >= 6 ? 1 : 2)))
+template <class T, int ND1, int ND2, int WM, int WN, int MT, int NT, int EPI, int OCC>
+__global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OCC)))
 k_gemm_nt(const NtArgs<T> p) {
   constexpr int C = 1 + ND1 + ND2;
-  constexpr int BM = 32 * WM;
+  constexpr int BM = 32 * MT * WM;
   constexpr int BN = 32 * NT * WN;
   constexpr int NTH = 64 * WM * WN;
   constexpr int ES = (int)sizeof(T);
@@ -129,13 +129,15 @@ k_gemm_nt(const NtArgs<T> p) {
     }
   }
 
-  f32x16 acc[C][NT];
+  f32x16 acc[MT][C][NT];
 #pragma unroll
-  for (int k = 0; k < C; ++k)
+  for (int u = 0; u < MT; ++u)
 #pragma unroll
-    for (int t = 0; t < NT; ++t)
+    for (int k = 0; k < C; ++k)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[k][t][r] = 0.0f;
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[u][k][t][r] = 0.0f;
 
   auto gload = [&](uint4* buf, int kt) {
 #pragma unroll
@@ -160,47 +162,66 @@ k_gemm_nt(const NtArgs<T> p) {
       for (int t = 0; t < NT; ++t)
         bfr[t] = *(const frag*)(base + (C * BM + 32 * (wn * NT + t) + (lane & 31)) * LDS_PITCH + koff);
 #pragma unroll
-      for (int k = 0; k < C; ++k) {
-        const frag afr = *(const frag*)(base + (k * BM + 32 * wm + (lane & 31)) * LDS_PITCH + koff);
+      for (int u = 0; u < MT; ++u)
 #pragma unroll
-        for (int t = 0; t < NT; ++t) Elem<T>::mma(acc[k][t], bfr[t], afr);   // rows: columns n; cols: points
-      }
+        for (int k = 0; k < C; ++k) {
+          const frag afr = *(const frag*)(base + (k * BM + 32 * (MT * wm + u) + (lane & 31)) * LDS_PITCH + koff);
+#pragma unroll
+          for (int t = 0; t < NT; ++t) Elem<T>::mma(acc[u][k][t], bfr[t], afr);   // rows: columns n; cols: points
+        }
     }
   };
 
-  // two LDS stages, two register buffers: the global loads of stage kt+2 are
-  // issued before stage kt is multiplied; one barrier per stage
   const int nk = p.K / KS;
-  uint4 b0[PPT], b1[PPT];
-  gload(b0, 0);
-  lstore(b0, 0);
-  if (nk > 1) gload(b1, 1);
-  __syncthreads();
-  for (int kt = 0; kt < nk; kt += 2) {
-    if (kt + 2 < nk) gload(b0, kt + 2);
-    compute(0);
-    if (kt + 1 < nk) lstore(b1, 1);
+  if constexpr (OCC >= 2) {
+    // two LDS stages, two register buffers: the global loads of stage kt+2
+    // are issued before stage kt is multiplied; one barrier per stage
+    uint4 b0[PPT], b1[PPT];
+    gload(b0, 0);
+    lstore(b0, 0);
+    if (nk > 1) gload(b1, 1);
     __syncthreads();
-    if (kt + 1 >= nk) break;
-    if (kt + 3 < nk) gload(b1, kt + 3);
-    compute(1);
-    if (kt + 2 < nk) lstore(b0, 0);
+    for (int kt = 0; kt < nk; kt += 2) {
+      if (kt + 2 < nk) gload(b0, kt + 2);
+      compute(0);
+      if (kt + 1 < nk) lstore(b1, 1);
+      __syncthreads();
+      if (kt + 1 >= nk) break;
+      if (kt + 3 < nk) gload(b1, kt + 3);
+      compute(1);
+      if (kt + 2 < nk) lstore(b0, 0);
+      __syncthreads();
+    }
+  } else {
+    // large tiles (one wave per SIMD): two LDS stages, one register buffer
+    // loaded one stage ahead
+    uint4 b0[PPT];
+    gload(b0, 0);
+    lstore(b0, 0);
     __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt + 1 < nk) gload(b0, kt + 1);
+      compute(kt & 1);
+      if (kt + 1 < nk) lstore(b0, (kt + 1) & 1);
+      __syncthreads();
+    }
   }
 
-  // ---- epilogue.  The products were formed as W . X^T, so lane (m = lane & 31)
-  // owns one point and, in register group q (regs 4q..4q+3), four consecutive
-  // columns 8q + 4*(lane >> 5) + 0..3 of every 32x32 tile: all jet streams of a
-  // (point, column) sit in the same lane.  Results are staged through LDS one
-  // stream at a time and leave in full 16-byte row segments.
+  // ---- epilogue.  The products were formed as W . X^T, so lane (lane & 31)
+  // owns one point of each of its MT point sub-tiles and, in register group q
+  // (regs 4q..4q+3), four consecutive columns 8q + 4*(lane >> 5) + 0..3 of
+  // every 32x32 tile: all jet streams of a (point, column) sit in the same
+  // lane.  Results are staged through LDS one stream at a time and leave in
+  // full 16-byte row segments.
   const int hh = lane >> 5;
-  const int ml = 32 * wm + (lane & 31);            // point within the block
-  const int64_t pt = m0 + ml;
-  const bool pvalid = pt < npts;
+  auto mloc = [&](int u) { return 32 * (MT * wm + u) + (lane & 31); };            // point within the block
   auto ncol = [&](int t, int q) { return 32 * (wn * NT + t) + 8 * q + 4 * hh; };   // column within the block
 
   if (EPI == EPI_DF) {
-    if (pvalid) {
+#pragma unroll
+    for (int u = 0; u < MT; ++u) {
+      const int64_t pt = m0 + mloc(u);
+      if (pt >= npts) continue;
 #pragma unroll
       for (int t = 0; t < NT; ++t)
 #pragma unroll
@@ -208,7 +229,7 @@ k_gemm_nt(const NtArgs<T> p) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int n = n0 + ncol(t, q) + e;
-            const float v = p.df_sign * acc[0][t][4 * q + e];
+            const float v = p.df_sign * acc[u][0][t][4 * q + e];
             if (n < p.nY) p.seedY[g * p.sY_g + pt * p.nY + n] = v;
             else if (n < p.nY + p.nU) p.seedU[g * p.sU_g + pt * p.nU + (n - p.nY)] = v;
           }
@@ -222,14 +243,17 @@ k_gemm_nt(const NtArgs<T> p) {
   constexpr int CHUNKS = BM * CPR;
   auto stage_out = [&](int k, T* dst) {
 #pragma unroll
-    for (int t = 0; t < NT; ++t)
+    for (int u = 0; u < MT; ++u)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float v[4];
+      for (int t = 0; t < NT; ++t)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = acc[k][t][4 * q + e];
-        store4<T>((T*)(lds + ml * OPITCH + ncol(t, q) * ES), v);
-      }
+        for (int q = 0; q < 4; ++q) {
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = acc[u][k][t][4 * q + e];
+          store4<T>((T*)(lds + mloc(u) * OPITCH + ncol(t, q) * ES), v);
+          __builtin_amdgcn_sched_barrier(0);
+        }
     __syncthreads();
 #pragma unroll
     for (int i = tid; i < CHUNKS; i += NTH) {
@@ -247,30 +271,34 @@ k_gemm_nt(const NtArgs<T> p) {
     // pre-activations (bias on the value stream), then activations in place:
     //   h = t, h'_i = s a'_i, h''_i = s a''_i + s' (a'_i)^2
 #pragma unroll
-    for (int t = 0; t < NT; ++t)
+    for (int u = 0; u < MT; ++u)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int n = n0 + ncol(t, r >> 2) + (r & 3);
-        if (p.bias && n < p.N) acc[0][t][r] += p.bias[g * p.b_g + n];
-      }
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int n = n0 + ncol(t, r >> 2) + (r & 3);
+          if (p.bias && n < p.N) acc[u][0][t][r] += p.bias[g * p.b_g + n];
+        }
     if (p.out_a) {
 #pragma unroll
       for (int k = 0; k < C; ++k) stage_out(k, p.out_a);
     }
 #pragma unroll
-    for (int t = 0; t < NT; ++t)
+    for (int u = 0; u < MT; ++u)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float tt, s;
-        tanh_ts(acc[0][t][r], tt, s);
-        const float sp = -2.0f * tt * s;
+      for (int t = 0; t < NT; ++t)
 #pragma unroll
-        for (int i = 0; i < ND2; ++i)
-          acc[1 + ND1 + i][t][r] = s * acc[1 + ND1 + i][t][r] + sp * acc[1 + i][t][r] * acc[1 + i][t][r];
+        for (int r = 0; r < 16; ++r) {
+          float tt, s;
+          tanh_ts(acc[u][0][t][r], tt, s);
+          const float sp = -2.0f * tt * s;
 #pragma unroll
-        for (int i = 0; i < ND1; ++i) acc[1 + i][t][r] *= s;
-        acc[0][t][r] = tt;
-      }
+          for (int i = 0; i < ND2; ++i)
+            acc[u][1 + ND1 + i][t][r] = s * acc[u][1 + ND1 + i][t][r] + sp * acc[u][1 + i][t][r] * acc[u][1 + i][t][r];
+#pragma unroll
+          for (int i = 0; i < ND1; ++i) acc[u][1 + i][t][r] *= s;
+          acc[u][0][t][r] = tt;
+        }
 #pragma unroll
     for (int k = 0; k < C; ++k) stage_out(k, p.out_h);
     return;
@@ -279,40 +307,46 @@ k_gemm_nt(const NtArgs<T> p) {
   // reverse carry, in place: acc[k] becomes the cotangent of the saved
   // pre-activation a_k of the layer below
 #pragma unroll
-  for (int t = 0; t < NT; ++t)
+  for (int u = 0; u < MT; ++u) {
+    const int64_t pt = m0 + mloc(u);
+    const bool pvalid = pt < npts;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int nb = n0 + ncol(t, q);
-      float ap[C][4];
+    for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int k = 0; k < C; ++k) {
-        if (pvalid && nb < p.N) load4<T>(p.aprev + g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + nb, ap[k]);
-        else ap[k][0] = ap[k][1] = ap[k][2] = ap[k][3] = 0.0f;
-      }
+      for (int q = 0; q < 4; ++q) {
+        const int nb = n0 + ncol(t, q);
+        float ap[C][4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = 4 * q + e;
-        float tt, s;
-        tanh_ts(ap[0][e], tt, s);
-        const float sp = -2.0f * tt * s;
-        const float spp = 2.0f * s * (3.0f * tt * tt - 1.0f);
-        float ga = s * acc[0][t][r];
-#pragma unroll
-        for (int i = 0; i < ND1; ++i) ga += sp * ap[1 + i][e] * acc[1 + i][t][r];
-#pragma unroll
-        for (int i = 0; i < ND2; ++i)
-          ga += (sp * ap[1 + ND1 + i][e] + spp * ap[1 + i][e] * ap[1 + i][e]) * acc[1 + ND1 + i][t][r];
-#pragma unroll
-        for (int i = 0; i < ND1; ++i) {
-          float v = s * acc[1 + i][t][r];
-          if (i < ND2) v += 2.0f * sp * ap[1 + i][e] * acc[1 + ND1 + i][t][r];
-          acc[1 + i][t][r] = v;
+        for (int k = 0; k < C; ++k) {
+          if (pvalid && nb < p.N) load4<T>(p.aprev + g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + nb, ap[k]);
+          else ap[k][0] = ap[k][1] = ap[k][2] = ap[k][3] = 0.0f;
         }
 #pragma unroll
-        for (int i = 0; i < ND2; ++i) acc[1 + ND1 + i][t][r] *= s;
-        acc[0][t][r] = ga;
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * q + e;
+          float tt, s;
+          tanh_ts(ap[0][e], tt, s);
+          const float sp = -2.0f * tt * s;
+          const float spp = 2.0f * s * (3.0f * tt * tt - 1.0f);
+          float ga = s * acc[u][0][t][r];
+#pragma unroll
+          for (int i = 0; i < ND1; ++i) ga += sp * ap[1 + i][e] * acc[u][1 + i][t][r];
+#pragma unroll
+          for (int i = 0; i < ND2; ++i)
+            ga += (sp * ap[1 + ND1 + i][e] + spp * ap[1 + i][e] * ap[1 + i][e]) * acc[u][1 + ND1 + i][t][r];
+#pragma unroll
+          for (int i = 0; i < ND1; ++i) {
+            float v = s * acc[u][1 + i][t][r];
+            if (i < ND2) v += 2.0f * sp * ap[1 + i][e] * acc[u][1 + ND1 + i][t][r];
+            acc[u][1 + i][t][r] = v;
+          }
+#pragma unroll
+          for (int i = 0; i < ND2; ++i) acc[u][1 + ND1 + i][t][r] *= s;
+          acc[u][0][t][r] = ga;
+        }
+        __builtin_amdgcn_sched_barrier(0);
       }
-    }
+  }
 #pragma unroll
   for (int k = 0; k < C; ++k) stage_out(k, p.out_da);
 }
@@ -331,8 +365,8 @@ __device__ __forceinline__ int dw_col(int c) {
   return (c >> 5) * 2624 + (c & 31) * 80 + ((c & 16) ? 64 : 0);
 }
 
-template <class T, int WM, int WN, int NT>
-__global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2)))
+template <class T, int WM, int WN, int NT, int OCC>
+__global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OCC)))
 k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restrict__ H, int64_t h_g,
           int64_t ldh, int64_t R, int64_t n_value, int N, int J, float* __restrict__ partial,
           double* __restrict__ pdb, int n_split, int64_t rows_per_split) {
@@ -456,24 +490,40 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
     }
   };
 
-  // two LDS stages, two register buffers, loads issued two stages ahead
-  uint4 b0[PPT][RPP], b1[PPT][RPP];
-  if (nst > 0) {
-    gload(b0, r0);
-    lstore(b0, 0);
-    if (nst > 1) gload(b1, r0 + SR);
-  }
-  __syncthreads();
-  for (int st = 0; st < nst; st += 2) {
-    if (st + 2 < nst) gload(b0, r0 + (int64_t)(st + 2) * SR);
-    compute(0, r0 + (int64_t)st * SR);
-    if (st + 1 < nst) lstore(b1, 1);
+  if constexpr (OCC >= 2) {
+    // two LDS stages, two register buffers, loads issued two stages ahead
+    uint4 b0[PPT][RPP], b1[PPT][RPP];
+    if (nst > 0) {
+      gload(b0, r0);
+      lstore(b0, 0);
+      if (nst > 1) gload(b1, r0 + SR);
+    }
     __syncthreads();
-    if (st + 1 >= nst) break;
-    if (st + 3 < nst) gload(b1, r0 + (int64_t)(st + 3) * SR);
-    compute(1, r0 + (int64_t)(st + 1) * SR);
-    if (st + 2 < nst) lstore(b0, 0);
+    for (int st = 0; st < nst; st += 2) {
+      if (st + 2 < nst) gload(b0, r0 + (int64_t)(st + 2) * SR);
+      compute(0, r0 + (int64_t)st * SR);
+      if (st + 1 < nst) lstore(b1, 1);
+      __syncthreads();
+      if (st + 1 >= nst) break;
+      if (st + 3 < nst) gload(b1, r0 + (int64_t)(st + 3) * SR);
+      compute(1, r0 + (int64_t)(st + 1) * SR);
+      if (st + 2 < nst) lstore(b0, 0);
+      __syncthreads();
+    }
+  } else {
+    // large tiles (one wave per SIMD): one register buffer, one stage ahead
+    uint4 b0[PPT][RPP];
+    if (nst > 0) {
+      gload(b0, r0);
+      lstore(b0, 0);
+    }
     __syncthreads();
+    for (int st = 0; st < nst; ++st) {
+      if (st + 1 < nst) gload(b0, r0 + (int64_t)(st + 1) * SR);
+      compute(st & 1, r0 + (int64_t)st * SR);
+      if (st + 1 < nst) lstore(b0, (st + 1) & 1);
+      __syncthreads();
+    }
   }
 
   const int hh = lane >> 5;
@@ -500,10 +550,11 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
 // ---------------------------------------------------------------------------
 namespace {
 
-// Tile per stream count: a wave owns 32 points x 32*NT columns of every
-// stream; NT = 4 for one stream, 2 for two, 1 beyond (the accumulators stay
-// within the register budget of two waves per SIMD).  Narrow layers (N <= 32) use a
-// 4 x 1 wave block.
+// Tiles.  A wave owns 32 points x 32*NT columns of every stream: NT = 4 / 2 /
+// 1 for 1 / 2 / 3+ streams (2 x 2 waves, two waves per SIMD); narrow layers
+// (N <= 32) use 4 x 1 waves.  (Larger block tiles at one wave per SIMD, and
+// 2 x 4 wave blocks, measured slower: the loop is latency-bound, so occupancy
+// matters more than per-block intensity.)
 template <class T, int ND1, int ND2, int EPI>
 hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   constexpr int C = 1 + ND1 + ND2;
@@ -512,11 +563,11 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   if (npts <= 0) return hipSuccess;
   if (a.N <= 32) {
     dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 31) / 32)), 1, G);
-    k_gemm_nt<T, ND1, ND2, 4, 1, 1, EPI><<<grid, 256, 0, st>>>(a);
+    k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, 2><<<grid, 256, 0, st>>>(a);
   } else {
     constexpr int BN = 64 * NTM;
     dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + BN - 1) / BN)), 1, G);
-    k_gemm_nt<T, ND1, ND2, 2, 2, NTM, EPI><<<grid, 256, 0, st>>>(a);
+    k_gemm_nt<T, ND1, ND2, 2, 2, 1, NTM, EPI, (C >= 7 ? 1 : 2)><<<grid, 256, 0, st>>>(a);
   }
   return hipGetLastError();
 }
@@ -571,15 +622,15 @@ hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int
   if (R <= 0) return hipSuccess;
   if (N >= 128 && J >= 128) {
     dim3 grid((unsigned)(((N + 127) / 128) * ((J + 127) / 128)) * n_split, 1, G);
-    k_gemm_dw<T, 2, 2, 2><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
-                                                 n_split, rows_per_split);
+    k_gemm_dw<T, 2, 2, 2, 2><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
+                                                    n_split, rows_per_split);
   } else if (N >= 64 && J >= 64) {
     dim3 grid((unsigned)(((N + 63) / 64) * ((J + 63) / 64)) * n_split, 1, G);
-    k_gemm_dw<T, 2, 2, 1><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
+    k_gemm_dw<T, 2, 2, 1, 2><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
                                                  n_split, rows_per_split);
   } else {
     dim3 grid((unsigned)(((N + 31) / 32) * ((J + 31) / 32)) * n_split, 1, G);
-    k_gemm_dw<T, 1, 1, 1><<<grid, 64, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
+    k_gemm_dw<T, 1, 1, 1, 2><<<grid, 64, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
                                                 n_split, rows_per_split);
   }
   return hipGetLastError();
