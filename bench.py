@@ -53,6 +53,36 @@ def device_inputs(wl, dev):
     return d, inp
 
 
+KERNEL_SOURCES = ("common.h", "gemm.hip", "pointwise.hip")
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_1910_13444_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(key, wl):
+    """HBM bytes per launch of the launch shape `key` on this workload, from a
+    committed counter summary (profiles/*.traffic.json: FETCH_SIZE and
+    WRITE_SIZE per dispatch, scaled by a known-size copy).  None when no
+    summary covers it or the kernel sources changed since it was taken."""
+    import glob
+    src = kernel_source_hash()
+    for f in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.traffic.json"))):
+        with open(f) as fh:
+            rec = json.load(fh)
+        if rec.get("workload") != wl.name or rec.get("kernel_sources_sha256") != src:
+            continue
+        v = rec.get("hbm_bytes_per_launch", {}).get(key)
+        if v is not None:
+            return float(v)
+    return None
+
+
 def run_steps(step, d, wl, k):
     for _ in range(k):
         step(d["pY"], d["pU"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["real"], f=None,
@@ -102,6 +132,9 @@ def main():
     ap.add_argument("--chunk-S", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
+    ap.add_argument("--copy-calib", type=int, default=0, metavar="BYTES",
+                    help="first run one plain device-to-device copy of BYTES bytes (a known-size reference "
+                         "dispatch for scaling HBM byte counters)")
     a = ap.parse_args()
 
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -117,6 +150,14 @@ def main():
     dev = torch.device("cuda:0")
     pigan.lib()
     log(f"bench: workload {wl.name} dtype {wl.dtype} S={wl.S} P={wl.P} W={wl.W} L={wl.L}")
+    if a.copy_calib > 0:
+        src = torch.ones(a.copy_calib, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"bench: calibration copy of {a.copy_calib} bytes done")
+        del src, dst
     d, inp = device_inputs(wl, dev)
     step = pigan.TrainStep(pigan.step_desc(wl, chunk_S=a.chunk_S), device=dev)
     log(f"bench: workspace {step.ws_bytes / 2**30:.2f} GiB; warmup {a.warmup}")
@@ -158,17 +199,18 @@ def main():
         fl = dom["flops"] / dom["launches"]
         by = dom["bytes"] / dom["launches"]
         ridge = PEAK_TFLOPS[wl.dtype] * 1e12 / (PEAK_GBS * 1e9)
+        traffic = recorded_traffic(dom["name"], wl)
         if by > 0 and fl / by < ridge:
             ach = by / (avg_ms * 1e-3) / 1e9
             roof = {"kernel": dom["name"], "bound": "hbm", "achieved": ach, "peak": PEAK_GBS, "unit": "GB/s",
-                    "frac": ach / PEAK_GBS, "traffic": None, "avg_launch_ms": avg_ms,
+                    "frac": ach / PEAK_GBS, "traffic": traffic, "traffic_unit": "HBM bytes per launch", "avg_launch_ms": avg_ms,
                     "launches_per_step": dom["launches"] / a.steps, "alg_bytes_per_launch": by,
                     "alg_flops_per_launch": fl}
         else:
             ach = fl / (avg_ms * 1e-3) / 1e12
             pk = PEAK_TFLOPS[wl.dtype]
             roof = {"kernel": dom["name"], "bound": "mfma", "achieved": ach, "peak": pk, "unit": "TFLOP/s",
-                    "frac": ach / pk, "traffic": None, "avg_launch_ms": avg_ms,
+                    "frac": ach / pk, "traffic": traffic, "traffic_unit": "HBM bytes per launch", "avg_launch_ms": avg_ms,
                     "launches_per_step": dom["launches"] / a.steps, "alg_bytes_per_launch": by,
                     "alg_flops_per_launch": fl}
         for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):

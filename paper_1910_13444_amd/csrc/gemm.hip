@@ -68,6 +68,16 @@ __device__ __forceinline__ void load4(const T* p, float* v) {
   }
 }
 
+// Barrier for data exchanged through LDS only.  __syncthreads() also fences
+// global memory, which makes every wave wait for all of its outstanding global
+// loads (s_waitcnt vmcnt(0)) and so defeats loads prefetched stages ahead;
+// here only the LDS writes must be complete before the barrier.
+__device__ __forceinline__ void lds_sync() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 template <class T, int ND1, int ND2, int WM, int WN, int MT, int NT, int EPI, int OCC>
 __global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OCC)))
 k_gemm_nt(const NtArgs<T> p) {
@@ -176,21 +186,26 @@ k_gemm_nt(const NtArgs<T> p) {
   if constexpr (OCC >= 2) {
     // two LDS stages, two register buffers: the global loads of stage kt+2
     // are issued before stage kt is multiplied; one barrier per stage
+    // prefetches are unconditional (the stage index is clamped; loads past
+    // the last stage are never stored): conditional loads would force
+    // register copies that wait for the data
     uint4 b0[PPT], b1[PPT];
     gload(b0, 0);
     lstore(b0, 0);
-    if (nk > 1) gload(b1, 1);
-    __syncthreads();
+    gload(b1, nk > 1 ? 1 : 0);
+    lds_sync();
     for (int kt = 0; kt < nk; kt += 2) {
-      if (kt + 2 < nk) gload(b0, kt + 2);
+      gload(b0, kt + 2 < nk ? kt + 2 : nk - 1);
       compute(0);
+      __builtin_amdgcn_sched_barrier(0);
       if (kt + 1 < nk) lstore(b1, 1);
-      __syncthreads();
+      lds_sync();
       if (kt + 1 >= nk) break;
-      if (kt + 3 < nk) gload(b1, kt + 3);
+      gload(b1, kt + 3 < nk ? kt + 3 : nk - 1);
       compute(1);
+      __builtin_amdgcn_sched_barrier(0);
       if (kt + 2 < nk) lstore(b0, 0);
-      __syncthreads();
+      lds_sync();
     }
   } else {
     // large tiles (one wave per SIMD): two LDS stages, one register buffer
@@ -198,12 +213,13 @@ k_gemm_nt(const NtArgs<T> p) {
     uint4 b0[PPT];
     gload(b0, 0);
     lstore(b0, 0);
-    __syncthreads();
+    lds_sync();
     for (int kt = 0; kt < nk; ++kt) {
-      if (kt + 1 < nk) gload(b0, kt + 1);
+      gload(b0, kt + 1 < nk ? kt + 1 : nk - 1);
       compute(kt & 1);
+      __builtin_amdgcn_sched_barrier(0);
       if (kt + 1 < nk) lstore(b0, (kt + 1) & 1);
-      __syncthreads();
+      lds_sync();
     }
   }
 
@@ -254,7 +270,7 @@ k_gemm_nt(const NtArgs<T> p) {
           store4<T>((T*)(lds + mloc(u) * OPITCH + ncol(t, q) * ES), v);
           __builtin_amdgcn_sched_barrier(0);
         }
-    __syncthreads();
+    lds_sync();
 #pragma unroll
     for (int i = tid; i < CHUNKS; i += NTH) {
       const int row = i / CPR, ch = i % CPR;
@@ -264,7 +280,7 @@ k_gemm_nt(const NtArgs<T> p) {
         *(uint4*)(dst + g * p.o_g + (p.seg.row0 + k * p.seg.plane + ptr) * p.ldo + n) =
             *(const uint4*)(lds + row * OPITCH + ch * 16);
     }
-    __syncthreads();
+    lds_sync();
   };
 
   if (EPI == EPI_FWD) {
@@ -432,17 +448,19 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
       const int rp = q % NRP, cg = q / NRP;
       const int col = (isA ? n0 : j0) + cg * EPP;
       const int lim = isA ? N : J;
+      // rows past the split range load a clamped row (zeroed when stored to
+      // LDS); columns past the end only reach outputs that are never stored
+      const int colc = col < lim ? col : lim - EPP;
 #pragma unroll
       for (int u = 0; u < RPP; ++u) {
         const int64_t row = k0 + rp * RPP + u;
-        if (piece < PIECES && row < r1 && col < lim)
-          buf[i][u] = isA ? *(const uint4*)(A + row * lda + col) : *(const uint4*)(B + row * ldh + col);
-        else
-          buf[i][u] = make_uint4(0u, 0u, 0u, 0u);
+        const int64_t rowc = row < r1 ? row : r1 - 1;
+        buf[i][u] = isA ? *(const uint4*)(A + rowc * lda + colc) : *(const uint4*)(B + rowc * ldh + colc);
       }
     }
+    __builtin_amdgcn_sched_barrier(0);   // keep the prefetch where it is issued
   };
-  auto lstore = [&](const uint4 (*buf)[RPP], int stage) {
+  auto lstore = [&](const uint4 (*buf)[RPP], int stage, int64_t k0) {
 #pragma unroll
     for (int i = 0; i < PPT; ++i) {
       const int piece = tid + i * NTH;
@@ -451,16 +469,19 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
       const int q = isA ? piece : piece - PA;
       const int rp = q % NRP, cg = q / NRP;
       char* base = lds + stage * STAGE + (isA ? 0 : REGA);
+      const uint32_t m0k = (k0 + rp * RPP < r1) ? 0xffffffffu : 0u;            // row validity masks
+      const uint32_t m1k = (k0 + rp * RPP + RPP - 1 < r1) ? 0xffffffffu : 0u;
       if (ES == 2) {
         const uint16_t* lo = (const uint16_t*)&buf[i][0];
         const uint16_t* hi = (const uint16_t*)&buf[i][RPP - 1];
 #pragma unroll
         for (int e = 0; e < EPP; ++e)
-          *(uint32_t*)(base + dw_col(cg * EPP + e) + rp * 4) = (uint32_t)lo[e] | ((uint32_t)hi[e] << 16);
+          *(uint32_t*)(base + dw_col(cg * EPP + e) + rp * 4) =
+              ((uint32_t)lo[e] & m0k & 0xffffu) | (((uint32_t)hi[e] << 16) & m1k);
       } else {
         const uint32_t* v = (const uint32_t*)&buf[i][0];
 #pragma unroll
-        for (int e = 0; e < EPP; ++e) *(uint32_t*)(base + dw_col(cg * EPP + e) + rp * 4) = v[e];
+        for (int e = 0; e < EPP; ++e) *(uint32_t*)(base + dw_col(cg * EPP + e) + rp * 4) = v[e] & m0k;
       }
     }
   };
@@ -493,36 +514,40 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
   if constexpr (OCC >= 2) {
     // two LDS stages, two register buffers, loads issued two stages ahead
     uint4 b0[PPT][RPP], b1[PPT][RPP];
+    const int last = nst > 0 ? nst - 1 : 0;
     if (nst > 0) {
       gload(b0, r0);
-      lstore(b0, 0);
-      if (nst > 1) gload(b1, r0 + SR);
+      lstore(b0, 0, r0);
     }
-    __syncthreads();
+    gload(b1, r0 + (int64_t)(nst > 1 ? 1 : 0) * SR);
+    lds_sync();
     for (int st = 0; st < nst; st += 2) {
-      if (st + 2 < nst) gload(b0, r0 + (int64_t)(st + 2) * SR);
+      gload(b0, r0 + (int64_t)(st + 2 < nst ? st + 2 : last) * SR);
       compute(0, r0 + (int64_t)st * SR);
-      if (st + 1 < nst) lstore(b1, 1);
-      __syncthreads();
+      __builtin_amdgcn_sched_barrier(0);
+      if (st + 1 < nst) lstore(b1, 1, r0 + (int64_t)(st + 1) * SR);
+      lds_sync();
       if (st + 1 >= nst) break;
-      if (st + 3 < nst) gload(b1, r0 + (int64_t)(st + 3) * SR);
+      gload(b1, r0 + (int64_t)(st + 3 < nst ? st + 3 : last) * SR);
       compute(1, r0 + (int64_t)(st + 1) * SR);
-      if (st + 2 < nst) lstore(b0, 0);
-      __syncthreads();
+      __builtin_amdgcn_sched_barrier(0);
+      if (st + 2 < nst) lstore(b0, 0, r0 + (int64_t)(st + 2) * SR);
+      lds_sync();
     }
   } else {
     // large tiles (one wave per SIMD): one register buffer, one stage ahead
     uint4 b0[PPT][RPP];
     if (nst > 0) {
       gload(b0, r0);
-      lstore(b0, 0);
+      lstore(b0, 0, r0);
     }
-    __syncthreads();
+    lds_sync();
     for (int st = 0; st < nst; ++st) {
-      if (st + 1 < nst) gload(b0, r0 + (int64_t)(st + 1) * SR);
+      gload(b0, r0 + (int64_t)(st + 1 < nst ? st + 1 : st) * SR);
       compute(st & 1, r0 + (int64_t)st * SR);
-      if (st + 1 < nst) lstore(b0, (st + 1) & 1);
-      __syncthreads();
+      __builtin_amdgcn_sched_barrier(0);
+      if (st + 1 < nst) lstore(b0, (st + 1) & 1, r0 + (int64_t)(st + 1) * SR);
+      lds_sync();
     }
   }
 
@@ -563,7 +588,7 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   if (npts <= 0) return hipSuccess;
   if (a.N <= 32) {
     dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 31) / 32)), 1, G);
-    k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, 2><<<grid, 256, 0, st>>>(a);
+    k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, (C >= 4 ? 1 : 2)><<<grid, 256, 0, st>>>(a);
   } else {
     constexpr int BN = 64 * NTM;
     dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + BN - 1) / BN)), 1, G);

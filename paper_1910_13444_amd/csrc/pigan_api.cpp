@@ -341,7 +341,10 @@ static pigan_status gemm_nt(int epi, int nd1, int nd2, const NtArgs<T>& a, int G
   if (epi == EPI_FWD) bytes += M * a.N * es * G * (a.out_a ? 2 : 1);
   else if (epi == EPI_BWD) bytes += 2.0 * M * a.N * es * G;
   else bytes += M * a.N * 4.0 * G;
-  ProfScope ps(st, name, flops, bytes);
+  // timing records are keyed by launch shape: one name = one kernel instantiation and size
+  char key[64];
+  snprintf(key, sizeof key, "%s_c%d_k%d_n%d", name, C, a.K, a.N);
+  ProfScope ps(st, key, flops, bytes);
   HIP_TRY(launch_gemm_nt<T>(epi, nd1, nd2, a, G, st));
   return PIGAN_OK;
 }
@@ -355,7 +358,9 @@ static pigan_status weight_grad(const T* dA, int64_t a_g, int64_t lda, const T* 
   int64_t rps;
   dw_split_plan(R, N, Jp, (int)sizeof(T), G, &ns, &rps);
   {
-    ProfScope ps(st, "gemm_dw", 2.0 * R * N * Jp * G, ((double)R * (N + Jp) * sizeof(T) + 4.0 * ns * N * Jp) * G);
+    char key[64];
+    snprintf(key, sizeof key, "gemm_dw_n%d_j%d", N, Jp);
+    ProfScope ps(st, key, 2.0 * R * N * Jp * G, ((double)R * (N + Jp) * sizeof(T) + 4.0 * ns * N * Jp) * G);
     HIP_TRY(launch_gemm_dw<T>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, Jp, part, pdb, ns, rps, G, st));
   }
   {
