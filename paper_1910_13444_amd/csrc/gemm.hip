@@ -78,6 +78,45 @@ __device__ __forceinline__ void lds_sync() {
   asm volatile("" ::: "memory");
 }
 
+// Jet carries through tanh of one (point, column); index k runs over the
+// streams: value, d/dx_1..d/dx_ND1, d^2/dx_1^2..d^2/dx_ND2^2.
+// Forward: pre-activations in, activations out.
+template <int ND1, int ND2>
+__device__ __forceinline__ void jet_fwd(float* v) {
+  float tt, s;
+  tanh_ts(v[0], tt, s);
+  const float sp = -2.0f * tt * s;
+#pragma unroll
+  for (int i = 0; i < ND2; ++i) v[1 + ND1 + i] = s * v[1 + ND1 + i] + sp * v[1 + i] * v[1 + i];
+#pragma unroll
+  for (int i = 0; i < ND1; ++i) v[1 + i] *= s;
+  v[0] = tt;
+}
+
+// Reverse: activation cotangents in, pre-activation cotangents out, given the
+// saved pre-activations ap.
+template <int ND1, int ND2>
+__device__ __forceinline__ void jet_bwd(float* g, const float* ap) {
+  float tt, s;
+  tanh_ts(ap[0], tt, s);
+  const float sp = -2.0f * tt * s;
+  const float spp = 2.0f * s * (3.0f * tt * tt - 1.0f);
+  float ga = s * g[0];
+#pragma unroll
+  for (int i = 0; i < ND1; ++i) ga += sp * ap[1 + i] * g[1 + i];
+#pragma unroll
+  for (int i = 0; i < ND2; ++i) ga += (sp * ap[1 + ND1 + i] + spp * ap[1 + i] * ap[1 + i]) * g[1 + ND1 + i];
+#pragma unroll
+  for (int i = 0; i < ND1; ++i) {
+    float v = s * g[1 + i];
+    if (i < ND2) v += 2.0f * sp * ap[1 + i] * g[1 + ND1 + i];
+    g[1 + i] = v;
+  }
+#pragma unroll
+  for (int i = 0; i < ND2; ++i) g[1 + ND1 + i] *= s;
+  g[0] = ga;
+}
+
 template <class T, int ND1, int ND2, int WM, int WN, int MT, int NT, int EPI, int OCC>
 __global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OCC)))
 k_gemm_nt(const NtArgs<T> p) {
@@ -305,15 +344,12 @@ k_gemm_nt(const NtArgs<T> p) {
       for (int t = 0; t < NT; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float tt, s;
-          tanh_ts(acc[u][0][t][r], tt, s);
-          const float sp = -2.0f * tt * s;
+          float v[C];
 #pragma unroll
-          for (int i = 0; i < ND2; ++i)
-            acc[u][1 + ND1 + i][t][r] = s * acc[u][1 + ND1 + i][t][r] + sp * acc[u][1 + i][t][r] * acc[u][1 + i][t][r];
+          for (int k = 0; k < C; ++k) v[k] = acc[u][k][t][r];
+          jet_fwd<ND1, ND2>(v);
 #pragma unroll
-          for (int i = 0; i < ND1; ++i) acc[u][1 + i][t][r] *= s;
-          acc[u][0][t][r] = tt;
+          for (int k = 0; k < C; ++k) acc[u][k][t][r] = v[k];
         }
 #pragma unroll
     for (int k = 0; k < C; ++k) stage_out(k, p.out_h);
@@ -340,31 +376,227 @@ k_gemm_nt(const NtArgs<T> p) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * q + e;
-          float tt, s;
-          tanh_ts(ap[0][e], tt, s);
-          const float sp = -2.0f * tt * s;
-          const float spp = 2.0f * s * (3.0f * tt * tt - 1.0f);
-          float ga = s * acc[u][0][t][r];
+          float gv[C], av[C];
 #pragma unroll
-          for (int i = 0; i < ND1; ++i) ga += sp * ap[1 + i][e] * acc[u][1 + i][t][r];
-#pragma unroll
-          for (int i = 0; i < ND2; ++i)
-            ga += (sp * ap[1 + ND1 + i][e] + spp * ap[1 + i][e] * ap[1 + i][e]) * acc[u][1 + ND1 + i][t][r];
-#pragma unroll
-          for (int i = 0; i < ND1; ++i) {
-            float v = s * acc[u][1 + i][t][r];
-            if (i < ND2) v += 2.0f * sp * ap[1 + i][e] * acc[u][1 + ND1 + i][t][r];
-            acc[u][1 + i][t][r] = v;
+          for (int k = 0; k < C; ++k) {
+            gv[k] = acc[u][k][t][r];
+            av[k] = ap[k][e];
           }
+          jet_bwd<ND1, ND2>(gv, av);
 #pragma unroll
-          for (int i = 0; i < ND2; ++i) acc[u][1 + ND1 + i][t][r] *= s;
-          acc[u][0][t][r] = ga;
+          for (int k = 0; k < C; ++k) acc[u][k][t][r] = gv[k];
         }
         __builtin_amdgcn_sched_barrier(0);
       }
   }
 #pragma unroll
   for (int k = 0; k < C; ++k) stage_out(k, p.out_da);
+}
+
+// ---------------------------------------------------------------------------
+// k_gemm_nt_wr: the products and epilogues of k_gemm_nt for 16-bit storage
+// and K = N = 128 (hidden layers of width 128), as a persistent kernel
+// built to keep HBM busy.  Each block copies the weight matrix into LDS once
+// and then walks tiles of 32 points (all jet streams, the whole K extent at
+// once).  While one tile is multiplied and written out, the activations of
+// its successor (and, in the reverse pass, the saved pre-activations of the
+// tile itself) are already on their way into registers, so every block keeps
+// a whole tile of loads in flight.  Four waves; wave w owns columns
+// 32w..32w+31 of every stream.
+// ---------------------------------------------------------------------------
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+template <class T, int ND1, int ND2, int EPI>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
+  static_assert(sizeof(T) == 2, "16-bit storage only");
+  constexpr int C = 1 + ND1 + ND2;
+  constexpr int BM = 32, BN = 128, NTH = 256, ES = 2;
+  constexpr int RB = 256;                          // bytes of one operand row (K = 128)
+  constexpr int PITCH = RB + 16;                   // LDS row pitch: conflict-free 16-byte fragment reads
+  constexpr int WREG = BN * PITCH;                 // weight tile
+  constexpr int XREG = C * BM * PITCH;             // activation tile, reused to stage the outputs
+  constexpr int OPITCH = BN * ES + 16;             // staging pitch of one output plane
+  static_assert(BM * OPITCH <= XREG, "staging must fit in the activation region");
+  constexpr int SEGS = RB / 16;                    // 16-byte pieces per row
+  constexpr int XP = C * BM * SEGS / NTH;          // pieces per thread of an activation tile
+  constexpr int WP = BN * SEGS / NTH;              // pieces per thread of the weights
+  constexpr int RPP = NTH / SEGS;                  // rows covered by one piece index
+  typedef typename Elem<T>::frag frag;
+  __shared__ __attribute__((aligned(16))) char lds[WREG + XREG];
+  char* const wl = lds;
+  char* const xl = lds + WREG;
+
+  const int g = blockIdx.z;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int hh = lane >> 5;
+  const int sg = tid % SEGS;
+  const int64_t npts = p.seg.n_points;
+  const char* Xb = (const char*)(p.X + g * p.x_g);
+  const char* Wb = (const char*)(p.Wm + g * p.w_g);
+
+  // weights (N = 128 rows)
+  {
+    u32x4 wb[WP];
+#pragma unroll
+    for (int i = 0; i < WP; ++i) wb[i] = *(const u32x4*)(Wb + (int64_t)(tid / SEGS + RPP * i) * p.ldw * ES + sg * 16);
+#pragma unroll
+    for (int i = 0; i < WP; ++i) *(u32x4*)(wl + (tid / SEGS + RPP * i) * PITCH + sg * 16) = wb[i];
+  }
+
+  // activation rows of a tile; points past the end repeat the last point.
+  // Stream bases are uniform (scalar); a thread's two point rows are 32-bit
+  // byte offsets (the host checks that a stream plane spans < 2^31 bytes).
+  static_assert(BM == 2 * RPP, "two point rows per thread");
+  u32x4 xb[XP];
+  auto xload = [&](int64_t tile) {
+    int64_t p0 = tile * BM + tid / SEGS, p1 = p0 + RPP;
+    if (p0 >= npts) p0 = npts - 1;
+    if (p1 >= npts) p1 = npts - 1;
+    const uint32_t o0 = (uint32_t)(p0 * p.ldx * ES) + sg * 16, o1 = (uint32_t)(p1 * p.ldx * ES) + sg * 16;
+#pragma unroll
+    for (int i = 0; i < XP; ++i) {
+      const char* base = Xb + (p.seg.row0 + (i >> 1) * p.seg.plane) * p.ldx * ES;
+      xb[i] = *(const u32x4*)(base + ((i & 1) ? o1 : o0));
+    }
+  };
+  auto ncol = [&](int q) { return 32 * wave + 8 * q + 4 * hh; };   // first of the lane's 4 columns in group q
+
+  // bias of the lane's 16 columns (fixed for the whole launch)
+  float bias[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) bias[r] = 0.0f;
+  if (EPI == EPI_FWD && p.bias) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) bias[r] = p.bias[g * p.b_g + ncol(r >> 2) + (r & 3)];
+  }
+
+  auto xstore = [&]() {
+#pragma unroll
+    for (int i = 0; i < XP; ++i) *(u32x4*)(xl + (tid / SEGS + RPP * i) * PITCH + sg * 16) = xb[i];
+  };
+
+  // The activations of a tile go from registers to LDS at the end of the
+  // previous iteration, after its stores were issued: the wait for the
+  // prefetch then leaves those stores in flight (the memory counter drains
+  // in issue order, and the same operations are pending on every iteration).
+  int64_t tile = blockIdx.x;
+  xload(tile);
+  xstore();
+  for (; tile < ntiles; tile += gridDim.x) {
+    const int64_t m0 = tile * BM;
+    lds_sync();
+
+    // reverse pass: the saved pre-activations of this tile, in the lane
+    // layout of the products (point lane & 31, four columns per group).
+    // Issued before the prefetch so that waiting for them (the memory
+    // counter drains in issue order) does not wait for the prefetch.
+    u32x2 apr[C][4];
+    if (EPI == EPI_BWD) {
+      int64_t pt = m0 + (lane & 31);
+      if (pt >= npts) pt = npts - 1;
+      const uint32_t po = (uint32_t)(pt * p.ldo * ES);
+#pragma unroll
+      for (int k = 0; k < C; ++k) {
+        const char* base = (const char*)(p.aprev + g * p.o_g + (p.seg.row0 + k * p.seg.plane) * p.ldo);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          apr[k][q] = *(const u32x2*)(base + po + ncol(q) * ES);
+        }
+      }
+    }
+    {
+      const int64_t nx = tile + gridDim.x;
+      xload(nx < ntiles ? nx : tile);              // unconditional: the last prefetch is never used
+    }
+    __builtin_amdgcn_sched_barrier(0);             // keep the loads ahead of the products
+
+    f32x16 acc[C];
+#pragma unroll
+    for (int k = 0; k < C; ++k)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[k][r] = 0.0f;
+#pragma unroll
+    for (int c = 0; c < RB / 32; ++c) {
+      const int koff = c * 32 + hh * 16;
+      const frag bfr = *(const frag*)(wl + (32 * wave + (lane & 31)) * PITCH + koff);
+#pragma unroll
+      for (int k = 0; k < C; ++k) {
+        const frag afr = *(const frag*)(xl + (k * BM + (lane & 31)) * PITCH + koff);
+        Elem<T>::mma(acc[k], bfr, afr);            // rows: columns n; cols: points
+      }
+    }
+    lds_sync();                                    // the activation region is free for staging
+
+    auto stage_out = [&](int k, T* dst) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = acc[k][4 * q + e];
+        store4<T>((T*)(xl + (lane & 31) * OPITCH + ncol(q) * ES), v);
+      }
+      lds_sync();
+#pragma unroll
+      // rows of points past the end hold exactly the values of the last
+      // point (same inputs, same arithmetic): they are written over it
+      // unconditionally, which keeps the memory counter static for the
+      // prefetch waits
+      for (int j = 0; j < BM * (BN * ES / 16) / NTH; ++j) {
+        const int i = tid + j * NTH;
+        const int row = i / (BN * ES / 16), ch = i % (BN * ES / 16);
+        int64_t pt = m0 + row;
+        if (pt >= npts) pt = npts - 1;
+        *(u32x4*)(dst + g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + ch * (16 / ES)) =
+            *(const u32x4*)(xl + row * OPITCH + ch * 16);
+      }
+      lds_sync();
+    };
+
+    if (EPI == EPI_FWD) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[0][r] += bias[r];
+      if (p.out_a) {
+#pragma unroll
+        for (int k = 0; k < C; ++k) stage_out(k, p.out_a);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float v[C];
+#pragma unroll
+        for (int k = 0; k < C; ++k) v[k] = acc[k][r];
+        jet_fwd<ND1, ND2>(v);
+#pragma unroll
+        for (int k = 0; k < C; ++k) acc[k][r] = v[k];
+      }
+#pragma unroll
+      for (int k = 0; k < C; ++k) stage_out(k, p.out_h);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * q + e;
+          float gv[C], av[C];
+#pragma unroll
+          for (int k = 0; k < C; ++k) {
+            gv[k] = acc[k][r];
+            const uint32_t w = apr[k][q][e >> 1];
+            const uint16_t h = (e & 1) ? (uint16_t)(w >> 16) : (uint16_t)(w & 0xffffu);
+            av[k] = Elem<T>::to_f(__builtin_bit_cast(T, h));
+          }
+          jet_bwd<ND1, ND2>(gv, av);
+#pragma unroll
+          for (int k = 0; k < C; ++k) acc[k][r] = gv[k];
+        }
+#pragma unroll
+      for (int k = 0; k < C; ++k) stage_out(k, p.out_da);
+    }
+    xstore();                                      // the next tile (the region is free again)
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -580,12 +812,38 @@ namespace {
 // (N <= 32) use 4 x 1 waves.  (Larger block tiles at one wave per SIMD, and
 // 2 x 4 wave blocks, measured slower: the loop is latency-bound, so occupancy
 // matters more than per-block intensity.)
+// compute units of the current device (cached per device)
+int cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (cached[dev] <= 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
 template <class T, int ND1, int ND2, int EPI>
 hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   constexpr int C = 1 + ND1 + ND2;
   constexpr int NTM = C == 1 ? 4 : (C == 2 ? 2 : 1);
   const int64_t npts = a.seg.n_points;
   if (npts <= 0) return hipSuccess;
+  if constexpr (sizeof(T) == 2 && C >= 2 && C <= 5 && EPI != EPI_DF) {
+    const int64_t span = (npts + 1) * (a.ldx > a.ldo ? a.ldx : a.ldo) * (int64_t)sizeof(T);
+    if (a.K == 128 && a.N == 128 && span < ((int64_t)1 << 31)) {
+      // persistent weight-resident kernel: two blocks per CU in total
+      const int64_t ntiles = (npts + 31) / 32;
+      int64_t nb = 2 * (int64_t)cu_count() / G;
+      if (nb < 1) nb = 1;
+      if (nb > ntiles) nb = ntiles;
+      dim3 grid((unsigned)nb, 1, G);
+      k_gemm_nt_wr<T, ND1, ND2, EPI><<<grid, 256, 0, st>>>(a, ntiles);
+      return hipGetLastError();
+    }
+  }
   if (a.N <= 32) {
     dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 31) / 32)), 1, G);
     k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, (C >= 4 ? 1 : 2)><<<grid, 256, 0, st>>>(a);

@@ -34,6 +34,9 @@ def _say(*a):
 @pytest.mark.parametrize("d,order,x_shared,L,W,S,P", [
     (1, 2, False, 3, 32, 5, 37),
     (2, 2, False, 3, 128, 3, 211),
+    (2, 2, False, 3, 128, 20, 500),
+    (1, 2, False, 3, 128, 4, 300),
+    (2, 1, False, 2, 128, 3, 97),
     (2, 1, True, 2, 64, 4, 100),
     (2, 0, False, 4, 256, 2, 150),
     (3, 2, False, 2, 128, 2, 70),
