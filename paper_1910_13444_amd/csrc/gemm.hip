@@ -418,7 +418,7 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
   constexpr int WREG = BN * PITCH;                 // weight tile
   constexpr int XREG = C * BM * PITCH;             // activation tile, reused to stage the outputs
   constexpr int OPITCH = BN * ES + 16;             // staging pitch of one output plane
-  static_assert(BM * OPITCH <= XREG, "staging must fit in the activation region");
+  static_assert(C * BM * OPITCH <= XREG, "staging must fit in the activation region");
   constexpr int SEGS = RB / 16;                    // 16-byte pieces per row
   constexpr int XP = C * BM * SEGS / NTH;          // pieces per thread of an activation tile
   constexpr int WP = BN * SEGS / NTH;              // pieces per thread of the weights
@@ -529,26 +529,34 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
         Elem<T>::mma(acc[k], bfr, afr);            // rows: columns n; cols: points
       }
     }
+    __builtin_amdgcn_sched_barrier(0);             // no epilogue work (waits on the loads) above here
     lds_sync();                                    // the activation region is free for staging
 
-    auto stage_out = [&](int k, T* dst) {
+    // all C output planes of the tile at once: stream k is staged in rows
+    // [32k, 32k+32) of the (free) activation region, then copied out in
+    // full 16-byte row segments
+    auto stage_out = [&](T* dst) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float v[4];
+      for (int k = 0; k < C; ++k)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = acc[k][4 * q + e];
-        store4<T>((T*)(xl + (lane & 31) * OPITCH + ncol(q) * ES), v);
-      }
+        for (int q = 0; q < 4; ++q) {
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = acc[k][4 * q + e];
+          store4<T>((T*)(xl + (k * BM + (lane & 31)) * OPITCH + ncol(q) * ES), v);
+        }
       lds_sync();
-#pragma unroll
       // rows of points past the end hold exactly the values of the last
       // point (same inputs, same arithmetic): they are written over it
       // unconditionally, which keeps the memory counter static for the
       // prefetch waits
-      for (int j = 0; j < BM * (BN * ES / 16) / NTH; ++j) {
+      constexpr int CPR = BN * ES / 16;            // 16-byte chunks per row
+#pragma unroll
+      for (int j = 0; j < C * BM * CPR / NTH; ++j) {
         const int i = tid + j * NTH;
-        const int row = i / (BN * ES / 16), ch = i % (BN * ES / 16);
-        int64_t pt = m0 + row;
+        const int row = i / CPR, ch = i % CPR;
+        const int k = row / BM;
+        int64_t pt = m0 + row % BM;
         if (pt >= npts) pt = npts - 1;
         *(u32x4*)(dst + g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + ch * (16 / ES)) =
             *(const u32x4*)(xl + row * OPITCH + ch * 16);
@@ -560,8 +568,7 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[0][r] += bias[r];
       if (p.out_a) {
-#pragma unroll
-        for (int k = 0; k < C; ++k) stage_out(k, p.out_a);
+        stage_out(p.out_a);
       }
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -572,8 +579,7 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
 #pragma unroll
         for (int k = 0; k < C; ++k) acc[k][r] = v[k];
       }
-#pragma unroll
-      for (int k = 0; k < C; ++k) stage_out(k, p.out_h);
+      stage_out(p.out_h);
     } else {
 #pragma unroll
       for (int q = 0; q < 4; ++q)
@@ -592,8 +598,7 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
 #pragma unroll
           for (int k = 0; k < C; ++k) acc[k][r] = gv[k];
         }
-#pragma unroll
-      for (int k = 0; k < C; ++k) stage_out(k, p.out_da);
+      stage_out(p.out_da);
     }
     xstore();                                      // the next tile (the region is free again)
   }
@@ -831,7 +836,7 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   constexpr int NTM = C == 1 ? 4 : (C == 2 ? 2 : 1);
   const int64_t npts = a.seg.n_points;
   if (npts <= 0) return hipSuccess;
-  if constexpr (sizeof(T) == 2 && C >= 2 && C <= 5 && EPI != EPI_DF) {
+  if constexpr (sizeof(T) == 2 && C <= 5 && EPI != EPI_DF) {
     const int64_t span = (npts + 1) * (a.ldx > a.ldo ? a.ldx : a.ldo) * (int64_t)sizeof(T);
     if (a.K == 128 && a.N == 128 && span < ((int64_t)1 << 31)) {
       // persistent weight-resident kernel: two blocks per CU in total
