@@ -107,6 +107,10 @@ template <class T> struct NtArgs {
   T* out_da;                               // EPI_BWD: its pre-activation cotangent
   float* seedY; float* seedU; int64_t sY_g; int64_t sU_g;  // EPI_DF outputs
   int32_t nY; int32_t nU; float df_sign;
+  // EPI_FWD of the last hidden layer with the output layer fused (only where
+  // nt_fuses_output holds): y[row] = w_out . h (+ b_out on the value stream),
+  // rows in the activation row layout; wout = [w_out (N), b_out]
+  float* y; int64_t y_g; const float* wout; int64_t wo_g;
   Seg seg;
   int32_t N, K;
 };
@@ -125,6 +129,11 @@ template <class T>
 hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int64_t h_g, int64_t ldh,
                           int64_t R, int64_t n_value, int N, int J, float* partial, double* pdb,
                           int n_split, int64_t rows_per_split, int G, hipStream_t st);
+
+// whether launch_gemm_nt can fuse the output layer into EPI_FWD for this
+// shape (16-bit storage, K = N = 128, at most 5 streams, rows addressable
+// with 32-bit offsets)
+bool nt_fuses_output(int elem_bytes, int C, int K, int N, int64_t n_points, int64_t ldx, int64_t ldo);
 
 void dw_split_plan(int64_t R, int N, int J, int elem_bytes, int G, int* n_split, int64_t* rows_per_split);
 

@@ -465,13 +465,19 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
   };
   auto ncol = [&](int q) { return 32 * wave + 8 * q + 4 * hh; };   // first of the lane's 4 columns in group q
 
-  // bias of the lane's 16 columns (fixed for the whole launch)
-  float bias[16];
+  // bias and output weights of the lane's 16 columns (fixed for the launch)
+  float bias[16], wo[16];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) bias[r] = 0.0f;
+  for (int r = 0; r < 16; ++r) bias[r] = wo[r] = 0.0f;
+  float bout = 0.0f;
   if (EPI == EPI_FWD && p.bias) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) bias[r] = p.bias[g * p.b_g + ncol(r >> 2) + (r & 3)];
+  }
+  if (EPI == EPI_FWD && p.y) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) wo[r] = p.wout[g * p.wo_g + ncol(r >> 2) + (r & 3)];
+    bout = p.wout[g * p.wo_g + BN];
   }
 
   auto xstore = [&]() {
@@ -579,7 +585,33 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
 #pragma unroll
         for (int k = 0; k < C; ++k) acc[k][r] = v[k];
       }
-      stage_out(p.out_h);
+      if (p.y) {
+        // output layer: y = w_out . h over the activations as stored, summed
+        // over the lane's columns, the two lane halves, then the four waves
+        // in wave order (through LDS)
+        float* red = (float*)xl;
+#pragma unroll
+        for (int k = 0; k < C; ++k) {
+          float part = 0.0f;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) part += wo[r] * Elem<T>::to_f(Elem<T>::from_f(acc[k][r]));
+          part += __shfl_xor(part, 32);
+          if (lane < 32) red[(wave * C + k) * 32 + lane] = part;
+        }
+        lds_sync();
+        if (tid < C * 32) {
+          const int k = tid >> 5, pp = tid & 31;
+          float v = red[k * 32 + pp];
+#pragma unroll
+          for (int w = 1; w < 4; ++w) v += red[(w * C + k) * 32 + pp];
+          if (k == 0) v += bout;
+          int64_t pt = m0 + pp;
+          if (pt >= npts) pt = npts - 1;             // past the end: the last point's value again
+          p.y[g * p.y_g + p.seg.row0 + k * p.seg.plane + pt] = v;
+        }
+        lds_sync();
+      }
+      if (p.out_h) stage_out(p.out_h);
     } else {
 #pragma unroll
       for (int q = 0; q < 4; ++q)
@@ -618,7 +650,7 @@ __device__ __forceinline__ int dw_col(int c) {
   return (c >> 5) * 2624 + (c & 31) * 80 + ((c & 16) ? 64 : 0);
 }
 
-template <class T, int WM, int WN, int NT, int OCC>
+template <class T, int WM, int WN, int NT, int OCC, int NB>
 __global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OCC)))
 k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restrict__ H, int64_t h_g,
           int64_t ldh, int64_t R, int64_t n_value, int N, int J, float* __restrict__ partial,
@@ -739,37 +771,49 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
         for (int b = 0; b < NT; ++b) Elem<T>::mma(acc[a][b], af[a], bf[b]);
     }
     // bias cotangent: value rows of this slice, one column per thread
+    // (the 64-byte column line is read as 16 independent words)
     if (pdb && tj == 0 && tid < BNn && k0 < rv) {
       const int nr = (int)((rv - k0) < SR ? (rv - k0) : SR);
-      const T* colp = (const T*)(base + dw_col(tid));
+      const uint32_t* colw = (const uint32_t*)(base + dw_col(tid));
       float part_sum = 0.0f;
-      for (int u = 0; u < nr; ++u) part_sum += Elem<T>::to_f(colp[u]);
+#pragma unroll
+      for (int w = 0; w < 16; ++w) {
+        const uint32_t v = colw[w];
+        if constexpr (ES == 2) {
+          const float lo = Elem<T>::to_f(__builtin_bit_cast(T, (uint16_t)(v & 0xffffu)));
+          const float hi = Elem<T>::to_f(__builtin_bit_cast(T, (uint16_t)(v >> 16)));
+          part_sum += (2 * w < nr ? lo : 0.0f) + (2 * w + 1 < nr ? hi : 0.0f);
+        } else {
+          part_sum += w < nr ? __uint_as_float(v) : 0.0f;
+        }
+      }
       dbacc += (double)part_sum;
     }
   };
 
   if constexpr (OCC >= 2) {
-    // two LDS stages, two register buffers, loads issued two stages ahead
-    uint4 b0[PPT][RPP], b1[PPT][RPP];
+    // two LDS stages and a ring of NB register buffers: buffer b holds the
+    // stages s = b (mod NB), so NB stages of loads are in flight while one is
+    // multiplied.  Loads are unconditional (stage index clamped, rows past
+    // the range zeroed at the LDS store), so the waits are static counts.
+    uint4 bufs[NB][PPT][RPP];
     const int last = nst > 0 ? nst - 1 : 0;
-    if (nst > 0) {
-      gload(b0, r0);
-      lstore(b0, 0, r0);
-    }
-    gload(b1, r0 + (int64_t)(nst > 1 ? 1 : 0) * SR);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) gload(bufs[b], r0 + (int64_t)(b < last ? b : last) * SR);
+    if (nst > 0) lstore(bufs[0], 0, r0);
+    gload(bufs[0], r0 + (int64_t)(NB < last ? NB : last) * SR);
     lds_sync();
-    for (int st = 0; st < nst; st += 2) {
-      gload(b0, r0 + (int64_t)(st + 2 < nst ? st + 2 : last) * SR);
-      compute(0, r0 + (int64_t)st * SR);
-      __builtin_amdgcn_sched_barrier(0);
-      if (st + 1 < nst) lstore(b1, 1, r0 + (int64_t)(st + 1) * SR);
-      lds_sync();
-      if (st + 1 >= nst) break;
-      gload(b1, r0 + (int64_t)(st + 3 < nst ? st + 3 : last) * SR);
-      compute(1, r0 + (int64_t)(st + 1) * SR);
-      __builtin_amdgcn_sched_barrier(0);
-      if (st + 2 < nst) lstore(b0, 0, r0 + (int64_t)(st + 2) * SR);
-      lds_sync();
+    for (int st = 0; st < nst; st += NB) {
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const int sc = st + u;                     // stage in LDS[sc & 1]
+        if (sc >= nst) break;
+        compute(sc & 1, r0 + (int64_t)sc * SR);
+        __builtin_amdgcn_sched_barrier(0);
+        if (sc + 1 < nst) lstore(bufs[(u + 1) % NB], (sc + 1) & 1, r0 + (int64_t)(sc + 1) * SR);
+        gload(bufs[(u + 1) % NB], r0 + (int64_t)(sc + 1 + NB < last ? sc + 1 + NB : last) * SR);
+        lds_sync();
+      }
     }
   } else {
     // large tiles (one wave per SIMD): one register buffer, one stage ahead
@@ -817,6 +861,15 @@ namespace {
 // (N <= 32) use 4 x 1 waves.  (Larger block tiles at one wave per SIMD, and
 // 2 x 4 wave blocks, measured slower: the loop is latency-bound, so occupancy
 // matters more than per-block intensity.)
+}  // namespace
+
+bool nt_fuses_output(int elem_bytes, int C, int K, int N, int64_t n_points, int64_t ldx, int64_t ldo) {
+  const int64_t span = (n_points + 1) * (ldx > ldo ? ldx : ldo) * (int64_t)elem_bytes;
+  return elem_bytes == 2 && C >= 1 && C <= 5 && K == 128 && N == 128 && span < ((int64_t)1 << 31);
+}
+
+namespace {
+
 // compute units of the current device (cached per device)
 int cu_count() {
   static int cached[64] = {0};
@@ -837,8 +890,7 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   const int64_t npts = a.seg.n_points;
   if (npts <= 0) return hipSuccess;
   if constexpr (sizeof(T) == 2 && C <= 5 && EPI != EPI_DF) {
-    const int64_t span = (npts + 1) * (a.ldx > a.ldo ? a.ldx : a.ldo) * (int64_t)sizeof(T);
-    if (a.K == 128 && a.N == 128 && span < ((int64_t)1 << 31)) {
+    if (nt_fuses_output((int)sizeof(T), C, a.K, a.N, npts, a.ldx, a.ldo)) {
       // persistent weight-resident kernel: two blocks per CU in total
       const int64_t ntiles = (npts + 31) / 32;
       int64_t nb = 2 * (int64_t)cu_count() / G;
@@ -849,6 +901,7 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
       return hipGetLastError();
     }
   }
+  if (a.y) return hipErrorInvalidValue;           // the output layer is fused only by the resident kernel
   if (a.N <= 32) {
     dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 31) / 32)), 1, G);
     k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, (C >= 4 ? 1 : 2)><<<grid, 256, 0, st>>>(a);
@@ -889,7 +942,10 @@ void dw_split_plan(int64_t R, int N, int J, int elem_bytes, int G, int* n_split,
   const int SR = 64 / elem_bytes;
   const int bt = (N >= 128 && J >= 128) ? 128 : ((N >= 64 && J >= 64) ? 64 : 32);
   const int64_t tiles = (int64_t)((N + bt - 1) / bt) * ((J + bt - 1) / bt) * G;
-  int64_t want = (1024 + tiles - 1) / tiles;
+  // about 1024 blocks; a single output tile takes 512 (each split writes a
+  // whole N x J fp32 partial, and one resident wave of blocks suffices)
+  const int64_t target = tiles > 1 ? 1024 : 512;
+  int64_t want = (target + tiles - 1) / tiles;
   const int64_t stages = (R + SR - 1) / SR;
   int64_t max_split = stages / 4 > 0 ? stages / 4 : 1;
   if (want > max_split) want = max_split;
@@ -910,15 +966,15 @@ hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int
   if (R <= 0) return hipSuccess;
   if (N >= 128 && J >= 128) {
     dim3 grid((unsigned)(((N + 127) / 128) * ((J + 127) / 128)) * n_split, 1, G);
-    k_gemm_dw<T, 2, 2, 2, 2><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
+    k_gemm_dw<T, 2, 2, 2, 2, 4><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
                                                     n_split, rows_per_split);
   } else if (N >= 64 && J >= 64) {
     dim3 grid((unsigned)(((N + 63) / 64) * ((J + 63) / 64)) * n_split, 1, G);
-    k_gemm_dw<T, 2, 2, 1, 2><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
+    k_gemm_dw<T, 2, 2, 1, 2, 4><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
                                                  n_split, rows_per_split);
   } else {
     dim3 grid((unsigned)(((N + 31) / 32) * ((J + 31) / 32)) * n_split, 1, G);
-    k_gemm_dw<T, 1, 1, 1, 2><<<grid, 64, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
+    k_gemm_dw<T, 1, 1, 1, 2, 4><<<grid, 64, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
                                                 n_split, rows_per_split);
   }
   return hipGetLastError();

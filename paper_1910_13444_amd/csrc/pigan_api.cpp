@@ -335,10 +335,10 @@ template <class T>
 static pigan_status gemm_nt(int epi, int nd1, int nd2, const NtArgs<T>& a, int G, hipStream_t st, const char* name) {
   const int C = 1 + nd1 + nd2;
   const double M = (double)C * a.seg.n_points;
-  const double flops = 2.0 * M * a.N * a.K * G;
+  const double flops = 2.0 * M * a.N * a.K * G + (a.y ? 2.0 * M * a.N * G : 0.0);
   const double es = sizeof(T);
   double bytes = (M * a.K + (double)a.N * a.K) * es * G;
-  if (epi == EPI_FWD) bytes += M * a.N * es * G * (a.out_a ? 2 : 1);
+  if (epi == EPI_FWD) bytes += M * a.N * es * G * ((a.out_a ? 1 : 0) + (a.out_h ? 1 : 0)) + (a.y ? M * 4.0 * G : 0.0);
   else if (epi == EPI_BWD) bytes += 2.0 * M * a.N * es * G;
   else bytes += M * a.N * 4.0 * G;
   // timing records are keyed by launch shape: one name = one kernel instantiation and size
@@ -405,12 +405,21 @@ static pigan_status gen_chunk_fwd(void* ws, const NetBuf& nb, const float* param
     ProfScope ps(st, "first_fwd", 2.0 * nb.n_col * W * d * G, (double)nb.n_col * C * W * 2 * sizeof(T) * G);
     HIP_TRY(launch_first_fwd<T>(nb.nd1, nb.nd2, fa, G, st));
   }
+  // the output layer rides on the last hidden layer's epilogue where the
+  // kernel supports it (then the last activations are never stored)
+  const int C = 1 + nb.nd1 + nb.nd2;
+  const bool fuse_out = L >= 2 && nt_fuses_output((int)sizeof(T), 1, W, W, nb.n_sen, W, W) &&
+                        nt_fuses_output((int)sizeof(T), C, W, W, nb.n_col, W, W);
   for (int l = 2; l <= L; ++l) {
     NtArgs<T> a{};
     a.X = tp<T>(ws, nb.H[l - 1]); a.x_g = actg; a.ldx = W;
     a.Wm = tp<T>(ws, nb.wc) + (size_t)(l - 2) * W * W; a.w_g = (int64_t)std::max(L - 1, 1) * W * W; a.ldw = W;
     a.bias = params + nb.off.b[l]; a.b_g = pg;
     a.out_a = tp<T>(ws, nb.A[l]); a.out_h = tp<T>(ws, nb.H[l]); a.o_g = actg; a.ldo = W;
+    if (l == L && fuse_out) {
+      a.out_h = nullptr;
+      a.y = tp<float>(ws, nb.jet); a.y_g = nb.R; a.wout = params + nb.off.wout; a.wo_g = pg;
+    }
     a.N = W; a.K = W;
     a.seg = Seg{nb.n_sen, 0, 0};
     pigan_status s1 = gemm_nt<T>(EPI_FWD, 0, 0, a, G, st, "gemm_fwd");
@@ -419,7 +428,7 @@ static pigan_status gen_chunk_fwd(void* ws, const NetBuf& nb, const float* param
     s1 = gemm_nt<T>(EPI_FWD, nb.nd1, nb.nd2, a, G, st, "gemm_fwd");
     if (s1 != PIGAN_OK) return s1;
   }
-  {
+  if (!fuse_out) {
     ProfScope ps(st, "out_fwd", 2.0 * nb.rows * W * G, (double)nb.rows * W * sizeof(T) * G);
     HIP_TRY(launch_out_fwd<T>(tp<T>(ws, nb.H[L]), actg, W, nb.rows, nb.n_sen + nb.n_col, W, params + nb.off.wout, pg,
                               tp<float>(ws, nb.jet), nb.R, G, st));
@@ -772,6 +781,7 @@ static pigan_status run_gen_fwd(const pigan_mlp* net, const float* params, int d
     ProfScope ps(st, "first_fwd", 2.0 * M * W * d * G, (double)M * (1 + nd1 + nd2) * W * sizeof(T) * G);
     HIP_TRY(launch_first_fwd<T>(nd1, nd2, fa, G, st));
   }
+  const bool fuse_out = L >= 2 && nt_fuses_output((int)sizeof(T), 1 + nd1 + nd2, W, W, M, W, W);
   int cur = 0;
   for (int l = 2; l <= L; ++l) {
     NtArgs<T> a{};
@@ -779,12 +789,16 @@ static pigan_status run_gen_fwd(const pigan_mlp* net, const float* params, int d
     a.Wm = tp<T>(ws, p.wc) + (size_t)(l - 2) * W * W; a.w_g = (int64_t)std::max(L - 1, 1) * W * W; a.ldw = W;
     a.bias = params + off.b[l]; a.b_g = off.n;
     a.out_a = nullptr; a.out_h = tp<T>(ws, p.h[1 - cur]); a.o_g = actg; a.ldo = W;
+    if (l == L && fuse_out) {
+      a.out_h = nullptr;
+      a.y = jet; a.y_g = p.R; a.wout = params + off.wout; a.wo_g = off.n;
+    }
     a.N = W; a.K = W; a.seg = Seg{M, 0, M};
     pigan_status s1 = gemm_nt<T>(EPI_FWD, nd1, nd2, a, G, st, "gemm_fwd");
     if (s1 != PIGAN_OK) return s1;
     cur = 1 - cur;
   }
-  {
+  if (!fuse_out) {
     ProfScope ps(st, "out_fwd", 2.0 * p.R * W * G, (double)p.R * W * sizeof(T) * G);
     HIP_TRY(launch_out_fwd<T>(tp<T>(ws, p.h[cur]), actg, W, p.R, M, W, params + off.wout, off.n, jet, p.R, G, st));
   }
