@@ -852,6 +852,224 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
 }
 
 // ---------------------------------------------------------------------------
+// k_gemm_dw_tr: the same weight gradient for 16-bit storage, with row-major
+// operand stages in LDS.  Global loads are whole 16-byte row segments, 16
+// lanes per 256-byte row (fully used cache lines); the matrix-core fragments,
+// which need 8 consecutive rows of one column per lane, are gathered with the
+// transposing LDS read of gfx950: within each 16-lane group, lanes 4r..4r+3
+// address the four 8-byte pieces of row r of a 4 x 16 block and lane i
+// receives column i of the block.  Two such reads give a lane its 8 rows.
+// Row pitch = row bytes + pad with pitch/4 = 16 or 48 (mod 64), so the four
+// rows of one read fall in disjoint bank ranges.
+// ---------------------------------------------------------------------------
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 tr_bf16x4;
+typedef __attribute__((__vector_size__(4 * sizeof(__fp16)))) __fp16 tr_f16x4;
+
+template <class T>
+__device__ __forceinline__ u32x2 lds_read_tr(const char* p) {
+  if constexpr (__is_same(T, bf16)) {
+    return __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                                         (__attribute__((address_space(3))) tr_bf16x4*)(p)));
+  } else {
+    return __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4f16(
+                                         (__attribute__((address_space(3))) tr_f16x4*)(p)));
+  }
+}
+
+__host__ __device__ constexpr int dw_tr_pitch(int row_bytes) {
+  // smallest pitch >= row_bytes (multiple of 64 bytes) with pitch/4 = 16 or 48 mod 64
+  return (row_bytes / 4) % 64 == 16 || (row_bytes / 4) % 64 == 48 ? row_bytes
+         : (row_bytes / 4) % 64 == 0 ? row_bytes + 64 : row_bytes + 64 * ((row_bytes / 4) % 64 == 32 ? 1 : 0);
+}
+
+template <class T, int WM, int WN, int NT, int NB>
+__global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2)))
+k_gemm_dw_tr(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restrict__ H, int64_t h_g,
+             int64_t ldh, int64_t R, int64_t n_value, int N, int J, float* __restrict__ partial,
+             double* __restrict__ pdb, int n_split, int64_t rows_per_split) {
+  static_assert(sizeof(T) == 2, "16-bit storage only");
+  constexpr int BNn = 32 * NT * WM;
+  constexpr int BJ = 32 * NT * WN;
+  constexpr int NTH = 64 * WM * WN;
+  constexpr int SR = 32;                    // rows per stage (two 16-row k chunks)
+  constexpr int SA = BNn / 8, SB = BJ / 8;  // 16-byte segments per row
+  constexpr int PA = dw_tr_pitch(BNn * 2), PB = dw_tr_pitch(BJ * 2);
+  constexpr int REGA = SR * PA;
+  constexpr int STAGE = REGA + SR * PB;
+  constexpr int PIECES = SR * (SA + SB);
+  static_assert(PIECES % NTH == 0, "whole pieces per thread");
+  constexpr int PPT = PIECES / NTH;
+  typedef typename Elem<T>::frag frag;
+  __shared__ __attribute__((aligned(16))) char lds[2 * STAGE];
+
+  const int tiles_n = (N + BNn - 1) / BNn;
+  const int tiles = tiles_n * ((J + BJ - 1) / BJ);
+  const int64_t lb = xcd_remap(blockIdx.x, gridDim.x);
+  const int tile = (int)(lb % tiles);
+  const int tn = tile % tiles_n;
+  const int tj = tile / tiles_n;
+  const int split = (int)(lb / tiles);
+  const int g = blockIdx.z;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave % WM;
+  const int wn = wave / WM;
+  const int n0 = tn * BNn;
+  const int j0 = tj * BJ;
+  // stages are dealt round-robin over the splits (split s takes stages s,
+  // s + n_split, ...), so at any time the blocks stream one contiguous window
+  // of rows (page and DRAM locality) instead of n_split separate ranges
+  (void)rows_per_split;
+  const int64_t r1 = R;
+  const int64_t rv = R < n_value ? R : n_value;
+  const int64_t tot = (R + SR - 1) / SR;
+  const int nst = (int)(split < tot ? (tot - split + n_split - 1) / n_split : 0);
+  auto krow = [&](int sc) { return ((int64_t)split + (int64_t)sc * n_split) * SR; };
+  const T* A = dA + g * a_g;
+  const T* B = H + g * h_g;
+
+  f32x16 acc[NT][NT];
+#pragma unroll
+  for (int a = 0; a < NT; ++a)
+#pragma unroll
+    for (int b = 0; b < NT; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
+  float dbp[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) dbp[t] = 0.0f;
+  double dbacc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) dbacc[t] = 0.0;
+  const bool want_db = pdb && tj == 0 && wn == 0;
+
+  // piece q: operand A for q < SR * SA (row q / SA, segment q % SA), else B.
+  // Rows past the range load a clamped row and are zeroed at the LDS store;
+  // columns past the end load a clamped column (never stored outputs).
+  auto gload = [&](u32x4* buf, int64_t k0) {
+#pragma unroll
+    for (int i = 0; i < PPT; ++i) {
+      const int q = tid + i * NTH;
+      const bool isA = q < SR * SA;
+      const int qq = isA ? q : q - SR * SA;
+      const int sg = isA ? qq % SA : qq % SB;
+      const int row = isA ? qq / SA : qq / SB;
+      int64_t gr = k0 + row;
+      if (gr >= r1) gr = r1 - 1;
+      int col = (isA ? n0 : j0) + sg * 8;
+      const int lim = isA ? N : J;
+      if (col >= lim) col = lim - 8;
+      buf[i] = isA ? *(const u32x4*)(A + gr * lda + col) : *(const u32x4*)(B + gr * ldh + col);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  auto lstore = [&](const u32x4* buf, int stage, int64_t k0) {
+    char* base = lds + stage * STAGE;
+#pragma unroll
+    for (int i = 0; i < PPT; ++i) {
+      const int q = tid + i * NTH;
+      const bool isA = q < SR * SA;
+      const int qq = isA ? q : q - SR * SA;
+      const int sg = isA ? qq % SA : qq % SB;
+      const int row = isA ? qq / SA : qq / SB;
+      const uint32_t m = (k0 + row < r1) ? 0xffffffffu : 0u;
+      const u32x4 v = buf[i] & m;
+      *(u32x4*)(base + (isA ? row * PA : REGA + row * PB) + sg * 16) = v;
+    }
+  };
+  // fragments: lane l holds rows 8 (l / 32) .. +7 of its column (l % 32) of
+  // the 32-column block, as two transposing reads of 4 rows
+  const int grp = lane >> 4, t16 = lane & 15;
+  const int rr = t16 >> 2, qq4 = t16 & 3;
+  const int kb = 8 * (lane >> 5);
+  auto frag_at = [&](const char* region, int pitch, int c, int colblk) {
+    const char* p0 = region + (c * 16 + kb + rr) * pitch + (colblk + 16 * (grp & 1) + 4 * qq4) * 2;
+    const u32x2 lo = lds_read_tr<T>(p0);
+    const u32x2 hi = lds_read_tr<T>(p0 + 4 * pitch);
+    const u32x4 w = {lo.x, lo.y, hi.x, hi.y};
+    return __builtin_bit_cast(frag, w);
+  };
+  auto compute = [&](int stage, int64_t k0) {
+    const char* base = lds + stage * STAGE;
+#pragma unroll
+    for (int c = 0; c < SR / 16; ++c) {
+      frag af[NT], bf[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        af[t] = frag_at(base, PA, c, 32 * (wm * NT + t));
+        bf[t] = frag_at(base + REGA, PB, c, 32 * (wn * NT + t));
+      }
+#pragma unroll
+      for (int a = 0; a < NT; ++a)
+#pragma unroll
+        for (int b = 0; b < NT; ++b) Elem<T>::mma(acc[a][b], af[a], bf[b]);
+      // bias cotangent: value rows of the lane's 8 rows of its dA columns
+      if (want_db && k0 + c * 16 < rv) {
+        const int64_t rw0 = k0 + c * 16 + kb;
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) dbp[t] += rw0 + e < rv ? Elem<T>::to_f(af[t][e]) : 0.0f;
+      }
+    }
+    if (want_db) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        dbacc[t] += (double)dbp[t];
+        dbp[t] = 0.0f;
+      }
+    }
+  };
+
+  // ring of NB register stages (as in k_gemm_dw)
+  u32x4 bufs[NB][PPT];
+  const int last = nst > 0 ? nst - 1 : 0;
+#pragma unroll
+  for (int b = 0; b < NB; ++b) gload(bufs[b], krow(b < last ? b : last));
+  if (nst > 0) lstore(bufs[0], 0, krow(0));
+  gload(bufs[0], krow(NB < last ? NB : last));
+  lds_sync();
+  for (int st = 0; st < nst; st += NB) {
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+      const int sc = st + u;
+      if (sc >= nst) break;
+      compute(sc & 1, krow(sc));
+      __builtin_amdgcn_sched_barrier(0);
+      if (sc + 1 < nst) lstore(bufs[(u + 1) % NB], (sc + 1) & 1, krow(sc + 1));
+      gload(bufs[(u + 1) % NB], krow(sc + 1 + NB < last ? sc + 1 + NB : last));
+      lds_sync();
+    }
+  }
+
+  const int hh = lane >> 5;
+  float* out = partial + ((int64_t)g * n_split + split) * (int64_t)N * J;
+#pragma unroll
+  for (int a = 0; a < NT; ++a) {
+#pragma unroll
+    for (int b = 0; b < NT; ++b) {
+      const int j = j0 + 32 * (wn * NT + b) + (lane & 31);
+      if (j >= J) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int n = n0 + 32 * (wm * NT + a) + 8 * (r >> 2) + 4 * hh + (r & 3);
+        if (n < N) out[(int64_t)n * J + j] = acc[a][b][r];
+      }
+    }
+  }
+  if (want_db) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      double v = dbacc[t];
+      v += __shfl_xor(v, 32);                      // the other 8-row half of the same column
+      const int n = n0 + 32 * (wm * NT + t) + (lane & 31);
+      if (lane < 32 && n < N) pdb[((int64_t)g * n_split + split) * N + n] = v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // host launchers
 // ---------------------------------------------------------------------------
 namespace {
@@ -964,6 +1182,22 @@ hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int
                           int64_t R, int64_t n_value, int N, int J, float* partial, double* pdb,
                           int n_split, int64_t rows_per_split, int G, hipStream_t st) {
   if (R <= 0) return hipSuccess;
+  if constexpr (sizeof(T) == 2) {
+    if (N >= 128 && J >= 128) {
+      dim3 grid((unsigned)(((N + 127) / 128) * ((J + 127) / 128)) * n_split, 1, G);
+      k_gemm_dw_tr<T, 2, 2, 2, 4><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
+                                                       n_split, rows_per_split);
+    } else if (N >= 64 && J >= 64) {
+      dim3 grid((unsigned)(((N + 63) / 64) * ((J + 63) / 64)) * n_split, 1, G);
+      k_gemm_dw_tr<T, 2, 2, 1, 4><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
+                                                       n_split, rows_per_split);
+    } else {
+      dim3 grid((unsigned)(((N + 31) / 32) * ((J + 31) / 32)) * n_split, 1, G);
+      k_gemm_dw_tr<T, 1, 1, 1, 4><<<grid, 64, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
+                                                      n_split, rows_per_split);
+    }
+    return hipGetLastError();
+  }
   if (N >= 128 && J >= 128) {
     dim3 grid((unsigned)(((N + 127) / 128) * ((J + 127) / 128)) * n_split, 1, G);
     k_gemm_dw<T, 2, 2, 2, 2, 4><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
