@@ -474,6 +474,7 @@ k_first_bwd(FirstBwdArgs<T> p) {
       }
     }
     const int q0 = (int)((int64_t)p.P * rc / p.nrc), q1 = (int)((int64_t)p.P * (rc + 1) / p.nrc);
+#pragma unroll 4
     for (int q = q0 + lp; q < q1; q += PPP) {
       const int64_t pt = (int64_t)s * p.P + q;
       float v[8];
@@ -521,30 +522,31 @@ k_first_bwd(FirstBwdArgs<T> p) {
 // dW1[n][c] and db1[n] from the partials (fp64 sums, fixed order):
 //   c < d : sum_{s,rc} gx_c + gd_c ;  c >= d : sum_{s,rc} gs * z_s[c-d] ;
 //   bias (blockIdx.y == in_dim) : sum_{s,rc} gs
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(1024)
 k_first_wgrad(const float* __restrict__ part, int S, int nrc, int W, int d, int nd1, int in_dim,
               const float* __restrict__ z, int64_t z_g, int n_z, float* grad, int64_t g_g, int accumulate,
               float scale, int32_t* nonfinite) {
-  __shared__ double red[8][32];
+  __shared__ double red[32][32];
   const int g = blockIdx.z;
   const int c = blockIdx.y;
-  const int lane = threadIdx.x & 31, grp = threadIdx.x >> 5;
+  const int lane = threadIdx.x & 31, grp = threadIdx.x >> 5;   // 32 sample groups
   const int n = blockIdx.x * 32 + lane;
   double acc = 0.0;
   if (n < W) {
     const float* pp = part + (int64_t)g * S * nrc * 7 * W + n;
-    for (int s = grp; s < S; s += 8) {
-      float zz = 1.0f;
-      if (c >= d && c < in_dim) zz = z[g * z_g + (int64_t)s * n_z + (c - d)];
+    const bool xcol = c < d;                       // weight of coordinate c: sum of gx_c and gd_c
+    const bool two = xcol && c < nd1;
+    const int64_t o1 = xcol ? (int64_t)(1 + c) * W : 0, o2 = (int64_t)(4 + c) * W;
+    for (int s = grp; s < S; s += 32) {
+      const float* b = pp + (int64_t)s * nrc * 7 * W;
+      double t = 0.0;
+#pragma unroll 4
       for (int r = 0; r < nrc; ++r) {
-        const float* b = pp + ((int64_t)s * nrc + r) * 7 * W;
-        if (c < d) {
-          acc += (double)b[(int64_t)(1 + c) * W];
-          if (c < nd1) acc += (double)b[(int64_t)(4 + c) * W];
-        } else {
-          acc += (double)b[0] * (double)zz;
-        }
+        t += (double)b[(int64_t)r * 7 * W + o1];
+        if (two) t += (double)b[(int64_t)r * 7 * W + o2];
       }
+      if (!xcol && c < in_dim) t *= (double)z[g * z_g + (int64_t)s * n_z + (c - d)];
+      acc += t;
     }
   }
   red[grp][lane] = acc;
@@ -552,7 +554,7 @@ k_first_wgrad(const float* __restrict__ part, int S, int nrc, int W, int d, int 
   if (grp == 0 && n < W) {
     double v = 0.0;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) v += red[q][lane];
+    for (int q = 0; q < 32; ++q) v += red[q][lane];
     const int64_t o = c < in_dim ? (int64_t)n * in_dim + c : (int64_t)W * in_dim + n;
     float* dst = grad + g * g_g + o;
     float r = (float)(v * (double)scale);
@@ -717,8 +719,8 @@ hipError_t launch_first_bwd(const FirstBwdArgs<T>& a, int G, hipStream_t st) {
 hipError_t launch_first_wgrad(const float* part, int S, int nrc, int W, int d, int nd1, int in_dim, const float* z,
                               int64_t z_g, int n_z, float* grad, int64_t g_g, int accumulate, float scale,
                               int32_t* nonfinite, int G, hipStream_t st) {
-  k_first_wgrad<<<dim3(nblk(W, 32), in_dim + 1, G), 256, 0, st>>>(part, S, nrc, W, d, nd1, in_dim, z, z_g, n_z, grad,
-                                                                  g_g, accumulate, scale, nonfinite);
+  k_first_wgrad<<<dim3(nblk(W, 32), in_dim + 1, G), 1024, 0, st>>>(part, S, nrc, W, d, nd1, in_dim, z, z_g, n_z,
+                                                                   grad, g_g, accumulate, scale, nonfinite);
   return hipGetLastError();
 }
 
