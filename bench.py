@@ -83,6 +83,39 @@ def recorded_traffic(key, wl):
     return None
 
 
+def measured_peaks(dev):
+    """Achievable rates on this GPU from two micro-benchmarks (context for
+    the roofline): a 2 GiB device-to-device copy (bytes read + written per
+    second) and an 8192^3 bf16 matrix product through the vendor BLAS."""
+    import torch
+    out = {}
+    n = 1 << 31
+    a = torch.empty(n, dtype=torch.uint8, device=dev)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    out["copy_GBps"] = 2.0 * n * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del a, b
+    m = 8192
+    x = torch.randn(m, m, dtype=torch.bfloat16, device=dev)
+    y = torch.randn(m, m, dtype=torch.bfloat16, device=dev)
+    torch.matmul(x, y)
+    e0.record()
+    for _ in range(10):
+        torch.matmul(x, y)
+    e1.record()
+    torch.cuda.synchronize()
+    out["bf16_gemm_TFLOPs"] = 2.0 * m ** 3 * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e12
+    del x, y
+    torch.cuda.empty_cache()
+    return out
+
+
 def run_steps(step, d, wl, k):
     for _ in range(k):
         step(d["pY"], d["pU"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["real"], f=None,
@@ -132,6 +165,7 @@ def main():
     ap.add_argument("--chunk-S", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the copy / GEMM micro-benchmarks")
     ap.add_argument("--copy-calib", type=int, default=0, metavar="BYTES",
                     help="first run one plain device-to-device copy of BYTES bytes (a known-size reference "
                          "dispatch for scaling HBM byte counters)")
@@ -217,6 +251,7 @@ def main():
             log(f"  {k:12s} {v['ms_per_step']:.4f} ms/step  {100 * v['share']:.1f}%  "
                 f"launches/step {v['launches_per_step']:.0f}")
 
+    peaks = None if a.no_peaks else measured_peaks(dev)
     cpu = None if a.no_cpu_baseline else cpu_baseline(wl)
 
     out = {
@@ -231,6 +266,7 @@ def main():
         "mfma_frac_step": tflops / PEAK_TFLOPS[wl.dtype],
         "nonfinite": nf,
         "roofline": roof,
+        "measured_peaks": peaks,
         "cpu_baseline": cpu,
         "kernels": kernels,
     }

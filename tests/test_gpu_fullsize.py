@@ -47,6 +47,32 @@ def test_full_jets_sampled(full):
         check({f"{name}.c{k}": rel(got[k], ref[k]) for k in range(len(ref))}, TOL[WL.dtype], f"full jets {name}")
 
 
+@pytest.mark.parametrize("wl", [configs.C3, configs.C5], ids=["c3", "c5"])
+def test_full_jets_sampled_large(wl):
+    """Generator jets of the 6x512 (S=512, P=4096) and 6x1024 (S=1024,
+    P=2048) workloads at full size, bf16, at 16 sampled (sample, point)
+    pairs against the oracle."""
+    import torch
+    print(f"full-size jets, sampled: {wl.name}", flush=True)
+    inp = make_inputs(wl)
+    shape = wl.gen_shape()
+    rng = np.random.default_rng(12)
+    ss = rng.integers(0, wl.S, 16)
+    pp = rng.integers(0, wl.P, 16)
+    xc = to_dev(inp.xc)
+    z = to_dev(inp.z)
+    for name, p, order in (("Y", inp.pY, 1), ("U", inp.pU, 2)):
+        jet = pigan.gen_forward(to_dev(p), shape, wl.d, z, xc, order, dtype=wl.dtype)
+        torch.cuda.synchronize()
+        got = jet[0][:, ss, pp].cpu().numpy()
+        del jet
+        o = oracle.gen_forward(p[0], shape, wl.d, inp.xc[0][ss, pp], inp.z[0][ss], order)
+        ref = [o["y"]] + ([o["dy"][i] for i in range(wl.d)] if order >= 1 else []) + \
+              ([o["ddy"][i] for i in range(wl.d)] if order >= 2 else [])
+        check({f"{name}.c{k}": rel(got[k], ref[k]) for k in range(len(ref))}, TOL[wl.dtype], f"{wl.name} jets {name}")
+    torch.cuda.empty_cache()
+
+
 def _oracle_losses(inp, real, prec=None, with_pde=True, chunk=32):
     """Losses of the step at full size from the oracle's forward passes."""
     gs, ds, d = WL.gen_shape(), WL.disc_shape(), WL.d
