@@ -108,9 +108,19 @@ template <class T> struct NtArgs {
   float* seedY; float* seedU; int64_t sY_g; int64_t sU_g;  // EPI_DF outputs
   int32_t nY; int32_t nU; float df_sign;
   // EPI_FWD of the last hidden layer with the output layer fused (only where
-  // nt_fuses_output holds): y[row] = w_out . h (+ b_out on the value stream),
+  // nt_resident_ok holds): y[row] = w_out . h (+ b_out on the value stream),
   // rows in the activation row layout; wout = [w_out (N), b_out]
   float* y; int64_t y_g; const float* wout; int64_t wo_g;
+  // second-layer calls with the first layer formed in the kernel (only where
+  // nt_resident_ok holds; fp1 != null): the forward builds its operand X,
+  // and the reverse pass its saved pre-activations, from the coordinates, the
+  // per-sample z-projection (+ b1) and the fp32 W1 instead of reading them.
+  // Point pt of the segment is sample pt / fPn at coordinate row
+  // (fx_shared ? pt % fPn : pt).
+  const float* fp1; int64_t fp_g; int32_t f_in; int32_t f_d;
+  const float* fzp; int64_t fzp_g;
+  const float* fx; int64_t fx_g; int32_t fx_shared; int64_t fPn;
+  T* f_out_h;                              // forward: also store the generated activations (may be null)
   Seg seg;
   int32_t N, K;
 };
@@ -130,10 +140,11 @@ hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int
                           int64_t R, int64_t n_value, int N, int J, float* partial, double* pdb,
                           int n_split, int64_t rows_per_split, int G, hipStream_t st);
 
-// whether launch_gemm_nt can fuse the output layer into EPI_FWD for this
-// shape (16-bit storage, K = N = 128, at most 5 streams, rows addressable
-// with 32-bit offsets)
-bool nt_fuses_output(int elem_bytes, int C, int K, int N, int64_t n_points, int64_t ldx, int64_t ldo);
+// whether launch_gemm_nt runs this shape on the persistent resident-weight
+// kernel, which alone fuses the output layer and the first layer (16-bit
+// storage, K = N = 128, at most 5 streams, rows addressable with 32-bit
+// offsets)
+bool nt_resident_ok(int elem_bytes, int C, int K, int N, int64_t n_points, int64_t ldx, int64_t ldo);
 
 void dw_split_plan(int64_t R, int N, int J, int elem_bytes, int G, int* n_split, int64_t* rows_per_split);
 

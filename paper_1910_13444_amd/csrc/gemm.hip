@@ -407,7 +407,7 @@ k_gemm_nt(const NtArgs<T> p) {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-template <class T, int ND1, int ND2, int EPI>
+template <class T, int ND1, int ND2, int EPI, bool FIRST>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
 k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
   static_assert(sizeof(T) == 2, "16-bit storage only");
@@ -424,9 +424,11 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
   constexpr int WP = BN * SEGS / NTH;              // pieces per thread of the weights
   constexpr int RPP = NTH / SEGS;                  // rows covered by one piece index
   typedef typename Elem<T>::frag frag;
-  __shared__ __attribute__((aligned(16))) char lds[WREG + XREG];
+  constexpr int W1REG = FIRST ? BN * 4 * 4 : 0;   // W1 columns 0..2 of every unit (fp32, padded to 4)
+  __shared__ __attribute__((aligned(16))) char lds[WREG + XREG + W1REG];
   char* const wl = lds;
   char* const xl = lds + WREG;
+  float* const w1l = (float*)(lds + WREG + XREG);
 
   const int g = blockIdx.z;
   const int tid = threadIdx.x;
@@ -447,20 +449,52 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
     for (int i = 0; i < WP; ++i) *(u32x4*)(wl + (tid / SEGS + RPP * i) * PITCH + sg * 16) = wb[i];
   }
 
+  // first layer formed in the kernel: W1[n][0..d-1] for every unit n
+  if constexpr (FIRST) {
+    if (tid < BN) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        w1l[tid * 4 + i] = i < p.f_d ? p.fp1[g * p.fp_g + (int64_t)tid * p.f_in + i] : 0.0f;
+    }
+    lds_sync();
+  }
+  // sample and coordinate row of point pt of the segment
+  auto f_sample = [&](int64_t pt) { return pt / p.fPn; };
+  auto f_xrow = [&](int64_t pt) { return p.fx_shared ? pt % p.fPn : pt; };
+
   // activation rows of a tile; points past the end repeat the last point.
   // Stream bases are uniform (scalar); a thread's two point rows are 32-bit
   // byte offsets (the host checks that a stream plane spans < 2^31 bytes).
   static_assert(BM == 2 * RPP, "two point rows per thread");
-  u32x4 xb[XP];
+  constexpr bool GENX = FIRST && EPI == EPI_FWD;   // forward: X is the first layer's activations
+  constexpr int XPR = GENX ? 1 : XP;
+  u32x4 xb[XPR];
+  // first layer: the thread's two points (rows tid / SEGS + RPP j) and its 8
+  // units 8 sg..8 sg+7: coordinates and z-projection of the next tile
+  float fxv[2][3], fzv[2][8];
   auto xload = [&](int64_t tile) {
     int64_t p0 = tile * BM + tid / SEGS, p1 = p0 + RPP;
     if (p0 >= npts) p0 = npts - 1;
     if (p1 >= npts) p1 = npts - 1;
-    const uint32_t o0 = (uint32_t)(p0 * p.ldx * ES) + sg * 16, o1 = (uint32_t)(p1 * p.ldx * ES) + sg * 16;
+    if constexpr (GENX) {
 #pragma unroll
-    for (int i = 0; i < XP; ++i) {
-      const char* base = Xb + (p.seg.row0 + (i >> 1) * p.seg.plane) * p.ldx * ES;
-      xb[i] = *(const u32x4*)(base + ((i & 1) ? o1 : o0));
+      for (int jj = 0; jj < 2; ++jj) {
+        const int64_t pt = jj ? p1 : p0;
+        const float* xv = p.fx + g * p.fx_g + f_xrow(pt) * p.f_d;
+#pragma unroll
+        for (int i = 0; i < 3; ++i) fxv[jj][i] = i < p.f_d ? xv[i] : 0.0f;
+        const float4* zv = (const float4*)(p.fzp + g * p.fzp_g + f_sample(pt) * BN + 8 * sg);
+        const float4 z0 = zv[0], z1 = zv[1];
+        fzv[jj][0] = z0.x; fzv[jj][1] = z0.y; fzv[jj][2] = z0.z; fzv[jj][3] = z0.w;
+        fzv[jj][4] = z1.x; fzv[jj][5] = z1.y; fzv[jj][6] = z1.z; fzv[jj][7] = z1.w;
+      }
+    } else {
+      const uint32_t o0 = (uint32_t)(p0 * p.ldx * ES) + sg * 16, o1 = (uint32_t)(p1 * p.ldx * ES) + sg * 16;
+#pragma unroll
+      for (int i = 0; i < XP; ++i) {
+        const char* base = Xb + (p.seg.row0 + (i >> 1) * p.seg.plane) * p.ldx * ES;
+        xb[i] = *(const u32x4*)(base + ((i & 1) ? o1 : o0));
+      }
     }
   };
   auto ncol = [&](int q) { return 32 * wave + 8 * q + 4 * hh; };   // first of the lane's 4 columns in group q
@@ -480,9 +514,57 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
     bout = p.wout[g * p.wo_g + BN];
   }
 
-  auto xstore = [&]() {
+  auto pack8 = [&](const float* v) {
+    u32x4 w;
 #pragma unroll
-    for (int i = 0; i < XP; ++i) *(u32x4*)(xl + (tid / SEGS + RPP * i) * PITCH + sg * 16) = xb[i];
+    for (int h2 = 0; h2 < 4; ++h2) {
+      const T lo = Elem<T>::from_f(v[2 * h2]), hi = Elem<T>::from_f(v[2 * h2 + 1]);
+      w[h2] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+    }
+    return w;
+  };
+  auto xstore = [&](int64_t tile) {
+    if constexpr (GENX) {
+      // first layer, as in the standalone kernel: a = zproj + sum_i W1[:, i] x_i,
+      // h = t, h'_i = s W1[:, i], h''_i = s' W1[:, i]^2 (a' = W1[:, i], a'' = 0)
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        int64_t pt = tile * BM + tid / SEGS + RPP * jj;
+        if (pt >= npts) pt = npts - 1;
+        float a[8], hv[8], s8[8], sp8[8], fwc[3][8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float4 w4 = *(const float4*)(w1l + (8 * sg + e) * 4);
+          fwc[0][e] = w4.x; fwc[1][e] = w4.y; fwc[2][e] = w4.z;
+          a[e] = fzv[jj][e];
+#pragma unroll
+          for (int i = 0; i < 3; ++i) a[e] += fwc[i][e] * fxv[jj][i];
+          float t, sd;
+          tanh_ts(a[e], t, sd);
+          hv[e] = t;
+          s8[e] = sd;
+          sp8[e] = -2.0f * t * sd;
+        }
+        const int row = tid / SEGS + RPP * jj;
+#pragma unroll
+        for (int k = 0; k < C; ++k) {
+          float v[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            if (k == 0) v[e] = hv[e];
+            else if (k <= ND1) v[e] = s8[e] * fwc[k - 1][e];
+            else v[e] = sp8[e] * fwc[k - 1 - ND1][e] * fwc[k - 1 - ND1][e];
+          }
+          const u32x4 w = pack8(v);
+          *(u32x4*)(xl + (k * BM + row) * PITCH + sg * 16) = w;
+          if (p.f_out_h)                           // past the end: the last point's values again
+            *(u32x4*)(p.f_out_h + g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + 8 * sg) = w;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < XP; ++i) *(u32x4*)(xl + (tid / SEGS + RPP * i) * PITCH + sg * 16) = xb[i];
+    }
   };
 
   // The activations of a tile go from registers to LDS at the end of the
@@ -491,7 +573,7 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
   // in issue order, and the same operations are pending on every iteration).
   int64_t tile = blockIdx.x;
   xload(tile);
-  xstore();
+  xstore(tile);
   for (; tile < ntiles; tile += gridDim.x) {
     const int64_t m0 = tile * BM;
     lds_sync();
@@ -500,8 +582,22 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
     // layout of the products (point lane & 31, four columns per group).
     // Issued before the prefetch so that waiting for them (the memory
     // counter drains in issue order) does not wait for the prefetch.
-    u32x2 apr[C][4];
-    if (EPI == EPI_BWD) {
+    u32x2 apr[FIRST ? 1 : C][4];
+    float fzb[16], fxb[3];
+    if (FIRST && EPI == EPI_BWD) {
+      // first layer: z-projection of the lane's 16 units and its coordinates
+      int64_t pt = m0 + (lane & 31);
+      if (pt >= npts) pt = npts - 1;
+      const float* zr = p.fzp + g * p.fzp_g + f_sample(pt) * BN;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 z4 = *(const float4*)(zr + ncol(q));
+        fzb[4 * q] = z4.x; fzb[4 * q + 1] = z4.y; fzb[4 * q + 2] = z4.z; fzb[4 * q + 3] = z4.w;
+      }
+      const float* xv = p.fx + g * p.fx_g + f_xrow(pt) * p.f_d;
+#pragma unroll
+      for (int i = 0; i < 3; ++i) fxb[i] = i < p.f_d ? xv[i] : 0.0f;
+    } else if (EPI == EPI_BWD) {
       int64_t pt = m0 + (lane & 31);
       if (pt >= npts) pt = npts - 1;
       const uint32_t po = (uint32_t)(pt * p.ldo * ES);
@@ -614,25 +710,44 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
       if (p.out_h) stage_out(p.out_h);
     } else {
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int q = 0; q < 4; ++q) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * q + e;
           float gv[C], av[C];
 #pragma unroll
-          for (int k = 0; k < C; ++k) {
-            gv[k] = acc[k][r];
-            const uint32_t w = apr[k][q][e >> 1];
-            const uint16_t h = (e & 1) ? (uint16_t)(w >> 16) : (uint16_t)(w & 0xffffu);
-            av[k] = Elem<T>::to_f(__builtin_bit_cast(T, h));
+          for (int k = 0; k < C; ++k) gv[k] = acc[k][r];
+          if constexpr (FIRST) {
+            // the first layer's pre-activations as the standalone pass stores
+            // them: a (rounded), a'_i = W1[n][i] (rounded), a''_i = 0
+            const float* w1 = w1l + (ncol(q) + e) * 4;
+            float a = fzb[r];
+#pragma unroll
+            for (int i = 0; i < 3; ++i) a += w1[i] * fxb[i];
+            av[0] = Elem<T>::to_f(Elem<T>::from_f(a));
+#pragma unroll
+            for (int i = 0; i < ND1; ++i) av[1 + i] = Elem<T>::to_f(Elem<T>::from_f(w1[i]));
+#pragma unroll
+            for (int i = 0; i < ND2; ++i) av[1 + ND1 + i] = 0.0f;
+          } else {
+#pragma unroll
+            for (int k = 0; k < C; ++k) {
+              const uint32_t w = apr[k][q][e >> 1];
+              const uint16_t h = (e & 1) ? (uint16_t)(w >> 16) : (uint16_t)(w & 0xffffu);
+              av[k] = Elem<T>::to_f(__builtin_bit_cast(T, h));
+            }
           }
           jet_bwd<ND1, ND2>(gv, av);
 #pragma unroll
           for (int k = 0; k < C; ++k) acc[k][r] = gv[k];
         }
+      }
       stage_out(p.out_da);
     }
-    xstore();                                      // the next tile (the region is free again)
+    {
+      const int64_t nx = tile + gridDim.x;
+      xstore(nx < ntiles ? nx : tile);             // the next tile (the region is free again)
+    }
   }
 }
 
@@ -1081,7 +1196,7 @@ namespace {
 // matters more than per-block intensity.)
 }  // namespace
 
-bool nt_fuses_output(int elem_bytes, int C, int K, int N, int64_t n_points, int64_t ldx, int64_t ldo) {
+bool nt_resident_ok(int elem_bytes, int C, int K, int N, int64_t n_points, int64_t ldx, int64_t ldo) {
   const int64_t span = (n_points + 1) * (ldx > ldo ? ldx : ldo) * (int64_t)elem_bytes;
   return elem_bytes == 2 && C >= 1 && C <= 5 && K == 128 && N == 128 && span < ((int64_t)1 << 31);
 }
@@ -1108,18 +1223,19 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   const int64_t npts = a.seg.n_points;
   if (npts <= 0) return hipSuccess;
   if constexpr (sizeof(T) == 2 && C <= 5 && EPI != EPI_DF) {
-    if (nt_fuses_output((int)sizeof(T), C, a.K, a.N, npts, a.ldx, a.ldo)) {
+    if (nt_resident_ok((int)sizeof(T), C, a.K, a.N, npts, a.ldx, a.ldo)) {
       // persistent weight-resident kernel: two blocks per CU in total
       const int64_t ntiles = (npts + 31) / 32;
       int64_t nb = 2 * (int64_t)cu_count() / G;
       if (nb < 1) nb = 1;
       if (nb > ntiles) nb = ntiles;
       dim3 grid((unsigned)nb, 1, G);
-      k_gemm_nt_wr<T, ND1, ND2, EPI><<<grid, 256, 0, st>>>(a, ntiles);
+      if (a.fp1) k_gemm_nt_wr<T, ND1, ND2, EPI, true><<<grid, 256, 0, st>>>(a, ntiles);
+      else k_gemm_nt_wr<T, ND1, ND2, EPI, false><<<grid, 256, 0, st>>>(a, ntiles);
       return hipGetLastError();
     }
   }
-  if (a.y) return hipErrorInvalidValue;           // the output layer is fused only by the resident kernel
+  if (a.y || a.fp1) return hipErrorInvalidValue;  // output / first-layer fusion only in the resident kernel
   if (a.N <= 32) {
     dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 31) / 32)), 1, G);
     k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, (C >= 4 ? 1 : 2)><<<grid, 256, 0, st>>>(a);

@@ -337,9 +337,11 @@ static pigan_status gemm_nt(int epi, int nd1, int nd2, const NtArgs<T>& a, int G
   const double M = (double)C * a.seg.n_points;
   const double flops = 2.0 * M * a.N * a.K * G + (a.y ? 2.0 * M * a.N * G : 0.0);
   const double es = sizeof(T);
-  double bytes = (M * a.K + (double)a.N * a.K) * es * G;
+  // operand X is read unless the first layer is formed in the kernel (then
+  // its activations may be stored instead)
+  double bytes = ((a.fp1 ? (a.f_out_h ? M * a.K : 0.0) : M * a.K) + (double)a.N * a.K) * es * G;
   if (epi == EPI_FWD) bytes += M * a.N * es * G * ((a.out_a ? 1 : 0) + (a.out_h ? 1 : 0)) + (a.y ? M * 4.0 * G : 0.0);
-  else if (epi == EPI_BWD) bytes += 2.0 * M * a.N * es * G;
+  else if (epi == EPI_BWD) bytes += (a.fp1 ? 1.0 : 2.0) * M * a.N * es * G;
   else bytes += M * a.N * 4.0 * G;
   // timing records are keyed by launch shape: one name = one kernel instantiation and size
   char key[64];
@@ -375,6 +377,23 @@ static pigan_status weight_grad(const T* dA, int64_t a_g, int64_t lda, const T* 
 }
 
 // Forward of one generator over a chunk: sensor rows then collocation rows.
+// whether both segments of a generator's chunk run on the resident kernel
+// (then the first and output layers are fused into the hidden GEMMs)
+template <class T>
+static bool resident_net(const NetBuf& nb) {
+  const int W = nb.off.W, C = 1 + nb.nd1 + nb.nd2;
+  return nt_resident_ok((int)sizeof(T), 1, W, W, nb.n_sen, W, W) &&
+         nt_resident_ok((int)sizeof(T), C, W, W, nb.n_col, W, W);
+}
+
+// first-layer source of a second-layer GEMM (coordinates are per segment)
+template <class T>
+static void first_src(NtArgs<T>& a, const float* params, int64_t pg, int in_dim, int d, const float* zp,
+                      int64_t zp_g) {
+  a.fp1 = params; a.fp_g = pg; a.f_in = in_dim; a.f_d = d;
+  a.fzp = zp; a.fzp_g = zp_g;
+}
+
 template <class T>
 static pigan_status gen_chunk_fwd(void* ws, const NetBuf& nb, const float* params, const float* xs, int64_t xs_g,
                                   const float* xc, int64_t xc_g, const float* z, int64_t z_g, int d, int n_z, int Sc,
@@ -387,29 +406,32 @@ static pigan_status gen_chunk_fwd(void* ws, const NetBuf& nb, const float* param
     HIP_TRY(launch_zproj(params, pg, nb.off.in_dim, d, W, z, z_g, n_z, Sc, tp<float>(ws, nb.zp), (int64_t)Sc * W, G,
                          st));
   }
-  FirstArgs<T> fa{};
-  fa.p1 = params; fa.p_g = pg; fa.in_dim = nb.off.in_dim; fa.d = d; fa.W = W;
-  fa.zp = tp<float>(ws, nb.zp); fa.zp_g = (int64_t)Sc * W;
-  fa.out_a = tp<T>(ws, nb.A[1]); fa.out_h = tp<T>(ws, nb.H[1]); fa.o_g = actg; fa.ldo = W;
-  // sensors: shared locations, value stream only
-  fa.x = xs; fa.x_g = xs_g; fa.x_shared = 1; fa.Pn = nb.n_s;
-  fa.seg = Seg{nb.n_sen, 0, 0};
-  {
-    ProfScope ps(st, "first_fwd", 2.0 * nb.n_sen * W * d * G, (double)nb.n_sen * W * 2 * sizeof(T) * G);
-    HIP_TRY(launch_first_fwd<T>(0, 0, fa, G, st));
+  // On the resident kernel the first layer is formed inside the second
+  // layer's GEMM (its pre-activations are never stored; its activations are,
+  // for the weight gradient), and the output layer rides on the last hidden
+  // layer's epilogue (the last activations are never stored).
+  const bool resident = L >= 2 && resident_net<T>(nb);
+  if (!resident) {
+    FirstArgs<T> fa{};
+    fa.p1 = params; fa.p_g = pg; fa.in_dim = nb.off.in_dim; fa.d = d; fa.W = W;
+    fa.zp = tp<float>(ws, nb.zp); fa.zp_g = (int64_t)Sc * W;
+    fa.out_a = tp<T>(ws, nb.A[1]); fa.out_h = tp<T>(ws, nb.H[1]); fa.o_g = actg; fa.ldo = W;
+    // sensors: shared locations, value stream only
+    fa.x = xs; fa.x_g = xs_g; fa.x_shared = 1; fa.Pn = nb.n_s;
+    fa.seg = Seg{nb.n_sen, 0, 0};
+    {
+      ProfScope ps(st, "first_fwd", 2.0 * nb.n_sen * W * d * G, (double)nb.n_sen * W * 2 * sizeof(T) * G);
+      HIP_TRY(launch_first_fwd<T>(0, 0, fa, G, st));
+    }
+    fa.x = xc; fa.x_g = xc_g; fa.x_shared = 0; fa.Pn = P;
+    fa.seg = Seg{nb.n_col, nb.n_sen, nb.n_col};
+    {
+      const int C = 1 + nb.nd1 + nb.nd2;
+      ProfScope ps(st, "first_fwd", 2.0 * nb.n_col * W * d * G, (double)nb.n_col * C * W * 2 * sizeof(T) * G);
+      HIP_TRY(launch_first_fwd<T>(nb.nd1, nb.nd2, fa, G, st));
+    }
   }
-  fa.x = xc; fa.x_g = xc_g; fa.x_shared = 0; fa.Pn = P;
-  fa.seg = Seg{nb.n_col, nb.n_sen, nb.n_col};
-  {
-    const int C = 1 + nb.nd1 + nb.nd2;
-    ProfScope ps(st, "first_fwd", 2.0 * nb.n_col * W * d * G, (double)nb.n_col * C * W * 2 * sizeof(T) * G);
-    HIP_TRY(launch_first_fwd<T>(nb.nd1, nb.nd2, fa, G, st));
-  }
-  // the output layer rides on the last hidden layer's epilogue where the
-  // kernel supports it (then the last activations are never stored)
-  const int C = 1 + nb.nd1 + nb.nd2;
-  const bool fuse_out = L >= 2 && nt_fuses_output((int)sizeof(T), 1, W, W, nb.n_sen, W, W) &&
-                        nt_fuses_output((int)sizeof(T), C, W, W, nb.n_col, W, W);
+  const bool fuse_out = resident;
   for (int l = 2; l <= L; ++l) {
     NtArgs<T> a{};
     a.X = tp<T>(ws, nb.H[l - 1]); a.x_g = actg; a.ldx = W;
@@ -420,11 +442,17 @@ static pigan_status gen_chunk_fwd(void* ws, const NetBuf& nb, const float* param
       a.out_h = nullptr;
       a.y = tp<float>(ws, nb.jet); a.y_g = nb.R; a.wout = params + nb.off.wout; a.wo_g = pg;
     }
+    if (l == 2 && resident) {
+      first_src(a, params, pg, nb.off.in_dim, d, tp<float>(ws, nb.zp), (int64_t)Sc * W);
+      a.f_out_h = tp<T>(ws, nb.H[1]);
+    }
     a.N = W; a.K = W;
     a.seg = Seg{nb.n_sen, 0, 0};
+    a.fx = xs; a.fx_g = xs_g; a.fx_shared = 1; a.fPn = nb.n_s;
     pigan_status s1 = gemm_nt<T>(EPI_FWD, 0, 0, a, G, st, "gemm_fwd");
     if (s1 != PIGAN_OK) return s1;
     a.seg = Seg{nb.n_col, nb.n_sen, nb.n_col};
+    a.fx = xc; a.fx_g = xc_g; a.fx_shared = 0; a.fPn = P;
     s1 = gemm_nt<T>(EPI_FWD, nb.nd1, nb.nd2, a, G, st, "gemm_fwd");
     if (s1 != PIGAN_OK) return s1;
   }
@@ -472,11 +500,15 @@ static pigan_status gen_chunk_bwd(void* ws, const StepPlan& pl, const NetBuf& nb
     a.X = tp<T>(ws, nb.dA[cur]); a.x_g = actg; a.ldx = W;
     a.Wm = tp<T>(ws, nb.wcT) + (size_t)(l - 2) * W * W; a.w_g = (int64_t)std::max(L - 1, 1) * W * W; a.ldw = W;
     a.aprev = tp<T>(ws, nb.A[l - 1]); a.out_da = tp<T>(ws, nb.dA[1 - cur]); a.o_g = actg; a.ldo = W;
+    if (l == 2 && resident_net<T>(nb))             // the first layer's pre-activations were never stored
+      first_src(a, params, pg, nb.off.in_dim, d, tp<float>(ws, nb.zp), (int64_t)Sc * W);
     a.N = W; a.K = W;
     a.seg = Seg{nb.n_sen, 0, 0};
+    a.fx = xs; a.fx_g = xs_g; a.fx_shared = 1; a.fPn = nb.n_s;
     s1 = gemm_nt<T>(EPI_BWD, 0, 0, a, G, st, "gemm_bwd");
     if (s1 != PIGAN_OK) return s1;
     a.seg = Seg{nb.n_col, nb.n_sen, nb.n_col};
+    a.fx = xc; a.fx_g = xc_g; a.fx_shared = 0; a.fPn = P;
     s1 = gemm_nt<T>(EPI_BWD, nb.nd1, nb.nd2, a, G, st, "gemm_bwd");
     if (s1 != PIGAN_OK) return s1;
     cur = 1 - cur;
@@ -771,17 +803,20 @@ static pigan_status run_gen_fwd(const pigan_mlp* net, const float* params, int d
     HIP_TRY(launch_zproj(params, off.n, in_dim, d, W, z, (int64_t)S * n_z, n_z, S, tp<float>(ws, p.zp),
                          (int64_t)S * W, G, st));
   }
-  FirstArgs<T> fa{};
-  fa.p1 = params; fa.p_g = off.n; fa.in_dim = in_dim; fa.d = d; fa.W = W;
-  fa.zp = tp<float>(ws, p.zp); fa.zp_g = (int64_t)S * W;
-  fa.x = x; fa.x_g = x_shared ? (int64_t)P * d : M * d; fa.x_shared = x_shared ? 1 : 0; fa.Pn = P;
-  fa.out_a = nullptr; fa.out_h = tp<T>(ws, p.h[0]); fa.o_g = actg; fa.ldo = W;
-  fa.seg = Seg{M, 0, M};
-  {
+  // on the resident kernel the first layer is formed inside the second
+  // layer's GEMM and the output layer rides on the last one's epilogue
+  const bool fuse_out = L >= 2 && nt_resident_ok((int)sizeof(T), 1 + nd1 + nd2, W, W, M, W, W);
+  const int64_t x_g = x_shared ? (int64_t)P * d : M * d;
+  if (!fuse_out) {
+    FirstArgs<T> fa{};
+    fa.p1 = params; fa.p_g = off.n; fa.in_dim = in_dim; fa.d = d; fa.W = W;
+    fa.zp = tp<float>(ws, p.zp); fa.zp_g = (int64_t)S * W;
+    fa.x = x; fa.x_g = x_g; fa.x_shared = x_shared ? 1 : 0; fa.Pn = P;
+    fa.out_a = nullptr; fa.out_h = tp<T>(ws, p.h[0]); fa.o_g = actg; fa.ldo = W;
+    fa.seg = Seg{M, 0, M};
     ProfScope ps(st, "first_fwd", 2.0 * M * W * d * G, (double)M * (1 + nd1 + nd2) * W * sizeof(T) * G);
     HIP_TRY(launch_first_fwd<T>(nd1, nd2, fa, G, st));
   }
-  const bool fuse_out = L >= 2 && nt_fuses_output((int)sizeof(T), 1 + nd1 + nd2, W, W, M, W, W);
   int cur = 0;
   for (int l = 2; l <= L; ++l) {
     NtArgs<T> a{};
@@ -792,6 +827,10 @@ static pigan_status run_gen_fwd(const pigan_mlp* net, const float* params, int d
     if (l == L && fuse_out) {
       a.out_h = nullptr;
       a.y = jet; a.y_g = p.R; a.wout = params + off.wout; a.wo_g = off.n;
+    }
+    if (l == 2 && fuse_out) {
+      first_src(a, params, off.n, in_dim, d, tp<float>(ws, p.zp), (int64_t)S * W);
+      a.fx = x; a.fx_g = x_g; a.fx_shared = x_shared ? 1 : 0; a.fPn = P;
     }
     a.N = W; a.K = W; a.seg = Seg{M, 0, M};
     pigan_status s1 = gemm_nt<T>(EPI_FWD, nd1, nd2, a, G, st, "gemm_fwd");
