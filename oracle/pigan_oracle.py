@@ -24,6 +24,9 @@ the definitions state):
 * WGAN critic losses per subdomain group, weighted by the subdomain weight
   (Sec. III.B.1): L_D = w (mean D(fake) - mean D(real)),
   L_adv = -w mean D(fake), L_pde = w lambda mean r^2, L_G = L_adv + L_pde.
+* Optionally the critic's gradient penalty (the WGAN-GP member of the WGAN
+  family the paper cites): P = w lambda_gp mean_b (||grad_v D(x_b)|| - 1)^2 at
+  x_b = eps_b R_b + (1 - eps_b) F_b, added to L_D.
 * Exact weight gradients of L_D (discriminator) and L_G (both generators) by
   an explicit reverse pass.  Losses are means, so the step is additive over
   sample chunks, the same identity the paper uses to fold subdomain losses into
@@ -321,6 +324,89 @@ def mlp_backward(params, shape, cache, g_y, want_input_grad: bool = False, prec=
 
 
 # ----------------------------------------------------------------------------
+# gradient penalty of the critic (optional term of the critic loss)
+# ----------------------------------------------------------------------------
+# The paper trains WGAN critics and cites the gradient-penalty variant of that
+# family (Sec. II, Sec. III.B.1) without writing it out.  Its definition:
+#   x_b = eps_b R_b + (1 - eps_b) F_b                (one pair per row b)
+#   P   = w lambda_gp mean_b (||grad_v D(x_b)||_2 - 1)^2
+# is added to the critic loss L_D, and its gradient to the critic weights.
+
+def critic_input_grad(params, shape, V, prec=None):
+    """g_b = dD/dv at every row v_b of V: the reverse pass of D to its input."""
+    num = prec if isinstance(prec, _Num) else _Num(prec)
+    _, cache = mlp_forward(params, shape, V, keep=True, prec=num)
+    _, g = mlp_backward(params, shape, cache, np.ones(np.asarray(V).shape[0], F64), want_input_grad=True,
+                        prec=num)
+    return g
+
+
+def tangent_output_grad(params, shape, V, Cdir, prec=None):
+    """Weight gradient of J = sum_b dD(v_b + t c_b)/dt |_{t=0}.
+
+    The directional derivative is carried forward with the activations
+    (h, h_dot), h_dot_0 = c:  a = W h + b,  a_dot = W h_dot,  h = tanh(a),
+    h_dot = s a_dot  (s = 1 - tanh^2);  J = sum_b w_out . h_dot_L.  Its
+    reverse pass, with s' = ds/da = -2 t s:
+      g_a     = s g_h + s' a_dot g_hdot,     g_adot = s g_hdot,
+      dJ/dW_l = g_a^T h_{l-1} + g_adot^T h_dot_{l-1},  dJ/db_l = sum_b g_a,
+      g_h(l-1) = g_a W_l,  g_hdot(l-1) = g_adot W_l;
+    at the top g_h = 0, g_hdot = w_out, dJ/dw_out = sum_b h_dot_L, dJ/db_out = 0."""
+    in_dim, L, W = shape
+    num = prec if isinstance(prec, _Num) else _Num(prec)
+    q = num.q
+    layers, w_out, b_out = unpack(params, in_dim, L, W)
+    h = q(np.asarray(V, F64))
+    hd = q(np.asarray(Cdir, F64))
+    hs, hds, ts, ads = [h], [hd], [], []
+    for Wl, bl in layers:
+        Wq = q(Wl)
+        a = q(num.mm(h, Wq.T) + bl)
+        ad = q(num.mm(hd, Wq.T))
+        t = np.tanh(a)
+        h = q(t)
+        hd = q((1.0 - t * t) * ad)
+        ts.append(t)
+        ads.append(ad)
+        hs.append(h)
+        hds.append(hd)
+    gw_out = hds[-1].sum(axis=0)
+    g_h = np.zeros_like(hs[-1])
+    g_hd = np.tile(w_out, (hs[-1].shape[0], 1))
+    grads = [None] * L
+    for l in reversed(range(L)):
+        t, ad = ts[l], ads[l]
+        sl = 1.0 - t * t
+        g_a = q(sl * g_h - 2.0 * t * sl * ad * g_hd)
+        g_ad = q(sl * g_hd)
+        grads[l] = (num.mm(g_a.T, hs[l]) + num.mm(g_ad.T, hds[l]), num.colsum(g_a))
+        Wq = q(layers[l][0])
+        g_h = num.mm(g_a, Wq)
+        g_hd = num.mm(g_ad, Wq)
+    return pack(grads, gw_out, 0.0)
+
+
+def gradient_penalty(params, shape, F, R, eps, lambda_gp, w=1.0, n_total=None, prec=None):
+    """P (summed over these pairs with the 1/n_total of the mean) and dP/dphi.
+
+    dP/dphi = sum_b c_b . dg_b/dphi with c_b = dP/dg_b held fixed, and
+    c_b . g_b is the directional derivative of D at x_b along c_b, so dP/dphi
+    is tangent_output_grad along c.  A row with g_b = 0 has no gradient
+    direction; it contributes P but no weight gradient."""
+    num = prec if isinstance(prec, _Num) else _Num(prec)
+    eps = np.asarray(eps, F64)[:, None]
+    X = num.q(eps * np.asarray(R, F64) + (1.0 - eps) * np.asarray(F, F64))
+    n = X.shape[0] if n_total is None else n_total
+    g = critic_input_grad(params, shape, X, prec=num)
+    nrm = np.sqrt((g * g).sum(axis=1))
+    P = w * lambda_gp * float(((nrm - 1.0) ** 2).sum()) / n
+    with np.errstate(divide="ignore", invalid="ignore"):
+        coef = np.where(nrm > 0, (nrm - 1.0) / nrm, 0.0)
+    Cdir = (2.0 * w * lambda_gp / n) * coef[:, None] * g
+    return P, tangent_output_grad(params, shape, X, Cdir, prec=num)
+
+
+# ----------------------------------------------------------------------------
 # Darcy residual (Eq. 1 with k = exp(Y), Eq. 2)
 # ----------------------------------------------------------------------------
 
@@ -384,13 +470,16 @@ def snapshots(pY, pU, shape, d, xsY, xsU, z):
 # ----------------------------------------------------------------------------
 
 def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
-                     w=1.0, lambda_pde=1.0, chunk_S=None, prec=None):
+                     w=1.0, lambda_pde=1.0, chunk_S=None, prec=None, lambda_gp=0.0, gp_eps=None):
     """One subdomain group's losses and gradients.
 
-    Returns dict(L_D, L_adv, L_pde, gY, gU, gD) with gradients of
+    Returns dict(L_D, L_adv, L_pde, gY, gU, gD, P_gp) with gradients of
     L_D (discriminator weights) and of L_G = L_adv + L_pde (generator weights).
     ``f`` is an [S, P] array.  Samples are processed in chunks of ``chunk_S``
     (all at once by default); the result does not depend on the chunking.
+    With lambda_gp > 0 the gradient penalty on the pairs (F_b, R_b),
+    b < min(S, B), with mixing weights gp_eps[b] is added to L_D (and reported
+    as P_gp) and its gradient to the critic weights.
     """
     z = np.asarray(z, F64)
     xc = np.asarray(xc, F64)
@@ -403,7 +492,8 @@ def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
     if prec == "fp32":
         with _working_type(np.float32):
             return train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real, w=w,
-                                    lambda_pde=lambda_pde, chunk_S=chunk_S, prec=None)
+                                    lambda_pde=lambda_pde, chunk_S=chunk_S, prec=None, lambda_gp=lambda_gp,
+                                    gp_eps=gp_eps)
     num = _Num(prec)
 
     gY = np.zeros(np.asarray(pY).size, F64)
@@ -411,6 +501,8 @@ def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
     gD = np.zeros(np.asarray(pD).size, F64)
     sum_DF = 0.0
     sum_r2 = 0.0
+    P_gp = 0.0
+    n_gp = min(S, B)
 
     # real snapshots: dL_D/dD(real_b) = -w/B
     DR, hsR = mlp_forward(pD, dshape, real, keep=True, prec=num)
@@ -439,6 +531,14 @@ def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
         sum_DF += float(DF.sum())
         gDc, gF = mlp_backward(pD, dshape, hsF, np.full(Sc, w / S, F64), want_input_grad=True, prec=num)
         gD += gDc
+        # --- gradient penalty on this chunk's pairs (F_b, R_b), b < n_gp
+        if lambda_gp != 0.0:
+            b1 = min(n_gp, s0 + Sc)
+            if b1 > s0:
+                Pc, gPc = gradient_penalty(pD, dshape, F[:b1 - s0], real[s0:b1], np.asarray(gp_eps, F64)[s0:b1],
+                                           lambda_gp, w=w, n_total=n_gp, prec=num)
+                P_gp += Pc
+                gD += gPc
         # L_adv = -w mean D(F): its snapshot cotangent is the negated L_D one
         gF = -gF
         # --- residual cotangents: dL_pde/dr = 2 w lambda r / (S P)
@@ -455,16 +555,17 @@ def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
         gY += gen_backward(pY, gshape, d, XC, ZC, jY, g_Yval, g_Ydy, prec=num)
         gU += gen_backward(pU, gshape, d, XC, ZC, jU, g_Uval, g_Udy, g_Uddy, prec=num)
 
-    L_D = w * (sum_DF / S - sum_DR / B)
+    L_D = w * (sum_DF / S - sum_DR / B) + P_gp
     L_adv = -w * sum_DF / S
     L_pde = w * lambda_pde * sum_r2 / (S * P)
-    return dict(L_D=L_D, L_adv=L_adv, L_pde=L_pde, gY=gY, gU=gU, gD=gD)
+    return dict(L_D=L_D, L_adv=L_adv, L_pde=L_pde, gY=gY, gU=gU, gD=gD, P_gp=P_gp)
 
 
-def train_step(wl, inp, real, lambda_pde=None, chunk_S=None, prec=None):
+def train_step(wl, inp, real, lambda_pde=None, chunk_S=None, prec=None, lambda_gp=0.0, gp_eps=None):
     """All groups of a workload.  ``inp`` is an inputs.StepInputs-like object,
     ``real`` the real snapshots [G, B_r, n_in].  Returns dict of stacked arrays:
-    loss [G, 3] (L_D, L_adv, L_pde), gY [G, nY], gU [G, nU], gD [G, nD]."""
+    loss [G, 3] (L_D, L_adv, L_pde), gY [G, nY], gU [G, nU], gD [G, nD], and
+    P_gp [G] (the gradient penalty, included in L_D; gp_eps is [G, min(S, B_r)])."""
     lam = wl.lambda_pde if lambda_pde is None else lambda_pde
     gshape = (wl.d + wl.n_z, wl.L, wl.W)
     dshape = (wl.n_sY + wl.n_sU, wl.L_D, wl.W_D)
@@ -476,11 +577,13 @@ def train_step(wl, inp, real, lambda_pde=None, chunk_S=None, prec=None):
         outs.append(train_step_group(gshape, dshape, wl.d, inp.pY[g], inp.pU[g], inp.pD[g],
                                      inp.z[g], inp.xc[g], inp.xsY[g], inp.xsU[g], f, real[g],
                                      w=float(inp.w_group[g]), lambda_pde=lam, chunk_S=chunk_S,
-                                     prec=prec))
+                                     prec=prec, lambda_gp=lambda_gp,
+                                     gp_eps=None if gp_eps is None else gp_eps[g]))
     return dict(loss=np.array([[o["L_D"], o["L_adv"], o["L_pde"]] for o in outs]),
                 gY=np.stack([o["gY"] for o in outs]),
                 gU=np.stack([o["gU"] for o in outs]),
-                gD=np.stack([o["gD"] for o in outs]))
+                gD=np.stack([o["gD"] for o in outs]),
+                P_gp=np.array([o["P_gp"] for o in outs]))
 
 
 def real_snapshots(wl, inp):
