@@ -156,7 +156,9 @@ typedef struct {
   int32_t chunk_S;             /* samples per chunk, 0 = automatic */
   pigan_dtype dt;
   float lambda_pde;            /* weight of the residual penalty (>= 0) */
-  float lambda_gp;             /* gradient-penalty weight: must be 0 (not implemented) */
+  float lambda_gp;             /* critic gradient-penalty weight (>= 0); must be 0 for
+                                  pigan_train_step_grads (ENOTSUP otherwise), any value for
+                                  pigan_train_step_grads_gp */
   float loss_scale;            /* static loss scale (> 0; 1 unless fp16) */
 } pigan_step_desc;
 
@@ -180,6 +182,30 @@ pigan_status pigan_train_step_grads(const pigan_step_desc* s, const float* pY, c
                                     float f_const, const float* real, const float* w_group,
                                     float* gY, float* gU, float* gD, float* loss,
                                     int32_t* nonfinite, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * pigan_train_step_grads plus the critic's gradient penalty, the member of the
+ * WGAN family the paper cites for its critics (Sec. I.C, Sec. II.C):
+ *   x_b = eps_b real_b + (1 - eps_b) F_b,   b < n_gp = min(S, B_r)
+ *         (fake snapshot b is noise sample b),
+ *   P_g = w_g lambda_gp mean_b (||grad_v D(x_b)||_2 - 1)^2.
+ * P_g is added to L_D (loss[g][0]) and its gradient to gD; gY and gU are
+ * unchanged.  The weight gradient is the reverse pass of the critic's
+ * directional derivative along c_b = dP/d(grad_v D(x_b)) (a pair whose input
+ * gradient is exactly zero contributes to P but not to the gradient).
+ *   gp_eps : [G, n_gp] fp32 mixing weights (device), required when
+ *            lambda_gp > 0 (EINVAL if NULL); unused when lambda_gp = 0.
+ *   gp     : [G] fp32 output P_g (device) or NULL.
+ * Everything else as pigan_train_step_grads; pigan_workspace_bytes accounts
+ * for the penalty's buffers when lambda_gp > 0.
+ */
+pigan_status pigan_train_step_grads_gp(const pigan_step_desc* s, const float* pY, const float* pU,
+                                       const float* pD, const float* z, const float* xc,
+                                       const float* xsY, const float* xsU, const float* f,
+                                       float f_const, const float* real, const float* w_group,
+                                       const float* gp_eps, float* gY, float* gU, float* gD,
+                                       float* loss, float* gp, int32_t* nonfinite, void* ws,
+                                       size_t ws_bytes, void* stream);
 
 /* Thread-local description of the last non-OK status ("" if none). */
 const char* pigan_last_error(void);

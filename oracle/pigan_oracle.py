@@ -326,8 +326,8 @@ def mlp_backward(params, shape, cache, g_y, want_input_grad: bool = False, prec=
 # ----------------------------------------------------------------------------
 # gradient penalty of the critic (optional term of the critic loss)
 # ----------------------------------------------------------------------------
-# The paper trains WGAN critics and cites the gradient-penalty variant of that
-# family (Sec. II, Sec. III.B.1) without writing it out.  Its definition:
+# The paper trains WGAN critics and cites the gradient-penalty member of that
+# family (Sec. I.C, Sec. II.C) without writing it out.  Its definition:
 #   x_b = eps_b R_b + (1 - eps_b) F_b                (one pair per row b)
 #   P   = w lambda_gp mean_b (||grad_v D(x_b)||_2 - 1)^2
 # is added to the critic loss L_D, and its gradient to the critic weights.

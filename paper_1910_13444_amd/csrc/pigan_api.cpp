@@ -190,6 +190,7 @@ struct StepPlan {
   NetBuf Y, U;
   DiscBuf D;
   size_t dwp = 0, dwdb = 0, rpart = 0, acc = 0;
+  size_t gpg = 0, gpp = 0;   // gradient penalty: critic input gradients [Sc x n_in] fp32, row terms [Sc] fp64
   int64_t dwp_floats = 0, dwdb_floats = 0;
   int rblocks = 0;
   size_t total = 0;
@@ -283,6 +284,10 @@ static void plan_step(const pigan_step_desc* s, int Sc, StepPlan& pl) {
   pl.rblocks = residual_blocks((int64_t)Sc * s->P);
   pl.rpart = cv.take((size_t)pl.rblocks * 8 * G);
   pl.acc = cv.take((size_t)4 * 8 * G);
+  if (s->lambda_gp > 0.0f) {
+    pl.gpg = cv.take((size_t)Sc * s->disc.in_dim * 4 * G);
+    pl.gpp = cv.take((size_t)Sc * 8 * G);
+  }
   pl.total = round_up((int64_t)cv.off, 256);
 }
 
@@ -299,7 +304,7 @@ static int choose_chunk(const pigan_step_desc* s) {
   }
 }
 
-static pigan_status check_step(const pigan_step_desc* s) {
+static pigan_status check_step(const pigan_step_desc* s, bool gp_entry = false) {
   if (!s) return fail(PIGAN_EINVAL, "null step descriptor");
   pigan_status st;
   if ((st = check_mlp(&s->genY, "genY")) != PIGAN_OK) return st;
@@ -320,7 +325,10 @@ static pigan_status check_step(const pigan_step_desc* s) {
   if (s->chunk_S < 0) return fail(PIGAN_EINVAL, "chunk_S=%d must be >= 0", s->chunk_S);
   if (!(s->lambda_pde >= 0.0f) || !__builtin_isfinite(s->lambda_pde))
     return fail(PIGAN_EINVAL, "lambda_pde must be finite and >= 0");
-  if (s->lambda_gp != 0.0f) return fail(PIGAN_ENOTSUP, "lambda_gp != 0: gradient penalty not implemented");
+  if (!(s->lambda_gp >= 0.0f) || !__builtin_isfinite(s->lambda_gp))
+    return fail(PIGAN_EINVAL, "lambda_gp must be finite and >= 0");
+  if (!gp_entry && s->lambda_gp != 0.0f)
+    return fail(PIGAN_ENOTSUP, "lambda_gp != 0 needs the per-pair mixing weights: use pigan_train_step_grads_gp");
   if (!(s->loss_scale > 0.0f) || !__builtin_isfinite(s->loss_scale))
     return fail(PIGAN_EINVAL, "loss_scale must be finite and > 0");
   return PIGAN_OK;
@@ -537,11 +545,132 @@ static pigan_status cast_gen_weights(void* ws, const NetBuf& nb, const float* pa
   return PIGAN_OK;
 }
 
+// discriminator forward over `seg` (nd1 = 1: value and one tangent stream)
+template <class T>
+static pigan_status disc_forward(void* ws, const DiscBuf& D, const float* pD, int WD, int LD, Seg seg, int nd1,
+                                 int G, hipStream_t st, const char* name) {
+  const int64_t dact = D.Bmax * WD;
+  for (int l = 1; l <= LD; ++l) {
+    NtArgs<T> a{};
+    if (l == 1) {
+      a.X = tp<T>(ws, D.X0); a.x_g = D.Bmax * D.Kp; a.ldx = D.Kp;
+      a.Wm = tp<T>(ws, D.w1); a.w_g = (int64_t)WD * D.Kp; a.ldw = D.Kp; a.K = D.Kp;
+    } else {
+      a.X = tp<T>(ws, D.H[l - 1]); a.x_g = dact; a.ldx = WD;
+      a.Wm = tp<T>(ws, D.wc) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD;
+      a.ldw = WD; a.K = WD;
+    }
+    a.bias = pD + D.off.b[l]; a.b_g = D.off.n;
+    a.out_a = tp<T>(ws, D.A[l]); a.out_h = tp<T>(ws, D.H[l]); a.o_g = dact; a.ldo = WD;
+    a.N = WD;
+    a.seg = seg;
+    pigan_status r = gemm_nt<T>(EPI_FWD, nd1, 0, a, G, st, name);
+    if (r != PIGAN_OK) return r;
+  }
+  return PIGAN_OK;
+}
+
+// Critic gradient penalty on the pairs b0..b0+n-1 of this chunk (fake row i is
+// the chunk's sample i):  P = w lambda_gp / n_gp sum_b (|g_b| - 1)^2 with
+// g_b = dD/dv at x_b = eps_b R_b + (1 - eps_b) F_b.  dP/dphi = sum_b c_b .
+// dg_b/dphi with c_b = dP/dg_b fixed, and c_b . g_b is the directional
+// derivative of D at x_b along c_b: so the weight gradient is the reverse
+// pass of a (value, tangent) jet of D seeded with (x_b, c_b), with cotangent
+// 1 on the tangent output.  Added to gD; the row terms go to acc[g][3].
+template <class T>
+static pigan_status critic_penalty(void* ws, const StepPlan& pl, const pigan_step_desc* s, const float* pD,
+                                   const NetBuf& Yc, const NetBuf& Uc, const float* real, const float* gp_eps,
+                                   const float* w_group, int b0, int n, float* gD, float inv, int32_t* nonfinite,
+                                   double* acc, int G, hipStream_t st) {
+  const DiscBuf& D = pl.D;
+  const int WD = s->disc.width, LD = s->disc.n_hidden, n_in = s->disc.in_dim;
+  const int64_t dact = D.Bmax * WD, xg = D.Bmax * D.Kp;
+  const int n_gp = std::min(s->S, s->B_r);
+  const int64_t gg = (int64_t)pl.Sc * n_in;
+  pigan_status r;
+  {
+    ProfScope ps(st, "gp_misc", 0.0, 0.0);
+    HIP_TRY(launch_gp_mix<T>(tp<float>(ws, Yc.jet), Yc.R, tp<float>(ws, Uc.jet), Uc.R, s->n_sY, s->n_sU, real,
+                             (int64_t)s->B_r * n_in, gp_eps, n_gp, b0, n, n_in, tp<T>(ws, D.X0), xg, D.Kp, G, st));
+    HIP_TRY(launch_fill2(tp<float>(ws, D.seed), D.Bmax, n, 1.0f, 0.0f, 0, G, st));
+  }
+  // 1. D on the interpolates, then its reverse pass to the input: g = dD/dv
+  if ((r = disc_forward<T>(ws, D, pD, WD, LD, Seg{n, 0, 0}, 0, G, st, "gp_fwd")) != PIGAN_OK) return r;
+  OutBwdArgs<T> ob{};
+  ob.A = tp<T>(ws, D.A[LD]); ob.dA = tp<T>(ws, D.dA[0]); ob.o_g = dact; ob.ldo = WD;
+  ob.gbar = tp<float>(ws, D.seed); ob.gb_g = D.Bmax;
+  ob.wout = pD + D.off.wout; ob.w_g = D.off.n;
+  ob.W = WD; ob.ppb = D.ppb; ob.part = tp<double>(ws, D.ob); ob.n_slots = out_bwd_blocks(n, (int)D.ppb);
+  ob.slot0 = 0; ob.seg = Seg{n, 0, 0};
+  {
+    ProfScope ps(st, "gp_bwd", 0.0, (double)n * WD * 2 * sizeof(T) * G);
+    HIP_TRY(launch_out_bwd<T>(0, 0, ob, G, st));   // (its output-weight partials are not used)
+  }
+  int cur = 0;
+  for (int l = LD; l >= 2; --l) {
+    NtArgs<T> a{};
+    a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
+    a.Wm = tp<T>(ws, D.wcT) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD; a.ldw = WD;
+    a.aprev = tp<T>(ws, D.A[l - 1]); a.out_da = tp<T>(ws, D.dA[1 - cur]); a.o_g = dact; a.ldo = WD;
+    a.N = WD; a.K = WD; a.seg = Seg{n, 0, 0};
+    if ((r = gemm_nt<T>(EPI_BWD, 0, 0, a, G, st, "gp_bwd")) != PIGAN_OK) return r;
+    cur = 1 - cur;
+  }
+  {
+    NtArgs<T> a{};
+    a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
+    a.Wm = tp<T>(ws, D.w1T); a.w_g = (int64_t)WD * D.Kp; a.ldw = WD;
+    a.N = D.Kp; a.K = WD; a.seg = Seg{n, 0, 0};
+    a.seedY = tp<float>(ws, pl.gpg); a.sY_g = gg; a.seedU = nullptr; a.sU_g = 0;
+    a.nY = n_in; a.nU = 0; a.df_sign = 1.0f;
+    if ((r = gemm_nt<T>(EPI_DF, 0, 0, a, G, st, "gp_bwd")) != PIGAN_OK) return r;
+  }
+  // 2. row terms (|g| - 1)^2 and tangent rows c = dP/dg (times the loss scale)
+  {
+    ProfScope ps(st, "gp_misc", 0.0, 0.0);
+    const float scale = (float)(2.0 * s->lambda_gp * s->loss_scale / n_gp);
+    HIP_TRY(launch_gp_norm<T>(tp<float>(ws, pl.gpg), gg, n, n_in, w_group, scale, tp<double>(ws, pl.gpp), n,
+                              tp<T>(ws, D.X0), xg, D.Kp, G, st));
+    HIP_TRY(launch_sum_partials(tp<double>(ws, pl.gpp), n, acc, 4, 3, G, st));
+    HIP_TRY(launch_fill2(tp<float>(ws, D.seed), D.Bmax, n, 0.0f, 1.0f, 1, G, st));
+  }
+  // 3. (value, tangent) jet of D and its reverse pass with cotangent 1 on the
+  //    tangent output: the weight gradient of the penalty
+  if ((r = disc_forward<T>(ws, D, pD, WD, LD, Seg{n, 0, n}, 1, G, st, "gp_fwd")) != PIGAN_OK) return r;
+  ob.A = tp<T>(ws, D.A[LD]); ob.dA = tp<T>(ws, D.dA[0]);
+  ob.n_slots = out_bwd_blocks(n, (int)D.ppb);     // blocks run over points, every stream of a point in one
+  ob.seg = Seg{n, 0, n};
+  {
+    ProfScope ps(st, "gp_bwd", 0.0, (double)2 * n * WD * 2 * sizeof(T) * G);
+    HIP_TRY(launch_out_bwd<T>(1, 0, ob, G, st));
+    HIP_TRY(launch_colsum<double>(tp<double>(ws, D.ob), (int64_t)ob.n_slots * (WD + 1), ob.n_slots, WD + 1, WD + 1,
+                                  1, 1, gD + D.off.wout, D.off.n, 1, inv, nonfinite, G, st));
+  }
+  cur = 0;
+  for (int l = LD; l >= 2; --l) {
+    if ((r = weight_grad<T>(tp<T>(ws, D.dA[cur]), dact, WD, tp<T>(ws, D.H[l - 1]), dact, WD, 2 * (int64_t)n, n, WD,
+                            WD, WD, gD + D.off.w[l], gD + D.off.b[l], D.off.n, 1, inv, nonfinite,
+                            tp<float>(ws, pl.dwp), tp<double>(ws, pl.dwdb), G, st)) != PIGAN_OK)
+      return r;
+    NtArgs<T> a{};
+    a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
+    a.Wm = tp<T>(ws, D.wcT) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD; a.ldw = WD;
+    a.aprev = tp<T>(ws, D.A[l - 1]); a.out_da = tp<T>(ws, D.dA[1 - cur]); a.o_g = dact; a.ldo = WD;
+    a.N = WD; a.K = WD; a.seg = Seg{n, 0, n};
+    if ((r = gemm_nt<T>(EPI_BWD, 1, 0, a, G, st, "gp_bwd")) != PIGAN_OK) return r;
+    cur = 1 - cur;
+  }
+  return weight_grad<T>(tp<T>(ws, D.dA[cur]), dact, WD, tp<T>(ws, D.X0), xg, D.Kp, 2 * (int64_t)n, n, WD, D.Kp,
+                        n_in, gD + D.off.w[1], gD + D.off.b[1], D.off.n, 1, inv, nonfinite, tp<float>(ws, pl.dwp),
+                        tp<double>(ws, pl.dwdb), G, st);
+}
+
 template <class T>
 static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const float* pY, const float* pU,
                              const float* pD, const float* z, const float* xc, const float* xsY, const float* xsU,
                              const float* f, float f_const, const float* real, const float* w_group, float* gY,
-                             float* gU, float* gD, float* loss, int32_t* nonfinite, void* ws, hipStream_t st) {
+                             float* gU, float* gD, float* loss, int32_t* nonfinite, void* ws, hipStream_t st,
+                             const float* gp_eps, float* gp) {
   const int G = pl.G, d = s->d, n_z = s->n_z, P = s->P, S = s->S;
   const float ls = s->loss_scale;
   const float inv = 1.0f / ls;
@@ -668,6 +797,13 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
       a.nY = s->n_sY; a.nU = s->n_sU; a.df_sign = -1.0f;
       if ((r = gemm_nt<T>(EPI_DF, 0, 0, a, G, st, "disc_bwd")) != PIGAN_OK) return r;
     }
+    // critic gradient penalty on the pairs of this chunk's samples
+    if (s->lambda_gp > 0.0f) {
+      const int npair = std::min(std::min(S, s->B_r), s0 + Sc) - s0;
+      if (npair > 0 && (r = critic_penalty<T>(ws, pl, s, pD, Yc, Uc, real, gp_eps, w_group, s0, npair, gD, inv,
+                                              nonfinite, acc, G, st)) != PIGAN_OK)
+        return r;
+    }
     // generator reverse passes
     if ((r = gen_chunk_bwd<T>(ws, pl, Yc, pY, xsY, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, gY, accum, inv, nonfinite,
                               G, st)) != PIGAN_OK)
@@ -678,7 +814,8 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
   }
   {
     ProfScope ps(st, "misc", 0.0, 0.0);
-    HIP_TRY(launch_losses(acc, 4, w_group, S, s->B_r, (int64_t)S * P, s->lambda_pde, loss, nonfinite, G, st));
+    HIP_TRY(launch_losses(acc, 4, w_group, S, s->B_r, (int64_t)S * P, s->lambda_pde, s->lambda_gp,
+                          std::min(S, s->B_r), loss, gp, nonfinite, G, st));
   }
   return PIGAN_OK;
 }
@@ -702,22 +839,25 @@ int64_t pigan_mlp_n_params(const pigan_mlp* net) {
 }
 
 size_t pigan_workspace_bytes(const pigan_step_desc* s) {
-  if (check_step(s) != PIGAN_OK) return 0;
+  if (check_step(s, true) != PIGAN_OK) return 0;   // either entry point: includes the penalty's buffers
   StepPlan pl;
   plan_step(s, choose_chunk(s), pl);
   return pl.total;
 }
 
-pigan_status pigan_train_step_grads(const pigan_step_desc* s, const float* pY, const float* pU, const float* pD,
-                                    const float* z, const float* xc, const float* xsY, const float* xsU,
-                                    const float* f, float f_const, const float* real, const float* w_group,
-                                    float* gY, float* gU, float* gD, float* loss, int32_t* nonfinite, void* ws,
-                                    size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+static pigan_status train_step_entry(const pigan_step_desc* s, const float* pY, const float* pU, const float* pD,
+                                     const float* z, const float* xc, const float* xsY, const float* xsU,
+                                     const float* f, float f_const, const float* real, const float* w_group,
+                                     const float* gp_eps, float* gY, float* gU, float* gD, float* loss, float* gp,
+                                     int32_t* nonfinite, void* ws, size_t ws_bytes, void* stream, bool gp_entry) {
   g_err.clear();
-  pigan_status st = check_step(s);
+  pigan_status st = check_step(s, gp_entry);
   if (st != PIGAN_OK) return st;
   if (!pY || !pU || !pD || !z || !xc || !xsY || !xsU || !real || !gY || !gU || !gD || !loss || !nonfinite)
     return fail(PIGAN_EINVAL, "null input or output pointer");
+  if (s->lambda_gp > 0.0f && !gp_eps) return fail(PIGAN_EINVAL, "lambda_gp > 0 needs gp_eps");
   if (!__builtin_isfinite(f_const)) return fail(PIGAN_EINVAL, "f_const must be finite");
   StepPlan pl;
   plan_step(s, choose_chunk(s), pl);
@@ -728,14 +868,34 @@ pigan_status pigan_train_step_grads(const pigan_step_desc* s, const float* pY, c
   switch (s->dt) {
     case PIGAN_FP32:
       return run_step<float>(s, pl, pY, pU, pD, z, xc, xsY, xsU, f, f_const, real, w_group, gY, gU, gD, loss,
-                             nonfinite, ws, hs);
+                             nonfinite, ws, hs, gp_eps, gp);
     case PIGAN_BF16:
       return run_step<bf16>(s, pl, pY, pU, pD, z, xc, xsY, xsU, f, f_const, real, w_group, gY, gU, gD, loss,
-                            nonfinite, ws, hs);
+                            nonfinite, ws, hs, gp_eps, gp);
     default:
       return run_step<f16>(s, pl, pY, pU, pD, z, xc, xsY, xsU, f, f_const, real, w_group, gY, gU, gD, loss,
-                           nonfinite, ws, hs);
+                           nonfinite, ws, hs, gp_eps, gp);
   }
+}
+
+extern "C" {
+
+pigan_status pigan_train_step_grads(const pigan_step_desc* s, const float* pY, const float* pU, const float* pD,
+                                    const float* z, const float* xc, const float* xsY, const float* xsU,
+                                    const float* f, float f_const, const float* real, const float* w_group,
+                                    float* gY, float* gU, float* gD, float* loss, int32_t* nonfinite, void* ws,
+                                    size_t ws_bytes, void* stream) {
+  return train_step_entry(s, pY, pU, pD, z, xc, xsY, xsU, f, f_const, real, w_group, nullptr, gY, gU, gD, loss,
+                          nullptr, nonfinite, ws, ws_bytes, stream, false);
+}
+
+pigan_status pigan_train_step_grads_gp(const pigan_step_desc* s, const float* pY, const float* pU, const float* pD,
+                                       const float* z, const float* xc, const float* xsY, const float* xsU,
+                                       const float* f, float f_const, const float* real, const float* w_group,
+                                       const float* gp_eps, float* gY, float* gU, float* gD, float* loss, float* gp,
+                                       int32_t* nonfinite, void* ws, size_t ws_bytes, void* stream) {
+  return train_step_entry(s, pY, pU, pD, z, xc, xsY, xsU, f, f_const, real, w_group, gp_eps, gY, gU, gD, loss, gp,
+                          nonfinite, ws, ws_bytes, stream, true);
 }
 
 }  // extern "C"

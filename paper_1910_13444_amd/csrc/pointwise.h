@@ -60,6 +60,14 @@ hipError_t launch_disc_seed(const float* score, int64_t sc_g, int n_fake, int n_
                             const float* w_group, float loss_scale, float* seed, double* acc, int acc_stride,
                             int G, hipStream_t st);
 int out_bwd_blocks(int64_t n_points, int ppb);
+template <class T>
+hipError_t launch_gp_mix(const float* yY, int64_t yY_g, const float* yU, int64_t yU_g, int nY, int nU,
+                         const float* real, int64_t real_g, const float* eps, int64_t eps_g, int b0, int n, int n_in,
+                         T* X, int64_t x_g, int ldx, int G, hipStream_t st);
+hipError_t launch_fill2(float* seed, int64_t s_g, int n, float v0, float v1, int two, int G, hipStream_t st);
+template <class T>
+hipError_t launch_gp_norm(const float* gin, int64_t g_g, int n, int n_in, const float* w_group, float scale,
+                          double* part, int64_t p_g, T* X, int64_t x_g, int ldx, int G, hipStream_t st);
 template <class T> hipError_t launch_out_bwd(int nd1, int nd2, const OutBwdArgs<T>& a, int G, hipStream_t st);
 // dst[(col/Jp)*J + col%Jp] (+)= scale * sum_slots part[g][slot][col]  (fp64, fixed order)
 template <class Tin>
@@ -71,7 +79,8 @@ hipError_t launch_first_wgrad(const float* part, int S, int nrc, int W, int d, i
                               int64_t z_g, int n_z, float* grad, int64_t g_g, int accumulate, float scale,
                               int32_t* nonfinite, int G, hipStream_t st);
 hipError_t launch_losses(const double* acc, int acc_stride, const float* w_group, int S, int B, int64_t SP,
-                         float lambda_pde, float* loss, int32_t* nonfinite, int G, hipStream_t st);
+                         float lambda_pde, float lambda_gp, int n_gp, float* loss, float* gp, int32_t* nonfinite,
+                         int G, hipStream_t st);
 hipError_t launch_zero(double* acc, int n, int32_t* flag, hipStream_t st);
 template <class T>
 hipError_t launch_cast(const float* src, int64_t s_g, int N, int K, int Kp, T* dst, T* dstT, int64_t d_g, int G,

@@ -239,6 +239,66 @@ __global__ void k_snap_fill(const float* __restrict__ yY, int64_t yY_g, const fl
 }
 
 // ---------------------------------------------------------------------------
+// Critic gradient penalty (WGAN-GP member of the critic family the paper
+// cites): interpolates x_b = eps_b R_b + (1 - eps_b) F_b of the n pairs of a
+// chunk (fake row i is the chunk's sample i, global pair b = b0 + i), stored
+// in the discriminator's input rows [0, n) in the storage type.
+// ---------------------------------------------------------------------------
+template <class T>
+__global__ void k_gp_mix(const float* __restrict__ yY, int64_t yY_g, const float* __restrict__ yU, int64_t yU_g,
+                         int nY, int nU, const float* __restrict__ real, int64_t real_g, const float* __restrict__ eps,
+                         int64_t eps_g, int b0, int n, int n_in, T* __restrict__ X, int64_t x_g, int ldx) {
+  const int g = blockIdx.z;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)n * ldx) return;
+  const int i = (int)(idx / ldx), j = (int)(idx % ldx);
+  float v = 0.0f;
+  if (j < n_in) {
+    const float f = j < nY ? yY[g * yY_g + (int64_t)i * nY + j] : yU[g * yU_g + (int64_t)i * nU + (j - nY)];
+    const float r = real[g * real_g + (int64_t)(b0 + i) * n_in + j];
+    const float e = eps[g * eps_g + b0 + i];
+    v = e * r + (1.0f - e) * f;
+  }
+  X[g * x_g + idx] = Elem<T>::from_f(v);
+}
+
+// seeds [0, n) = v0, [n, 2n) = v1 (fp32), one group per grid z
+__global__ void k_fill2(float* __restrict__ seed, int64_t s_g, int n, float v0, float v1, int two) {
+  const int g = blockIdx.z;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) seed[g * s_g + i] = v0;
+  if (two && i < n) seed[g * s_g + n + i] = v1;
+}
+
+// One block per pair row: norm of the critic's input gradient g_i, the
+// penalty term (|g_i| - 1)^2 (double, per row; summed later in row order),
+// and the tangent row c_i = scale (|g_i| - 1)/|g_i| g_i stored as input row
+// n + i (zero for g_i = 0, which has no gradient direction).
+template <class T>
+__global__ void __launch_bounds__(256)
+k_gp_norm(const float* __restrict__ gin, int64_t g_g, int n, int n_in, const float* __restrict__ w_group,
+          float scale, double* __restrict__ part, int64_t p_g, T* __restrict__ X, int64_t x_g, int ldx) {
+  __shared__ double red[256];
+  const int g = blockIdx.z;
+  const int i = blockIdx.x;
+  const float* gi = gin + g * g_g + (int64_t)i * n_in;
+  double acc = 0.0;
+  for (int j = threadIdx.x; j < n_in; j += 256) acc += (double)gi[j] * (double)gi[j];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if ((int)threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+    __syncthreads();
+  }
+  const double nrm = sqrt(red[0]);
+  if (threadIdx.x == 0) part[g * p_g + i] = (nrm - 1.0) * (nrm - 1.0);
+  const float w = w_group ? w_group[g] : 1.0f;
+  const float coef = nrm > 0.0 ? (float)((nrm - 1.0) / nrm) * scale * w : 0.0f;
+  T* xr = X + g * x_g + (int64_t)(n + i) * ldx;
+  for (int j = threadIdx.x; j < ldx; j += 256) xr[j] = Elem<T>::from_f(j < n_in ? coef * gi[j] : 0.0f);
+}
+
+// ---------------------------------------------------------------------------
 // critic cotangents and score sums (one block per group):
 //   dL_D/dD(fake_s) = w/S,  dL_D/dD(real_b) = -w/B_r   (times the loss scale)
 //   acc[g][0] += sum D(fake), acc[g][1] += sum D(real)
@@ -566,20 +626,25 @@ k_first_wgrad(const float* __restrict__ part, int S, int nrc, int W, int d, int 
 
 // ---------------------------------------------------------------------------
 // losses from the accumulated sums (double): acc[g] = {sum D(fake),
-// sum D(real), sum r^2}
+// sum D(real), sum r^2, sum (|grad D| - 1)^2 over the penalty pairs}; the
+// penalty P = w lambda_gp acc[3] / n_gp is part of L_D and also stored in gp
+// (when gp is not null)
 // ---------------------------------------------------------------------------
 __global__ void k_losses(const double* __restrict__ acc, int acc_stride, const float* __restrict__ w_group,
-                         int S, int B, int64_t SP, float lambda_pde, float* loss, int32_t* nonfinite, int G) {
+                         int S, int B, int64_t SP, float lambda_pde, float lambda_gp, int n_gp, float* loss, float* gp,
+                         int32_t* nonfinite, int G) {
   const int g = blockIdx.x * blockDim.x + threadIdx.x;
   if (g >= G) return;
   const double w = w_group ? (double)w_group[g] : 1.0;
   const double* a = acc + g * acc_stride;
-  const double LD = w * (a[0] / S - a[1] / B);
+  const double Pg = n_gp > 0 ? w * (double)lambda_gp * a[3] / (double)n_gp : 0.0;
+  const double LD = w * (a[0] / S - a[1] / B) + Pg;
   const double La = -w * a[0] / S;
   const double Lp = w * (double)lambda_pde * a[2] / (double)SP;
   loss[3 * g + 0] = (float)LD;
   loss[3 * g + 1] = (float)La;
   loss[3 * g + 2] = (float)Lp;
+  if (gp) gp[g] = (float)Pg;
   if (!__builtin_isfinite(LD) || !__builtin_isfinite(La) || !__builtin_isfinite(Lp)) *nonfinite = 1;
 }
 
@@ -667,6 +732,31 @@ hipError_t launch_snap_fill(const float* yY, int64_t yY_g, const float* yU, int6
   return hipGetLastError();
 }
 
+template <class T>
+hipError_t launch_gp_mix(const float* yY, int64_t yY_g, const float* yU, int64_t yU_g, int nY, int nU,
+                         const float* real, int64_t real_g, const float* eps, int64_t eps_g, int b0, int n, int n_in,
+                         T* X, int64_t x_g, int ldx, int G, hipStream_t st) {
+  const int64_t tot = (int64_t)n * ldx;
+  if (tot <= 0) return hipSuccess;
+  k_gp_mix<T><<<dim3(nblk(tot, 256), 1, G), 256, 0, st>>>(yY, yY_g, yU, yU_g, nY, nU, real, real_g, eps, eps_g, b0,
+                                                          n, n_in, X, x_g, ldx);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill2(float* seed, int64_t s_g, int n, float v0, float v1, int two, int G, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  k_fill2<<<dim3(nblk(n, 256), 1, G), 256, 0, st>>>(seed, s_g, n, v0, v1, two);
+  return hipGetLastError();
+}
+
+template <class T>
+hipError_t launch_gp_norm(const float* gin, int64_t g_g, int n, int n_in, const float* w_group, float scale,
+                          double* part, int64_t p_g, T* X, int64_t x_g, int ldx, int G, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  k_gp_norm<T><<<dim3(n, 1, G), 256, 0, st>>>(gin, g_g, n, n_in, w_group, scale, part, p_g, X, x_g, ldx);
+  return hipGetLastError();
+}
+
 hipError_t launch_disc_seed(const float* score, int64_t sc_g, int n_fake, int n_real, int S_total, int B_total,
                             const float* w_group, float loss_scale, float* seed, double* acc, int acc_stride,
                             int G, hipStream_t st) {
@@ -725,8 +815,10 @@ hipError_t launch_first_wgrad(const float* part, int S, int nrc, int W, int d, i
 }
 
 hipError_t launch_losses(const double* acc, int acc_stride, const float* w_group, int S, int B, int64_t SP,
-                         float lambda_pde, float* loss, int32_t* nonfinite, int G, hipStream_t st) {
-  k_losses<<<nblk(G, 64), 64, 0, st>>>(acc, acc_stride, w_group, S, B, SP, lambda_pde, loss, nonfinite, G);
+                         float lambda_pde, float lambda_gp, int n_gp, float* loss, float* gp, int32_t* nonfinite,
+                         int G, hipStream_t st) {
+  k_losses<<<nblk(G, 64), 64, 0, st>>>(acc, acc_stride, w_group, S, B, SP, lambda_pde, lambda_gp, n_gp, loss, gp,
+                                       nonfinite, G);
   return hipGetLastError();
 }
 
@@ -750,6 +842,11 @@ hipError_t launch_cast(const float* src, int64_t s_g, int N, int K, int Kp, T* d
                                           const float*, int64_t, int, int, T*, int64_t, int, int, hipStream_t); \
   template hipError_t launch_out_bwd<T>(int, int, const OutBwdArgs<T>&, int, hipStream_t);                    \
   template hipError_t launch_first_bwd<T>(const FirstBwdArgs<T>&, int, hipStream_t);                          \
+  template hipError_t launch_gp_mix<T>(const float*, int64_t, const float*, int64_t, int, int, const float*,    \
+                                       int64_t, const float*, int64_t, int, int, int, T*, int64_t, int, int,   \
+                                       hipStream_t);                                                            \
+  template hipError_t launch_gp_norm<T>(const float*, int64_t, int, int, const float*, float, double*, int64_t, \
+                                        T*, int64_t, int, int, hipStream_t);                                    \
   template hipError_t launch_cast<T>(const float*, int64_t, int, int, int, T*, T*, int64_t, int, hipStream_t);
 PIGAN_INST(float)
 PIGAN_INST(bf16)

@@ -71,6 +71,7 @@ def lib():
         "pigan_disc_forward": (i32, [P, P, P, i32, i32, P, P, sz, P]),
         "pigan_workspace_bytes": (sz, [P]),
         "pigan_train_step_grads": (i32, [P, P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, sz, P]),
+        "pigan_train_step_grads_gp": (i32, [P, P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, P, P, sz, P]),
         "pigan_last_error": (C.c_char_p, []),
         "pigan_profile_enable": (i32, [i32]),
         "pigan_profile_read": (i32, [P, i32, P]),
@@ -205,6 +206,7 @@ class StepOut:
     gD: torch.Tensor
     loss: torch.Tensor
     nonfinite: torch.Tensor
+    gp: torch.Tensor | None = None      # [G] critic gradient penalty (included in loss[:, 0])
 
 
 class TrainStep:
@@ -225,20 +227,28 @@ class TrainStep:
         f32 = dict(dtype=torch.float32, device=self.device)
         self.out = StepOut(torch.empty((G, self.nY), **f32), torch.empty((G, self.nU), **f32),
                            torch.empty((G, self.nD), **f32), torch.empty((G, 3), **f32),
-                           torch.zeros((1,), dtype=torch.int32, device=self.device))
+                           torch.zeros((1,), dtype=torch.int32, device=self.device),
+                           torch.zeros((G,), **f32) if desc.lambda_gp != 0.0 else None)
 
-    def __call__(self, pY, pU, pD, z, xc, xsY, xsU, real, f=None, f_const=0.0, w_group=None) -> StepOut:
+    def __call__(self, pY, pU, pD, z, xc, xsY, xsU, real, f=None, f_const=0.0, w_group=None,
+                 gp_eps=None) -> StepOut:
+        """gp_eps: [G, min(S, B_r)] mixing weights of the critic gradient
+        penalty (required when the descriptor's lambda_gp is non-zero)."""
         d = self.desc
         G, S, Pn = d.genY.n_groups, d.S, d.P
         o = self.out
-        st = lib().pigan_train_step_grads(
-            C.byref(d), _ptr(pY, "pY", G * self.nY), _ptr(pU, "pU", G * self.nU), _ptr(pD, "pD", G * self.nD),
-            _ptr(z, "z", G * S * d.n_z), _ptr(xc, "xc", G * S * Pn * d.d), _ptr(xsY, "xsY", G * d.n_sY * d.d),
-            _ptr(xsU, "xsU", G * d.n_sU * d.d), _ptr(f, "f", G * S * Pn), float(f_const),
-            _ptr(real, "real", G * d.B_r * (d.n_sY + d.n_sU)), _ptr(w_group, "w_group", G),
-            _ptr(o.gY, "gY"), _ptr(o.gU, "gU"), _ptr(o.gD, "gD"), _ptr(o.loss, "loss"),
-            _ptr(o.nonfinite, "nonfinite", 1, dtype=torch.int32), _ptr(self.ws, "ws", dtype=torch.uint8),
-            self.ws_bytes, _stream())
+        args = [C.byref(d), _ptr(pY, "pY", G * self.nY), _ptr(pU, "pU", G * self.nU), _ptr(pD, "pD", G * self.nD),
+                _ptr(z, "z", G * S * d.n_z), _ptr(xc, "xc", G * S * Pn * d.d), _ptr(xsY, "xsY", G * d.n_sY * d.d),
+                _ptr(xsU, "xsU", G * d.n_sU * d.d), _ptr(f, "f", G * S * Pn), float(f_const),
+                _ptr(real, "real", G * d.B_r * (d.n_sY + d.n_sU)), _ptr(w_group, "w_group", G)]
+        outs = [_ptr(o.gY, "gY"), _ptr(o.gU, "gU"), _ptr(o.gD, "gD"), _ptr(o.loss, "loss")]
+        tail = [_ptr(o.nonfinite, "nonfinite", 1, dtype=torch.int32), _ptr(self.ws, "ws", dtype=torch.uint8),
+                self.ws_bytes, _stream()]
+        if d.lambda_gp != 0.0:
+            eps = _ptr(gp_eps, "gp_eps", G * min(S, d.B_r))
+            st = lib().pigan_train_step_grads_gp(*args, eps, *outs, _ptr(o.gp, "gp", G), *tail)
+        else:
+            st = lib().pigan_train_step_grads(*args, *outs, *tail)
         _check(st)
         return o
 

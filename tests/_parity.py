@@ -73,20 +73,25 @@ def to_dev(a, dev="cuda"):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
 
 
-def run_step_gpu(wl, inp, real, chunk_S=0, dtype=None, loss_scale=1.0, lambda_pde=None):
-    """One training step through pigan_train_step_grads; returns numpy outputs."""
+def run_step_gpu(wl, inp, real, chunk_S=0, dtype=None, loss_scale=1.0, lambda_pde=None, lambda_gp=0.0,
+                 gp_eps=None):
+    """One training step through pigan_train_step_grads (or, with lambda_gp,
+    pigan_train_step_grads_gp); returns numpy outputs."""
     import torch
     from paper_1910_13444_amd import pigan
     S = inp.z.shape[1]
     desc = pigan.step_desc(wl, S=S, B_r=real.shape[1], chunk_S=chunk_S, dtype=dtype, loss_scale=loss_scale,
-                           lambda_pde=lambda_pde)
+                           lambda_pde=lambda_pde, lambda_gp=lambda_gp)
     step = pigan.TrainStep(desc)
     o = step(to_dev(inp.pY), to_dev(inp.pU), to_dev(inp.pD), to_dev(inp.z), to_dev(inp.xc), to_dev(inp.xsY),
              to_dev(inp.xsU), to_dev(real), f=None if inp.f is None else to_dev(inp.f), f_const=inp.f_const,
-             w_group=to_dev(inp.w_group))
+             w_group=to_dev(inp.w_group), gp_eps=None if gp_eps is None else to_dev(gp_eps))
     torch.cuda.synchronize()
-    return dict(gY=o.gY.cpu().numpy(), gU=o.gU.cpu().numpy(), gD=o.gD.cpu().numpy(), loss=o.loss.cpu().numpy(),
-                nonfinite=int(o.nonfinite.cpu().item()))
+    out = dict(gY=o.gY.cpu().numpy(), gU=o.gU.cpu().numpy(), gD=o.gD.cpu().numpy(), loss=o.loss.cpu().numpy(),
+               nonfinite=int(o.nonfinite.cpu().item()))
+    if o.gp is not None:
+        out["P_gp"] = o.gp.cpu().numpy()
+    return out
 
 
 def step_errors(wl, out, ref):
@@ -96,4 +101,6 @@ def step_errors(wl, out, ref):
     errs.update(grad_errors(out["gD"], ref["gD"], wl.disc_shape(), "gD"))
     for i, k in enumerate(("L_D", "L_adv", "L_pde")):
         errs[k] = rel(out["loss"][:, i], ref["loss"][:, i])
+    if "P_gp" in out:
+        errs["P_gp"] = rel(out["P_gp"], ref["P_gp"])
     return errs

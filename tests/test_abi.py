@@ -39,7 +39,7 @@ def _step(desc, ws_bytes, ptr=FAKE, f=None, wg=None):
 @pytest.mark.parametrize("field,value,status", [
     ("d", 0, pigan.EINVAL), ("d", 4, pigan.EINVAL), ("n_z", 0, pigan.EINVAL), ("S", 0, pigan.EINVAL),
     ("P", -1, pigan.EINVAL), ("n_sY", 0, pigan.EINVAL), ("B_r", 0, pigan.EINVAL), ("chunk_S", -2, pigan.EINVAL),
-    ("lambda_gp", 0.5, pigan.ENOTSUP), ("loss_scale", 0.0, pigan.EINVAL), ("lambda_pde", -1.0, pigan.EINVAL),
+    ("lambda_gp", -0.5, pigan.EINVAL), ("loss_scale", 0.0, pigan.EINVAL), ("lambda_pde", -1.0, pigan.EINVAL),
     ("dt", 7, pigan.EINVAL),
 ])
 def test_step_rejects_bad_descriptor(field, value, status):
@@ -48,6 +48,26 @@ def test_step_rejects_bad_descriptor(field, value, status):
     assert _step(d, 1 << 40) == status
     assert pigan.lib().pigan_last_error()
     assert pigan.workspace_bytes(d) == 0
+
+
+def _step_gp(desc, ws_bytes, eps, ptr=FAKE):
+    L = pigan.lib()
+    return L.pigan_train_step_grads_gp(C.byref(desc), *([ptr] * 7), None, 0.0, ptr, None, eps, ptr, ptr, ptr, ptr,
+                                       None, ptr, ptr, ws_bytes, None)
+
+
+def test_gradient_penalty_entry_validation():
+    d = pigan.step_desc(configs.C1, lambda_gp=10.0)
+    need = pigan.workspace_bytes(d)
+    assert need > pigan.workspace_bytes(pigan.step_desc(configs.C1)) > 0   # the penalty's buffers
+    assert _step(d, need) == pigan.ENOTSUP             # the plain entry has no mixing weights
+    assert b"pigan_train_step_grads_gp" in pigan.lib().pigan_last_error()
+    assert _step_gp(d, need, None) == pigan.EINVAL     # lambda_gp > 0 needs gp_eps
+    d.lambda_gp = float("nan")
+    assert _step_gp(d, need, FAKE) == pigan.EINVAL
+    assert pigan.workspace_bytes(d) == 0
+    d = pigan.step_desc(configs.C1, lambda_gp=10.0)
+    assert _step_gp(d, need - 1, FAKE) == pigan.EWORKSPACE
 
 
 def test_step_rejects_inconsistent_shapes():
