@@ -119,7 +119,7 @@ def measured_peaks(dev):
 def run_steps(step, d, wl, k):
     for _ in range(k):
         step(d["pY"], d["pU"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["real"], f=None,
-             f_const=wl.f_const, w_group=d["w_group"])
+             f_const=wl.f_const, w_group=d["w_group"], gp_eps=d.get("gp_eps"))
 
 
 def cpu_baseline(wl, budget_s: float = 15.0):
@@ -166,6 +166,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--no-peaks", action="store_true", help="skip the copy / GEMM micro-benchmarks")
+    ap.add_argument("--lambda-gp", type=float, default=0.0,
+                    help="add the critic gradient penalty with this weight (seeded mixing weights)")
     ap.add_argument("--copy-calib", type=int, default=0, metavar="BYTES",
                     help="first run one plain device-to-device copy of BYTES bytes (a known-size reference "
                          "dispatch for scaling HBM byte counters)")
@@ -193,7 +195,11 @@ def main():
         log(f"bench: calibration copy of {a.copy_calib} bytes done")
         del src, dst
     d, inp = device_inputs(wl, dev)
-    step = pigan.TrainStep(pigan.step_desc(wl, chunk_S=a.chunk_S), device=dev)
+    if a.lambda_gp > 0:
+        import numpy as np
+        eps = np.random.default_rng(wl.seed + 5).random((wl.G, min(wl.S, wl.B_r)), dtype=np.float32)
+        d["gp_eps"] = torch.from_numpy(eps).to(dev)
+    step = pigan.TrainStep(pigan.step_desc(wl, chunk_S=a.chunk_S, lambda_gp=a.lambda_gp), device=dev)
     log(f"bench: workspace {step.ws_bytes / 2**30:.2f} GiB; warmup {a.warmup}")
     run_steps(step, d, wl, a.warmup)
     torch.cuda.synchronize()
@@ -260,7 +266,7 @@ def main():
         "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
         "config": {"workload": wl.name, "G": wl.G, "d": wl.d, "n_z": wl.n_z, "gen": f"{wl.L}x{wl.W} tanh",
                    "disc": f"{wl.L_D}x{wl.W_D} tanh on {wl.n_in}", "S": wl.S, "P": wl.P,
-                   "sensors": [wl.n_sY, wl.n_sU], "B_r": wl.B_r, "chunk_S": a.chunk_S,
+                   "sensors": [wl.n_sY, wl.n_sU], "B_r": wl.B_r, "chunk_S": a.chunk_S, "lambda_gp": a.lambda_gp,
                    "collocation_points_per_step": pts, "alg_flops_per_step": F},
         "collocation_points_per_s": pts / (ms * 1e-3),
         "mfma_frac_step": tflops / PEAK_TFLOPS[wl.dtype],
