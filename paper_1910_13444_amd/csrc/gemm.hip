@@ -29,7 +29,16 @@
 
 namespace pigan {
 
-static constexpr int LDS_PITCH = 80;
+// Operand stages of k_gemm_nt: 64-byte rows (one k-slice) with the four
+// 16-byte segments of row r stored in the order s ^ ((r >> 2) & 3).  The
+// fragment reads (32 consecutive rows, one segment) and the stage writes (four
+// lanes per row) are then both free of bank conflicts (measured with the
+// LDS bank-conflict counter; an 80-byte padded pitch conflicted on the writes).
+static constexpr int LDS_PITCH = 64;
+typedef uint32_t u32x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ int lds_seg(int row, int seg) { return row * LDS_PITCH + ((seg ^ ((row >> 2) & 3)) << 4); }
 
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own
 // L2).  Map hardware block b to a logical tile so that every XCD walks one
@@ -117,7 +126,7 @@ __device__ __forceinline__ void jet_bwd(float* g, const float* ap) {
   g[0] = ga;
 }
 
-template <class T, int ND1, int ND2, int WM, int WN, int MT, int NT, int EPI, int OCC>
+template <class T, int ND1, int ND2, int WM, int WN, int MT, int NT, int EPI, int OCC, bool DB = (OCC >= 2)>
 __global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OCC)))
 k_gemm_nt(const NtArgs<T> p) {
   constexpr int C = 1 + ND1 + ND2;
@@ -198,23 +207,37 @@ k_gemm_nt(const NtArgs<T> p) {
 #pragma unroll
     for (int i = 0; i < PPT; ++i) {
       const int piece = tid + i * NTH;
-      if (piece < PIECES) *(uint4*)(base + (piece >> 2) * LDS_PITCH + (piece & 3) * 16) = buf[i];
+      if (piece < PIECES) *(uint4*)(base + lds_seg(piece >> 2, piece & 3)) = buf[i];
+    }
+  };
+  // a fragment: 8 consecutive k of one row (16 bytes in 16-bit types, two
+  // segments in fp32); every fragment row base is a multiple of 32, so the
+  // segment swizzle of the lane's row is (lane >> 2) & 3
+  const int gsw = (lane >> 2) & 3;
+  auto frag_at = [&](const char* base, int row, int c) {
+    if constexpr (ES == 2) {
+      const int seg = 2 * c + (lane >> 5);
+      return *(const frag*)(base + row * LDS_PITCH + ((seg ^ gsw) << 4));
+    } else {
+      const int seg = 2 * (lane >> 5);
+      const u32x4 lo = *(const u32x4*)(base + row * LDS_PITCH + ((seg ^ gsw) << 4));
+      const u32x4 hi = *(const u32x4*)(base + row * LDS_PITCH + (((seg + 1) ^ gsw) << 4));
+      const u32x8 w = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      return __builtin_bit_cast(frag, w);
     }
   };
   auto compute = [&](int stage) {
     const char* base = lds + stage * STAGE;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-      const int koff = c * 32 + (lane >> 5) * (8 * ES);
       frag bfr[NT];
 #pragma unroll
-      for (int t = 0; t < NT; ++t)
-        bfr[t] = *(const frag*)(base + (C * BM + 32 * (wn * NT + t) + (lane & 31)) * LDS_PITCH + koff);
+      for (int t = 0; t < NT; ++t) bfr[t] = frag_at(base, C * BM + 32 * (wn * NT + t) + (lane & 31), c);
 #pragma unroll
       for (int u = 0; u < MT; ++u)
 #pragma unroll
         for (int k = 0; k < C; ++k) {
-          const frag afr = *(const frag*)(base + (k * BM + 32 * (MT * wm + u) + (lane & 31)) * LDS_PITCH + koff);
+          const frag afr = frag_at(base, k * BM + 32 * (MT * wm + u) + (lane & 31), c);
 #pragma unroll
           for (int t = 0; t < NT; ++t) Elem<T>::mma(acc[u][k][t], bfr[t], afr);   // rows: columns n; cols: points
         }
@@ -222,7 +245,7 @@ k_gemm_nt(const NtArgs<T> p) {
   };
 
   const int nk = p.K / KS;
-  if constexpr (OCC >= 2) {
+  if constexpr (DB) {
     // two LDS stages, two register buffers: the global loads of stage kt+2
     // are issued before stage kt is multiplied; one barrier per stage
     // prefetches are unconditional (the stage index is clamped; loads past
@@ -404,9 +427,6 @@ k_gemm_nt(const NtArgs<T> p) {
 // a whole tile of loads in flight.  Four waves; wave w owns columns
 // 32w..32w+31 of every stream.
 // ---------------------------------------------------------------------------
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
 template <class T, int ND1, int ND2, int EPI, bool FIRST>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
 k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
@@ -1216,6 +1236,9 @@ int cu_count() {
   return cached[dev];
 }
 
+template <class T, int C>
+constexpr bool wide_ok() { return sizeof(T) == 2 && (C == 1 || C == 5); }
+
 template <class T, int ND1, int ND2, int EPI>
 hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   constexpr int C = 1 + ND1 + ND2;
@@ -1239,6 +1262,19 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   if (a.N <= 32) {
     dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 31) / 32)), 1, G);
     k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, (C >= 4 ? 1 : 2)><<<grid, 256, 0, st>>>(a);
+  } else if (wide_ok<T, C>() && a.K >= 512 && a.N >= 256) {
+    // wide layers (matrix-core bound): fewer LDS fragment reads per MFMA (the
+    // LDS serves about one 1 KB fragment read per MFMA per CU) and fewer L2
+    // re-reads of each activation tile
+    if constexpr (C == 1) {
+      // one stream: 128 points x 128 columns, 2 x 2 fragments per wave
+      dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 127) / 128)), 1, G);
+      k_gemm_nt<T, ND1, ND2, 2, 2, 2, 2, EPI, 2, true><<<grid, 256, 0, st>>>(a);
+    } else if constexpr (C == 5) {
+      // five streams: eight waves (2 x 4), 64 points x 128 columns
+      dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + 127) / 128)), 1, G);
+      k_gemm_nt<T, ND1, ND2, 2, 4, 1, 1, EPI, 2, true><<<grid, 512, 0, st>>>(a);
+    }
   } else {
     constexpr int BN = 64 * NTM;
     dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + BN - 1) / BN)), 1, G);
