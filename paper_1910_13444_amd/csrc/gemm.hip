@@ -126,7 +126,22 @@ __device__ __forceinline__ void jet_bwd(float* g, const float* ap) {
   g[0] = ga;
 }
 
-template <class T, int ND1, int ND2, int WM, int WN, int MT, int NT, int EPI, int OCC, bool DB = (OCC >= 2)>
+// Wait until at most N vector-memory operations of this wave are outstanding
+// (N is an immediate).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// NS > 0 (16-bit types): the operand stages move from global memory straight
+// into an NS-deep LDS ring (global_load_lds_dwordx4, no register staging),
+// issued NS - 1 stages ahead of the multiply, so that the load latency is
+// covered by several stages of matrix-core work.
+template <class T, int ND1, int ND2, int WM, int WN, int MT, int NT, int EPI, int OCC, bool DB = (OCC >= 2),
+          int NS = 0>
 __global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OCC)))
 k_gemm_nt(const NtArgs<T> p) {
   constexpr int C = 1 + ND1 + ND2;
@@ -142,7 +157,9 @@ k_gemm_nt(const NtArgs<T> p) {
   constexpr int PPT = (PIECES + NTH - 1) / NTH;
   constexpr int OPITCH = BN * ES + 16;             // epilogue staging pitch (bytes)
   constexpr int OUTB = BM * OPITCH;
-  constexpr int LDSB = 2 * STAGE > OUTB ? 2 * STAGE : OUTB;
+  constexpr int RING = (NS > 0 ? NS : 2) * STAGE;
+  constexpr int LDSB = RING > OUTB ? RING : OUTB;
+  static_assert(NS == 0 || (ES == 2 && NS >= 2 && ROWS % 16 == 0), "direct-to-LDS stages: 16-bit types");
   typedef typename Elem<T>::frag frag;
   __shared__ __attribute__((aligned(16))) char lds[LDSB];
 
@@ -168,7 +185,7 @@ k_gemm_nt(const NtArgs<T> p) {
   const char* src[PPT];
   bool valid[PPT];
 #pragma unroll
-  for (int i = 0; i < PPT; ++i) {
+  for (int i = 0; i < (NS > 0 ? 0 : PPT); ++i) {
     const int piece = tid + i * NTH;
     const int row = piece >> 2, sg = piece & 3;
     valid[i] = false;
@@ -245,7 +262,72 @@ k_gemm_nt(const NtArgs<T> p) {
   };
 
   const int nk = p.K / KS;
-  if constexpr (DB) {
+  if constexpr (NS > 0) {
+    // One DMA instruction of a wave fills 1 KB of LDS, lane l at byte 16 l:
+    // 16 stage rows (row 16 g + l / 4, physical segment l % 4, holding the
+    // logical segment (l % 4) ^ ((row >> 2) & 3) of the swizzled layout).
+    // The NG row groups of a stage are dealt to the waves round-robin; a wave
+    // with fewer groups repeats its last one (identical data to identical
+    // bytes), so that every wave issues GPW loads per stage and one
+    // immediate vmcnt fits all.  Points past the segment end and columns past
+    // N read a clamped (valid) row: their products are never stored.
+    constexpr int NG = ROWS / 16;
+    constexpr int GPW = (NG + NTH / 64 - 1) / (NTH / 64);
+    static_assert((NS - 2) * GPW <= 63, "outstanding loads exceed the vmcnt range");
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const char* dsrc[GPW];
+    int dlds[GPW];
+#pragma unroll
+    for (int i = 0; i < GPW; ++i) {
+      int grp = wv + i * (NTH / 64);
+      if (grp > NG - 1) grp = NG - 1;
+      dlds[i] = grp * 1024;
+      const int row = grp * 16 + (lane >> 2);
+      const int ls = (lane & 3) ^ ((row >> 2) & 3);
+      if (row < C * BM) {
+        const int k = row / BM, pp = row % BM;
+        int64_t pt = m0 + pp;
+        if (pt > npts - 1) pt = npts - 1;
+        dsrc[i] = Xb + (p.seg.row0 + k * p.seg.plane + pt) * p.ldx * (int64_t)ES + ls * 16;
+      } else {
+        int n = n0 + row - C * BM;
+        if (n > p.N - 1) n = p.N - 1;
+        dsrc[i] = Wb + (int64_t)n * p.ldw * (int64_t)ES + ls * 16;
+      }
+    }
+    auto issue = [&](int kt, int stage) {
+#pragma unroll
+      for (int i = 0; i < GPW; ++i)
+        __builtin_amdgcn_global_load_lds((const void*)(dsrc[i] + (int64_t)kt * 64),
+                                         (lds_ptr_t)(lds + stage * STAGE + dlds[i]), 16, 0, 0);
+    };
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+      if (s < nk) issue(s, s);
+    int st = 0;
+    for (int kt = 0; kt < nk; ++kt) {
+      // own loads of stage kt complete: the later stages issued so far may
+      // still be in flight
+      const int later = nk - 1 - kt;
+      if constexpr (NS >= 4) {
+        if (later >= 2) wait_vmcnt<2 * GPW>();
+        else if (later == 1) wait_vmcnt<GPW>();
+        else wait_vmcnt<0>();
+      } else if constexpr (NS == 3) {
+        if (later >= 1) wait_vmcnt<GPW>();
+        else wait_vmcnt<0>();
+      } else {
+        wait_vmcnt<0>();
+      }
+      // every wave's loads of stage kt have landed, and every wave is done
+      // with stage kt - 1, whose buffer the next issue refills
+      lds_sync();
+      if (kt + NS - 1 < nk) issue(kt + NS - 1, st == 0 ? NS - 1 : st - 1);
+      compute(st);
+      st = st + 1 == NS ? 0 : st + 1;
+    }
+    lds_sync();
+  } else if constexpr (DB) {
     // two LDS stages, two register buffers: the global loads of stage kt+2
     // are issued before stage kt is multiplied; one barrier per stage
     // prefetches are unconditional (the stage index is clamped; loads past
@@ -1237,7 +1319,7 @@ int cu_count() {
 }
 
 template <class T, int C>
-constexpr bool wide_ok() { return sizeof(T) == 2 && (C == 1 || C == 5); }
+constexpr bool wide_ok() { return sizeof(T) == 2 && (C == 1 || C == 3 || C == 5); }
 
 template <class T, int ND1, int ND2, int EPI>
 hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
@@ -1263,17 +1345,31 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
     dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 31) / 32)), 1, G);
     k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, (C >= 4 ? 1 : 2)><<<grid, 256, 0, st>>>(a);
   } else if (wide_ok<T, C>() && a.K >= 512 && a.N >= 256) {
-    // wide layers (matrix-core bound): fewer LDS fragment reads per MFMA (the
-    // LDS serves about one 1 KB fragment read per MFMA per CU) and fewer L2
-    // re-reads of each activation tile
-    if constexpr (C == 1) {
-      // one stream: 128 points x 128 columns, 2 x 2 fragments per wave
-      dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 127) / 128)), 1, G);
-      k_gemm_nt<T, ND1, ND2, 2, 2, 2, 2, EPI, 2, true><<<grid, 256, 0, st>>>(a);
-    } else if constexpr (C == 5) {
-      // five streams: eight waves (2 x 4), 64 points x 128 columns
+    // wide layers (matrix-core bound): operand stages loaded straight into an
+    // LDS ring several stages ahead, larger wave tiles (fewer LDS fragment
+    // reads per MFMA) and fewer L2 re-reads of each activation tile.  Tile
+    // shapes are the fastest measured per stream count and epilogue.
+    if constexpr (!wide_ok<T, C>()) {
+      return hipErrorInvalidValue;
+    } else if constexpr (C == 1) {
+      if constexpr (EPI == EPI_BWD) {
+        // 128 points x 256 columns, 2 x 4 fragments per wave, 3-stage ring
+        dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 255) / 256)), 1, G);
+        k_gemm_nt<T, ND1, ND2, 2, 2, 2, 4, EPI, 2, true, 3><<<grid, 256, 0, st>>>(a);
+      } else {
+        // 128 points x 128 columns, 2 x 2 fragments per wave, 3-stage ring
+        dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 127) / 128)), 1, G);
+        k_gemm_nt<T, ND1, ND2, 2, 2, 2, 2, EPI, 2, true, 3><<<grid, 256, 0, st>>>(a);
+      }
+    } else if constexpr (C == 5 && EPI == EPI_BWD) {
+      // eight waves (2 x 4), 64 points x 128 columns, 4-stage ring
       dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + 127) / 128)), 1, G);
-      k_gemm_nt<T, ND1, ND2, 2, 4, 1, 1, EPI, 2, true><<<grid, 512, 0, st>>>(a);
+      k_gemm_nt<T, ND1, ND2, 2, 4, 1, 1, EPI, 2, true, 4><<<grid, 512, 0, st>>>(a);
+    } else {
+      // three or five streams: eight waves (2 x 4), 64 points x 256 columns,
+      // 4-stage ring
+      dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + 255) / 256)), 1, G);
+      k_gemm_nt<T, ND1, ND2, 2, 4, 1, 2, EPI, 1, false, 4><<<grid, 512, 0, st>>>(a);
     }
   } else {
     constexpr int BN = 64 * NTM;
