@@ -1099,8 +1099,13 @@ __host__ __device__ constexpr int dw_tr_pitch(int row_bytes) {
          : (row_bytes / 4) % 64 == 0 ? row_bytes + 64 : row_bytes + 64 * ((row_bytes / 4) % 64 == 32 ? 1 : 0);
 }
 
-template <class T, int WM, int WN, int NT, int NB>
-__global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2)))
+// NS > 0 (tile sides of 128 or 256 columns): the stages move straight from
+// global memory into an NS-deep LDS ring (global_load_lds_dwordx4).  Rows are
+// then unpadded (256 or 512 bytes); the 16-byte segment s of row r sits at
+// s ^ 4 (r & 3), which keeps the four rows of a transposing read in disjoint
+// bank ranges.
+template <class T, int WM, int WN, int NT, int NB, int NS = 0, int OCC = 2>
+__global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OCC)))
 k_gemm_dw_tr(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restrict__ H, int64_t h_g,
              int64_t ldh, int64_t R, int64_t n_value, int N, int J, float* __restrict__ partial,
              double* __restrict__ pdb, int n_split, int64_t rows_per_split) {
@@ -1116,8 +1121,13 @@ k_gemm_dw_tr(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __rest
   constexpr int PIECES = SR * (SA + SB);
   static_assert(PIECES % NTH == 0, "whole pieces per thread");
   constexpr int PPT = PIECES / NTH;
+  static_assert(NS == 0 || ((BNn == 128 || BNn == 256) && (BJ == 128 || BJ == 256) && NS >= 2),
+                "direct-to-LDS stages: tile sides of 128 or 256");
+  constexpr int RBA = BNn * 2, RBB = BJ * 2;  // unpadded ring row bytes
+  constexpr int DSTAGE = SR * (RBA + RBB);    // ring stage: SR rows of A, then SR rows of B
+  constexpr int LDSB = NS > 0 ? NS * DSTAGE : 2 * STAGE;
   typedef typename Elem<T>::frag frag;
-  __shared__ __attribute__((aligned(16))) char lds[2 * STAGE];
+  __shared__ __attribute__((aligned(16))) char lds[LDSB];
 
   const int tiles_n = (N + BNn - 1) / BNn;
   const int tiles = tiles_n * ((J + BJ - 1) / BJ);
@@ -1201,21 +1211,25 @@ k_gemm_dw_tr(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __rest
   const int rr = t16 >> 2, qq4 = t16 & 3;
   const int kb = 8 * (lane >> 5);
   auto frag_at = [&](const char* region, int pitch, int c, int colblk) {
-    const char* p0 = region + (c * 16 + kb + rr) * pitch + (colblk + 16 * (grp & 1) + 4 * qq4) * 2;
+    const int byte = (colblk + 16 * (grp & 1) + 4 * qq4) * 2;
+    // the row of both reads is = rr (mod 4): one swizzle for the pair
+    const char* p0 = NS > 0 ? region + (c * 16 + kb + rr) * pitch + (((byte >> 4) ^ (4 * rr)) << 4) + (byte & 15)
+                            : region + (c * 16 + kb + rr) * pitch + byte;
     const u32x2 lo = lds_read_tr<T>(p0);
     const u32x2 hi = lds_read_tr<T>(p0 + 4 * pitch);
     const u32x4 w = {lo.x, lo.y, hi.x, hi.y};
     return __builtin_bit_cast(frag, w);
   };
   auto compute = [&](int stage, int64_t k0) {
-    const char* base = lds + stage * STAGE;
+    const char* base = lds + stage * (NS > 0 ? DSTAGE : STAGE);
+    const char* bbase = base + (NS > 0 ? SR * RBA : REGA);
 #pragma unroll
     for (int c = 0; c < SR / 16; ++c) {
       frag af[NT], bf[NT];
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        af[t] = frag_at(base, PA, c, 32 * (wm * NT + t));
-        bf[t] = frag_at(base + REGA, PB, c, 32 * (wn * NT + t));
+        af[t] = frag_at(base, NS > 0 ? RBA : PA, c, 32 * (wm * NT + t));
+        bf[t] = frag_at(bbase, NS > 0 ? RBB : PB, c, 32 * (wn * NT + t));
       }
 #pragma unroll
       for (int a = 0; a < NT; ++a)
@@ -1239,6 +1253,80 @@ k_gemm_dw_tr(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __rest
     }
   };
 
+  if constexpr (NS > 0) {
+    // One DMA instruction of a wave fills 1 KB: 1024 / RB rows of one
+    // operand (RB = its row bytes), lane l at byte 16 l (physical segment
+    // l % (RB / 16) of its row, holding the logical segment of that index
+    // ^ 4 (row & 3)).  A stage is GA such groups of A rows and GB of B rows,
+    // dealt to the waves round-robin.  A stage that reaches past row R (the
+    // last one, at most) is loaded through registers instead, with the rows
+    // past R zeroed; its loads wait for every earlier one, so the immediate
+    // vmcnt counts below stay conservative.
+    constexpr int GA = SR * RBA / 1024, GB = SR * RBB / 1024;
+    constexpr int NG = GA + GB;
+    constexpr int NW = NTH / 64;
+    static_assert(NG % NW == 0, "whole row groups per wave");
+    constexpr int GPW = NG / NW;
+    static_assert((NS - 2) * GPW <= 63, "outstanding loads exceed the vmcnt range");
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const T* dsrc[GPW];
+    int64_t dld[GPW];
+    int drow[GPW];
+#pragma unroll
+    for (int i = 0; i < GPW; ++i) {
+      const int gq = wv + i * NW;
+      const bool isA = gq < GA;
+      const int spr = (isA ? RBA : RBB) / 16;  // segments per row
+      const int row = (isA ? gq : gq - GA) * (64 / spr) + lane / spr;
+      const int sg = (lane % spr) ^ (4 * (row & 3));
+      int col = (isA ? n0 : j0) + sg * 8;
+      const int lim = isA ? N : J;
+      if (col >= lim) col = lim - 8;
+      dsrc[i] = (isA ? A : B) + (int64_t)row * (isA ? lda : ldh) + col;
+      dld[i] = isA ? lda : ldh;
+      drow[i] = row;
+    }
+    auto issue = [&](int sc, int buf) {
+      const int64_t k0 = krow(sc);
+      char* dst = lds + buf * DSTAGE;
+      if (k0 + SR <= r1) {
+#pragma unroll
+        for (int i = 0; i < GPW; ++i)
+          __builtin_amdgcn_global_load_lds((const void*)(dsrc[i] + k0 * dld[i]),
+                                           (lds_ptr_t)(dst + (wv + i * NW) * 1024), 16, 0, 0);
+      } else {
+        u32x4 v[GPW];
+#pragma unroll
+        for (int i = 0; i < GPW; ++i) {
+          const bool ok = k0 + drow[i] < r1;
+          v[i] = ok ? *(const u32x4*)(dsrc[i] + k0 * dld[i]) : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int i = 0; i < GPW; ++i) *(u32x4*)(dst + (wv + i * NW) * 1024 + lane * 16) = v[i];
+      }
+    };
+#pragma unroll
+    for (int b = 0; b < NS - 1; ++b)
+      if (b < nst) issue(b, b);
+    int stg = 0;
+    for (int sc = 0; sc < nst; ++sc) {
+      const int later = nst - 1 - sc;
+      if constexpr (NS >= 4) {
+        if (later >= 2) wait_vmcnt<2 * GPW>();
+        else if (later == 1) wait_vmcnt<GPW>();
+        else wait_vmcnt<0>();
+      } else if constexpr (NS == 3) {
+        if (later >= 1) wait_vmcnt<GPW>();
+        else wait_vmcnt<0>();
+      } else {
+        wait_vmcnt<0>();
+      }
+      lds_sync();
+      if (sc + NS - 1 < nst) issue(sc + NS - 1, stg == 0 ? NS - 1 : stg - 1);
+      compute(stg, krow(sc));
+      stg = stg + 1 == NS ? 0 : stg + 1;
+    }
+  } else {
   // ring of NB register stages (as in k_gemm_dw)
   u32x4 bufs[NB][PPT];
   const int last = nst > 0 ? nst - 1 : 0;
@@ -1258,6 +1346,7 @@ k_gemm_dw_tr(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __rest
       gload(bufs[(u + 1) % NB], krow(sc + 1 + NB < last ? sc + 1 + NB : last));
       lds_sync();
     }
+  }
   }
 
   const int hh = lane >> 5;
@@ -1291,11 +1380,12 @@ k_gemm_dw_tr(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __rest
 // ---------------------------------------------------------------------------
 namespace {
 
-// Tiles.  A wave owns 32 points x 32*NT columns of every stream: NT = 4 / 2 /
-// 1 for 1 / 2 / 3+ streams (2 x 2 waves, two waves per SIMD); narrow layers
-// (N <= 32) use 4 x 1 waves.  (Larger block tiles at one wave per SIMD, and
-// 2 x 4 wave blocks, measured slower: the loop is latency-bound, so occupancy
-// matters more than per-block intensity.)
+// Tiles.  A wave owns 32 points x 32*NT columns of every stream.  Layers
+// below the wide path: NT = 4 / 2 / 1 for 1 / 2 / 3+ streams (2 x 2 waves,
+// two waves per SIMD), and 4 x 1 waves for narrow layers (N <= 32).  The wide
+// path (K >= 512, N >= 256) stages operands straight into an LDS ring, which
+// hides the load latency that otherwise bounds it, and uses the block shapes
+// measured fastest per stream count.
 }  // namespace
 
 bool nt_resident_ok(int elem_bytes, int C, int K, int N, int64_t n_points, int64_t ldx, int64_t ldo) {
@@ -1406,11 +1496,14 @@ hipError_t launch_gemm_nt(int epi, int nd1, int nd2, const NtArgs<T>& a, int G, 
 
 void dw_split_plan(int64_t R, int N, int J, int elem_bytes, int G, int* n_split, int64_t* rows_per_split) {
   const int SR = 64 / elem_bytes;
-  const int bt = (N >= 128 && J >= 128) ? 128 : ((N >= 64 && J >= 64) ? 64 : 32);
+  // 16-bit storage, both sides >= 512: 256 x 256 tiles of 16 waves, about
+  // 512 blocks; otherwise about 1024 blocks of the 128 x 128 (or smaller)
+  // tile grid, and 512 for a single output tile (each split writes a whole
+  // N x J fp32 partial, and one resident wave of blocks suffices)
+  const bool big = elem_bytes == 2 && N >= 512 && J >= 512;
+  const int bt = big ? 256 : (N >= 128 && J >= 128) ? 128 : ((N >= 64 && J >= 64) ? 64 : 32);
   const int64_t tiles = (int64_t)((N + bt - 1) / bt) * ((J + bt - 1) / bt) * G;
-  // about 1024 blocks; a single output tile takes 512 (each split writes a
-  // whole N x J fp32 partial, and one resident wave of blocks suffices)
-  const int64_t target = tiles > 1 ? 1024 : 512;
+  const int64_t target = big || tiles == 1 ? 512 : 1024;
   int64_t want = (target + tiles - 1) / tiles;
   const int64_t stages = (R + SR - 1) / SR;
   int64_t max_split = stages / 4 > 0 ? stages / 4 : 1;
@@ -1431,10 +1524,23 @@ hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int
                           int n_split, int64_t rows_per_split, int G, hipStream_t st) {
   if (R <= 0) return hipSuccess;
   if constexpr (sizeof(T) == 2) {
-    if (N >= 128 && J >= 128) {
+    // operand stages straight into an LDS ring; 64 x 64 columns per wave.
+    // Block shapes per width are the fastest measured.
+    if (N >= 512 && J >= 512) {
+      // 256 x 256, 16 waves, 2-stage ring
+      dim3 grid((unsigned)(((N + 255) / 256) * ((J + 255) / 256)) * n_split, 1, G);
+      k_gemm_dw_tr<T, 4, 4, 2, 4, 2, 1><<<grid, 1024, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial,
+                                                              pdb, n_split, rows_per_split);
+    } else if (N >= 128 && J >= 256) {
+      // 128 x 256, 8 waves, 3-stage ring
+      dim3 grid((unsigned)(((N + 127) / 128) * ((J + 255) / 256)) * n_split, 1, G);
+      k_gemm_dw_tr<T, 2, 4, 2, 4, 3, 1><<<grid, 512, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial,
+                                                             pdb, n_split, rows_per_split);
+    } else if (N >= 128 && J >= 128) {
+      // 128 x 128, 4 waves, 3-stage ring
       dim3 grid((unsigned)(((N + 127) / 128) * ((J + 127) / 128)) * n_split, 1, G);
-      k_gemm_dw_tr<T, 2, 2, 2, 4><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
-                                                       n_split, rows_per_split);
+      k_gemm_dw_tr<T, 2, 2, 2, 4, 3><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
+                                                          n_split, rows_per_split);
     } else if (N >= 64 && J >= 64) {
       dim3 grid((unsigned)(((N + 63) / 64) * ((J + 63) / 64)) * n_split, 1, G);
       k_gemm_dw_tr<T, 2, 2, 1, 4><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
