@@ -1383,7 +1383,7 @@ namespace {
 // Tiles.  A wave owns 32 points x 32*NT columns of every stream.  Layers
 // below the wide path: NT = 4 / 2 / 1 for 1 / 2 / 3+ streams (2 x 2 waves,
 // two waves per SIMD), and 4 x 1 waves for narrow layers (N <= 32).  The wide
-// path (K >= 512, N >= 256) stages operands straight into an LDS ring, which
+// path (K, N >= 256) stages operands straight into an LDS ring, which
 // hides the load latency that otherwise bounds it, and uses the block shapes
 // measured fastest per stream count.
 }  // namespace
@@ -1434,30 +1434,44 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   if (a.N <= 32) {
     dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 31) / 32)), 1, G);
     k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, (C >= 4 ? 1 : 2)><<<grid, 256, 0, st>>>(a);
-  } else if (wide_ok<T, C>() && a.K >= 512 && a.N >= 256) {
-    // wide layers (matrix-core bound): operand stages loaded straight into an
-    // LDS ring several stages ahead, larger wave tiles (fewer LDS fragment
-    // reads per MFMA) and fewer L2 re-reads of each activation tile.  Tile
-    // shapes are the fastest measured per stream count and epilogue.
+  } else if (wide_ok<T, C>() && a.K >= 256 && a.N >= 256 && !(C == 3 && EPI == EPI_BWD && a.K < 512)) {
+    // wide layers: operand stages loaded straight into an LDS ring several
+    // stages ahead, larger wave tiles (fewer LDS fragment reads per MFMA) and
+    // fewer L2 re-reads of each activation tile.  Tile shapes are the
+    // fastest measured per stream count, epilogue and depth (K = 256 layers
+    // are bound by HBM traffic, K >= 512 by the matrix cores).
+    const bool deep = a.K >= 512;
     if constexpr (!wide_ok<T, C>()) {
       return hipErrorInvalidValue;
     } else if constexpr (C == 1) {
       if constexpr (EPI == EPI_BWD) {
-        // 128 points x 256 columns, 2 x 4 fragments per wave, 3-stage ring
-        dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 255) / 256)), 1, G);
-        k_gemm_nt<T, ND1, ND2, 2, 2, 2, 4, EPI, 2, true, 3><<<grid, 256, 0, st>>>(a);
-      } else {
+        if (deep) {
+          // 128 points x 256 columns, 2 x 4 fragments per wave, 3-stage ring
+          dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 255) / 256)), 1, G);
+          k_gemm_nt<T, ND1, ND2, 2, 2, 2, 4, EPI, 2, true, 3><<<grid, 256, 0, st>>>(a);
+          return hipGetLastError();
+        }
+      }
+      {
         // 128 points x 128 columns, 2 x 2 fragments per wave, 3-stage ring
         dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 127) / 128)), 1, G);
         k_gemm_nt<T, ND1, ND2, 2, 2, 2, 2, EPI, 2, true, 3><<<grid, 256, 0, st>>>(a);
       }
     } else if constexpr (C == 5 && EPI == EPI_BWD) {
-      // eight waves (2 x 4), 64 points x 128 columns, 4-stage ring
+      // eight waves (2 x 4), 64 points x 128 columns, 4- (3-) stage ring
       dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + 127) / 128)), 1, G);
-      k_gemm_nt<T, ND1, ND2, 2, 4, 1, 1, EPI, 2, true, 4><<<grid, 512, 0, st>>>(a);
+      if (deep) k_gemm_nt<T, ND1, ND2, 2, 4, 1, 1, EPI, 2, true, 4><<<grid, 512, 0, st>>>(a);
+      else k_gemm_nt<T, ND1, ND2, 2, 4, 1, 1, EPI, 2, true, 3><<<grid, 512, 0, st>>>(a);
     } else {
-      // three or five streams: eight waves (2 x 4), 64 points x 256 columns,
-      // 4-stage ring
+      if constexpr (C == 3 && EPI == EPI_FWD) {
+        if (!deep) {
+          // eight waves (2 x 4), 64 points x 128 columns, 4-stage ring
+          dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + 127) / 128)), 1, G);
+          k_gemm_nt<T, ND1, ND2, 2, 4, 1, 1, EPI, 2, true, 4><<<grid, 512, 0, st>>>(a);
+          return hipGetLastError();
+        }
+      }
+      // eight waves (2 x 4), 64 points x 256 columns, 4-stage ring
       dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + 255) / 256)), 1, G);
       k_gemm_nt<T, ND1, ND2, 2, 4, 1, 2, EPI, 1, false, 4><<<grid, 512, 0, st>>>(a);
     }
