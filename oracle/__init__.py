@@ -8,4 +8,6 @@ from .pigan_oracle import (  # noqa: F401
     darcy_residual, sensor_rows, colloc_rows, gen_jets, snapshots,
     train_step_group, train_step, real_snapshots,
     critic_input_grad, tangent_output_grad, gradient_penalty,
+    trunk_unpack, trunk_pack, trunk_skip, trunk_forward, trunk_backward, trunk_snapshots,
+    train_step_group_trunk, train_step_trunk, real_snapshots_trunk,
 )

@@ -10,7 +10,9 @@ the definitions state):
 * Generator networks G(x, z) for Y = log k and for the head u: a tanh MLP on the
   narrow input [x_1..x_d, z_1..z_nz] (one location plus the noise vector,
   Sec. III.C "Single Node optimizations"), L tanh layers of width W, then a
-  linear scalar output.
+  linear scalar output.  Or the paper's own generator (same section): one
+  shared tanh trunk with residual skips over pairs of layers and a linear
+  two-output head (Y, u); see trunk_forward.
 * Exact spatial jets (value, d/dx_i, d^2/dx_i^2) of the generator, carried
   forward layer by layer by the chain rule.  The paper obtains the source term
   f by applying the differential operator to the generator with automatic
@@ -274,6 +276,195 @@ def gen_backward(params, shape, d: int, X, Z, fwd, g_y, g_dy=None, g_ddy=None, p
                 gW1[:, i] += num.colsum(gda[i])   # a'_i = W1[:, i] for every row
             grads[0] = (gW1, num.colsum(ga))
     return pack(grads, gw_out, gb_out)
+
+
+# ----------------------------------------------------------------------------
+# shared-trunk generator: one network with a log-conductivity head and a head
+# for u (the paper's own generator, Sec. III.C "Single Node optimizations")
+# ----------------------------------------------------------------------------
+
+def trunk_unpack(params, in_dim: int, L: int, W: int):
+    """Split a packed trunk vector [W1, b1, ..., W_L, b_L, w_Y, b_Y, w_u, b_u]
+    into ([(W_l, b_l)], [(w_Y, b_Y), (w_u, b_u)])."""
+    p = np.asarray(params, dtype=F64).reshape(-1)
+    layers = []
+    off = 0
+    fan = in_dim
+    for _ in range(L):
+        Wl = p[off:off + W * fan].reshape(W, fan)
+        off += W * fan
+        bl = p[off:off + W]
+        off += W
+        layers.append((Wl, bl))
+        fan = W
+    heads = []
+    for _ in range(2):
+        w = p[off:off + W]
+        off += W
+        b = float(p[off])
+        off += 1
+        heads.append((w, b))
+    if off != p.size:
+        raise ValueError(f"parameter vector has {p.size} entries, trunk shape needs {off}")
+    return layers, heads
+
+
+def trunk_pack(layer_grads, head_grads) -> np.ndarray:
+    parts = []
+    for gW, gb in layer_grads:
+        parts.append(np.asarray(gW, F64).reshape(-1))
+        parts.append(np.asarray(gb, F64).reshape(-1))
+    for gw, gb in head_grads:
+        parts.append(np.asarray(gw, F64).reshape(-1))
+        parts.append(np.array([gb], F64))
+    return np.concatenate(parts)
+
+
+def trunk_skip(l: int) -> bool:
+    """Whether layer l (1-based) adds the activation of layer l - 2: after the
+    first layer, every pair of layers is one residual block whose output is
+    its second tanh plus the block's input (the paper's depths 5, 11 and 21
+    are one layer plus 2, 5 and 10 such blocks)."""
+    return l >= 3 and l % 2 == 1
+
+
+def trunk_forward(params, shape, d: int, X, Z, order: int, keep: bool = False, prec=None):
+    """Evaluate the trunk and the jets of both heads at rows (X[n], Z[n]).
+
+    h_1 = tanh(W_1 [x ; z] + b_1); h_l = tanh(W_l h_{l-1} + b_l), plus h_{l-2}
+    when trunk_skip(l).  Heads Y = w_Y . h_L + b_Y and u = w_u . h_L + b_u
+    (biases on the value only).  The skip is linear, so every jet stream of
+    h_{l-2} is added to the same stream of h_l.  Returns dict(Y, dY, ddY, u,
+    du, ddu) with dY/du [d, N] (order >= 1) and ddY/ddu [d, N] (order 2).
+    """
+    in_dim, L, W = shape
+    num = prec if isinstance(prec, _Num) else _Num(prec)
+    q = num.q
+    layers, heads = trunk_unpack(params, in_dim, L, W)
+    X = np.asarray(X, F64)
+    Z = np.asarray(Z, F64)
+    N = X.shape[0]
+    W1, b1 = layers[0]
+    a = X @ W1[:, :d].T + Z @ W1[:, d:].T + b1
+    da = [np.broadcast_to(W1[:, i], (N, W)).copy() for i in range(d)] if order >= 1 else []
+    dda = [np.zeros((N, W), F64) for _ in range(d)] if order >= 2 else []
+    acts = [None]          # acts[l] = (h, dh, ddh) of layer l, 1-based
+    cache = []
+    h = dh = ddh = None
+    for l in range(1, L + 1):
+        if l > 1:
+            Wl, bl = layers[l - 1]
+            Wq = q(Wl).T
+            a = num.mm(h, Wq) + bl
+            da = [num.mm(g, Wq) for g in dh]
+            dda = [num.mm(g, Wq) for g in ddh]
+        t, s, sp, _ = _tanh_derivs(a)
+        if keep:
+            cache.append((q(a), [q(g) for g in da], [q(g) for g in dda], (h, dh, ddh)))
+        nh = t
+        ndh = [s * g for g in da]
+        nddh = [s * g2 + sp * g1 * g1 for g1, g2 in zip(da, dda)]
+        if trunk_skip(l):
+            sh, sdh, sddh = acts[l - 2]
+            nh = nh + sh
+            ndh = [g + gs for g, gs in zip(ndh, sdh)]
+            nddh = [g + gs for g, gs in zip(nddh, sddh)]
+        h = q(nh)
+        dh = [q(g) for g in ndh]
+        ddh = [q(g) for g in nddh]
+        acts.append((h, dh, ddh))
+    out = {}
+    for name, (w, b) in zip(("Y", "u"), heads):
+        out[name] = h @ w + b
+        out["d" + name] = np.stack([g @ w for g in dh]) if order >= 1 else None
+        out["dd" + name] = np.stack([g @ w for g in ddh]) if order >= 2 else None
+    if keep:
+        out["cache"] = cache
+        out["top"] = (h, dh, ddh)
+    return out
+
+
+def trunk_backward(params, shape, d: int, X, Z, fwd, gY=None, gdY=None, gddY=None, gu=None, gdu=None, gddu=None,
+                   prec=None) -> np.ndarray:
+    """Reverse pass of trunk_forward (keep=True) for cotangents of the head
+    jets (each [N] or [d, N]; None means zero).  Returns the packed gradient."""
+    in_dim, L, W = shape
+    num = prec if isinstance(prec, _Num) else _Num(prec)
+    q = num.q
+    layers, heads = trunk_unpack(params, in_dim, L, W)
+    X = np.asarray(X, F64)
+    Z = np.asarray(Z, F64)
+    N = X.shape[0]
+    hL, dhL, ddhL = fwd["top"]
+    nd1, nd2 = len(dhL), len(ddhL)
+
+    def cot(v, nd):
+        if nd == 0:
+            return []
+        return [np.zeros(N, F64) if v is None else np.asarray(v[i], F64) for i in range(nd)]
+
+    g_heads = [(np.zeros(N, F64) if gY is None else np.asarray(gY, F64), cot(gdY, nd1), cot(gddY, nd2)),
+               (np.zeros(N, F64) if gu is None else np.asarray(gu, F64), cot(gdu, nd1), cot(gddu, nd2))]
+    head_grads = []
+    gh = np.zeros((N, W), F64)
+    gdh = [np.zeros((N, W), F64) for _ in range(nd1)]
+    gddh = [np.zeros((N, W), F64) for _ in range(nd2)]
+    for (w, _), (g0, g1, g2) in zip(heads, g_heads):
+        gw = hL.T @ g0
+        for i in range(nd1):
+            gw = gw + dhL[i].T @ g1[i]
+        for i in range(nd2):
+            gw = gw + ddhL[i].T @ g2[i]
+        head_grads.append((gw, g0.sum()))
+        gh = gh + np.outer(g0, w)
+        gdh = [a + np.outer(g, w) for a, g in zip(gdh, g1)]
+        gddh = [a + np.outer(g, w) for a, g in zip(gddh, g2)]
+    pending = {}           # layer l - 2 -> total cotangent of h_l carried by the skip
+    grads = [None] * L
+    for l in range(L, 0, -1):
+        if l in pending:   # h_l is the input of a residual block: add the skip's cotangent
+            sg, sdg, sddg = pending.pop(l)
+            gh = gh + sg
+            gdh = [a + b for a, b in zip(gdh, sdg)]
+            gddh = [a + b for a, b in zip(gddh, sddg)]
+        if trunk_skip(l):
+            pending[l - 2] = (q(gh), [q(g) for g in gdh], [q(g) for g in gddh])
+        a, da, dda, prev = fwd["cache"][l - 1]
+        t, s, sp, spp = _tanh_derivs(a)
+        ga = s * gh
+        for i in range(nd1):
+            ga = ga + sp * da[i] * gdh[i]
+        for i in range(nd2):
+            ga = ga + (sp * dda[i] + spp * da[i] * da[i]) * gddh[i]
+        gda = []
+        for i in range(nd1):
+            g = s * gdh[i]
+            if nd2:
+                g = g + 2.0 * sp * da[i] * gddh[i]
+            gda.append(q(g))
+        gdda = [q(s * g) for g in gddh]
+        ga = q(ga)
+        if l > 1:
+            Wl, _ = layers[l - 1]
+            h, dh, ddh = prev
+            gW = num.mm(ga.T, h)
+            for i in range(nd1):
+                gW = gW + num.mm(gda[i].T, dh[i])
+            for i in range(nd2):
+                gW = gW + num.mm(gdda[i].T, ddh[i])
+            grads[l - 1] = (gW, num.colsum(ga))
+            Wq = q(Wl)
+            gh = num.mm(ga, Wq)
+            gdh = [num.mm(g, Wq) for g in gda]
+            gddh = [num.mm(g, Wq) for g in gdda]
+        else:
+            gW1 = np.zeros((W, in_dim), F64)
+            gW1[:, :d] = ga.T @ X
+            gW1[:, d:] = ga.T @ Z
+            for i in range(nd1):
+                gW1[:, i] += num.colsum(gda[i])
+            grads[0] = (gW1, num.colsum(ga))
+    return trunk_pack(grads, head_grads)
 
 
 # ----------------------------------------------------------------------------
@@ -584,6 +775,105 @@ def train_step(wl, inp, real, lambda_pde=None, chunk_S=None, prec=None, lambda_g
                 gU=np.stack([o["gU"] for o in outs]),
                 gD=np.stack([o["gD"] for o in outs]),
                 P_gp=np.array([o["P_gp"] for o in outs]))
+
+
+def trunk_snapshots(pT, shape, d, xsY, xsU, z):
+    """Sensor snapshots of a trunk generator: [Y head at Y sensors | u head at u sensors]."""
+    S = np.asarray(z).shape[0]
+    XY, ZY = sensor_rows(xsY, z)
+    XU, ZU = sensor_rows(xsU, z)
+    yY = trunk_forward(pT, shape, d, XY, ZY, 0)["Y"].reshape(S, -1)
+    yU = trunk_forward(pT, shape, d, XU, ZU, 0)["u"].reshape(S, -1)
+    return np.concatenate([yY, yU], axis=1)
+
+
+def train_step_group_trunk(gshape, dshape, d, pT, pD, z, xc, xsY, xsU, f, real,
+                           w=1.0, lambda_pde=1.0, chunk_S=None, prec=None):
+    """One group's losses and gradients with the shared-trunk generator.
+
+    Same losses as train_step_group; both heads come from one network, so one
+    gradient gT of L_G = L_adv + L_pde is returned.  Returns dict(L_D, L_adv,
+    L_pde, gT, gD)."""
+    z = np.asarray(z, F64)
+    xc = np.asarray(xc, F64)
+    f = np.asarray(f, F64)
+    real = np.asarray(real, F64)
+    S, P = xc.shape[0], xc.shape[1]
+    B = real.shape[0]
+    nY = np.asarray(xsY).shape[0]
+    chunk_S = S if not chunk_S else chunk_S
+    if prec == "fp32":
+        with _working_type(np.float32):
+            return train_step_group_trunk(gshape, dshape, d, pT, pD, z, xc, xsY, xsU, f, real, w=w,
+                                          lambda_pde=lambda_pde, chunk_S=chunk_S, prec=None)
+    num = _Num(prec)
+    gT = np.zeros(np.asarray(pT).size, F64)
+    gD = np.zeros(np.asarray(pD).size, F64)
+    sum_DF = 0.0
+    sum_r2 = 0.0
+    DR, hsR = mlp_forward(pD, dshape, real, keep=True, prec=num)
+    gD += mlp_backward(pD, dshape, hsR, np.full(B, -w / B, F64), prec=num)
+    sum_DR = DR.sum()
+    for s0 in range(0, S, chunk_S):
+        sl = slice(s0, min(S, s0 + chunk_S))
+        zc = z[sl]
+        Sc = zc.shape[0]
+        # trunk at the Y sensors (Y head) and at the u sensors (u head)
+        XY, ZY = sensor_rows(xsY, zc)
+        XU, ZU = sensor_rows(xsU, zc)
+        fY_s = trunk_forward(pT, gshape, d, XY, ZY, 0, keep=True, prec=num)
+        fU_s = trunk_forward(pT, gshape, d, XU, ZU, 0, keep=True, prec=num)
+        F = np.concatenate([fY_s["Y"].reshape(Sc, -1), fU_s["u"].reshape(Sc, -1)], axis=1)
+        # trunk at the collocation points: jets of both heads
+        XC, ZC = colloc_rows(xc[sl], zc)
+        jc = trunk_forward(pT, gshape, d, XC, ZC, 2, keep=True, prec=num)
+        fc = f[sl].reshape(-1)
+        r = darcy_residual(jc["Y"], jc["dY"], jc["du"], jc["ddu"], fc)
+        sum_r2 += float((r * r).sum())
+        DF, hsF = mlp_forward(pD, dshape, F, keep=True, prec=num)
+        sum_DF += float(DF.sum())
+        gDc, gF = mlp_backward(pD, dshape, hsF, np.full(Sc, w / S, F64), want_input_grad=True, prec=num)
+        gD += gDc
+        gF = -gF
+        q = 2.0 * w * lambda_pde * r / (S * P)
+        eY = np.exp(jc["Y"])
+        g_Yval = q * (r + fc)
+        g_Ydy = np.stack([-q * eY * jc["du"][i] for i in range(d)])
+        g_Udy = np.stack([-q * eY * jc["dY"][i] for i in range(d)])
+        g_Uddy = np.stack([-q * eY for _ in range(d)])
+        gT += trunk_backward(pT, gshape, d, XY, ZY, fY_s, gY=gF[:, :nY].reshape(-1), prec=num)
+        gT += trunk_backward(pT, gshape, d, XU, ZU, fU_s, gu=gF[:, nY:].reshape(-1), prec=num)
+        gT += trunk_backward(pT, gshape, d, XC, ZC, jc, gY=g_Yval, gdY=g_Ydy, gdu=g_Udy, gddu=g_Uddy, prec=num)
+    L_D = w * (sum_DF / S - sum_DR / B)
+    L_adv = -w * sum_DF / S
+    L_pde = w * lambda_pde * sum_r2 / (S * P)
+    return dict(L_D=L_D, L_adv=L_adv, L_pde=L_pde, gT=gT, gD=gD)
+
+
+def train_step_trunk(wl, inp, real, lambda_pde=None, chunk_S=None, prec=None):
+    """All groups of a trunk workload (inp.pT holds the trunk weights).
+    Returns loss [G, 3], gT [G, nT], gD [G, nD]."""
+    lam = wl.lambda_pde if lambda_pde is None else lambda_pde
+    gshape = (wl.d + wl.n_z, wl.L, wl.W)
+    dshape = (wl.n_sY + wl.n_sU, wl.L_D, wl.W_D)
+    G = inp.z.shape[0]
+    S, P = inp.xc.shape[1], inp.xc.shape[2]
+    outs = []
+    for g in range(G):
+        f = inp.f[g] if inp.f is not None else np.full((S, P), inp.f_const)
+        outs.append(train_step_group_trunk(gshape, dshape, wl.d, inp.pT[g], inp.pD[g], inp.z[g], inp.xc[g],
+                                           inp.xsY[g], inp.xsU[g], f, real[g], w=float(inp.w_group[g]),
+                                           lambda_pde=lam, chunk_S=chunk_S, prec=prec))
+    return dict(loss=np.array([[o["L_D"], o["L_adv"], o["L_pde"]] for o in outs]),
+                gT=np.stack([o["gT"] for o in outs]),
+                gD=np.stack([o["gD"] for o in outs]))
+
+
+def real_snapshots_trunk(wl, inp):
+    """Teacher snapshots [G, B_r, n_in] of a trunk workload (teacher trunk inp.tT)."""
+    gshape = (wl.d + wl.n_z, wl.L, wl.W)
+    return np.stack([trunk_snapshots(inp.tT[g], gshape, wl.d, inp.xsY[g], inp.xsU[g], inp.z_teach[g])
+                     for g in range(inp.z.shape[0])])
 
 
 def real_snapshots(wl, inp):

@@ -35,6 +35,7 @@ class Workload:
     f_const: float      # source term used when no f array is given
     lambda_pde: float = 1.0
     seed: int = 1910
+    arch: str = "pair"  # "pair": two tanh MLPs (Y, u); "trunk": one shared trunk, two heads
 
     @property
     def n_in(self) -> int:
@@ -73,6 +74,12 @@ def n_params(in_dim: int, L: int, W: int) -> int:
     return W * in_dim + W + (L - 1) * (W * W + W) + W + 1
 
 
+def n_params_trunk(in_dim: int, L: int, W: int) -> int:
+    """Parameter count of a shared trunk packed as
+    [W1, b1, ..., W_L, b_L, w_Y (W), b_Y, w_u (W), b_u]."""
+    return n_params(in_dim, L, W) + W + 1
+
+
 C1 = Workload("darcy1d_toy_fp32", "fp32", G=1, d=1, n_z=4, L=3, W=32, S=64, P=32,
               n_sY=8, n_sU=8, L_D=2, W_D=32, B_r=64, f_const=1.0, seed=1911)
 C2 = Workload("darcy2d_w128_bf16", "bf16", G=1, d=2, n_z=20, L=4, W=128, S=256, P=1024,
@@ -85,8 +92,15 @@ C5 = Workload("bigstep_w1024_disc2048_bf16", "bf16", G=1, d=2, n_z=128, L=6, W=1
               P=2048, n_sY=4096, n_sU=4096, L_D=5, W_D=2048, B_r=1024, f_const=0.0, seed=1915)
 C5H = C5.with_(name="bigstep_w1024_disc2048_fp16", dtype="fp16")
 
-WORKLOADS = {w.name: w for w in (C1, C2, C3, C4, C5, C5H)}
-ALIASES = {"c1": C1, "c2": C2, "c3": C3, "c4": C4, "c5": C5, "c5h": C5H}
+# The paper's own generator: one shared trunk of 5 x 128, 11 x 512 or 21 x 1024
+# tanh layers (Sec. III.C) with residual blocks and two heads, on the sample,
+# point and sensor counts of the 2-D, thousand-sensor and large-step workloads.
+T5 = C2.with_(name="trunk5x128_darcy2d_bf16", L=5, arch="trunk", seed=1921)
+T11 = C3.with_(name="trunk11x512_sd1000_bf16", L=11, arch="trunk", seed=1922)
+T21 = C5.with_(name="trunk21x1024_bigstep_bf16", L=21, arch="trunk", seed=1923)
+
+WORKLOADS = {w.name: w for w in (C1, C2, C3, C4, C5, C5H, T5, T11, T21)}
+ALIASES = {"c1": C1, "c2": C2, "c3": C3, "c4": C4, "c5": C5, "c5h": C5H, "t5": T5, "t11": T11, "t21": T21}
 
 
 def get(name: str) -> Workload:

@@ -19,7 +19,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from .configs import Workload, n_params
+from .configs import Workload, n_params, n_params_trunk
 
 _ROLES = ("genY", "genU", "disc", "teachY", "teachU", "z", "z_teach", "xc", "xsY", "xsU", "f")
 
@@ -44,6 +44,24 @@ def glorot_mlp(rng: np.random.Generator, in_dim: int, L: int, W: int) -> np.ndar
     return out
 
 
+def glorot_trunk(rng: np.random.Generator, in_dim: int, L: int, W: int) -> np.ndarray:
+    """One packed trunk vector [W1, b1, ..., W_L, b_L, w_Y, b_Y, w_u, b_u] (float32):
+    Glorot-normal layers as glorot_mlp, the two heads as one 2 x W matrix."""
+    out = np.zeros(n_params_trunk(in_dim, L, W), dtype=np.float32)
+    off = 0
+    fan_in = in_dim
+    for _ in range(L):
+        std = np.sqrt(2.0 / (fan_in + W))
+        out[off:off + W * fan_in] = rng.standard_normal(W * fan_in) * std
+        off += W * fan_in + W
+        fan_in = W
+    std = np.sqrt(2.0 / (W + 2))
+    for _ in range(2):
+        out[off:off + W] = rng.standard_normal(W) * std
+        off += W + 1
+    return out
+
+
 @dataclass
 class StepInputs:
     """Everything one training step consumes except the real snapshots."""
@@ -60,6 +78,8 @@ class StepInputs:
     f: np.ndarray | None  # [G, S, P] or None (then f_const is used)
     f_const: float
     w_group: np.ndarray   # [G]
+    pT: np.ndarray | None = None   # [G, nT] shared-trunk weights (trunk workloads; then pY..tU are None)
+    tT: np.ndarray | None = None   # [G, nT] teacher trunk
 
 
 def make_inputs(wl: Workload, seed: int | None = None, f_array: bool = False,
@@ -75,11 +95,17 @@ def make_inputs(wl: Workload, seed: int | None = None, f_array: bool = False,
     def nets(rng, in_dim, L, W):
         return np.stack([glorot_mlp(rng, in_dim, L, W) for _ in range(G)])
 
-    pY = nets(r["genY"], wl.in_dim, wl.L, wl.W)
-    pU = nets(r["genU"], wl.in_dim, wl.L, wl.W)
+    pT = tT = None
+    if wl.arch == "trunk":
+        pT = np.stack([glorot_trunk(r["genY"], wl.in_dim, wl.L, wl.W) for _ in range(G)])
+        tT = np.stack([glorot_trunk(r["teachY"], wl.in_dim, wl.L, wl.W) for _ in range(G)])
+        pY = pU = tY = tU = None
+    else:
+        pY = nets(r["genY"], wl.in_dim, wl.L, wl.W)
+        pU = nets(r["genU"], wl.in_dim, wl.L, wl.W)
+        tY = nets(r["teachY"], wl.in_dim, wl.L, wl.W)
+        tU = nets(r["teachU"], wl.in_dim, wl.L, wl.W)
     pD = nets(r["disc"], wl.n_in, wl.L_D, wl.W_D)
-    tY = nets(r["teachY"], wl.in_dim, wl.L, wl.W)
-    tU = nets(r["teachU"], wl.in_dim, wl.L, wl.W)
     z = r["z"].standard_normal((G, S, wl.n_z)).astype(np.float32)
     zt = r["z_teach"].standard_normal((G, B_r, wl.n_z)).astype(np.float32)
     xc = r["xc"].random((G, S, wl.P, wl.d)).astype(np.float32)
@@ -87,4 +113,4 @@ def make_inputs(wl: Workload, seed: int | None = None, f_array: bool = False,
     xsU = r["xsU"].random((G, wl.n_sU, wl.d)).astype(np.float32)
     f = r["f"].standard_normal((G, S, wl.P)).astype(np.float32) if f_array else None
     wg = np.full((G,), wl.w_group, dtype=np.float32)
-    return StepInputs(pY, pU, pD, tY, tU, z, zt, xc, xsY, xsU, f, wl.f_const, wg)
+    return StepInputs(pY, pU, pD, tY, tU, z, zt, xc, xsY, xsU, f, wl.f_const, wg, pT, tT)

@@ -1,0 +1,225 @@
+"""Pins of the oracle's shared-trunk generator (the paper's own generator,
+Sec. III.C): finite differences of the head jets and of every weight gradient,
+torch.autograd in float64, reduction to the plain-MLP oracle where no skip is
+present, a closed form through one residual block, and chunking invariance."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1910_13444_amd.configs import Workload
+from paper_1910_13444_amd.inputs import glorot_trunk, make_inputs
+
+torch.set_default_dtype(torch.float64)
+
+TT = Workload("tinytrunk", "fp32", G=1, d=2, n_z=2, L=3, W=3, S=2, P=2, n_sY=2, n_sU=2,
+              L_D=1, W_D=3, B_r=2, f_const=0.5, seed=17, arch="trunk")
+
+
+def _rand_trunk(seed, in_dim, L, W, scale=0.7):
+    rng = np.random.default_rng(seed)
+    p = glorot_trunk(rng, in_dim, L, W).astype(np.float64)
+    return p + scale * rng.standard_normal(p.size) * (p == 0)    # nonzero biases too
+
+
+def test_skip_pattern():
+    assert [oracle.trunk_skip(l) for l in range(1, 9)] == [False, False, True, False, True, False, True, False]
+
+
+@pytest.mark.parametrize("L", [3, 4, 5])
+def test_trunk_jets_fd(L):
+    d, nz, W = 2, 2, 4
+    shape = (d + nz, L, W)
+    p = _rand_trunk(3 + L, d + nz, L, W)
+    rng = np.random.default_rng(11)
+    X = rng.random((5, d))
+    Z = rng.standard_normal((5, nz))
+    out = oracle.trunk_forward(p, shape, d, X, Z, 2)
+    for head in ("Y", "u"):
+        f0 = lambda XX: oracle.trunk_forward(p, shape, d, XX, Z, 0)[head]
+        for i in range(d):
+            e = np.zeros(d)
+            e[i] = 1.0
+            h1, h2 = 1e-6, 1e-4
+            fd1 = (f0(X + h1 * e) - f0(X - h1 * e)) / (2 * h1)
+            fd2 = (f0(X + h2 * e) - 2 * f0(X) + f0(X - h2 * e)) / (h2 * h2)
+            assert np.allclose(out["d" + head][i], fd1, rtol=1e-7, atol=1e-9)
+            assert np.allclose(out["dd" + head][i], fd2, rtol=1e-5, atol=1e-6)
+
+
+def _trunk_losses(wl, inp, real, pT=None, pD=None):
+    if pT is not None:
+        inp.pT = pT[None]
+    if pD is not None:
+        inp.pD = pD[None]
+    o = oracle.train_step_trunk(wl, inp, real)
+    return o["loss"][0]
+
+
+def test_trunk_step_grads_fd():
+    inp = make_inputs(TT)
+    real = oracle.real_snapshots_trunk(TT, inp)
+    pT0 = inp.pT[0].astype(np.float64)
+    pD0 = inp.pD[0].astype(np.float64)
+    o = oracle.train_step_trunk(TT, inp, real)
+    gT, gD = o["gT"][0], o["gD"][0]
+    h = 1e-6
+    fdT = np.zeros_like(pT0)
+    for k in range(pT0.size):
+        e = np.zeros_like(pT0)
+        e[k] = h
+        lp = _trunk_losses(TT, inp, real, pT=pT0 + e, pD=pD0)
+        lm = _trunk_losses(TT, inp, real, pT=pT0 - e, pD=pD0)
+        fdT[k] = ((lp[1] + lp[2]) - (lm[1] + lm[2])) / (2 * h)     # L_G = L_adv + L_pde
+    fdD = np.zeros_like(pD0)
+    for k in range(pD0.size):
+        e = np.zeros_like(pD0)
+        e[k] = h
+        lp = _trunk_losses(TT, inp, real, pT=pT0, pD=pD0 + e)
+        lm = _trunk_losses(TT, inp, real, pT=pT0, pD=pD0 - e)
+        fdD[k] = (lp[0] - lm[0]) / (2 * h)
+    assert np.abs(gT - fdT).max() <= 1e-6 * max(1.0, np.abs(fdT).max())
+    assert np.abs(gD - fdD).max() <= 1e-6 * max(1.0, np.abs(fdD).max())
+    assert np.abs(gT).max() > 1e-3       # the check is not vacuous
+
+
+# ---------------------------------------------------------------------------
+# torch.autograd: jets by nested reverse mode, weight gradients by reverse mode
+# ---------------------------------------------------------------------------
+
+def _trunk_t(p, in_dim, L, W, inp):
+    off = 0
+    fan = in_dim
+    acts = [None]
+    h = inp
+    for l in range(1, L + 1):
+        Wm = p[off:off + W * fan].reshape(W, fan)
+        off += W * fan
+        b = p[off:off + W]
+        off += W
+        fan = W
+        h = torch.tanh(h @ Wm.T + b) + (acts[l - 2] if (l >= 3 and l % 2 == 1) else 0.0)
+        acts.append(h)
+    wY, bY = p[off:off + W], p[off + W]
+    wU, bU = p[off + W + 1:off + 2 * W + 1], p[off + 2 * W + 1]
+    return h @ wY + bY, h @ wU + bU
+
+
+def test_trunk_autograd():
+    wl = TT.with_(L=5, S=2, P=3)
+    inp = make_inputs(wl)
+    real = oracle.real_snapshots_trunk(wl, inp)
+    o = oracle.train_step_trunk(wl, inp, real)
+    d, in_dim, L, W = wl.d, wl.in_dim, wl.L, wl.W
+    pT = torch.tensor(inp.pT[0], dtype=torch.float64, requires_grad=True)
+    pD = torch.tensor(inp.pD[0], dtype=torch.float64, requires_grad=True)
+    z = torch.tensor(inp.z[0], dtype=torch.float64)
+    xc = torch.tensor(inp.xc[0], dtype=torch.float64)
+    S, P = xc.shape[0], xc.shape[1]
+    xsY = torch.tensor(inp.xsY[0], dtype=torch.float64)
+    xsU = torch.tensor(inp.xsU[0], dtype=torch.float64)
+    w = float(inp.w_group[0])
+    Ys = torch.stack([_trunk_t(pT, in_dim, L, W, torch.cat([xsY, z[s].expand(xsY.shape[0], -1)], 1))[0]
+                      for s in range(S)])
+    Us = torch.stack([_trunk_t(pT, in_dim, L, W, torch.cat([xsU, z[s].expand(xsU.shape[0], -1)], 1))[1]
+                      for s in range(S)])
+    F = torch.cat([Ys, Us], dim=1)
+    X = xc.reshape(S * P, d).clone().requires_grad_(True)
+    Zr = z.repeat_interleave(P, dim=0)
+    Y, U = _trunk_t(pT, in_dim, L, W, torch.cat([X, Zr], 1))
+    gYx = torch.autograd.grad(Y.sum(), X, create_graph=True)[0]
+    gUx = torch.autograd.grad(U.sum(), X, create_graph=True)[0]
+    lap = sum(torch.autograd.grad(gUx[:, i].sum(), X, create_graph=True)[0][:, i] for i in range(d))
+    r = -torch.exp(Y) * ((gYx * gUx).sum(1) + lap) - inp.f_const
+    dshape = wl.disc_shape()
+
+    def mlp(p, v):
+        off = 0
+        fan = dshape[0]
+        h = v
+        for _ in range(dshape[1]):
+            Wm = p[off:off + dshape[2] * fan].reshape(dshape[2], fan)
+            off += dshape[2] * fan
+            h = torch.tanh(h @ Wm.T + p[off:off + dshape[2]])
+            off += dshape[2]
+            fan = dshape[2]
+        return h @ p[off:off + dshape[2]] + p[off + dshape[2]]
+
+    DF = mlp(pD, F)
+    DR = mlp(pD, torch.tensor(real[0], dtype=torch.float64))
+    L_D = w * (DF.mean() - DR.mean())
+    L_G = -w * DF.mean() + w * wl.lambda_pde * (r * r).mean()
+    gD = torch.autograd.grad(L_D, pD, retain_graph=True)[0].numpy()
+    gT = torch.autograd.grad(L_G, pT)[0].numpy()
+    assert np.allclose(o["loss"][0], [L_D.item(), (-w * DF.mean()).item(), (L_G + w * DF.mean()).item()],
+                       rtol=1e-12, atol=1e-14)
+    assert np.abs(o["gT"][0] - gT).max() <= 1e-11 * np.abs(gT).max()
+    assert np.abs(o["gD"][0] - gD).max() <= 1e-11 * np.abs(gD).max()
+
+
+def test_trunk_without_skip_is_two_plain_heads():
+    """L <= 2 has no residual block: each head equals the plain-MLP oracle on
+    the shared layers with that head, and the trunk's reverse pass is the sum
+    of the two plain ones on the shared layers."""
+    d, nz, W, L = 2, 3, 5, 2
+    in_dim = d + nz
+    p = _rand_trunk(21, in_dim, L, W)
+    layers, heads = oracle.trunk_unpack(p, in_dim, L, W)
+    body = p[:p.size - 2 * (W + 1)]
+    plainY = np.concatenate([body, heads[0][0], [heads[0][1]]])
+    plainU = np.concatenate([body, heads[1][0], [heads[1][1]]])
+    rng = np.random.default_rng(5)
+    X = rng.random((7, d))
+    Z = rng.standard_normal((7, nz))
+    tr = oracle.trunk_forward(p, (in_dim, L, W), d, X, Z, 2, keep=True)
+    fy = oracle.gen_forward(plainY, (in_dim, L, W), d, X, Z, 2, keep=True)
+    fu = oracle.gen_forward(plainU, (in_dim, L, W), d, X, Z, 2, keep=True)
+    assert np.allclose(tr["Y"], fy["y"], rtol=0, atol=1e-14)
+    assert np.allclose(tr["ddu"], fu["ddy"], rtol=0, atol=1e-13)
+    gy, gdy, gddy = rng.standard_normal(7), rng.standard_normal((d, 7)), rng.standard_normal((d, 7))
+    gu, gdu, gddu = rng.standard_normal(7), rng.standard_normal((d, 7)), rng.standard_normal((d, 7))
+    gt = oracle.trunk_backward(p, (in_dim, L, W), d, X, Z, tr, gy, gdy, gddy, gu, gdu, gddu)
+    a = oracle.gen_backward(plainY, (in_dim, L, W), d, X, Z, fy, gy, gdy, gddy)
+    b = oracle.gen_backward(plainU, (in_dim, L, W), d, X, Z, fu, gu, gdu, gddu)
+    nb = body.size
+    assert np.allclose(gt[:nb], a[:nb] + b[:nb], rtol=1e-12, atol=1e-12)
+    assert np.allclose(gt[nb:nb + W + 1], a[nb:], rtol=1e-12, atol=1e-12)
+    assert np.allclose(gt[nb + W + 1:], b[nb:], rtol=1e-12, atol=1e-12)
+
+
+def test_trunk_closed_form_one_block():
+    """L = 3 with the block's first layer zeroed: h_2 = 0, so a_3 = b_3 and
+    h_3 = tanh(b_3) + h_1.  Then Y = w_Y . (tanh(b_3) + tanh(W_1 [x; z] + b_1))
+    + b_Y, whose derivatives are the single-layer closed forms
+    dY/dx_i = sum_j w_j s_j W1[j, i] and d2Y/dx_i2 = -2 sum_j w_j t_j s_j W1[j, i]^2."""
+    d, nz, W, L = 2, 2, 4, 3
+    in_dim = d + nz
+    p = _rand_trunk(31, in_dim, L, W)
+    layers, heads = oracle.trunk_unpack(p, in_dim, L, W)
+    off2 = W * in_dim + W
+    p[off2:off2 + W * W + W] = 0.0           # W_2 = 0, b_2 = 0
+    layers, heads = oracle.trunk_unpack(p, in_dim, L, W)
+    W1, b1 = layers[0]
+    b3 = layers[2][1]
+    rng = np.random.default_rng(9)
+    X = rng.random((6, d))
+    Z = rng.standard_normal((6, nz))
+    out = oracle.trunk_forward(p, (in_dim, L, W), d, X, Z, 2)
+    a1 = X @ W1[:, :d].T + Z @ W1[:, d:].T + b1
+    t = np.tanh(a1)
+    s = 1.0 / np.cosh(a1) ** 2
+    for name, (w, b) in zip(("Y", "u"), heads):
+        assert np.allclose(out[name], np.tanh(b3) @ w + t @ w + b, rtol=1e-13, atol=1e-13)
+        for i in range(d):
+            assert np.allclose(out["d" + name][i], (s * W1[:, i]) @ w, rtol=1e-12, atol=1e-13)
+            assert np.allclose(out["dd" + name][i], (-2.0 * t * s * W1[:, i] ** 2) @ w, rtol=1e-12, atol=1e-13)
+
+
+def test_trunk_chunking():
+    wl = TT.with_(S=3, L=5)
+    inp = make_inputs(wl)
+    real = oracle.real_snapshots_trunk(wl, inp)
+    a = oracle.train_step_trunk(wl, inp, real)
+    b = oracle.train_step_trunk(wl, inp, real, chunk_S=1)
+    for k in ("loss", "gT", "gD"):
+        assert np.allclose(a[k], b[k], rtol=1e-12, atol=1e-14)
