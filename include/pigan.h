@@ -207,6 +207,55 @@ pigan_status pigan_train_step_grads_gp(const pigan_step_desc* s, const float* pY
                                        float* loss, float* gp, int32_t* nonfinite, void* ws,
                                        size_t ws_bytes, void* stream);
 
+/*
+ * Shared-trunk generator: the paper's own generator (Sec. III.C, "Single Node
+ * optimizations"), one set of weights producing both log k and u.  A tanh
+ * trunk on [x ; z] of L layers of width W (the paper uses 5 x 128, 11 x 512
+ * and 21 x 1024); after the first layer every pair of layers is a residual
+ * block, h_l = tanh(W_l h_{l-1} + b_l) + h_{l-2} for odd l >= 3 (skips for
+ * gradient propagation, same section), then a linear head with two outputs,
+ * Y = w_Y . h_L + b_Y and u = w_u . h_L + b_u.  The spatial jets of the trunk
+ * carry 1 + 2d streams at the collocation points (u needs d2/dx_i2; Y uses
+ * the value and first-derivative streams of the same trunk).
+ *
+ * Packing per group (fp32): [W1 (W x in_dim), b1, W2, b2, ..., W_L, b_L,
+ *                            w_Y (W), b_Y, w_u (W), b_u].
+ */
+int64_t pigan_trunk_param_count(const pigan_mlp* trunk);
+
+typedef struct {
+  pigan_mlp trunk, disc;       /* equal n_groups; trunk in_dim = d + n_z;
+                                  disc in_dim = n_sY + n_sU */
+  int32_t d, n_z, S, P;        /* as pigan_step_desc */
+  int32_t n_sY, n_sU, B_r, chunk_S;
+  pigan_dtype dt;
+  float lambda_pde;            /* weight of the residual penalty (>= 0) */
+  float loss_scale;            /* static loss scale (> 0; 1 unless fp16) */
+} pigan_trunk_desc;
+
+/* Workspace bytes for pigan_trunk_step_grads (0 if the descriptor is invalid). */
+size_t pigan_trunk_workspace_bytes(const pigan_trunk_desc* s);
+
+/*
+ * The training step of pigan_train_step_grads with the shared-trunk generator
+ * (same losses, critic and residual; no gradient penalty).  The trunk is
+ * evaluated at the Y sensors (Y head), the u sensors (u head) and the
+ * collocation points (jets of both heads).
+ *   pT : [G, pigan_trunk_param_count] trunk weights; gT : same shape, the
+ *        gradient of L_G = L_adv + L_pde.
+ *   pD, gD, z, xc, xsY, xsU, f, f_const, real, w_group, loss, nonfinite, ws,
+ *   ws_bytes, stream : as pigan_train_step_grads (device pointers, caller
+ *   owned, outputs overwritten, asynchronous on `stream`).
+ * Errors: EINVAL for null pointers or invalid shapes (as pigan_train_step_grads),
+ * ENOTSUP for unsupported widths, EWORKSPACE, EDEVICE.
+ */
+pigan_status pigan_trunk_step_grads(const pigan_trunk_desc* s, const float* pT, const float* pD,
+                                    const float* z, const float* xc, const float* xsY,
+                                    const float* xsU, const float* f, float f_const,
+                                    const float* real, const float* w_group, float* gT, float* gD,
+                                    float* loss, int32_t* nonfinite, void* ws, size_t ws_bytes,
+                                    void* stream);
+
 /* Thread-local description of the last non-OK status ("" if none). */
 const char* pigan_last_error(void);
 

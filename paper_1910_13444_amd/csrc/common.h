@@ -121,6 +121,17 @@ template <class T> struct NtArgs {
   const float* fzp; int64_t fzp_g;
   const float* fx; int64_t fx_g; int32_t fx_shared; int64_t fPn;
   T* f_out_h;                              // forward: also store the generated activations (may be null)
+  // residual blocks of a shared trunk (tiled kernels only).  EPI_FWD: skip
+  // (the activations of layer l - 2, every stream) is added to the
+  // activations.  EPI_BWD: skip_g (the total activation cotangent carried
+  // back by a skip) is added to the product, and out_gh, when set, receives
+  // that total before the reverse carry; out_gh may alias skip_g (a block
+  // reads its whole tile of skip_g before the barrier that precedes its
+  // stores, and tiles are disjoint).
+  const T* skip; const T* skip_g; T* out_gh;
+  // EPI_DF: seeds per point are sY_ld / sU_ld apart (0: nY / nU) and the u
+  // seeds start sU_off entries into a point's row
+  int32_t sY_ld; int32_t sU_ld; int32_t sU_off;
   Seg seg;
   int32_t N, K;
 };

@@ -378,6 +378,7 @@ k_gemm_nt(const NtArgs<T> p) {
   auto ncol = [&](int t, int q) { return 32 * (wn * NT + t) + 8 * q + 4 * hh; };   // column within the block
 
   if (EPI == EPI_DF) {
+    const int64_t ldY = p.sY_ld > 0 ? p.sY_ld : p.nY, ldU = p.sU_ld > 0 ? p.sU_ld : p.nU;
 #pragma unroll
     for (int u = 0; u < MT; ++u) {
       const int64_t pt = m0 + mloc(u);
@@ -390,12 +391,36 @@ k_gemm_nt(const NtArgs<T> p) {
           for (int e = 0; e < 4; ++e) {
             const int n = n0 + ncol(t, q) + e;
             const float v = p.df_sign * acc[u][0][t][4 * q + e];
-            if (n < p.nY) p.seedY[g * p.sY_g + pt * p.nY + n] = v;
-            else if (n < p.nY + p.nU) p.seedU[g * p.sU_g + pt * p.nU + (n - p.nY)] = v;
+            if (n < p.nY) p.seedY[g * p.sY_g + pt * ldY + n] = v;
+            else if (n < p.nY + p.nU) p.seedU[g * p.sU_g + pt * ldU + p.sU_off + (n - p.nY)] = v;
           }
     }
     return;
   }
+
+  // adds a [points x columns] array of every stream (rows laid out as the
+  // outputs) to the accumulators: residual skips of a shared trunk
+  auto add_rows = [&](const T* src) {
+#pragma unroll
+    for (int u = 0; u < MT; ++u) {
+      const int64_t pt = m0 + mloc(u);
+      const bool pvalid = pt < npts;
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int nb = n0 + ncol(t, q);
+          if (!pvalid || nb >= p.N) continue;
+#pragma unroll
+          for (int k = 0; k < C; ++k) {
+            float v[4];
+            load4<T>(src + g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + nb, v);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[u][k][t][4 * q + e] += v[e];
+          }
+        }
+    }
+  };
 
   // staging: one [BM x BN] plane at a time through LDS, copied out in full
   // 16-byte row segments
@@ -456,9 +481,19 @@ k_gemm_nt(const NtArgs<T> p) {
 #pragma unroll
           for (int k = 0; k < C; ++k) acc[u][k][t][r] = v[k];
         }
+    // residual block output: h_l = tanh carry + h_{l-2}, stream by stream
+    if (p.skip) add_rows(p.skip);
 #pragma unroll
     for (int k = 0; k < C; ++k) stage_out(k, p.out_h);
     return;
+  }
+
+  // skip cotangent of a residual block's input, and the total kept for the
+  // skip below it
+  if (p.skip_g) add_rows(p.skip_g);
+  if (p.out_gh) {
+#pragma unroll
+    for (int k = 0; k < C; ++k) stage_out(k, p.out_gh);
   }
 
   // reverse carry, in place: acc[k] becomes the cotangent of the saved
@@ -1418,7 +1453,7 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   const int64_t npts = a.seg.n_points;
   if (npts <= 0) return hipSuccess;
   if constexpr (sizeof(T) == 2 && C <= 5 && EPI != EPI_DF) {
-    if (nt_resident_ok((int)sizeof(T), C, a.K, a.N, npts, a.ldx, a.ldo)) {
+    if (nt_resident_ok((int)sizeof(T), C, a.K, a.N, npts, a.ldx, a.ldo) && !a.skip && !a.skip_g && !a.out_gh) {
       // persistent weight-resident kernel: two blocks per CU in total
       const int64_t ntiles = (npts + 31) / 32;
       int64_t nb = 2 * (int64_t)cu_count() / G;
@@ -1431,6 +1466,9 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
     }
   }
   if (a.y || a.fp1) return hipErrorInvalidValue;  // output / first-layer fusion only in the resident kernel
+  if constexpr (EPI == EPI_DF) {
+    if (a.skip || a.skip_g || a.out_gh) return hipErrorInvalidValue;
+  }
   if (a.N <= 32) {
     dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 31) / 32)), 1, G);
     k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, (C >= 4 ? 1 : 2)><<<grid, 256, 0, st>>>(a);

@@ -103,8 +103,8 @@ struct MlpOff {  // offsets (in floats) of one group's packed parameters
   int in_dim, L, W;
   int64_t n;
   std::vector<int64_t> w, b;
-  int64_t wout;
-  void init(int in_dim_, int L_, int W_) {
+  int64_t wout;      // output layer: heads x [w (W), b]
+  void init(int in_dim_, int L_, int W_, int heads = 1) {
     in_dim = in_dim_;
     L = L_;
     W = W_;
@@ -120,9 +120,12 @@ struct MlpOff {  // offsets (in floats) of one group's packed parameters
       fan = W;
     }
     wout = off;
-    n = off + W + 1;
+    n = off + (int64_t)heads * (W + 1);
   }
 };
+
+// layer l (1-based) of a shared trunk ends a residual block: h_l = tanh(a_l) + h_{l-2}
+static bool trunk_skip(int l) { return l >= 3 && l % 2 == 1; }
 
 static bool width_ok(int W) {
   if (W < 32 || W > 4096 || W % 32) return false;
@@ -173,6 +176,12 @@ struct NetBuf {
   int64_t ob_slots = 0;
   int64_t ppb_sen = 8, ppb_col = 8;
   int nrc = 1;       // row chunks per sample in the first-layer reverse pass
+  // shared trunk: residual blocks, a second head (u) with its own jets and
+  // cotangents, the skip cotangent buffer, and the concatenated sensor
+  // locations [Y sensors ; u sensors]
+  bool skip = false;
+  int heads = 1;
+  size_t jet2 = 0, gbar2 = 0, gh = 0, xsc = 0;
 };
 
 struct DiscBuf {
@@ -185,6 +194,7 @@ struct DiscBuf {
 };
 
 struct StepPlan {
+  bool trunk = false;   // one shared-trunk generator (in Y) instead of the Y / u pair
   int G = 1, Sc = 1;
   size_t es = 4;
   NetBuf Y, U;
@@ -197,8 +207,10 @@ struct StepPlan {
 };
 
 static void plan_net(Carver& cv, NetBuf& nb, const pigan_mlp& m, int d, int nd2, int n_s, int Sc, int P, size_t es,
-                     int G) {
-  nb.off.init(m.in_dim, m.n_hidden, m.width);
+                     int G, bool trunk = false) {
+  nb.skip = trunk;
+  nb.heads = trunk ? 2 : 1;
+  nb.off.init(m.in_dim, m.n_hidden, m.width, nb.heads);
   nb.nd1 = d;
   nb.nd2 = nd2;
   nb.n_s = n_s;
@@ -228,17 +240,28 @@ static void plan_net(Carver& cv, NetBuf& nb, const pigan_mlp& m, int d, int nd2,
   nb.ppb_sen = ob_ppb(nb.n_sen);
   nb.ppb_col = ob_ppb(nb.n_col);
   nb.ob_slots = out_bwd_blocks(nb.n_sen, (int)nb.ppb_sen) + out_bwd_blocks(nb.n_col, (int)nb.ppb_col);
-  nb.ob = cv.take((size_t)nb.ob_slots * (W + 1) * 8 * G);
+  nb.ob = cv.take((size_t)nb.ob_slots * nb.heads * (W + 1) * 8 * G);
+  if (trunk) {
+    nb.jet2 = cv.take((size_t)nb.R * 4 * G);
+    nb.gbar2 = cv.take((size_t)nb.R * 4 * G);
+    if (L >= 3) nb.gh = cv.take(act);
+    nb.xsc = cv.take((size_t)n_s * d * 4 * G);
+  }
 }
 
-static void plan_step(const pigan_step_desc* s, int Sc, StepPlan& pl) {
+static void plan_step(const pigan_step_desc* s, int Sc, StepPlan& pl, bool trunk = false) {
   Carver cv;
+  pl.trunk = trunk;
   pl.G = s->genY.n_groups;
   pl.Sc = Sc;
   pl.es = esize(s->dt);
   const int G = pl.G;
-  plan_net(cv, pl.Y, s->genY, s->d, 0, s->n_sY, Sc, s->P, pl.es, G);
-  plan_net(cv, pl.U, s->genU, s->d, s->d, s->n_sU, Sc, s->P, pl.es, G);
+  if (trunk) {
+    plan_net(cv, pl.Y, s->genY, s->d, s->d, s->n_sY + s->n_sU, Sc, s->P, pl.es, G, true);
+  } else {
+    plan_net(cv, pl.Y, s->genY, s->d, 0, s->n_sY, Sc, s->P, pl.es, G);
+    plan_net(cv, pl.U, s->genU, s->d, s->d, s->n_sU, Sc, s->P, pl.es, G);
+  }
   DiscBuf& D = pl.D;
   D.off.init(s->disc.in_dim, s->disc.n_hidden, s->disc.width);
   const int WD = s->disc.width, LD = s->disc.n_hidden;
@@ -274,7 +297,7 @@ static void plan_step(const pigan_step_desc* s, int Sc, StepPlan& pl) {
     mxb = std::max(mxb, (int64_t)ns * N);
   };
   if (s->genY.n_hidden > 1) consider(pl.Y.R, s->genY.width, s->genY.width);
-  if (s->genU.n_hidden > 1) consider(pl.U.R, s->genU.width, s->genU.width);
+  if (!trunk && s->genU.n_hidden > 1) consider(pl.U.R, s->genU.width, s->genU.width);
   consider(D.Bmax, WD, D.Kp);
   if (LD > 1) consider(D.Bmax, WD, WD);
   pl.dwp_floats = mx;
@@ -293,12 +316,12 @@ static void plan_step(const pigan_step_desc* s, int Sc, StepPlan& pl) {
 
 static const size_t kAutoCap = (size_t)64 << 30;
 
-static int choose_chunk(const pigan_step_desc* s) {
+static int choose_chunk(const pigan_step_desc* s, bool trunk = false) {
   if (s->chunk_S > 0) return std::min(s->chunk_S, s->S);
   int Sc = s->S;
   StepPlan pl;
   while (true) {
-    plan_step(s, Sc, pl);
+    plan_step(s, Sc, pl, trunk);
     if (pl.total <= kAutoCap || Sc == 1) return Sc;
     Sc = (Sc + 1) / 2;
   }
@@ -418,7 +441,7 @@ static pigan_status gen_chunk_fwd(void* ws, const NetBuf& nb, const float* param
   // layer's GEMM (its pre-activations are never stored; its activations are,
   // for the weight gradient), and the output layer rides on the last hidden
   // layer's epilogue (the last activations are never stored).
-  const bool resident = L >= 2 && resident_net<T>(nb);
+  const bool resident = L >= 2 && !nb.skip && nb.heads == 1 && resident_net<T>(nb);
   if (!resident) {
     FirstArgs<T> fa{};
     fa.p1 = params; fa.p_g = pg; fa.in_dim = nb.off.in_dim; fa.d = d; fa.W = W;
@@ -454,6 +477,7 @@ static pigan_status gen_chunk_fwd(void* ws, const NetBuf& nb, const float* param
       first_src(a, params, pg, nb.off.in_dim, d, tp<float>(ws, nb.zp), (int64_t)Sc * W);
       a.f_out_h = tp<T>(ws, nb.H[1]);
     }
+    if (nb.skip && trunk_skip(l)) a.skip = tp<T>(ws, nb.H[l - 2]);   // residual block output
     a.N = W; a.K = W;
     a.seg = Seg{nb.n_sen, 0, 0};
     a.fx = xs; a.fx_g = xs_g; a.fx_shared = 1; a.fPn = nb.n_s;
@@ -465,9 +489,12 @@ static pigan_status gen_chunk_fwd(void* ws, const NetBuf& nb, const float* param
     if (s1 != PIGAN_OK) return s1;
   }
   if (!fuse_out) {
-    ProfScope ps(st, "out_fwd", 2.0 * nb.rows * W * G, (double)nb.rows * W * sizeof(T) * G);
+    ProfScope ps(st, "out_fwd", 2.0 * nb.heads * nb.rows * W * G, (double)nb.heads * nb.rows * W * sizeof(T) * G);
     HIP_TRY(launch_out_fwd<T>(tp<T>(ws, nb.H[L]), actg, W, nb.rows, nb.n_sen + nb.n_col, W, params + nb.off.wout, pg,
                               tp<float>(ws, nb.jet), nb.R, G, st));
+    if (nb.heads == 2)   // second head (u): [w_u, b_u] follows [w_Y, b_Y]
+      HIP_TRY(launch_out_fwd<T>(tp<T>(ws, nb.H[L]), actg, W, nb.rows, nb.n_sen + nb.n_col, W,
+                                params + nb.off.wout + W + 1, pg, tp<float>(ws, nb.jet2), nb.R, G, st));
   }
   return PIGAN_OK;
 }
@@ -482,6 +509,26 @@ static pigan_status gen_chunk_bwd(void* ws, const StepPlan& pl, const NetBuf& nb
   const int W = nb.off.W, L = nb.off.L;
   const int64_t pg = nb.off.n;
   const int64_t actg = nb.R * W;
+  if (nb.heads == 2) {
+    // two heads on the trunk's last activations; their cotangent is also the
+    // skip cotangent of the top residual block's input
+    Out2BwdArgs<T> ob{};
+    ob.A = tp<T>(ws, nb.A[L]); ob.H = tp<T>(ws, nb.H[L]); ob.dA = tp<T>(ws, nb.dA[0]);
+    ob.gh = nb.skip && trunk_skip(L) ? tp<T>(ws, nb.gh) : nullptr;
+    ob.o_g = actg; ob.ldo = W;
+    ob.gbar0 = tp<float>(ws, nb.gbar); ob.gbar1 = tp<float>(ws, nb.gbar2); ob.gb_g = nb.R;
+    ob.wout = params + nb.off.wout; ob.w_g = pg;
+    const int blk_sen = out_bwd_blocks(nb.n_sen, (int)nb.ppb_sen);
+    const int n_slots = blk_sen + out_bwd_blocks(nb.n_col, (int)nb.ppb_col);
+    ob.W = W; ob.part = tp<double>(ws, nb.ob); ob.n_slots = n_slots;
+    ob.ppb = nb.ppb_sen; ob.slot0 = 0; ob.seg = Seg{nb.n_sen, 0, 0};
+    ProfScope ps(st, "out_bwd", 0.0, (double)nb.rows * W * (ob.gh ? 4 : 3) * sizeof(T) * G);
+    HIP_TRY(launch_out2_bwd<T>(0, 0, ob, G, st));
+    ob.ppb = nb.ppb_col; ob.slot0 = blk_sen; ob.seg = Seg{nb.n_col, nb.n_sen, nb.n_col};
+    HIP_TRY(launch_out2_bwd<T>(nb.nd1, nb.nd2, ob, G, st));
+    HIP_TRY(launch_colsum<double>(tp<double>(ws, nb.ob), (int64_t)n_slots * 2 * (W + 1), n_slots, 2 * (W + 1),
+                                  2 * (W + 1), 1, 1, grad + nb.off.wout, pg, accumulate, scale, nonfinite, G, st));
+  } else {
   OutBwdArgs<T> ob{};
   ob.A = tp<T>(ws, nb.A[L]); ob.dA = tp<T>(ws, nb.dA[0]); ob.o_g = actg; ob.ldo = W;
   ob.gbar = tp<float>(ws, nb.gbar); ob.gb_g = nb.R;
@@ -498,6 +545,7 @@ static pigan_status gen_chunk_bwd(void* ws, const StepPlan& pl, const NetBuf& nb
     HIP_TRY(launch_colsum<double>(tp<double>(ws, nb.ob), (int64_t)n_slots * (W + 1), n_slots, W + 1, W + 1, 1, 1,
                                   grad + nb.off.wout, pg, accumulate, scale, nonfinite, G, st));
   }
+  }
   int cur = 0;
   for (int l = L; l >= 2; --l) {
     pigan_status s1 = weight_grad<T>(tp<T>(ws, nb.dA[cur]), actg, W, tp<T>(ws, nb.H[l - 1]), actg, W, nb.rows,
@@ -508,8 +556,15 @@ static pigan_status gen_chunk_bwd(void* ws, const StepPlan& pl, const NetBuf& nb
     a.X = tp<T>(ws, nb.dA[cur]); a.x_g = actg; a.ldx = W;
     a.Wm = tp<T>(ws, nb.wcT) + (size_t)(l - 2) * W * W; a.w_g = (int64_t)std::max(L - 1, 1) * W * W; a.ldw = W;
     a.aprev = tp<T>(ws, nb.A[l - 1]); a.out_da = tp<T>(ws, nb.dA[1 - cur]); a.o_g = actg; a.ldo = W;
-    if (l == 2 && resident_net<T>(nb))             // the first layer's pre-activations were never stored
+    if (l == 2 && !nb.skip && nb.heads == 1 && resident_net<T>(nb))   // the first layer's pre-activations were never stored
       first_src(a, params, pg, nb.off.in_dim, d, tp<float>(ws, nb.zp), (int64_t)Sc * W);
+    if (nb.skip && (l - 1) % 2 == 1) {
+      // h_{l-1} is a residual block's input (when l + 1 <= L): add the total
+      // cotangent of that block's output; when h_{l-1} is itself a block's
+      // output (l - 1 >= 3), keep its total for the block below (in place)
+      if (l + 1 <= L) a.skip_g = tp<T>(ws, nb.gh);
+      if (l - 1 >= 3) a.out_gh = tp<T>(ws, nb.gh);
+    }
     a.N = W; a.K = W;
     a.seg = Seg{nb.n_sen, 0, 0};
     a.fx = xs; a.fx_g = xs_g; a.fx_shared = 1; a.fPn = nb.n_s;
@@ -683,7 +738,10 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
     ProfScope ps(st, "misc", 0.0, 0.0);
     HIP_TRY(launch_zero(acc, 4 * G, nonfinite, st));
     if ((r = cast_gen_weights<T>(ws, pl.Y, pY, G, st)) != PIGAN_OK) return r;
-    if ((r = cast_gen_weights<T>(ws, pl.U, pU, G, st)) != PIGAN_OK) return r;
+    if (!pl.trunk && (r = cast_gen_weights<T>(ws, pl.U, pU, G, st)) != PIGAN_OK) return r;
+    if (pl.trunk)   // the trunk sees both sensor sets: locations [Y sensors ; u sensors]
+      HIP_TRY(launch_concat_rows(xsY, (int64_t)s->n_sY * d, s->n_sY, xsU, (int64_t)s->n_sU * d, s->n_sU, d,
+                                 tp<float>(ws, pl.Y.xsc), (int64_t)(s->n_sY + s->n_sU) * d, G, st));
     const int64_t dg1 = (int64_t)WD * D.Kp;
     HIP_TRY(launch_cast<T>(pD + D.off.w[1], D.off.n, WD, n_in, D.Kp, tp<T>(ws, D.w1), tp<T>(ws, D.w1T), dg1, G, st));
     const int64_t dgl = (int64_t)std::max(LD - 1, 1) * WD * WD;
@@ -692,8 +750,12 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
                              tp<T>(ws, D.wcT) + (size_t)(l - 2) * WD * WD, dgl, G, st));
   }
 
-  const int64_t xs_gY = (int64_t)s->n_sY * d, xs_gU = (int64_t)s->n_sU * d;
+  const int64_t xs_gU = (int64_t)s->n_sU * d;
   const int64_t xc_g = (int64_t)S * P * d, z_g = (int64_t)S * n_z;
+  const int n_s = s->n_sY + s->n_sU;
+  // the Y generator's sensor locations (the trunk's: both sets)
+  const float* xsG = pl.trunk ? tp<float>(ws, pl.Y.xsc) : xsY;
+  const int64_t xs_gY = pl.trunk ? (int64_t)n_s * d : (int64_t)s->n_sY * d;
   for (int s0 = 0, ci = 0; s0 < S; s0 += pl.Sc, ++ci) {
     const int Sc = std::min(pl.Sc, S - s0);
     const int accum = ci > 0;
@@ -708,16 +770,29 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
       nb->rows = nb->n_sen + (1 + nb->nd1 + nb->nd2) * nb->n_col;
     }
     // generator forward passes
-    if ((r = gen_chunk_fwd<T>(ws, Yc, pY, xsY, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, G, st)) != PIGAN_OK) return r;
-    if ((r = gen_chunk_fwd<T>(ws, Uc, pU, xsU, xs_gU, xcc, xc_g, zc, z_g, d, n_z, Sc, P, G, st)) != PIGAN_OK) return r;
+    if ((r = gen_chunk_fwd<T>(ws, Yc, pY, xsG, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, G, st)) != PIGAN_OK) return r;
+    if (!pl.trunk &&
+        (r = gen_chunk_fwd<T>(ws, Uc, pU, xsU, xs_gU, xcc, xc_g, zc, z_g, d, n_z, Sc, P, G, st)) != PIGAN_OK)
+      return r;
+    // the trunk's head cotangents: the residual and the critic fill only
+    // their own rows and streams (Y: value and first derivatives at the
+    // collocation points, Y sensors; u: all streams, u sensors)
+    const float* jetU = pl.trunk ? tp<float>(ws, Yc.jet2) : tp<float>(ws, Uc.jet);
+    float* gbarU = pl.trunk ? tp<float>(ws, Yc.gbar2) : tp<float>(ws, Uc.gbar);
+    const int64_t ju_g = pl.trunk ? Yc.R : Uc.R;
+    if (pl.trunk) {
+      ProfScope ps(st, "misc", 0.0, 0.0);
+      HIP_TRY(launch_fill_f32(tp<float>(ws, Yc.gbar), Yc.rows, Yc.R, 0.0f, G, st));
+      HIP_TRY(launch_fill_f32(gbarU, Yc.rows, Yc.R, 0.0f, G, st));
+    }
     // residual and its cotangents
     {
       ResidArgs ra{};
       ra.jY = tp<float>(ws, Yc.jet); ra.jy_g = Yc.R; ra.offY = Yc.n_sen;
-      ra.jU = tp<float>(ws, Uc.jet); ra.ju_g = Uc.R; ra.offU = Uc.n_sen;
+      ra.jU = jetU; ra.ju_g = ju_g; ra.offU = pl.trunk ? Yc.n_sen : Uc.n_sen;
       ra.plane = Yc.n_col; ra.M = (int64_t)Sc * P; ra.d = d;
       ra.f = f ? f + (int64_t)s0 * P : nullptr; ra.f_g = (int64_t)S * P; ra.f_const = f_const;
-      ra.gY = tp<float>(ws, Yc.gbar); ra.gU = tp<float>(ws, Uc.gbar);
+      ra.gY = tp<float>(ws, Yc.gbar); ra.gU = gbarU;
       ra.w_group = w_group; ra.qscale = (float)(2.0 * s->lambda_pde * ls / ((double)S * P));
       ra.part = tp<double>(ws, pl.rpart);
       ProfScope ps(st, "residual", 0.0, (double)ra.M * (3 * d + 2) * 4.0 * 2 * G);
@@ -730,8 +805,14 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
     const int64_t dact = D.Bmax * WD;
     {
       ProfScope ps(st, "misc", 0.0, 0.0);
-      HIP_TRY(launch_snap_fill<T>(tp<float>(ws, Yc.jet), Yc.R, tp<float>(ws, Uc.jet), Uc.R, s->n_sY, s->n_sU, Sc, real,
-                                  (int64_t)s->B_r * n_in, n_real, n_in, tp<T>(ws, D.X0), D.Bmax * D.Kp, D.Kp, G, st));
+      if (pl.trunk)   // sample s's sensor rows: [Y sensors ; u sensors], Y head then u head values
+        HIP_TRY(launch_snap_fill_rows<T>(tp<float>(ws, Yc.jet), Yc.R, jetU, ju_g, s->n_sY, s->n_sU, n_s, s->n_sY,
+                                         Sc, real, (int64_t)s->B_r * n_in, n_real, n_in, tp<T>(ws, D.X0),
+                                         D.Bmax * D.Kp, D.Kp, G, st));
+      else
+        HIP_TRY(launch_snap_fill<T>(tp<float>(ws, Yc.jet), Yc.R, tp<float>(ws, Uc.jet), Uc.R, s->n_sY, s->n_sU, Sc,
+                                    real, (int64_t)s->B_r * n_in, n_real, n_in, tp<T>(ws, D.X0), D.Bmax * D.Kp, D.Kp,
+                                    G, st));
     }
     for (int l = 1; l <= LD; ++l) {
       NtArgs<T> a{};
@@ -793,8 +874,11 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
       a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
       a.Wm = tp<T>(ws, D.w1T); a.w_g = (int64_t)WD * D.Kp; a.ldw = WD;
       a.N = D.Kp; a.K = WD; a.seg = Seg{Sc, 0, 0};
-      a.seedY = tp<float>(ws, Yc.gbar); a.sY_g = Yc.R; a.seedU = tp<float>(ws, Uc.gbar); a.sU_g = Uc.R;
+      a.seedY = tp<float>(ws, Yc.gbar); a.sY_g = Yc.R; a.seedU = gbarU; a.sU_g = ju_g;
       a.nY = s->n_sY; a.nU = s->n_sU; a.df_sign = -1.0f;
+      if (pl.trunk) {
+        a.sY_ld = n_s; a.sU_ld = n_s; a.sU_off = s->n_sY;
+      }
       if ((r = gemm_nt<T>(EPI_DF, 0, 0, a, G, st, "disc_bwd")) != PIGAN_OK) return r;
     }
     // critic gradient penalty on the pairs of this chunk's samples
@@ -805,11 +889,11 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
         return r;
     }
     // generator reverse passes
-    if ((r = gen_chunk_bwd<T>(ws, pl, Yc, pY, xsY, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, gY, accum, inv, nonfinite,
+    if ((r = gen_chunk_bwd<T>(ws, pl, Yc, pY, xsG, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, gY, accum, inv, nonfinite,
                               G, st)) != PIGAN_OK)
       return r;
-    if ((r = gen_chunk_bwd<T>(ws, pl, Uc, pU, xsU, xs_gU, xcc, xc_g, zc, z_g, d, n_z, Sc, P, gU, accum, inv, nonfinite,
-                              G, st)) != PIGAN_OK)
+    if (!pl.trunk && (r = gen_chunk_bwd<T>(ws, pl, Uc, pU, xsU, xs_gU, xcc, xc_g, zc, z_g, d, n_z, Sc, P, gU, accum,
+                                           inv, nonfinite, G, st)) != PIGAN_OK)
       return r;
   }
   {
@@ -878,7 +962,64 @@ static pigan_status train_step_entry(const pigan_step_desc* s, const float* pY, 
   }
 }
 
+// the trunk step runs on the step machinery: the trunk in the Y slot (and,
+// for the shape checks, the U slot), no gradient penalty
+static pigan_step_desc trunk_as_step(const pigan_trunk_desc* t) {
+  pigan_step_desc s{};
+  s.genY = t->trunk; s.genU = t->trunk; s.disc = t->disc;
+  s.d = t->d; s.n_z = t->n_z; s.S = t->S; s.P = t->P; s.n_sY = t->n_sY; s.n_sU = t->n_sU; s.B_r = t->B_r;
+  s.chunk_S = t->chunk_S; s.dt = t->dt; s.lambda_pde = t->lambda_pde; s.lambda_gp = 0.0f; s.loss_scale = t->loss_scale;
+  return s;
+}
+
 extern "C" {
+
+int64_t pigan_trunk_param_count(const pigan_mlp* net) {
+  if (!net || net->in_dim < 1 || net->n_hidden < 1 || net->width < 1) return 0;
+  MlpOff o;
+  o.init(net->in_dim, net->n_hidden, net->width, 2);
+  return o.n;
+}
+
+size_t pigan_trunk_workspace_bytes(const pigan_trunk_desc* t) {
+  if (!t) return 0;
+  const pigan_step_desc s = trunk_as_step(t);
+  if (check_step(&s) != PIGAN_OK) return 0;
+  StepPlan pl;
+  plan_step(&s, choose_chunk(&s, true), pl, true);
+  return pl.total;
+}
+
+pigan_status pigan_trunk_step_grads(const pigan_trunk_desc* t, const float* pT, const float* pD, const float* z,
+                                    const float* xc, const float* xsY, const float* xsU, const float* f, float f_const,
+                                    const float* real, const float* w_group, float* gT, float* gD, float* loss,
+                                    int32_t* nonfinite, void* ws, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  if (!t) return fail(PIGAN_EINVAL, "null trunk step descriptor");
+  const pigan_step_desc s = trunk_as_step(t);
+  pigan_status st = check_step(&s);
+  if (st != PIGAN_OK) return st;
+  if (!pT || !pD || !z || !xc || !xsY || !xsU || !real || !gT || !gD || !loss || !nonfinite)
+    return fail(PIGAN_EINVAL, "null input or output pointer");
+  if (!__builtin_isfinite(f_const)) return fail(PIGAN_EINVAL, "f_const must be finite");
+  StepPlan pl;
+  plan_step(&s, choose_chunk(&s, true), pl, true);
+  if (!ws) return fail(PIGAN_EWORKSPACE, "null workspace (need %zu bytes)", pl.total);
+  if (ws_bytes < pl.total) return fail(PIGAN_EWORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, pl.total);
+  if ((uintptr_t)ws % 256) return fail(PIGAN_EINVAL, "workspace must be 256-byte aligned");
+  hipStream_t hs = (hipStream_t)stream;
+  switch (s.dt) {
+    case PIGAN_FP32:
+      return run_step<float>(&s, pl, pT, nullptr, pD, z, xc, xsY, xsU, f, f_const, real, w_group, gT, nullptr, gD,
+                             loss, nonfinite, ws, hs, nullptr, nullptr);
+    case PIGAN_BF16:
+      return run_step<bf16>(&s, pl, pT, nullptr, pD, z, xc, xsY, xsU, f, f_const, real, w_group, gT, nullptr, gD,
+                            loss, nonfinite, ws, hs, nullptr, nullptr);
+    default:
+      return run_step<f16>(&s, pl, pT, nullptr, pD, z, xc, xsY, xsU, f, f_const, real, w_group, gT, nullptr, gD,
+                           loss, nonfinite, ws, hs, nullptr, nullptr);
+  }
+}
 
 pigan_status pigan_train_step_grads(const pigan_step_desc* s, const float* pY, const float* pU, const float* pD,
                                     const float* z, const float* xc, const float* xsY, const float* xsU,

@@ -32,6 +32,16 @@ template <class T> struct OutBwdArgs {
   Seg seg;
 };
 
+// output layer of a shared trunk (two heads), reverse pass
+template <class T> struct Out2BwdArgs {
+  const T* A; const T* H; T* dA; T* gh; int64_t o_g; int64_t ldo;  // top pre-activation / activation; outputs
+  const float* gbar0; const float* gbar1; int64_t gb_g;        // cotangents of the Y and u heads (jet layout)
+  const float* wout; int64_t w_g;                              // [w_Y (W), b_Y, w_u (W), b_u]
+  int W; int64_t ppb;                                          // points per block
+  double* part; int n_slots; int slot0;                        // [G][n_slots][2 (W+1)] fp64 partials
+  Seg seg;
+};
+
 template <class T> struct FirstBwdArgs {
   const T* dA; int64_t a_g; int64_t lda;
   int64_t n_sen; int64_t n_col;
@@ -69,6 +79,16 @@ template <class T>
 hipError_t launch_gp_norm(const float* gin, int64_t g_g, int n, int n_in, const float* w_group, float scale,
                           double* part, int64_t p_g, T* X, int64_t x_g, int ldx, int G, hipStream_t st);
 template <class T> hipError_t launch_out_bwd(int nd1, int nd2, const OutBwdArgs<T>& a, int G, hipStream_t st);
+template <class T> hipError_t launch_out2_bwd(int nd1, int nd2, const Out2BwdArgs<T>& a, int G, hipStream_t st);
+// snapshot rows from sensor values laid out ld apart per sample (u values
+// offU into the row), then the real rows
+template <class T>
+hipError_t launch_snap_fill_rows(const float* yY, int64_t yY_g, const float* yU, int64_t yU_g, int nY, int nU,
+                                 int ld, int offU, int n_fake, const float* real, int64_t real_g, int n_real, int n_in,
+                                 T* X, int64_t x_g, int ldx, int G, hipStream_t st);
+hipError_t launch_concat_rows(const float* a, int64_t a_g, int na, const float* b, int64_t b_g, int nb, int d,
+                              float* out, int64_t o_g, int G, hipStream_t st);
+hipError_t launch_fill_f32(float* p, int64_t n, int64_t p_g, float v, int G, hipStream_t st);
 // dst[(col/Jp)*J + col%Jp] (+)= scale * sum_slots part[g][slot][col]  (fp64, fixed order)
 template <class Tin>
 hipError_t launch_colsum(const Tin* part, int64_t p_g, int n_slots, int64_t slot_stride, int64_t ncols, int Jp, int J,

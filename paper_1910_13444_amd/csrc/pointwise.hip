@@ -220,8 +220,9 @@ k_sum_partials(const double* __restrict__ part, int nb, double* acc, int acc_str
 // ---------------------------------------------------------------------------
 template <class T>
 __global__ void k_snap_fill(const float* __restrict__ yY, int64_t yY_g, const float* __restrict__ yU,
-                            int64_t yU_g, int nY, int nU, int n_fake, const float* __restrict__ real,
-                            int64_t real_g, int n_real, int n_in, T* __restrict__ X, int64_t x_g, int ldx) {
+                            int64_t yU_g, int nY, int nU, int ldY, int ldU, int offU, int n_fake,
+                            const float* __restrict__ real, int64_t real_g, int n_real, int n_in, T* __restrict__ X,
+                            int64_t x_g, int ldx) {
   const int g = blockIdx.z;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int B = n_fake + n_real;
@@ -230,7 +231,7 @@ __global__ void k_snap_fill(const float* __restrict__ yY, int64_t yY_g, const fl
   float v = 0.0f;
   if (j < n_in) {
     if (b < n_fake) {
-      v = j < nY ? yY[g * yY_g + (int64_t)b * nY + j] : yU[g * yU_g + (int64_t)b * nU + (j - nY)];
+      v = j < nY ? yY[g * yY_g + (int64_t)b * ldY + j] : yU[g * yU_g + (int64_t)b * ldU + offU + (j - nY)];
     } else {
       v = real[g * real_g + (int64_t)(b - n_fake) * n_in + j];
     }
@@ -446,6 +447,160 @@ k_out_bwd(OutBwdArgs<T> p) {
     for (int q = 0; q < PPP; ++q) s += red[q * TPP];
     pw[W] = s;
   }
+}
+
+// ---------------------------------------------------------------------------
+// Output layer of a shared trunk, reverse pass: two linear heads (Y, u) on the
+// last trunk activations h_L.  Per point and stream k the activation cotangent
+// is g_h_k = w_Y gY_k + w_u gu_k; the head weight gradients are sums over rows
+// of g_k h_k (h_L read as stored: with a residual block on top it is not
+// tanh(a_L)), the bias gradients sums of the value cotangents.  g_h is stored
+// (for the skip below the top block) when p.gh is set, then carried back
+// through tanh into dA.  fp64 per-block partials [2 (W + 1)], fixed order.
+// ---------------------------------------------------------------------------
+template <class T, int ND1, int ND2>
+__global__ void __launch_bounds__(256)
+k_out2_bwd(Out2BwdArgs<T> p) {
+  constexpr int C = 1 + ND1 + ND2;
+  __shared__ double red[256 * 8];
+  const int g = blockIdx.z;
+  const int W = p.W;
+  const int G8 = W / 8;
+  const int TPP = G8 < 256 ? G8 : 256;
+  const int PPP = 256 / TPP;
+  const int lt = threadIdx.x % TPP;
+  const int lp = threadIdx.x / TPP;
+  const int64_t pbeg = (int64_t)blockIdx.x * p.ppb;
+  int64_t pend = pbeg + p.ppb;
+  if (pend > p.seg.n_points) pend = p.seg.n_points;
+  const float* w0 = p.wout + g * p.w_g;
+  const float* w1 = w0 + W + 1;
+  const float* gb0 = p.gbar0 + g * p.gb_g;
+  const float* gb1 = p.gbar1 + g * p.gb_g;
+  double dw[2][2][8];
+#pragma unroll
+  for (int hd = 0; hd < 2; ++hd)
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dw[hd][c][e] = 0.0;
+  double db0 = 0.0, db1 = 0.0;
+  const int64_t pl = p.seg.plane * p.ldo;
+  for (int64_t pt = pbeg + lp; pt < pend; pt += PPP) {
+    float g0[C], g1[C];
+#pragma unroll
+    for (int k = 0; k < C; ++k) {
+      g0[k] = gb0[p.seg.row0 + k * p.seg.plane + pt];
+      g1[k] = gb1[p.seg.row0 + k * p.seg.plane + pt];
+    }
+    if (lt == 0) {
+      db0 += g0[0];
+      db1 += g1[0];
+    }
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int cg = lt + 256 * c;
+      if (cg >= G8) continue;
+      const int n0 = cg * 8;
+      float wa[8], wb[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        wa[e] = w0[n0 + e];   // parameter vectors are only 4-byte aligned
+        wb[e] = w1[n0 + e];
+      }
+      const int64_t base = g * p.o_g + (p.seg.row0 + pt) * p.ldo + n0;
+      float gh[C][8];
+#pragma unroll
+      for (int k = 0; k < C; ++k) {
+        float hv[8];
+        load8<T>(p.H + base + k * pl, hv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          dw[0][c][e] += (double)(g0[k] * hv[e]);
+          dw[1][c][e] += (double)(g1[k] * hv[e]);
+          gh[k][e] = wa[e] * g0[k] + wb[e] * g1[k];
+        }
+      }
+      if (p.gh) {
+#pragma unroll
+        for (int k = 0; k < C; ++k) store8<T>(p.gh + base + k * pl, gh[k]);
+      }
+      float ap[C][8];
+#pragma unroll
+      for (int k = 0; k < C; ++k) load8<T>(p.A + base + k * pl, ap[k]);
+      float da[C][8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float t, s;
+        tanh_ts(ap[0][e], t, s);
+        const float sp = -2.0f * t * s;
+        const float spp = 2.0f * s * (3.0f * t * t - 1.0f);
+        float ga = s * gh[0][e];
+#pragma unroll
+        for (int i = 0; i < ND1; ++i) ga += sp * ap[1 + i][e] * gh[1 + i][e];
+#pragma unroll
+        for (int i = 0; i < ND2; ++i)
+          ga += (sp * ap[1 + ND1 + i][e] + spp * ap[1 + i][e] * ap[1 + i][e]) * gh[1 + ND1 + i][e];
+        da[0][e] = ga;
+#pragma unroll
+        for (int i = 0; i < ND1; ++i) {
+          float gd = s * gh[1 + i][e];
+          if (i < ND2) gd += 2.0f * sp * ap[1 + i][e] * gh[1 + ND1 + i][e];
+          da[1 + i][e] = gd;
+        }
+#pragma unroll
+        for (int i = 0; i < ND2; ++i) da[1 + ND1 + i][e] = s * gh[1 + ND1 + i][e];
+      }
+#pragma unroll
+      for (int k = 0; k < C; ++k) store8<T>(p.dA + base + k * pl, da[k]);
+    }
+  }
+  // block reduction over the PPP point lanes, fixed order, fp64
+  double* pw = p.part + ((int64_t)g * p.n_slots + p.slot0 + blockIdx.x) * 2 * (W + 1);
+#pragma unroll
+  for (int hd = 0; hd < 2; ++hd) {
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      if (G8 <= 256 * c) continue;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) red[threadIdx.x * 8 + e] = dw[hd][c][e];
+      __syncthreads();
+      const int cg = lt + 256 * c;
+      if (lp == 0 && cg < G8) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          double sm = 0.0;
+          for (int q = 0; q < PPP; ++q) sm += red[(q * TPP + lt) * 8 + e];
+          pw[hd * (W + 1) + cg * 8 + e] = sm;
+        }
+      }
+      __syncthreads();
+    }
+    red[threadIdx.x] = hd == 0 ? db0 : db1;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      double sm = 0.0;
+      for (int q = 0; q < PPP; ++q) sm += red[q * TPP];
+      pw[hd * (W + 1) + W] = sm;
+    }
+    __syncthreads();
+  }
+}
+
+// rows [0, na) of a then [0, nb) of b, d floats each, per group
+__global__ void k_concat_rows(const float* __restrict__ a, int64_t a_g, int na, const float* __restrict__ b,
+                              int64_t b_g, int nb, int d, float* __restrict__ out, int64_t o_g) {
+  const int g = blockIdx.z;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)(na + nb) * d) return;
+  const int64_t row = i / d, c = i % d;
+  out[g * o_g + i] = row < na ? a[g * a_g + row * d + c] : b[g * b_g + (row - na) * d + c];
+}
+
+__global__ void k_fill_f32(float* __restrict__ p, int64_t n, int64_t p_g, float v) {
+  const int g = blockIdx.z;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[g * p_g + i] = v;
 }
 
 // ---------------------------------------------------------------------------
@@ -727,8 +882,19 @@ hipError_t launch_snap_fill(const float* yY, int64_t yY_g, const float* yU, int6
                             int64_t x_g, int ldx, int G, hipStream_t st) {
   const int64_t tot = (int64_t)(n_fake + n_real) * ldx;
   if (tot <= 0) return hipSuccess;
-  k_snap_fill<T><<<dim3(nblk(tot, 256), 1, G), 256, 0, st>>>(yY, yY_g, yU, yU_g, nY, nU, n_fake, real, real_g,
-                                                             n_real, n_in, X, x_g, ldx);
+  k_snap_fill<T><<<dim3(nblk(tot, 256), 1, G), 256, 0, st>>>(yY, yY_g, yU, yU_g, nY, nU, nY, nU, 0, n_fake, real,
+                                                             real_g, n_real, n_in, X, x_g, ldx);
+  return hipGetLastError();
+}
+
+template <class T>
+hipError_t launch_snap_fill_rows(const float* yY, int64_t yY_g, const float* yU, int64_t yU_g, int nY, int nU,
+                                 int ld, int offU, int n_fake, const float* real, int64_t real_g, int n_real, int n_in,
+                                 T* X, int64_t x_g, int ldx, int G, hipStream_t st) {
+  const int64_t tot = (int64_t)(n_fake + n_real) * ldx;
+  if (tot <= 0) return hipSuccess;
+  k_snap_fill<T><<<dim3(nblk(tot, 256), 1, G), 256, 0, st>>>(yY, yY_g, yU, yU_g, nY, nU, ld, ld, offU, n_fake, real,
+                                                             real_g, n_real, n_in, X, x_g, ldx);
   return hipGetLastError();
 }
 
@@ -781,6 +947,34 @@ hipError_t launch_out_bwd(int nd1, int nd2, const OutBwdArgs<T>& a, int G, hipSt
     case 33: k_out_bwd<T, 3, 3><<<grid, 256, 0, st>>>(a); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+template <class T>
+hipError_t launch_out2_bwd(int nd1, int nd2, const Out2BwdArgs<T>& a, int G, hipStream_t st) {
+  if (a.seg.n_points <= 0) return hipSuccess;
+  dim3 grid(nblk(a.seg.n_points, a.ppb), 1, G);
+  switch (nd1 * 10 + nd2) {
+    case 0: k_out2_bwd<T, 0, 0><<<grid, 256, 0, st>>>(a); break;
+    case 11: k_out2_bwd<T, 1, 1><<<grid, 256, 0, st>>>(a); break;
+    case 22: k_out2_bwd<T, 2, 2><<<grid, 256, 0, st>>>(a); break;
+    case 33: k_out2_bwd<T, 3, 3><<<grid, 256, 0, st>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_concat_rows(const float* a, int64_t a_g, int na, const float* b, int64_t b_g, int nb, int d,
+                              float* out, int64_t o_g, int G, hipStream_t st) {
+  const int64_t tot = (int64_t)(na + nb) * d;
+  if (tot <= 0) return hipSuccess;
+  k_concat_rows<<<dim3(nblk(tot, 256), 1, G), 256, 0, st>>>(a, a_g, na, b, b_g, nb, d, out, o_g);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_f32(float* p, int64_t n, int64_t p_g, float v, int G, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  k_fill_f32<<<dim3(nblk(n, 256), 1, G), 256, 0, st>>>(p, n, p_g, v);
   return hipGetLastError();
 }
 
@@ -841,6 +1035,10 @@ hipError_t launch_cast(const float* src, int64_t s_g, int N, int K, int Kp, T* d
   template hipError_t launch_snap_fill<T>(const float*, int64_t, const float*, int64_t, int, int, int,         \
                                           const float*, int64_t, int, int, T*, int64_t, int, int, hipStream_t); \
   template hipError_t launch_out_bwd<T>(int, int, const OutBwdArgs<T>&, int, hipStream_t);                    \
+  template hipError_t launch_out2_bwd<T>(int, int, const Out2BwdArgs<T>&, int, hipStream_t);                  \
+  template hipError_t launch_snap_fill_rows<T>(const float*, int64_t, const float*, int64_t, int, int, int, int, \
+                                               int, const float*, int64_t, int, int, T*, int64_t, int, int,     \
+                                               hipStream_t);                                                    \
   template hipError_t launch_first_bwd<T>(const FirstBwdArgs<T>&, int, hipStream_t);                          \
   template hipError_t launch_gp_mix<T>(const float*, int64_t, const float*, int64_t, int, int, const float*,    \
                                        int64_t, const float*, int64_t, int, int, int, T*, int64_t, int, int,   \

@@ -44,6 +44,13 @@ class StepDesc(C.Structure):
                 ("loss_scale", C.c_float)]
 
 
+class TrunkDesc(C.Structure):
+    _fields_ = [("trunk", Mlp), ("disc", Mlp),
+                ("d", C.c_int32), ("n_z", C.c_int32), ("S", C.c_int32), ("P", C.c_int32),
+                ("n_sY", C.c_int32), ("n_sU", C.c_int32), ("B_r", C.c_int32), ("chunk_S", C.c_int32),
+                ("dt", C.c_int32), ("lambda_pde", C.c_float), ("loss_scale", C.c_float)]
+
+
 class KernelStat(C.Structure):
     _fields_ = [("name", C.c_char * 48), ("launches", C.c_int64), ("total_ms", C.c_double),
                 ("flops", C.c_double), ("bytes", C.c_double)]
@@ -72,6 +79,9 @@ def lib():
         "pigan_workspace_bytes": (sz, [P]),
         "pigan_train_step_grads": (i32, [P, P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, sz, P]),
         "pigan_train_step_grads_gp": (i32, [P, P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, P, P, sz, P]),
+        "pigan_trunk_param_count": (i64, [P]),
+        "pigan_trunk_workspace_bytes": (sz, [P]),
+        "pigan_trunk_step_grads": (i32, [P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, sz, P]),
         "pigan_last_error": (C.c_char_p, []),
         "pigan_profile_enable": (i32, [i32]),
         "pigan_profile_read": (i32, [P, i32, P]),
@@ -249,6 +259,60 @@ class TrainStep:
             st = lib().pigan_train_step_grads_gp(*args, eps, *outs, _ptr(o.gp, "gp", G), *tail)
         else:
             st = lib().pigan_train_step_grads(*args, *outs, *tail)
+        _check(st)
+        return o
+
+
+def trunk_desc(wl: Workload, S: int | None = None, B_r: int | None = None, chunk_S: int = 0,
+               dtype: str | None = None, lambda_pde: float | None = None, loss_scale: float = 1.0) -> TrunkDesc:
+    S = wl.S if S is None else S
+    B_r = wl.B_r if B_r is None else B_r
+    return TrunkDesc(Mlp(wl.G, wl.in_dim, wl.L, wl.W), Mlp(wl.G, wl.n_in, wl.L_D, wl.W_D), wl.d, wl.n_z, S, wl.P,
+                     wl.n_sY, wl.n_sU, B_r, chunk_S, DTYPES[dtype or wl.dtype],
+                     wl.lambda_pde if lambda_pde is None else lambda_pde, loss_scale)
+
+
+def trunk_workspace_bytes(desc: TrunkDesc) -> int:
+    return int(lib().pigan_trunk_workspace_bytes(C.byref(desc)))
+
+
+@dataclass
+class TrunkOut:
+    gT: torch.Tensor
+    gD: torch.Tensor
+    loss: torch.Tensor
+    nonfinite: torch.Tensor
+
+
+class TrunkStep:
+    """Repeated training steps with the shared-trunk generator."""
+
+    def __init__(self, desc: TrunkDesc, device="cuda"):
+        self.desc = desc
+        self.device = torch.device(device)
+        G = desc.trunk.n_groups
+        self.nT = int(lib().pigan_trunk_param_count(C.byref(desc.trunk)))
+        self.nD = n_params(desc.disc.in_dim, desc.disc.n_hidden, desc.disc.width)
+        need = trunk_workspace_bytes(desc)
+        if need == 0:
+            _check(lib().pigan_trunk_step_grads(C.byref(desc), *([None] * 7), 0.0, *([None] * 7), 0, None))
+        self.ws_bytes = need
+        self.ws = _workspace(need, self.device)
+        f32 = dict(dtype=torch.float32, device=self.device)
+        self.out = TrunkOut(torch.empty((G, self.nT), **f32), torch.empty((G, self.nD), **f32),
+                            torch.empty((G, 3), **f32), torch.zeros((1,), dtype=torch.int32, device=self.device))
+
+    def __call__(self, pT, pD, z, xc, xsY, xsU, real, f=None, f_const=0.0, w_group=None) -> TrunkOut:
+        d = self.desc
+        G, S, Pn = d.trunk.n_groups, d.S, d.P
+        o = self.out
+        st = lib().pigan_trunk_step_grads(
+            C.byref(d), _ptr(pT, "pT", G * self.nT), _ptr(pD, "pD", G * self.nD), _ptr(z, "z", G * S * d.n_z),
+            _ptr(xc, "xc", G * S * Pn * d.d), _ptr(xsY, "xsY", G * d.n_sY * d.d), _ptr(xsU, "xsU", G * d.n_sU * d.d),
+            _ptr(f, "f", G * S * Pn), float(f_const), _ptr(real, "real", G * d.B_r * (d.n_sY + d.n_sU)),
+            _ptr(w_group, "w_group", G), _ptr(o.gT, "gT"), _ptr(o.gD, "gD"), _ptr(o.loss, "loss"),
+            _ptr(o.nonfinite, "nonfinite", 1, dtype=torch.int32), _ptr(self.ws, "ws", dtype=torch.uint8),
+            self.ws_bytes, _stream())
         _check(st)
         return o
 

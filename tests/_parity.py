@@ -104,3 +104,38 @@ def step_errors(wl, out, ref):
     if "P_gp" in out:
         errs["P_gp"] = rel(out["P_gp"], ref["P_gp"])
     return errs
+
+
+def trunk_slices(in_dim, L, W):
+    """(name, slice) of every weight tensor of a packed shared trunk."""
+    out = [kv for kv in param_slices(in_dim, L, W) if kv[0] not in ("w_out", "b_out")]
+    off = out[-1][1].stop
+    out += [("w_Y", slice(off, off + W)), ("b_Y", slice(off + W, off + W + 1)),
+            ("w_u", slice(off + W + 1, off + 2 * W + 1)), ("b_u", slice(off + 2 * W + 1, off + 2 * W + 2))]
+    return out
+
+
+def run_trunk_gpu(wl, inp, real, chunk_S=0, dtype=None, loss_scale=1.0):
+    """One training step through pigan_trunk_step_grads; returns numpy outputs."""
+    import torch
+    from paper_1910_13444_amd import pigan
+    desc = pigan.trunk_desc(wl, S=inp.z.shape[1], B_r=real.shape[1], chunk_S=chunk_S, dtype=dtype,
+                            loss_scale=loss_scale)
+    step = pigan.TrunkStep(desc)
+    o = step(to_dev(inp.pT), to_dev(inp.pD), to_dev(inp.z), to_dev(inp.xc), to_dev(inp.xsY), to_dev(inp.xsU),
+             to_dev(real), f=None if inp.f is None else to_dev(inp.f), f_const=inp.f_const,
+             w_group=to_dev(inp.w_group))
+    torch.cuda.synchronize()
+    return dict(gT=o.gT.cpu().numpy(), gD=o.gD.cpu().numpy(), loss=o.loss.cpu().numpy(),
+                nonfinite=int(o.nonfinite.cpu().item()))
+
+
+def trunk_errors(wl, out, ref):
+    errs = {}
+    G = ref["gT"].shape[0]
+    for name, sl in trunk_slices(*wl.gen_shape()):
+        errs[f"gT.{name}"] = max(rel(out["gT"][g, sl], ref["gT"][g, sl]) for g in range(G))
+    errs.update(grad_errors(out["gD"], ref["gD"], wl.disc_shape(), "gD"))
+    for i, k in enumerate(("L_D", "L_adv", "L_pde")):
+        errs[k] = rel(out["loss"][:, i], ref["loss"][:, i])
+    return errs

@@ -1,0 +1,70 @@
+"""GPU parity of the shared-trunk training step (pigan_trunk_step_grads)
+against the fp64 oracle: every weight tensor of the trunk and of the critic,
+and the three losses, normwise per tensor (fp32 1e-5, bf16 2e-2; a tensor whose
+oracle precision model shows cancellation gets the conditioned bar)."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1910_13444_amd import configs
+from paper_1910_13444_amd.configs import Workload
+from paper_1910_13444_amd.inputs import make_inputs
+from _parity import TOL, check, check_conditioned, run_trunk_gpu, trunk_errors
+
+pytestmark = pytest.mark.gpu
+
+TTG = Workload("tinytrunk_gpu", "fp32", G=1, d=2, n_z=3, L=5, W=32, S=2, P=3, n_sY=3, n_sU=2,
+               L_D=2, W_D=32, B_r=2, f_const=0.5, seed=29, arch="trunk")
+
+CASES = {
+    "tiny_trunk_L5_fp32": (TTG, dict(f_array=True)),
+    "tiny_trunk_L4_groups_fp32": (TTG.with_(L=4, G=3, d=1, seed=30), {}),
+    "tiny_trunk_L3_d3_fp32": (TTG.with_(L=3, d=3, W=64, P=5, seed=31), {}),
+    "t5_S3_ragged_bf16": (configs.T5.with_(S=3, P=500, B_r=3), {}),
+    "t5_S3_fp32": (configs.T5.with_(S=3, P=333, B_r=2, dtype="fp32"), dict(f_array=True)),
+    "t5_groups_S2_bf16": (configs.C4.with_(arch="trunk", L=5, S=2, P=96, B_r=2, seed=1924), {}),
+    "t11_S2_bf16": (configs.T11.with_(S=2, P=256, B_r=2, L=7), {}),
+    "t11_S2_fp32": (configs.T11.with_(S=2, P=128, B_r=2, L=7, dtype="fp32"), {}),
+    "t21_S1_bf16": (configs.T21.with_(S=1, P=64, B_r=1, L=5, n_sY=256, n_sU=256, W_D=512, L_D=2), {}),
+}
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _case(wl, inp, label, **kw):
+    real = oracle.real_snapshots_trunk(wl, inp)
+    ref = oracle.train_step_trunk(wl, inp, real)
+    out = run_trunk_gpu(wl, inp, real, **kw)
+    assert out["nonfinite"] == 0
+    errs = trunk_errors(wl, out, ref)
+    tol = TOL[wl.dtype]
+    if max(errs.values()) <= tol:
+        check(errs, tol, label)
+        return
+    model = oracle.train_step_trunk(wl, inp, real, prec=wl.dtype)
+    check_conditioned(errs, trunk_errors(wl, model, ref), tol, label)
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_trunk_step(case):
+    wl, kw = CASES[case]
+    _say(f"trunk_step case={case} dtype={wl.dtype} G={wl.G} L={wl.L} W={wl.W} S={wl.S} P={wl.P}")
+    _case(wl, make_inputs(wl, **kw), case)
+
+
+def test_trunk_chunking_matches_unchunked():
+    wl = configs.T5.with_(S=5, P=200, B_r=3, dtype="fp32")
+    _say("trunk_step chunk_S=2 vs unchunked, fp32 T5-shaped S=5")
+    inp = make_inputs(wl)
+    real = oracle.real_snapshots_trunk(wl, inp)
+    a = run_trunk_gpu(wl, inp, real)
+    b = run_trunk_gpu(wl, inp, real, chunk_S=2)
+    for k in ("gT", "gD", "loss"):
+        err = np.abs(a[k] - b[k]).max() / max(1e-30, np.abs(a[k]).max())
+        print(f"chunking {k}: {err:.3g}")
+        assert err <= 1e-5
