@@ -41,13 +41,21 @@ def device_inputs(wl, dev):
     def t(a):
         return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
 
-    d = dict(pY=t(inp.pY), pU=t(inp.pU), pD=t(inp.pD), z=t(inp.z), xc=t(inp.xc), xsY=t(inp.xsY),
-             xsU=t(inp.xsU), w_group=t(inp.w_group))
+    d = dict(pD=t(inp.pD), z=t(inp.z), xc=t(inp.xc), xsY=t(inp.xsY), xsU=t(inp.xsU), w_group=t(inp.w_group))
+    if wl.arch == "trunk":
+        d["pT"] = t(inp.pT)
+        # real snapshots for timing: a seeded teacher pair of plain generators
+        # of the trunk's depth and width (same sensors and teacher noise)
+        teach = make_inputs(wl.with_(arch="pair"))
+        tY, tU = teach.tY, teach.tU
+    else:
+        d["pY"], d["pU"] = t(inp.pY), t(inp.pU)
+        tY, tU = inp.tY, inp.tU
     # real snapshots: the seeded teacher generators at the sensors, on the device
     shape = wl.gen_shape()
     zt = t(inp.z_teach)
-    yY = pigan.gen_forward(t(inp.tY), shape, wl.d, zt, d["xsY"], 0, dtype="fp32", x_shared=True)
-    yU = pigan.gen_forward(t(inp.tU), shape, wl.d, zt, d["xsU"], 0, dtype="fp32", x_shared=True)
+    yY = pigan.gen_forward(t(tY), shape, wl.d, zt, d["xsY"], 0, dtype="fp32", x_shared=True)
+    yU = pigan.gen_forward(t(tU), shape, wl.d, zt, d["xsU"], 0, dtype="fp32", x_shared=True)
     d["real"] = torch.cat([yY[:, 0], yU[:, 0]], dim=-1).contiguous()
     torch.cuda.synchronize()
     return d, inp
@@ -118,8 +126,12 @@ def measured_peaks(dev):
 
 def run_steps(step, d, wl, k):
     for _ in range(k):
-        step(d["pY"], d["pU"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["real"], f=None,
-             f_const=wl.f_const, w_group=d["w_group"], gp_eps=d.get("gp_eps"))
+        if wl.arch == "trunk":
+            step(d["pT"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["real"], f=None, f_const=wl.f_const,
+                 w_group=d["w_group"])
+        else:
+            step(d["pY"], d["pU"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["real"], f=None,
+                 f_const=wl.f_const, w_group=d["w_group"], gp_eps=d.get("gp_eps"))
 
 
 def cpu_baseline(wl, budget_s: float = 15.0):
@@ -142,7 +154,10 @@ def cpu_baseline(wl, budget_s: float = 15.0):
         inp = make_inputs(w2)
         real = np.random.default_rng(0).standard_normal((w2.G, w2.B_r, w2.n_in)).astype(np.float32)
         t0 = time.perf_counter()
-        oracle.train_step(w2, inp, real)
+        if w2.arch == "trunk":
+            oracle.train_step_trunk(w2, inp, real)
+        else:
+            oracle.train_step(w2, inp, real)
         return w2, time.perf_counter() - t0
 
     w2, t2 = timed(min(2, wl.S))
@@ -199,7 +214,12 @@ def main():
         import numpy as np
         eps = np.random.default_rng(wl.seed + 5).random((wl.G, min(wl.S, wl.B_r)), dtype=np.float32)
         d["gp_eps"] = torch.from_numpy(eps).to(dev)
-    step = pigan.TrainStep(pigan.step_desc(wl, chunk_S=a.chunk_S, lambda_gp=a.lambda_gp), device=dev)
+    if wl.arch == "trunk":
+        if a.lambda_gp > 0:
+            raise SystemExit("bench: the shared-trunk step has no gradient penalty")
+        step = pigan.TrunkStep(pigan.trunk_desc(wl, chunk_S=a.chunk_S), device=dev)
+    else:
+        step = pigan.TrainStep(pigan.step_desc(wl, chunk_S=a.chunk_S, lambda_gp=a.lambda_gp), device=dev)
     log(f"bench: workspace {step.ws_bytes / 2**30:.2f} GiB; warmup {a.warmup}")
     run_steps(step, d, wl, a.warmup)
     torch.cuda.synchronize()
@@ -264,7 +284,9 @@ def main():
         "metric": METRIC, "value": tflops, "unit": "TFLOP/s", "n_gpus": 1, "steps": a.steps,
         "warmup": a.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
-        "config": {"workload": wl.name, "G": wl.G, "d": wl.d, "n_z": wl.n_z, "gen": f"{wl.L}x{wl.W} tanh",
+        "config": {"workload": wl.name, "G": wl.G, "d": wl.d, "n_z": wl.n_z,
+                   "gen": (f"shared trunk {wl.L}x{wl.W} tanh, residual blocks, 2 heads" if wl.arch == "trunk"
+                           else f"{wl.L}x{wl.W} tanh"),
                    "disc": f"{wl.L_D}x{wl.W_D} tanh on {wl.n_in}", "S": wl.S, "P": wl.P,
                    "sensors": [wl.n_sY, wl.n_sU], "B_r": wl.B_r, "chunk_S": a.chunk_S, "lambda_gp": a.lambda_gp,
                    "collocation_points_per_step": pts, "alg_flops_per_step": F},

@@ -11,6 +11,8 @@ the value stream only):
   backward  weight gradient and input cotangent of every hidden layer and the
             output layer (2x their forward), first-layer weight gradient
             (same count as its forward)
+Shared trunk (trunk_flops): one network on R = S*(n_sY + n_sU) + (1+2d)*S*P
+rows with a two-output head.
 Discriminator on R_D = S + B_r rows:
   forward   2*R_D*(n_in*W_D + (L_D-1)*W_D^2 + W_D)
   backward  weight gradients (same as forward) + input cotangents of layers
@@ -42,11 +44,27 @@ def disc_flops(wl: Workload, S: int | None = None, B_r: int | None = None) -> fl
     return fwd + bwd
 
 
+def trunk_flops(wl: Workload, S: int | None = None) -> float:
+    """Shared trunk (one network, both sensor sets, 1 + 2d streams at the
+    collocation points, a two-output head); the residual adds are not matrix
+    work and are not counted."""
+    S = wl.S if S is None else S
+    W, L, d = wl.W, wl.L, wl.d
+    n_s = wl.n_sY + wl.n_sU
+    n_v = S * n_s + S * wl.P
+    R = S * n_s + (1 + 2 * d) * S * wl.P
+    first = 2.0 * d * W * n_v + 2.0 * wl.n_z * W * S
+    rest = (L - 1) * 2.0 * W * W * R + 2.0 * 2 * W * R
+    return 2.0 * first + 3.0 * rest
+
+
 def step_flops(wl: Workload, S: int | None = None, B_r: int | None = None) -> float:
     """Algorithmic FLOPs of one training step over all groups."""
-    per_group = (gen_flops(wl, wl.c_Y, wl.n_sY, S) + gen_flops(wl, wl.c_U, wl.n_sU, S)
-                 + disc_flops(wl, S, B_r))
-    return wl.G * per_group
+    if wl.arch == "trunk":
+        gen = trunk_flops(wl, S)
+    else:
+        gen = gen_flops(wl, wl.c_Y, wl.n_sY, S) + gen_flops(wl, wl.c_U, wl.n_sU, S)
+    return wl.G * (gen + disc_flops(wl, S, B_r))
 
 
 def collocation_points(wl: Workload, S: int | None = None) -> int:
