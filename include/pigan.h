@@ -256,6 +256,27 @@ pigan_status pigan_trunk_step_grads(const pigan_trunk_desc* s, const float* pT, 
                                     float* loss, int32_t* nonfinite, void* ws, size_t ws_bytes,
                                     void* stream);
 
+/*
+ * pigan_adam_update — one update of fp32 master weights from the fp32
+ * gradients of a training step (the paper keeps single-precision master
+ * weights and adaptive loss scaling, Sec. III.C; it names no optimizer, so
+ * the update is Adam in its textbook form):
+ *   m = beta1 m + (1 - beta1) g,  v = beta2 v + (1 - beta2) g^2,
+ *   p = p - lr (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps).
+ *   n      : number of parameters (>= 0);
+ *   params, m, v : [n] fp32 device arrays, updated in place (m, v start at 0);
+ *   grads  : [n] fp32 device gradients (already divided by the loss scale);
+ *   t      : 1-based count of updates including this one;
+ *   skip   : device int32 (the step's `nonfinite` flag) or NULL; when it
+ *            holds a non-zero value the launch leaves params, m and v
+ *            unchanged (decided on the device, no host synchronisation).
+ * Asynchronous on `stream`.  EINVAL for null arrays (n > 0), t < 1, betas
+ * outside [0, 1), non-finite lr or negative eps; EDEVICE on launch failure.
+ */
+pigan_status pigan_adam_update(int64_t n, float* params, const float* grads, float* m, float* v,
+                               float lr, float beta1, float beta2, float eps, int32_t t,
+                               const int32_t* skip, void* stream);
+
 /* Thread-local description of the last non-OK status ("" if none). */
 const char* pigan_last_error(void);
 

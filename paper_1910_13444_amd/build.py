@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libpigan.so")
 
-SOURCES = ["gemm.hip", "pointwise.hip", "pigan_api.cpp"]
+SOURCES = ["gemm.hip", "pointwise.hip", "optim.hip", "pigan_api.cpp"]
 ARCH = "gfx950"
 
 

@@ -6,12 +6,14 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cmath>
 #include <mutex>
 #include <string>
 #include <vector>
 
 #include "common.h"
 #include "pointwise.h"
+#include "optim.h"
 
 namespace pigan {
 
@@ -973,6 +975,23 @@ static pigan_step_desc trunk_as_step(const pigan_trunk_desc* t) {
 }
 
 extern "C" {
+
+pigan_status pigan_adam_update(int64_t n, float* params, const float* grads, float* m, float* v, float lr,
+                               float beta1, float beta2, float eps, int32_t t, const int32_t* skip, void* stream) {
+  g_err.clear();
+  if (n < 0) return fail(PIGAN_EINVAL, "n=%lld must be >= 0", (long long)n);
+  if (n > 0 && (!params || !grads || !m || !v)) return fail(PIGAN_EINVAL, "null parameter, gradient or moment pointer");
+  if (t < 1) return fail(PIGAN_EINVAL, "t=%d must be >= 1", t);
+  if (!(beta1 >= 0.0f && beta1 < 1.0f) || !(beta2 >= 0.0f && beta2 < 1.0f))
+    return fail(PIGAN_EINVAL, "beta1=%g and beta2=%g must lie in [0, 1)", beta1, beta2);
+  if (!__builtin_isfinite(lr) || !(eps >= 0.0f) || !__builtin_isfinite(eps))
+    return fail(PIGAN_EINVAL, "lr must be finite and eps finite and >= 0");
+  const float c1 = (float)(1.0 / (1.0 - std::pow((double)beta1, (double)t)));
+  const float c2 = (float)(1.0 / (1.0 - std::pow((double)beta2, (double)t)));
+  hipError_t e = launch_adam(n, params, grads, m, v, lr, beta1, beta2, eps, c1, c2, skip, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(PIGAN_EDEVICE, "adam update: %s", hipGetErrorString(e));
+  return PIGAN_OK;
+}
 
 int64_t pigan_trunk_param_count(const pigan_mlp* net) {
   if (!net || net->in_dim < 1 || net->n_hidden < 1 || net->width < 1) return 0;

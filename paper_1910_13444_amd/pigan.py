@@ -79,6 +79,7 @@ def lib():
         "pigan_workspace_bytes": (sz, [P]),
         "pigan_train_step_grads": (i32, [P, P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, sz, P]),
         "pigan_train_step_grads_gp": (i32, [P, P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, P, P, sz, P]),
+        "pigan_adam_update": (i32, [i64, P, P, P, P, f32, f32, f32, f32, i32, P, P]),
         "pigan_trunk_param_count": (i64, [P]),
         "pigan_trunk_workspace_bytes": (sz, [P]),
         "pigan_trunk_step_grads": (i32, [P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, sz, P]),

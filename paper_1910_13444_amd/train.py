@@ -1,0 +1,170 @@
+"""Training loop on one GPU around the C-ABI training step.
+
+Host logic only: every gradient and every parameter update runs in
+libpigan.so kernels (pigan_train_step_grads / pigan_trunk_step_grads and
+pigan_adam_update) on the current stream.
+
+* fp32 master weights updated by Adam (the paper keeps single-precision
+  master weights, Sec. III.C, and names no optimizer).
+* Adaptive loss scaling (Sec. III.C): with dynamic scaling the step's
+  non-finite flag is read after each call; a flagged step is skipped (the
+  update kernel also reads the flag on the device), halves the scale, and
+  `growth_interval` clean steps in a row double it.  Without dynamic scaling
+  nothing is synchronised.
+* Model-exchange schedules of the paper's generator and critic workers
+  (Sec. III.D.2) on one device: "sequential" -- n_critic critic updates, then
+  one generator update against the updated critic; "parallel" -- each network
+  takes steps_per_exchange updates against the copy of the other it received
+  at the last exchange, then the copies are exchanged (device copies).
+"""
+from __future__ import annotations
+
+import ctypes as C
+from dataclasses import dataclass
+
+import torch
+
+from . import pigan
+from .configs import Workload
+
+
+class Adam:
+    """fp32 Adam state for one device parameter tensor."""
+
+    def __init__(self, params: torch.Tensor, lr: float, beta1: float = 0.5, beta2: float = 0.9, eps: float = 1e-8):
+        if params.dtype != torch.float32 or not params.is_cuda or not params.is_contiguous():
+            raise ValueError("params must be a contiguous fp32 device tensor")
+        self.p = params
+        self.m = torch.zeros_like(params)
+        self.v = torch.zeros_like(params)
+        self.lr, self.beta1, self.beta2, self.eps = float(lr), float(beta1), float(beta2), float(eps)
+        self.t = 0
+
+    def step(self, grads: torch.Tensor, skip: torch.Tensor | None = None, count: bool = True):
+        """Apply one update (skipped on the device when *skip != 0).  `count`
+        advances the update counter (False when the host knows the step was
+        skipped, so the bias correction follows the applied updates only)."""
+        if count:
+            self.t += 1
+        t = max(self.t, 1)
+        pigan._check(pigan.lib().pigan_adam_update(
+            self.p.numel(), pigan._ptr(self.p, "params"), pigan._ptr(grads, "grads", self.p.numel()),
+            pigan._ptr(self.m, "m"), pigan._ptr(self.v, "v"), self.lr, self.beta1, self.beta2, self.eps, t,
+            None if skip is None else pigan._ptr(skip, "skip", 1, dtype=torch.int32), pigan._stream()))
+
+
+class LossScaler:
+    """Dynamic loss scale (halve on a non-finite step, double after
+    growth_interval clean steps)."""
+
+    def __init__(self, init_scale: float = 2.0 ** 15, growth_interval: int = 2000, min_scale: float = 1.0):
+        self.scale = float(init_scale)
+        self.growth_interval = int(growth_interval)
+        self.min_scale = float(min_scale)
+        self.good = 0
+
+    def update(self, nonfinite: bool) -> bool:
+        if nonfinite:
+            self.scale = max(self.min_scale, self.scale * 0.5)
+            self.good = 0
+            return True
+        self.good += 1
+        if self.good >= self.growth_interval:
+            self.scale *= 2.0
+            self.good = 0
+        return False
+
+
+@dataclass
+class TrainConfig:
+    schedule: str = "sequential"       # or "parallel"
+    n_critic: int = 1                  # sequential: critic updates per generator update
+    steps_per_exchange: int = 1        # parallel: updates of each network between exchanges
+    lr_g: float = 1e-4
+    lr_d: float = 1e-4
+    beta1: float = 0.5
+    beta2: float = 0.9
+    eps: float = 1e-8
+    dynamic_loss_scale: bool = False   # fp16: adaptive loss scaling
+    init_scale: float = 2.0 ** 15
+    growth_interval: int = 2000
+    chunk_S: int = 0
+
+
+class Trainer:
+    """Owns the master weights (generator: pY and pU, or the trunk pT; critic
+    pD), their Adam states, the loss scale and the schedule.  `inputs` are the
+    batch's device tensors: z, xc, xsY, xsU, real, w_group (and optionally f)."""
+
+    def __init__(self, wl: Workload, gen: list[torch.Tensor], pD: torch.Tensor, inputs: dict, cfg: TrainConfig):
+        self.wl, self.cfg, self.inp = wl, cfg, inputs
+        self.trunk = wl.arch == "trunk"
+        if cfg.schedule not in ("sequential", "parallel"):
+            raise ValueError(f"unknown schedule {cfg.schedule!r}")
+        S, B_r = inputs["z"].shape[1], inputs["real"].shape[1]
+        if self.trunk:
+            self.desc = pigan.trunk_desc(wl, S=S, B_r=B_r, chunk_S=cfg.chunk_S)
+            self.step_fn = pigan.TrunkStep(self.desc)
+        else:
+            self.desc = pigan.step_desc(wl, S=S, B_r=B_r, chunk_S=cfg.chunk_S)
+            self.step_fn = pigan.TrainStep(self.desc)
+        self.gen = [g.contiguous() for g in gen]
+        self.pD = pD.contiguous()
+        self.opt_g = [Adam(g, cfg.lr_g, cfg.beta1, cfg.beta2, cfg.eps) for g in self.gen]
+        self.opt_d = Adam(self.pD, cfg.lr_d, cfg.beta1, cfg.beta2, cfg.eps)
+        self.scaler = LossScaler(cfg.init_scale, cfg.growth_interval) if cfg.dynamic_loss_scale else None
+        self.losses: list[torch.Tensor] = []
+        self.skipped = 0
+        # parallel schedule: each worker's copy of the other network
+        self.gen_copy = [g.clone() for g in self.gen]
+        self.pD_copy = self.pD.clone()
+
+    def _call(self, gen, pD):
+        if self.scaler is not None:
+            self.desc.loss_scale = self.scaler.scale
+        i = self.inp
+        if self.trunk:
+            o = self.step_fn(gen[0], pD, i["z"], i["xc"], i["xsY"], i["xsU"], i["real"], f=i.get("f"),
+                             f_const=self.wl.f_const, w_group=i["w_group"])
+            grads_g = [o.gT]
+        else:
+            o = self.step_fn(gen[0], gen[1], pD, i["z"], i["xc"], i["xsY"], i["xsU"], i["real"], f=i.get("f"),
+                             f_const=self.wl.f_const, w_group=i["w_group"])
+            grads_g = [o.gY, o.gU]
+        self.losses.append(o.loss.clone())
+        skipped = False
+        if self.scaler is not None:
+            skipped = self.scaler.update(bool(o.nonfinite.item()))
+            self.skipped += int(skipped)
+        return o, grads_g, skipped
+
+    def _update_g(self, grads_g, flag, skipped):
+        for opt, g in zip(self.opt_g, grads_g):
+            opt.step(g, skip=flag, count=not skipped)
+
+    def _update_d(self, gD, flag, skipped):
+        self.opt_d.step(gD, skip=flag, count=not skipped)
+
+    def round(self):
+        """One round of the schedule."""
+        cfg = self.cfg
+        if cfg.schedule == "sequential":
+            for _ in range(cfg.n_critic):
+                o, _, sk = self._call(self.gen, self.pD)
+                self._update_d(o.gD, o.nonfinite, sk)
+            o, grads_g, sk = self._call(self.gen, self.pD)
+            self._update_g(grads_g, o.nonfinite, sk)
+        else:
+            for _ in range(cfg.steps_per_exchange):
+                o, grads_g, sk = self._call(self.gen, self.pD_copy)
+                self._update_g(grads_g, o.nonfinite, sk)
+                o, _, sk = self._call(self.gen_copy, self.pD)
+                self._update_d(o.gD, o.nonfinite, sk)
+            for c, g in zip(self.gen_copy, self.gen):
+                c.copy_(g)
+            self.pD_copy.copy_(self.pD)
+
+    def run(self, n_rounds: int) -> torch.Tensor:
+        for _ in range(n_rounds):
+            self.round()
+        return torch.stack(self.losses) if self.losses else torch.empty(0)

@@ -132,3 +132,60 @@ def test_gen_forward_and_disc_forward_validation():
     assert st == pigan.EINVAL
     st = L.pigan_pde_residual(2, 1, 10, None, FAKE, None, 0.0, FAKE, None)
     assert st == pigan.EINVAL
+
+
+# ---------------------------------------------------------------------------
+# shared trunk and parameter update
+# ---------------------------------------------------------------------------
+
+def test_trunk_param_count_matches_packing():
+    L = pigan.lib()
+    for wl in (configs.T5, configs.T11, configs.T21):
+        m = pigan.Mlp(1, wl.in_dim, wl.L, wl.W)
+        assert L.pigan_trunk_param_count(C.byref(m)) == configs.n_params_trunk(wl.in_dim, wl.L, wl.W)
+    assert L.pigan_trunk_param_count(None) == 0
+
+
+def _trunk_step(desc, ws_bytes, ptr=FAKE, ws=FAKE):
+    return pigan.lib().pigan_trunk_step_grads(C.byref(desc), *([ptr] * 6), None, 0.0, ptr, None, ptr, ptr, ptr, ptr,
+                                              ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("field,value", [("d", 0), ("n_z", 0), ("S", 0), ("P", 0), ("n_sU", 0), ("B_r", 0),
+                                         ("chunk_S", -1), ("loss_scale", -1.0), ("lambda_pde", -2.0), ("dt", 9)])
+def test_trunk_step_rejects_bad_descriptor(field, value):
+    d = pigan.trunk_desc(configs.T5)
+    setattr(d, field, value)
+    assert _trunk_step(d, 1 << 40) == pigan.EINVAL
+    assert pigan.trunk_workspace_bytes(d) == 0
+
+
+def test_trunk_step_validation():
+    d = pigan.trunk_desc(configs.T5)
+    need = pigan.trunk_workspace_bytes(d)
+    assert need > 0
+    assert _trunk_step(d, need, ptr=None) == pigan.EINVAL
+    assert _trunk_step(d, need - 1) == pigan.EWORKSPACE
+    assert _trunk_step(d, need, ws=None) == pigan.EWORKSPACE
+    assert _trunk_step(d, need, ws=C.c_void_p(4096 + 64)) == pigan.EINVAL      # misaligned workspace
+    d.trunk.width = 96                                                           # neither divides nor fills 256
+    assert _trunk_step(d, 1 << 40) == pigan.ENOTSUP
+    d = pigan.trunk_desc(configs.T5)
+    d.disc.in_dim = 7
+    assert _trunk_step(d, 1 << 40) == pigan.EINVAL
+    assert pigan.lib().pigan_trunk_step_grads(None, *([FAKE] * 6), None, 0.0, FAKE, None, FAKE, FAKE, FAKE, FAKE,
+                                              FAKE, 1 << 40, None) == pigan.EINVAL
+    assert 0 < pigan.trunk_workspace_bytes(pigan.trunk_desc(configs.T21)) <= (64 << 30)
+
+
+def test_adam_update_validation():
+    L = pigan.lib()
+
+    def adam(n, ptr=FAKE, lr=1e-3, b1=0.5, b2=0.9, eps=1e-8, t=1):
+        return L.pigan_adam_update(n, ptr, ptr, ptr, ptr, lr, b1, b2, eps, t, None, None)
+    assert adam(0, ptr=None) == pigan.OK            # nothing to update: no launch
+    assert adam(-1) == pigan.EINVAL
+    assert adam(10, ptr=None) == pigan.EINVAL
+    assert adam(10, t=0) == pigan.EINVAL
+    assert adam(10, b1=1.0) == pigan.EINVAL and adam(10, b2=-0.1) == pigan.EINVAL
+    assert adam(10, lr=float("inf")) == pigan.EINVAL and adam(10, eps=-1.0) == pigan.EINVAL

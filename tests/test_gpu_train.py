@@ -1,0 +1,138 @@
+"""GPU checks of the training loop: the Adam update kernel against the oracle
+update, the GPU trainer against the oracle trainer for both exchange schedules,
+dynamic loss scaling in fp16, and the residual loss falling while training."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.trainer import adam_update, train as oracle_train
+from paper_1910_13444_amd import configs, pigan
+from paper_1910_13444_amd.configs import Workload
+from paper_1910_13444_amd.inputs import make_inputs
+from paper_1910_13444_amd.train import Adam, TrainConfig, Trainer
+from _parity import rel, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def test_adam_kernel_matches_oracle():
+    _say("adam kernel: n=100003, 3 updates, then a flagged (skipped) update")
+    rng = np.random.default_rng(3)
+    n = 100003
+    p0 = rng.standard_normal(n).astype(np.float32)
+    p = to_dev(p0)
+    opt = Adam(p, lr=1e-3, beta1=0.5, beta2=0.9, eps=1e-8)
+    pr, m, v = p0.astype(np.float64), np.zeros(n), np.zeros(n)
+    for t in range(1, 4):
+        g = (rng.standard_normal(n) * 10.0 ** rng.integers(-3, 2, n)).astype(np.float32)
+        opt.step(to_dev(g))
+        pr, m, v = adam_update(pr, g, m, v, t, 1e-3, 0.5, 0.9, 1e-8)
+    torch.cuda.synchronize()
+    pg = p.cpu().numpy().astype(np.float64)
+    # the master weights are fp32: each update rounds p (|p| ~ 1, ulp ~ 1.2e-7),
+    # so the weights agree to ~1e-7 relative while their change (~3 lr) carries
+    # a few 1e-5 relative rounding; both bars follow from that
+    err_p = rel(pg, pr)
+    err_d = rel(pg - p0, pr - p0)
+    print(f"adam update rel err: weights {err_p:.3g}, weight change {err_d:.3g}")
+    assert err_p <= 1e-6 and err_d <= 1e-4
+    assert rel(opt.m.cpu().numpy(), m) <= 1e-6 and rel(opt.v.cpu().numpy(), v) <= 1e-6
+    before = p.clone()
+    flag = torch.ones(1, dtype=torch.int32, device="cuda")
+    opt.step(to_dev(np.full(n, np.inf, np.float32)), skip=flag)
+    torch.cuda.synchronize()
+    assert torch.equal(before, p)
+
+
+TW = Workload("train_tiny", "fp32", G=1, d=2, n_z=3, L=3, W=32, S=3, P=16, n_sY=4, n_sU=3,
+              L_D=2, W_D=32, B_r=3, f_const=0.5, seed=41)
+
+
+def _oracle_step_fn(wl, inp, real):
+    gshape, dshape = wl.gen_shape(), wl.disc_shape()
+    f = np.full((wl.S, wl.P), wl.f_const)
+    if wl.arch == "trunk":
+        def fn(pG, pD):
+            o = oracle.train_step_group_trunk(gshape, dshape, wl.d, pG, pD, inp.z[0], inp.xc[0], inp.xsY[0],
+                                              inp.xsU[0], f, real[0], w=float(inp.w_group[0]))
+            return np.array([o["L_D"], o["L_adv"], o["L_pde"]]), o["gT"], o["gD"]
+    else:
+        nY = inp.pY.shape[1]
+
+        def fn(pG, pD):
+            o = oracle.train_step_group(gshape, dshape, wl.d, pG[:nY], pG[nY:], pD, inp.z[0], inp.xc[0],
+                                        inp.xsY[0], inp.xsU[0], f, real[0], w=float(inp.w_group[0]))
+            return (np.array([o["L_D"], o["L_adv"], o["L_pde"]]), np.concatenate([o["gY"], o["gU"]]), o["gD"])
+    return fn
+
+
+def _gpu_trainer(wl, inp, real, cfg):
+    gen = [to_dev(inp.pT)] if wl.arch == "trunk" else [to_dev(inp.pY), to_dev(inp.pU)]
+    dev = dict(z=to_dev(inp.z), xc=to_dev(inp.xc), xsY=to_dev(inp.xsY), xsU=to_dev(inp.xsU), real=to_dev(real),
+               w_group=to_dev(inp.w_group))
+    return Trainer(wl, gen, to_dev(inp.pD), dev, cfg)
+
+
+@pytest.mark.parametrize("schedule,arch", [("sequential", "pair"), ("parallel", "pair"), ("sequential", "trunk")])
+def test_trainer_matches_oracle(schedule, arch):
+    wl = TW.with_(arch=arch, L=3 if arch == "pair" else 5)
+    _say(f"trainer {schedule} {arch}: 3 rounds fp32 vs the oracle loop")
+    inp = make_inputs(wl)
+    real = oracle.real_snapshots_trunk(wl, inp) if arch == "trunk" else oracle.real_snapshots(wl, inp)
+    cfg = TrainConfig(schedule=schedule, n_critic=2, steps_per_exchange=2, lr_g=1e-3, lr_d=2e-3)
+    tr = _gpu_trainer(wl, inp, real, cfg)
+    losses = tr.run(3).cpu().numpy()
+    pG0 = inp.pT[0] if arch == "trunk" else np.concatenate([inp.pY[0], inp.pU[0]])
+    pG, pD, ref_losses = oracle_train(_oracle_step_fn(wl, inp, real), pG0, inp.pD[0], 3, schedule=schedule,
+                                      n_critic=2, steps_per_exchange=2, lr_g=1e-3, lr_d=2e-3)
+    gpu_G = np.concatenate([g.cpu().numpy().ravel() for g in tr.gen])
+    gpu_D = tr.pD.cpu().numpy().ravel()
+    eG = rel(gpu_G - pG0, pG - pG0)
+    eD = rel(gpu_D - inp.pD[0], pD - inp.pD[0])
+    eL = rel(losses.reshape(ref_losses.shape), ref_losses)
+    print(f"weight change rel err: generator {eG:.3g}, critic {eD:.3g}; losses {eL:.3g}")
+    assert losses.shape[0] == ref_losses.shape[0]
+    assert eG <= 1e-3 and eD <= 1e-3 and eL <= 1e-4
+
+
+def test_dynamic_loss_scale_fp16_skips_overflow():
+    wl = configs.C2.with_(S=2, P=64, B_r=2, dtype="fp16", seed=43)
+    _say("trainer fp16 with an overflowing initial loss scale 2^40")
+    inp = make_inputs(wl)
+    real = oracle.real_snapshots(wl, inp)
+    cfg = TrainConfig(dynamic_loss_scale=True, init_scale=2.0 ** 40, growth_interval=1000, lr_g=1e-4, lr_d=1e-4)
+    tr = _gpu_trainer(wl, inp, real, cfg)
+    pD0 = tr.pD.clone()
+    tr.round()                                   # critic step then generator step, both overflow
+    torch.cuda.synchronize()
+    assert tr.skipped == 2 and tr.scaler.scale == 2.0 ** 38
+    assert torch.equal(pD0, tr.pD)               # skipped on the device: weights untouched
+    tr.run(20)
+    print(f"after 21 rounds: scale 2^{np.log2(tr.scaler.scale):.0f}, skipped {tr.skipped}")
+    assert tr.scaler.scale <= 2.0 ** 24 and tr.skipped < 42
+    assert not torch.equal(pD0, tr.pD)
+    assert torch.isfinite(tr.pD).all() and all(torch.isfinite(g).all() for g in tr.gen)
+
+
+def test_training_reduces_the_residual():
+    """The 1-D Darcy toy (fp32): the residual penalty is a direct term of the
+    generator loss, so training lowers it."""
+    wl = configs.C1
+    _say("trainer C1 toy: 150 rounds, residual loss must drop")
+    inp = make_inputs(wl)
+    real = oracle.real_snapshots(wl, inp)
+    cfg = TrainConfig(n_critic=1, lr_g=2e-3, lr_d=2e-3)
+    tr = _gpu_trainer(wl, inp, real, cfg)
+    losses = tr.run(150).cpu().numpy()[:, 0, :]    # [calls, 3]
+    first, last = losses[:4, 2].mean(), losses[-4:, 2].mean()
+    print(f"L_pde first {first:.4g} last {last:.4g}; L_D last {losses[-1, 0]:.4g}")
+    assert np.isfinite(losses).all()
+    assert last < 0.5 * first
