@@ -10,4 +10,5 @@ from .pigan_oracle import (  # noqa: F401
     critic_input_grad, tangent_output_grad, gradient_penalty,
     trunk_unpack, trunk_pack, trunk_skip, trunk_forward, trunk_backward, trunk_snapshots,
     train_step_group_trunk, train_step_trunk, real_snapshots_trunk,
+    train_step_hier, real_snapshots_hier,
 )

@@ -876,6 +876,110 @@ def real_snapshots_trunk(wl, inp):
                      for g in range(inp.z.shape[0])])
 
 
+def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, idxU, idxF, real, w,
+                    lambda_pde=0.0, chunk_S=None, prec=None):
+    """Domain decomposition (Sec. III.B.1): one generator pair, one critic per
+    subdomain of every level.  Critic k sees the paper's snapshot of its
+    subdomain: [Y at Y sensors idxY[k] | u at u sensors idxU[k] | the
+    generated source f = -div(exp(Y) grad u) at the free sensors idxF[k] (a
+    subset of each sample's collocation points) | those free sensors'
+    coordinates], real[k] its real snapshots ([B, n_in], f = 0 there).
+    Weights w[k] = 1 / (levels * subdomains of the level).  Losses per critic:
+    L_D[k] = w_k (mean D_k(fake) - mean D_k(real)), L_adv[k] = -w_k mean D_k(fake);
+    the generator loss is sum_k L_adv[k] + L_pde with L_pde = lambda mean r^2.
+    Returns dict(L_D [D], L_adv [D], L_pde, gY, gU, gD [D, nD])."""
+    z = np.asarray(z, F64)
+    xc = np.asarray(xc, F64)
+    f = np.asarray(f, F64)
+    S, P = xc.shape[0], xc.shape[1]
+    D = len(pDs)
+    chunk_S = S if not chunk_S else chunk_S
+    if prec == "fp32":
+        with _working_type(np.float32):
+            return train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, idxU, idxF, real, w,
+                                   lambda_pde=lambda_pde, chunk_S=chunk_S, prec=None)
+    num = _Num(prec)
+    gY = np.zeros(np.asarray(pY).size, F64)
+    gU = np.zeros(np.asarray(pU).size, F64)
+    gD = np.zeros((D, np.asarray(pDs[0]).size), F64)
+    sum_DF = np.zeros(D)
+    sum_DR = np.zeros(D)
+    sum_r2 = 0.0
+    for k in range(D):
+        Rk = np.asarray(real[k], F64)
+        DR, hsR = mlp_forward(pDs[k], dshape, Rk, keep=True, prec=num)
+        gD[k] += mlp_backward(pDs[k], dshape, hsR, np.full(Rk.shape[0], -w[k] / Rk.shape[0], F64), prec=num)
+        sum_DR[k] = DR.sum()
+    B = np.asarray(real[0]).shape[0]
+    nYs, nUs = np.asarray(xsY).shape[0], np.asarray(xsU).shape[0]
+    for s0 in range(0, S, chunk_S):
+        sl = slice(s0, min(S, s0 + chunk_S))
+        zc = z[sl]
+        Sc = zc.shape[0]
+        XY, ZY = sensor_rows(xsY, zc)
+        XU, ZU = sensor_rows(xsU, zc)
+        fY_s = gen_forward(pY, gshape, d, XY, ZY, 0, keep=True, prec=num)
+        fU_s = gen_forward(pU, gshape, d, XU, ZU, 0, keep=True, prec=num)
+        Ys = fY_s["y"].reshape(Sc, nYs)
+        Us = fU_s["y"].reshape(Sc, nUs)
+        XC, ZC = colloc_rows(xc[sl], zc)
+        jY = gen_forward(pY, gshape, d, XC, ZC, 1, keep=True, prec=num)
+        jU = gen_forward(pU, gshape, d, XC, ZC, 2, keep=True, prec=num)
+        fc = f[sl].reshape(-1)
+        r = darcy_residual(jY["y"], jY["dy"], jU["dy"], jU["ddy"], fc)
+        sum_r2 += float((r * r).sum())
+        Nf = (r + fc).reshape(Sc, P)                    # the generated source at every point
+        gYs = np.zeros((Sc, nYs))
+        gUs = np.zeros((Sc, nUs))
+        gN = np.zeros((Sc, P))
+        for k in range(D):
+            iY, iU, iF = np.asarray(idxY[k]), np.asarray(idxU[k]), np.asarray(idxF[k])
+            F = np.concatenate([Ys[:, iY], Us[:, iU], Nf[:, iF], xc[sl][:, iF, :].reshape(Sc, -1)], axis=1)
+            DF, hsF = mlp_forward(pDs[k], dshape, F, keep=True, prec=num)
+            sum_DF[k] += float(DF.sum())
+            gDc, gF = mlp_backward(pDs[k], dshape, hsF, np.full(Sc, w[k] / S, F64), want_input_grad=True, prec=num)
+            gD[k] += gDc
+            gF = -gF                                      # L_adv = -w mean D(F)
+            nY_, nU_, nF_ = len(iY), len(iU), len(iF)
+            np.add.at(gYs, (slice(None), iY), gF[:, :nY_])
+            np.add.at(gUs, (slice(None), iU), gF[:, nY_:nY_ + nU_])
+            np.add.at(gN, (slice(None), iF), gF[:, nY_ + nU_:nY_ + nU_ + nF_])
+            # the coordinates are inputs, not generated: their cotangent is dropped
+        # cotangent of r (= of the generated source) from the penalty and the critics
+        q = 2.0 * lambda_pde * r / (S * P) + gN.reshape(-1)
+        eY = np.exp(jY["y"])
+        g_Yval = q * (r + fc)
+        g_Ydy = np.stack([-q * eY * jU["dy"][i] for i in range(d)])
+        g_Udy = np.stack([-q * eY * jY["dy"][i] for i in range(d)])
+        g_Uddy = np.stack([-q * eY for _ in range(d)])
+        gY += gen_backward(pY, gshape, d, XY, ZY, fY_s, gYs.reshape(-1), prec=num)
+        gU += gen_backward(pU, gshape, d, XU, ZU, fU_s, gUs.reshape(-1), prec=num)
+        gY += gen_backward(pY, gshape, d, XC, ZC, jY, g_Yval, g_Ydy, prec=num)
+        gU += gen_backward(pU, gshape, d, XC, ZC, jU, np.zeros_like(r), g_Udy, g_Uddy, prec=num)
+    w = np.asarray(w, F64)
+    return dict(L_D=w * (sum_DF / S - sum_DR / B), L_adv=-w * sum_DF / S, L_pde=lambda_pde * sum_r2 / (S * P),
+                gY=gY, gU=gU, gD=gD)
+
+
+def real_snapshots_hier(wl, hin, lambda_unused=None):
+    """Real snapshots [D, B_r, n_in] of a hierarchical step: the teacher pair
+    at each critic's Y and u sensors, f = 0 at its free sensors (the true field
+    satisfies the equation with the paper's zero source), and the coordinates
+    of the real realisations' free sensors (hin.xf_real)."""
+    b = hin.base
+    gshape = (wl.d + wl.n_z, wl.L, wl.W)
+    Y = snapshots(b.tY[0], b.tU[0], gshape, wl.d, b.xsY[0], b.xsU[0], b.z_teach[0])
+    nY = b.xsY.shape[1]
+    Yv, Uv = Y[:, :nY], Y[:, nY:]
+    B = Y.shape[0]
+    h = hin.hier
+    out = []
+    for k in range(h.D):
+        out.append(np.concatenate([Yv[:, h.idxY[k]], Uv[:, h.idxU[k]], np.zeros((B, h.idxF.shape[1])),
+                                   hin.xf_real[:, h.idxF[k], :].reshape(B, -1)], axis=1))
+    return np.stack(out)
+
+
 def real_snapshots(wl, inp):
     """Teacher snapshots [G, B_r, n_in] from the teacher weights and noise z'."""
     gshape = (wl.d + wl.n_z, wl.L, wl.W)

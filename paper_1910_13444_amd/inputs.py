@@ -114,3 +114,102 @@ def make_inputs(wl: Workload, seed: int | None = None, f_array: bool = False,
     f = r["f"].standard_normal((G, S, wl.P)).astype(np.float32) if f_array else None
     wg = np.full((G,), wl.w_group, dtype=np.float32)
     return StepInputs(pY, pU, pD, tY, tU, z, zt, xc, xsY, xsU, f, wl.f_const, wg, pT, tT)
+
+
+# ---------------------------------------------------------------------------
+# Hierarchical subdomains (Sec. III.B.1, domain decomposition): one generator,
+# one discriminator per subdomain of every level, all levels partitioning the
+# whole domain.  Stand-in for the paper's METIS partitions of the Hanford site:
+# nested regular grids of the unit square with sides `sides` (e.g. 1, 2, 4 ->
+# 1 + 4 + 16 subdomains).  Sensors and collocation points are stratified over
+# the finest grid's cells (the same count in every cell), so every
+# discriminator can take the same number of sensors from its subdomain
+# (coarser levels take sparser subsets, as the paper balances them).
+# ---------------------------------------------------------------------------
+
+@dataclass
+class Hierarchy:
+    sides: tuple            # grid side per level, coarsest first; each divides the finest
+    idxY: np.ndarray        # [D, mY] int32 indices into the Y sensors
+    idxU: np.ndarray        # [D, mU] int32 indices into the u sensors
+    idxF: np.ndarray        # [D, nF] int32 indices into each sample's collocation points (free sensors)
+    w: np.ndarray           # [D] float32 weight 1 / (levels * subdomains of the level)
+    level: np.ndarray       # [D] level of each discriminator
+
+    @property
+    def D(self) -> int:
+        return int(self.idxY.shape[0])
+
+
+def _cells_of(side: int, fine: int, ci: int, cj: int) -> list[int]:
+    """Finest cells (row-major index) inside subdomain (ci, cj) of a side x side grid."""
+    r = fine // side
+    return [(ci * r + a) * fine + (cj * r + b) for a in range(r) for b in range(r)]
+
+
+def make_hierarchy(sides, m_sensors: int, n_free: int, per_cell_sensors: int, per_cell_points: int) -> Hierarchy:
+    """Index lists of every subdomain's discriminator.  Sensors of finest cell
+    c are c * per_cell_sensors + [0, per_cell_sensors); points of cell c are
+    c * per_cell_points + [0, per_cell_points).  A subdomain covering k cells
+    takes m_sensors / k sensors and n_free / k points from each (the first ones)."""
+    fine = sides[-1]
+    idxY, idxF, w, level = [], [], [], []
+    for lv, side in enumerate(sides):
+        for ci in range(side):
+            for cj in range(side):
+                cells = _cells_of(side, fine, ci, cj)
+                k = len(cells)
+                if m_sensors % k or n_free % k or m_sensors // k > per_cell_sensors or n_free // k > per_cell_points:
+                    raise ValueError("sensor or point counts do not divide over the subdomain's cells")
+                idxY.append([c * per_cell_sensors + j for c in cells for j in range(m_sensors // k)])
+                idxF.append([c * per_cell_points + j for c in cells for j in range(n_free // k)])
+                w.append(1.0 / (len(sides) * side * side))
+                level.append(lv)
+    idxY = np.array(idxY, np.int32)
+    return Hierarchy(tuple(sides), idxY, idxY.copy(), np.array(idxF, np.int32), np.array(w, np.float32),
+                     np.array(level, np.int32))
+
+
+def stratified_points(rng: np.random.Generator, lead: tuple, fine: int, per_cell: int) -> np.ndarray:
+    """[*lead, fine*fine*per_cell, 2] points, per_cell uniform points in each
+    cell of a fine x fine grid of the unit square (cell-major order)."""
+    u = rng.random(lead + (fine * fine, per_cell, 2))
+    ci = np.arange(fine * fine) // fine
+    cj = np.arange(fine * fine) % fine
+    off = np.stack([ci, cj], axis=-1).astype(np.float64)[:, None, :]
+    return ((off + u) / fine).reshape(lead + (fine * fine * per_cell, 2)).astype(np.float32)
+
+
+@dataclass
+class HierInputs:
+    base: StepInputs        # weights (G = 1 generator pair), z, stratified xc / xsY / xsU, f
+    hier: Hierarchy
+    pD: np.ndarray          # [D, nD] one critic per subdomain
+    xf_real: np.ndarray     # [B_r, P, 2] free-sensor locations of the real snapshots
+
+
+def make_hier_inputs(wl: Workload, sides=(1, 2, 4), m_sensors: int = 16, n_free: int = 16,
+                     seed: int | None = None, S: int | None = None, B_r: int | None = None) -> HierInputs:
+    """Inputs of a hierarchical step (2-D): the workload's generator pair and
+    sample counts; sensors and collocation points stratified over the finest
+    cells (n_sY, n_sU and P must be multiples of the cell count); one
+    Glorot-normal critic per subdomain on n_in = 2 m_sensors + n_free (1 + d)."""
+    if wl.d != 2:
+        raise ValueError("the hierarchy is built on the unit square (d = 2)")
+    fine = sides[-1]
+    cells = fine * fine
+    if wl.n_sY % cells or wl.n_sU % cells or wl.P % cells:
+        raise ValueError("n_sY, n_sU and P must be multiples of the finest cell count")
+    seed = wl.seed if seed is None else seed
+    base = make_inputs(wl, seed=seed, S=S, B_r=B_r)
+    r = np.random.default_rng(np.random.SeedSequence(seed).spawn(len(_ROLES) + 2)[-1])
+    Sn, G = base.z.shape[1], base.z.shape[0]
+    base.xsY = stratified_points(r, (G,), fine, wl.n_sY // cells)
+    base.xsU = stratified_points(r, (G,), fine, wl.n_sU // cells)
+    base.xc = stratified_points(r, (G, Sn), fine, wl.P // cells)
+    hier = make_hierarchy(sides, m_sensors, n_free, min(wl.n_sY, wl.n_sU) // cells, wl.P // cells)
+    n_in = 2 * m_sensors + n_free * (1 + wl.d)
+    rd = np.random.default_rng(np.random.SeedSequence(seed).spawn(len(_ROLES) + 3)[-1])
+    pD = np.stack([glorot_mlp(rd, n_in, wl.L_D, wl.W_D) for _ in range(hier.D)])
+    xf_real = stratified_points(rd, (base.z_teach.shape[1],), fine, wl.P // cells)
+    return HierInputs(base, hier, pD, xf_real)
