@@ -257,6 +257,55 @@ pigan_status pigan_trunk_step_grads(const pigan_trunk_desc* s, const float* pT, 
                                     void* stream);
 
 /*
+ * Domain decomposition (Sec. III.B.1): one generator pair for the whole
+ * domain and one critic per subdomain of every level of a hierarchy of
+ * partitions; critic k is weighted w_k = 1 / (levels x subdomains of its
+ * level).  Critic k sees the paper's snapshot of its subdomain,
+ *   [Y at the Y sensors idxY[k] | u at the u sensors idxU[k] |
+ *    the generated source f = -div(exp(Y) grad u) at the free sensors
+ *    idxF[k] (collocation points of the sample) | their coordinates],
+ * and real snapshots in the same layout (f = 0 there, their own free-sensor
+ * coordinates).  Losses per critic: L_D[k] = w_k (mean D_k(fake) -
+ * mean D_k(real)), L_adv[k] = -w_k mean D_k(fake); the generator's loss is
+ * sum_k L_adv[k] + L_pde with L_pde = lambda_pde mean r^2 (0 for the paper's
+ * purely adversarial form).
+ */
+typedef struct {
+  pigan_mlp genY, genU;        /* n_groups = 1; in_dim = d + n_z */
+  pigan_mlp disc;              /* n_groups = D critics; in_dim = mY + mU + nF (1 + d) */
+  int32_t d, n_z, S, P;
+  int32_t n_sY, n_sU, B_r, chunk_S;
+  int32_t mY, mU, nF;          /* inputs of every critic: Y sensors, u sensors, free sensors */
+  pigan_dtype dt;
+  float lambda_pde;            /* >= 0 */
+  float loss_scale;            /* > 0 */
+} pigan_hier_desc;
+
+/* Workspace bytes for pigan_hier_step_grads (0 if the descriptor is invalid). */
+size_t pigan_hier_workspace_bytes(const pigan_hier_desc* s);
+
+/*
+ *   pY, pU : [n_params] generator weights; pD : [D, n_params(disc)] critics.
+ *   z, xc, xsY, xsU, f, f_const : as pigan_train_step_grads with G = 1.
+ *   idxY : [D, mY], idxU : [D, mU] int32 sensor indices; idxF : [D, nF]
+ *          int32 indices into each sample's P collocation points (device).
+ *          An index out of range reads zero and sets *nonfinite = 1.
+ *   real : [D, B_r, disc in_dim] real snapshots; w_disc : [D] critic weights.
+ *   gY, gU : [n_params] gradients of the generator loss; gD : [D, n_params]
+ *   gradients of each L_D[k]; loss : [D, 3] = (L_D[k], L_adv[k], L_pde).
+ *   nonfinite, ws, ws_bytes, stream : as pigan_train_step_grads.
+ * Errors: EINVAL (null pointers, generator n_groups != 1, in_dim mismatch,
+ * negative counts), ENOTSUP (widths), EWORKSPACE, EDEVICE.
+ */
+pigan_status pigan_hier_step_grads(const pigan_hier_desc* s, const float* pY, const float* pU,
+                                   const float* pD, const float* z, const float* xc,
+                                   const float* xsY, const float* xsU, const float* f, float f_const,
+                                   const int32_t* idxY, const int32_t* idxU, const int32_t* idxF,
+                                   const float* real, const float* w_disc, float* gY, float* gU,
+                                   float* gD, float* loss, int32_t* nonfinite, void* ws,
+                                   size_t ws_bytes, void* stream);
+
+/*
  * pigan_adam_update — one update of fp32 master weights from the fp32
  * gradients of a training step (the paper keeps single-precision master
  * weights and adaptive loss scaling, Sec. III.C; it names no optimizer, so

@@ -203,6 +203,10 @@ struct StepPlan {
   DiscBuf D;
   size_t dwp = 0, dwdb = 0, rpart = 0, acc = 0;
   size_t gpg = 0, gpp = 0;   // gradient penalty: critic input gradients [Sc x n_in] fp32, row terms [Sc] fp64
+  // domain decomposition: residual and its critic cotangent [Sc*P] fp32, the
+  // critics' fake-row input cotangents [D][Sc][Kp] fp32
+  size_t hr = 0, hgn = 0, hdx = 0;
+  int GD = 1;
   int64_t dwp_floats = 0, dwdb_floats = 0;
   int rblocks = 0;
   size_t total = 0;
@@ -316,14 +320,75 @@ static void plan_step(const pigan_step_desc* s, int Sc, StepPlan& pl, bool trunk
   pl.total = round_up((int64_t)cv.off, 256);
 }
 
+// one generator pair (a single group) and s->disc.n_groups critics
+static void plan_hier(const pigan_step_desc* s, int Sc, StepPlan& pl) {
+  Carver cv;
+  pl.G = 1;
+  pl.GD = s->disc.n_groups;
+  pl.Sc = Sc;
+  pl.es = esize(s->dt);
+  const int GD = pl.GD;
+  plan_net(cv, pl.Y, s->genY, s->d, 0, s->n_sY, Sc, s->P, pl.es, 1);
+  plan_net(cv, pl.U, s->genU, s->d, s->d, s->n_sU, Sc, s->P, pl.es, 1);
+  DiscBuf& D = pl.D;
+  D.off.init(s->disc.in_dim, s->disc.n_hidden, s->disc.width);
+  const int WD = s->disc.width, LD = s->disc.n_hidden;
+  D.Kp = (int)round_up(s->disc.in_dim, 32);
+  D.Bmax = (int64_t)Sc + s->B_r;
+  D.X0 = cv.take((size_t)D.Bmax * D.Kp * pl.es * GD);
+  D.A.assign(LD + 1, 0);
+  D.H.assign(LD + 1, 0);
+  const size_t act = (size_t)D.Bmax * WD * pl.es * GD;
+  for (int l = 1; l <= LD; ++l) {
+    D.A[l] = cv.take(act);
+    D.H[l] = cv.take(act);
+  }
+  D.dA[0] = cv.take(act);
+  D.dA[1] = cv.take(act);
+  D.score = cv.take((size_t)D.Bmax * 4 * GD);
+  D.seed = cv.take((size_t)D.Bmax * 4 * GD);
+  D.w1 = cv.take((size_t)WD * D.Kp * pl.es * GD);
+  D.w1T = cv.take((size_t)WD * D.Kp * pl.es * GD);
+  const size_t wsz = (size_t)std::max(LD - 1, 1) * WD * WD * pl.es * GD;
+  D.wc = cv.take(wsz);
+  D.wcT = cv.take(wsz);
+  D.ppb = ob_ppb(D.Bmax);
+  D.ob_slots = out_bwd_blocks(D.Bmax, (int)D.ppb);
+  D.ob = cv.take((size_t)D.ob_slots * (WD + 1) * 8 * GD);
+  int64_t mx = 0, mxb = 0;
+  auto consider = [&](int64_t R, int N, int J, int Gx) {
+    int ns;
+    int64_t rps;
+    dw_split_plan(R, N, J, (int)pl.es, Gx, &ns, &rps);
+    mx = std::max(mx, (int64_t)ns * N * J * Gx);
+    mxb = std::max(mxb, (int64_t)ns * N * Gx);
+  };
+  if (s->genY.n_hidden > 1) consider(pl.Y.R, s->genY.width, s->genY.width, 1);
+  if (s->genU.n_hidden > 1) consider(pl.U.R, s->genU.width, s->genU.width, 1);
+  consider(D.Bmax, WD, D.Kp, GD);
+  if (LD > 1) consider(D.Bmax, WD, WD, GD);
+  pl.dwp_floats = mx;
+  pl.dwdb_floats = mxb;
+  pl.dwp = cv.take((size_t)mx * 4);
+  pl.dwdb = cv.take((size_t)mxb * 8);
+  pl.rblocks = residual_blocks((int64_t)Sc * s->P);
+  pl.rpart = cv.take((size_t)pl.rblocks * 8);
+  pl.acc = cv.take((size_t)4 * 8 * GD);
+  pl.hr = cv.take((size_t)Sc * s->P * 4);
+  pl.hgn = cv.take((size_t)Sc * s->P * 4);
+  pl.hdx = cv.take((size_t)Sc * D.Kp * 4 * GD);
+  pl.total = round_up((int64_t)cv.off, 256);
+}
+
 static const size_t kAutoCap = (size_t)64 << 30;
 
-static int choose_chunk(const pigan_step_desc* s, bool trunk = false) {
+static int choose_chunk(const pigan_step_desc* s, bool trunk = false, bool hier = false) {
   if (s->chunk_S > 0) return std::min(s->chunk_S, s->S);
   int Sc = s->S;
   StepPlan pl;
   while (true) {
-    plan_step(s, Sc, pl, trunk);
+    if (hier) plan_hier(s, Sc, pl);
+    else plan_step(s, Sc, pl, trunk);
     if (pl.total <= kAutoCap || Sc == 1) return Sc;
     Sc = (Sc + 1) / 2;
   }
@@ -722,6 +787,75 @@ static pigan_status critic_penalty(void* ws, const StepPlan& pl, const pigan_ste
                         tp<double>(ws, pl.dwdb), G, st);
 }
 
+// Discriminator forward on the B rows of D.X0 (fake rows first, then n_real
+// real rows), its seeds (+w/S fake, -w/B_r real, times the loss scale) and the
+// reverse pass with every weight gradient (accumulated when accum != 0).  On
+// return D.dA[*cur] holds the first layer's pre-activation cotangents.
+template <class T>
+static pigan_status disc_pass(void* ws, const StepPlan& pl, const float* pD, int WD, int LD, int n_in, int B, int Sc,
+                              int n_real, int S, int B_r, const float* w_group, float ls, float inv, int accum,
+                              float* gD, int32_t* nonfinite, double* acc, int G, hipStream_t st, int* cur_out) {
+  const DiscBuf& D = pl.D;
+  const int64_t dact = D.Bmax * WD;
+  pigan_status r;
+  for (int l = 1; l <= LD; ++l) {
+    NtArgs<T> a{};
+    if (l == 1) {
+      a.X = tp<T>(ws, D.X0); a.x_g = D.Bmax * D.Kp; a.ldx = D.Kp;
+      a.Wm = tp<T>(ws, D.w1); a.w_g = (int64_t)WD * D.Kp; a.ldw = D.Kp; a.K = D.Kp;
+    } else {
+      a.X = tp<T>(ws, D.H[l - 1]); a.x_g = dact; a.ldx = WD;
+      a.Wm = tp<T>(ws, D.wc) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD;
+      a.ldw = WD; a.K = WD;
+    }
+    a.bias = pD + D.off.b[l]; a.b_g = D.off.n;
+    a.out_a = tp<T>(ws, D.A[l]); a.out_h = tp<T>(ws, D.H[l]); a.o_g = dact; a.ldo = WD;
+    a.N = WD;
+    a.seg = Seg{B, 0, 0};
+    if ((r = gemm_nt<T>(EPI_FWD, 0, 0, a, G, st, "disc_fwd")) != PIGAN_OK) return r;
+  }
+  {
+    ProfScope ps(st, "out_fwd", 2.0 * B * WD * G, (double)B * WD * sizeof(T) * G);
+    HIP_TRY(launch_out_fwd<T>(tp<T>(ws, D.H[LD]), dact, WD, B, B, WD, pD + D.off.wout, D.off.n,
+                              tp<float>(ws, D.score), D.Bmax, G, st));
+    HIP_TRY(launch_disc_seed(tp<float>(ws, D.score), D.Bmax, Sc, n_real, S, B_r, w_group, ls,
+                             tp<float>(ws, D.seed), acc, 4, G, st));
+  }
+  // discriminator reverse pass
+  {
+    OutBwdArgs<T> ob{};
+    ob.A = tp<T>(ws, D.A[LD]); ob.dA = tp<T>(ws, D.dA[0]); ob.o_g = dact; ob.ldo = WD;
+    ob.gbar = tp<float>(ws, D.seed); ob.gb_g = D.Bmax;
+    ob.wout = pD + D.off.wout; ob.w_g = D.off.n;
+    ob.W = WD; ob.ppb = D.ppb; ob.part = tp<double>(ws, D.ob); ob.n_slots = out_bwd_blocks(B, (int)D.ppb);
+    ob.slot0 = 0; ob.seg = Seg{B, 0, 0};
+    ProfScope ps(st, "out_bwd", 0.0, (double)B * WD * 2 * sizeof(T) * G);
+    HIP_TRY(launch_out_bwd<T>(0, 0, ob, G, st));
+    HIP_TRY(launch_colsum<double>(tp<double>(ws, D.ob), (int64_t)ob.n_slots * (WD + 1), ob.n_slots, WD + 1, WD + 1,
+                                  1, 1, gD + D.off.wout, D.off.n, accum, inv, nonfinite, G, st));
+  }
+  int cur = 0;
+  for (int l = LD; l >= 2; --l) {
+    if ((r = weight_grad<T>(tp<T>(ws, D.dA[cur]), dact, WD, tp<T>(ws, D.H[l - 1]), dact, WD, B, B, WD, WD, WD,
+                            gD + D.off.w[l], gD + D.off.b[l], D.off.n, accum, inv, nonfinite, tp<float>(ws, pl.dwp),
+                            tp<double>(ws, pl.dwdb), G, st)) != PIGAN_OK)
+      return r;
+    NtArgs<T> a{};
+    a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
+    a.Wm = tp<T>(ws, D.wcT) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD; a.ldw = WD;
+    a.aprev = tp<T>(ws, D.A[l - 1]); a.out_da = tp<T>(ws, D.dA[1 - cur]); a.o_g = dact; a.ldo = WD;
+    a.N = WD; a.K = WD; a.seg = Seg{B, 0, 0};
+    if ((r = gemm_nt<T>(EPI_BWD, 0, 0, a, G, st, "disc_bwd")) != PIGAN_OK) return r;
+    cur = 1 - cur;
+  }
+  if ((r = weight_grad<T>(tp<T>(ws, D.dA[cur]), dact, WD, tp<T>(ws, D.X0), D.Bmax * D.Kp, D.Kp, B, B, WD, D.Kp, n_in,
+                          gD + D.off.w[1], gD + D.off.b[1], D.off.n, accum, inv, nonfinite, tp<float>(ws, pl.dwp),
+                          tp<double>(ws, pl.dwdb), G, st)) != PIGAN_OK)
+    return r;
+  *cur_out = cur;
+  return PIGAN_OK;
+}
+
 template <class T>
 static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const float* pY, const float* pU,
                              const float* pD, const float* z, const float* xc, const float* xsY, const float* xsU,
@@ -816,59 +950,9 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
                                     real, (int64_t)s->B_r * n_in, n_real, n_in, tp<T>(ws, D.X0), D.Bmax * D.Kp, D.Kp,
                                     G, st));
     }
-    for (int l = 1; l <= LD; ++l) {
-      NtArgs<T> a{};
-      if (l == 1) {
-        a.X = tp<T>(ws, D.X0); a.x_g = D.Bmax * D.Kp; a.ldx = D.Kp;
-        a.Wm = tp<T>(ws, D.w1); a.w_g = (int64_t)WD * D.Kp; a.ldw = D.Kp; a.K = D.Kp;
-      } else {
-        a.X = tp<T>(ws, D.H[l - 1]); a.x_g = dact; a.ldx = WD;
-        a.Wm = tp<T>(ws, D.wc) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD;
-        a.ldw = WD; a.K = WD;
-      }
-      a.bias = pD + D.off.b[l]; a.b_g = D.off.n;
-      a.out_a = tp<T>(ws, D.A[l]); a.out_h = tp<T>(ws, D.H[l]); a.o_g = dact; a.ldo = WD;
-      a.N = WD;
-      a.seg = Seg{B, 0, 0};
-      if ((r = gemm_nt<T>(EPI_FWD, 0, 0, a, G, st, "disc_fwd")) != PIGAN_OK) return r;
-    }
-    {
-      ProfScope ps(st, "out_fwd", 2.0 * B * WD * G, (double)B * WD * sizeof(T) * G);
-      HIP_TRY(launch_out_fwd<T>(tp<T>(ws, D.H[LD]), dact, WD, B, B, WD, pD + D.off.wout, D.off.n,
-                                tp<float>(ws, D.score), D.Bmax, G, st));
-      HIP_TRY(launch_disc_seed(tp<float>(ws, D.score), D.Bmax, Sc, n_real, S, s->B_r, w_group, ls,
-                               tp<float>(ws, D.seed), acc, 4, G, st));
-    }
-    // discriminator reverse pass
-    {
-      OutBwdArgs<T> ob{};
-      ob.A = tp<T>(ws, D.A[LD]); ob.dA = tp<T>(ws, D.dA[0]); ob.o_g = dact; ob.ldo = WD;
-      ob.gbar = tp<float>(ws, D.seed); ob.gb_g = D.Bmax;
-      ob.wout = pD + D.off.wout; ob.w_g = D.off.n;
-      ob.W = WD; ob.ppb = D.ppb; ob.part = tp<double>(ws, D.ob); ob.n_slots = out_bwd_blocks(B, (int)D.ppb);
-      ob.slot0 = 0; ob.seg = Seg{B, 0, 0};
-      ProfScope ps(st, "out_bwd", 0.0, (double)B * WD * 2 * sizeof(T) * G);
-      HIP_TRY(launch_out_bwd<T>(0, 0, ob, G, st));
-      HIP_TRY(launch_colsum<double>(tp<double>(ws, D.ob), (int64_t)ob.n_slots * (WD + 1), ob.n_slots, WD + 1, WD + 1,
-                                    1, 1, gD + D.off.wout, D.off.n, accum, inv, nonfinite, G, st));
-    }
     int cur = 0;
-    for (int l = LD; l >= 2; --l) {
-      if ((r = weight_grad<T>(tp<T>(ws, D.dA[cur]), dact, WD, tp<T>(ws, D.H[l - 1]), dact, WD, B, B, WD, WD, WD,
-                              gD + D.off.w[l], gD + D.off.b[l], D.off.n, accum, inv, nonfinite, tp<float>(ws, pl.dwp),
-                              tp<double>(ws, pl.dwdb), G, st)) != PIGAN_OK)
-        return r;
-      NtArgs<T> a{};
-      a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
-      a.Wm = tp<T>(ws, D.wcT) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD; a.ldw = WD;
-      a.aprev = tp<T>(ws, D.A[l - 1]); a.out_da = tp<T>(ws, D.dA[1 - cur]); a.o_g = dact; a.ldo = WD;
-      a.N = WD; a.K = WD; a.seg = Seg{B, 0, 0};
-      if ((r = gemm_nt<T>(EPI_BWD, 0, 0, a, G, st, "disc_bwd")) != PIGAN_OK) return r;
-      cur = 1 - cur;
-    }
-    if ((r = weight_grad<T>(tp<T>(ws, D.dA[cur]), dact, WD, tp<T>(ws, D.X0), D.Bmax * D.Kp, D.Kp, B, B, WD, D.Kp, n_in,
-                            gD + D.off.w[1], gD + D.off.b[1], D.off.n, accum, inv, nonfinite, tp<float>(ws, pl.dwp),
-                            tp<double>(ws, pl.dwdb), G, st)) != PIGAN_OK)
+    if ((r = disc_pass<T>(ws, pl, pD, WD, LD, n_in, B, Sc, n_real, S, s->B_r, w_group, ls, inv, accum, gD, nonfinite,
+                          acc, G, st, &cur)) != PIGAN_OK)
       return r;
     {
       // d(L_adv)/dF = -dL_D/dF for the fake rows -> generator sensor cotangents
@@ -902,6 +986,124 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
     ProfScope ps(st, "misc", 0.0, 0.0);
     HIP_TRY(launch_losses(acc, 4, w_group, S, s->B_r, (int64_t)S * P, s->lambda_pde, s->lambda_gp,
                           std::min(S, s->B_r), loss, gp, nonfinite, G, st));
+  }
+  return PIGAN_OK;
+}
+
+// Domain decomposition: one generator pair, s->disc.n_groups critics (one per
+// subdomain), each on the paper's snapshot of its subdomain (Y and u sensors,
+// the generated source at free sensors and their coordinates).
+template <class T>
+static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const float* pY, const float* pU,
+                             const float* pD, const float* z, const float* xc, const float* xsY, const float* xsU,
+                             const float* f, float f_const, const int32_t* idxY, const int32_t* idxU,
+                             const int32_t* idxF, int mY, int mU, int nF, const float* real, const float* w_disc,
+                             float* gY, float* gU, float* gD, float* loss, int32_t* nonfinite, void* ws,
+                             hipStream_t st) {
+  const int GD = pl.GD, d = s->d, n_z = s->n_z, P = s->P, S = s->S;
+  const float ls = s->loss_scale;
+  const float inv = 1.0f / ls;
+  const DiscBuf& D = pl.D;
+  const int WD = s->disc.width, LD = s->disc.n_hidden, n_in = s->disc.in_dim;
+  double* acc = tp<double>(ws, pl.acc);
+  pigan_status r;
+  {
+    ProfScope ps(st, "misc", 0.0, 0.0);
+    HIP_TRY(launch_zero(acc, 4 * GD, nonfinite, st));
+    if ((r = cast_gen_weights<T>(ws, pl.Y, pY, 1, st)) != PIGAN_OK) return r;
+    if ((r = cast_gen_weights<T>(ws, pl.U, pU, 1, st)) != PIGAN_OK) return r;
+    HIP_TRY(launch_cast<T>(pD + D.off.w[1], D.off.n, WD, n_in, D.Kp, tp<T>(ws, D.w1), tp<T>(ws, D.w1T),
+                           (int64_t)WD * D.Kp, GD, st));
+    const int64_t dgl = (int64_t)std::max(LD - 1, 1) * WD * WD;
+    for (int l = 2; l <= LD; ++l)
+      HIP_TRY(launch_cast<T>(pD + D.off.w[l], D.off.n, WD, WD, WD, tp<T>(ws, D.wc) + (size_t)(l - 2) * WD * WD,
+                             tp<T>(ws, D.wcT) + (size_t)(l - 2) * WD * WD, dgl, GD, st));
+  }
+  const int64_t xs_gY = (int64_t)s->n_sY * d, xs_gU = (int64_t)s->n_sU * d;
+  const int64_t xc_g = (int64_t)S * P * d, z_g = (int64_t)S * n_z;
+  float* rbuf = tp<float>(ws, pl.hr);
+  float* gN = tp<float>(ws, pl.hgn);
+  float* dX = tp<float>(ws, pl.hdx);
+  const int64_t dx_g = (int64_t)pl.Sc * D.Kp;
+  for (int s0 = 0, ci = 0; s0 < S; s0 += pl.Sc, ++ci) {
+    const int Sc = std::min(pl.Sc, S - s0);
+    const int accum = ci > 0;
+    const float* zc = z + (int64_t)s0 * n_z;
+    const float* xcc = xc + (int64_t)s0 * P * d;
+    NetBuf Yc = pl.Y, Uc = pl.U;
+    for (NetBuf* nb : {&Yc, &Uc}) {
+      nb->n_sen = (int64_t)Sc * nb->n_s;
+      nb->n_col = (int64_t)Sc * P;
+      nb->rows = nb->n_sen + (1 + nb->nd1 + nb->nd2) * nb->n_col;
+    }
+    if ((r = gen_chunk_fwd<T>(ws, Yc, pY, xsY, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, 1, st)) != PIGAN_OK) return r;
+    if ((r = gen_chunk_fwd<T>(ws, Uc, pU, xsU, xs_gU, xcc, xc_g, zc, z_g, d, n_z, Sc, P, 1, st)) != PIGAN_OK) return r;
+    const int64_t M = (int64_t)Sc * P;
+    ResidArgs ra{};
+    ra.jY = tp<float>(ws, Yc.jet); ra.jy_g = Yc.R; ra.offY = Yc.n_sen;
+    ra.jU = tp<float>(ws, Uc.jet); ra.ju_g = Uc.R; ra.offU = Uc.n_sen;
+    ra.plane = Yc.n_col; ra.M = M; ra.d = d;
+    ra.f = f ? f + (int64_t)s0 * P : nullptr; ra.f_g = (int64_t)S * P; ra.f_const = f_const;
+    {
+      // the residual (its values feed the critics' free sensors) and the penalty's sum
+      ProfScope ps(st, "residual", 0.0, (double)M * (3 * d + 2) * 4.0);
+      ResidArgs r1 = ra;
+      r1.r = rbuf; r1.r_g = M; r1.part = tp<double>(ws, pl.rpart);
+      HIP_TRY(launch_residual(r1, 1, st));
+      HIP_TRY(launch_sum_partials(tp<double>(ws, pl.rpart), residual_blocks(M), acc, 4, 2, 1, st));
+    }
+    HierSnap h{};
+    h.jY = tp<float>(ws, Yc.jet); h.jU = tp<float>(ws, Uc.jet); h.nsY = s->n_sY; h.nsU = s->n_sU;
+    h.r = rbuf; h.f = ra.f; h.f_const = f_const; h.xc = xcc; h.P = P; h.d = d;
+    h.idxY = idxY; h.idxU = idxU; h.idxF = idxF; h.mY = mY; h.mU = mU; h.nF = nF; h.n_in = n_in;
+    h.bad = nonfinite;
+    const int n_real = ci == 0 ? s->B_r : 0;
+    const int B = Sc + n_real;
+    {
+      ProfScope ps(st, "misc", 0.0, 0.0);
+      HIP_TRY(launch_fill_f32(tp<float>(ws, Yc.gbar), Yc.rows, Yc.R, 0.0f, 1, st));
+      HIP_TRY(launch_fill_f32(tp<float>(ws, Uc.gbar), Uc.rows, Uc.R, 0.0f, 1, st));
+      HIP_TRY(launch_fill_f32(gN, M, M, 0.0f, 1, st));
+      HIP_TRY(launch_hier_snap<T>(h, Sc, real, (int64_t)s->B_r * n_in, n_real, tp<T>(ws, D.X0), D.Bmax * D.Kp,
+                                  D.Kp, GD, st));
+    }
+    int cur = 0;
+    if ((r = disc_pass<T>(ws, pl, pD, WD, LD, n_in, B, Sc, n_real, S, s->B_r, w_disc, ls, inv, accum, gD, nonfinite,
+                          acc, GD, st, &cur)) != PIGAN_OK)
+      return r;
+    {
+      // -dL_D/dX of every critic's fake rows (all inputs), then added to the
+      // generator outputs they were read from
+      const int64_t dact = D.Bmax * WD;
+      NtArgs<T> a{};
+      a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
+      a.Wm = tp<T>(ws, D.w1T); a.w_g = (int64_t)WD * D.Kp; a.ldw = WD;
+      a.N = D.Kp; a.K = WD; a.seg = Seg{Sc, 0, 0};
+      a.seedY = dX; a.sY_g = dx_g; a.sY_ld = D.Kp; a.nY = n_in; a.nU = 0; a.df_sign = -1.0f;
+      if ((r = gemm_nt<T>(EPI_DF, 0, 0, a, GD, st, "disc_bwd")) != PIGAN_OK) return r;
+      ProfScope ps(st, "misc", 0.0, 0.0);
+      HIP_TRY(launch_hier_scatter(h, dX, dx_g, D.Kp, Sc, GD, tp<float>(ws, Yc.gbar), tp<float>(ws, Uc.gbar), gN, st));
+    }
+    {
+      // jet cotangents from the penalty and the critics' source cotangents
+      ProfScope ps(st, "residual", 0.0, (double)M * (3 * d + 2) * 4.0 * 2);
+      ResidArgs r2 = ra;
+      r2.gY = tp<float>(ws, Yc.gbar); r2.gU = tp<float>(ws, Uc.gbar); r2.gq = gN; r2.gq_g = M;
+      r2.qscale = (float)(2.0 * s->lambda_pde * ls / ((double)S * P));
+      HIP_TRY(launch_residual(r2, 1, st));
+    }
+    if ((r = gen_chunk_bwd<T>(ws, pl, Yc, pY, xsY, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, gY, accum, inv, nonfinite,
+                              1, st)) != PIGAN_OK)
+      return r;
+    if ((r = gen_chunk_bwd<T>(ws, pl, Uc, pU, xsU, xs_gU, xcc, xc_g, zc, z_g, d, n_z, Sc, P, gU, accum, inv, nonfinite,
+                              1, st)) != PIGAN_OK)
+      return r;
+  }
+  {
+    ProfScope ps(st, "misc", 0.0, 0.0);
+    HIP_TRY(launch_losses(acc, 4, w_disc, S, s->B_r, (int64_t)S * P, 0.0f, 0.0f, 0, loss, nullptr, nonfinite, GD,
+                          st));
+    HIP_TRY(launch_hier_pde_loss(acc, 2, s->lambda_pde, (int64_t)S * P, loss, GD, nonfinite, st));
   }
   return PIGAN_OK;
 }
@@ -964,6 +1166,41 @@ static pigan_status train_step_entry(const pigan_step_desc* s, const float* pY, 
   }
 }
 
+// descriptor of the domain-decomposition step as the shared step fields
+static pigan_status check_hier(const pigan_hier_desc* h, pigan_step_desc* out) {
+  if (!h) return fail(PIGAN_EINVAL, "null hierarchical step descriptor");
+  pigan_status st;
+  if ((st = check_mlp(&h->genY, "genY")) != PIGAN_OK) return st;
+  if ((st = check_mlp(&h->genU, "genU")) != PIGAN_OK) return st;
+  if ((st = check_mlp(&h->disc, "disc")) != PIGAN_OK) return st;
+  if ((st = check_dtype(h->dt)) != PIGAN_OK) return st;
+  if (h->genY.n_groups != 1 || h->genU.n_groups != 1)
+    return fail(PIGAN_EINVAL, "one generator pair for the whole domain: genY/genU n_groups must be 1");
+  if (h->d < 1 || h->d > 3) return fail(PIGAN_EINVAL, "d=%d must be 1, 2 or 3", h->d);
+  if (h->n_z < 1) return fail(PIGAN_EINVAL, "n_z=%d must be >= 1", h->n_z);
+  if (h->genY.in_dim != h->d + h->n_z || h->genU.in_dim != h->d + h->n_z)
+    return fail(PIGAN_EINVAL, "generator in_dim must equal d + n_z = %d", h->d + h->n_z);
+  if (h->S < 1 || h->P < 1) return fail(PIGAN_EINVAL, "S=%d and P=%d must be >= 1", h->S, h->P);
+  if (h->n_sY < 1 || h->n_sU < 1) return fail(PIGAN_EINVAL, "n_sY=%d and n_sU=%d must be >= 1", h->n_sY, h->n_sU);
+  if (h->mY < 0 || h->mU < 0 || h->nF < 0 || h->mY + h->mU + h->nF < 1)
+    return fail(PIGAN_EINVAL, "mY=%d, mU=%d, nF=%d must be >= 0 with at least one input", h->mY, h->mU, h->nF);
+  if (h->disc.in_dim != h->mY + h->mU + h->nF * (1 + h->d))
+    return fail(PIGAN_EINVAL, "disc in_dim=%d must equal mY + mU + nF (1 + d) = %d", h->disc.in_dim,
+                h->mY + h->mU + h->nF * (1 + h->d));
+  if (h->B_r < 1) return fail(PIGAN_EINVAL, "B_r=%d must be >= 1", h->B_r);
+  if (h->chunk_S < 0) return fail(PIGAN_EINVAL, "chunk_S=%d must be >= 0", h->chunk_S);
+  if (!(h->lambda_pde >= 0.0f) || !__builtin_isfinite(h->lambda_pde))
+    return fail(PIGAN_EINVAL, "lambda_pde must be finite and >= 0");
+  if (!(h->loss_scale > 0.0f) || !__builtin_isfinite(h->loss_scale))
+    return fail(PIGAN_EINVAL, "loss_scale must be finite and > 0");
+  pigan_step_desc s{};
+  s.genY = h->genY; s.genU = h->genU; s.disc = h->disc;
+  s.d = h->d; s.n_z = h->n_z; s.S = h->S; s.P = h->P; s.n_sY = h->n_sY; s.n_sU = h->n_sU; s.B_r = h->B_r;
+  s.chunk_S = h->chunk_S; s.dt = h->dt; s.lambda_pde = h->lambda_pde; s.lambda_gp = 0.0f; s.loss_scale = h->loss_scale;
+  *out = s;
+  return PIGAN_OK;
+}
+
 // the trunk step runs on the step machinery: the trunk in the Y slot (and,
 // for the shape checks, the U slot), no gradient penalty
 static pigan_step_desc trunk_as_step(const pigan_trunk_desc* t) {
@@ -991,6 +1228,48 @@ pigan_status pigan_adam_update(int64_t n, float* params, const float* grads, flo
   hipError_t e = launch_adam(n, params, grads, m, v, lr, beta1, beta2, eps, c1, c2, skip, (hipStream_t)stream);
   if (e != hipSuccess) return fail(PIGAN_EDEVICE, "adam update: %s", hipGetErrorString(e));
   return PIGAN_OK;
+}
+
+size_t pigan_hier_workspace_bytes(const pigan_hier_desc* h) {
+  pigan_step_desc s;
+  if (check_hier(h, &s) != PIGAN_OK) return 0;
+  StepPlan pl;
+  plan_hier(&s, choose_chunk(&s, false, true), pl);
+  return pl.total;
+}
+
+pigan_status pigan_hier_step_grads(const pigan_hier_desc* h, const float* pY, const float* pU, const float* pD,
+                                   const float* z, const float* xc, const float* xsY, const float* xsU,
+                                   const float* f, float f_const, const int32_t* idxY, const int32_t* idxU,
+                                   const int32_t* idxF, const float* real, const float* w_disc, float* gY, float* gU,
+                                   float* gD, float* loss, int32_t* nonfinite, void* ws, size_t ws_bytes,
+                                   void* stream) {
+  g_err.clear();
+  pigan_step_desc s;
+  pigan_status st = check_hier(h, &s);
+  if (st != PIGAN_OK) return st;
+  if (!pY || !pU || !pD || !z || !xc || !xsY || !xsU || !real || !w_disc || !gY || !gU || !gD || !loss || !nonfinite)
+    return fail(PIGAN_EINVAL, "null input or output pointer");
+  if ((h->mY > 0 && !idxY) || (h->mU > 0 && !idxU) || (h->nF > 0 && !idxF))
+    return fail(PIGAN_EINVAL, "null sensor index list");
+  if (!__builtin_isfinite(f_const)) return fail(PIGAN_EINVAL, "f_const must be finite");
+  StepPlan pl;
+  plan_hier(&s, choose_chunk(&s, false, true), pl);
+  if (!ws) return fail(PIGAN_EWORKSPACE, "null workspace (need %zu bytes)", pl.total);
+  if (ws_bytes < pl.total) return fail(PIGAN_EWORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, pl.total);
+  if ((uintptr_t)ws % 256) return fail(PIGAN_EINVAL, "workspace must be 256-byte aligned");
+  hipStream_t hs = (hipStream_t)stream;
+  switch (s.dt) {
+    case PIGAN_FP32:
+      return run_hier<float>(&s, pl, pY, pU, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, h->mY, h->mU, h->nF,
+                             real, w_disc, gY, gU, gD, loss, nonfinite, ws, hs);
+    case PIGAN_BF16:
+      return run_hier<bf16>(&s, pl, pY, pU, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, h->mY, h->mU, h->nF,
+                            real, w_disc, gY, gU, gD, loss, nonfinite, ws, hs);
+    default:
+      return run_hier<f16>(&s, pl, pY, pU, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, h->mY, h->mU, h->nF,
+                           real, w_disc, gY, gU, gD, loss, nonfinite, ws, hs);
+  }
 }
 
 int64_t pigan_trunk_param_count(const pigan_mlp* net) {

@@ -19,6 +19,7 @@ struct ResidArgs {
   const float* f; int64_t f_g; float f_const;
   float* r; int64_t r_g;
   float* gY; float* gU;                          // cotangent vectors (same layout as the jets) or null
+  const float* gq; int64_t gq_g;                 // extra cotangent of r per point (critics of the free sensors) or null
   const float* w_group; float qscale;            // q = qscale * w_g * r
   double* part;                                  // [G][blocks] partial sums of r^2, or null
 };
@@ -89,6 +90,25 @@ hipError_t launch_snap_fill_rows(const float* yY, int64_t yY_g, const float* yU,
 hipError_t launch_concat_rows(const float* a, int64_t a_g, int na, const float* b, int64_t b_g, int nb, int d,
                               float* out, int64_t o_g, int G, hipStream_t st);
 hipError_t launch_fill_f32(float* p, int64_t n, int64_t p_g, float v, int G, hipStream_t st);
+
+// domain decomposition: the snapshots of D critics (one per subdomain) and the
+// scatter of their input cotangents back to the generator's outputs
+struct HierSnap {
+  const float* jY; const float* jU; int nsY; int nsU;    // sensor values of the chunk: [s * ns + sensor]
+  const float* r; const float* f; float f_const;         // residual [s * P + p]; source (chunk view) or null
+  const float* xc; int P; int d;                         // collocation points of the chunk [s][P][d]
+  const int32_t* idxY; const int32_t* idxU; const int32_t* idxF;  // [D][mY], [D][mU], [D][nF]
+  int mY; int mU; int nF; int n_in;
+  int32_t* bad;                                          // set to 1 on an index out of range
+};
+template <class T>
+hipError_t launch_hier_snap(const HierSnap& h, int n_fake, const float* real, int64_t real_g, int n_real, T* X,
+                            int64_t x_g, int ldx, int D, hipStream_t st);
+hipError_t launch_hier_scatter(const HierSnap& h, const float* dX, int64_t dx_g, int ldx, int n_fake, int D,
+                               float* gY, float* gU, float* gN, hipStream_t st);
+// loss[k][2] = lambda_pde * acc[slot] / SP for every critic k
+hipError_t launch_hier_pde_loss(const double* acc, int slot, float lambda_pde, int64_t SP, float* loss, int D,
+                                int32_t* nonfinite, hipStream_t st);
 // dst[(col/Jp)*J + col%Jp] (+)= scale * sum_slots part[g][slot][col]  (fp64, fixed order)
 template <class Tin>
 hipError_t launch_colsum(const Tin* part, int64_t p_g, int n_slots, int64_t slot_stride, int64_t ncols, int Jp, int J,

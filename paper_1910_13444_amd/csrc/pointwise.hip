@@ -175,7 +175,7 @@ k_residual(ResidArgs p) {
     r2 = (double)r * (double)r;
     if (p.gY) {
       const float w = p.w_group ? p.w_group[g] : 1.0f;
-      const float q = p.qscale * w * r;
+      const float q = p.qscale * w * r + (p.gq ? p.gq[g * p.gq_g + pt] : 0.0f);
       float* gy = p.gY + g * p.jy_g + p.offY;
       float* gu = p.gU + g * p.ju_g + p.offU;
       gy[pt] = q * (r + f);
@@ -604,6 +604,82 @@ __global__ void k_fill_f32(float* __restrict__ p, int64_t n, int64_t p_g, float 
 }
 
 // ---------------------------------------------------------------------------
+// Domain decomposition (one critic per subdomain, grid z = critic k).  Fake
+// row b (sample b of the chunk) of critic k's snapshot: [Y at sensors
+// idxY[k] | u at sensors idxU[k] | the generated source N = r + f at the free
+// sensors idxF[k] (collocation points of the sample) | their coordinates];
+// real rows follow.  Indices out of range read zero and raise h.bad.
+// ---------------------------------------------------------------------------
+template <class T>
+__global__ void k_hier_snap(HierSnap h, int n_fake, const float* __restrict__ real, int64_t real_g, int n_real,
+                            T* __restrict__ X, int64_t x_g, int ldx) {
+  const int k = blockIdx.z;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)(n_fake + n_real) * ldx) return;
+  const int b = (int)(idx / ldx), j = (int)(idx % ldx);
+  float v = 0.0f;
+  if (j < h.n_in) {
+    if (b < n_fake) {
+      const int e1 = h.mY, e2 = e1 + h.mU, e3 = e2 + h.nF;
+      if (j < e1) {
+        const int i = h.idxY[(int64_t)k * h.mY + j];
+        if (i >= 0 && i < h.nsY) v = h.jY[(int64_t)b * h.nsY + i];
+        else *h.bad = 1;
+      } else if (j < e2) {
+        const int i = h.idxU[(int64_t)k * h.mU + (j - e1)];
+        if (i >= 0 && i < h.nsU) v = h.jU[(int64_t)b * h.nsU + i];
+        else *h.bad = 1;
+      } else {
+        const int q = j < e3 ? j - e2 : (j - e3) / h.d;
+        const int i = h.idxF[(int64_t)k * h.nF + q];
+        if (i >= 0 && i < h.P) {
+          const int64_t pt = (int64_t)b * h.P + i;
+          v = j < e3 ? h.r[pt] + (h.f ? h.f[pt] : h.f_const) : h.xc[pt * h.d + (j - e3) % h.d];
+        } else {
+          *h.bad = 1;
+        }
+      }
+    } else {
+      v = real[k * real_g + (int64_t)(b - n_fake) * h.n_in + j];
+    }
+  }
+  X[k * x_g + idx] = Elem<T>::from_f(v);
+}
+
+// One thread per sample: critics in order, then their inputs in order, so
+// every target accumulates in a fixed order (indices repeated within or across
+// critics add up deterministically).  Coordinates carry no cotangent.
+__global__ void k_hier_scatter(HierSnap h, const float* __restrict__ dX, int64_t dx_g, int ldx, int n_fake, int D,
+                               float* __restrict__ gY, float* __restrict__ gU, float* __restrict__ gN) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= n_fake) return;
+  for (int k = 0; k < D; ++k) {
+    const float* row = dX + k * dx_g + (int64_t)b * ldx;
+    for (int j = 0; j < h.mY; ++j) {
+      const int i = h.idxY[(int64_t)k * h.mY + j];
+      if (i >= 0 && i < h.nsY) gY[(int64_t)b * h.nsY + i] += row[j];
+    }
+    for (int j = 0; j < h.mU; ++j) {
+      const int i = h.idxU[(int64_t)k * h.mU + j];
+      if (i >= 0 && i < h.nsU) gU[(int64_t)b * h.nsU + i] += row[h.mY + j];
+    }
+    for (int j = 0; j < h.nF; ++j) {
+      const int i = h.idxF[(int64_t)k * h.nF + j];
+      if (i >= 0 && i < h.P) gN[(int64_t)b * h.P + i] += row[h.mY + h.mU + j];
+    }
+  }
+}
+
+__global__ void k_hier_pde_loss(const double* __restrict__ acc, int slot, float lambda_pde, int64_t SP, float* loss,
+                                int D, int32_t* nonfinite) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= D) return;
+  const double Lp = (double)lambda_pde * acc[slot] / (double)SP;
+  loss[3 * k + 2] = (float)Lp;
+  if (k == 0 && !__builtin_isfinite(Lp)) *nonfinite = 1;
+}
+
+// ---------------------------------------------------------------------------
 // dst (+)= scale * sum over slots of part[g][slot][col], fp64, fixed order.
 // 32 columns x 8 slot groups per block; group q sums slots q, q+8, ...; the
 // eight group sums are added in group order.  Column col maps to
@@ -972,6 +1048,29 @@ hipError_t launch_concat_rows(const float* a, int64_t a_g, int na, const float* 
   return hipGetLastError();
 }
 
+template <class T>
+hipError_t launch_hier_snap(const HierSnap& h, int n_fake, const float* real, int64_t real_g, int n_real, T* X,
+                            int64_t x_g, int ldx, int D, hipStream_t st) {
+  const int64_t tot = (int64_t)(n_fake + n_real) * ldx;
+  if (tot <= 0 || D <= 0) return hipSuccess;
+  k_hier_snap<T><<<dim3(nblk(tot, 256), 1, D), 256, 0, st>>>(h, n_fake, real, real_g, n_real, X, x_g, ldx);
+  return hipGetLastError();
+}
+
+hipError_t launch_hier_scatter(const HierSnap& h, const float* dX, int64_t dx_g, int ldx, int n_fake, int D,
+                               float* gY, float* gU, float* gN, hipStream_t st) {
+  if (n_fake <= 0 || D <= 0) return hipSuccess;
+  k_hier_scatter<<<nblk(n_fake, 64), 64, 0, st>>>(h, dX, dx_g, ldx, n_fake, D, gY, gU, gN);
+  return hipGetLastError();
+}
+
+hipError_t launch_hier_pde_loss(const double* acc, int slot, float lambda_pde, int64_t SP, float* loss, int D,
+                                int32_t* nonfinite, hipStream_t st) {
+  if (D <= 0) return hipSuccess;
+  k_hier_pde_loss<<<nblk(D, 64), 64, 0, st>>>(acc, slot, lambda_pde, SP, loss, D, nonfinite);
+  return hipGetLastError();
+}
+
 hipError_t launch_fill_f32(float* p, int64_t n, int64_t p_g, float v, int G, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   k_fill_f32<<<dim3(nblk(n, 256), 1, G), 256, 0, st>>>(p, n, p_g, v);
@@ -1036,6 +1135,8 @@ hipError_t launch_cast(const float* src, int64_t s_g, int N, int K, int Kp, T* d
                                           const float*, int64_t, int, int, T*, int64_t, int, int, hipStream_t); \
   template hipError_t launch_out_bwd<T>(int, int, const OutBwdArgs<T>&, int, hipStream_t);                    \
   template hipError_t launch_out2_bwd<T>(int, int, const Out2BwdArgs<T>&, int, hipStream_t);                  \
+  template hipError_t launch_hier_snap<T>(const HierSnap&, int, const float*, int64_t, int, T*, int64_t, int, int, \
+                                          hipStream_t);                                                          \
   template hipError_t launch_snap_fill_rows<T>(const float*, int64_t, const float*, int64_t, int, int, int, int, \
                                                int, const float*, int64_t, int, int, T*, int64_t, int, int,     \
                                                hipStream_t);                                                    \

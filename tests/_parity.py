@@ -139,3 +139,34 @@ def trunk_errors(wl, out, ref):
     for i, k in enumerate(("L_D", "L_adv", "L_pde")):
         errs[k] = rel(out["loss"][:, i], ref["loss"][:, i])
     return errs
+
+
+def run_hier_gpu(wl, hi, real, lam=0.0, chunk_S=0, dtype=None, idx=None, f=None, f_const=0.0):
+    """One domain-decomposition step through pigan_hier_step_grads."""
+    import torch
+    from paper_1910_13444_amd import pigan
+    b, h = hi.base, hi.hier
+    iY, iU, iF = idx if idx is not None else (h.idxY, h.idxU, h.idxF)
+    desc = pigan.hier_desc(wl, h.D, iY.shape[1], iU.shape[1], iF.shape[1], S=b.z.shape[1], B_r=real.shape[1],
+                           chunk_S=chunk_S, dtype=dtype, lambda_pde=lam)
+    step = pigan.HierStep(desc)
+
+    def ti(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+    o = step(to_dev(b.pY[0]), to_dev(b.pU[0]), to_dev(hi.pD), to_dev(b.z[0]), to_dev(b.xc[0]), to_dev(b.xsY[0]),
+             to_dev(b.xsU[0]), ti(iY), ti(iU), ti(iF), to_dev(real), to_dev(h.w),
+             f=None if f is None else to_dev(f), f_const=f_const)
+    torch.cuda.synchronize()
+    return dict(gY=o.gY.cpu().numpy(), gU=o.gU.cpu().numpy(), gD=o.gD.cpu().numpy(), loss=o.loss.cpu().numpy(),
+                nonfinite=int(o.nonfinite.cpu().item()))
+
+
+def hier_errors(wl, out, ref, n_in):
+    errs = {}
+    errs.update(grad_errors(out["gY"][None], ref["gY"][None], wl.gen_shape(), "gY"))
+    errs.update(grad_errors(out["gU"][None], ref["gU"][None], wl.gen_shape(), "gU"))
+    errs.update(grad_errors(out["gD"], ref["gD"], (n_in, wl.L_D, wl.W_D), "gD"))
+    errs["L_D"] = rel(out["loss"][:, 0], ref["L_D"])
+    errs["L_adv"] = rel(out["loss"][:, 1], ref["L_adv"])
+    errs["L_pde"] = rel(out["loss"][:, 2], np.full(len(ref["L_D"]), ref["L_pde"]))
+    return errs

@@ -189,3 +189,31 @@ def test_adam_update_validation():
     assert adam(10, t=0) == pigan.EINVAL
     assert adam(10, b1=1.0) == pigan.EINVAL and adam(10, b2=-0.1) == pigan.EINVAL
     assert adam(10, lr=float("inf")) == pigan.EINVAL and adam(10, eps=-1.0) == pigan.EINVAL
+
+
+def _hier(desc, ws_bytes, ptr=FAKE, idx=FAKE, ws=FAKE):
+    return pigan.lib().pigan_hier_step_grads(C.byref(desc), *([ptr] * 7), None, 0.0, idx, idx, idx, ptr, ptr, ptr, ptr,
+                                             ptr, ptr, ptr, ws, ws_bytes, None)
+
+
+def test_hier_step_validation():
+    wl = configs.C2.with_(n_sY=256, n_sU=256)
+    d = pigan.hier_desc(wl, 21, 16, 16, 16)
+    need = int(pigan.lib().pigan_hier_workspace_bytes(C.byref(d)))
+    assert need > 0
+    assert _hier(d, need, ptr=None) == pigan.EINVAL
+    assert _hier(d, need, idx=None) == pigan.EINVAL
+    assert _hier(d, need - 1) == pigan.EWORKSPACE
+    assert _hier(d, need, ws=C.c_void_p(4096 + 32)) == pigan.EINVAL
+    for field, value in (("mY", -1), ("nF", -3), ("B_r", 0), ("lambda_pde", -1.0), ("d", 5)):
+        e = pigan.hier_desc(wl, 21, 16, 16, 16)
+        setattr(e, field, value)
+        assert _hier(e, 1 << 40) == pigan.EINVAL, field
+    e = pigan.hier_desc(wl, 21, 16, 16, 16)
+    e.genY.n_groups = 2                                    # one generator pair only
+    assert _hier(e, 1 << 40) == pigan.EINVAL
+    e = pigan.hier_desc(wl, 21, 16, 16, 16)
+    e.disc.in_dim = 81                                     # != mY + mU + nF (1 + d)
+    assert _hier(e, 1 << 40) == pigan.EINVAL
+    e = pigan.hier_desc(wl, 21, 0, 0, 0)
+    assert _hier(e, 1 << 40) == pigan.EINVAL

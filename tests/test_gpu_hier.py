@@ -1,0 +1,87 @@
+"""GPU parity of the domain-decomposition step (pigan_hier_step_grads): one
+generator pair, one critic per subdomain of a 1 + 4 (+ 16) hierarchy, the
+paper's snapshot with free-sensor sources and coordinates; every weight tensor
+of the generators and of every critic, and the losses, against the oracle."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1910_13444_amd import configs
+from paper_1910_13444_amd.inputs import make_hier_inputs
+from _parity import TOL, check, check_conditioned, hier_errors, run_hier_gpu
+
+pytestmark = pytest.mark.gpu
+
+TINY = configs.C2.with_(n_sY=16, n_sU=16, S=3, P=16, B_r=2, W=32, W_D=32, L=3, L_D=2, n_z=3, dtype="fp32", seed=81)
+
+CASES = {
+    # name: (workload, sides, sensors per critic, free sensors per critic, lambda_pde, f_const)
+    "tiny_1x2_fp32": (TINY, (1, 2), 4, 4, 0.5, 0.3),
+    "c2_1x2x4_bf16": (configs.C2.with_(n_sY=256, n_sU=256, S=4, P=1024, B_r=4, seed=82), (1, 2, 4), 16, 16, 0.0, 0.0),
+    "c2_1x2x4_fp32": (configs.C2.with_(n_sY=256, n_sU=256, S=3, P=256, B_r=3, dtype="fp32", seed=83), (1, 2, 4), 16,
+                      16, 1.0, 0.0),
+    "c3_1x2_bf16": (configs.C3.with_(n_sY=64, n_sU=64, S=2, P=128, B_r=2, L=4, W_D=512, L_D=2, seed=84), (1, 2), 16,
+                    8, 0.0, 0.0),
+}
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _oracle(wl, hi, real, lam, f_const, chunk=None, prec=None):
+    b, h = hi.base, hi.hier
+    return oracle.train_step_hier(wl.gen_shape(), (real.shape[2], wl.L_D, wl.W_D), wl.d, b.pY[0], b.pU[0], hi.pD,
+                                  b.z[0], b.xc[0], b.xsY[0], b.xsU[0], np.full((wl.S, wl.P), f_const), h.idxY, h.idxU,
+                                  h.idxF, real, h.w, lambda_pde=lam, chunk_S=chunk, prec=prec)
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_hier_step(case):
+    wl, sides, m, nf, lam, fc = CASES[case]
+    _say(f"hier_step case={case} dtype={wl.dtype} sides={sides} W={wl.W} S={wl.S} P={wl.P}")
+    hi = make_hier_inputs(wl, sides=sides, m_sensors=m, n_free=nf)
+    real = oracle.real_snapshots_hier(wl, hi)
+    ref = _oracle(wl, hi, real, lam, fc)
+    out = run_hier_gpu(wl, hi, real, lam=lam, f_const=fc)
+    assert out["nonfinite"] == 0
+    errs = hier_errors(wl, out, ref, real.shape[2])
+    tol = TOL[wl.dtype]
+    if max(errs.values()) <= tol:
+        check(errs, tol, case)
+        return
+    model = _oracle(wl, hi, real, lam, fc, prec=wl.dtype)
+    check_conditioned(errs, hier_errors(wl, dict(gY=model["gY"], gU=model["gU"], gD=model["gD"],
+                                                 loss=np.stack([model["L_D"], model["L_adv"],
+                                                                np.full(len(model["L_D"]), model["L_pde"])], 1)),
+                                         ref, real.shape[2]), tol, case)
+
+
+def test_hier_chunking_matches_unchunked():
+    wl = configs.C2.with_(n_sY=256, n_sU=256, S=5, P=256, B_r=3, dtype="fp32", seed=85)
+    _say("hier_step chunk_S=2 vs unchunked, fp32")
+    hi = make_hier_inputs(wl, sides=(1, 2, 4), m_sensors=16, n_free=16)
+    real = oracle.real_snapshots_hier(wl, hi)
+    a = run_hier_gpu(wl, hi, real, lam=0.5)
+    b = run_hier_gpu(wl, hi, real, lam=0.5, chunk_S=2)
+    for k in ("gY", "gU", "gD", "loss"):
+        err = np.abs(a[k] - b[k]).max() / max(1e-30, np.abs(a[k]).max())
+        print(f"chunking {k}: {err:.3g}")
+        assert err <= 1e-5
+
+
+def test_hier_index_out_of_range_is_flagged():
+    """An index past the sensor count is read as zero and raises the
+    non-finite flag (the kernels bound every index before using it)."""
+    wl = TINY
+    _say("hier_step with one Y-sensor index out of range")
+    hi = make_hier_inputs(wl, sides=(1, 2), m_sensors=4, n_free=4)
+    real = oracle.real_snapshots_hier(wl, hi)
+    iY = hi.hier.idxY.copy()
+    iY[2, 1] = wl.n_sY            # one past the end
+    out = run_hier_gpu(wl, hi, real, idx=(iY, hi.hier.idxU, hi.hier.idxF))
+    assert out["nonfinite"] == 1
+    assert np.isfinite(out["gY"]).all() and np.isfinite(out["gD"]).all()
