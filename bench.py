@@ -36,6 +36,8 @@ def device_inputs(wl, dev):
     from paper_1910_13444_amd import pigan
     from paper_1910_13444_amd.inputs import make_inputs
 
+    if wl.arch == "hier":
+        return hier_inputs(wl, dev)
     inp = make_inputs(wl)
 
     def t(a):
@@ -59,6 +61,43 @@ def device_inputs(wl, dev):
     d["real"] = torch.cat([yY[:, 0], yU[:, 0]], dim=-1).contiguous()
     torch.cuda.synchronize()
     return d, inp
+
+
+def hier_inputs(wl, dev):
+    """Device inputs of a domain-decomposition step: the generator pair, the
+    stratified sensors and points, the critics' index lists and weights, and
+    real snapshots per critic (teacher pair at its sensors on the device,
+    f = 0 at its free sensors, their coordinates)."""
+    import numpy as np
+    import torch
+
+    from paper_1910_13444_amd import pigan
+    from paper_1910_13444_amd.inputs import make_hier_inputs
+
+    hi = make_hier_inputs(wl, sides=wl.sides, m_sensors=wl.m_sensors, n_free=wl.n_free)
+    b, h = hi.base, hi.hier
+
+    def t(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+
+    def ti(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+    d = dict(pY=t(b.pY[0]), pU=t(b.pU[0]), pD=t(hi.pD), z=t(b.z[0]), xc=t(b.xc[0]), xsY=t(b.xsY[0]),
+             xsU=t(b.xsU[0]), idxY=ti(h.idxY), idxU=ti(h.idxU), idxF=ti(h.idxF), w_disc=t(h.w))
+    shape = wl.gen_shape()
+    zt = t(b.z_teach)
+    yY = pigan.gen_forward(t(b.tY), shape, wl.d, zt, t(b.xsY), 0, dtype="fp32", x_shared=True)[0, 0]
+    yU = pigan.gen_forward(t(b.tU), shape, wl.d, zt, t(b.xsU), 0, dtype="fp32", x_shared=True)[0, 0]
+    xf = t(hi.xf_real)                                            # [B, P, 2]
+    Bn = yY.shape[0]
+    real = []
+    for k in range(h.D):
+        real.append(torch.cat([yY[:, d["idxY"][k].long()], yU[:, d["idxU"][k].long()],
+                               torch.zeros(Bn, h.idxF.shape[1], device=dev),
+                               xf[:, d["idxF"][k].long(), :].reshape(Bn, -1)], dim=1))
+    d["real"] = torch.stack(real).contiguous()
+    torch.cuda.synchronize()
+    return d, hi
 
 
 KERNEL_SOURCES = ("common.h", "gemm.hip", "pointwise.hip")
@@ -126,7 +165,10 @@ def measured_peaks(dev):
 
 def run_steps(step, d, wl, k):
     for _ in range(k):
-        if wl.arch == "trunk":
+        if wl.arch == "hier":
+            step(d["pY"], d["pU"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["idxY"], d["idxU"], d["idxF"],
+                 d["real"], d["w_disc"], f=None, f_const=wl.f_const)
+        elif wl.arch == "trunk":
             step(d["pT"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["real"], f=None, f_const=wl.f_const,
                  w_group=d["w_group"])
         else:
@@ -214,7 +256,12 @@ def main():
         import numpy as np
         eps = np.random.default_rng(wl.seed + 5).random((wl.G, min(wl.S, wl.B_r)), dtype=np.float32)
         d["gp_eps"] = torch.from_numpy(eps).to(dev)
-    if wl.arch == "trunk":
+    if wl.arch == "hier":
+        if a.lambda_gp > 0:
+            raise SystemExit("bench: the domain-decomposition step has no gradient penalty")
+        step = pigan.HierStep(pigan.hier_desc(wl, wl.n_critics, wl.m_sensors, wl.m_sensors, wl.n_free,
+                                              chunk_S=a.chunk_S, lambda_pde=wl.lambda_pde), device=dev)
+    elif wl.arch == "trunk":
         if a.lambda_gp > 0:
             raise SystemExit("bench: the shared-trunk step has no gradient penalty")
         step = pigan.TrunkStep(pigan.trunk_desc(wl, chunk_S=a.chunk_S), device=dev)
@@ -278,7 +325,8 @@ def main():
                 f"launches/step {v['launches_per_step']:.0f}")
 
     peaks = None if a.no_peaks else measured_peaks(dev)
-    cpu = None if a.no_cpu_baseline else cpu_baseline(wl)
+    # the oracle baseline covers the paired and shared-trunk steps
+    cpu = None if (a.no_cpu_baseline or wl.arch == "hier") else cpu_baseline(wl)
 
     out = {
         "metric": METRIC, "value": tflops, "unit": "TFLOP/s", "n_gpus": 1, "steps": a.steps,
@@ -287,6 +335,8 @@ def main():
         "config": {"workload": wl.name, "G": wl.G, "d": wl.d, "n_z": wl.n_z,
                    "gen": (f"shared trunk {wl.L}x{wl.W} tanh, residual blocks, 2 heads" if wl.arch == "trunk"
                            else f"{wl.L}x{wl.W} tanh"),
+                   "critics": (f"{wl.n_critics} subdomain critics, levels {list(wl.sides)}, "
+                               f"{wl.n_in_hier} inputs each" if wl.arch == "hier" else wl.G),
                    "disc": f"{wl.L_D}x{wl.W_D} tanh on {wl.n_in}", "S": wl.S, "P": wl.P,
                    "sensors": [wl.n_sY, wl.n_sU], "B_r": wl.B_r, "chunk_S": a.chunk_S, "lambda_gp": a.lambda_gp,
                    "collocation_points_per_step": pts, "alg_flops_per_step": F},

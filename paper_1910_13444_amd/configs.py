@@ -35,7 +35,19 @@ class Workload:
     f_const: float      # source term used when no f array is given
     lambda_pde: float = 1.0
     seed: int = 1910
-    arch: str = "pair"  # "pair": two tanh MLPs (Y, u); "trunk": one shared trunk, two heads
+    arch: str = "pair"  # "pair": two tanh MLPs (Y, u); "trunk": one shared trunk, two heads;
+                        # "hier": one pair and one critic per subdomain of a hierarchy
+    sides: tuple = ()   # hier: grid side of each level (coarsest first)
+    m_sensors: int = 0  # hier: Y (and u) sensors of every critic
+    n_free: int = 0     # hier: free sensors of every critic
+
+    @property
+    def n_critics(self) -> int:
+        return sum(k * k for k in self.sides) if self.arch == "hier" else self.G
+
+    @property
+    def n_in_hier(self) -> int:
+        return 2 * self.m_sensors + self.n_free * (1 + self.d)
 
     @property
     def n_in(self) -> int:
@@ -99,8 +111,16 @@ T5 = C2.with_(name="trunk5x128_darcy2d_bf16", L=5, arch="trunk", seed=1921)
 T11 = C3.with_(name="trunk11x512_sd1000_bf16", L=11, arch="trunk", seed=1922)
 T21 = C5.with_(name="trunk21x1024_bigstep_bf16", L=21, arch="trunk", seed=1923)
 
-WORKLOADS = {w.name: w for w in (C1, C2, C3, C4, C5, C5H, T5, T11, T21)}
-ALIASES = {"c1": C1, "c2": C2, "c3": C3, "c4": C4, "c5": C5, "c5h": C5H, "t5": T5, "t11": T11, "t21": T21}
+# Domain decomposition (Sec. III.B.1): the 2-D workload's generator pair and
+# samples, 1 + 4 + 16 subdomain critics (3 x 256 each) on the paper's snapshot
+# (16 Y + 16 u sensors, 16 free sensors with their coordinates), no residual
+# penalty (the source enters through the critics).
+H2 = C2.with_(name="hier21_darcy2d_bf16", n_sY=256, n_sU=256, lambda_pde=0.0, arch="hier", sides=(1, 2, 4),
+              m_sensors=16, n_free=16, seed=1931)
+
+WORKLOADS = {w.name: w for w in (C1, C2, C3, C4, C5, C5H, T5, T11, T21, H2)}
+ALIASES = {"c1": C1, "c2": C2, "c3": C3, "c4": C4, "c5": C5, "c5h": C5H, "t5": T5, "t11": T11, "t21": T21,
+           "h2": H2}
 
 
 def get(name: str) -> Workload:

@@ -11,6 +11,8 @@ the value stream only):
   backward  weight gradient and input cotangent of every hidden layer and the
             output layer (2x their forward), first-layer weight gradient
             (same count as its forward)
+Domain decomposition: one generator pair and n_critics critics on
+n_in = 2 m_sensors + n_free (1 + d) inputs each.
 Shared trunk (trunk_flops): one network on R = S*(n_sY + n_sU) + (1+2d)*S*P
 rows with a two-output head.
 Discriminator on R_D = S + B_r rows:
@@ -38,7 +40,8 @@ def disc_flops(wl: Workload, S: int | None = None, B_r: int | None = None) -> fl
     S = wl.S if S is None else S
     B_r = wl.B_r if B_r is None else B_r
     RD = S + B_r
-    W, L, n_in = wl.W_D, wl.L_D, wl.n_in
+    W, L = wl.W_D, wl.L_D
+    n_in = wl.n_in_hier if wl.arch == "hier" else wl.n_in
     fwd = 2.0 * RD * (n_in * W + (L - 1) * W * W + W)
     bwd = fwd + 2.0 * RD * ((L - 1) * W * W + W) + 2.0 * S * n_in * W
     return fwd + bwd
@@ -64,6 +67,8 @@ def step_flops(wl: Workload, S: int | None = None, B_r: int | None = None) -> fl
         gen = trunk_flops(wl, S)
     else:
         gen = gen_flops(wl, wl.c_Y, wl.n_sY, S) + gen_flops(wl, wl.c_U, wl.n_sU, S)
+    if wl.arch == "hier":   # one generator pair, one critic per subdomain
+        return gen + wl.n_critics * disc_flops(wl, S, B_r)
     return wl.G * (gen + disc_flops(wl, S, B_r))
 
 
