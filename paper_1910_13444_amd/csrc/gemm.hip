@@ -13,18 +13,22 @@
 //              g_a   = s g_h + sum_i s' a'_i g_h'_i + (s' a''_i + s'' a'_i^2) g_h''_i
 //              g_a'_i = s g_h'_i + 2 s' a'_i g_h''_i,   g_a''_i = s g_h''_i
 //   EPI_DF   reverse pass through the discriminator's first layer for the
-//            fake snapshots: writes -dL_D/dF into the generators' sensor-row
-//            cotangents (the adversarial generator loss is the negated
-//            critic term).
+//            fake snapshots: writes -dL_D/dF (the adversarial generator loss
+//            is the negated critic term) into the generators' sensor-row
+//            cotangents, or into a per-critic input-cotangent array.
+//   Residual blocks of a shared trunk add the skip activations (forward) and
+//   the skip cotangent (reverse) in the same epilogues.
 // k_gemm_dw  : dW = sum_rows dA^T H (split over rows, fp32 partials), plus
 //              the bias cotangent sum over the value rows.
 // The split partials are summed in fp64, in split order, by k_colsum.
 //
 // Tiles: a 64-lane wave owns 32 points x 32*NT columns for every stream; the
 // block is WM x WN waves.  The MFMA computes W . X^T so that a lane holds one
-// point and runs of four columns (vector stores, lane-local derivative carry).  Operands are staged through LDS in 64-byte k-slices
-// (80-byte row pitch, conflict-free 16-byte fragment reads) with the next
-// slice prefetched into registers while the current one is multiplied.
+// point and runs of four columns (vector stores, lane-local derivative
+// carry).  Operands are staged through LDS in 64-byte k-slices (swizzled
+// segments, conflict-free writes and fragment reads): wide layers load them
+// straight into a 3- or 4-deep LDS ring, the others prefetch the next slices
+// into registers while the current one is multiplied.
 #include "common.h"
 
 namespace pigan {
@@ -33,7 +37,8 @@ namespace pigan {
 // 16-byte segments of row r stored in the order s ^ ((r >> 2) & 3).  The
 // fragment reads (32 consecutive rows, one segment) and the stage writes (four
 // lanes per row) are then both free of bank conflicts (measured with the
-// LDS bank-conflict counter; an 80-byte padded pitch conflicted on the writes).
+// LDS bank-conflict counter; a padded pitch without the swizzle conflicted on
+// the writes).
 static constexpr int LDS_PITCH = 64;
 typedef uint32_t u32x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
