@@ -59,64 +59,77 @@ __device__ __forceinline__ void store8(T* p, const float* v) {
 // first layer: a = zp[s] + W1[:, :d] x ; a'_i = W1[:, i] ; a''_i = 0
 // one thread per (point, 8 columns)
 // ---------------------------------------------------------------------------
+// A thread keeps one group of 8 columns (and its x-part weights, loaded once)
+// and walks FF_PPB points of the block, PPI = 256 / (W / 8) at a time; stores
+// leave as full 16-byte pieces of consecutive columns.
+constexpr int FF_PPB = 32;
+
 template <class T, int ND1, int ND2>
 __global__ void __launch_bounds__(256)
 k_first_fwd(FirstArgs<T> p) {
   constexpr int C = 1 + ND1 + ND2;
   const int g = blockIdx.z;
   const int G8 = p.W / 8;
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= p.seg.n_points * G8) return;
-  const int64_t pt = idx / G8;
-  const int n0 = (int)(idx % G8) * 8;
-  const int64_t s = pt / p.Pn;
-  const int64_t xr = p.x_shared ? pt % p.Pn : pt;
-  const float* xv = p.x + g * p.x_g + xr * p.d;
-  float x[3] = {0.0f, 0.0f, 0.0f};
+  const int TPP = G8 < 256 ? G8 : 256;   // threads per point
+  const int PPI = 256 / TPP;             // points per iteration
+  const int cg0 = threadIdx.x % TPP;
+  const int64_t pbeg = (int64_t)blockIdx.x * FF_PPB;
+  int64_t pend = pbeg + FF_PPB;
+  if (pend > p.seg.n_points) pend = p.seg.n_points;
+  const int64_t pl = p.seg.plane * p.ldo;
+  for (int cg = cg0; cg < G8; cg += TPP) {
+    const int n0 = cg * 8;
+    const float* W1 = p.p1 + g * p.p_g + (int64_t)n0 * p.in_dim;
+    float wc[3][8];
 #pragma unroll
-  for (int i = 0; i < 3; ++i)
-    if (i < p.d) x[i] = xv[i];
-  const float* W1 = p.p1 + g * p.p_g + (int64_t)n0 * p.in_dim;
-  float a[8], wc[3][8];
-  load8<float>(p.zp + g * p.zp_g + s * p.W + n0, a);
+    for (int e = 0; e < 8; ++e)
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
+      for (int i = 0; i < 3; ++i) wc[i][e] = i < p.d ? W1[(int64_t)e * p.in_dim + i] : 0.0f;
+    for (int64_t pt = pbeg + threadIdx.x / TPP; pt < pend; pt += PPI) {
+      const int64_t s = pt / p.Pn;
+      const int64_t xr = p.x_shared ? pt % p.Pn : pt;
+      const float* xv = p.x + g * p.x_g + xr * p.d;
+      float x[3] = {0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int i = 0; i < 3; ++i) {
-      wc[i][e] = i < p.d ? W1[(int64_t)e * p.in_dim + i] : 0.0f;
-      a[e] += wc[i][e] * x[i];
+      for (int i = 0; i < 3; ++i)
+        if (i < p.d) x[i] = xv[i];
+      float a[8];
+      load8<float>(p.zp + g * p.zp_g + s * p.W + n0, a);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+#pragma unroll
+        for (int i = 0; i < 3; ++i) a[e] += wc[i][e] * x[i];
+      float h[C][8];
+      float s8[8], sp8[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float t, sd;
+        tanh_ts(a[e], t, sd);
+        h[0][e] = t;
+        s8[e] = sd;
+        sp8[e] = -2.0f * t * sd;
+      }
+#pragma unroll
+      for (int i = 0; i < ND1; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) h[1 + i][e] = s8[e] * wc[i][e];
+#pragma unroll
+      for (int i = 0; i < ND2; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) h[1 + ND1 + i][e] = sp8[e] * wc[i][e] * wc[i][e];
+      const int64_t base = g * p.o_g + (p.seg.row0 + pt) * p.ldo + n0;
+      if (p.out_a) {
+        store8<T>(p.out_a + base, a);
+#pragma unroll
+        for (int i = 0; i < ND1; ++i) store8<T>(p.out_a + base + (1 + i) * pl, wc[i]);
+        float z8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+        for (int i = 0; i < ND2; ++i) store8<T>(p.out_a + base + (1 + ND1 + i) * pl, z8);
+      }
+#pragma unroll
+      for (int k = 0; k < C; ++k) store8<T>(p.out_h + base + k * pl, h[k]);
     }
   }
-  float h[C][8];
-  float s8[8], sp8[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    float t, sd;
-    tanh_ts(a[e], t, sd);
-    h[0][e] = t;
-    s8[e] = sd;
-    sp8[e] = -2.0f * t * sd;
-  }
-#pragma unroll
-  for (int i = 0; i < ND1; ++i)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) h[1 + i][e] = s8[e] * wc[i][e];
-#pragma unroll
-  for (int i = 0; i < ND2; ++i)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) h[1 + ND1 + i][e] = sp8[e] * wc[i][e] * wc[i][e];
-  const int64_t base = g * p.o_g + (p.seg.row0 + pt) * p.ldo + n0;
-  const int64_t pl = p.seg.plane * p.ldo;
-  if (p.out_a) {
-    store8<T>(p.out_a + base, a);
-#pragma unroll
-    for (int i = 0; i < ND1; ++i) store8<T>(p.out_a + base + (1 + i) * pl, wc[i]);
-    float z8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-    for (int i = 0; i < ND2; ++i) store8<T>(p.out_a + base + (1 + ND1 + i) * pl, z8);
-  }
-#pragma unroll
-  for (int k = 0; k < C; ++k) store8<T>(p.out_h + base + k * pl, h[k]);
 }
 
 // ---------------------------------------------------------------------------
@@ -916,7 +929,7 @@ hipError_t launch_zproj(const float* p1, int64_t p_g, int in_dim, int d, int W, 
 template <class T>
 hipError_t launch_first_fwd(int nd1, int nd2, const FirstArgs<T>& a, int G, hipStream_t st) {
   if (a.seg.n_points <= 0) return hipSuccess;
-  dim3 grid(nblk(a.seg.n_points * (a.W / 8), 256), 1, G);
+  dim3 grid(nblk(a.seg.n_points, FF_PPB), 1, G);
   switch (nd1 * 10 + nd2) {
     case 0: k_first_fwd<T, 0, 0><<<grid, 256, 0, st>>>(a); break;
     case 10: k_first_fwd<T, 1, 0><<<grid, 256, 0, st>>>(a); break;
