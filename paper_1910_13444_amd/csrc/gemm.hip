@@ -1554,13 +1554,14 @@ hipError_t launch_gemm_nt(int epi, int nd1, int nd2, const NtArgs<T>& a, int G, 
 void dw_split_plan(int64_t R, int N, int J, int elem_bytes, int G, int* n_split, int64_t* rows_per_split) {
   const int SR = 64 / elem_bytes;
   // 16-bit storage, both sides >= 512: 256 x 256 tiles of 16 waves, about
-  // 512 blocks; otherwise about 1024 blocks of the 128 x 128 (or smaller)
-  // tile grid, and 512 for a single output tile (each split writes a whole
-  // N x J fp32 partial, and one resident wave of blocks suffices)
+  // 256 blocks (one per CU; as fast as 512 and half the partials to write and
+  // reduce); otherwise about 1024 blocks of the 128 x 128 (or smaller) tile
+  // grid, and 512 for a single output tile (each split writes a whole N x J
+  // fp32 partial, and one resident wave of blocks suffices)
   const bool big = elem_bytes == 2 && N >= 512 && J >= 512;
   const int bt = big ? 256 : (N >= 128 && J >= 128) ? 128 : ((N >= 64 && J >= 64) ? 64 : 32);
   const int64_t tiles = (int64_t)((N + bt - 1) / bt) * ((J + bt - 1) / bt) * G;
-  const int64_t target = big || tiles == 1 ? 512 : 1024;
+  const int64_t target = big ? 256 : (tiles == 1 ? 512 : 1024);
   int64_t want = (target + tiles - 1) / tiles;
   const int64_t stages = (R + SR - 1) / SR;
   int64_t max_split = stages / 4 > 0 ? stages / 4 : 1;

@@ -698,34 +698,55 @@ __global__ void k_hier_pde_loss(const double* __restrict__ acc, int slot, float 
 // eight group sums are added in group order.  Column col maps to
 // dst[(col / Jp) * J + col % Jp] and is skipped when col % Jp >= J (padding).
 // ---------------------------------------------------------------------------
-template <class Tin>
+// VEC consecutive columns per lane (VEC = 4: one 16-byte load per slot, 512
+// contiguous bytes per slot group); the per-column summation order is the
+// same for every VEC.
+template <class Tin, int VEC>
 __global__ void __launch_bounds__(256)
 k_colsum(const Tin* __restrict__ part, int64_t p_g, int n_slots, int64_t slot_stride, int64_t ncols, int Jp, int J,
          float* dst, int64_t d_g, int accumulate, float scale, int32_t* nonfinite) {
-  __shared__ double red[8][32];
+  __shared__ double red[8][32 * VEC];
   const int g = blockIdx.z;
   const int lane = threadIdx.x & 31, grp = threadIdx.x >> 5;
-  const int64_t col = (int64_t)blockIdx.x * 32 + lane;
-  double s = 0.0;
-  if (col < ncols) {
-    const Tin* src = part + g * p_g + col;
-#pragma unroll 8
-    for (int q = grp; q < n_slots; q += 8) s += (double)src[(int64_t)q * slot_stride];
-  }
-  red[grp][lane] = s;
-  __syncthreads();
-  if (grp == 0 && col < ncols) {
-    double v = 0.0;
+  const int64_t col0 = ((int64_t)blockIdx.x * 32 + lane) * VEC;
+  double s[VEC];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) v += red[q][lane];
-    const int64_t n = col / Jp;
-    const int j = (int)(col % Jp);
-    if (j < J) {
-      float* o = dst + g * d_g + n * J + j;
-      float r = (float)(v * (double)scale);
-      if (accumulate) r += *o;
-      *o = r;
-      if (!__builtin_isfinite(r)) *nonfinite = 1;
+  for (int e = 0; e < VEC; ++e) s[e] = 0.0;
+  if (col0 < ncols) {
+    const Tin* src = part + g * p_g + col0;
+    if constexpr (VEC == 4) {
+#pragma unroll 4
+      for (int q = grp; q < n_slots; q += 8) {
+        const float4 v = *(const float4*)(src + (int64_t)q * slot_stride);
+        s[0] += (double)v.x;
+        s[1] += (double)v.y;
+        s[2] += (double)v.z;
+        s[3] += (double)v.w;
+      }
+    } else {
+#pragma unroll 8
+      for (int q = grp; q < n_slots; q += 8) s[0] += (double)src[(int64_t)q * slot_stride];
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) red[grp][lane * VEC + e] = s[e];
+  __syncthreads();
+  if (grp == 0 && col0 < ncols) {
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      const int64_t col = col0 + e;
+      double v = 0.0;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v += red[q][lane * VEC + e];
+      const int64_t n = col / Jp;
+      const int j = (int)(col % Jp);
+      if (j < J) {
+        float* o = dst + g * d_g + n * J + j;
+        float r = (float)(v * (double)scale);
+        if (accumulate) r += *o;
+        *o = r;
+        if (!__builtin_isfinite(r)) *nonfinite = 1;
+      }
     }
   }
 }
@@ -1095,8 +1116,19 @@ hipError_t launch_colsum(const Tin* part, int64_t p_g, int n_slots, int64_t slot
                          float* dst, int64_t d_g, int accumulate, float scale, int32_t* nonfinite, int G,
                          hipStream_t st) {
   if (ncols <= 0) return hipSuccess;
-  k_colsum<Tin><<<dim3(nblk(ncols, 32), 1, G), 256, 0, st>>>(part, p_g, n_slots, slot_stride, ncols, Jp, J, dst, d_g,
-                                                            accumulate, scale, nonfinite);
+  // four columns per lane where every slot row and group slab is 16-byte
+  // aligned and whole (the workspace is 256-byte aligned)
+  if constexpr (sizeof(Tin) == 4) {
+    if (ncols % 4 == 0 && slot_stride % 4 == 0 && p_g % 4 == 0 && ((uintptr_t)part & 15) == 0) {
+      k_colsum<Tin, 4><<<dim3(nblk(ncols, 128), 1, G), 256, 0, st>>>(part, p_g, n_slots, slot_stride, ncols, Jp, J,
+                                                                    dst, d_g, accumulate, scale, nonfinite);
+      return hipGetLastError();
+    }
+  }
+  {
+    k_colsum<Tin, 1><<<dim3(nblk(ncols, 32), 1, G), 256, 0, st>>>(part, p_g, n_slots, slot_stride, ncols, Jp, J, dst,
+                                                                  d_g, accumulate, scale, nonfinite);
+  }
   return hipGetLastError();
 }
 template hipError_t launch_colsum<float>(const float*, int64_t, int, int64_t, int64_t, int, int, float*, int64_t, int,
