@@ -157,9 +157,13 @@ static int first_bwd_chunks(int S) {
   return c < 1 ? 1 : (c > 64 ? 64 : c);
 }
 
-// points per block of the output-layer reverse pass
-static int64_t ob_ppb(int64_t n_points) {
-  int64_t p = (n_points + 511) / 512;
+// points per block of the output-layer reverse pass: about 2048 blocks for
+// widths >= 512 (a block then covers only one or two points per pass over
+// its threads; eight blocks per CU keep enough loads in flight), 512 below
+// (a block covers 16 points per pass; more blocks only add partials)
+static int64_t ob_ppb(int64_t n_points, int W) {
+  const int64_t blocks = W >= 512 ? 2048 : 512;
+  int64_t p = (n_points + blocks - 1) / blocks;
   return p < 8 ? 8 : p;
 }
 
@@ -243,8 +247,8 @@ static void plan_net(Carver& cv, NetBuf& nb, const pigan_mlp& m, int d, int nd2,
   nb.wcT = cv.take(wsz);
   nb.nrc = first_bwd_chunks(Sc);
   nb.fb = cv.take((size_t)Sc * nb.nrc * 7 * W * 4 * G);
-  nb.ppb_sen = ob_ppb(nb.n_sen);
-  nb.ppb_col = ob_ppb(nb.n_col);
+  nb.ppb_sen = ob_ppb(nb.n_sen, W);
+  nb.ppb_col = ob_ppb(nb.n_col, W);
   nb.ob_slots = out_bwd_blocks(nb.n_sen, (int)nb.ppb_sen) + out_bwd_blocks(nb.n_col, (int)nb.ppb_col);
   nb.ob = cv.take((size_t)nb.ob_slots * nb.heads * (W + 1) * 8 * G);
   if (trunk) {
@@ -290,7 +294,7 @@ static void plan_step(const pigan_step_desc* s, int Sc, StepPlan& pl, bool trunk
   const size_t wsz = (size_t)std::max(LD - 1, 1) * WD * WD * pl.es * G;
   D.wc = cv.take(wsz);
   D.wcT = cv.take(wsz);
-  D.ppb = ob_ppb(D.Bmax);
+  D.ppb = ob_ppb(D.Bmax, WD);
   D.ob_slots = out_bwd_blocks(D.Bmax, (int)D.ppb);
   D.ob = cv.take((size_t)D.ob_slots * (WD + 1) * 8 * G);
   // split-K partials: the largest of all weight-gradient launches
@@ -352,7 +356,7 @@ static void plan_hier(const pigan_step_desc* s, int Sc, StepPlan& pl) {
   const size_t wsz = (size_t)std::max(LD - 1, 1) * WD * WD * pl.es * GD;
   D.wc = cv.take(wsz);
   D.wcT = cv.take(wsz);
-  D.ppb = ob_ppb(D.Bmax);
+  D.ppb = ob_ppb(D.Bmax, WD);
   D.ob_slots = out_bwd_blocks(D.Bmax, (int)D.ppb);
   D.ob = cv.take((size_t)D.ob_slots * (WD + 1) * 8 * GD);
   int64_t mx = 0, mxb = 0;
