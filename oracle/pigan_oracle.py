@@ -877,7 +877,7 @@ def real_snapshots_trunk(wl, inp):
 
 
 def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, idxU, idxF, real, w,
-                    lambda_pde=0.0, chunk_S=None, prec=None):
+                    lambda_pde=0.0, chunk_S=None, prec=None, trunk=False):
     """Domain decomposition (Sec. III.B.1): one generator pair, one critic per
     subdomain of every level.  Critic k sees the paper's snapshot of its
     subdomain: [Y at Y sensors idxY[k] | u at u sensors idxU[k] | the
@@ -887,6 +887,9 @@ def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, id
     Weights w[k] = 1 / (levels * subdomains of the level).  Losses per critic:
     L_D[k] = w_k (mean D_k(fake) - mean D_k(real)), L_adv[k] = -w_k mean D_k(fake);
     the generator loss is sum_k L_adv[k] + L_pde with L_pde = lambda mean r^2.
+    With trunk=True the generator is the shared trunk pY (pU unused): its Y
+    head at the Y sensors, its u head at the u sensors, both heads' jets at the
+    collocation points; gY is then the trunk's gradient and gU is empty.
     Returns dict(L_D [D], L_adv [D], L_pde, gY, gU, gD [D, nD])."""
     z = np.asarray(z, F64)
     xc = np.asarray(xc, F64)
@@ -897,10 +900,10 @@ def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, id
     if prec == "fp32":
         with _working_type(np.float32):
             return train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, idxU, idxF, real, w,
-                                   lambda_pde=lambda_pde, chunk_S=chunk_S, prec=None)
+                                   lambda_pde=lambda_pde, chunk_S=chunk_S, prec=None, trunk=trunk)
     num = _Num(prec)
     gY = np.zeros(np.asarray(pY).size, F64)
-    gU = np.zeros(np.asarray(pU).size, F64)
+    gU = np.zeros(0 if trunk else np.asarray(pU).size, F64)
     gD = np.zeros((D, np.asarray(pDs[0]).size), F64)
     sum_DF = np.zeros(D)
     sum_DR = np.zeros(D)
@@ -918,13 +921,22 @@ def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, id
         Sc = zc.shape[0]
         XY, ZY = sensor_rows(xsY, zc)
         XU, ZU = sensor_rows(xsU, zc)
-        fY_s = gen_forward(pY, gshape, d, XY, ZY, 0, keep=True, prec=num)
-        fU_s = gen_forward(pU, gshape, d, XU, ZU, 0, keep=True, prec=num)
-        Ys = fY_s["y"].reshape(Sc, nYs)
-        Us = fU_s["y"].reshape(Sc, nUs)
         XC, ZC = colloc_rows(xc[sl], zc)
-        jY = gen_forward(pY, gshape, d, XC, ZC, 1, keep=True, prec=num)
-        jU = gen_forward(pU, gshape, d, XC, ZC, 2, keep=True, prec=num)
+        if trunk:
+            fY_s = trunk_forward(pY, gshape, d, XY, ZY, 0, keep=True, prec=num)
+            fU_s = trunk_forward(pY, gshape, d, XU, ZU, 0, keep=True, prec=num)
+            Ys = fY_s["Y"].reshape(Sc, nYs)
+            Us = fU_s["u"].reshape(Sc, nUs)
+            jc = trunk_forward(pY, gshape, d, XC, ZC, 2, keep=True, prec=num)
+            jY = dict(y=jc["Y"], dy=jc["dY"])
+            jU = dict(y=jc["u"], dy=jc["du"], ddy=jc["ddu"])
+        else:
+            fY_s = gen_forward(pY, gshape, d, XY, ZY, 0, keep=True, prec=num)
+            fU_s = gen_forward(pU, gshape, d, XU, ZU, 0, keep=True, prec=num)
+            Ys = fY_s["y"].reshape(Sc, nYs)
+            Us = fU_s["y"].reshape(Sc, nUs)
+            jY = gen_forward(pY, gshape, d, XC, ZC, 1, keep=True, prec=num)
+            jU = gen_forward(pU, gshape, d, XC, ZC, 2, keep=True, prec=num)
         fc = f[sl].reshape(-1)
         r = darcy_residual(jY["y"], jY["dy"], jU["dy"], jU["ddy"], fc)
         sum_r2 += float((r * r).sum())
@@ -952,23 +964,31 @@ def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, id
         g_Ydy = np.stack([-q * eY * jU["dy"][i] for i in range(d)])
         g_Udy = np.stack([-q * eY * jY["dy"][i] for i in range(d)])
         g_Uddy = np.stack([-q * eY for _ in range(d)])
-        gY += gen_backward(pY, gshape, d, XY, ZY, fY_s, gYs.reshape(-1), prec=num)
-        gU += gen_backward(pU, gshape, d, XU, ZU, fU_s, gUs.reshape(-1), prec=num)
-        gY += gen_backward(pY, gshape, d, XC, ZC, jY, g_Yval, g_Ydy, prec=num)
-        gU += gen_backward(pU, gshape, d, XC, ZC, jU, np.zeros_like(r), g_Udy, g_Uddy, prec=num)
+        if trunk:
+            gY += trunk_backward(pY, gshape, d, XY, ZY, fY_s, gY=gYs.reshape(-1), prec=num)
+            gY += trunk_backward(pY, gshape, d, XU, ZU, fU_s, gu=gUs.reshape(-1), prec=num)
+            gY += trunk_backward(pY, gshape, d, XC, ZC, jc, gY=g_Yval, gdY=g_Ydy, gdu=g_Udy, gddu=g_Uddy, prec=num)
+        else:
+            gY += gen_backward(pY, gshape, d, XY, ZY, fY_s, gYs.reshape(-1), prec=num)
+            gU += gen_backward(pU, gshape, d, XU, ZU, fU_s, gUs.reshape(-1), prec=num)
+            gY += gen_backward(pY, gshape, d, XC, ZC, jY, g_Yval, g_Ydy, prec=num)
+            gU += gen_backward(pU, gshape, d, XC, ZC, jU, np.zeros_like(r), g_Udy, g_Uddy, prec=num)
     w = np.asarray(w, F64)
     return dict(L_D=w * (sum_DF / S - sum_DR / B), L_adv=-w * sum_DF / S, L_pde=lambda_pde * sum_r2 / (S * P),
                 gY=gY, gU=gU, gD=gD)
 
 
-def real_snapshots_hier(wl, hin, lambda_unused=None):
+def real_snapshots_hier(wl, hin, trunk_teacher=None):
     """Real snapshots [D, B_r, n_in] of a hierarchical step: the teacher pair
     at each critic's Y and u sensors, f = 0 at its free sensors (the true field
     satisfies the equation with the paper's zero source), and the coordinates
     of the real realisations' free sensors (hin.xf_real)."""
     b = hin.base
     gshape = (wl.d + wl.n_z, wl.L, wl.W)
-    Y = snapshots(b.tY[0], b.tU[0], gshape, wl.d, b.xsY[0], b.xsU[0], b.z_teach[0])
+    if trunk_teacher is not None:
+        Y = trunk_snapshots(trunk_teacher, gshape, wl.d, b.xsY[0], b.xsU[0], b.z_teach[0])
+    else:
+        Y = snapshots(b.tY[0], b.tU[0], gshape, wl.d, b.xsY[0], b.xsU[0], b.z_teach[0])
     nY = b.xsY.shape[1]
     Yv, Uv = Y[:, :nY], Y[:, nY:]
     B = Y.shape[0]

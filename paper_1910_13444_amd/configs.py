@@ -36,14 +36,23 @@ class Workload:
     lambda_pde: float = 1.0
     seed: int = 1910
     arch: str = "pair"  # "pair": two tanh MLPs (Y, u); "trunk": one shared trunk, two heads;
-                        # "hier": one pair and one critic per subdomain of a hierarchy
+                        # "hier": one pair and one critic per subdomain of a hierarchy;
+                        # "hier_trunk": the shared trunk and one critic per subdomain
     sides: tuple = ()   # hier: grid side of each level (coarsest first)
     m_sensors: int = 0  # hier: Y (and u) sensors of every critic
     n_free: int = 0     # hier: free sensors of every critic
 
     @property
     def n_critics(self) -> int:
-        return sum(k * k for k in self.sides) if self.arch == "hier" else self.G
+        return sum(k * k for k in self.sides) if self.is_hier else self.G
+
+    @property
+    def is_hier(self) -> bool:
+        return self.arch in ("hier", "hier_trunk")
+
+    @property
+    def trunk_gen(self) -> bool:
+        return self.arch in ("trunk", "hier_trunk")
 
     @property
     def n_in_hier(self) -> int:
@@ -118,9 +127,13 @@ T21 = C5.with_(name="trunk21x1024_bigstep_bf16", L=21, arch="trunk", seed=1923)
 H2 = C2.with_(name="hier21_darcy2d_bf16", n_sY=256, n_sU=256, lambda_pde=0.0, arch="hier", sides=(1, 2, 4),
               m_sensors=16, n_free=16, seed=1931)
 
-WORKLOADS = {w.name: w for w in (C1, C2, C3, C4, C5, C5H, T5, T11, T21, H2)}
+# The paper's full method on the 2-D workload: the shared 5 x 128 trunk and
+# the same 1 + 4 + 16 subdomain critics.
+HT5 = H2.with_(name="hier21_trunk5x128_darcy2d_bf16", L=5, arch="hier_trunk", seed=1932)
+
+WORKLOADS = {w.name: w for w in (C1, C2, C3, C4, C5, C5H, T5, T11, T21, H2, HT5)}
 ALIASES = {"c1": C1, "c2": C2, "c3": C3, "c4": C4, "c5": C5, "c5h": C5H, "t5": T5, "t11": T11, "t21": T21,
-           "h2": H2}
+           "h2": H2, "ht5": HT5}
 
 
 def get(name: str) -> Workload:

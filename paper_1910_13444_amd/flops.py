@@ -41,7 +41,7 @@ def disc_flops(wl: Workload, S: int | None = None, B_r: int | None = None) -> fl
     B_r = wl.B_r if B_r is None else B_r
     RD = S + B_r
     W, L = wl.W_D, wl.L_D
-    n_in = wl.n_in_hier if wl.arch == "hier" else wl.n_in
+    n_in = wl.n_in_hier if wl.is_hier else wl.n_in
     fwd = 2.0 * RD * (n_in * W + (L - 1) * W * W + W)
     bwd = fwd + 2.0 * RD * ((L - 1) * W * W + W) + 2.0 * S * n_in * W
     return fwd + bwd
@@ -63,11 +63,11 @@ def trunk_flops(wl: Workload, S: int | None = None) -> float:
 
 def step_flops(wl: Workload, S: int | None = None, B_r: int | None = None) -> float:
     """Algorithmic FLOPs of one training step over all groups."""
-    if wl.arch == "trunk":
+    if wl.trunk_gen:
         gen = trunk_flops(wl, S)
     else:
         gen = gen_flops(wl, wl.c_Y, wl.n_sY, S) + gen_flops(wl, wl.c_U, wl.n_sU, S)
-    if wl.arch == "hier":   # one generator pair, one critic per subdomain
+    if wl.is_hier:   # one generator, one critic per subdomain
         return gen + wl.n_critics * disc_flops(wl, S, B_r)
     return wl.G * (gen + disc_flops(wl, S, B_r))
 

@@ -190,8 +190,9 @@ class HierInputs:
 
 def make_hier_inputs(wl: Workload, sides=(1, 2, 4), m_sensors: int = 16, n_free: int = 16,
                      seed: int | None = None, S: int | None = None, B_r: int | None = None) -> HierInputs:
-    """Inputs of a hierarchical step (2-D): the workload's generator pair and
-    sample counts; sensors and collocation points stratified over the finest
+    """Inputs of a hierarchical step (2-D): the workload's generator pair (or,
+    for arch "hier_trunk", a shared trunk in base.pT / base.tT) and sample
+    counts; sensors and collocation points stratified over the finest
     cells (n_sY, n_sU and P must be multiples of the cell count); one
     Glorot-normal critic per subdomain on n_in = 2 m_sensors + n_free (1 + d)."""
     if wl.d != 2:
@@ -201,7 +202,7 @@ def make_hier_inputs(wl: Workload, sides=(1, 2, 4), m_sensors: int = 16, n_free:
     if wl.n_sY % cells or wl.n_sU % cells or wl.P % cells:
         raise ValueError("n_sY, n_sU and P must be multiples of the finest cell count")
     seed = wl.seed if seed is None else seed
-    base = make_inputs(wl, seed=seed, S=S, B_r=B_r)
+    base = make_inputs(wl.with_(arch="trunk" if wl.trunk_gen else "pair"), seed=seed, S=S, B_r=B_r)
     r = np.random.default_rng(np.random.SeedSequence(seed).spawn(len(_ROLES) + 2)[-1])
     Sn, G = base.z.shape[1], base.z.shape[0]
     base.xsY = stratified_points(r, (G,), fine, wl.n_sY // cells)

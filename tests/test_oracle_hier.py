@@ -119,3 +119,50 @@ def test_hier_chunking():
     b = _run(wl, hi, real, chunk=1)
     for k in ("L_D", "L_adv", "gY", "gU", "gD"):
         assert np.allclose(a[k], b[k], rtol=1e-12, atol=1e-15)
+
+
+def _trunk_setup():
+    wl = WL.with_(arch="hier_trunk", L=3, W=4)
+    hi = make_hier_inputs(wl, sides=(1, 2), m_sensors=4, n_free=4)
+    real = oracle.real_snapshots_hier(wl, hi, trunk_teacher=hi.base.tT[0])
+    return wl, hi, real
+
+
+def _run_trunk(wl, hi, real, pT=None, pDs=None, lam=0.5, idx=None, w=None):
+    b, h = hi.base, hi.hier
+    iY, iU, iF = idx if idx is not None else (h.idxY, h.idxU, h.idxF)
+    return oracle.train_step_hier(wl.gen_shape(), (real.shape[2], wl.L_D, wl.W_D), wl.d,
+                                  b.pT[0] if pT is None else pT, None, hi.pD if pDs is None else pDs, b.z[0],
+                                  b.xc[0], b.xsY[0], b.xsU[0], np.full((wl.S, wl.P), 0.3), iY, iU, iF, real,
+                                  h.w if w is None else w, lambda_pde=lam, trunk=True)
+
+
+def test_trunk_hier_one_critic_is_the_trunk_step():
+    wl, hi, _ = _trunk_setup()
+    b = hi.base
+    real = oracle.real_snapshots_trunk(wl, b)[0]
+    pD = glorot_mlp(np.random.default_rng(2), wl.n_sY + wl.n_sU, wl.L_D, wl.W_D).astype(np.float64)
+    idx = (np.arange(wl.n_sY)[None], np.arange(wl.n_sU)[None], np.zeros((1, 0), np.int64))
+    o = _run_trunk(wl, hi, real[None], pDs=pD[None], idx=idx, w=np.array([0.6]), lam=0.9)
+    ref = oracle.train_step_group_trunk(wl.gen_shape(), wl.disc_shape(), wl.d, b.pT[0], pD, b.z[0], b.xc[0],
+                                        b.xsY[0], b.xsU[0], np.full((wl.S, wl.P), 0.3), real, w=0.6,
+                                        lambda_pde=0.9 / 0.6)
+    assert np.isclose(o["L_D"][0], ref["L_D"], rtol=1e-13)
+    assert np.allclose(o["gY"], ref["gT"], rtol=1e-12, atol=1e-15)
+    assert np.allclose(o["gD"][0], ref["gD"], rtol=1e-12, atol=1e-15)
+
+
+def test_trunk_hier_grads_fd():
+    wl, hi, real = _trunk_setup()
+    o = _run_trunk(wl, hi, real)
+    p0 = hi.base.pT[0].astype(np.float64)
+    h = 1e-6
+    fd = np.zeros_like(p0)
+    for k in range(p0.size):
+        e = np.zeros_like(p0)
+        e[k] = h
+        a = _run_trunk(wl, hi, real, pT=p0 + e)
+        b = _run_trunk(wl, hi, real, pT=p0 - e)
+        fd[k] = ((a["L_adv"].sum() + a["L_pde"]) - (b["L_adv"].sum() + b["L_pde"])) / (2 * h)
+    assert np.abs(o["gY"] - fd).max() <= 1e-6 * max(1.0, np.abs(fd).max())
+    assert np.abs(o["gY"]).max() > 1e-4
