@@ -36,7 +36,7 @@ def device_inputs(wl, dev):
     from paper_1910_13444_amd import pigan
     from paper_1910_13444_amd.inputs import make_inputs
 
-    if wl.arch == "hier":
+    if wl.is_hier:
         return hier_inputs(wl, dev)
     inp = make_inputs(wl)
 
@@ -64,15 +64,15 @@ def device_inputs(wl, dev):
 
 
 def hier_inputs(wl, dev):
-    """Device inputs of a domain-decomposition step: the generator pair, the
-    stratified sensors and points, the critics' index lists and weights, and
-    real snapshots per critic (teacher pair at its sensors on the device,
-    f = 0 at its free sensors, their coordinates)."""
+    """Device inputs of a domain-decomposition step: the generator (pair or
+    shared trunk), the stratified sensors and points, the critics' index lists
+    and weights, and real snapshots per critic (a teacher pair at its sensors
+    on the device, f = 0 at its free sensors, their coordinates)."""
     import numpy as np
     import torch
 
     from paper_1910_13444_amd import pigan
-    from paper_1910_13444_amd.inputs import make_hier_inputs
+    from paper_1910_13444_amd.inputs import make_hier_inputs, make_inputs
 
     hi = make_hier_inputs(wl, sides=wl.sides, m_sensors=wl.m_sensors, n_free=wl.n_free)
     b, h = hi.base, hi.hier
@@ -82,12 +82,19 @@ def hier_inputs(wl, dev):
 
     def ti(a):
         return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
-    d = dict(pY=t(b.pY[0]), pU=t(b.pU[0]), pD=t(hi.pD), z=t(b.z[0]), xc=t(b.xc[0]), xsY=t(b.xsY[0]),
+    d = dict(pD=t(hi.pD), z=t(b.z[0]), xc=t(b.xc[0]), xsY=t(b.xsY[0]),
              xsU=t(b.xsU[0]), idxY=ti(h.idxY), idxU=ti(h.idxU), idxF=ti(h.idxF), w_disc=t(h.w))
+    if wl.trunk_gen:
+        d["pT"] = t(b.pT[0])
+        teach = make_inputs(wl.with_(arch="pair"))   # same teacher noise, plain teacher pair
+        tY, tU = teach.tY, teach.tU
+    else:
+        d["pY"], d["pU"] = t(b.pY[0]), t(b.pU[0])
+        tY, tU = b.tY, b.tU
     shape = wl.gen_shape()
     zt = t(b.z_teach)
-    yY = pigan.gen_forward(t(b.tY), shape, wl.d, zt, t(b.xsY), 0, dtype="fp32", x_shared=True)[0, 0]
-    yU = pigan.gen_forward(t(b.tU), shape, wl.d, zt, t(b.xsU), 0, dtype="fp32", x_shared=True)[0, 0]
+    yY = pigan.gen_forward(t(tY), shape, wl.d, zt, t(b.xsY), 0, dtype="fp32", x_shared=True)[0, 0]
+    yU = pigan.gen_forward(t(tU), shape, wl.d, zt, t(b.xsU), 0, dtype="fp32", x_shared=True)[0, 0]
     xf = t(hi.xf_real)                                            # [B, P, 2]
     Bn = yY.shape[0]
     real = []
@@ -165,7 +172,10 @@ def measured_peaks(dev):
 
 def run_steps(step, d, wl, k):
     for _ in range(k):
-        if wl.arch == "hier":
+        if wl.arch == "hier_trunk":
+            step(d["pT"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["idxY"], d["idxU"], d["idxF"],
+                 d["real"], d["w_disc"], f=None, f_const=wl.f_const)
+        elif wl.arch == "hier":
             step(d["pY"], d["pU"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["idxY"], d["idxU"], d["idxF"],
                  d["real"], d["w_disc"], f=None, f_const=wl.f_const)
         elif wl.arch == "trunk":
@@ -256,11 +266,15 @@ def main():
         import numpy as np
         eps = np.random.default_rng(wl.seed + 5).random((wl.G, min(wl.S, wl.B_r)), dtype=np.float32)
         d["gp_eps"] = torch.from_numpy(eps).to(dev)
-    if wl.arch == "hier":
+    if wl.is_hier:
         if a.lambda_gp > 0:
             raise SystemExit("bench: the domain-decomposition step has no gradient penalty")
-        step = pigan.HierStep(pigan.hier_desc(wl, wl.n_critics, wl.m_sensors, wl.m_sensors, wl.n_free,
-                                              chunk_S=a.chunk_S, lambda_pde=wl.lambda_pde), device=dev)
+        if wl.trunk_gen:
+            step = pigan.HierTrunkStep(pigan.hier_trunk_desc(wl, wl.n_critics, wl.m_sensors, wl.m_sensors, wl.n_free,
+                                                             chunk_S=a.chunk_S, lambda_pde=wl.lambda_pde), device=dev)
+        else:
+            step = pigan.HierStep(pigan.hier_desc(wl, wl.n_critics, wl.m_sensors, wl.m_sensors, wl.n_free,
+                                                  chunk_S=a.chunk_S, lambda_pde=wl.lambda_pde), device=dev)
     elif wl.arch == "trunk":
         if a.lambda_gp > 0:
             raise SystemExit("bench: the shared-trunk step has no gradient penalty")
@@ -326,17 +340,17 @@ def main():
 
     peaks = None if a.no_peaks else measured_peaks(dev)
     # the oracle baseline covers the paired and shared-trunk steps
-    cpu = None if (a.no_cpu_baseline or wl.arch == "hier") else cpu_baseline(wl)
+    cpu = None if (a.no_cpu_baseline or wl.is_hier) else cpu_baseline(wl)
 
     out = {
         "metric": METRIC, "value": tflops, "unit": "TFLOP/s", "n_gpus": 1, "steps": a.steps,
         "warmup": a.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
         "config": {"workload": wl.name, "G": wl.G, "d": wl.d, "n_z": wl.n_z,
-                   "gen": (f"shared trunk {wl.L}x{wl.W} tanh, residual blocks, 2 heads" if wl.arch == "trunk"
+                   "gen": (f"shared trunk {wl.L}x{wl.W} tanh, residual blocks, 2 heads" if wl.trunk_gen
                            else f"{wl.L}x{wl.W} tanh"),
                    "critics": (f"{wl.n_critics} subdomain critics, levels {list(wl.sides)}, "
-                               f"{wl.n_in_hier} inputs each" if wl.arch == "hier" else wl.G),
+                               f"{wl.n_in_hier} inputs each" if wl.is_hier else wl.G),
                    "disc": f"{wl.L_D}x{wl.W_D} tanh on {wl.n_in}", "S": wl.S, "P": wl.P,
                    "sensors": [wl.n_sY, wl.n_sU], "B_r": wl.B_r, "chunk_S": a.chunk_S, "lambda_gp": a.lambda_gp,
                    "collocation_points_per_step": pts, "alg_flops_per_step": F},

@@ -306,6 +306,44 @@ pigan_status pigan_hier_step_grads(const pigan_hier_desc* s, const float* pY, co
                                    size_t ws_bytes, void* stream);
 
 /*
+ * Domain decomposition with the shared-trunk generator: the step of
+ * pigan_hier_step_grads (same critics, snapshots, weights and losses) with the
+ * paper's generator of pigan_trunk_step_grads in place of the pair.  The
+ * trunk is evaluated at the Y sensors (Y head), the u sensors (u head) and
+ * the collocation points (jets of both heads); the free sensors read the
+ * source formed from both heads' jets.
+ */
+typedef struct {
+  pigan_mlp trunk;             /* n_groups = 1; in_dim = d + n_z */
+  pigan_mlp disc;              /* n_groups = D critics; in_dim = mY + mU + nF (1 + d) */
+  int32_t d, n_z, S, P;
+  int32_t n_sY, n_sU, B_r, chunk_S;
+  int32_t mY, mU, nF;
+  pigan_dtype dt;
+  float lambda_pde;            /* >= 0 */
+  float loss_scale;            /* > 0 */
+} pigan_hier_trunk_desc;
+
+/* Workspace bytes for pigan_hier_trunk_step_grads (0 if the descriptor is invalid). */
+size_t pigan_hier_trunk_workspace_bytes(const pigan_hier_trunk_desc* s);
+
+/*
+ *   pT : [pigan_trunk_param_count] trunk weights; gT : same shape, the
+ *        gradient of the generator loss sum_k L_adv[k] + L_pde.
+ *   pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, real, w_disc, gD,
+ *   loss, nonfinite, ws, ws_bytes, stream : as pigan_hier_step_grads.
+ * Errors: as pigan_hier_step_grads (trunk n_groups != 1 is EINVAL).
+ */
+pigan_status pigan_hier_trunk_step_grads(const pigan_hier_trunk_desc* s, const float* pT,
+                                         const float* pD, const float* z, const float* xc,
+                                         const float* xsY, const float* xsU, const float* f,
+                                         float f_const, const int32_t* idxY, const int32_t* idxU,
+                                         const int32_t* idxF, const float* real,
+                                         const float* w_disc, float* gT, float* gD, float* loss,
+                                         int32_t* nonfinite, void* ws, size_t ws_bytes,
+                                         void* stream);
+
+/*
  * pigan_adam_update — one update of fp32 master weights from the fp32
  * gradients of a training step (the paper keeps single-precision master
  * weights and adaptive loss scaling, Sec. III.C; it names no optimizer, so

@@ -324,16 +324,22 @@ static void plan_step(const pigan_step_desc* s, int Sc, StepPlan& pl, bool trunk
   pl.total = round_up((int64_t)cv.off, 256);
 }
 
-// one generator pair (a single group) and s->disc.n_groups critics
-static void plan_hier(const pigan_step_desc* s, int Sc, StepPlan& pl) {
+// one generator (a pair, or the shared trunk in the Y slot; a single group)
+// and s->disc.n_groups critics
+static void plan_hier(const pigan_step_desc* s, int Sc, StepPlan& pl, bool trunk = false) {
   Carver cv;
+  pl.trunk = trunk;
   pl.G = 1;
   pl.GD = s->disc.n_groups;
   pl.Sc = Sc;
   pl.es = esize(s->dt);
   const int GD = pl.GD;
-  plan_net(cv, pl.Y, s->genY, s->d, 0, s->n_sY, Sc, s->P, pl.es, 1);
-  plan_net(cv, pl.U, s->genU, s->d, s->d, s->n_sU, Sc, s->P, pl.es, 1);
+  if (trunk) {
+    plan_net(cv, pl.Y, s->genY, s->d, s->d, s->n_sY + s->n_sU, Sc, s->P, pl.es, 1, true);
+  } else {
+    plan_net(cv, pl.Y, s->genY, s->d, 0, s->n_sY, Sc, s->P, pl.es, 1);
+    plan_net(cv, pl.U, s->genU, s->d, s->d, s->n_sU, Sc, s->P, pl.es, 1);
+  }
   DiscBuf& D = pl.D;
   D.off.init(s->disc.in_dim, s->disc.n_hidden, s->disc.width);
   const int WD = s->disc.width, LD = s->disc.n_hidden;
@@ -368,7 +374,7 @@ static void plan_hier(const pigan_step_desc* s, int Sc, StepPlan& pl) {
     mxb = std::max(mxb, (int64_t)ns * N * Gx);
   };
   if (s->genY.n_hidden > 1) consider(pl.Y.R, s->genY.width, s->genY.width, 1);
-  if (s->genU.n_hidden > 1) consider(pl.U.R, s->genU.width, s->genU.width, 1);
+  if (!trunk && s->genU.n_hidden > 1) consider(pl.U.R, s->genU.width, s->genU.width, 1);
   consider(D.Bmax, WD, D.Kp, GD);
   if (LD > 1) consider(D.Bmax, WD, WD, GD);
   pl.dwp_floats = mx;
@@ -391,7 +397,7 @@ static int choose_chunk(const pigan_step_desc* s, bool trunk = false, bool hier 
   int Sc = s->S;
   StepPlan pl;
   while (true) {
-    if (hier) plan_hier(s, Sc, pl);
+    if (hier) plan_hier(s, Sc, pl, trunk);
     else plan_step(s, Sc, pl, trunk);
     if (pl.total <= kAutoCap || Sc == 1) return Sc;
     Sc = (Sc + 1) / 2;
@@ -994,9 +1000,11 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
   return PIGAN_OK;
 }
 
-// Domain decomposition: one generator pair, s->disc.n_groups critics (one per
-// subdomain), each on the paper's snapshot of its subdomain (Y and u sensors,
-// the generated source at free sensors and their coordinates).
+// Domain decomposition: one generator (a pair, or the shared trunk when
+// pl.trunk: then pY is the trunk, pU and gU are unused), s->disc.n_groups
+// critics (one per subdomain), each on the paper's snapshot of its subdomain
+// (Y and u sensors, the generated source at free sensors and their
+// coordinates).
 template <class T>
 static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const float* pY, const float* pU,
                              const float* pD, const float* z, const float* xc, const float* xsY, const float* xsU,
@@ -1015,7 +1023,10 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
     ProfScope ps(st, "misc", 0.0, 0.0);
     HIP_TRY(launch_zero(acc, 4 * GD, nonfinite, st));
     if ((r = cast_gen_weights<T>(ws, pl.Y, pY, 1, st)) != PIGAN_OK) return r;
-    if ((r = cast_gen_weights<T>(ws, pl.U, pU, 1, st)) != PIGAN_OK) return r;
+    if (!pl.trunk && (r = cast_gen_weights<T>(ws, pl.U, pU, 1, st)) != PIGAN_OK) return r;
+    if (pl.trunk)   // the trunk sees both sensor sets: locations [Y sensors ; u sensors]
+      HIP_TRY(launch_concat_rows(xsY, (int64_t)s->n_sY * d, s->n_sY, xsU, (int64_t)s->n_sU * d, s->n_sU, d,
+                                 tp<float>(ws, pl.Y.xsc), (int64_t)(s->n_sY + s->n_sU) * d, 1, st));
     HIP_TRY(launch_cast<T>(pD + D.off.w[1], D.off.n, WD, n_in, D.Kp, tp<T>(ws, D.w1), tp<T>(ws, D.w1T),
                            (int64_t)WD * D.Kp, GD, st));
     const int64_t dgl = (int64_t)std::max(LD - 1, 1) * WD * WD;
@@ -1023,7 +1034,9 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
       HIP_TRY(launch_cast<T>(pD + D.off.w[l], D.off.n, WD, WD, WD, tp<T>(ws, D.wc) + (size_t)(l - 2) * WD * WD,
                              tp<T>(ws, D.wcT) + (size_t)(l - 2) * WD * WD, dgl, GD, st));
   }
-  const int64_t xs_gY = (int64_t)s->n_sY * d, xs_gU = (int64_t)s->n_sU * d;
+  const int n_s = s->n_sY + s->n_sU;
+  const float* xsG = pl.trunk ? tp<float>(ws, pl.Y.xsc) : xsY;
+  const int64_t xs_gY = pl.trunk ? (int64_t)n_s * d : (int64_t)s->n_sY * d, xs_gU = (int64_t)s->n_sU * d;
   const int64_t xc_g = (int64_t)S * P * d, z_g = (int64_t)S * n_z;
   float* rbuf = tp<float>(ws, pl.hr);
   float* gN = tp<float>(ws, pl.hgn);
@@ -1040,12 +1053,18 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
       nb->n_col = (int64_t)Sc * P;
       nb->rows = nb->n_sen + (1 + nb->nd1 + nb->nd2) * nb->n_col;
     }
-    if ((r = gen_chunk_fwd<T>(ws, Yc, pY, xsY, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, 1, st)) != PIGAN_OK) return r;
-    if ((r = gen_chunk_fwd<T>(ws, Uc, pU, xsU, xs_gU, xcc, xc_g, zc, z_g, d, n_z, Sc, P, 1, st)) != PIGAN_OK) return r;
+    if ((r = gen_chunk_fwd<T>(ws, Yc, pY, xsG, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, 1, st)) != PIGAN_OK) return r;
+    if (!pl.trunk &&
+        (r = gen_chunk_fwd<T>(ws, Uc, pU, xsU, xs_gU, xcc, xc_g, zc, z_g, d, n_z, Sc, P, 1, st)) != PIGAN_OK)
+      return r;
+    // the u outputs and their cotangents: the trunk's second head, or the u network
+    const float* jetU = pl.trunk ? tp<float>(ws, Yc.jet2) : tp<float>(ws, Uc.jet);
+    float* gbarU = pl.trunk ? tp<float>(ws, Yc.gbar2) : tp<float>(ws, Uc.gbar);
+    const int64_t rowsU = pl.trunk ? Yc.rows : Uc.rows, ju_g = pl.trunk ? Yc.R : Uc.R;
     const int64_t M = (int64_t)Sc * P;
     ResidArgs ra{};
     ra.jY = tp<float>(ws, Yc.jet); ra.jy_g = Yc.R; ra.offY = Yc.n_sen;
-    ra.jU = tp<float>(ws, Uc.jet); ra.ju_g = Uc.R; ra.offU = Uc.n_sen;
+    ra.jU = jetU; ra.ju_g = ju_g; ra.offU = pl.trunk ? Yc.n_sen : Uc.n_sen;
     ra.plane = Yc.n_col; ra.M = M; ra.d = d;
     ra.f = f ? f + (int64_t)s0 * P : nullptr; ra.f_g = (int64_t)S * P; ra.f_const = f_const;
     {
@@ -1057,7 +1076,8 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
       HIP_TRY(launch_sum_partials(tp<double>(ws, pl.rpart), residual_blocks(M), acc, 4, 2, 1, st));
     }
     HierSnap h{};
-    h.jY = tp<float>(ws, Yc.jet); h.jU = tp<float>(ws, Uc.jet); h.nsY = s->n_sY; h.nsU = s->n_sU;
+    h.jY = tp<float>(ws, Yc.jet); h.jU = jetU; h.nsY = s->n_sY; h.nsU = s->n_sU;
+    h.ldY = pl.trunk ? n_s : s->n_sY; h.ldU = pl.trunk ? n_s : s->n_sU; h.offU = pl.trunk ? s->n_sY : 0;
     h.r = rbuf; h.f = ra.f; h.f_const = f_const; h.xc = xcc; h.P = P; h.d = d;
     h.idxY = idxY; h.idxU = idxU; h.idxF = idxF; h.mY = mY; h.mU = mU; h.nF = nF; h.n_in = n_in;
     h.bad = nonfinite;
@@ -1066,7 +1086,7 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
     {
       ProfScope ps(st, "misc", 0.0, 0.0);
       HIP_TRY(launch_fill_f32(tp<float>(ws, Yc.gbar), Yc.rows, Yc.R, 0.0f, 1, st));
-      HIP_TRY(launch_fill_f32(tp<float>(ws, Uc.gbar), Uc.rows, Uc.R, 0.0f, 1, st));
+      HIP_TRY(launch_fill_f32(gbarU, rowsU, ju_g, 0.0f, 1, st));
       HIP_TRY(launch_fill_f32(gN, M, M, 0.0f, 1, st));
       HIP_TRY(launch_hier_snap<T>(h, Sc, real, (int64_t)s->B_r * n_in, n_real, tp<T>(ws, D.X0), D.Bmax * D.Kp,
                                   D.Kp, GD, st));
@@ -1086,21 +1106,21 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
       a.seedY = dX; a.sY_g = dx_g; a.sY_ld = D.Kp; a.nY = n_in; a.nU = 0; a.df_sign = -1.0f;
       if ((r = gemm_nt<T>(EPI_DF, 0, 0, a, GD, st, "disc_bwd")) != PIGAN_OK) return r;
       ProfScope ps(st, "misc", 0.0, 0.0);
-      HIP_TRY(launch_hier_scatter(h, dX, dx_g, D.Kp, Sc, GD, tp<float>(ws, Yc.gbar), tp<float>(ws, Uc.gbar), gN, st));
+      HIP_TRY(launch_hier_scatter(h, dX, dx_g, D.Kp, Sc, GD, tp<float>(ws, Yc.gbar), gbarU, gN, st));
     }
     {
       // jet cotangents from the penalty and the critics' source cotangents
       ProfScope ps(st, "residual", 0.0, (double)M * (3 * d + 2) * 4.0 * 2);
       ResidArgs r2 = ra;
-      r2.gY = tp<float>(ws, Yc.gbar); r2.gU = tp<float>(ws, Uc.gbar); r2.gq = gN; r2.gq_g = M;
+      r2.gY = tp<float>(ws, Yc.gbar); r2.gU = gbarU; r2.gq = gN; r2.gq_g = M;
       r2.qscale = (float)(2.0 * s->lambda_pde * ls / ((double)S * P));
       HIP_TRY(launch_residual(r2, 1, st));
     }
-    if ((r = gen_chunk_bwd<T>(ws, pl, Yc, pY, xsY, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, gY, accum, inv, nonfinite,
+    if ((r = gen_chunk_bwd<T>(ws, pl, Yc, pY, xsG, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, gY, accum, inv, nonfinite,
                               1, st)) != PIGAN_OK)
       return r;
-    if ((r = gen_chunk_bwd<T>(ws, pl, Uc, pU, xsU, xs_gU, xcc, xc_g, zc, z_g, d, n_z, Sc, P, gU, accum, inv, nonfinite,
-                              1, st)) != PIGAN_OK)
+    if (!pl.trunk && (r = gen_chunk_bwd<T>(ws, pl, Uc, pU, xsU, xs_gU, xcc, xc_g, zc, z_g, d, n_z, Sc, P, gU, accum,
+                                           inv, nonfinite, 1, st)) != PIGAN_OK)
       return r;
   }
   {
@@ -1179,7 +1199,7 @@ static pigan_status check_hier(const pigan_hier_desc* h, pigan_step_desc* out) {
   if ((st = check_mlp(&h->disc, "disc")) != PIGAN_OK) return st;
   if ((st = check_dtype(h->dt)) != PIGAN_OK) return st;
   if (h->genY.n_groups != 1 || h->genU.n_groups != 1)
-    return fail(PIGAN_EINVAL, "one generator pair for the whole domain: genY/genU n_groups must be 1");
+    return fail(PIGAN_EINVAL, "one generator for the whole domain: its n_groups must be 1");
   if (h->d < 1 || h->d > 3) return fail(PIGAN_EINVAL, "d=%d must be 1, 2 or 3", h->d);
   if (h->n_z < 1) return fail(PIGAN_EINVAL, "n_z=%d must be >= 1", h->n_z);
   if (h->genY.in_dim != h->d + h->n_z || h->genU.in_dim != h->d + h->n_z)
@@ -1215,6 +1235,17 @@ static pigan_step_desc trunk_as_step(const pigan_trunk_desc* t) {
   return s;
 }
 
+// the hierarchical trunk step runs on the hierarchy machinery: the trunk in
+// the Y slot (and, for the shape checks, the U slot)
+static pigan_hier_desc hier_trunk_as_hier(const pigan_hier_trunk_desc* t) {
+  pigan_hier_desc h{};
+  h.genY = t->trunk; h.genU = t->trunk; h.disc = t->disc;
+  h.d = t->d; h.n_z = t->n_z; h.S = t->S; h.P = t->P; h.n_sY = t->n_sY; h.n_sU = t->n_sU; h.B_r = t->B_r;
+  h.chunk_S = t->chunk_S; h.mY = t->mY; h.mU = t->mU; h.nF = t->nF; h.dt = t->dt; h.lambda_pde = t->lambda_pde;
+  h.loss_scale = t->loss_scale;
+  return h;
+}
+
 extern "C" {
 
 pigan_status pigan_adam_update(int64_t n, float* params, const float* grads, float* m, float* v, float lr,
@@ -1240,6 +1271,52 @@ size_t pigan_hier_workspace_bytes(const pigan_hier_desc* h) {
   StepPlan pl;
   plan_hier(&s, choose_chunk(&s, false, true), pl);
   return pl.total;
+}
+
+size_t pigan_hier_trunk_workspace_bytes(const pigan_hier_trunk_desc* t) {
+  if (!t) return 0;
+  const pigan_hier_desc h = hier_trunk_as_hier(t);
+  pigan_step_desc s;
+  if (check_hier(&h, &s) != PIGAN_OK) return 0;
+  StepPlan pl;
+  plan_hier(&s, choose_chunk(&s, true, true), pl, true);
+  return pl.total;
+}
+
+pigan_status pigan_hier_trunk_step_grads(const pigan_hier_trunk_desc* t, const float* pT, const float* pD,
+                                         const float* z, const float* xc, const float* xsY, const float* xsU,
+                                         const float* f, float f_const, const int32_t* idxY, const int32_t* idxU,
+                                         const int32_t* idxF, const float* real, const float* w_disc, float* gT,
+                                         float* gD, float* loss, int32_t* nonfinite, void* ws, size_t ws_bytes,
+                                         void* stream) {
+  g_err.clear();
+  if (!t) return fail(PIGAN_EINVAL, "null hierarchical trunk step descriptor");
+  const pigan_hier_desc h = hier_trunk_as_hier(t);
+  pigan_step_desc s;
+  pigan_status st = check_hier(&h, &s);
+  if (st != PIGAN_OK) return st;
+  if (!pT || !pD || !z || !xc || !xsY || !xsU || !real || !w_disc || !gT || !gD || !loss || !nonfinite)
+    return fail(PIGAN_EINVAL, "null input or output pointer");
+  if ((h.mY > 0 && !idxY) || (h.mU > 0 && !idxU) || (h.nF > 0 && !idxF))
+    return fail(PIGAN_EINVAL, "null sensor index list");
+  if (!__builtin_isfinite(f_const)) return fail(PIGAN_EINVAL, "f_const must be finite");
+  StepPlan pl;
+  plan_hier(&s, choose_chunk(&s, true, true), pl, true);
+  if (!ws) return fail(PIGAN_EWORKSPACE, "null workspace (need %zu bytes)", pl.total);
+  if (ws_bytes < pl.total) return fail(PIGAN_EWORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, pl.total);
+  if ((uintptr_t)ws % 256) return fail(PIGAN_EINVAL, "workspace must be 256-byte aligned");
+  hipStream_t hs = (hipStream_t)stream;
+  switch (s.dt) {
+    case PIGAN_FP32:
+      return run_hier<float>(&s, pl, pT, nullptr, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, h.mY, h.mU,
+                             h.nF, real, w_disc, gT, nullptr, gD, loss, nonfinite, ws, hs);
+    case PIGAN_BF16:
+      return run_hier<bf16>(&s, pl, pT, nullptr, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, h.mY, h.mU,
+                            h.nF, real, w_disc, gT, nullptr, gD, loss, nonfinite, ws, hs);
+    default:
+      return run_hier<f16>(&s, pl, pT, nullptr, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, h.mY, h.mU,
+                           h.nF, real, w_disc, gT, nullptr, gD, loss, nonfinite, ws, hs);
+  }
 }
 
 pigan_status pigan_hier_step_grads(const pigan_hier_desc* h, const float* pY, const float* pU, const float* pD,

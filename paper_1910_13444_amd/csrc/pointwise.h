@@ -94,7 +94,8 @@ hipError_t launch_fill_f32(float* p, int64_t n, int64_t p_g, float v, int G, hip
 // domain decomposition: the snapshots of D critics (one per subdomain) and the
 // scatter of their input cotangents back to the generator's outputs
 struct HierSnap {
-  const float* jY; const float* jU; int nsY; int nsU;    // sensor values of the chunk: [s * ns + sensor]
+  const float* jY; const float* jU; int nsY; int nsU;    // sensor values of the chunk:
+  int ldY; int ldU; int offU;                            //   jY[s * ldY + i], jU[s * ldU + offU + i]
   const float* r; const float* f; float f_const;         // residual [s * P + p]; source (chunk view) or null
   const float* xc; int P; int d;                         // collocation points of the chunk [s][P][d]
   const int32_t* idxY; const int32_t* idxU; const int32_t* idxF;  // [D][mY], [D][mU], [D][nF]

@@ -621,7 +621,10 @@ __global__ void k_fill_f32(float* __restrict__ p, int64_t n, int64_t p_g, float 
 // row b (sample b of the chunk) of critic k's snapshot: [Y at sensors
 // idxY[k] | u at sensors idxU[k] | the generated source N = r + f at the free
 // sensors idxF[k] (collocation points of the sample) | their coordinates];
-// real rows follow.  Indices out of range read zero and raise h.bad.
+// real rows follow.  Indices out of range read zero and raise h.bad.  The
+// sensor rows of sample b sit at b * ldY (Y) and b * ldU + offU (u): a
+// generator pair keeps them in separate arrays, the shared trunk in one row
+// block per sample ([Y sensors ; u sensors], Y head and u head arrays).
 // ---------------------------------------------------------------------------
 template <class T>
 __global__ void k_hier_snap(HierSnap h, int n_fake, const float* __restrict__ real, int64_t real_g, int n_real,
@@ -636,11 +639,11 @@ __global__ void k_hier_snap(HierSnap h, int n_fake, const float* __restrict__ re
       const int e1 = h.mY, e2 = e1 + h.mU, e3 = e2 + h.nF;
       if (j < e1) {
         const int i = h.idxY[(int64_t)k * h.mY + j];
-        if (i >= 0 && i < h.nsY) v = h.jY[(int64_t)b * h.nsY + i];
+        if (i >= 0 && i < h.nsY) v = h.jY[(int64_t)b * h.ldY + i];
         else *h.bad = 1;
       } else if (j < e2) {
         const int i = h.idxU[(int64_t)k * h.mU + (j - e1)];
-        if (i >= 0 && i < h.nsU) v = h.jU[(int64_t)b * h.nsU + i];
+        if (i >= 0 && i < h.nsU) v = h.jU[(int64_t)b * h.ldU + h.offU + i];
         else *h.bad = 1;
       } else {
         const int q = j < e3 ? j - e2 : (j - e3) / h.d;
@@ -659,28 +662,33 @@ __global__ void k_hier_snap(HierSnap h, int n_fake, const float* __restrict__ re
   X[k * x_g + idx] = Elem<T>::from_f(v);
 }
 
-// One thread per sample: critics in order, then their inputs in order, so
-// every target accumulates in a fixed order (indices repeated within or across
-// critics add up deterministically).  Coordinates carry no cotangent.
-__global__ void k_hier_scatter(HierSnap h, const float* __restrict__ dX, int64_t dx_g, int ldx, int n_fake, int D,
-                               float* __restrict__ gY, float* __restrict__ gU, float* __restrict__ gN) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= n_fake) return;
-  for (int k = 0; k < D; ++k) {
-    const float* row = dX + k * dx_g + (int64_t)b * ldx;
-    for (int j = 0; j < h.mY; ++j) {
-      const int i = h.idxY[(int64_t)k * h.mY + j];
-      if (i >= 0 && i < h.nsY) gY[(int64_t)b * h.nsY + i] += row[j];
+// One block per sample b.  A thread owns targets (Y sensors, u sensors,
+// collocation points of the sample) and adds every critic input read from it,
+// in the order critic k, then input j: a fixed order, so indices repeated
+// within or across critics add up deterministically.  The index lists and the
+// sample's cotangent rows are uniform across the block (scalar loads).
+// Coordinates carry no cotangent.
+__device__ __forceinline__ void hier_gather(const int32_t* __restrict__ idx, int m, const float* __restrict__ rows,
+                                            int64_t row_g, int D, int n_t, float* __restrict__ dst) {
+  for (int t = threadIdx.x; t < n_t; t += blockDim.x) {
+    float acc = dst[t];
+    for (int k = 0; k < D; ++k) {
+      const int32_t* ik = idx + (int64_t)k * m;
+      const float* rk = rows + k * row_g;
+      for (int j = 0; j < m; ++j)
+        if (ik[j] == t) acc += rk[j];
     }
-    for (int j = 0; j < h.mU; ++j) {
-      const int i = h.idxU[(int64_t)k * h.mU + j];
-      if (i >= 0 && i < h.nsU) gU[(int64_t)b * h.nsU + i] += row[h.mY + j];
-    }
-    for (int j = 0; j < h.nF; ++j) {
-      const int i = h.idxF[(int64_t)k * h.nF + j];
-      if (i >= 0 && i < h.P) gN[(int64_t)b * h.P + i] += row[h.mY + h.mU + j];
-    }
+    dst[t] = acc;
   }
+}
+
+__global__ void k_hier_scatter(HierSnap h, const float* __restrict__ dX, int64_t dx_g, int ldx, int D,
+                               float* __restrict__ gY, float* __restrict__ gU, float* __restrict__ gN) {
+  const int b = blockIdx.x;
+  const float* row = dX + (int64_t)b * ldx;
+  hier_gather(h.idxY, h.mY, row, dx_g, D, h.nsY, gY + (int64_t)b * h.ldY);
+  hier_gather(h.idxU, h.mU, row + h.mY, dx_g, D, h.nsU, gU + (int64_t)b * h.ldU + h.offU);
+  hier_gather(h.idxF, h.nF, row + h.mY + h.mU, dx_g, D, h.P, gN + (int64_t)b * h.P);
 }
 
 __global__ void k_hier_pde_loss(const double* __restrict__ acc, int slot, float lambda_pde, int64_t SP, float* loss,
@@ -1094,7 +1102,7 @@ hipError_t launch_hier_snap(const HierSnap& h, int n_fake, const float* real, in
 hipError_t launch_hier_scatter(const HierSnap& h, const float* dX, int64_t dx_g, int ldx, int n_fake, int D,
                                float* gY, float* gU, float* gN, hipStream_t st) {
   if (n_fake <= 0 || D <= 0) return hipSuccess;
-  k_hier_scatter<<<nblk(n_fake, 64), 64, 0, st>>>(h, dX, dx_g, ldx, n_fake, D, gY, gU, gN);
+  k_hier_scatter<<<n_fake, 256, 0, st>>>(h, dX, dx_g, ldx, D, gY, gU, gN);
   return hipGetLastError();
 }
 

@@ -59,6 +59,14 @@ class HierDesc(C.Structure):
                 ("dt", C.c_int32), ("lambda_pde", C.c_float), ("loss_scale", C.c_float)]
 
 
+class HierTrunkDesc(C.Structure):
+    _fields_ = [("trunk", Mlp), ("disc", Mlp),
+                ("d", C.c_int32), ("n_z", C.c_int32), ("S", C.c_int32), ("P", C.c_int32),
+                ("n_sY", C.c_int32), ("n_sU", C.c_int32), ("B_r", C.c_int32), ("chunk_S", C.c_int32),
+                ("mY", C.c_int32), ("mU", C.c_int32), ("nF", C.c_int32),
+                ("dt", C.c_int32), ("lambda_pde", C.c_float), ("loss_scale", C.c_float)]
+
+
 class KernelStat(C.Structure):
     _fields_ = [("name", C.c_char * 48), ("launches", C.c_int64), ("total_ms", C.c_double),
                 ("flops", C.c_double), ("bytes", C.c_double)]
@@ -90,6 +98,8 @@ def lib():
         "pigan_adam_update": (i32, [i64, P, P, P, P, f32, f32, f32, f32, i32, P, P]),
         "pigan_hier_workspace_bytes": (sz, [P]),
         "pigan_hier_step_grads": (i32, [P, P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, P, P, P, sz, P]),
+        "pigan_hier_trunk_workspace_bytes": (sz, [P]),
+        "pigan_hier_trunk_step_grads": (i32, [P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, P, P, sz, P]),
         "pigan_trunk_param_count": (i64, [P]),
         "pigan_trunk_workspace_bytes": (sz, [P]),
         "pigan_trunk_step_grads": (i32, [P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, sz, P]),
@@ -380,6 +390,61 @@ class HierStep:
             _ptr(idxY, "idxY", D * d.mY, dtype=i32), _ptr(idxU, "idxU", D * d.mU, dtype=i32),
             _ptr(idxF, "idxF", D * d.nF, dtype=i32), _ptr(real, "real", D * d.B_r * d.disc.in_dim),
             _ptr(w_disc, "w_disc", D), _ptr(o.gY, "gY"), _ptr(o.gU, "gU"), _ptr(o.gD, "gD"), _ptr(o.loss, "loss"),
+            _ptr(o.nonfinite, "nonfinite", 1, dtype=i32), _ptr(self.ws, "ws", dtype=torch.uint8), self.ws_bytes,
+            _stream())
+        _check(st)
+        return o
+
+
+def hier_trunk_desc(wl: Workload, D: int, mY: int, mU: int, nF: int, S: int | None = None,
+                    B_r: int | None = None, chunk_S: int = 0, dtype: str | None = None, lambda_pde: float = 0.0,
+                    loss_scale: float = 1.0) -> HierTrunkDesc:
+    S = wl.S if S is None else S
+    B_r = wl.B_r if B_r is None else B_r
+    n_in = mY + mU + nF * (1 + wl.d)
+    return HierTrunkDesc(Mlp(1, wl.in_dim, wl.L, wl.W), Mlp(D, n_in, wl.L_D, wl.W_D), wl.d, wl.n_z, S, wl.P,
+                         wl.n_sY, wl.n_sU, B_r, chunk_S, mY, mU, nF, DTYPES[dtype or wl.dtype], lambda_pde,
+                         loss_scale)
+
+
+@dataclass
+class HierTrunkOut:
+    gT: torch.Tensor
+    gD: torch.Tensor      # [D, nD]
+    loss: torch.Tensor    # [D, 3]: L_D[k], L_adv[k], L_pde
+    nonfinite: torch.Tensor
+
+
+class HierTrunkStep:
+    """Repeated domain-decomposition steps with the shared-trunk generator."""
+
+    def __init__(self, desc: HierTrunkDesc, device="cuda"):
+        self.desc = desc
+        self.device = torch.device(device)
+        D = desc.disc.n_groups
+        self.nT = int(lib().pigan_trunk_param_count(C.byref(desc.trunk)))
+        self.nD = n_params(desc.disc.in_dim, desc.disc.n_hidden, desc.disc.width)
+        need = int(lib().pigan_hier_trunk_workspace_bytes(C.byref(desc)))
+        if need == 0:
+            _check(lib().pigan_hier_trunk_step_grads(C.byref(desc), *([None] * 7), 0.0, *([None] * 10), 0, None))
+        self.ws_bytes = need
+        self.ws = _workspace(need, self.device)
+        f32 = dict(dtype=torch.float32, device=self.device)
+        self.out = HierTrunkOut(torch.empty((self.nT,), **f32), torch.empty((D, self.nD), **f32),
+                                torch.empty((D, 3), **f32), torch.zeros((1,), dtype=torch.int32, device=self.device))
+
+    def __call__(self, pT, pD, z, xc, xsY, xsU, idxY, idxU, idxF, real, w_disc, f=None, f_const=0.0) -> HierTrunkOut:
+        d = self.desc
+        D, S, Pn = d.disc.n_groups, d.S, d.P
+        o = self.out
+        i32 = torch.int32
+        st = lib().pigan_hier_trunk_step_grads(
+            C.byref(d), _ptr(pT, "pT", self.nT), _ptr(pD, "pD", D * self.nD), _ptr(z, "z", S * d.n_z),
+            _ptr(xc, "xc", S * Pn * d.d), _ptr(xsY, "xsY", d.n_sY * d.d), _ptr(xsU, "xsU", d.n_sU * d.d),
+            _ptr(f, "f", S * Pn), float(f_const),
+            _ptr(idxY, "idxY", D * d.mY, dtype=i32), _ptr(idxU, "idxU", D * d.mU, dtype=i32),
+            _ptr(idxF, "idxF", D * d.nF, dtype=i32), _ptr(real, "real", D * d.B_r * d.disc.in_dim),
+            _ptr(w_disc, "w_disc", D), _ptr(o.gT, "gT"), _ptr(o.gD, "gD"), _ptr(o.loss, "loss"),
             _ptr(o.nonfinite, "nonfinite", 1, dtype=i32), _ptr(self.ws, "ws", dtype=torch.uint8), self.ws_bytes,
             _stream())
         _check(st)

@@ -161,10 +161,32 @@ def run_hier_gpu(wl, hi, real, lam=0.0, chunk_S=0, dtype=None, idx=None, f=None,
                 nonfinite=int(o.nonfinite.cpu().item()))
 
 
-def hier_errors(wl, out, ref, n_in):
+def run_hier_trunk_gpu(wl, hi, real, lam=0.0, chunk_S=0, dtype=None, f_const=0.0):
+    """One domain-decomposition step with the shared trunk (pigan_hier_trunk_step_grads)."""
+    import torch
+    from paper_1910_13444_amd import pigan
+    b, h = hi.base, hi.hier
+    desc = pigan.hier_trunk_desc(wl, h.D, h.idxY.shape[1], h.idxU.shape[1], h.idxF.shape[1], S=b.z.shape[1],
+                                 B_r=real.shape[1], chunk_S=chunk_S, dtype=dtype, lambda_pde=lam)
+    step = pigan.HierTrunkStep(desc)
+
+    def ti(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+    o = step(to_dev(b.pT[0]), to_dev(hi.pD), to_dev(b.z[0]), to_dev(b.xc[0]), to_dev(b.xsY[0]), to_dev(b.xsU[0]),
+             ti(h.idxY), ti(h.idxU), ti(h.idxF), to_dev(real), to_dev(h.w), f_const=f_const)
+    torch.cuda.synchronize()
+    return dict(gY=o.gT.cpu().numpy(), gD=o.gD.cpu().numpy(), loss=o.loss.cpu().numpy(),
+                nonfinite=int(o.nonfinite.cpu().item()))
+
+
+def hier_errors(wl, out, ref, n_in, trunk=False):
     errs = {}
-    errs.update(grad_errors(out["gY"][None], ref["gY"][None], wl.gen_shape(), "gY"))
-    errs.update(grad_errors(out["gU"][None], ref["gU"][None], wl.gen_shape(), "gU"))
+    if trunk:
+        for name, sl in trunk_slices(*wl.gen_shape()):
+            errs[f"gT.{name}"] = rel(out["gY"][sl], ref["gY"][sl])
+    else:
+        errs.update(grad_errors(out["gY"][None], ref["gY"][None], wl.gen_shape(), "gY"))
+        errs.update(grad_errors(out["gU"][None], ref["gU"][None], wl.gen_shape(), "gU"))
     errs.update(grad_errors(out["gD"], ref["gD"], (n_in, wl.L_D, wl.W_D), "gD"))
     errs["L_D"] = rel(out["loss"][:, 0], ref["L_D"])
     errs["L_adv"] = rel(out["loss"][:, 1], ref["L_adv"])

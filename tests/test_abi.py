@@ -217,3 +217,33 @@ def test_hier_step_validation():
     assert _hier(e, 1 << 40) == pigan.EINVAL
     e = pigan.hier_desc(wl, 21, 0, 0, 0)
     assert _hier(e, 1 << 40) == pigan.EINVAL
+
+
+def _hier_trunk(desc, ws_bytes, ptr=FAKE, idx=FAKE, ws=FAKE):
+    return pigan.lib().pigan_hier_trunk_step_grads(C.byref(desc), *([ptr] * 6), None, 0.0, idx, idx, idx, ptr, ptr,
+                                                   ptr, ptr, ptr, ptr, ws, ws_bytes, None)
+
+
+def test_hier_trunk_step_validation():
+    wl = configs.HT5
+    d = pigan.hier_trunk_desc(wl, 21, 16, 16, 16)
+    need = int(pigan.lib().pigan_hier_trunk_workspace_bytes(C.byref(d)))
+    # the trunk sees both sensor sets in one network: a different plan from the pair's
+    pair = int(pigan.lib().pigan_hier_workspace_bytes(C.byref(pigan.hier_desc(wl, 21, 16, 16, 16))))
+    assert need > 0 and pair > 0 and need != pair
+    assert _hier_trunk(d, need, ptr=None) == pigan.EINVAL
+    assert _hier_trunk(d, need, idx=None) == pigan.EINVAL
+    assert _hier_trunk(d, need - 1) == pigan.EWORKSPACE
+    assert _hier_trunk(d, need, ws=C.c_void_p(4096 + 32)) == pigan.EINVAL
+    for field, value in (("mY", -1), ("B_r", 0), ("lambda_pde", -1.0), ("loss_scale", 0.0)):
+        e = pigan.hier_trunk_desc(wl, 21, 16, 16, 16)
+        setattr(e, field, value)
+        assert _hier_trunk(e, 1 << 40) == pigan.EINVAL, field
+        assert pigan.lib().pigan_hier_trunk_workspace_bytes(C.byref(e)) == 0
+    e = pigan.hier_trunk_desc(wl, 21, 16, 16, 16)
+    e.trunk.n_groups = 2                                   # one generator for the whole domain
+    assert _hier_trunk(e, 1 << 40) == pigan.EINVAL
+    e = pigan.hier_trunk_desc(wl, 21, 16, 16, 16)
+    e.trunk.in_dim = wl.in_dim + 1
+    assert _hier_trunk(e, 1 << 40) == pigan.EINVAL
+    assert pigan.lib().pigan_hier_trunk_step_grads(None, *([None] * 7), 0.0, *([None] * 10), 0, None) == pigan.EINVAL
