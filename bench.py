@@ -305,6 +305,7 @@ def main():
     # per-kernel timing: the same steps again with HIP events around every launch
     roof = None
     kernels = None
+    step_roof = None
     if not a.no_profile:
         pigan.profile_enable(True)
         run_steps(step, d, wl, a.steps)
@@ -314,7 +315,19 @@ def main():
         tot = sum(s["total_ms"] for s in stats)
         kernels = {s["name"]: {"launches_per_step": s["launches"] / a.steps,
                                "ms_per_step": s["total_ms"] / a.steps,
-                               "share": s["total_ms"] / tot if tot else 0.0} for s in stats}
+                               "share": s["total_ms"] / tot if tot else 0.0,
+                               "alg_flops_per_step": s["flops"] / a.steps,
+                               "alg_bytes_per_step": s["bytes"] / a.steps} for s in stats}
+        # the step's own roofline: every launch at the faster of its two
+        # bounds (algorithmic FLOPs at the dense peak, algorithmic bytes at
+        # 8 TB/s); launches that record neither count zero, so this is a
+        # lower bound on the step time
+        bound_s = sum(max(s["flops"] / (PEAK_TFLOPS[wl.dtype] * 1e12), s["bytes"] / (PEAK_GBS * 1e9))
+                      for s in stats) / a.steps
+        step_roof = {"bound_ms": bound_s * 1e3, "frac": bound_s * 1e3 / ms,
+                     "mfma_bound_share": sum(s["total_ms"] for s in stats
+                                             if s["flops"] / (PEAK_TFLOPS[wl.dtype] * 1e12) >
+                                             s["bytes"] / (PEAK_GBS * 1e9)) / tot if tot else 0.0}
         dom = max(stats, key=lambda s: s["total_ms"])
         avg_ms = dom["total_ms"] / dom["launches"]
         fl = dom["flops"] / dom["launches"]
@@ -358,6 +371,7 @@ def main():
         "mfma_frac_step": tflops / PEAK_TFLOPS[wl.dtype],
         "nonfinite": nf,
         "roofline": roof,
+        "step_roofline": step_roof,
         "measured_peaks": peaks,
         "cpu_baseline": cpu,
         "kernels": kernels,
