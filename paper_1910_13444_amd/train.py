@@ -1,8 +1,9 @@
 """Training loop on one GPU around the C-ABI training step.
 
 Host logic only: every gradient and every parameter update runs in
-libpigan.so kernels (pigan_train_step_grads / pigan_trunk_step_grads and
-pigan_adam_update) on the current stream.
+libpigan.so kernels (pigan_train_step_grads, pigan_trunk_step_grads,
+pigan_hier_step_grads or pigan_hier_trunk_step_grads, and pigan_adam_update)
+on the current stream.
 
 * fp32 master weights updated by Adam (the paper keeps single-precision
   master weights, Sec. III.C, and names no optimizer).
@@ -93,19 +94,34 @@ class TrainConfig:
 
 class Trainer:
     """Owns the master weights (generator: pY and pU, or the trunk pT; critic
-    pD), their Adam states, the loss scale and the schedule.  `inputs` are the
-    batch's device tensors: z, xc, xsY, xsU, real, w_group (and optionally f)."""
+    pD: [G, nD], or [D, nD] for the subdomain critics of a hierarchy), their
+    Adam states, the loss scale and the schedule.  `inputs` are the batch's
+    device tensors: z, xc, xsY, xsU, real, w_group (and optionally f); for a
+    hierarchy (arch "hier" or "hier_trunk", one generator, no group axis) z,
+    xc, xsY, xsU, real, idxY, idxU, idxF, w_disc (and optionally f)."""
 
     def __init__(self, wl: Workload, gen: list[torch.Tensor], pD: torch.Tensor, inputs: dict, cfg: TrainConfig):
         self.wl, self.cfg, self.inp = wl, cfg, inputs
-        self.trunk = wl.arch == "trunk"
+        self.trunk = wl.trunk_gen
+        self.hier = wl.is_hier
         if cfg.schedule not in ("sequential", "parallel"):
             raise ValueError(f"unknown schedule {cfg.schedule!r}")
-        S, B_r = inputs["z"].shape[1], inputs["real"].shape[1]
-        if self.trunk:
+        if self.hier:
+            S, B_r, D = inputs["z"].shape[0], inputs["real"].shape[1], inputs["w_disc"].shape[0]
+            m = (inputs["idxY"].shape[1], inputs["idxU"].shape[1], inputs["idxF"].shape[1])
+            if self.trunk:
+                self.desc = pigan.hier_trunk_desc(wl, D, *m, S=S, B_r=B_r, chunk_S=cfg.chunk_S,
+                                                  lambda_pde=wl.lambda_pde)
+                self.step_fn = pigan.HierTrunkStep(self.desc)
+            else:
+                self.desc = pigan.hier_desc(wl, D, *m, S=S, B_r=B_r, chunk_S=cfg.chunk_S, lambda_pde=wl.lambda_pde)
+                self.step_fn = pigan.HierStep(self.desc)
+        elif self.trunk:
+            S, B_r = inputs["z"].shape[1], inputs["real"].shape[1]
             self.desc = pigan.trunk_desc(wl, S=S, B_r=B_r, chunk_S=cfg.chunk_S)
             self.step_fn = pigan.TrunkStep(self.desc)
         else:
+            S, B_r = inputs["z"].shape[1], inputs["real"].shape[1]
             self.desc = pigan.step_desc(wl, S=S, B_r=B_r, chunk_S=cfg.chunk_S)
             self.step_fn = pigan.TrainStep(self.desc)
         self.gen = [g.contiguous() for g in gen]
@@ -123,7 +139,17 @@ class Trainer:
         if self.scaler is not None:
             self.desc.loss_scale = self.scaler.scale
         i = self.inp
-        if self.trunk:
+        if self.hier:
+            idx = (i["idxY"], i["idxU"], i["idxF"], i["real"], i["w_disc"])
+            if self.trunk:
+                o = self.step_fn(gen[0], pD, i["z"], i["xc"], i["xsY"], i["xsU"], *idx, f=i.get("f"),
+                                 f_const=self.wl.f_const)
+                grads_g = [o.gT]
+            else:
+                o = self.step_fn(gen[0], gen[1], pD, i["z"], i["xc"], i["xsY"], i["xsU"], *idx, f=i.get("f"),
+                                 f_const=self.wl.f_const)
+                grads_g = [o.gY, o.gU]
+        elif self.trunk:
             o = self.step_fn(gen[0], pD, i["z"], i["xc"], i["xsY"], i["xsU"], i["real"], f=i.get("f"),
                              f_const=self.wl.f_const, w_group=i["w_group"])
             grads_g = [o.gT]

@@ -136,3 +136,50 @@ def test_training_reduces_the_residual():
     print(f"L_pde first {first:.4g} last {last:.4g}; L_D last {losses[-1, 0]:.4g}")
     assert np.isfinite(losses).all()
     assert last < 0.5 * first
+
+
+HW = configs.C2.with_(n_sY=16, n_sU=16, S=3, P=16, B_r=2, W=32, W_D=32, L=3, L_D=2, n_z=3, dtype="fp32",
+                      lambda_pde=0.5, f_const=0.3, seed=45)
+
+
+@pytest.mark.parametrize("schedule,arch", [("sequential", "hier"), ("parallel", "hier_trunk")])
+def test_hier_trainer_matches_oracle(schedule, arch):
+    """The training loop of the domain-decomposition step: one generator
+    (pair or shared trunk) and 1 + 4 subdomain critics updated together."""
+    from paper_1910_13444_amd.inputs import make_hier_inputs
+    wl = HW.with_(arch=arch, L=3 if arch == "hier" else 5)
+    _say(f"hier trainer {schedule} {arch}: 3 rounds fp32 vs the oracle loop")
+    hi = make_hier_inputs(wl, sides=(1, 2), m_sensors=4, n_free=4)
+    b, h = hi.base, hi.hier
+    trunk = arch == "hier_trunk"
+    real = oracle.real_snapshots_hier(wl, hi, trunk_teacher=b.tT[0] if trunk else None)
+    f = np.full((wl.S, wl.P), wl.f_const)
+    dshape = (real.shape[2], wl.L_D, wl.W_D)
+    nY = 0 if trunk else b.pY.shape[1]
+
+    def fn(pG, pD):
+        pY, pU = (pG, None) if trunk else (pG[:nY], pG[nY:])
+        o = oracle.train_step_hier(wl.gen_shape(), dshape, wl.d, pY, pU, pD, b.z[0], b.xc[0], b.xsY[0], b.xsU[0], f,
+                                   h.idxY, h.idxU, h.idxF, real, h.w, lambda_pde=wl.lambda_pde, trunk=trunk)
+        loss = np.stack([o["L_D"], o["L_adv"], np.full(len(o["L_D"]), o["L_pde"])], 1)
+        return loss, (o["gY"] if trunk else np.concatenate([o["gY"], o["gU"]])), o["gD"]
+
+    def ti(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+    dev = dict(z=to_dev(b.z[0]), xc=to_dev(b.xc[0]), xsY=to_dev(b.xsY[0]), xsU=to_dev(b.xsU[0]), real=to_dev(real),
+               idxY=ti(h.idxY), idxU=ti(h.idxU), idxF=ti(h.idxF), w_disc=to_dev(h.w))
+    gen = [to_dev(b.pT[0])] if trunk else [to_dev(b.pY[0]), to_dev(b.pU[0])]
+    cfg = TrainConfig(schedule=schedule, n_critic=2, steps_per_exchange=2, lr_g=1e-3, lr_d=2e-3)
+    tr = Trainer(wl, gen, to_dev(hi.pD), dev, cfg)
+    losses = tr.run(3).cpu().numpy()
+    pG0 = b.pT[0] if trunk else np.concatenate([b.pY[0], b.pU[0]])
+    pG, pD, ref_losses = oracle_train(fn, pG0, hi.pD, 3, schedule=schedule, n_critic=2, steps_per_exchange=2,
+                                      lr_g=1e-3, lr_d=2e-3)
+    gpu_G = np.concatenate([g.cpu().numpy().ravel() for g in tr.gen])
+    gpu_D = tr.pD.cpu().numpy()
+    eG = rel(gpu_G - pG0, pG - pG0)
+    eD = rel(gpu_D - hi.pD, pD - hi.pD)
+    eL = rel(losses, ref_losses)
+    print(f"weight change rel err: generator {eG:.3g}, critics {eD:.3g}; losses {eL:.3g}")
+    assert losses.shape == ref_losses.shape
+    assert eG <= 1e-3 and eD <= 1e-3 and eL <= 1e-4
