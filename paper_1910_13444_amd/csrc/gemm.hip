@@ -547,12 +547,21 @@ k_gemm_nt(const NtArgs<T> p) {
 // its successor (and, in the reverse pass, the saved pre-activations of the
 // tile itself) are already on their way into registers, so every block keeps
 // a whole tile of loads in flight.  Four waves; wave w owns columns
-// 32w..32w+31 of every stream.
+// 32w..32w+31 of every stream.  SKIP: the residual blocks of a shared trunk
+// (forward: h_l += h_{l-2}; reverse: the block's skip cotangent added, the
+// total kept), read like the saved pre-activations, ahead of the prefetch.
 // ---------------------------------------------------------------------------
-template <class T, int ND1, int ND2, int EPI, bool FIRST>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+// one block per CU (and the whole register file) for the skip variant of
+// five streams, whose skip rows do not fit beside the prefetch otherwise
+template <int C, bool SKIP>
+constexpr int wr_blocks_per_cu() { return SKIP && C >= 5 ? 1 : 2; }
+
+template <class T, int ND1, int ND2, int EPI, bool FIRST, bool SKIP = false>
+__global__ void __launch_bounds__(256)
+__attribute__((amdgpu_waves_per_eu(wr_blocks_per_cu<1 + ND1 + ND2, SKIP>())))
 k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
   static_assert(sizeof(T) == 2, "16-bit storage only");
+  static_assert(!(SKIP && FIRST), "residual blocks never start at the first layer");
   constexpr int C = 1 + ND1 + ND2;
   constexpr int BM = 32, BN = 128, NTH = 256, ES = 2;
   constexpr int RB = 256;                          // bytes of one operand row (K = 128)
@@ -650,7 +659,7 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) bias[r] = p.bias[g * p.b_g + ncol(r >> 2) + (r & 3)];
   }
-  if (EPI == EPI_FWD && p.y) {
+  if (!SKIP && EPI == EPI_FWD && p.y) {           // (the output layer is never fused with a skip)
 #pragma unroll
     for (int r = 0; r < 16; ++r) wo[r] = p.wout[g * p.wo_g + ncol(r >> 2) + (r & 3)];
     bout = p.wout[g * p.wo_g + BN];
@@ -752,6 +761,22 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
         }
       }
     }
+    // residual skip of the tile in the same lane layout: the block input
+    // h_{l-2} (forward) or the skip cotangent of a block input (reverse)
+    u32x2 skp[SKIP ? C : 1][4];
+    const T* const skip_src = EPI == EPI_FWD ? p.skip : p.skip_g;
+    if (SKIP && skip_src) {
+      int64_t pt = m0 + (lane & 31);
+      if (pt >= npts) pt = npts - 1;
+      const uint32_t po = (uint32_t)(pt * p.ldo * ES);
+#pragma unroll
+      for (int k = 0; k < (SKIP ? C : 1); ++k) {
+        const char* base = (const char*)(skip_src + g * p.o_g + (p.seg.row0 + k * p.seg.plane) * p.ldo);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) skp[k][q] = *(const u32x2*)(base + po + ncol(q) * ES);
+      }
+    }
+
     {
       const int64_t nx = tile + gridDim.x;
       xload(nx < ntiles ? nx : tile);              // unconditional: the last prefetch is never used
@@ -763,6 +788,18 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
     for (int k = 0; k < C; ++k)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[k][r] = 0.0f;
+    // register r of a lane holds column ncol(r / 4) + r % 4 of its point,
+    // which is element r % 4 of the lane's u32x2 pair (r / 4)
+    auto add_skip = [&]() {
+#pragma unroll
+      for (int k = 0; k < (SKIP ? C : 1); ++k)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const uint32_t w = skp[k][r >> 2][(r & 3) >> 1];
+          const uint16_t h = (r & 1) ? (uint16_t)(w >> 16) : (uint16_t)(w & 0xffffu);
+          acc[k][r] += Elem<T>::to_f(__builtin_bit_cast(T, h));
+        }
+    };
 #pragma unroll
     for (int c = 0; c < RB / 32; ++c) {
       const int koff = c * 32 + hh * 16;
@@ -823,7 +860,10 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
 #pragma unroll
         for (int k = 0; k < C; ++k) acc[k][r] = v[k];
       }
-      if (p.y) {
+      if constexpr (SKIP) {
+        if (p.skip) add_skip();                    // residual block output
+      }
+      if (!SKIP && p.y) {
         // output layer: y = w_out . h over the activations as stored, summed
         // over the lane's columns, the two lane halves, then the four waves
         // in wave order (through LDS)
@@ -851,6 +891,13 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
       }
       if (p.out_h) stage_out(p.out_h);
     } else {
+      if constexpr (SKIP) {
+        // skip cotangent of a residual block's input, and the total kept for
+        // the skip below it (all loads of the tile were consumed before the
+        // staging barrier, so an in-place total is safe)
+        if (p.skip_g) add_skip();
+        if (p.out_gh) stage_out(p.out_gh);
+      }
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
 #pragma unroll
@@ -1458,14 +1505,17 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   const int64_t npts = a.seg.n_points;
   if (npts <= 0) return hipSuccess;
   if constexpr (sizeof(T) == 2 && C <= 5 && EPI != EPI_DF) {
-    if (nt_resident_ok((int)sizeof(T), C, a.K, a.N, npts, a.ldx, a.ldo) && !a.skip && !a.skip_g && !a.out_gh) {
-      // persistent weight-resident kernel: two blocks per CU in total
+    const bool skip = a.skip || a.skip_g || a.out_gh;
+    if (nt_resident_ok((int)sizeof(T), C, a.K, a.N, npts, a.ldx, a.ldo) && !(skip && (a.fp1 || a.y))) {
+      // persistent weight-resident kernel: two blocks per CU in total (one
+      // for the five-stream skip variant)
       const int64_t ntiles = (npts + 31) / 32;
-      int64_t nb = 2 * (int64_t)cu_count() / G;
+      int64_t nb = (skip ? wr_blocks_per_cu<C, true>() : 2) * (int64_t)cu_count() / G;
       if (nb < 1) nb = 1;
       if (nb > ntiles) nb = ntiles;
       dim3 grid((unsigned)nb, 1, G);
       if (a.fp1) k_gemm_nt_wr<T, ND1, ND2, EPI, true><<<grid, 256, 0, st>>>(a, ntiles);
+      else if (skip) k_gemm_nt_wr<T, ND1, ND2, EPI, false, true><<<grid, 256, 0, st>>>(a, ntiles);
       else k_gemm_nt_wr<T, ND1, ND2, EPI, false><<<grid, 256, 0, st>>>(a, ntiles);
       return hipGetLastError();
     }
