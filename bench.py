@@ -232,6 +232,8 @@ def main():
     ap.add_argument("--chunk-S", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of one step captured in a HIP graph instead of eager calls")
     ap.add_argument("--no-peaks", action="store_true", help="skip the copy / GEMM micro-benchmarks")
     ap.add_argument("--lambda-gp", type=float, default=0.0,
                     help="add the critic gradient penalty with this weight (seeded mixing weights)")
@@ -286,12 +288,18 @@ def main():
     torch.cuda.synchronize()
     nf = int(step.out.nonfinite.item())
 
+    graph = pigan.StepGraph(lambda: run_steps(step, d, wl, 1)) if a.graph else None
+
     # timed region
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     ev0.record()
-    run_steps(step, d, wl, a.steps)
+    if graph is not None:
+        for _ in range(a.steps):
+            graph.replay()
+    else:
+        run_steps(step, d, wl, a.steps)
     ev1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
@@ -366,6 +374,7 @@ def main():
                                f"{wl.n_in_hier} inputs each" if wl.is_hier else wl.G),
                    "disc": f"{wl.L_D}x{wl.W_D} tanh on {wl.n_in}", "S": wl.S, "P": wl.P,
                    "sensors": [wl.n_sY, wl.n_sU], "B_r": wl.B_r, "chunk_S": a.chunk_S, "lambda_gp": a.lambda_gp,
+                   "launch": "hip_graph" if a.graph else "eager",
                    "collocation_points_per_step": pts, "alg_flops_per_step": F},
         "collocation_points_per_s": pts / (ms * 1e-3),
         "mfma_frac_step": tflops / PEAK_TFLOPS[wl.dtype],

@@ -451,6 +451,33 @@ class HierTrunkStep:
         return o
 
 
+class StepGraph:
+    """A step call captured once in a HIP graph (torch.cuda.CUDAGraph) and
+    replayed: the same kernels on the same device buffers, launched as one
+    graph (no per-kernel launch gaps).  `fn` issues the work on the current
+    stream and takes no arguments (e.g. a lambda around a TrainStep call with
+    fixed device tensors); it runs once eagerly on a side stream first.  The
+    library's launches are all kernels (no memset or host synchronisation), so
+    every replay recomputes the outputs from the current contents of the
+    inputs."""
+
+    def __init__(self, fn):
+        self.fn = fn
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            fn()
+        torch.cuda.synchronize()
+
+    def replay(self):
+        self.graph.replay()
+
+
 def profile_enable(on: bool = True):
     _check(lib().pigan_profile_enable(1 if on else 0))
 
