@@ -180,7 +180,7 @@ def run_steps(step, d, wl, k):
                  d["real"], d["w_disc"], f=None, f_const=wl.f_const)
         elif wl.arch == "trunk":
             step(d["pT"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["real"], f=None, f_const=wl.f_const,
-                 w_group=d["w_group"])
+                 w_group=d["w_group"], gp_eps=d.get("gp_eps"))
         else:
             step(d["pY"], d["pU"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["real"], f=None,
                  f_const=wl.f_const, w_group=d["w_group"], gp_eps=d.get("gp_eps"))
@@ -278,9 +278,7 @@ def main():
             step = pigan.HierStep(pigan.hier_desc(wl, wl.n_critics, wl.m_sensors, wl.m_sensors, wl.n_free,
                                                   chunk_S=a.chunk_S, lambda_pde=wl.lambda_pde), device=dev)
     elif wl.arch == "trunk":
-        if a.lambda_gp > 0:
-            raise SystemExit("bench: the shared-trunk step has no gradient penalty")
-        step = pigan.TrunkStep(pigan.trunk_desc(wl, chunk_S=a.chunk_S), device=dev)
+        step = pigan.TrunkStep(pigan.trunk_desc(wl, chunk_S=a.chunk_S, lambda_gp=a.lambda_gp), device=dev)
     else:
         step = pigan.TrainStep(pigan.step_desc(wl, chunk_S=a.chunk_S, lambda_gp=a.lambda_gp), device=dev)
     log(f"bench: workspace {step.ws_bytes / 2**30:.2f} GiB; warmup {a.warmup}")

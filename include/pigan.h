@@ -231,14 +231,18 @@ typedef struct {
   pigan_dtype dt;
   float lambda_pde;            /* weight of the residual penalty (>= 0) */
   float loss_scale;            /* static loss scale (> 0; 1 unless fp16) */
+  float lambda_gp;             /* critic gradient penalty weight: 0 for pigan_trunk_step_grads,
+                                  >= 0 for pigan_trunk_step_grads_gp */
 } pigan_trunk_desc;
 
-/* Workspace bytes for pigan_trunk_step_grads (0 if the descriptor is invalid). */
+/* Workspace bytes for pigan_trunk_step_grads(_gp) (0 if the descriptor is invalid;
+ * includes the penalty's buffers when lambda_gp > 0). */
 size_t pigan_trunk_workspace_bytes(const pigan_trunk_desc* s);
 
 /*
  * The training step of pigan_train_step_grads with the shared-trunk generator
- * (same losses, critic and residual; no gradient penalty).  The trunk is
+ * (same losses, critic and residual; the gradient penalty is
+ * pigan_trunk_step_grads_gp).  The trunk is
  * evaluated at the Y sensors (Y head), the u sensors (u head) and the
  * collocation points (jets of both heads).
  *   pT : [G, pigan_trunk_param_count] trunk weights; gT : same shape, the
@@ -247,7 +251,7 @@ size_t pigan_trunk_workspace_bytes(const pigan_trunk_desc* s);
  *   ws_bytes, stream : as pigan_train_step_grads (device pointers, caller
  *   owned, outputs overwritten, asynchronous on `stream`).
  * Errors: EINVAL for null pointers or invalid shapes (as pigan_train_step_grads),
- * ENOTSUP for unsupported widths, EWORKSPACE, EDEVICE.
+ * ENOTSUP for unsupported widths or lambda_gp != 0, EWORKSPACE, EDEVICE.
  */
 pigan_status pigan_trunk_step_grads(const pigan_trunk_desc* s, const float* pT, const float* pD,
                                     const float* z, const float* xc, const float* xsY,
@@ -255,6 +259,23 @@ pigan_status pigan_trunk_step_grads(const pigan_trunk_desc* s, const float* pT, 
                                     const float* real, const float* w_group, float* gT, float* gD,
                                     float* loss, int32_t* nonfinite, void* ws, size_t ws_bytes,
                                     void* stream);
+
+/*
+ * pigan_trunk_step_grads plus the critic gradient penalty of
+ * pigan_train_step_grads_gp (same definition, Sec. I.C and Sec. II.C), the
+ * fake snapshot b being the trunk's Y head at the Y sensors and its u head at
+ * the u sensors for noise sample b:
+ *   gp_eps : [G, min(S, B_r)] fp32 mixing weights (device), required when
+ *            lambda_gp > 0 (EINVAL if NULL); gp : [G] fp32 output P_g or NULL.
+ * P_g is added to L_D (loss[g][0]) and its gradient to gD; gT is unchanged.
+ * Everything else as pigan_trunk_step_grads.
+ */
+pigan_status pigan_trunk_step_grads_gp(const pigan_trunk_desc* s, const float* pT, const float* pD,
+                                       const float* z, const float* xc, const float* xsY,
+                                       const float* xsU, const float* f, float f_const,
+                                       const float* real, const float* w_group, const float* gp_eps,
+                                       float* gT, float* gD, float* loss, float* gp,
+                                       int32_t* nonfinite, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Domain decomposition (Sec. III.B.1): one generator pair for the whole

@@ -788,12 +788,13 @@ def trunk_snapshots(pT, shape, d, xsY, xsU, z):
 
 
 def train_step_group_trunk(gshape, dshape, d, pT, pD, z, xc, xsY, xsU, f, real,
-                           w=1.0, lambda_pde=1.0, chunk_S=None, prec=None):
+                           w=1.0, lambda_pde=1.0, chunk_S=None, prec=None, lambda_gp=0.0, gp_eps=None):
     """One group's losses and gradients with the shared-trunk generator.
 
-    Same losses as train_step_group; both heads come from one network, so one
-    gradient gT of L_G = L_adv + L_pde is returned.  Returns dict(L_D, L_adv,
-    L_pde, gT, gD)."""
+    Same losses as train_step_group (including its optional critic gradient
+    penalty on the pairs (F_b, R_b), b < min(S, B)); both heads come from one
+    network, so one gradient gT of L_G = L_adv + L_pde is returned.  Returns
+    dict(L_D, L_adv, L_pde, gT, gD, P_gp)."""
     z = np.asarray(z, F64)
     xc = np.asarray(xc, F64)
     f = np.asarray(f, F64)
@@ -805,12 +806,15 @@ def train_step_group_trunk(gshape, dshape, d, pT, pD, z, xc, xsY, xsU, f, real,
     if prec == "fp32":
         with _working_type(np.float32):
             return train_step_group_trunk(gshape, dshape, d, pT, pD, z, xc, xsY, xsU, f, real, w=w,
-                                          lambda_pde=lambda_pde, chunk_S=chunk_S, prec=None)
+                                          lambda_pde=lambda_pde, chunk_S=chunk_S, prec=None, lambda_gp=lambda_gp,
+                                          gp_eps=gp_eps)
     num = _Num(prec)
     gT = np.zeros(np.asarray(pT).size, F64)
     gD = np.zeros(np.asarray(pD).size, F64)
     sum_DF = 0.0
     sum_r2 = 0.0
+    P_gp = 0.0
+    n_gp = min(S, B)
     DR, hsR = mlp_forward(pD, dshape, real, keep=True, prec=num)
     gD += mlp_backward(pD, dshape, hsR, np.full(B, -w / B, F64), prec=num)
     sum_DR = DR.sum()
@@ -834,6 +838,13 @@ def train_step_group_trunk(gshape, dshape, d, pT, pD, z, xc, xsY, xsU, f, real,
         sum_DF += float(DF.sum())
         gDc, gF = mlp_backward(pD, dshape, hsF, np.full(Sc, w / S, F64), want_input_grad=True, prec=num)
         gD += gDc
+        if lambda_gp != 0.0:
+            b1 = min(n_gp, s0 + Sc)
+            if b1 > s0:
+                Pc, gPc = gradient_penalty(pD, dshape, F[:b1 - s0], real[s0:b1], np.asarray(gp_eps, F64)[s0:b1],
+                                           lambda_gp, w=w, n_total=n_gp, prec=num)
+                P_gp += Pc
+                gD += gPc
         gF = -gF
         q = 2.0 * w * lambda_pde * r / (S * P)
         eY = np.exp(jc["Y"])
@@ -844,15 +855,16 @@ def train_step_group_trunk(gshape, dshape, d, pT, pD, z, xc, xsY, xsU, f, real,
         gT += trunk_backward(pT, gshape, d, XY, ZY, fY_s, gY=gF[:, :nY].reshape(-1), prec=num)
         gT += trunk_backward(pT, gshape, d, XU, ZU, fU_s, gu=gF[:, nY:].reshape(-1), prec=num)
         gT += trunk_backward(pT, gshape, d, XC, ZC, jc, gY=g_Yval, gdY=g_Ydy, gdu=g_Udy, gddu=g_Uddy, prec=num)
-    L_D = w * (sum_DF / S - sum_DR / B)
+    L_D = w * (sum_DF / S - sum_DR / B) + P_gp
     L_adv = -w * sum_DF / S
     L_pde = w * lambda_pde * sum_r2 / (S * P)
-    return dict(L_D=L_D, L_adv=L_adv, L_pde=L_pde, gT=gT, gD=gD)
+    return dict(L_D=L_D, L_adv=L_adv, L_pde=L_pde, gT=gT, gD=gD, P_gp=P_gp)
 
 
-def train_step_trunk(wl, inp, real, lambda_pde=None, chunk_S=None, prec=None):
+def train_step_trunk(wl, inp, real, lambda_pde=None, chunk_S=None, prec=None, lambda_gp=0.0, gp_eps=None):
     """All groups of a trunk workload (inp.pT holds the trunk weights).
-    Returns loss [G, 3], gT [G, nT], gD [G, nD]."""
+    Returns loss [G, 3], gT [G, nT], gD [G, nD], P_gp [G] (gp_eps is
+    [G, min(S, B_r)] when lambda_gp > 0)."""
     lam = wl.lambda_pde if lambda_pde is None else lambda_pde
     gshape = (wl.d + wl.n_z, wl.L, wl.W)
     dshape = (wl.n_sY + wl.n_sU, wl.L_D, wl.W_D)
@@ -863,10 +875,12 @@ def train_step_trunk(wl, inp, real, lambda_pde=None, chunk_S=None, prec=None):
         f = inp.f[g] if inp.f is not None else np.full((S, P), inp.f_const)
         outs.append(train_step_group_trunk(gshape, dshape, wl.d, inp.pT[g], inp.pD[g], inp.z[g], inp.xc[g],
                                            inp.xsY[g], inp.xsU[g], f, real[g], w=float(inp.w_group[g]),
-                                           lambda_pde=lam, chunk_S=chunk_S, prec=prec))
+                                           lambda_pde=lam, chunk_S=chunk_S, prec=prec, lambda_gp=lambda_gp,
+                                           gp_eps=None if gp_eps is None else gp_eps[g]))
     return dict(loss=np.array([[o["L_D"], o["L_adv"], o["L_pde"]] for o in outs]),
                 gT=np.stack([o["gT"] for o in outs]),
-                gD=np.stack([o["gD"] for o in outs]))
+                gD=np.stack([o["gD"] for o in outs]),
+                P_gp=np.array([o["P_gp"] for o in outs]))
 
 
 def real_snapshots_trunk(wl, inp):

@@ -404,7 +404,9 @@ static int choose_chunk(const pigan_step_desc* s, bool trunk = false, bool hier 
   }
 }
 
-static pigan_status check_step(const pigan_step_desc* s, bool gp_entry = false) {
+// gp_name: the entry point that takes the penalty's mixing weights
+static pigan_status check_step(const pigan_step_desc* s, bool gp_entry = false,
+                               const char* gp_name = "pigan_train_step_grads_gp") {
   if (!s) return fail(PIGAN_EINVAL, "null step descriptor");
   pigan_status st;
   if ((st = check_mlp(&s->genY, "genY")) != PIGAN_OK) return st;
@@ -428,7 +430,7 @@ static pigan_status check_step(const pigan_step_desc* s, bool gp_entry = false) 
   if (!(s->lambda_gp >= 0.0f) || !__builtin_isfinite(s->lambda_gp))
     return fail(PIGAN_EINVAL, "lambda_gp must be finite and >= 0");
   if (!gp_entry && s->lambda_gp != 0.0f)
-    return fail(PIGAN_ENOTSUP, "lambda_gp != 0 needs the per-pair mixing weights: use pigan_train_step_grads_gp");
+    return fail(PIGAN_ENOTSUP, "lambda_gp != 0 needs the per-pair mixing weights: use %s", gp_name);
   if (!(s->loss_scale > 0.0f) || !__builtin_isfinite(s->loss_scale))
     return fail(PIGAN_EINVAL, "loss_scale must be finite and > 0");
   return PIGAN_OK;
@@ -710,10 +712,13 @@ static pigan_status disc_forward(void* ws, const DiscBuf& D, const float* pD, in
 // pass of a (value, tangent) jet of D seeded with (x_b, c_b), with cotangent
 // 1 on the tangent output.  Added to gD; the row terms go to acc[g][3].
 template <class T>
+// The fake snapshot of chunk sample i is read from the generators' sensor
+// outputs: Y values jY[i * ldY + j], u values jU[i * ldU + offU + j].
 static pigan_status critic_penalty(void* ws, const StepPlan& pl, const pigan_step_desc* s, const float* pD,
-                                   const NetBuf& Yc, const NetBuf& Uc, const float* real, const float* gp_eps,
-                                   const float* w_group, int b0, int n, float* gD, float inv, int32_t* nonfinite,
-                                   double* acc, int G, hipStream_t st) {
+                                   const float* jY, int64_t jy_g, const float* jU, int64_t ju_g, int ldY, int ldU,
+                                   int offU, const float* real, const float* gp_eps, const float* w_group, int b0,
+                                   int n, float* gD, float inv, int32_t* nonfinite, double* acc, int G,
+                                   hipStream_t st) {
   const DiscBuf& D = pl.D;
   const int WD = s->disc.width, LD = s->disc.n_hidden, n_in = s->disc.in_dim;
   const int64_t dact = D.Bmax * WD, xg = D.Bmax * D.Kp;
@@ -722,7 +727,7 @@ static pigan_status critic_penalty(void* ws, const StepPlan& pl, const pigan_ste
   pigan_status r;
   {
     ProfScope ps(st, "gp_misc", 0.0, 0.0);
-    HIP_TRY(launch_gp_mix<T>(tp<float>(ws, Yc.jet), Yc.R, tp<float>(ws, Uc.jet), Uc.R, s->n_sY, s->n_sU, real,
+    HIP_TRY(launch_gp_mix<T>(jY, jy_g, jU, ju_g, s->n_sY, s->n_sU, ldY, ldU, offU, real,
                              (int64_t)s->B_r * n_in, gp_eps, n_gp, b0, n, n_in, tp<T>(ws, D.X0), xg, D.Kp, G, st));
     HIP_TRY(launch_fill2(tp<float>(ws, D.seed), D.Bmax, n, 1.0f, 0.0f, 0, G, st));
   }
@@ -980,8 +985,10 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
     // critic gradient penalty on the pairs of this chunk's samples
     if (s->lambda_gp > 0.0f) {
       const int npair = std::min(std::min(S, s->B_r), s0 + Sc) - s0;
-      if (npair > 0 && (r = critic_penalty<T>(ws, pl, s, pD, Yc, Uc, real, gp_eps, w_group, s0, npair, gD, inv,
-                                              nonfinite, acc, G, st)) != PIGAN_OK)
+      const int ldY = pl.trunk ? n_s : s->n_sY, ldU = pl.trunk ? n_s : s->n_sU, offU = pl.trunk ? s->n_sY : 0;
+      if (npair > 0 && (r = critic_penalty<T>(ws, pl, s, pD, tp<float>(ws, Yc.jet), Yc.R, jetU, ju_g, ldY, ldU, offU,
+                                              real, gp_eps, w_group, s0, npair, gD, inv, nonfinite, acc, G, st)) !=
+                           PIGAN_OK)
         return r;
     }
     // generator reverse passes
@@ -1231,7 +1238,8 @@ static pigan_step_desc trunk_as_step(const pigan_trunk_desc* t) {
   pigan_step_desc s{};
   s.genY = t->trunk; s.genU = t->trunk; s.disc = t->disc;
   s.d = t->d; s.n_z = t->n_z; s.S = t->S; s.P = t->P; s.n_sY = t->n_sY; s.n_sU = t->n_sU; s.B_r = t->B_r;
-  s.chunk_S = t->chunk_S; s.dt = t->dt; s.lambda_pde = t->lambda_pde; s.lambda_gp = 0.0f; s.loss_scale = t->loss_scale;
+  s.chunk_S = t->chunk_S; s.dt = t->dt; s.lambda_pde = t->lambda_pde; s.lambda_gp = t->lambda_gp;
+  s.loss_scale = t->loss_scale;
   return s;
 }
 
@@ -1363,23 +1371,25 @@ int64_t pigan_trunk_param_count(const pigan_mlp* net) {
 size_t pigan_trunk_workspace_bytes(const pigan_trunk_desc* t) {
   if (!t) return 0;
   const pigan_step_desc s = trunk_as_step(t);
-  if (check_step(&s) != PIGAN_OK) return 0;
+  if (check_step(&s, true) != PIGAN_OK) return 0;   // accounts for the penalty's buffers when lambda_gp > 0
   StepPlan pl;
   plan_step(&s, choose_chunk(&s, true), pl, true);
   return pl.total;
 }
 
-pigan_status pigan_trunk_step_grads(const pigan_trunk_desc* t, const float* pT, const float* pD, const float* z,
-                                    const float* xc, const float* xsY, const float* xsU, const float* f, float f_const,
-                                    const float* real, const float* w_group, float* gT, float* gD, float* loss,
-                                    int32_t* nonfinite, void* ws, size_t ws_bytes, void* stream) {
+static pigan_status trunk_step_entry(const pigan_trunk_desc* t, const float* pT, const float* pD, const float* z,
+                                     const float* xc, const float* xsY, const float* xsU, const float* f,
+                                     float f_const, const float* real, const float* w_group, const float* gp_eps,
+                                     float* gT, float* gD, float* loss, float* gp, int32_t* nonfinite, void* ws,
+                                     size_t ws_bytes, void* stream, bool gp_entry) {
   g_err.clear();
   if (!t) return fail(PIGAN_EINVAL, "null trunk step descriptor");
   const pigan_step_desc s = trunk_as_step(t);
-  pigan_status st = check_step(&s);
+  pigan_status st = check_step(&s, gp_entry, "pigan_trunk_step_grads_gp");
   if (st != PIGAN_OK) return st;
   if (!pT || !pD || !z || !xc || !xsY || !xsU || !real || !gT || !gD || !loss || !nonfinite)
     return fail(PIGAN_EINVAL, "null input or output pointer");
+  if (s.lambda_gp > 0.0f && !gp_eps) return fail(PIGAN_EINVAL, "lambda_gp > 0 needs gp_eps");
   if (!__builtin_isfinite(f_const)) return fail(PIGAN_EINVAL, "f_const must be finite");
   StepPlan pl;
   plan_step(&s, choose_chunk(&s, true), pl, true);
@@ -1390,14 +1400,31 @@ pigan_status pigan_trunk_step_grads(const pigan_trunk_desc* t, const float* pT, 
   switch (s.dt) {
     case PIGAN_FP32:
       return run_step<float>(&s, pl, pT, nullptr, pD, z, xc, xsY, xsU, f, f_const, real, w_group, gT, nullptr, gD,
-                             loss, nonfinite, ws, hs, nullptr, nullptr);
+                             loss, nonfinite, ws, hs, gp_eps, gp);
     case PIGAN_BF16:
       return run_step<bf16>(&s, pl, pT, nullptr, pD, z, xc, xsY, xsU, f, f_const, real, w_group, gT, nullptr, gD,
-                            loss, nonfinite, ws, hs, nullptr, nullptr);
+                            loss, nonfinite, ws, hs, gp_eps, gp);
     default:
       return run_step<f16>(&s, pl, pT, nullptr, pD, z, xc, xsY, xsU, f, f_const, real, w_group, gT, nullptr, gD,
-                           loss, nonfinite, ws, hs, nullptr, nullptr);
+                           loss, nonfinite, ws, hs, gp_eps, gp);
   }
+}
+
+pigan_status pigan_trunk_step_grads(const pigan_trunk_desc* t, const float* pT, const float* pD, const float* z,
+                                    const float* xc, const float* xsY, const float* xsU, const float* f, float f_const,
+                                    const float* real, const float* w_group, float* gT, float* gD, float* loss,
+                                    int32_t* nonfinite, void* ws, size_t ws_bytes, void* stream) {
+  return trunk_step_entry(t, pT, pD, z, xc, xsY, xsU, f, f_const, real, w_group, nullptr, gT, gD, loss, nullptr,
+                          nonfinite, ws, ws_bytes, stream, false);
+}
+
+pigan_status pigan_trunk_step_grads_gp(const pigan_trunk_desc* t, const float* pT, const float* pD, const float* z,
+                                       const float* xc, const float* xsY, const float* xsU, const float* f,
+                                       float f_const, const float* real, const float* w_group, const float* gp_eps,
+                                       float* gT, float* gD, float* loss, float* gp, int32_t* nonfinite, void* ws,
+                                       size_t ws_bytes, void* stream) {
+  return trunk_step_entry(t, pT, pD, z, xc, xsY, xsU, f, f_const, real, w_group, gp_eps, gT, gD, loss, gp,
+                          nonfinite, ws, ws_bytes, stream, true);
 }
 
 pigan_status pigan_train_step_grads(const pigan_step_desc* s, const float* pY, const float* pU, const float* pD,

@@ -72,9 +72,10 @@ hipError_t launch_disc_seed(const float* score, int64_t sc_g, int n_fake, int n_
                             int G, hipStream_t st);
 int out_bwd_blocks(int64_t n_points, int ppb);
 template <class T>
-hipError_t launch_gp_mix(const float* yY, int64_t yY_g, const float* yU, int64_t yU_g, int nY, int nU,
-                         const float* real, int64_t real_g, const float* eps, int64_t eps_g, int b0, int n, int n_in,
-                         T* X, int64_t x_g, int ldx, int G, hipStream_t st);
+// fake row i: Y values yY[i * ldY + j], u values yU[i * ldU + offU + j]
+hipError_t launch_gp_mix(const float* yY, int64_t yY_g, const float* yU, int64_t yU_g, int nY, int nU, int ldY,
+                         int ldU, int offU, const float* real, int64_t real_g, const float* eps, int64_t eps_g, int b0,
+                         int n, int n_in, T* X, int64_t x_g, int ldx, int G, hipStream_t st);
 hipError_t launch_fill2(float* seed, int64_t s_g, int n, float v0, float v1, int two, int G, hipStream_t st);
 template <class T>
 hipError_t launch_gp_norm(const float* gin, int64_t g_g, int n, int n_in, const float* w_group, float scale,

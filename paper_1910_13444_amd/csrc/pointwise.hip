@@ -260,15 +260,16 @@ __global__ void k_snap_fill(const float* __restrict__ yY, int64_t yY_g, const fl
 // ---------------------------------------------------------------------------
 template <class T>
 __global__ void k_gp_mix(const float* __restrict__ yY, int64_t yY_g, const float* __restrict__ yU, int64_t yU_g,
-                         int nY, int nU, const float* __restrict__ real, int64_t real_g, const float* __restrict__ eps,
-                         int64_t eps_g, int b0, int n, int n_in, T* __restrict__ X, int64_t x_g, int ldx) {
+                         int nY, int nU, int ldY, int ldU, int offU, const float* __restrict__ real, int64_t real_g,
+                         const float* __restrict__ eps, int64_t eps_g, int b0, int n, int n_in, T* __restrict__ X,
+                         int64_t x_g, int ldx) {
   const int g = blockIdx.z;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (int64_t)n * ldx) return;
   const int i = (int)(idx / ldx), j = (int)(idx % ldx);
   float v = 0.0f;
   if (j < n_in) {
-    const float f = j < nY ? yY[g * yY_g + (int64_t)i * nY + j] : yU[g * yU_g + (int64_t)i * nU + (j - nY)];
+    const float f = j < nY ? yY[g * yY_g + (int64_t)i * ldY + j] : yU[g * yU_g + (int64_t)i * ldU + offU + (j - nY)];
     const float r = real[g * real_g + (int64_t)(b0 + i) * n_in + j];
     const float e = eps[g * eps_g + b0 + i];
     v = e * r + (1.0f - e) * f;
@@ -1017,13 +1018,13 @@ hipError_t launch_snap_fill_rows(const float* yY, int64_t yY_g, const float* yU,
 }
 
 template <class T>
-hipError_t launch_gp_mix(const float* yY, int64_t yY_g, const float* yU, int64_t yU_g, int nY, int nU,
-                         const float* real, int64_t real_g, const float* eps, int64_t eps_g, int b0, int n, int n_in,
-                         T* X, int64_t x_g, int ldx, int G, hipStream_t st) {
+hipError_t launch_gp_mix(const float* yY, int64_t yY_g, const float* yU, int64_t yU_g, int nY, int nU, int ldY,
+                         int ldU, int offU, const float* real, int64_t real_g, const float* eps, int64_t eps_g, int b0,
+                         int n, int n_in, T* X, int64_t x_g, int ldx, int G, hipStream_t st) {
   const int64_t tot = (int64_t)n * ldx;
   if (tot <= 0) return hipSuccess;
-  k_gp_mix<T><<<dim3(nblk(tot, 256), 1, G), 256, 0, st>>>(yY, yY_g, yU, yU_g, nY, nU, real, real_g, eps, eps_g, b0,
-                                                          n, n_in, X, x_g, ldx);
+  k_gp_mix<T><<<dim3(nblk(tot, 256), 1, G), 256, 0, st>>>(yY, yY_g, yU, yU_g, nY, nU, ldY, ldU, offU, real, real_g,
+                                                          eps, eps_g, b0, n, n_in, X, x_g, ldx);
   return hipGetLastError();
 }
 
@@ -1194,9 +1195,9 @@ hipError_t launch_cast(const float* src, int64_t s_g, int N, int K, int Kp, T* d
                                                int, const float*, int64_t, int, int, T*, int64_t, int, int,     \
                                                hipStream_t);                                                    \
   template hipError_t launch_first_bwd<T>(const FirstBwdArgs<T>&, int, hipStream_t);                          \
-  template hipError_t launch_gp_mix<T>(const float*, int64_t, const float*, int64_t, int, int, const float*,    \
-                                       int64_t, const float*, int64_t, int, int, int, T*, int64_t, int, int,   \
-                                       hipStream_t);                                                            \
+  template hipError_t launch_gp_mix<T>(const float*, int64_t, const float*, int64_t, int, int, int, int, int,  \
+                                       const float*, int64_t, const float*, int64_t, int, int, int, T*, int64_t, \
+                                       int, int, hipStream_t);                                                  \
   template hipError_t launch_gp_norm<T>(const float*, int64_t, int, int, const float*, float, double*, int64_t, \
                                         T*, int64_t, int, int, hipStream_t);                                    \
   template hipError_t launch_cast<T>(const float*, int64_t, int, int, int, T*, T*, int64_t, int, hipStream_t);

@@ -48,7 +48,8 @@ class TrunkDesc(C.Structure):
     _fields_ = [("trunk", Mlp), ("disc", Mlp),
                 ("d", C.c_int32), ("n_z", C.c_int32), ("S", C.c_int32), ("P", C.c_int32),
                 ("n_sY", C.c_int32), ("n_sU", C.c_int32), ("B_r", C.c_int32), ("chunk_S", C.c_int32),
-                ("dt", C.c_int32), ("lambda_pde", C.c_float), ("loss_scale", C.c_float)]
+                ("dt", C.c_int32), ("lambda_pde", C.c_float), ("loss_scale", C.c_float),
+                ("lambda_gp", C.c_float)]
 
 
 class HierDesc(C.Structure):
@@ -103,6 +104,7 @@ def lib():
         "pigan_trunk_param_count": (i64, [P]),
         "pigan_trunk_workspace_bytes": (sz, [P]),
         "pigan_trunk_step_grads": (i32, [P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, sz, P]),
+        "pigan_trunk_step_grads_gp": (i32, [P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, P, sz, P]),
         "pigan_last_error": (C.c_char_p, []),
         "pigan_profile_enable": (i32, [i32]),
         "pigan_profile_read": (i32, [P, i32, P]),
@@ -285,12 +287,13 @@ class TrainStep:
 
 
 def trunk_desc(wl: Workload, S: int | None = None, B_r: int | None = None, chunk_S: int = 0,
-               dtype: str | None = None, lambda_pde: float | None = None, loss_scale: float = 1.0) -> TrunkDesc:
+               dtype: str | None = None, lambda_pde: float | None = None, loss_scale: float = 1.0,
+               lambda_gp: float = 0.0) -> TrunkDesc:
     S = wl.S if S is None else S
     B_r = wl.B_r if B_r is None else B_r
     return TrunkDesc(Mlp(wl.G, wl.in_dim, wl.L, wl.W), Mlp(wl.G, wl.n_in, wl.L_D, wl.W_D), wl.d, wl.n_z, S, wl.P,
                      wl.n_sY, wl.n_sU, B_r, chunk_S, DTYPES[dtype or wl.dtype],
-                     wl.lambda_pde if lambda_pde is None else lambda_pde, loss_scale)
+                     wl.lambda_pde if lambda_pde is None else lambda_pde, loss_scale, lambda_gp)
 
 
 def trunk_workspace_bytes(desc: TrunkDesc) -> int:
@@ -303,6 +306,7 @@ class TrunkOut:
     gD: torch.Tensor
     loss: torch.Tensor
     nonfinite: torch.Tensor
+    gp: torch.Tensor | None = None    # [G] gradient penalty (when lambda_gp > 0)
 
 
 class TrunkStep:
@@ -321,19 +325,26 @@ class TrunkStep:
         self.ws = _workspace(need, self.device)
         f32 = dict(dtype=torch.float32, device=self.device)
         self.out = TrunkOut(torch.empty((G, self.nT), **f32), torch.empty((G, self.nD), **f32),
-                            torch.empty((G, 3), **f32), torch.zeros((1,), dtype=torch.int32, device=self.device))
+                            torch.empty((G, 3), **f32), torch.zeros((1,), dtype=torch.int32, device=self.device),
+                            torch.empty((G,), **f32) if desc.lambda_gp > 0 else None)
 
-    def __call__(self, pT, pD, z, xc, xsY, xsU, real, f=None, f_const=0.0, w_group=None) -> TrunkOut:
+    def __call__(self, pT, pD, z, xc, xsY, xsU, real, f=None, f_const=0.0, w_group=None, gp_eps=None) -> TrunkOut:
         d = self.desc
         G, S, Pn = d.trunk.n_groups, d.S, d.P
         o = self.out
-        st = lib().pigan_trunk_step_grads(
-            C.byref(d), _ptr(pT, "pT", G * self.nT), _ptr(pD, "pD", G * self.nD), _ptr(z, "z", G * S * d.n_z),
-            _ptr(xc, "xc", G * S * Pn * d.d), _ptr(xsY, "xsY", G * d.n_sY * d.d), _ptr(xsU, "xsU", G * d.n_sU * d.d),
-            _ptr(f, "f", G * S * Pn), float(f_const), _ptr(real, "real", G * d.B_r * (d.n_sY + d.n_sU)),
-            _ptr(w_group, "w_group", G), _ptr(o.gT, "gT"), _ptr(o.gD, "gD"), _ptr(o.loss, "loss"),
-            _ptr(o.nonfinite, "nonfinite", 1, dtype=torch.int32), _ptr(self.ws, "ws", dtype=torch.uint8),
-            self.ws_bytes, _stream())
+        args = [C.byref(d), _ptr(pT, "pT", G * self.nT), _ptr(pD, "pD", G * self.nD), _ptr(z, "z", G * S * d.n_z),
+                _ptr(xc, "xc", G * S * Pn * d.d), _ptr(xsY, "xsY", G * d.n_sY * d.d),
+                _ptr(xsU, "xsU", G * d.n_sU * d.d), _ptr(f, "f", G * S * Pn), float(f_const),
+                _ptr(real, "real", G * d.B_r * (d.n_sY + d.n_sU)), _ptr(w_group, "w_group", G)]
+        tail = [_ptr(o.nonfinite, "nonfinite", 1, dtype=torch.int32), _ptr(self.ws, "ws", dtype=torch.uint8),
+                self.ws_bytes, _stream()]
+        if d.lambda_gp > 0:
+            eps = _ptr(gp_eps, "gp_eps", G * min(S, d.B_r))
+            st = lib().pigan_trunk_step_grads_gp(*args, eps, _ptr(o.gT, "gT"), _ptr(o.gD, "gD"),
+                                                 _ptr(o.loss, "loss"), _ptr(o.gp, "gp", G), *tail)
+        else:
+            st = lib().pigan_trunk_step_grads(*args, _ptr(o.gT, "gT"), _ptr(o.gD, "gD"), _ptr(o.loss, "loss"),
+                                              *tail)
         _check(st)
         return o
 

@@ -115,19 +115,23 @@ def trunk_slices(in_dim, L, W):
     return out
 
 
-def run_trunk_gpu(wl, inp, real, chunk_S=0, dtype=None, loss_scale=1.0):
-    """One training step through pigan_trunk_step_grads; returns numpy outputs."""
+def run_trunk_gpu(wl, inp, real, chunk_S=0, dtype=None, loss_scale=1.0, lambda_gp=0.0, gp_eps=None):
+    """One training step through pigan_trunk_step_grads (or, with lambda_gp >
+    0, pigan_trunk_step_grads_gp); returns numpy outputs."""
     import torch
     from paper_1910_13444_amd import pigan
     desc = pigan.trunk_desc(wl, S=inp.z.shape[1], B_r=real.shape[1], chunk_S=chunk_S, dtype=dtype,
-                            loss_scale=loss_scale)
+                            loss_scale=loss_scale, lambda_gp=lambda_gp)
     step = pigan.TrunkStep(desc)
     o = step(to_dev(inp.pT), to_dev(inp.pD), to_dev(inp.z), to_dev(inp.xc), to_dev(inp.xsY), to_dev(inp.xsU),
              to_dev(real), f=None if inp.f is None else to_dev(inp.f), f_const=inp.f_const,
-             w_group=to_dev(inp.w_group))
+             w_group=to_dev(inp.w_group), gp_eps=None if gp_eps is None else to_dev(gp_eps))
     torch.cuda.synchronize()
-    return dict(gT=o.gT.cpu().numpy(), gD=o.gD.cpu().numpy(), loss=o.loss.cpu().numpy(),
-                nonfinite=int(o.nonfinite.cpu().item()))
+    out = dict(gT=o.gT.cpu().numpy(), gD=o.gD.cpu().numpy(), loss=o.loss.cpu().numpy(),
+               nonfinite=int(o.nonfinite.cpu().item()))
+    if o.gp is not None:
+        out["P_gp"] = o.gp.cpu().numpy()
+    return out
 
 
 def trunk_errors(wl, out, ref):

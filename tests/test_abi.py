@@ -247,3 +247,21 @@ def test_hier_trunk_step_validation():
     e.trunk.in_dim = wl.in_dim + 1
     assert _hier_trunk(e, 1 << 40) == pigan.EINVAL
     assert pigan.lib().pigan_hier_trunk_step_grads(None, *([None] * 7), 0.0, *([None] * 10), 0, None) == pigan.EINVAL
+
+
+def test_trunk_gradient_penalty_validation():
+    wl = configs.T5
+    d = pigan.trunk_desc(wl, lambda_gp=10.0)
+    need = int(pigan.lib().pigan_trunk_workspace_bytes(C.byref(d)))
+    plain = int(pigan.lib().pigan_trunk_workspace_bytes(C.byref(pigan.trunk_desc(wl))))
+    assert need > plain > 0                                # the penalty's buffers
+    args = (C.byref(d), *([FAKE] * 7), 0.0, FAKE, FAKE)
+    # the plain entry refuses a penalty, the penalty entry needs the mixing weights
+    assert pigan.lib().pigan_trunk_step_grads(*args, FAKE, FAKE, FAKE, FAKE, FAKE, need, None) == pigan.ENOTSUP
+    assert pigan.lib().pigan_trunk_step_grads_gp(*args, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need,
+                                                 None) == pigan.EINVAL
+    e = pigan.trunk_desc(wl, lambda_gp=-1.0)
+    assert pigan.lib().pigan_trunk_step_grads_gp(C.byref(e), *([FAKE] * 7), 0.0, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                                 FAKE, FAKE, FAKE, FAKE, need, None) == pigan.EINVAL
+    assert pigan.lib().pigan_trunk_step_grads(*args, FAKE, FAKE, FAKE, FAKE, FAKE, need, None) == pigan.ENOTSUP
+    assert b"pigan_trunk_step_grads_gp" in pigan.lib().pigan_last_error()

@@ -11,7 +11,7 @@ import oracle
 from paper_1910_13444_amd import configs
 from paper_1910_13444_amd.configs import Workload
 from paper_1910_13444_amd.inputs import make_inputs
-from _parity import TOL, check, check_conditioned, run_trunk_gpu, trunk_errors
+from _parity import TOL, check, check_conditioned, rel, run_trunk_gpu, trunk_errors
 
 pytestmark = pytest.mark.gpu
 
@@ -68,3 +68,38 @@ def test_trunk_chunking_matches_unchunked():
         err = np.abs(a[k] - b[k]).max() / max(1e-30, np.abs(a[k]).max())
         print(f"chunking {k}: {err:.3g}")
         assert err <= 1e-5
+
+
+GP_CASES = {
+    "tiny_trunk_gp_fp32": TTG.with_(S=3, B_r=3, seed=33),
+    "t5_S3_gp_bf16": configs.T5.with_(S=3, P=256, B_r=3, seed=34),
+    "t5_groups_gp_S2_fp32": configs.C4.with_(arch="trunk", L=5, S=2, P=64, B_r=2, dtype="fp32", seed=35),
+}
+
+
+@pytest.mark.parametrize("case", list(GP_CASES))
+def test_trunk_step_with_gradient_penalty(case):
+    """pigan_trunk_step_grads_gp: critic gradients, L_D (with the penalty) and
+    the penalty against the oracle; the trunk gradient is the plain step's,
+    bit for bit."""
+    wl = GP_CASES[case]
+    _say(f"trunk gradient penalty case={case} dtype={wl.dtype} G={wl.G} L={wl.L} W={wl.W} S={wl.S}")
+    inp = make_inputs(wl)
+    real = oracle.real_snapshots_trunk(wl, inp)
+    eps = np.random.default_rng(wl.seed + 5).random((wl.G, min(wl.S, wl.B_r))).astype(np.float32)
+    lam = 10.0
+    ref = oracle.train_step_trunk(wl, inp, real, lambda_gp=lam, gp_eps=eps)
+    out = run_trunk_gpu(wl, inp, real, lambda_gp=lam, gp_eps=eps)
+    plain = run_trunk_gpu(wl, inp, real)
+    assert out["nonfinite"] == 0 and np.all(ref["P_gp"] > 0)
+    np.testing.assert_array_equal(out["gT"], plain["gT"])
+    errs = trunk_errors(wl, out, ref)
+    errs["P_gp"] = rel(out["P_gp"], ref["P_gp"])
+    tol = TOL[wl.dtype]
+    if max(errs.values()) <= tol:
+        check(errs, tol, case)
+        return
+    model = oracle.train_step_trunk(wl, inp, real, prec=wl.dtype, lambda_gp=lam, gp_eps=eps)
+    merr = trunk_errors(wl, model, ref)
+    merr["P_gp"] = rel(model["P_gp"], ref["P_gp"])
+    check_conditioned(errs, merr, tol, case)

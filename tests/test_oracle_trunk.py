@@ -223,3 +223,33 @@ def test_trunk_chunking():
     b = oracle.train_step_trunk(wl, inp, real, chunk_S=1)
     for k in ("loss", "gT", "gD"):
         assert np.allclose(a[k], b[k], rtol=1e-12, atol=1e-14)
+
+
+def test_trunk_step_with_gradient_penalty_fd():
+    """The critic gradient penalty with the trunk's snapshots: central
+    differences of L_D (with P) in every critic weight, the trunk gradient
+    unchanged by the penalty, and P > 0 added to L_D."""
+    wl = TT.with_(B_r=3, S=3, seed=7)
+    inp = make_inputs(wl)
+    real = oracle.real_snapshots_trunk(wl, inp)
+    eps = np.random.default_rng(5).random((1, min(wl.S, wl.B_r)))
+    pD0 = inp.pD[0].astype(np.float64)
+    lam = 3.0
+    o = oracle.train_step_trunk(wl, inp, real, lambda_gp=lam, gp_eps=eps)
+    o0 = oracle.train_step_trunk(wl, inp, real)
+    assert o["P_gp"][0] > 1e-6
+    assert np.isclose(o["loss"][0, 0], o0["loss"][0, 0] + o["P_gp"][0], rtol=1e-13)
+    assert np.array_equal(o["gT"], o0["gT"])
+    h = 1e-6
+    fd = np.zeros_like(pD0)
+    for k in range(pD0.size):
+        e = np.zeros_like(pD0)
+        e[k] = h
+        inp.pD = (pD0 + e)[None]
+        lp = oracle.train_step_trunk(wl, inp, real, lambda_gp=lam, gp_eps=eps)["loss"][0, 0]
+        inp.pD = (pD0 - e)[None]
+        lm = oracle.train_step_trunk(wl, inp, real, lambda_gp=lam, gp_eps=eps)["loss"][0, 0]
+        fd[k] = (lp - lm) / (2 * h)
+    gD = o["gD"][0]
+    assert np.abs(gD - fd).max() <= 1e-6 * max(1.0, np.abs(fd).max())
+    assert np.abs(gD - o0["gD"][0]).max() > 1e-4      # the penalty moved the critic gradient
