@@ -244,7 +244,7 @@ def main():
 
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print(f"bench.py measures one GPU only: the PI-GAN step is built and timed on a single MI355X "
-              f"(requested --gpus {a.gpus}); multi-GPU runs are not part of this build.", file=sys.stderr)
+              f"(requested --gpus {a.gpus}); multi-GPU execution is not implemented.", file=sys.stderr)
         sys.exit(2)
 
     import torch
