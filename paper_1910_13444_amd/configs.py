@@ -131,9 +131,15 @@ H2 = C2.with_(name="hier21_darcy2d_bf16", n_sY=256, n_sU=256, lambda_pde=0.0, ar
 # the same 1 + 4 + 16 subdomain critics.
 HT5 = H2.with_(name="hier21_trunk5x128_darcy2d_bf16", L=5, arch="hier_trunk", seed=1932)
 
-WORKLOADS = {w.name: w for w in (C1, C2, C3, C4, C5, C5H, T5, T11, T21, H2, HT5)}
+# A hierarchy at the scale of the paper's finest level (hundreds of
+# subdomains): 1 + 16 + 256 critics of 3 x 256, each on 4 Y + 4 u sensors and
+# 4 free sensors of its subdomain (coarse levels take evenly spaced cells).
+H273 = H2.with_(name="hier273_darcy2d_bf16", n_sY=1024, n_sU=1024, sides=(1, 4, 16), m_sensors=4, n_free=4,
+                seed=1933)
+
+WORKLOADS = {w.name: w for w in (C1, C2, C3, C4, C5, C5H, T5, T11, T21, H2, HT5, H273)}
 ALIASES = {"c1": C1, "c2": C2, "c3": C3, "c4": C4, "c5": C5, "c5h": C5H, "t5": T5, "t11": T11, "t21": T21,
-           "h2": H2, "ht5": HT5}
+           "h2": H2, "ht5": HT5, "h273": H273}
 
 
 def get(name: str) -> Workload:

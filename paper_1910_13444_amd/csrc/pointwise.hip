@@ -663,33 +663,71 @@ __global__ void k_hier_snap(HierSnap h, int n_fake, const float* __restrict__ re
   X[k * x_g + idx] = Elem<T>::from_f(v);
 }
 
-// One block per sample b.  A thread owns targets (Y sensors, u sensors,
-// collocation points of the sample) and adds every critic input read from it,
-// in the order critic k, then input j: a fixed order, so indices repeated
-// within or across critics add up deterministically.  The index lists and the
-// sample's cotangent rows are uniform across the block (scalar loads).
-// Coordinates carry no cotangent.
-__device__ __forceinline__ void hier_gather(const int32_t* __restrict__ idx, int m, const float* __restrict__ rows,
-                                            int64_t row_g, int D, int n_t, float* __restrict__ dst) {
-  for (int t = threadIdx.x; t < n_t; t += blockDim.x) {
-    float acc = dst[t];
-    for (int k = 0; k < D; ++k) {
-      const int32_t* ik = idx + (int64_t)k * m;
-      const float* rk = rows + k * row_g;
-      for (int j = 0; j < m; ++j)
-        if (ik[j] == t) acc += rk[j];
-    }
-    dst[t] = acc;
-  }
-}
+// One block per sample b.  Its targets -- Y sensors, u sensors, then the
+// sample's collocation points -- are owned round-robin by the threads (slot t
+// of a tile by thread t % HS_NTH).  The critic inputs of one index list are
+// staged through LDS in chunks (target and cotangent of each input, in the
+// order critic k, then input j); every thread then walks the chunk and adds
+// the inputs read from its own targets into its LDS slots, so each target
+// accumulates in (k, j) order and no two threads touch one slot.  The cost is
+// one pass over the inputs per tile of targets, whatever the number of
+// critics.  Coordinates carry no cotangent.
+constexpr int HS_TILE = 8192, HS_NTH = 256, HS_CHUNK = 2048;
 
-__global__ void k_hier_scatter(HierSnap h, const float* __restrict__ dX, int64_t dx_g, int ldx, int D,
-                               float* __restrict__ gY, float* __restrict__ gU, float* __restrict__ gN) {
+__global__ void __launch_bounds__(HS_NTH)
+k_hier_scatter(HierSnap h, const float* __restrict__ dX, int64_t dx_g, int ldx, int D, float* __restrict__ gY,
+               float* __restrict__ gU, float* __restrict__ gN) {
+  __shared__ float acc[HS_TILE];
+  __shared__ __attribute__((aligned(16))) int etgt[HS_CHUNK];
+  __shared__ __attribute__((aligned(16))) float eval[HS_CHUNK];
   const int b = blockIdx.x;
+  const int tid = threadIdx.x;
   const float* row = dX + (int64_t)b * ldx;
-  hier_gather(h.idxY, h.mY, row, dx_g, D, h.nsY, gY + (int64_t)b * h.ldY);
-  hier_gather(h.idxU, h.mU, row + h.mY, dx_g, D, h.nsU, gU + (int64_t)b * h.ldU + h.offU);
-  hier_gather(h.idxF, h.nF, row + h.mY + h.mU, dx_g, D, h.P, gN + (int64_t)b * h.P);
+  const int nT = h.nsY + h.nsU + h.P;
+  auto target = [&](int t) -> float* {
+    if (t < h.nsY) return gY + (int64_t)b * h.ldY + t;
+    if (t < h.nsY + h.nsU) return gU + (int64_t)b * h.ldU + h.offU + (t - h.nsY);
+    return gN + (int64_t)b * h.P + (t - h.nsY - h.nsU);
+  };
+  for (int t0 = 0; t0 < nT; t0 += HS_TILE) {
+    const int len = t0 + HS_TILE < nT ? HS_TILE : nT - t0;
+    for (int t = tid; t < len; t += HS_NTH) acc[t] = *target(t0 + t);
+    // inputs of list `idx` (m per critic, columns col0.. of the rows) read
+    // from targets base + i, i in [0, n)
+    auto pass = [&](const int32_t* __restrict__ idx, int m, int col0, int n, int base) {
+      const int total = D * m;
+      for (int c0 = 0; c0 < total; c0 += HS_CHUNK) {
+        const int cnt = c0 + HS_CHUNK < total ? HS_CHUNK : total - c0;
+        __syncthreads();                           // the previous chunk is consumed
+        for (int q = tid; q < cnt; q += HS_NTH) {
+          const int e = c0 + q, k = e / m, j = e - k * m;
+          const int i = idx[e];
+          etgt[q] = (i >= 0 && i < n) ? base + i - t0 : -1;
+          eval[q] = row[k * dx_g + col0 + j];
+        }
+        for (int q = cnt + tid; q < ((cnt + 3) & ~3); q += HS_NTH) etgt[q] = -1;   // pad to a multiple of 4
+        __syncthreads();
+        // four inputs per LDS read (all lanes read the same words), several reads in flight
+#pragma unroll 4
+        for (int q = 0; q < cnt; q += 4) {
+          const int4 t4 = *(const int4*)(etgt + q);
+          const float4 v4 = *(const float4*)(eval + q);
+          const int tt[4] = {t4.x, t4.y, t4.z, t4.w};
+          const float vv[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int t = tt[u];
+            if (t >= 0 && t < len && (t & (HS_NTH - 1)) == tid) acc[t] += vv[u];
+          }
+        }
+      }
+    };
+    pass(h.idxY, h.mY, 0, h.nsY, 0);
+    pass(h.idxU, h.mU, h.mY, h.nsU, h.nsY);
+    pass(h.idxF, h.nF, h.mY + h.mU, h.P, h.nsY + h.nsU);
+    for (int t = tid; t < len; t += HS_NTH) *target(t0 + t) = acc[t];
+    __syncthreads();                               // before the next tile's staging
+  }
 }
 
 __global__ void k_hier_pde_loss(const double* __restrict__ acc, int slot, float lambda_pde, int64_t SP, float* loss,
@@ -1103,7 +1141,7 @@ hipError_t launch_hier_snap(const HierSnap& h, int n_fake, const float* real, in
 hipError_t launch_hier_scatter(const HierSnap& h, const float* dX, int64_t dx_g, int ldx, int n_fake, int D,
                                float* gY, float* gU, float* gN, hipStream_t st) {
   if (n_fake <= 0 || D <= 0) return hipSuccess;
-  k_hier_scatter<<<n_fake, 256, 0, st>>>(h, dX, dx_g, ldx, D, gY, gU, gN);
+  k_hier_scatter<<<n_fake, HS_NTH, 0, st>>>(h, dX, dx_g, ldx, D, gY, gU, gN);
   return hipGetLastError();
 }
 

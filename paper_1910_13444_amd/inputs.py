@@ -147,22 +147,40 @@ def _cells_of(side: int, fine: int, ci: int, cj: int) -> list[int]:
     return [(ci * r + a) * fine + (cj * r + b) for a in range(r) for b in range(r)]
 
 
+def _pick(side: int, fine: int, ci: int, cj: int, m: int, per_cell: int) -> list[int]:
+    """m indices (sensors or points, per_cell per finest cell) spread evenly
+    over subdomain (ci, cj): m / k from each of its k cells when m >= k, else
+    the first one of every cell of an evenly spaced q x q sub-grid (m = q^2)."""
+    cells = _cells_of(side, fine, ci, cj)
+    k = len(cells)
+    if m >= k:
+        if m % k or m // k > per_cell:
+            raise ValueError("sensor or point counts do not divide over the subdomain's cells")
+        return [c * per_cell + j for c in cells for j in range(m // k)]
+    r = fine // side
+    q = int(round(m ** 0.5))
+    if q * q != m or r % q:
+        raise ValueError("a subdomain with more cells than picks needs a square pick count dividing its side")
+    st = r // q
+    return [((ci * r + a * st + st // 2) * fine + (cj * r + b * st + st // 2)) * per_cell
+            for a in range(q) for b in range(q)]
+
+
 def make_hierarchy(sides, m_sensors: int, n_free: int, per_cell_sensors: int, per_cell_points: int) -> Hierarchy:
     """Index lists of every subdomain's discriminator.  Sensors of finest cell
     c are c * per_cell_sensors + [0, per_cell_sensors); points of cell c are
     c * per_cell_points + [0, per_cell_points).  A subdomain covering k cells
-    takes m_sensors / k sensors and n_free / k points from each (the first ones)."""
+    takes m_sensors / k sensors and n_free / k points from each (the first
+    ones), or, when it has more cells than picks, one from each cell of an
+    evenly spaced sub-grid (so hundreds of finest subdomains still leave the
+    coarse critics a modest input)."""
     fine = sides[-1]
     idxY, idxF, w, level = [], [], [], []
     for lv, side in enumerate(sides):
         for ci in range(side):
             for cj in range(side):
-                cells = _cells_of(side, fine, ci, cj)
-                k = len(cells)
-                if m_sensors % k or n_free % k or m_sensors // k > per_cell_sensors or n_free // k > per_cell_points:
-                    raise ValueError("sensor or point counts do not divide over the subdomain's cells")
-                idxY.append([c * per_cell_sensors + j for c in cells for j in range(m_sensors // k)])
-                idxF.append([c * per_cell_points + j for c in cells for j in range(n_free // k)])
+                idxY.append(_pick(side, fine, ci, cj, m_sensors, per_cell_sensors))
+                idxF.append(_pick(side, fine, ci, cj, n_free, per_cell_points))
                 w.append(1.0 / (len(sides) * side * side))
                 level.append(lv)
     idxY = np.array(idxY, np.int32)

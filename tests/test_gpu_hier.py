@@ -25,6 +25,11 @@ CASES = {
                       16, 1.0, 0.0),
     "c3_1x2_bf16": (configs.C3.with_(n_sY=64, n_sU=64, S=2, P=128, B_r=2, L=4, W_D=512, L_D=2, seed=84), (1, 2), 16,
                     8, 0.0, 0.0),
+    # 1 + 16 + 64 critics; the coarse ones take evenly spaced cells
+    "c2_1x4x8_81critics_fp32": (configs.C2.with_(n_sY=256, n_sU=256, S=3, P=256, B_r=3, dtype="fp32", seed=90),
+                                (1, 4, 8), 4, 4, 0.5, 0.2),
+    "c2_1x4x8_81critics_bf16": (configs.C2.with_(n_sY=256, n_sU=256, S=4, P=256, B_r=4, seed=91), (1, 4, 8), 4, 4,
+                                0.0, 0.0),
 }
 
 
