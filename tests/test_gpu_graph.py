@@ -56,3 +56,49 @@ def test_graph_replays_match_eager(dtype, chunk):
     for a, b in zip(_outs(step.out), ref):
         assert torch.equal(a, b)
     assert not torch.equal(ref[2], eager[2])
+
+
+def test_graph_replays_trunk_and_hierarchy():
+    """The same for the shared-trunk step and the domain-decomposition step
+    (grouped critic launches, the snapshot gather and the cotangent scatter)."""
+    from paper_1910_13444_amd.inputs import make_hier_inputs
+    print("graph replay: trunk 5x128 and 1 + 4 + 16 critic hierarchy, bf16", flush=True)
+    wl = configs.T5.with_(S=3, P=256, B_r=3, seed=62)
+    inp = make_inputs(wl)
+    real = oracle.real_snapshots_trunk(wl, inp)
+    dt = dict(pT=to_dev(inp.pT), pD=to_dev(inp.pD), z=to_dev(inp.z), xc=to_dev(inp.xc), xsY=to_dev(inp.xsY),
+              xsU=to_dev(inp.xsU), real=to_dev(real), w=to_dev(inp.w_group))
+    tstep = pigan.TrunkStep(pigan.trunk_desc(wl))
+
+    def tcall():
+        return tstep(dt["pT"], dt["pD"], dt["z"], dt["xc"], dt["xsY"], dt["xsU"], dt["real"], f_const=wl.f_const,
+                     w_group=dt["w"])
+
+    wh = configs.H2.with_(S=3, P=1024, B_r=3, seed=63)
+    hi = make_hier_inputs(wh, sides=wh.sides, m_sensors=wh.m_sensors, n_free=wh.n_free)
+    b, h = hi.base, hi.hier
+    realh = oracle.real_snapshots_hier(wh, hi)
+
+    def ti(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+    dh = dict(pY=to_dev(b.pY[0]), pU=to_dev(b.pU[0]), pD=to_dev(hi.pD), z=to_dev(b.z[0]), xc=to_dev(b.xc[0]),
+              xsY=to_dev(b.xsY[0]), xsU=to_dev(b.xsU[0]), iY=ti(h.idxY), iU=ti(h.idxU), iF=ti(h.idxF),
+              real=to_dev(realh), w=to_dev(h.w))
+    hstep = pigan.HierStep(pigan.hier_desc(wh, h.D, wh.m_sensors, wh.m_sensors, wh.n_free, lambda_pde=0.5))
+
+    def hcall():
+        return hstep(dh["pY"], dh["pU"], dh["pD"], dh["z"], dh["xc"], dh["xsY"], dh["xsU"], dh["iY"], dh["iU"],
+                     dh["iF"], dh["real"], dh["w"])
+
+    for call, names in ((tcall, ("gT", "gD", "loss", "nonfinite")), (hcall, ("gY", "gU", "gD", "loss", "nonfinite"))):
+        o = call()
+        eager = [getattr(o, k).detach().cpu().clone() for k in names]
+        g = pigan.StepGraph(call)
+        for rep in range(3):
+            for k in names[:-1]:
+                getattr(o, k).fill_(float("nan"))
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            for k, e in zip(names, eager):
+                assert torch.equal(getattr(o, k).cpu(), e), f"{k}: replay {rep} differs from the eager call"
