@@ -143,7 +143,7 @@ pigan_status pigan_disc_forward(const pigan_mlp* net, const float* params, const
  * gU = d(L_adv + L_pde)/d(u params).  Gradients are OVERWRITTEN (not
  * accumulated).  The step is exactly additive over noise samples, so the
  * library processes samples in chunks of chunk_S (0 = the largest chunk whose
- * workspace stays within 64 GiB); the result does not depend on the chunking
+ * workspace stays within 128 GiB); the result does not depend on the chunking
  * up to fp32 summation order.
  */
 typedef struct {

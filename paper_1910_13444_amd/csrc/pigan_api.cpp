@@ -390,7 +390,10 @@ static void plan_hier(const pigan_step_desc* s, int Sc, StepPlan& pl, bool trunk
   pl.total = round_up((int64_t)cv.off, 256);
 }
 
-static const size_t kAutoCap = (size_t)64 << 30;
+// automatic chunking: the largest power-of-two share of the samples whose
+// workspace fits in 128 GiB (under half of the 288 GB of HBM; larger chunks
+// mean fewer, longer launches and fewer partial reductions)
+static const size_t kAutoCap = (size_t)128 << 30;
 
 static int choose_chunk(const pigan_step_desc* s, bool trunk = false, bool hier = false) {
   if (s->chunk_S > 0) return std::min(s->chunk_S, s->S);

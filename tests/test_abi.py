@@ -112,7 +112,9 @@ def test_workspace_grows_with_chunk():
 
 def test_auto_chunk_keeps_large_steps_bounded():
     for wl in (configs.C3, configs.C5):
-        assert 0 < pigan.workspace_bytes(pigan.step_desc(wl)) <= (64 << 30)
+        assert 0 < pigan.workspace_bytes(pigan.step_desc(wl)) <= (128 << 30)
+    import ctypes as C
+    assert 0 < pigan.lib().pigan_trunk_workspace_bytes(C.byref(pigan.trunk_desc(configs.T21))) <= (128 << 30)
 
 
 def test_gen_forward_and_disc_forward_validation():
@@ -175,7 +177,7 @@ def test_trunk_step_validation():
     assert _trunk_step(d, 1 << 40) == pigan.EINVAL
     assert pigan.lib().pigan_trunk_step_grads(None, *([FAKE] * 6), None, 0.0, FAKE, None, FAKE, FAKE, FAKE, FAKE,
                                               FAKE, 1 << 40, None) == pigan.EINVAL
-    assert 0 < pigan.trunk_workspace_bytes(pigan.trunk_desc(configs.T21)) <= (64 << 30)
+    assert 0 < pigan.trunk_workspace_bytes(pigan.trunk_desc(configs.T21)) <= (128 << 30)
 
 
 def test_adam_update_validation():
