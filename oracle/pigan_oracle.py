@@ -585,6 +585,7 @@ def gradient_penalty(params, shape, F, R, eps, lambda_gp, w=1.0, n_total=None, p
     is tangent_output_grad along c.  A row with g_b = 0 has no gradient
     direction; it contributes P but no weight gradient."""
     num = prec if isinstance(prec, _Num) else _Num(prec)
+    w = float(w)                                  # a float32 weight would round P to single precision
     eps = np.asarray(eps, F64)[:, None]
     X = num.q(eps * np.asarray(R, F64) + (1.0 - eps) * np.asarray(F, F64))
     n = X.shape[0] if n_total is None else n_total
@@ -891,7 +892,7 @@ def real_snapshots_trunk(wl, inp):
 
 
 def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, idxU, idxF, real, w,
-                    lambda_pde=0.0, chunk_S=None, prec=None, trunk=False):
+                    lambda_pde=0.0, chunk_S=None, prec=None, trunk=False, lambda_gp=0.0, gp_eps=None):
     """Domain decomposition (Sec. III.B.1): one generator pair, one critic per
     subdomain of every level.  Critic k sees the paper's snapshot of its
     subdomain: [Y at Y sensors idxY[k] | u at u sensors idxU[k] | the
@@ -904,7 +905,11 @@ def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, id
     With trunk=True the generator is the shared trunk pY (pU unused): its Y
     head at the Y sensors, its u head at the u sensors, both heads' jets at the
     collocation points; gY is then the trunk's gradient and gU is empty.
-    Returns dict(L_D [D], L_adv [D], L_pde, gY, gU, gD [D, nD])."""
+    With lambda_gp > 0 every critic k also takes the gradient penalty of
+    gradient_penalty on its pairs (F_b, R_b), b < min(S, B), with mixing
+    weights gp_eps[k, b], weight w_k; it is added to L_D[k] and reported as
+    P_gp[k].
+    Returns dict(L_D [D], L_adv [D], L_pde, gY, gU, gD [D, nD], P_gp [D])."""
     z = np.asarray(z, F64)
     xc = np.asarray(xc, F64)
     f = np.asarray(f, F64)
@@ -914,7 +919,8 @@ def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, id
     if prec == "fp32":
         with _working_type(np.float32):
             return train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, idxU, idxF, real, w,
-                                   lambda_pde=lambda_pde, chunk_S=chunk_S, prec=None, trunk=trunk)
+                                   lambda_pde=lambda_pde, chunk_S=chunk_S, prec=None, trunk=trunk,
+                                   lambda_gp=lambda_gp, gp_eps=gp_eps)
     num = _Num(prec)
     gY = np.zeros(np.asarray(pY).size, F64)
     gU = np.zeros(0 if trunk else np.asarray(pU).size, F64)
@@ -922,6 +928,8 @@ def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, id
     sum_DF = np.zeros(D)
     sum_DR = np.zeros(D)
     sum_r2 = 0.0
+    P_gp = np.zeros(D)
+    n_gp = min(S, np.asarray(real[0]).shape[0])
     for k in range(D):
         Rk = np.asarray(real[k], F64)
         DR, hsR = mlp_forward(pDs[k], dshape, Rk, keep=True, prec=num)
@@ -965,6 +973,14 @@ def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, id
             sum_DF[k] += float(DF.sum())
             gDc, gF = mlp_backward(pDs[k], dshape, hsF, np.full(Sc, w[k] / S, F64), want_input_grad=True, prec=num)
             gD[k] += gDc
+            if lambda_gp != 0.0:
+                b1 = min(n_gp, s0 + Sc)
+                if b1 > s0:
+                    Pc, gPc = gradient_penalty(pDs[k], dshape, F[:b1 - s0], np.asarray(real[k], F64)[s0:b1],
+                                               np.asarray(gp_eps, F64)[k, s0:b1], lambda_gp, w=w[k],
+                                               n_total=n_gp, prec=num)
+                    P_gp[k] += Pc
+                    gD[k] += gPc
             gF = -gF                                      # L_adv = -w mean D(F)
             nY_, nU_, nF_ = len(iY), len(iU), len(iF)
             np.add.at(gYs, (slice(None), iY), gF[:, :nY_])
@@ -988,8 +1004,8 @@ def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, id
             gY += gen_backward(pY, gshape, d, XC, ZC, jY, g_Yval, g_Ydy, prec=num)
             gU += gen_backward(pU, gshape, d, XC, ZC, jU, np.zeros_like(r), g_Udy, g_Uddy, prec=num)
     w = np.asarray(w, F64)
-    return dict(L_D=w * (sum_DF / S - sum_DR / B), L_adv=-w * sum_DF / S, L_pde=lambda_pde * sum_r2 / (S * P),
-                gY=gY, gU=gU, gD=gD)
+    return dict(L_D=w * (sum_DF / S - sum_DR / B) + P_gp, L_adv=-w * sum_DF / S,
+                L_pde=lambda_pde * sum_r2 / (S * P), gY=gY, gU=gU, gD=gD, P_gp=P_gp)
 
 
 def real_snapshots_hier(wl, hin, trunk_teacher=None):

@@ -166,3 +166,36 @@ def test_trunk_hier_grads_fd():
         fd[k] = ((a["L_adv"].sum() + a["L_pde"]) - (b["L_adv"].sum() + b["L_pde"])) / (2 * h)
     assert np.abs(o["gY"] - fd).max() <= 1e-6 * max(1.0, np.abs(fd).max())
     assert np.abs(o["gY"]).max() > 1e-4
+
+
+def test_hier_gradient_penalty_fd():
+    """Each subdomain critic's gradient penalty: central differences of the
+    summed L_D (with the penalties) in two critics' weights; the generator
+    gradients are unchanged; each P_gp[k] > 0 is added to L_D[k]."""
+    wl = WL
+    hi, real = _setup()
+    h = hi.hier
+    eps = np.random.default_rng(9).random((h.D, min(wl.S, real.shape[1])))
+    lam = 4.0
+
+    def run(pDs):
+        b = hi.base
+        return oracle.train_step_hier(wl.gen_shape(), (real.shape[2], wl.L_D, wl.W_D), wl.d, b.pY[0], b.pU[0], pDs,
+                                      b.z[0], b.xc[0], b.xsY[0], b.xsU[0], np.full((wl.S, wl.P), 0.3), h.idxY,
+                                      h.idxU, h.idxF, real, h.w, lambda_pde=0.5, lambda_gp=lam, gp_eps=eps)
+    pDs = hi.pD.astype(np.float64)
+    o = run(pDs)
+    o0 = _run(wl, hi, real)
+    assert np.all(o["P_gp"] > 0)
+    assert np.allclose(o["L_D"], o0["L_D"] + o["P_gp"], rtol=1e-13)
+    assert np.array_equal(o["gY"], o0["gY"]) and np.array_equal(o["gU"], o0["gU"])
+    hstep = 1e-6
+    for k in (0, 3):
+        fd = np.zeros(pDs.shape[1])
+        for j in range(pDs.shape[1]):
+            pp, pm = pDs.copy(), pDs.copy()
+            pp[k, j] += hstep
+            pm[k, j] -= hstep
+            fd[j] = (run(pp)["L_D"].sum() - run(pm)["L_D"].sum()) / (2 * hstep)
+        assert np.abs(o["gD"][k] - fd).max() <= 1e-6 * max(1.0, np.abs(fd).max())
+        assert np.abs(o["gD"][k] - o0["gD"][k]).max() > 1e-5
