@@ -174,10 +174,10 @@ def run_steps(step, d, wl, k):
     for _ in range(k):
         if wl.arch == "hier_trunk":
             step(d["pT"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["idxY"], d["idxU"], d["idxF"],
-                 d["real"], d["w_disc"], f=None, f_const=wl.f_const)
+                 d["real"], d["w_disc"], f=None, f_const=wl.f_const, gp_eps=d.get("gp_eps"))
         elif wl.arch == "hier":
             step(d["pY"], d["pU"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["idxY"], d["idxU"], d["idxF"],
-                 d["real"], d["w_disc"], f=None, f_const=wl.f_const)
+                 d["real"], d["w_disc"], f=None, f_const=wl.f_const, gp_eps=d.get("gp_eps"))
         elif wl.arch == "trunk":
             step(d["pT"], d["pD"], d["z"], d["xc"], d["xsY"], d["xsU"], d["real"], f=None, f_const=wl.f_const,
                  w_group=d["w_group"], gp_eps=d.get("gp_eps"))
@@ -266,17 +266,18 @@ def main():
     d, inp = device_inputs(wl, dev)
     if a.lambda_gp > 0:
         import numpy as np
-        eps = np.random.default_rng(wl.seed + 5).random((wl.G, min(wl.S, wl.B_r)), dtype=np.float32)
+        n_crit = wl.n_critics if wl.is_hier else wl.G       # one row of mixing weights per critic
+        eps = np.random.default_rng(wl.seed + 5).random((n_crit, min(wl.S, wl.B_r)), dtype=np.float32)
         d["gp_eps"] = torch.from_numpy(eps).to(dev)
     if wl.is_hier:
-        if a.lambda_gp > 0:
-            raise SystemExit("bench: the domain-decomposition step has no gradient penalty")
         if wl.trunk_gen:
             step = pigan.HierTrunkStep(pigan.hier_trunk_desc(wl, wl.n_critics, wl.m_sensors, wl.m_sensors, wl.n_free,
-                                                             chunk_S=a.chunk_S, lambda_pde=wl.lambda_pde), device=dev)
+                                                             chunk_S=a.chunk_S, lambda_pde=wl.lambda_pde,
+                                                             lambda_gp=a.lambda_gp), device=dev)
         else:
             step = pigan.HierStep(pigan.hier_desc(wl, wl.n_critics, wl.m_sensors, wl.m_sensors, wl.n_free,
-                                                  chunk_S=a.chunk_S, lambda_pde=wl.lambda_pde), device=dev)
+                                                  chunk_S=a.chunk_S, lambda_pde=wl.lambda_pde,
+                                                  lambda_gp=a.lambda_gp), device=dev)
     elif wl.arch == "trunk":
         step = pigan.TrunkStep(pigan.trunk_desc(wl, chunk_S=a.chunk_S, lambda_gp=a.lambda_gp), device=dev)
     else:

@@ -300,9 +300,12 @@ typedef struct {
   pigan_dtype dt;
   float lambda_pde;            /* >= 0 */
   float loss_scale;            /* > 0 */
+  float lambda_gp;             /* critic gradient penalty weight: 0 for pigan_hier_step_grads,
+                                  >= 0 for pigan_hier_step_grads_gp */
 } pigan_hier_desc;
 
-/* Workspace bytes for pigan_hier_step_grads (0 if the descriptor is invalid). */
+/* Workspace bytes for pigan_hier_step_grads(_gp) (0 if the descriptor is invalid;
+ * includes the penalty's buffers when lambda_gp > 0). */
 size_t pigan_hier_workspace_bytes(const pigan_hier_desc* s);
 
 /*
@@ -316,7 +319,7 @@ size_t pigan_hier_workspace_bytes(const pigan_hier_desc* s);
  *   gradients of each L_D[k]; loss : [D, 3] = (L_D[k], L_adv[k], L_pde).
  *   nonfinite, ws, ws_bytes, stream : as pigan_train_step_grads.
  * Errors: EINVAL (null pointers, generator n_groups != 1, in_dim mismatch,
- * negative counts), ENOTSUP (widths), EWORKSPACE, EDEVICE.
+ * negative counts), ENOTSUP (widths, lambda_gp != 0), EWORKSPACE, EDEVICE.
  */
 pigan_status pigan_hier_step_grads(const pigan_hier_desc* s, const float* pY, const float* pU,
                                    const float* pD, const float* z, const float* xc,
@@ -325,6 +328,30 @@ pigan_status pigan_hier_step_grads(const pigan_hier_desc* s, const float* pY, co
                                    const float* real, const float* w_disc, float* gY, float* gU,
                                    float* gD, float* loss, int32_t* nonfinite, void* ws,
                                    size_t ws_bytes, void* stream);
+
+/*
+ * pigan_hier_step_grads plus every subdomain critic's gradient penalty, the
+ * penalty of pigan_train_step_grads_gp (Sec. I.C, Sec. II.C) taken by each
+ * critic of the decomposition (Sec. III.B.1) on its own snapshots:
+ *   x_kb = eps_kb real_kb + (1 - eps_kb) F_kb,   b < n_gp = min(S, B_r)
+ *          (F_kb: critic k's fake snapshot of noise sample b, all inputs,
+ *          the free-sensor coordinates included),
+ *   P_k  = w_k lambda_gp mean_b (||grad_v D_k(x_kb)||_2 - 1)^2.
+ * P_k is added to L_D[k] (loss[k][0]) and its gradient to gD[k]; gY and gU
+ * are unchanged.
+ *   gp_eps : [D, n_gp] fp32 mixing weights (device), required when
+ *            lambda_gp > 0 (EINVAL if NULL); unused when lambda_gp = 0.
+ *   gp     : [D] fp32 output P_k (device) or NULL.
+ * Everything else as pigan_hier_step_grads.
+ */
+pigan_status pigan_hier_step_grads_gp(const pigan_hier_desc* s, const float* pY, const float* pU,
+                                      const float* pD, const float* z, const float* xc,
+                                      const float* xsY, const float* xsU, const float* f,
+                                      float f_const, const int32_t* idxY, const int32_t* idxU,
+                                      const int32_t* idxF, const float* real, const float* w_disc,
+                                      const float* gp_eps, float* gY, float* gU, float* gD,
+                                      float* loss, float* gp, int32_t* nonfinite, void* ws,
+                                      size_t ws_bytes, void* stream);
 
 /*
  * Domain decomposition with the shared-trunk generator: the step of
@@ -343,9 +370,12 @@ typedef struct {
   pigan_dtype dt;
   float lambda_pde;            /* >= 0 */
   float loss_scale;            /* > 0 */
+  float lambda_gp;             /* critic gradient penalty weight: 0 for
+                                  pigan_hier_trunk_step_grads, >= 0 for its _gp form */
 } pigan_hier_trunk_desc;
 
-/* Workspace bytes for pigan_hier_trunk_step_grads (0 if the descriptor is invalid). */
+/* Workspace bytes for pigan_hier_trunk_step_grads(_gp) (0 if the descriptor is
+ * invalid; includes the penalty's buffers when lambda_gp > 0). */
 size_t pigan_hier_trunk_workspace_bytes(const pigan_hier_trunk_desc* s);
 
 /*
@@ -363,6 +393,21 @@ pigan_status pigan_hier_trunk_step_grads(const pigan_hier_trunk_desc* s, const f
                                          const float* w_disc, float* gT, float* gD, float* loss,
                                          int32_t* nonfinite, void* ws, size_t ws_bytes,
                                          void* stream);
+
+/*
+ * pigan_hier_trunk_step_grads plus every subdomain critic's gradient penalty,
+ * as pigan_hier_step_grads_gp (gp_eps [D, min(S, B_r)], gp [D] or NULL; gT
+ * unchanged by the penalty).
+ */
+pigan_status pigan_hier_trunk_step_grads_gp(const pigan_hier_trunk_desc* s, const float* pT,
+                                            const float* pD, const float* z, const float* xc,
+                                            const float* xsY, const float* xsU, const float* f,
+                                            float f_const, const int32_t* idxY,
+                                            const int32_t* idxU, const int32_t* idxF,
+                                            const float* real, const float* w_disc,
+                                            const float* gp_eps, float* gT, float* gD, float* loss,
+                                            float* gp, int32_t* nonfinite, void* ws,
+                                            size_t ws_bytes, void* stream);
 
 /*
  * pigan_adam_update — one update of fp32 master weights from the fp32

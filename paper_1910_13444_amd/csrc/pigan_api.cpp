@@ -387,6 +387,10 @@ static void plan_hier(const pigan_step_desc* s, int Sc, StepPlan& pl, bool trunk
   pl.hr = cv.take((size_t)Sc * s->P * 4);
   pl.hgn = cv.take((size_t)Sc * s->P * 4);
   pl.hdx = cv.take((size_t)Sc * D.Kp * 4 * GD);
+  if (s->lambda_gp > 0.0f) {
+    pl.gpg = cv.take((size_t)Sc * s->disc.in_dim * 4 * GD);
+    pl.gpp = cv.take((size_t)Sc * 8 * GD);
+  }
   pl.total = round_up((int64_t)cv.off, 256);
 }
 
@@ -707,21 +711,18 @@ static pigan_status disc_forward(void* ws, const DiscBuf& D, const float* pD, in
   return PIGAN_OK;
 }
 
-// Critic gradient penalty on the pairs b0..b0+n-1 of this chunk (fake row i is
-// the chunk's sample i):  P = w lambda_gp / n_gp sum_b (|g_b| - 1)^2 with
-// g_b = dD/dv at x_b = eps_b R_b + (1 - eps_b) F_b.  dP/dphi = sum_b c_b .
-// dg_b/dphi with c_b = dP/dg_b fixed, and c_b . g_b is the directional
-// derivative of D at x_b along c_b: so the weight gradient is the reverse
-// pass of a (value, tangent) jet of D seeded with (x_b, c_b), with cotangent
-// 1 on the tangent output.  Added to gD; the row terms go to acc[g][3].
+// Critic gradient penalty on n pairs of this chunk, whose interpolates
+// x_b = eps_b R_b + (1 - eps_b) F_b the caller has written to the critic's
+// input rows [0, n):  P = w lambda_gp / n_gp sum_b (|g_b| - 1)^2 with
+// g_b = dD/dv at x_b.  dP/dphi = sum_b c_b . dg_b/dphi with c_b = dP/dg_b
+// fixed, and c_b . g_b is the directional derivative of D at x_b along c_b:
+// so the weight gradient is the reverse pass of a (value, tangent) jet of D
+// seeded with (x_b, c_b), with cotangent 1 on the tangent output.  Added to
+// gD; the row terms go to acc[g][3].  G critics, one per grid z.
 template <class T>
-// The fake snapshot of chunk sample i is read from the generators' sensor
-// outputs: Y values jY[i * ldY + j], u values jU[i * ldU + offU + j].
 static pigan_status critic_penalty(void* ws, const StepPlan& pl, const pigan_step_desc* s, const float* pD,
-                                   const float* jY, int64_t jy_g, const float* jU, int64_t ju_g, int ldY, int ldU,
-                                   int offU, const float* real, const float* gp_eps, const float* w_group, int b0,
-                                   int n, float* gD, float inv, int32_t* nonfinite, double* acc, int G,
-                                   hipStream_t st) {
+                                   const float* w_group, int n, float* gD, float inv, int32_t* nonfinite,
+                                   double* acc, int G, hipStream_t st) {
   const DiscBuf& D = pl.D;
   const int WD = s->disc.width, LD = s->disc.n_hidden, n_in = s->disc.in_dim;
   const int64_t dact = D.Bmax * WD, xg = D.Bmax * D.Kp;
@@ -730,8 +731,6 @@ static pigan_status critic_penalty(void* ws, const StepPlan& pl, const pigan_ste
   pigan_status r;
   {
     ProfScope ps(st, "gp_misc", 0.0, 0.0);
-    HIP_TRY(launch_gp_mix<T>(jY, jy_g, jU, ju_g, s->n_sY, s->n_sU, ldY, ldU, offU, real,
-                             (int64_t)s->B_r * n_in, gp_eps, n_gp, b0, n, n_in, tp<T>(ws, D.X0), xg, D.Kp, G, st));
     HIP_TRY(launch_fill2(tp<float>(ws, D.seed), D.Bmax, n, 1.0f, 0.0f, 0, G, st));
   }
   // 1. D on the interpolates, then its reverse pass to the input: g = dD/dv
@@ -987,12 +986,18 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
     }
     // critic gradient penalty on the pairs of this chunk's samples
     if (s->lambda_gp > 0.0f) {
-      const int npair = std::min(std::min(S, s->B_r), s0 + Sc) - s0;
+      const int n_gp = std::min(S, s->B_r), npair = std::min(n_gp, s0 + Sc) - s0;
       const int ldY = pl.trunk ? n_s : s->n_sY, ldU = pl.trunk ? n_s : s->n_sU, offU = pl.trunk ? s->n_sY : 0;
-      if (npair > 0 && (r = critic_penalty<T>(ws, pl, s, pD, tp<float>(ws, Yc.jet), Yc.R, jetU, ju_g, ldY, ldU, offU,
-                                              real, gp_eps, w_group, s0, npair, gD, inv, nonfinite, acc, G, st)) !=
-                           PIGAN_OK)
-        return r;
+      if (npair > 0) {
+        {
+          ProfScope ps(st, "gp_misc", 0.0, 0.0);
+          HIP_TRY(launch_gp_mix<T>(tp<float>(ws, Yc.jet), Yc.R, jetU, ju_g, s->n_sY, s->n_sU, ldY, ldU, offU, real,
+                                   (int64_t)s->B_r * n_in, gp_eps, n_gp, s0, npair, n_in, tp<T>(ws, D.X0),
+                                   D.Bmax * D.Kp, D.Kp, G, st));
+        }
+        if ((r = critic_penalty<T>(ws, pl, s, pD, w_group, npair, gD, inv, nonfinite, acc, G, st)) != PIGAN_OK)
+          return r;
+      }
     }
     // generator reverse passes
     if ((r = gen_chunk_bwd<T>(ws, pl, Yc, pY, xsG, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, gY, accum, inv, nonfinite,
@@ -1021,7 +1026,7 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
                              const float* f, float f_const, const int32_t* idxY, const int32_t* idxU,
                              const int32_t* idxF, int mY, int mU, int nF, const float* real, const float* w_disc,
                              float* gY, float* gU, float* gD, float* loss, int32_t* nonfinite, void* ws,
-                             hipStream_t st) {
+                             hipStream_t st, const float* gp_eps, float* gp) {
   const int GD = pl.GD, d = s->d, n_z = s->n_z, P = s->P, S = s->S;
   const float ls = s->loss_scale;
   const float inv = 1.0f / ls;
@@ -1118,6 +1123,20 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
       ProfScope ps(st, "misc", 0.0, 0.0);
       HIP_TRY(launch_hier_scatter(h, dX, dx_g, D.Kp, Sc, GD, tp<float>(ws, Yc.gbar), gbarU, gN, st));
     }
+    // every critic's gradient penalty on the pairs of this chunk's samples
+    // (the critics' input rows are free again: the interpolates replace them)
+    if (s->lambda_gp > 0.0f) {
+      const int n_gp = std::min(S, s->B_r), npair = std::min(n_gp, s0 + Sc) - s0;
+      if (npair > 0) {
+        {
+          ProfScope ps(st, "gp_misc", 0.0, 0.0);
+          HIP_TRY(launch_hier_snap<T>(h, npair, real, (int64_t)s->B_r * n_in, 0, tp<T>(ws, D.X0), D.Bmax * D.Kp,
+                                      D.Kp, GD, st, gp_eps, n_gp, s0));
+        }
+        if ((r = critic_penalty<T>(ws, pl, s, pD, w_disc, npair, gD, inv, nonfinite, acc, GD, st)) != PIGAN_OK)
+          return r;
+      }
+    }
     {
       // jet cotangents from the penalty and the critics' source cotangents
       ProfScope ps(st, "residual", 0.0, (double)M * (3 * d + 2) * 4.0 * 2);
@@ -1135,8 +1154,8 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
   }
   {
     ProfScope ps(st, "misc", 0.0, 0.0);
-    HIP_TRY(launch_losses(acc, 4, w_disc, S, s->B_r, (int64_t)S * P, 0.0f, 0.0f, 0, loss, nullptr, nonfinite, GD,
-                          st));
+    HIP_TRY(launch_losses(acc, 4, w_disc, S, s->B_r, (int64_t)S * P, 0.0f, s->lambda_gp, std::min(S, s->B_r), loss,
+                          gp, nonfinite, GD, st));
     HIP_TRY(launch_hier_pde_loss(acc, 2, s->lambda_pde, (int64_t)S * P, loss, GD, nonfinite, st));
   }
   return PIGAN_OK;
@@ -1201,7 +1220,9 @@ static pigan_status train_step_entry(const pigan_step_desc* s, const float* pY, 
 }
 
 // descriptor of the domain-decomposition step as the shared step fields
-static pigan_status check_hier(const pigan_hier_desc* h, pigan_step_desc* out) {
+// gp_name: the entry point that takes the penalty's mixing weights
+static pigan_status check_hier(const pigan_hier_desc* h, pigan_step_desc* out, bool gp_entry = false,
+                               const char* gp_name = "pigan_hier_step_grads_gp") {
   if (!h) return fail(PIGAN_EINVAL, "null hierarchical step descriptor");
   pigan_status st;
   if ((st = check_mlp(&h->genY, "genY")) != PIGAN_OK) return st;
@@ -1227,10 +1248,15 @@ static pigan_status check_hier(const pigan_hier_desc* h, pigan_step_desc* out) {
     return fail(PIGAN_EINVAL, "lambda_pde must be finite and >= 0");
   if (!(h->loss_scale > 0.0f) || !__builtin_isfinite(h->loss_scale))
     return fail(PIGAN_EINVAL, "loss_scale must be finite and > 0");
+  if (!(h->lambda_gp >= 0.0f) || !__builtin_isfinite(h->lambda_gp))
+    return fail(PIGAN_EINVAL, "lambda_gp must be finite and >= 0");
+  if (!gp_entry && h->lambda_gp != 0.0f)
+    return fail(PIGAN_ENOTSUP, "lambda_gp != 0 needs the per-pair mixing weights: use %s", gp_name);
   pigan_step_desc s{};
   s.genY = h->genY; s.genU = h->genU; s.disc = h->disc;
   s.d = h->d; s.n_z = h->n_z; s.S = h->S; s.P = h->P; s.n_sY = h->n_sY; s.n_sU = h->n_sU; s.B_r = h->B_r;
-  s.chunk_S = h->chunk_S; s.dt = h->dt; s.lambda_pde = h->lambda_pde; s.lambda_gp = 0.0f; s.loss_scale = h->loss_scale;
+  s.chunk_S = h->chunk_S; s.dt = h->dt; s.lambda_pde = h->lambda_pde; s.lambda_gp = h->lambda_gp;
+  s.loss_scale = h->loss_scale;
   *out = s;
   return PIGAN_OK;
 }
@@ -1253,8 +1279,51 @@ static pigan_hier_desc hier_trunk_as_hier(const pigan_hier_trunk_desc* t) {
   h.genY = t->trunk; h.genU = t->trunk; h.disc = t->disc;
   h.d = t->d; h.n_z = t->n_z; h.S = t->S; h.P = t->P; h.n_sY = t->n_sY; h.n_sU = t->n_sU; h.B_r = t->B_r;
   h.chunk_S = t->chunk_S; h.mY = t->mY; h.mU = t->mU; h.nF = t->nF; h.dt = t->dt; h.lambda_pde = t->lambda_pde;
-  h.loss_scale = t->loss_scale;
+  h.loss_scale = t->loss_scale; h.lambda_gp = t->lambda_gp;
   return h;
+}
+
+// every hierarchical entry point: trunk selects the shared-trunk generator
+// (pY is the trunk, pU and gU unused), gp_entry the entry points that take the
+// penalty's mixing weights
+static pigan_status hier_entry(const pigan_hier_desc* h, bool trunk, bool gp_entry, const char* gp_name,
+                               const float* pY, const float* pU, const float* pD, const float* z, const float* xc,
+                               const float* xsY, const float* xsU, const float* f, float f_const,
+                               const int32_t* idxY, const int32_t* idxU, const int32_t* idxF, const float* real,
+                               const float* w_disc, const float* gp_eps, float* gY, float* gU, float* gD,
+                               float* loss, float* gp, int32_t* nonfinite, void* ws, size_t ws_bytes,
+                               void* stream) {
+  pigan_step_desc s;
+  pigan_status st = check_hier(h, &s, gp_entry, gp_name);
+  if (st != PIGAN_OK) return st;
+  if (!pY || (!trunk && (!pU || !gU)) || !pD || !z || !xc || !xsY || !xsU || !real || !w_disc || !gY || !gD ||
+      !loss || !nonfinite)
+    return fail(PIGAN_EINVAL, "null input or output pointer");
+  if ((h->mY > 0 && !idxY) || (h->mU > 0 && !idxU) || (h->nF > 0 && !idxF))
+    return fail(PIGAN_EINVAL, "null sensor index list");
+  if (s.lambda_gp > 0.0f && !gp_eps) return fail(PIGAN_EINVAL, "lambda_gp > 0 needs gp_eps");
+  if (!__builtin_isfinite(f_const)) return fail(PIGAN_EINVAL, "f_const must be finite");
+  StepPlan pl;
+  plan_hier(&s, choose_chunk(&s, trunk, true), pl, trunk);
+  if (!ws) return fail(PIGAN_EWORKSPACE, "null workspace (need %zu bytes)", pl.total);
+  if (ws_bytes < pl.total) return fail(PIGAN_EWORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, pl.total);
+  if ((uintptr_t)ws % 256) return fail(PIGAN_EINVAL, "workspace must be 256-byte aligned");
+  hipStream_t hs = (hipStream_t)stream;
+  if (trunk) {
+    pU = nullptr;
+    gU = nullptr;
+  }
+  switch (s.dt) {
+    case PIGAN_FP32:
+      return run_hier<float>(&s, pl, pY, pU, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, h->mY, h->mU, h->nF,
+                             real, w_disc, gY, gU, gD, loss, nonfinite, ws, hs, gp_eps, gp);
+    case PIGAN_BF16:
+      return run_hier<bf16>(&s, pl, pY, pU, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, h->mY, h->mU, h->nF,
+                            real, w_disc, gY, gU, gD, loss, nonfinite, ws, hs, gp_eps, gp);
+    default:
+      return run_hier<f16>(&s, pl, pY, pU, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, h->mY, h->mU, h->nF,
+                           real, w_disc, gY, gU, gD, loss, nonfinite, ws, hs, gp_eps, gp);
+  }
 }
 
 extern "C" {
@@ -1278,7 +1347,7 @@ pigan_status pigan_adam_update(int64_t n, float* params, const float* grads, flo
 
 size_t pigan_hier_workspace_bytes(const pigan_hier_desc* h) {
   pigan_step_desc s;
-  if (check_hier(h, &s) != PIGAN_OK) return 0;
+  if (check_hier(h, &s, true) != PIGAN_OK) return 0;   // either entry point: includes the penalty's buffers
   StepPlan pl;
   plan_hier(&s, choose_chunk(&s, false, true), pl);
   return pl.total;
@@ -1288,7 +1357,7 @@ size_t pigan_hier_trunk_workspace_bytes(const pigan_hier_trunk_desc* t) {
   if (!t) return 0;
   const pigan_hier_desc h = hier_trunk_as_hier(t);
   pigan_step_desc s;
-  if (check_hier(&h, &s) != PIGAN_OK) return 0;
+  if (check_hier(&h, &s, true) != PIGAN_OK) return 0;
   StepPlan pl;
   plan_hier(&s, choose_chunk(&s, true, true), pl, true);
   return pl.total;
@@ -1303,31 +1372,24 @@ pigan_status pigan_hier_trunk_step_grads(const pigan_hier_trunk_desc* t, const f
   g_err.clear();
   if (!t) return fail(PIGAN_EINVAL, "null hierarchical trunk step descriptor");
   const pigan_hier_desc h = hier_trunk_as_hier(t);
-  pigan_step_desc s;
-  pigan_status st = check_hier(&h, &s);
-  if (st != PIGAN_OK) return st;
-  if (!pT || !pD || !z || !xc || !xsY || !xsU || !real || !w_disc || !gT || !gD || !loss || !nonfinite)
-    return fail(PIGAN_EINVAL, "null input or output pointer");
-  if ((h.mY > 0 && !idxY) || (h.mU > 0 && !idxU) || (h.nF > 0 && !idxF))
-    return fail(PIGAN_EINVAL, "null sensor index list");
-  if (!__builtin_isfinite(f_const)) return fail(PIGAN_EINVAL, "f_const must be finite");
-  StepPlan pl;
-  plan_hier(&s, choose_chunk(&s, true, true), pl, true);
-  if (!ws) return fail(PIGAN_EWORKSPACE, "null workspace (need %zu bytes)", pl.total);
-  if (ws_bytes < pl.total) return fail(PIGAN_EWORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, pl.total);
-  if ((uintptr_t)ws % 256) return fail(PIGAN_EINVAL, "workspace must be 256-byte aligned");
-  hipStream_t hs = (hipStream_t)stream;
-  switch (s.dt) {
-    case PIGAN_FP32:
-      return run_hier<float>(&s, pl, pT, nullptr, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, h.mY, h.mU,
-                             h.nF, real, w_disc, gT, nullptr, gD, loss, nonfinite, ws, hs);
-    case PIGAN_BF16:
-      return run_hier<bf16>(&s, pl, pT, nullptr, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, h.mY, h.mU,
-                            h.nF, real, w_disc, gT, nullptr, gD, loss, nonfinite, ws, hs);
-    default:
-      return run_hier<f16>(&s, pl, pT, nullptr, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, h.mY, h.mU,
-                           h.nF, real, w_disc, gT, nullptr, gD, loss, nonfinite, ws, hs);
-  }
+  return hier_entry(&h, true, false, "pigan_hier_trunk_step_grads_gp", pT, nullptr, pD, z, xc, xsY, xsU, f, f_const,
+                    idxY, idxU, idxF, real, w_disc, nullptr, gT, nullptr, gD, loss, nullptr, nonfinite, ws, ws_bytes,
+                    stream);
+}
+
+pigan_status pigan_hier_trunk_step_grads_gp(const pigan_hier_trunk_desc* t, const float* pT, const float* pD,
+                                            const float* z, const float* xc, const float* xsY, const float* xsU,
+                                            const float* f, float f_const, const int32_t* idxY,
+                                            const int32_t* idxU, const int32_t* idxF, const float* real,
+                                            const float* w_disc, const float* gp_eps, float* gT, float* gD,
+                                            float* loss, float* gp, int32_t* nonfinite, void* ws, size_t ws_bytes,
+                                            void* stream) {
+  g_err.clear();
+  if (!t) return fail(PIGAN_EINVAL, "null hierarchical trunk step descriptor");
+  const pigan_hier_desc h = hier_trunk_as_hier(t);
+  return hier_entry(&h, true, true, "pigan_hier_trunk_step_grads_gp", pT, nullptr, pD, z, xc, xsY, xsU, f, f_const,
+                    idxY, idxU, idxF, real, w_disc, gp_eps, gT, nullptr, gD, loss, gp, nonfinite, ws, ws_bytes,
+                    stream);
 }
 
 pigan_status pigan_hier_step_grads(const pigan_hier_desc* h, const float* pY, const float* pU, const float* pD,
@@ -1337,31 +1399,19 @@ pigan_status pigan_hier_step_grads(const pigan_hier_desc* h, const float* pY, co
                                    float* gD, float* loss, int32_t* nonfinite, void* ws, size_t ws_bytes,
                                    void* stream) {
   g_err.clear();
-  pigan_step_desc s;
-  pigan_status st = check_hier(h, &s);
-  if (st != PIGAN_OK) return st;
-  if (!pY || !pU || !pD || !z || !xc || !xsY || !xsU || !real || !w_disc || !gY || !gU || !gD || !loss || !nonfinite)
-    return fail(PIGAN_EINVAL, "null input or output pointer");
-  if ((h->mY > 0 && !idxY) || (h->mU > 0 && !idxU) || (h->nF > 0 && !idxF))
-    return fail(PIGAN_EINVAL, "null sensor index list");
-  if (!__builtin_isfinite(f_const)) return fail(PIGAN_EINVAL, "f_const must be finite");
-  StepPlan pl;
-  plan_hier(&s, choose_chunk(&s, false, true), pl);
-  if (!ws) return fail(PIGAN_EWORKSPACE, "null workspace (need %zu bytes)", pl.total);
-  if (ws_bytes < pl.total) return fail(PIGAN_EWORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, pl.total);
-  if ((uintptr_t)ws % 256) return fail(PIGAN_EINVAL, "workspace must be 256-byte aligned");
-  hipStream_t hs = (hipStream_t)stream;
-  switch (s.dt) {
-    case PIGAN_FP32:
-      return run_hier<float>(&s, pl, pY, pU, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, h->mY, h->mU, h->nF,
-                             real, w_disc, gY, gU, gD, loss, nonfinite, ws, hs);
-    case PIGAN_BF16:
-      return run_hier<bf16>(&s, pl, pY, pU, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, h->mY, h->mU, h->nF,
-                            real, w_disc, gY, gU, gD, loss, nonfinite, ws, hs);
-    default:
-      return run_hier<f16>(&s, pl, pY, pU, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU, idxF, h->mY, h->mU, h->nF,
-                           real, w_disc, gY, gU, gD, loss, nonfinite, ws, hs);
-  }
+  return hier_entry(h, false, false, "pigan_hier_step_grads_gp", pY, pU, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU,
+                    idxF, real, w_disc, nullptr, gY, gU, gD, loss, nullptr, nonfinite, ws, ws_bytes, stream);
+}
+
+pigan_status pigan_hier_step_grads_gp(const pigan_hier_desc* h, const float* pY, const float* pU, const float* pD,
+                                      const float* z, const float* xc, const float* xsY, const float* xsU,
+                                      const float* f, float f_const, const int32_t* idxY, const int32_t* idxU,
+                                      const int32_t* idxF, const float* real, const float* w_disc,
+                                      const float* gp_eps, float* gY, float* gU, float* gD, float* loss, float* gp,
+                                      int32_t* nonfinite, void* ws, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  return hier_entry(h, false, true, "pigan_hier_step_grads_gp", pY, pU, pD, z, xc, xsY, xsU, f, f_const, idxY, idxU,
+                    idxF, real, w_disc, gp_eps, gY, gU, gD, loss, gp, nonfinite, ws, ws_bytes, stream);
 }
 
 int64_t pigan_trunk_param_count(const pigan_mlp* net) {

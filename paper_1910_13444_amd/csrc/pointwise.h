@@ -105,7 +105,8 @@ struct HierSnap {
 };
 template <class T>
 hipError_t launch_hier_snap(const HierSnap& h, int n_fake, const float* real, int64_t real_g, int n_real, T* X,
-                            int64_t x_g, int ldx, int D, hipStream_t st);
+                            int64_t x_g, int ldx, int D, hipStream_t st, const float* eps = nullptr,
+                            int64_t eps_g = 0, int b0 = 0);
 hipError_t launch_hier_scatter(const HierSnap& h, const float* dX, int64_t dx_g, int ldx, int n_fake, int D,
                                float* gY, float* gU, float* gN, hipStream_t st);
 // loss[k][2] = lambda_pde * acc[slot] / SP for every critic k

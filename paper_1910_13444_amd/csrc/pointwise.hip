@@ -626,10 +626,14 @@ __global__ void k_fill_f32(float* __restrict__ p, int64_t n, int64_t p_g, float 
 // sensor rows of sample b sit at b * ldY (Y) and b * ldU + offU (u): a
 // generator pair keeps them in separate arrays, the shared trunk in one row
 // block per sample ([Y sensors ; u sensors], Y head and u head arrays).
+// With eps set (and no real rows) fake row b becomes the gradient penalty's
+// interpolate of pair b0 + b: eps R + (1 - eps) F with R that pair's real
+// snapshot of critic k and eps = eps[k][b0 + b].
 // ---------------------------------------------------------------------------
 template <class T>
 __global__ void k_hier_snap(HierSnap h, int n_fake, const float* __restrict__ real, int64_t real_g, int n_real,
-                            T* __restrict__ X, int64_t x_g, int ldx) {
+                            T* __restrict__ X, int64_t x_g, int ldx, const float* __restrict__ eps, int64_t eps_g,
+                            int b0) {
   const int k = blockIdx.z;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (int64_t)(n_fake + n_real) * ldx) return;
@@ -655,6 +659,10 @@ __global__ void k_hier_snap(HierSnap h, int n_fake, const float* __restrict__ re
         } else {
           *h.bad = 1;
         }
+      }
+      if (eps) {   // penalty interpolate of the pair b0 + b
+        const float e = eps[k * eps_g + b0 + b];
+        v = e * real[k * real_g + (int64_t)(b0 + b) * h.n_in + j] + (1.0f - e) * v;
       }
     } else {
       v = real[k * real_g + (int64_t)(b - n_fake) * h.n_in + j];
@@ -1131,10 +1139,12 @@ hipError_t launch_concat_rows(const float* a, int64_t a_g, int na, const float* 
 
 template <class T>
 hipError_t launch_hier_snap(const HierSnap& h, int n_fake, const float* real, int64_t real_g, int n_real, T* X,
-                            int64_t x_g, int ldx, int D, hipStream_t st) {
+                            int64_t x_g, int ldx, int D, hipStream_t st, const float* eps, int64_t eps_g, int b0) {
   const int64_t tot = (int64_t)(n_fake + n_real) * ldx;
   if (tot <= 0 || D <= 0) return hipSuccess;
-  k_hier_snap<T><<<dim3(nblk(tot, 256), 1, D), 256, 0, st>>>(h, n_fake, real, real_g, n_real, X, x_g, ldx);
+  if (eps && n_real != 0) return hipErrorInvalidValue;   // interpolates replace the fake rows only
+  k_hier_snap<T><<<dim3(nblk(tot, 256), 1, D), 256, 0, st>>>(h, n_fake, real, real_g, n_real, X, x_g, ldx, eps,
+                                                             eps_g, b0);
   return hipGetLastError();
 }
 
@@ -1228,7 +1238,7 @@ hipError_t launch_cast(const float* src, int64_t s_g, int N, int K, int Kp, T* d
   template hipError_t launch_out_bwd<T>(int, int, const OutBwdArgs<T>&, int, hipStream_t);                    \
   template hipError_t launch_out2_bwd<T>(int, int, const Out2BwdArgs<T>&, int, hipStream_t);                  \
   template hipError_t launch_hier_snap<T>(const HierSnap&, int, const float*, int64_t, int, T*, int64_t, int, int, \
-                                          hipStream_t);                                                          \
+                                          hipStream_t, const float*, int64_t, int);                              \
   template hipError_t launch_snap_fill_rows<T>(const float*, int64_t, const float*, int64_t, int, int, int, int, \
                                                int, const float*, int64_t, int, int, T*, int64_t, int, int,     \
                                                hipStream_t);                                                    \

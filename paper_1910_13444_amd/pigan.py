@@ -57,7 +57,8 @@ class HierDesc(C.Structure):
                 ("d", C.c_int32), ("n_z", C.c_int32), ("S", C.c_int32), ("P", C.c_int32),
                 ("n_sY", C.c_int32), ("n_sU", C.c_int32), ("B_r", C.c_int32), ("chunk_S", C.c_int32),
                 ("mY", C.c_int32), ("mU", C.c_int32), ("nF", C.c_int32),
-                ("dt", C.c_int32), ("lambda_pde", C.c_float), ("loss_scale", C.c_float)]
+                ("dt", C.c_int32), ("lambda_pde", C.c_float), ("loss_scale", C.c_float),
+                ("lambda_gp", C.c_float)]
 
 
 class HierTrunkDesc(C.Structure):
@@ -65,7 +66,8 @@ class HierTrunkDesc(C.Structure):
                 ("d", C.c_int32), ("n_z", C.c_int32), ("S", C.c_int32), ("P", C.c_int32),
                 ("n_sY", C.c_int32), ("n_sU", C.c_int32), ("B_r", C.c_int32), ("chunk_S", C.c_int32),
                 ("mY", C.c_int32), ("mU", C.c_int32), ("nF", C.c_int32),
-                ("dt", C.c_int32), ("lambda_pde", C.c_float), ("loss_scale", C.c_float)]
+                ("dt", C.c_int32), ("lambda_pde", C.c_float), ("loss_scale", C.c_float),
+                ("lambda_gp", C.c_float)]
 
 
 class KernelStat(C.Structure):
@@ -99,8 +101,12 @@ def lib():
         "pigan_adam_update": (i32, [i64, P, P, P, P, f32, f32, f32, f32, i32, P, P]),
         "pigan_hier_workspace_bytes": (sz, [P]),
         "pigan_hier_step_grads": (i32, [P, P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, P, P, P, sz, P]),
+        "pigan_hier_step_grads_gp": (i32, [P, P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, P, P, P, P, P, sz,
+                                           P]),
         "pigan_hier_trunk_workspace_bytes": (sz, [P]),
         "pigan_hier_trunk_step_grads": (i32, [P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, P, P, sz, P]),
+        "pigan_hier_trunk_step_grads_gp": (i32, [P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, P, P, P, P, sz,
+                                                 P]),
         "pigan_trunk_param_count": (i64, [P]),
         "pigan_trunk_workspace_bytes": (sz, [P]),
         "pigan_trunk_step_grads": (i32, [P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, sz, P]),
@@ -351,13 +357,13 @@ class TrunkStep:
 
 def hier_desc(wl: Workload, D: int, mY: int, mU: int, nF: int, S: int | None = None, B_r: int | None = None,
               chunk_S: int = 0, dtype: str | None = None, lambda_pde: float = 0.0,
-              loss_scale: float = 1.0) -> HierDesc:
+              loss_scale: float = 1.0, lambda_gp: float = 0.0) -> HierDesc:
     S = wl.S if S is None else S
     B_r = wl.B_r if B_r is None else B_r
     n_in = mY + mU + nF * (1 + wl.d)
     return HierDesc(Mlp(1, wl.in_dim, wl.L, wl.W), Mlp(1, wl.in_dim, wl.L, wl.W), Mlp(D, n_in, wl.L_D, wl.W_D),
                     wl.d, wl.n_z, S, wl.P, wl.n_sY, wl.n_sU, B_r, chunk_S, mY, mU, nF, DTYPES[dtype or wl.dtype],
-                    lambda_pde, loss_scale)
+                    lambda_pde, loss_scale, lambda_gp)
 
 
 @dataclass
@@ -367,6 +373,7 @@ class HierOut:
     gD: torch.Tensor      # [D, nD]
     loss: torch.Tensor    # [D, 3]: L_D[k], L_adv[k], L_pde
     nonfinite: torch.Tensor
+    gp: torch.Tensor | None = None    # [D] every critic's gradient penalty (when lambda_gp > 0)
 
 
 class HierStep:
@@ -387,35 +394,44 @@ class HierStep:
         f32 = dict(dtype=torch.float32, device=self.device)
         self.out = HierOut(torch.empty((self.nY,), **f32), torch.empty((self.nU,), **f32),
                            torch.empty((D, self.nD), **f32), torch.empty((D, 3), **f32),
-                           torch.zeros((1,), dtype=torch.int32, device=self.device))
+                           torch.zeros((1,), dtype=torch.int32, device=self.device),
+                           torch.empty((D,), **f32) if desc.lambda_gp > 0 else None)
 
-    def __call__(self, pY, pU, pD, z, xc, xsY, xsU, idxY, idxU, idxF, real, w_disc, f=None, f_const=0.0) -> HierOut:
+    def __call__(self, pY, pU, pD, z, xc, xsY, xsU, idxY, idxU, idxF, real, w_disc, f=None, f_const=0.0,
+                 gp_eps=None) -> HierOut:
+        """gp_eps: [D, min(S, B_r)] mixing weights of the critics' gradient
+        penalty (required when the descriptor's lambda_gp is non-zero)."""
         d = self.desc
         D, S, Pn = d.disc.n_groups, d.S, d.P
         o = self.out
         i32 = torch.int32
-        st = lib().pigan_hier_step_grads(
-            C.byref(d), _ptr(pY, "pY", self.nY), _ptr(pU, "pU", self.nU), _ptr(pD, "pD", D * self.nD),
-            _ptr(z, "z", S * d.n_z), _ptr(xc, "xc", S * Pn * d.d), _ptr(xsY, "xsY", d.n_sY * d.d),
-            _ptr(xsU, "xsU", d.n_sU * d.d), _ptr(f, "f", S * Pn), float(f_const),
-            _ptr(idxY, "idxY", D * d.mY, dtype=i32), _ptr(idxU, "idxU", D * d.mU, dtype=i32),
-            _ptr(idxF, "idxF", D * d.nF, dtype=i32), _ptr(real, "real", D * d.B_r * d.disc.in_dim),
-            _ptr(w_disc, "w_disc", D), _ptr(o.gY, "gY"), _ptr(o.gU, "gU"), _ptr(o.gD, "gD"), _ptr(o.loss, "loss"),
-            _ptr(o.nonfinite, "nonfinite", 1, dtype=i32), _ptr(self.ws, "ws", dtype=torch.uint8), self.ws_bytes,
-            _stream())
+        args = [C.byref(d), _ptr(pY, "pY", self.nY), _ptr(pU, "pU", self.nU), _ptr(pD, "pD", D * self.nD),
+                _ptr(z, "z", S * d.n_z), _ptr(xc, "xc", S * Pn * d.d), _ptr(xsY, "xsY", d.n_sY * d.d),
+                _ptr(xsU, "xsU", d.n_sU * d.d), _ptr(f, "f", S * Pn), float(f_const),
+                _ptr(idxY, "idxY", D * d.mY, dtype=i32), _ptr(idxU, "idxU", D * d.mU, dtype=i32),
+                _ptr(idxF, "idxF", D * d.nF, dtype=i32), _ptr(real, "real", D * d.B_r * d.disc.in_dim),
+                _ptr(w_disc, "w_disc", D)]
+        outs = [_ptr(o.gY, "gY"), _ptr(o.gU, "gU"), _ptr(o.gD, "gD"), _ptr(o.loss, "loss")]
+        tail = [_ptr(o.nonfinite, "nonfinite", 1, dtype=i32), _ptr(self.ws, "ws", dtype=torch.uint8), self.ws_bytes,
+                _stream()]
+        if d.lambda_gp > 0:
+            eps = _ptr(gp_eps, "gp_eps", D * min(S, d.B_r))
+            st = lib().pigan_hier_step_grads_gp(*args, eps, *outs, _ptr(o.gp, "gp", D), *tail)
+        else:
+            st = lib().pigan_hier_step_grads(*args, *outs, *tail)
         _check(st)
         return o
 
 
 def hier_trunk_desc(wl: Workload, D: int, mY: int, mU: int, nF: int, S: int | None = None,
                     B_r: int | None = None, chunk_S: int = 0, dtype: str | None = None, lambda_pde: float = 0.0,
-                    loss_scale: float = 1.0) -> HierTrunkDesc:
+                    loss_scale: float = 1.0, lambda_gp: float = 0.0) -> HierTrunkDesc:
     S = wl.S if S is None else S
     B_r = wl.B_r if B_r is None else B_r
     n_in = mY + mU + nF * (1 + wl.d)
     return HierTrunkDesc(Mlp(1, wl.in_dim, wl.L, wl.W), Mlp(D, n_in, wl.L_D, wl.W_D), wl.d, wl.n_z, S, wl.P,
                          wl.n_sY, wl.n_sU, B_r, chunk_S, mY, mU, nF, DTYPES[dtype or wl.dtype], lambda_pde,
-                         loss_scale)
+                         loss_scale, lambda_gp)
 
 
 @dataclass
@@ -424,6 +440,7 @@ class HierTrunkOut:
     gD: torch.Tensor      # [D, nD]
     loss: torch.Tensor    # [D, 3]: L_D[k], L_adv[k], L_pde
     nonfinite: torch.Tensor
+    gp: torch.Tensor | None = None    # [D] every critic's gradient penalty (when lambda_gp > 0)
 
 
 class HierTrunkStep:
@@ -442,22 +459,29 @@ class HierTrunkStep:
         self.ws = _workspace(need, self.device)
         f32 = dict(dtype=torch.float32, device=self.device)
         self.out = HierTrunkOut(torch.empty((self.nT,), **f32), torch.empty((D, self.nD), **f32),
-                                torch.empty((D, 3), **f32), torch.zeros((1,), dtype=torch.int32, device=self.device))
+                                torch.empty((D, 3), **f32), torch.zeros((1,), dtype=torch.int32, device=self.device),
+                                torch.empty((D,), **f32) if desc.lambda_gp > 0 else None)
 
-    def __call__(self, pT, pD, z, xc, xsY, xsU, idxY, idxU, idxF, real, w_disc, f=None, f_const=0.0) -> HierTrunkOut:
+    def __call__(self, pT, pD, z, xc, xsY, xsU, idxY, idxU, idxF, real, w_disc, f=None, f_const=0.0,
+                 gp_eps=None) -> HierTrunkOut:
         d = self.desc
         D, S, Pn = d.disc.n_groups, d.S, d.P
         o = self.out
         i32 = torch.int32
-        st = lib().pigan_hier_trunk_step_grads(
-            C.byref(d), _ptr(pT, "pT", self.nT), _ptr(pD, "pD", D * self.nD), _ptr(z, "z", S * d.n_z),
-            _ptr(xc, "xc", S * Pn * d.d), _ptr(xsY, "xsY", d.n_sY * d.d), _ptr(xsU, "xsU", d.n_sU * d.d),
-            _ptr(f, "f", S * Pn), float(f_const),
-            _ptr(idxY, "idxY", D * d.mY, dtype=i32), _ptr(idxU, "idxU", D * d.mU, dtype=i32),
-            _ptr(idxF, "idxF", D * d.nF, dtype=i32), _ptr(real, "real", D * d.B_r * d.disc.in_dim),
-            _ptr(w_disc, "w_disc", D), _ptr(o.gT, "gT"), _ptr(o.gD, "gD"), _ptr(o.loss, "loss"),
-            _ptr(o.nonfinite, "nonfinite", 1, dtype=i32), _ptr(self.ws, "ws", dtype=torch.uint8), self.ws_bytes,
-            _stream())
+        args = [C.byref(d), _ptr(pT, "pT", self.nT), _ptr(pD, "pD", D * self.nD), _ptr(z, "z", S * d.n_z),
+                _ptr(xc, "xc", S * Pn * d.d), _ptr(xsY, "xsY", d.n_sY * d.d), _ptr(xsU, "xsU", d.n_sU * d.d),
+                _ptr(f, "f", S * Pn), float(f_const),
+                _ptr(idxY, "idxY", D * d.mY, dtype=i32), _ptr(idxU, "idxU", D * d.mU, dtype=i32),
+                _ptr(idxF, "idxF", D * d.nF, dtype=i32), _ptr(real, "real", D * d.B_r * d.disc.in_dim),
+                _ptr(w_disc, "w_disc", D)]
+        outs = [_ptr(o.gT, "gT"), _ptr(o.gD, "gD"), _ptr(o.loss, "loss")]
+        tail = [_ptr(o.nonfinite, "nonfinite", 1, dtype=i32), _ptr(self.ws, "ws", dtype=torch.uint8), self.ws_bytes,
+                _stream()]
+        if d.lambda_gp > 0:
+            eps = _ptr(gp_eps, "gp_eps", D * min(S, d.B_r))
+            st = lib().pigan_hier_trunk_step_grads_gp(*args, eps, *outs, _ptr(o.gp, "gp", D), *tail)
+        else:
+            st = lib().pigan_hier_trunk_step_grads(*args, *outs, *tail)
         _check(st)
         return o
 

@@ -145,42 +145,53 @@ def trunk_errors(wl, out, ref):
     return errs
 
 
-def run_hier_gpu(wl, hi, real, lam=0.0, chunk_S=0, dtype=None, idx=None, f=None, f_const=0.0):
-    """One domain-decomposition step through pigan_hier_step_grads."""
+def run_hier_gpu(wl, hi, real, lam=0.0, chunk_S=0, dtype=None, idx=None, f=None, f_const=0.0, lambda_gp=0.0,
+                 gp_eps=None):
+    """One domain-decomposition step through pigan_hier_step_grads (or, with
+    lambda_gp > 0, pigan_hier_step_grads_gp: then the result has P_gp)."""
     import torch
     from paper_1910_13444_amd import pigan
     b, h = hi.base, hi.hier
     iY, iU, iF = idx if idx is not None else (h.idxY, h.idxU, h.idxF)
     desc = pigan.hier_desc(wl, h.D, iY.shape[1], iU.shape[1], iF.shape[1], S=b.z.shape[1], B_r=real.shape[1],
-                           chunk_S=chunk_S, dtype=dtype, lambda_pde=lam)
+                           chunk_S=chunk_S, dtype=dtype, lambda_pde=lam, lambda_gp=lambda_gp)
     step = pigan.HierStep(desc)
 
     def ti(a):
         return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
     o = step(to_dev(b.pY[0]), to_dev(b.pU[0]), to_dev(hi.pD), to_dev(b.z[0]), to_dev(b.xc[0]), to_dev(b.xsY[0]),
              to_dev(b.xsU[0]), ti(iY), ti(iU), ti(iF), to_dev(real), to_dev(h.w),
-             f=None if f is None else to_dev(f), f_const=f_const)
+             f=None if f is None else to_dev(f), f_const=f_const, gp_eps=None if gp_eps is None else to_dev(gp_eps))
     torch.cuda.synchronize()
-    return dict(gY=o.gY.cpu().numpy(), gU=o.gU.cpu().numpy(), gD=o.gD.cpu().numpy(), loss=o.loss.cpu().numpy(),
-                nonfinite=int(o.nonfinite.cpu().item()))
+    out = dict(gY=o.gY.cpu().numpy(), gU=o.gU.cpu().numpy(), gD=o.gD.cpu().numpy(), loss=o.loss.cpu().numpy(),
+               nonfinite=int(o.nonfinite.cpu().item()))
+    if o.gp is not None:
+        out["P_gp"] = o.gp.cpu().numpy()
+    return out
 
 
-def run_hier_trunk_gpu(wl, hi, real, lam=0.0, chunk_S=0, dtype=None, f_const=0.0):
-    """One domain-decomposition step with the shared trunk (pigan_hier_trunk_step_grads)."""
+def run_hier_trunk_gpu(wl, hi, real, lam=0.0, chunk_S=0, dtype=None, f_const=0.0, lambda_gp=0.0, gp_eps=None):
+    """One domain-decomposition step with the shared trunk
+    (pigan_hier_trunk_step_grads, or its _gp form when lambda_gp > 0)."""
     import torch
     from paper_1910_13444_amd import pigan
     b, h = hi.base, hi.hier
     desc = pigan.hier_trunk_desc(wl, h.D, h.idxY.shape[1], h.idxU.shape[1], h.idxF.shape[1], S=b.z.shape[1],
-                                 B_r=real.shape[1], chunk_S=chunk_S, dtype=dtype, lambda_pde=lam)
+                                 B_r=real.shape[1], chunk_S=chunk_S, dtype=dtype, lambda_pde=lam,
+                                 lambda_gp=lambda_gp)
     step = pigan.HierTrunkStep(desc)
 
     def ti(a):
         return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
     o = step(to_dev(b.pT[0]), to_dev(hi.pD), to_dev(b.z[0]), to_dev(b.xc[0]), to_dev(b.xsY[0]), to_dev(b.xsU[0]),
-             ti(h.idxY), ti(h.idxU), ti(h.idxF), to_dev(real), to_dev(h.w), f_const=f_const)
+             ti(h.idxY), ti(h.idxU), ti(h.idxF), to_dev(real), to_dev(h.w), f_const=f_const,
+             gp_eps=None if gp_eps is None else to_dev(gp_eps))
     torch.cuda.synchronize()
-    return dict(gY=o.gT.cpu().numpy(), gD=o.gD.cpu().numpy(), loss=o.loss.cpu().numpy(),
-                nonfinite=int(o.nonfinite.cpu().item()))
+    out = dict(gY=o.gT.cpu().numpy(), gD=o.gD.cpu().numpy(), loss=o.loss.cpu().numpy(),
+               nonfinite=int(o.nonfinite.cpu().item()))
+    if o.gp is not None:
+        out["P_gp"] = o.gp.cpu().numpy()
+    return out
 
 
 def hier_errors(wl, out, ref, n_in, trunk=False):
@@ -195,4 +206,6 @@ def hier_errors(wl, out, ref, n_in, trunk=False):
     errs["L_D"] = rel(out["loss"][:, 0], ref["L_D"])
     errs["L_adv"] = rel(out["loss"][:, 1], ref["L_adv"])
     errs["L_pde"] = rel(out["loss"][:, 2], np.full(len(ref["L_D"]), ref["L_pde"]))
+    if "P_gp" in out:
+        errs["P_gp"] = rel(out["P_gp"], ref["P_gp"])
     return errs

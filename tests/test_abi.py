@@ -267,3 +267,29 @@ def test_trunk_gradient_penalty_validation():
                                                  FAKE, FAKE, FAKE, FAKE, need, None) == pigan.EINVAL
     assert pigan.lib().pigan_trunk_step_grads(*args, FAKE, FAKE, FAKE, FAKE, FAKE, need, None) == pigan.ENOTSUP
     assert b"pigan_trunk_step_grads_gp" in pigan.lib().pigan_last_error()
+
+
+def test_hier_gradient_penalty_validation():
+    """Both hierarchical _gp entry points: the penalty's buffers are in the
+    workspace, the plain entries refuse a penalty and name the _gp entry, the
+    _gp entries need the mixing weights and a finite lambda_gp >= 0."""
+    L = pigan.lib()
+    for wl, mk, ws_fn, plain_fn, gp_fn, n_gen in (
+            (configs.H2, pigan.hier_desc, L.pigan_hier_workspace_bytes, L.pigan_hier_step_grads,
+             L.pigan_hier_step_grads_gp, 2),
+            (configs.HT5, pigan.hier_trunk_desc, L.pigan_hier_trunk_workspace_bytes, L.pigan_hier_trunk_step_grads,
+             L.pigan_hier_trunk_step_grads_gp, 1)):
+        d = mk(wl, 21, 16, 16, 16, lambda_gp=10.0)
+        need = int(ws_fn(C.byref(d)))
+        plain = int(ws_fn(C.byref(mk(wl, 21, 16, 16, 16))))
+        assert need > plain > 0, wl.name
+        head = (C.byref(d), *([FAKE] * (n_gen + 5)), None, 0.0, FAKE, FAKE, FAKE, FAKE, FAKE)
+        outs = (FAKE,) * (n_gen + 2)
+        assert plain_fn(*head, *outs, FAKE, FAKE, need, None) == pigan.ENOTSUP
+        assert gp_fn.__name__.encode() in L.pigan_last_error()
+        assert gp_fn(*head, None, *outs, FAKE, FAKE, FAKE, need, None) == pigan.EINVAL      # no gp_eps
+        assert gp_fn(*head, FAKE, *outs, FAKE, FAKE, FAKE, need - 1, None) == pigan.EWORKSPACE
+        for bad in (-1.0, float("inf")):
+            e = mk(wl, 21, 16, 16, 16, lambda_gp=bad)
+            assert int(ws_fn(C.byref(e))) == 0
+            assert gp_fn(C.byref(e), *head[1:], FAKE, *outs, FAKE, FAKE, FAKE, 1 << 40, None) == pigan.EINVAL

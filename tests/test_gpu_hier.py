@@ -38,25 +38,27 @@ def _say(msg):
     sys.stdout.flush()
 
 
-def _oracle(wl, hi, real, lam, f_const, chunk=None, prec=None, trunk=False):
+def _oracle(wl, hi, real, lam, f_const, chunk=None, prec=None, trunk=False, lambda_gp=0.0, gp_eps=None):
     b, h = hi.base, hi.hier
     pY, pU = (b.pT[0], None) if trunk else (b.pY[0], b.pU[0])
     return oracle.train_step_hier(wl.gen_shape(), (real.shape[2], wl.L_D, wl.W_D), wl.d, pY, pU, hi.pD,
                                   b.z[0], b.xc[0], b.xsY[0], b.xsU[0], np.full((wl.S, wl.P), f_const), h.idxY, h.idxU,
-                                  h.idxF, real, h.w, lambda_pde=lam, chunk_S=chunk, prec=prec, trunk=trunk)
+                                  h.idxF, real, h.w, lambda_pde=lam, chunk_S=chunk, prec=prec, trunk=trunk,
+                                  lambda_gp=lambda_gp, gp_eps=gp_eps)
 
 
-def _compare(wl, hi, real, lam, fc, out, ref, case, trunk=False):
+def _compare(wl, hi, real, lam, fc, out, ref, case, trunk=False, lambda_gp=0.0, gp_eps=None):
     errs = hier_errors(wl, out, ref, real.shape[2], trunk=trunk)
     tol = TOL[wl.dtype]
     if max(errs.values()) <= tol:
         check(errs, tol, case)
         return
-    model = _oracle(wl, hi, real, lam, fc, prec=wl.dtype, trunk=trunk)
-    check_conditioned(errs, hier_errors(wl, dict(gY=model["gY"], gU=model["gU"], gD=model["gD"],
-                                                 loss=np.stack([model["L_D"], model["L_adv"],
-                                                                np.full(len(model["L_D"]), model["L_pde"])], 1)),
-                                         ref, real.shape[2], trunk=trunk), tol, case)
+    model = _oracle(wl, hi, real, lam, fc, prec=wl.dtype, trunk=trunk, lambda_gp=lambda_gp, gp_eps=gp_eps)
+    mout = dict(gY=model["gY"], gU=model["gU"], gD=model["gD"],
+                loss=np.stack([model["L_D"], model["L_adv"], np.full(len(model["L_D"]), model["L_pde"])], 1))
+    if "P_gp" in out:
+        mout["P_gp"] = model["P_gp"]
+    check_conditioned(errs, hier_errors(wl, mout, ref, real.shape[2], trunk=trunk), tol, case)
 
 
 @pytest.mark.parametrize("case", list(CASES))
@@ -131,3 +133,44 @@ def test_hier_index_out_of_range_is_flagged():
     out = run_hier_gpu(wl, hi, real, idx=(iY, hi.hier.idxU, hi.hier.idxF))
     assert out["nonfinite"] == 1
     assert np.isfinite(out["gY"]).all() and np.isfinite(out["gD"]).all()
+
+
+GP_CASES = {
+    # name: (workload, sides, sensors per critic, free sensors per critic, lambda_pde, f_const, chunk_S, trunk)
+    "tiny_gp_1x2_fp32": (TINY.with_(S=3, B_r=3, seed=92), (1, 2), 4, 4, 0.5, 0.3, 0, False),
+    # pairs 0, 1 in the first chunk, pair 2 in the second, none in the third
+    "tiny_gp_chunked_fp32": (TINY.with_(S=5, B_r=3, seed=93), (1, 2), 4, 4, 0.5, 0.0, 2, False),
+    "c2_gp_1x2x4_bf16": (configs.C2.with_(n_sY=256, n_sU=256, S=4, P=1024, B_r=4, seed=94), (1, 2, 4), 16, 16, 0.0,
+                         0.0, 0, False),
+    "c2_gp_1x4x8_81critics_bf16": (configs.C2.with_(n_sY=256, n_sU=256, S=4, P=256, B_r=4, seed=95), (1, 4, 8), 4,
+                                   4, 0.0, 0.0, 0, False),
+    "tiny_trunk5_gp_fp32": (TINY.with_(arch="hier_trunk", L=5, S=3, B_r=2, seed=96), (1, 2), 4, 4, 0.5, 0.3, 0,
+                            True),
+    "c2_trunk5_gp_1x2x4_bf16": (configs.HT5.with_(S=4, P=1024, B_r=4, seed=97), (1, 2, 4), 16, 16, 0.0, 0.0, 0,
+                                True),
+}
+
+
+@pytest.mark.parametrize("case", list(GP_CASES))
+def test_hier_step_with_gradient_penalty(case):
+    """pigan_hier_step_grads_gp / pigan_hier_trunk_step_grads_gp: every
+    critic's gradients, L_D (with its penalty) and the penalties against the
+    oracle; the generator gradients are the plain step's, bit for bit."""
+    wl, sides, m, nf, lam, fc, chunk, trunk = GP_CASES[case]
+    _say(f"hier gradient penalty case={case} dtype={wl.dtype} sides={sides} L={wl.L} W={wl.W} S={wl.S} "
+         f"B_r={wl.B_r} chunk_S={chunk} trunk={trunk}")
+    hi = make_hier_inputs(wl, sides=sides, m_sensors=m, n_free=nf)
+    real = oracle.real_snapshots_hier(wl, hi, trunk_teacher=hi.base.tT[0] if trunk else None)
+    eps = np.random.default_rng(wl.seed + 5).random((hi.hier.D, min(wl.S, wl.B_r))).astype(np.float32)
+    lgp = 10.0
+    ref = _oracle(wl, hi, real, lam, fc, trunk=trunk, lambda_gp=lgp, gp_eps=eps)
+    run = run_hier_trunk_gpu if trunk else run_hier_gpu
+    out = run(wl, hi, real, lam=lam, chunk_S=chunk, f_const=fc, lambda_gp=lgp, gp_eps=eps)
+    plain = run(wl, hi, real, lam=lam, chunk_S=chunk, f_const=fc)
+    assert out["nonfinite"] == 0 and np.all(ref["P_gp"] > 0)
+    np.testing.assert_array_equal(out["gY"], plain["gY"])
+    if trunk:
+        out["gU"] = None
+    else:
+        np.testing.assert_array_equal(out["gU"], plain["gU"])
+    _compare(wl, hi, real, lam, fc, out, ref, case, trunk=trunk, lambda_gp=lgp, gp_eps=eps)
