@@ -6,7 +6,13 @@ bf16), in the launch configuration the benchmark times:
 * the three losses against the oracle evaluated at full size;
 * gradients through a property that holds at any size: the step is a mean
   over noise samples, so the full step equals the average of the steps on
-  the two halves of the samples (same real batch)."""
+  the two halves of the samples (same real batch).
+
+The grouped 16-subdomain workload (4x256, S=128, P=1024) and the 6x1024 step
+with the 5x2048 critic (S=1024, P=2048) get sampled jets of several groups
+and the same sample-split property at their full sizes; their real batches
+are seeded Gaussian snapshots there (the property holds for any real batch,
+and the fp64 teacher at that size is beyond the CPU budget of a test)."""
 import numpy as np
 import pytest
 
@@ -126,3 +132,53 @@ def test_full_step_is_mean_of_half_steps(full):
         halves.append(run_step_gpu(WL, h, real))
     errs = {k: rel(0.5 * (halves[0][k] + halves[1][k]), a[k]) for k in ("gY", "gU", "gD", "loss")}
     check(errs, 1e-4, "sample split")
+
+
+def test_full_grouped_jets_sampled():
+    """C4 at full size: jets of groups 0, 9 and 15 at 12 sampled (sample,
+    point) pairs each against the oracle."""
+    import torch
+    wl = configs.C4
+    print(f"full-size grouped jets, sampled: {wl.name}", flush=True)
+    inp = make_inputs(wl)
+    shape = wl.gen_shape()
+    rng = np.random.default_rng(13)
+    z, xc = to_dev(inp.z), to_dev(inp.xc)
+    for name, p, order in (("Y", inp.pY, 1), ("U", inp.pU, 2)):
+        jet = pigan.gen_forward(to_dev(p), shape, wl.d, z, xc, order, dtype=wl.dtype)
+        torch.cuda.synchronize()
+        errs = {}
+        for g in (0, 9, 15):
+            ss = rng.integers(0, wl.S, 12)
+            pp = rng.integers(0, wl.P, 12)
+            got = jet[g][:, ss, pp].cpu().numpy()
+            o = oracle.gen_forward(p[g], shape, wl.d, inp.xc[g][ss, pp], inp.z[g][ss], order)
+            ref = [o["y"]] + [o["dy"][i] for i in range(wl.d)] + \
+                  ([o["ddy"][i] for i in range(wl.d)] if order >= 2 else [])
+            errs.update({f"{name}.g{g}.c{k}": rel(got[k], ref[k]) for k in range(len(ref))})
+        del jet
+        check(errs, TOL[wl.dtype], f"{wl.name} jets {name}")
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("wl", [configs.C4, configs.C5], ids=["c4", "c5"])
+def test_full_step_is_mean_of_half_steps_large(wl):
+    """The grouped and the large step at full size, in the benchmark's launch
+    configuration (automatic chunking): every gradient and loss of the full
+    step equals the mean of the two half-sample steps (same real batch)."""
+    import torch
+    print(f"full-size sample split: {wl.name} S={wl.S} P={wl.P}", flush=True)
+    inp = make_inputs(wl)
+    real = np.random.default_rng(wl.seed + 3).standard_normal((wl.G, wl.B_r, wl.n_in)).astype(np.float32)
+    a = run_step_gpu(wl, inp, real)
+    assert a["nonfinite"] == 0
+    halves = []
+    for lo, hi in ((0, wl.S // 2), (wl.S // 2, wl.S)):
+        h = make_inputs(wl)
+        h.z = inp.z[:, lo:hi].copy()
+        h.xc = inp.xc[:, lo:hi].copy()
+        halves.append(run_step_gpu(wl, h, real))
+        assert halves[-1]["nonfinite"] == 0
+        torch.cuda.empty_cache()
+    errs = {k: rel(0.5 * (halves[0][k] + halves[1][k]), a[k]) for k in ("gY", "gU", "gD", "loss")}
+    check(errs, 1e-4, f"{wl.name} sample split")
