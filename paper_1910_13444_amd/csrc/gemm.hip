@@ -20,7 +20,7 @@
 //   the skip cotangent (reverse) in the same epilogues.
 // k_gemm_dw  : dW = sum_rows dA^T H (split over rows, fp32 partials), plus
 //              the bias cotangent sum over the value rows.
-// The split partials are summed in fp64, in split order, by k_colsum.
+// The split partials are summed in fp64, in a fixed order, by k_colsum.
 //
 // Tiles: a 64-lane wave owns 32 points x 32*NT columns for every stream; the
 // block is WM x WN waves.  The MFMA computes W . X^T so that a lane holds one

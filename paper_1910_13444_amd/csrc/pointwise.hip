@@ -749,21 +749,22 @@ __global__ void k_hier_pde_loss(const double* __restrict__ acc, int slot, float 
 
 // ---------------------------------------------------------------------------
 // dst (+)= scale * sum over slots of part[g][slot][col], fp64, fixed order.
-// 32 columns x 8 slot groups per block; group q sums slots q, q+8, ...; the
-// eight group sums are added in group order.  Column col maps to
-// dst[(col / Jp) * J + col % Jp] and is skipped when col % Jp >= J (padding).
+// A block is 256 / SG column lanes x SG slot groups; group q sums slots q,
+// q + SG, ... and the SG group sums are combined by a fixed pairwise tree.
+// Column col maps to dst[(col / Jp) * J + col % Jp] and is skipped when
+// col % Jp >= J (padding).  VEC consecutive columns per lane (VEC = 4: one
+// 16-byte load per slot); the per-column summation order depends on SG only.
+// Few columns take many slot groups so that a launch still spans the chip.
 // ---------------------------------------------------------------------------
-// VEC consecutive columns per lane (VEC = 4: one 16-byte load per slot, 512
-// contiguous bytes per slot group); the per-column summation order is the
-// same for every VEC.
-template <class Tin, int VEC>
+template <class Tin, int VEC, int SG>
 __global__ void __launch_bounds__(256)
 k_colsum(const Tin* __restrict__ part, int64_t p_g, int n_slots, int64_t slot_stride, int64_t ncols, int Jp, int J,
          float* dst, int64_t d_g, int accumulate, float scale, int32_t* nonfinite) {
-  __shared__ double red[8][32 * VEC];
+  constexpr int LANES = 256 / SG;
+  __shared__ double red[SG][LANES * VEC];
   const int g = blockIdx.z;
-  const int lane = threadIdx.x & 31, grp = threadIdx.x >> 5;
-  const int64_t col0 = ((int64_t)blockIdx.x * 32 + lane) * VEC;
+  const int lane = threadIdx.x % LANES, grp = threadIdx.x / LANES;
+  const int64_t col0 = ((int64_t)blockIdx.x * LANES + lane) * VEC;
   double s[VEC];
 #pragma unroll
   for (int e = 0; e < VEC; ++e) s[e] = 0.0;
@@ -771,7 +772,7 @@ k_colsum(const Tin* __restrict__ part, int64_t p_g, int n_slots, int64_t slot_st
     const Tin* src = part + g * p_g + col0;
     if constexpr (VEC == 4) {
 #pragma unroll 4
-      for (int q = grp; q < n_slots; q += 8) {
+      for (int q = grp; q < n_slots; q += SG) {
         const float4 v = *(const float4*)(src + (int64_t)q * slot_stride);
         s[0] += (double)v.x;
         s[1] += (double)v.y;
@@ -780,19 +781,25 @@ k_colsum(const Tin* __restrict__ part, int64_t p_g, int n_slots, int64_t slot_st
       }
     } else {
 #pragma unroll 8
-      for (int q = grp; q < n_slots; q += 8) s[0] += (double)src[(int64_t)q * slot_stride];
+      for (int q = grp; q < n_slots; q += SG) s[0] += (double)src[(int64_t)q * slot_stride];
     }
   }
 #pragma unroll
   for (int e = 0; e < VEC; ++e) red[grp][lane * VEC + e] = s[e];
   __syncthreads();
+#pragma unroll
+  for (int h = SG / 2; h >= 1; h >>= 1) {
+    if (grp < h) {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) red[grp][lane * VEC + e] += red[grp + h][lane * VEC + e];
+    }
+    __syncthreads();
+  }
   if (grp == 0 && col0 < ncols) {
 #pragma unroll
     for (int e = 0; e < VEC; ++e) {
       const int64_t col = col0 + e;
-      double v = 0.0;
-#pragma unroll
-      for (int q = 0; q < 8; ++q) v += red[q][lane * VEC + e];
+      const double v = red[0][lane * VEC + e];
       const int64_t n = col / Jp;
       const int j = (int)(col % Jp);
       if (j < J) {
@@ -1175,17 +1182,30 @@ hipError_t launch_colsum(const Tin* part, int64_t p_g, int n_slots, int64_t slot
   if (ncols <= 0) return hipSuccess;
   // four columns per lane where every slot row and group slab is 16-byte
   // aligned and whole (the workspace is 256-byte aligned)
+  int vec = 1;
   if constexpr (sizeof(Tin) == 4) {
-    if (ncols % 4 == 0 && slot_stride % 4 == 0 && p_g % 4 == 0 && ((uintptr_t)part & 15) == 0) {
-      k_colsum<Tin, 4><<<dim3(nblk(ncols, 128), 1, G), 256, 0, st>>>(part, p_g, n_slots, slot_stride, ncols, Jp, J,
-                                                                    dst, d_g, accumulate, scale, nonfinite);
+    if (ncols % 4 == 0 && slot_stride % 4 == 0 && p_g % 4 == 0 && ((uintptr_t)part & 15) == 0) vec = 4;
+  }
+  // the fewest slot groups that still give 256 blocks (and no more groups than slots)
+  const int64_t lanes = (ncols + vec - 1) / vec;
+  int sg = 8;
+  while (sg < 128 && 2 * sg <= n_slots && (lanes + 256 / sg - 1) / (256 / sg) * G < 256) sg *= 4;
+  const unsigned nb = (unsigned)((lanes + 256 / sg - 1) / (256 / sg));
+#define PIGAN_COLSUM(V, S)                                                                                      \
+  k_colsum<Tin, V, S><<<dim3(nb, 1, G), 256, 0, st>>>(part, p_g, n_slots, slot_stride, ncols, Jp, J, dst, d_g, \
+                                                      accumulate, scale, nonfinite)
+  if constexpr (sizeof(Tin) == 4) {
+    if (vec == 4) {
+      if (sg == 8) PIGAN_COLSUM(4, 8);
+      else if (sg == 32) PIGAN_COLSUM(4, 32);
+      else PIGAN_COLSUM(4, 128);
       return hipGetLastError();
     }
   }
-  {
-    k_colsum<Tin, 1><<<dim3(nblk(ncols, 32), 1, G), 256, 0, st>>>(part, p_g, n_slots, slot_stride, ncols, Jp, J, dst,
-                                                                  d_g, accumulate, scale, nonfinite);
-  }
+  if (sg == 8) PIGAN_COLSUM(1, 8);
+  else if (sg == 32) PIGAN_COLSUM(1, 32);
+  else PIGAN_COLSUM(1, 128);
+#undef PIGAN_COLSUM
   return hipGetLastError();
 }
 template hipError_t launch_colsum<float>(const float*, int64_t, int, int64_t, int64_t, int, int, float*, int64_t, int,
