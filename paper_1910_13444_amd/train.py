@@ -17,6 +17,10 @@ on the current stream.
   one generator update against the updated critic; "parallel" -- each network
   takes steps_per_exchange updates against the copy of the other it received
   at the last exchange, then the copies are exchanged (device copies).
+* Optional critic gradient penalty (lambda_gp > 0, the WGAN-GP member of the
+  critic family the paper cites, Sec. I.C, Sec. II.C): every step call takes
+  fresh mixing weights, one per (critic, pair), uniform on [0, 1) from a
+  seeded device generator (or from a caller's function of the call index).
 """
 from __future__ import annotations
 
@@ -90,6 +94,8 @@ class TrainConfig:
     init_scale: float = 2.0 ** 15
     growth_interval: int = 2000
     chunk_S: int = 0
+    lambda_gp: float = 0.0             # critic gradient penalty weight (0: none)
+    gp_seed: int = 0                   # seed of the penalty's mixing weights
 
 
 class Trainer:
@@ -98,10 +104,15 @@ class Trainer:
     Adam states, the loss scale and the schedule.  `inputs` are the batch's
     device tensors: z, xc, xsY, xsU, real, w_group (and optionally f); for a
     hierarchy (arch "hier" or "hier_trunk", one generator, no group axis) z,
-    xc, xsY, xsU, real, idxY, idxU, idxF, w_disc (and optionally f)."""
+    xc, xsY, xsU, real, idxY, idxU, idxF, w_disc (and optionally f).
+    With cfg.lambda_gp > 0, gp_eps_fn(call_index) -> [critics, min(S, B_r)]
+    fp32 device tensor supplies the penalty's mixing weights of each step
+    call (default: uniform draws from a device generator seeded gp_seed)."""
 
-    def __init__(self, wl: Workload, gen: list[torch.Tensor], pD: torch.Tensor, inputs: dict, cfg: TrainConfig):
+    def __init__(self, wl: Workload, gen: list[torch.Tensor], pD: torch.Tensor, inputs: dict, cfg: TrainConfig,
+                 gp_eps_fn=None):
         self.wl, self.cfg, self.inp = wl, cfg, inputs
+        lgp = float(cfg.lambda_gp)
         self.trunk = wl.trunk_gen
         self.hier = wl.is_hier
         if cfg.schedule not in ("sequential", "parallel"):
@@ -111,19 +122,30 @@ class Trainer:
             m = (inputs["idxY"].shape[1], inputs["idxU"].shape[1], inputs["idxF"].shape[1])
             if self.trunk:
                 self.desc = pigan.hier_trunk_desc(wl, D, *m, S=S, B_r=B_r, chunk_S=cfg.chunk_S,
-                                                  lambda_pde=wl.lambda_pde)
+                                                  lambda_pde=wl.lambda_pde, lambda_gp=lgp)
                 self.step_fn = pigan.HierTrunkStep(self.desc)
             else:
-                self.desc = pigan.hier_desc(wl, D, *m, S=S, B_r=B_r, chunk_S=cfg.chunk_S, lambda_pde=wl.lambda_pde)
+                self.desc = pigan.hier_desc(wl, D, *m, S=S, B_r=B_r, chunk_S=cfg.chunk_S, lambda_pde=wl.lambda_pde,
+                                            lambda_gp=lgp)
                 self.step_fn = pigan.HierStep(self.desc)
+            n_crit = D
         elif self.trunk:
             S, B_r = inputs["z"].shape[1], inputs["real"].shape[1]
-            self.desc = pigan.trunk_desc(wl, S=S, B_r=B_r, chunk_S=cfg.chunk_S)
+            self.desc = pigan.trunk_desc(wl, S=S, B_r=B_r, chunk_S=cfg.chunk_S, lambda_gp=lgp)
             self.step_fn = pigan.TrunkStep(self.desc)
+            n_crit = inputs["z"].shape[0]
         else:
             S, B_r = inputs["z"].shape[1], inputs["real"].shape[1]
-            self.desc = pigan.step_desc(wl, S=S, B_r=B_r, chunk_S=cfg.chunk_S)
+            self.desc = pigan.step_desc(wl, S=S, B_r=B_r, chunk_S=cfg.chunk_S, lambda_gp=lgp)
             self.step_fn = pigan.TrainStep(self.desc)
+            n_crit = inputs["z"].shape[0]
+        self.gp_shape = (n_crit, min(S, B_r))
+        self.gp_eps_fn = gp_eps_fn
+        self.gp_gen = None
+        if lgp > 0 and gp_eps_fn is None:
+            self.gp_gen = torch.Generator(device=inputs["z"].device)
+            self.gp_gen.manual_seed(int(cfg.gp_seed))
+        self.calls = 0
         self.gen = [g.contiguous() for g in gen]
         self.pD = pD.contiguous()
         self.opt_g = [Adam(g, cfg.lr_g, cfg.beta1, cfg.beta2, cfg.eps) for g in self.gen]
@@ -135,27 +157,36 @@ class Trainer:
         self.gen_copy = [g.clone() for g in self.gen]
         self.pD_copy = self.pD.clone()
 
+    def _gp_eps(self):
+        if self.cfg.lambda_gp <= 0:
+            return None
+        if self.gp_eps_fn is not None:
+            return self.gp_eps_fn(self.calls)
+        return torch.rand(self.gp_shape, generator=self.gp_gen, device=self.pD.device, dtype=torch.float32)
+
     def _call(self, gen, pD):
         if self.scaler is not None:
             self.desc.loss_scale = self.scaler.scale
         i = self.inp
+        eps = self._gp_eps()
+        self.calls += 1
         if self.hier:
             idx = (i["idxY"], i["idxU"], i["idxF"], i["real"], i["w_disc"])
             if self.trunk:
                 o = self.step_fn(gen[0], pD, i["z"], i["xc"], i["xsY"], i["xsU"], *idx, f=i.get("f"),
-                                 f_const=self.wl.f_const)
+                                 f_const=self.wl.f_const, gp_eps=eps)
                 grads_g = [o.gT]
             else:
                 o = self.step_fn(gen[0], gen[1], pD, i["z"], i["xc"], i["xsY"], i["xsU"], *idx, f=i.get("f"),
-                                 f_const=self.wl.f_const)
+                                 f_const=self.wl.f_const, gp_eps=eps)
                 grads_g = [o.gY, o.gU]
         elif self.trunk:
             o = self.step_fn(gen[0], pD, i["z"], i["xc"], i["xsY"], i["xsU"], i["real"], f=i.get("f"),
-                             f_const=self.wl.f_const, w_group=i["w_group"])
+                             f_const=self.wl.f_const, w_group=i["w_group"], gp_eps=eps)
             grads_g = [o.gT]
         else:
             o = self.step_fn(gen[0], gen[1], pD, i["z"], i["xc"], i["xsY"], i["xsU"], i["real"], f=i.get("f"),
-                             f_const=self.wl.f_const, w_group=i["w_group"])
+                             f_const=self.wl.f_const, w_group=i["w_group"], gp_eps=eps)
             grads_g = [o.gY, o.gU]
         self.losses.append(o.loss.clone())
         skipped = False

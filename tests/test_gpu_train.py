@@ -183,3 +183,83 @@ def test_hier_trainer_matches_oracle(schedule, arch):
     print(f"weight change rel err: generator {eG:.3g}, critics {eD:.3g}; losses {eL:.3g}")
     assert losses.shape == ref_losses.shape
     assert eG <= 1e-3 and eD <= 1e-3 and eL <= 1e-4
+
+
+@pytest.mark.parametrize("schedule,arch", [("sequential", "pair"), ("parallel", "trunk"), ("sequential", "hier")])
+def test_trainer_with_gradient_penalty_matches_oracle(schedule, arch):
+    """The training loop with the critics' gradient penalty: each step call
+    takes its own mixing weights (a seeded host sequence fed to both sides in
+    call order); 3 rounds fp32 against the oracle loop."""
+    lgp = 5.0
+    rng = np.random.default_rng(47)
+    if arch == "hier":
+        from paper_1910_13444_amd.inputs import make_hier_inputs
+        wl = HW.with_(arch="hier", seed=48)
+        hi = make_hier_inputs(wl, sides=(1, 2), m_sensors=4, n_free=4)
+        b, h = hi.base, hi.hier
+        real = oracle.real_snapshots_hier(wl, hi)
+        n_crit, pD0 = h.D, hi.pD
+    else:
+        wl = TW.with_(arch=arch, L=3 if arch == "pair" else 5, seed=49)
+        inp = make_inputs(wl)
+        real = oracle.real_snapshots_trunk(wl, inp) if arch == "trunk" else oracle.real_snapshots(wl, inp)
+        n_crit, pD0 = wl.G, inp.pD[0]
+    n_gp = min(wl.S, real.shape[1])
+    eps = [rng.random((n_crit, n_gp)).astype(np.float32) for _ in range(40)]
+    _say(f"trainer {schedule} {arch} with gradient penalty {lgp}: 3 rounds fp32 vs the oracle loop")
+    calls = [0]
+
+    def next_eps():
+        e = eps[calls[0]]
+        calls[0] += 1
+        return e
+
+    cfg = TrainConfig(schedule=schedule, n_critic=2, steps_per_exchange=2, lr_g=1e-3, lr_d=2e-3, lambda_gp=lgp)
+    if arch == "hier":
+        f = np.full((wl.S, wl.P), wl.f_const)
+        dshape = (real.shape[2], wl.L_D, wl.W_D)
+        nY = b.pY.shape[1]
+
+        def fn(pG, pD):
+            o = oracle.train_step_hier(wl.gen_shape(), dshape, wl.d, pG[:nY], pG[nY:], pD, b.z[0], b.xc[0], b.xsY[0],
+                                       b.xsU[0], f, h.idxY, h.idxU, h.idxF, real, h.w, lambda_pde=wl.lambda_pde,
+                                       lambda_gp=lgp, gp_eps=next_eps())
+            loss = np.stack([o["L_D"], o["L_adv"], np.full(len(o["L_D"]), o["L_pde"])], 1)
+            return loss, np.concatenate([o["gY"], o["gU"]]), o["gD"]
+
+        def ti(a):
+            return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+        dev = dict(z=to_dev(b.z[0]), xc=to_dev(b.xc[0]), xsY=to_dev(b.xsY[0]), xsU=to_dev(b.xsU[0]),
+                   real=to_dev(real), idxY=ti(h.idxY), idxU=ti(h.idxU), idxF=ti(h.idxF), w_disc=to_dev(h.w))
+        gen = [to_dev(b.pY[0]), to_dev(b.pU[0])]
+        pG0 = np.concatenate([b.pY[0], b.pU[0]])
+        tr = Trainer(wl, gen, to_dev(pD0), dev, cfg, gp_eps_fn=lambda k: to_dev(eps[k]))
+    else:
+        gshape, dshape = wl.gen_shape(), wl.disc_shape()
+        f = np.full((wl.S, wl.P), wl.f_const)
+        nY = 0 if arch == "trunk" else inp.pY.shape[1]
+
+        def fn(pG, pD):
+            e = next_eps()[0]
+            if arch == "trunk":
+                o = oracle.train_step_group_trunk(gshape, dshape, wl.d, pG, pD, inp.z[0], inp.xc[0], inp.xsY[0],
+                                                  inp.xsU[0], f, real[0], w=float(inp.w_group[0]), lambda_gp=lgp,
+                                                  gp_eps=e)
+                return np.array([o["L_D"], o["L_adv"], o["L_pde"]]), o["gT"], o["gD"]
+            o = oracle.train_step_group(gshape, dshape, wl.d, pG[:nY], pG[nY:], pD, inp.z[0], inp.xc[0], inp.xsY[0],
+                                        inp.xsU[0], f, real[0], w=float(inp.w_group[0]), lambda_gp=lgp, gp_eps=e)
+            return np.array([o["L_D"], o["L_adv"], o["L_pde"]]), np.concatenate([o["gY"], o["gU"]]), o["gD"]
+        pG0 = inp.pT[0] if arch == "trunk" else np.concatenate([inp.pY[0], inp.pU[0]])
+        tr = _gpu_trainer(wl, inp, real, cfg)
+        tr.gp_eps_fn = lambda k: to_dev(eps[k])
+    losses = tr.run(3).cpu().numpy()
+    pG, pD, ref_losses = oracle_train(fn, pG0, pD0, 3, schedule=schedule, n_critic=2, steps_per_exchange=2,
+                                      lr_g=1e-3, lr_d=2e-3)
+    assert tr.calls == calls[0]
+    gpu_G = np.concatenate([g.cpu().numpy().ravel() for g in tr.gen])
+    gpu_D = tr.pD.cpu().numpy().reshape(np.shape(pD))
+    eG = rel(gpu_G - pG0, pG - pG0)
+    eD = rel(gpu_D - pD0, pD - pD0)
+    eL = rel(losses.reshape(ref_losses.shape), ref_losses)
+    print(f"weight change rel err: generator {eG:.3g}, critic {eD:.3g}; losses {eL:.3g}")
+    assert eG <= 1e-3 and eD <= 1e-3 and eL <= 1e-4
