@@ -749,7 +749,7 @@ __global__ void k_hier_pde_loss(const double* __restrict__ acc, int slot, float 
 
 // ---------------------------------------------------------------------------
 // dst (+)= scale * sum over slots of part[g][slot][col], fp64, fixed order.
-// A block is 256 / SG column lanes x SG slot groups; group q sums slots q,
+// A block is 256 / SG column lanes x SG slot groups (SG = 1, 8, 32 or 128); group q sums slots q,
 // q + SG, ... and the SG group sums are combined by a fixed pairwise tree.
 // Column col maps to dst[(col / Jp) * J + col % Jp] and is skipped when
 // col % Jp >= J (padding).  VEC consecutive columns per lane (VEC = 4: one
@@ -983,8 +983,36 @@ __global__ void k_zero(double* acc, int n, int32_t* flag) {
 
 // ---------------------------------------------------------------------------
 // weight casts: src fp32 [N][K] -> dst [N][Kp] (zero padded) and optionally
-// dstT [Kp][N]
+// dstT [Kp][N].  With dstT, k_cast_tr goes through 32 x 32 tiles in LDS so
+// that both outputs are stored in whole rows (a direct transposed store
+// writes one element per row of dstT); k_cast serves dst alone.
 // ---------------------------------------------------------------------------
+template <class T>
+__global__ void __launch_bounds__(256)
+k_cast_tr(const float* __restrict__ src, int64_t s_g, int N, int K, int Kp, T* __restrict__ dst,
+          T* __restrict__ dstT, int64_t d_g) {
+  __shared__ T tile[32][33];
+  const int g = blockIdx.z;
+  const int k0 = blockIdx.x * 32, n0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+#pragma unroll
+  for (int r = ty; r < 32; r += 8) {
+    const int n = n0 + r, k = k0 + tx;
+    T tv = Elem<T>::from_f(0.0f);
+    if (n < N && k < Kp) {
+      tv = Elem<T>::from_f(k < K ? src[g * s_g + (int64_t)n * K + k] : 0.0f);
+      if (dst) dst[g * d_g + (int64_t)n * Kp + k] = tv;
+    }
+    tile[r][tx] = tv;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = ty; r < 32; r += 8) {
+    const int k = k0 + r, n = n0 + tx;
+    if (k < Kp && n < N) dstT[g * d_g + (int64_t)k * N + n] = tile[tx][r];
+  }
+}
+
 template <class T>
 __global__ void k_cast(const float* __restrict__ src, int64_t s_g, int N, int K, int Kp, T* __restrict__ dst,
                        T* __restrict__ dstT, int64_t d_g) {
@@ -1186,23 +1214,26 @@ hipError_t launch_colsum(const Tin* part, int64_t p_g, int n_slots, int64_t slot
   if constexpr (sizeof(Tin) == 4) {
     if (ncols % 4 == 0 && slot_stride % 4 == 0 && p_g % 4 == 0 && ((uintptr_t)part & 15) == 0) vec = 4;
   }
-  // the fewest slot groups that still give 256 blocks (and no more groups than slots)
+  // the fewest slot groups that still give 256 blocks (and no more groups than
+  // slots; one group when there are at most two slots)
   const int64_t lanes = (ncols + vec - 1) / vec;
-  int sg = 8;
-  while (sg < 128 && 2 * sg <= n_slots && (lanes + 256 / sg - 1) / (256 / sg) * G < 256) sg *= 4;
+  int sg = n_slots <= 2 ? 1 : 8;
+  while (sg >= 8 && sg < 128 && 2 * sg <= n_slots && (lanes + 256 / sg - 1) / (256 / sg) * G < 256) sg *= 4;
   const unsigned nb = (unsigned)((lanes + 256 / sg - 1) / (256 / sg));
 #define PIGAN_COLSUM(V, S)                                                                                      \
   k_colsum<Tin, V, S><<<dim3(nb, 1, G), 256, 0, st>>>(part, p_g, n_slots, slot_stride, ncols, Jp, J, dst, d_g, \
                                                       accumulate, scale, nonfinite)
   if constexpr (sizeof(Tin) == 4) {
     if (vec == 4) {
-      if (sg == 8) PIGAN_COLSUM(4, 8);
+      if (sg == 1) PIGAN_COLSUM(4, 1);
+      else if (sg == 8) PIGAN_COLSUM(4, 8);
       else if (sg == 32) PIGAN_COLSUM(4, 32);
       else PIGAN_COLSUM(4, 128);
       return hipGetLastError();
     }
   }
-  if (sg == 8) PIGAN_COLSUM(1, 8);
+  if (sg == 1) PIGAN_COLSUM(1, 1);
+  else if (sg == 8) PIGAN_COLSUM(1, 8);
   else if (sg == 32) PIGAN_COLSUM(1, 32);
   else PIGAN_COLSUM(1, 128);
 #undef PIGAN_COLSUM
@@ -1245,7 +1276,11 @@ hipError_t launch_zero(double* acc, int n, int32_t* flag, hipStream_t st) {
 template <class T>
 hipError_t launch_cast(const float* src, int64_t s_g, int N, int K, int Kp, T* dst, T* dstT, int64_t d_g, int G,
                        hipStream_t st) {
-  k_cast<T><<<dim3(nblk((int64_t)N * Kp, 256), 1, G), 256, 0, st>>>(src, s_g, N, K, Kp, dst, dstT, d_g);
+  if (dstT)
+    k_cast_tr<T><<<dim3((unsigned)((Kp + 31) / 32), (unsigned)((N + 31) / 32), G), 256, 0, st>>>(src, s_g, N, K, Kp,
+                                                                                                dst, dstT, d_g);
+  else
+    k_cast<T><<<dim3(nblk((int64_t)N * Kp, 256), 1, G), 256, 0, st>>>(src, s_g, N, K, Kp, dst, dstT, d_g);
   return hipGetLastError();
 }
 
