@@ -182,3 +182,40 @@ def test_full_step_is_mean_of_half_steps_large(wl):
         torch.cuda.empty_cache()
     errs = {k: rel(0.5 * (halves[0][k] + halves[1][k]), a[k]) for k in ("gY", "gU", "gD", "loss")}
     check(errs, 1e-4, f"{wl.name} sample split")
+
+
+@pytest.mark.parametrize("wl", [configs.H2, configs.H273, configs.HT5], ids=["h2", "h273", "ht5"])
+def test_full_hier_step_is_mean_of_half_steps(wl):
+    """The domain-decomposition steps at their benchmark sizes (1 + 4 + 16 and
+    1 + 16 + 256 critics with the generator pair, 1 + 4 + 16 with the 5x128
+    trunk; S=256, P=1024), automatic chunking: every gradient and every
+    critic's losses of the full step equal the mean of the two half-sample
+    steps (same real batch: seeded Gaussian snapshots per critic)."""
+    import copy
+
+    import torch
+    from paper_1910_13444_amd.inputs import make_hier_inputs
+    from _parity import run_hier_gpu, run_hier_trunk_gpu
+    print(f"full-size hierarchy sample split: {wl.name} S={wl.S} P={wl.P}", flush=True)
+    hi = make_hier_inputs(wl, sides=wl.sides, m_sensors=wl.m_sensors, n_free=wl.n_free)
+    h0 = hi.hier
+    n_in = h0.idxY.shape[1] + h0.idxU.shape[1] + h0.idxF.shape[1] * (1 + wl.d)
+    real = np.random.default_rng(wl.seed + 3).standard_normal((hi.hier.D, wl.B_r, n_in)).astype(np.float32)
+    run = run_hier_trunk_gpu if wl.trunk_gen else run_hier_gpu
+
+    def step(h):
+        return run(wl, h, real, lam=wl.lambda_pde, f_const=wl.f_const)
+    a = step(hi)
+    assert a["nonfinite"] == 0
+    halves = []
+    for lo, up in ((0, wl.S // 2), (wl.S // 2, wl.S)):
+        h = copy.copy(hi)
+        h.base = copy.copy(hi.base)
+        h.base.z = hi.base.z[:, lo:up].copy()
+        h.base.xc = hi.base.xc[:, lo:up].copy()
+        halves.append(step(h))
+        assert halves[-1]["nonfinite"] == 0
+        torch.cuda.empty_cache()
+    keys = ("gY", "gD", "loss") if wl.trunk_gen else ("gY", "gU", "gD", "loss")
+    errs = {k: rel(0.5 * (halves[0][k] + halves[1][k]), a[k]) for k in keys}
+    check(errs, 1e-4, f"{wl.name} sample split")
