@@ -1510,7 +1510,9 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
       // persistent weight-resident kernel: two blocks per CU in total (one
       // for the five-stream skip variant)
       const int64_t ntiles = (npts + 31) / 32;
-      int64_t nb = (skip ? wr_blocks_per_cu<C, true>() : 2) * (int64_t)cu_count() / G;
+      // one-stream launches (sensor rows: few tiles, small blocks) take three
+      // blocks per CU
+      int64_t nb = (skip ? wr_blocks_per_cu<C, true>() : (C == 1 ? 3 : 2)) * (int64_t)cu_count() / G;
       if (nb < 1) nb = 1;
       if (nb > ntiles) nb = ntiles;
       dim3 grid((unsigned)nb, 1, G);
