@@ -1547,7 +1547,12 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
           return hipGetLastError();
         }
       }
-      {
+      if (((npts + 127) / 128) * ((a.N + 127) / 128) * G < 64) {
+        // short launches (a critic's batch): 32 points x 128 columns, four
+        // waves of one fragment, for four times the blocks
+        dim3 grid((unsigned)(((npts + 31) / 32) * ((a.N + 127) / 128)), 1, G);
+        k_gemm_nt<T, ND1, ND2, 1, 4, 1, 1, EPI, 2, true, 3><<<grid, 256, 0, st>>>(a);
+      } else {
         // 128 points x 128 columns, 2 x 2 fragments per wave, 3-stage ring
         dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 127) / 128)), 1, G);
         k_gemm_nt<T, ND1, ND2, 2, 2, 2, 2, EPI, 2, true, 3><<<grid, 256, 0, st>>>(a);
