@@ -39,77 +39,12 @@ Parameter packing (float32 master copy in, float64 internally):
 
 Pins: see tests/test_oracle_*.py (closed forms, finite differences of the jets
 and of every weight gradient, torch.autograd in float64, invariants).
-
-Precision models (optional, off by default).  They do not change what is
-computed; their distance from the exact result measures how strongly each
-output amplifies rounding (its conditioning):
-* prec="bf16" / "fp16": the storage points of a mixed-precision evaluation are
-  rounded to that format -- hidden-layer and discriminator weights, every
-  stored pre-activation, activation and pre-activation cotangent, the
-  discriminator input -- and matrix products accumulate in fp32 (the paper
-  keeps half-precision activations and gradients with single-precision
-  accumulation, Sec. III.C);
-* prec="fp32": every array operation of the oracle runs in fp32.
 """
 from __future__ import annotations
 
 import numpy as np
 
-F64 = np.float64      # working type of every array; fp32 only inside _working_type
-
-
-def _round_bf16(x):
-    """Round to bfloat16 (round to nearest, ties to even), returned as float64."""
-    f = np.asarray(x, np.float64).astype(np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
-    return u.astype(np.uint32).view(np.float32).astype(np.float64)
-
-
-class _Num:
-    """Storage rounding q() and matrix product mm() of one precision model."""
-
-    def __init__(self, prec=None):
-        self.prec = prec
-        if prec is None:
-            self.q = lambda x: x
-        elif prec == "fp32":
-            self.q = lambda x: np.asarray(x, np.float64).astype(np.float32).astype(np.float64)
-        elif prec == "bf16":
-            self.q = _round_bf16
-        elif prec == "fp16":
-            self.q = lambda x: np.asarray(x, np.float64).astype(np.float16).astype(np.float64)
-        else:
-            raise ValueError(f"unknown precision model {prec!r}")
-
-    def mm(self, a, b):
-        if self.prec is None:
-            return a @ b
-        return (np.asarray(a, np.float32) @ np.asarray(b, np.float32)).astype(np.float64)
-
-    def colsum(self, a):
-        if self.prec is None:
-            return a.sum(axis=0)
-        return np.asarray(a, np.float32).sum(axis=0).astype(np.float64)
-
-
-EXACT = _Num(None)
-
-
-class _working_type:
-    """Run the oracle's array arithmetic in another floating type."""
-
-    def __init__(self, dt):
-        self.dt = dt
-
-    def __enter__(self):
-        global F64
-        self.saved, F64 = F64, self.dt
-
-    def __exit__(self, *exc):
-        global F64
-        F64 = self.saved
-        return False
+F64 = np.float64
 
 
 # ----------------------------------------------------------------------------
@@ -164,7 +99,7 @@ def _tanh_derivs(a):
 # generator: forward jets and reverse pass
 # ----------------------------------------------------------------------------
 
-def gen_forward(params, shape, d: int, X, Z, order: int, keep: bool = False, prec=None):
+def gen_forward(params, shape, d: int, X, Z, order: int, keep: bool = False):
     """Evaluate a generator and its spatial jets at rows (X[n], Z[n]).
 
     X: [N, d] locations, Z: [N, n_z] noise (one row per evaluation point).
@@ -173,8 +108,6 @@ def gen_forward(params, shape, d: int, X, Z, order: int, keep: bool = False, pre
     Returns dict(y=[N], dy=[d, N] or None, ddy=[d, N] or None, cache).
     """
     in_dim, L, W = shape
-    num = prec if isinstance(prec, _Num) else _Num(prec)
-    q = num.q
     layers, w_out, b_out = unpack(params, in_dim, L, W)
     X = np.asarray(X, F64)
     Z = np.asarray(Z, F64)
@@ -190,16 +123,16 @@ def gen_forward(params, shape, d: int, X, Z, order: int, keep: bool = False, pre
     for l in range(L):
         if l > 0:
             Wl, bl = layers[l]
-            Wq = q(Wl).T
-            a = num.mm(h, Wq) + bl                  # bias enters the value only
-            da = [num.mm(g, Wq) for g in dh]
-            dda = [num.mm(g, Wq) for g in ddh]
+            Wq = Wl.T
+            a = h @ Wq + bl                  # bias enters the value only
+            da = [g @ Wq for g in dh]
+            dda = [g @ Wq for g in ddh]
         t, s, sp, _ = _tanh_derivs(a)
         if keep:
-            cache.append((q(a), [q(g) for g in da], [q(g) for g in dda], (h, dh, ddh)))
-        h = q(t)
-        dh = [q(s * g) for g in da]
-        ddh = [q(s * g2 + sp * g1 * g1) for g1, g2 in zip(da, dda)]
+            cache.append((a, list(da), list(dda), (h, dh, ddh)))
+        h = t
+        dh = [s * g for g in da]
+        ddh = [s * g2 + sp * g1 * g1 for g1, g2 in zip(da, dda)]
     y = h @ w_out + b_out
     out = dict(y=y,
                dy=np.stack([g @ w_out for g in dh]) if order >= 1 else None,
@@ -210,14 +143,12 @@ def gen_forward(params, shape, d: int, X, Z, order: int, keep: bool = False, pre
     return out
 
 
-def gen_backward(params, shape, d: int, X, Z, fwd, g_y, g_dy=None, g_ddy=None, prec=None) -> np.ndarray:
+def gen_backward(params, shape, d: int, X, Z, fwd, g_y, g_dy=None, g_ddy=None) -> np.ndarray:
     """Reverse pass of gen_forward (keep=True) for output cotangents.
 
     g_y: [N]; g_dy, g_ddy: [d, N] or None.  Returns the packed gradient (fp64).
     """
     in_dim, L, W = shape
-    num = prec if isinstance(prec, _Num) else _Num(prec)
-    q = num.q
     layers, w_out, b_out = unpack(params, in_dim, L, W)
     X = np.asarray(X, F64)
     Z = np.asarray(Z, F64)
@@ -252,29 +183,29 @@ def gen_backward(params, shape, d: int, X, Z, fwd, g_y, g_dy=None, g_ddy=None, p
             g = s * gdh[i]
             if gddh:
                 g = g + 2.0 * sp * da[i] * gddh[i]
-            gda.append(q(g))
-        gdda = [q(s * g) for g in gddh]
-        ga = q(ga)
+            gda.append(g)
+        gdda = [s * g for g in gddh]
+        ga = ga
         if l > 0:
             Wl, _ = layers[l]
             h, dh, ddh = prev
-            gW = num.mm(ga.T, h)
+            gW = ga.T @ h
             for i in range(len(gda)):
-                gW = gW + num.mm(gda[i].T, dh[i])
+                gW = gW + gda[i].T @ dh[i]
             for i in range(len(gdda)):
-                gW = gW + num.mm(gdda[i].T, ddh[i])
-            grads[l] = (gW, num.colsum(ga))
-            Wq = q(Wl)
-            gh = num.mm(ga, Wq)
-            gdh = [num.mm(g, Wq) for g in gda]
-            gddh = [num.mm(g, Wq) for g in gdda]
+                gW = gW + gdda[i].T @ ddh[i]
+            grads[l] = (gW, ga.sum(axis=0))
+            Wq = Wl
+            gh = ga @ Wq
+            gdh = [g @ Wq for g in gda]
+            gddh = [g @ Wq for g in gdda]
         else:
             gW1 = np.zeros((W, in_dim), F64)
             gW1[:, :d] = ga.T @ X
             gW1[:, d:] = ga.T @ Z
             for i in range(len(gda)):
-                gW1[:, i] += num.colsum(gda[i])   # a'_i = W1[:, i] for every row
-            grads[0] = (gW1, num.colsum(ga))
+                gW1[:, i] += gda[i].sum(axis=0)   # a'_i = W1[:, i] for every row
+            grads[0] = (gW1, ga.sum(axis=0))
     return pack(grads, gw_out, gb_out)
 
 
@@ -328,7 +259,7 @@ def trunk_skip(l: int) -> bool:
     return l >= 3 and l % 2 == 1
 
 
-def trunk_forward(params, shape, d: int, X, Z, order: int, keep: bool = False, prec=None):
+def trunk_forward(params, shape, d: int, X, Z, order: int, keep: bool = False):
     """Evaluate the trunk and the jets of both heads at rows (X[n], Z[n]).
 
     h_1 = tanh(W_1 [x ; z] + b_1); h_l = tanh(W_l h_{l-1} + b_l), plus h_{l-2}
@@ -338,8 +269,6 @@ def trunk_forward(params, shape, d: int, X, Z, order: int, keep: bool = False, p
     du, ddu) with dY/du [d, N] (order >= 1) and ddY/ddu [d, N] (order 2).
     """
     in_dim, L, W = shape
-    num = prec if isinstance(prec, _Num) else _Num(prec)
-    q = num.q
     layers, heads = trunk_unpack(params, in_dim, L, W)
     X = np.asarray(X, F64)
     Z = np.asarray(Z, F64)
@@ -354,13 +283,13 @@ def trunk_forward(params, shape, d: int, X, Z, order: int, keep: bool = False, p
     for l in range(1, L + 1):
         if l > 1:
             Wl, bl = layers[l - 1]
-            Wq = q(Wl).T
-            a = num.mm(h, Wq) + bl
-            da = [num.mm(g, Wq) for g in dh]
-            dda = [num.mm(g, Wq) for g in ddh]
+            Wq = Wl.T
+            a = h @ Wq + bl
+            da = [g @ Wq for g in dh]
+            dda = [g @ Wq for g in ddh]
         t, s, sp, _ = _tanh_derivs(a)
         if keep:
-            cache.append((q(a), [q(g) for g in da], [q(g) for g in dda], (h, dh, ddh)))
+            cache.append((a, list(da), list(dda), (h, dh, ddh)))
         nh = t
         ndh = [s * g for g in da]
         nddh = [s * g2 + sp * g1 * g1 for g1, g2 in zip(da, dda)]
@@ -369,9 +298,9 @@ def trunk_forward(params, shape, d: int, X, Z, order: int, keep: bool = False, p
             nh = nh + sh
             ndh = [g + gs for g, gs in zip(ndh, sdh)]
             nddh = [g + gs for g, gs in zip(nddh, sddh)]
-        h = q(nh)
-        dh = [q(g) for g in ndh]
-        ddh = [q(g) for g in nddh]
+        h = nh
+        dh = [g for g in ndh]
+        ddh = [g for g in nddh]
         acts.append((h, dh, ddh))
     out = {}
     for name, (w, b) in zip(("Y", "u"), heads):
@@ -384,13 +313,10 @@ def trunk_forward(params, shape, d: int, X, Z, order: int, keep: bool = False, p
     return out
 
 
-def trunk_backward(params, shape, d: int, X, Z, fwd, gY=None, gdY=None, gddY=None, gu=None, gdu=None, gddu=None,
-                   prec=None) -> np.ndarray:
+def trunk_backward(params, shape, d: int, X, Z, fwd, gY=None, gdY=None, gddY=None, gu=None, gdu=None, gddu=None) -> np.ndarray:
     """Reverse pass of trunk_forward (keep=True) for cotangents of the head
     jets (each [N] or [d, N]; None means zero).  Returns the packed gradient."""
     in_dim, L, W = shape
-    num = prec if isinstance(prec, _Num) else _Num(prec)
-    q = num.q
     layers, heads = trunk_unpack(params, in_dim, L, W)
     X = np.asarray(X, F64)
     Z = np.asarray(Z, F64)
@@ -428,7 +354,7 @@ def trunk_backward(params, shape, d: int, X, Z, fwd, gY=None, gdY=None, gddY=Non
             gdh = [a + b for a, b in zip(gdh, sdg)]
             gddh = [a + b for a, b in zip(gddh, sddg)]
         if trunk_skip(l):
-            pending[l - 2] = (q(gh), [q(g) for g in gdh], [q(g) for g in gddh])
+            pending[l - 2] = (gh, list(gdh), list(gddh))
         a, da, dda, prev = fwd["cache"][l - 1]
         t, s, sp, spp = _tanh_derivs(a)
         ga = s * gh
@@ -441,29 +367,29 @@ def trunk_backward(params, shape, d: int, X, Z, fwd, gY=None, gdY=None, gddY=Non
             g = s * gdh[i]
             if nd2:
                 g = g + 2.0 * sp * da[i] * gddh[i]
-            gda.append(q(g))
-        gdda = [q(s * g) for g in gddh]
-        ga = q(ga)
+            gda.append(g)
+        gdda = [s * g for g in gddh]
+        ga = ga
         if l > 1:
             Wl, _ = layers[l - 1]
             h, dh, ddh = prev
-            gW = num.mm(ga.T, h)
+            gW = ga.T @ h
             for i in range(nd1):
-                gW = gW + num.mm(gda[i].T, dh[i])
+                gW = gW + gda[i].T @ dh[i]
             for i in range(nd2):
-                gW = gW + num.mm(gdda[i].T, ddh[i])
-            grads[l - 1] = (gW, num.colsum(ga))
-            Wq = q(Wl)
-            gh = num.mm(ga, Wq)
-            gdh = [num.mm(g, Wq) for g in gda]
-            gddh = [num.mm(g, Wq) for g in gdda]
+                gW = gW + gdda[i].T @ ddh[i]
+            grads[l - 1] = (gW, ga.sum(axis=0))
+            Wq = Wl
+            gh = ga @ Wq
+            gdh = [g @ Wq for g in gda]
+            gddh = [g @ Wq for g in gdda]
         else:
             gW1 = np.zeros((W, in_dim), F64)
             gW1[:, :d] = ga.T @ X
             gW1[:, d:] = ga.T @ Z
             for i in range(nd1):
-                gW1[:, i] += num.colsum(gda[i])
-            grads[0] = (gW1, num.colsum(ga))
+                gW1[:, i] += gda[i].sum(axis=0)
+            grads[0] = (gW1, ga.sum(axis=0))
     return trunk_pack(grads, head_grads)
 
 
@@ -471,45 +397,39 @@ def trunk_backward(params, shape, d: int, X, Z, fwd, gY=None, gdY=None, gddY=Non
 # plain tanh MLP (discriminator)
 # ----------------------------------------------------------------------------
 
-def mlp_forward(params, shape, V, keep: bool = False, prec=None):
+def mlp_forward(params, shape, V, keep: bool = False):
     """D(v) = w_out . h_L + b_out with h_l = tanh(W_l h_{l-1} + b_l), h_0 = v.
 
     keep=True also returns the cache (activations h_0..h_L, pre-activations)."""
     in_dim, L, W = shape
-    num = prec if isinstance(prec, _Num) else _Num(prec)
-    q = num.q
     layers, w_out, b_out = unpack(params, in_dim, L, W)
-    h = q(np.asarray(V, F64))
+    h = np.asarray(V, F64)
     hs = [h]
     pre = []
     for Wl, bl in layers:
-        a = num.mm(h, q(Wl).T) + bl
-        pre.append(q(a))
-        h = q(np.tanh(a))
+        a = h @ Wl.T + bl
+        pre.append(a)
+        h = np.tanh(a)
         hs.append(h)
     y = h @ w_out + b_out
     return (y, dict(h=hs, a=pre)) if keep else y
 
 
-def mlp_backward(params, shape, cache, g_y, want_input_grad: bool = False, prec=None):
+def mlp_backward(params, shape, cache, g_y, want_input_grad: bool = False):
     in_dim, L, W = shape
-    num = prec if isinstance(prec, _Num) else _Num(prec)
-    q = num.q
     layers, w_out, b_out = unpack(params, in_dim, L, W)
     hs = cache["h"]
     g_y = np.asarray(g_y, F64)
-    # in the precision model the activations are re-formed from the stored
-    # (rounded) pre-activations, as a mixed-precision reverse pass does
-    tops = [np.tanh(a) for a in cache["a"]] if num.prec is not None else hs[1:]
+    tops = hs[1:]
     gw_out = tops[-1].T @ g_y
     gb_out = g_y.sum()
     gh = np.outer(g_y, w_out)
     grads = [None] * L
     for l in reversed(range(L)):
         t = tops[l]
-        ga = q((1.0 - t * t) * gh)
-        grads[l] = (num.mm(ga.T, hs[l]), num.colsum(ga))
-        gh = num.mm(ga, q(layers[l][0]))
+        ga = (1.0 - t * t) * gh
+        grads[l] = (ga.T @ hs[l], ga.sum(axis=0))
+        gh = ga @ layers[l][0]
     g = pack(grads, gw_out, gb_out)
     return (g, gh) if want_input_grad else g
 
@@ -523,16 +443,14 @@ def mlp_backward(params, shape, cache, g_y, want_input_grad: bool = False, prec=
 #   P   = w lambda_gp mean_b (||grad_v D(x_b)||_2 - 1)^2
 # is added to the critic loss L_D, and its gradient to the critic weights.
 
-def critic_input_grad(params, shape, V, prec=None):
+def critic_input_grad(params, shape, V):
     """g_b = dD/dv at every row v_b of V: the reverse pass of D to its input."""
-    num = prec if isinstance(prec, _Num) else _Num(prec)
-    _, cache = mlp_forward(params, shape, V, keep=True, prec=num)
-    _, g = mlp_backward(params, shape, cache, np.ones(np.asarray(V).shape[0], F64), want_input_grad=True,
-                        prec=num)
+    _, cache = mlp_forward(params, shape, V, keep=True)
+    _, g = mlp_backward(params, shape, cache, np.ones(np.asarray(V).shape[0], F64), want_input_grad=True)
     return g
 
 
-def tangent_output_grad(params, shape, V, Cdir, prec=None):
+def tangent_output_grad(params, shape, V, Cdir):
     """Weight gradient of J = sum_b dD(v_b + t c_b)/dt |_{t=0}.
 
     The directional derivative is carried forward with the activations
@@ -544,19 +462,17 @@ def tangent_output_grad(params, shape, V, Cdir, prec=None):
       g_h(l-1) = g_a W_l,  g_hdot(l-1) = g_adot W_l;
     at the top g_h = 0, g_hdot = w_out, dJ/dw_out = sum_b h_dot_L, dJ/db_out = 0."""
     in_dim, L, W = shape
-    num = prec if isinstance(prec, _Num) else _Num(prec)
-    q = num.q
     layers, w_out, b_out = unpack(params, in_dim, L, W)
-    h = q(np.asarray(V, F64))
-    hd = q(np.asarray(Cdir, F64))
+    h = np.asarray(V, F64)
+    hd = np.asarray(Cdir, F64)
     hs, hds, ts, ads = [h], [hd], [], []
     for Wl, bl in layers:
-        Wq = q(Wl)
-        a = q(num.mm(h, Wq.T) + bl)
-        ad = q(num.mm(hd, Wq.T))
+        Wq = Wl
+        a = h @ Wq.T + bl
+        ad = hd @ Wq.T
         t = np.tanh(a)
-        h = q(t)
-        hd = q((1.0 - t * t) * ad)
+        h = t
+        hd = (1.0 - t * t) * ad
         ts.append(t)
         ads.append(ad)
         hs.append(h)
@@ -568,34 +484,33 @@ def tangent_output_grad(params, shape, V, Cdir, prec=None):
     for l in reversed(range(L)):
         t, ad = ts[l], ads[l]
         sl = 1.0 - t * t
-        g_a = q(sl * g_h - 2.0 * t * sl * ad * g_hd)
-        g_ad = q(sl * g_hd)
-        grads[l] = (num.mm(g_a.T, hs[l]) + num.mm(g_ad.T, hds[l]), num.colsum(g_a))
-        Wq = q(layers[l][0])
-        g_h = num.mm(g_a, Wq)
-        g_hd = num.mm(g_ad, Wq)
+        g_a = sl * g_h - 2.0 * t * sl * ad * g_hd
+        g_ad = sl * g_hd
+        grads[l] = (g_a.T @ hs[l] + g_ad.T @ hds[l], g_a.sum(axis=0))
+        Wq = layers[l][0]
+        g_h = g_a @ Wq
+        g_hd = g_ad @ Wq
     return pack(grads, gw_out, 0.0)
 
 
-def gradient_penalty(params, shape, F, R, eps, lambda_gp, w=1.0, n_total=None, prec=None):
+def gradient_penalty(params, shape, F, R, eps, lambda_gp, w=1.0, n_total=None):
     """P (summed over these pairs with the 1/n_total of the mean) and dP/dphi.
 
     dP/dphi = sum_b c_b . dg_b/dphi with c_b = dP/dg_b held fixed, and
     c_b . g_b is the directional derivative of D at x_b along c_b, so dP/dphi
     is tangent_output_grad along c.  A row with g_b = 0 has no gradient
     direction; it contributes P but no weight gradient."""
-    num = prec if isinstance(prec, _Num) else _Num(prec)
     w = float(w)                                  # a float32 weight would round P to single precision
     eps = np.asarray(eps, F64)[:, None]
-    X = num.q(eps * np.asarray(R, F64) + (1.0 - eps) * np.asarray(F, F64))
+    X = eps * np.asarray(R, F64) + (1.0 - eps) * np.asarray(F, F64)
     n = X.shape[0] if n_total is None else n_total
-    g = critic_input_grad(params, shape, X, prec=num)
+    g = critic_input_grad(params, shape, X)
     nrm = np.sqrt((g * g).sum(axis=1))
     P = w * lambda_gp * float(((nrm - 1.0) ** 2).sum()) / n
     with np.errstate(divide="ignore", invalid="ignore"):
         coef = np.where(nrm > 0, (nrm - 1.0) / nrm, 0.0)
     Cdir = (2.0 * w * lambda_gp / n) * coef[:, None] * g
-    return P, tangent_output_grad(params, shape, X, Cdir, prec=num)
+    return P, tangent_output_grad(params, shape, X, Cdir)
 
 
 # ----------------------------------------------------------------------------
@@ -662,7 +577,7 @@ def snapshots(pY, pU, shape, d, xsY, xsU, z):
 # ----------------------------------------------------------------------------
 
 def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
-                     w=1.0, lambda_pde=1.0, chunk_S=None, prec=None, lambda_gp=0.0, gp_eps=None):
+                     w=1.0, lambda_pde=1.0, chunk_S=None, lambda_gp=0.0, gp_eps=None):
     """One subdomain group's losses and gradients.
 
     Returns dict(L_D, L_adv, L_pde, gY, gU, gD, P_gp) with gradients of
@@ -681,13 +596,6 @@ def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
     B = real.shape[0]
     nY = np.asarray(xsY).shape[0]
     chunk_S = S if not chunk_S else chunk_S
-    if prec == "fp32":
-        with _working_type(np.float32):
-            return train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real, w=w,
-                                    lambda_pde=lambda_pde, chunk_S=chunk_S, prec=None, lambda_gp=lambda_gp,
-                                    gp_eps=gp_eps)
-    num = _Num(prec)
-
     gY = np.zeros(np.asarray(pY).size, F64)
     gU = np.zeros(np.asarray(pU).size, F64)
     gD = np.zeros(np.asarray(pD).size, F64)
@@ -697,8 +605,8 @@ def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
     n_gp = min(S, B)
 
     # real snapshots: dL_D/dD(real_b) = -w/B
-    DR, hsR = mlp_forward(pD, dshape, real, keep=True, prec=num)
-    gD += mlp_backward(pD, dshape, hsR, np.full(B, -w / B, F64), prec=num)
+    DR, hsR = mlp_forward(pD, dshape, real, keep=True)
+    gD += mlp_backward(pD, dshape, hsR, np.full(B, -w / B, F64))
     sum_DR = DR.sum()
 
     for s0 in range(0, S, chunk_S):
@@ -708,27 +616,27 @@ def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
         # --- generators at the sensors (value only) -> fake snapshots
         XY, ZY = sensor_rows(xsY, zc)
         XU, ZU = sensor_rows(xsU, zc)
-        fY_s = gen_forward(pY, gshape, d, XY, ZY, 0, keep=True, prec=num)
-        fU_s = gen_forward(pU, gshape, d, XU, ZU, 0, keep=True, prec=num)
+        fY_s = gen_forward(pY, gshape, d, XY, ZY, 0, keep=True)
+        fU_s = gen_forward(pU, gshape, d, XU, ZU, 0, keep=True)
         F = np.concatenate([fY_s["y"].reshape(Sc, -1), fU_s["y"].reshape(Sc, -1)], axis=1)
         # --- generators at the collocation points with jets
         XC, ZC = colloc_rows(xc[sl], zc)
-        jY = gen_forward(pY, gshape, d, XC, ZC, 1, keep=True, prec=num)
-        jU = gen_forward(pU, gshape, d, XC, ZC, 2, keep=True, prec=num)
+        jY = gen_forward(pY, gshape, d, XC, ZC, 1, keep=True)
+        jU = gen_forward(pU, gshape, d, XC, ZC, 2, keep=True)
         fc = f[sl].reshape(-1)
         r = darcy_residual(jY["y"], jY["dy"], jU["dy"], jU["ddy"], fc)
         sum_r2 += float((r * r).sum())
         # --- discriminator on the fake snapshots: dL_D/dD(F_s) = w/S
-        DF, hsF = mlp_forward(pD, dshape, F, keep=True, prec=num)
+        DF, hsF = mlp_forward(pD, dshape, F, keep=True)
         sum_DF += float(DF.sum())
-        gDc, gF = mlp_backward(pD, dshape, hsF, np.full(Sc, w / S, F64), want_input_grad=True, prec=num)
+        gDc, gF = mlp_backward(pD, dshape, hsF, np.full(Sc, w / S, F64), want_input_grad=True)
         gD += gDc
         # --- gradient penalty on this chunk's pairs (F_b, R_b), b < n_gp
         if lambda_gp != 0.0:
             b1 = min(n_gp, s0 + Sc)
             if b1 > s0:
                 Pc, gPc = gradient_penalty(pD, dshape, F[:b1 - s0], real[s0:b1], np.asarray(gp_eps, F64)[s0:b1],
-                                           lambda_gp, w=w, n_total=n_gp, prec=num)
+                                           lambda_gp, w=w, n_total=n_gp)
                 P_gp += Pc
                 gD += gPc
         # L_adv = -w mean D(F): its snapshot cotangent is the negated L_D one
@@ -742,10 +650,10 @@ def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
         g_Uddy = np.stack([-q * eY for _ in range(d)])
         g_Uval = np.zeros_like(r)                   # u itself does not enter r
         # --- reverse passes through both generators
-        gY += gen_backward(pY, gshape, d, XY, ZY, fY_s, gF[:, :nY].reshape(-1), prec=num)
-        gU += gen_backward(pU, gshape, d, XU, ZU, fU_s, gF[:, nY:].reshape(-1), prec=num)
-        gY += gen_backward(pY, gshape, d, XC, ZC, jY, g_Yval, g_Ydy, prec=num)
-        gU += gen_backward(pU, gshape, d, XC, ZC, jU, g_Uval, g_Udy, g_Uddy, prec=num)
+        gY += gen_backward(pY, gshape, d, XY, ZY, fY_s, gF[:, :nY].reshape(-1))
+        gU += gen_backward(pU, gshape, d, XU, ZU, fU_s, gF[:, nY:].reshape(-1))
+        gY += gen_backward(pY, gshape, d, XC, ZC, jY, g_Yval, g_Ydy)
+        gU += gen_backward(pU, gshape, d, XC, ZC, jU, g_Uval, g_Udy, g_Uddy)
 
     L_D = w * (sum_DF / S - sum_DR / B) + P_gp
     L_adv = -w * sum_DF / S
@@ -753,7 +661,7 @@ def train_step_group(gshape, dshape, d, pY, pU, pD, z, xc, xsY, xsU, f, real,
     return dict(L_D=L_D, L_adv=L_adv, L_pde=L_pde, gY=gY, gU=gU, gD=gD, P_gp=P_gp)
 
 
-def train_step(wl, inp, real, lambda_pde=None, chunk_S=None, prec=None, lambda_gp=0.0, gp_eps=None):
+def train_step(wl, inp, real, lambda_pde=None, chunk_S=None, lambda_gp=0.0, gp_eps=None):
     """All groups of a workload.  ``inp`` is an inputs.StepInputs-like object,
     ``real`` the real snapshots [G, B_r, n_in].  Returns dict of stacked arrays:
     loss [G, 3] (L_D, L_adv, L_pde), gY [G, nY], gU [G, nU], gD [G, nD], and
@@ -768,8 +676,7 @@ def train_step(wl, inp, real, lambda_pde=None, chunk_S=None, prec=None, lambda_g
         f = inp.f[g] if inp.f is not None else np.full((S, P), inp.f_const)
         outs.append(train_step_group(gshape, dshape, wl.d, inp.pY[g], inp.pU[g], inp.pD[g],
                                      inp.z[g], inp.xc[g], inp.xsY[g], inp.xsU[g], f, real[g],
-                                     w=float(inp.w_group[g]), lambda_pde=lam, chunk_S=chunk_S,
-                                     prec=prec, lambda_gp=lambda_gp,
+                                     w=float(inp.w_group[g]), lambda_pde=lam, chunk_S=chunk_S, lambda_gp=lambda_gp,
                                      gp_eps=None if gp_eps is None else gp_eps[g]))
     return dict(loss=np.array([[o["L_D"], o["L_adv"], o["L_pde"]] for o in outs]),
                 gY=np.stack([o["gY"] for o in outs]),
@@ -789,7 +696,7 @@ def trunk_snapshots(pT, shape, d, xsY, xsU, z):
 
 
 def train_step_group_trunk(gshape, dshape, d, pT, pD, z, xc, xsY, xsU, f, real,
-                           w=1.0, lambda_pde=1.0, chunk_S=None, prec=None, lambda_gp=0.0, gp_eps=None):
+                           w=1.0, lambda_pde=1.0, chunk_S=None, lambda_gp=0.0, gp_eps=None):
     """One group's losses and gradients with the shared-trunk generator.
 
     Same losses as train_step_group (including its optional critic gradient
@@ -804,20 +711,14 @@ def train_step_group_trunk(gshape, dshape, d, pT, pD, z, xc, xsY, xsU, f, real,
     B = real.shape[0]
     nY = np.asarray(xsY).shape[0]
     chunk_S = S if not chunk_S else chunk_S
-    if prec == "fp32":
-        with _working_type(np.float32):
-            return train_step_group_trunk(gshape, dshape, d, pT, pD, z, xc, xsY, xsU, f, real, w=w,
-                                          lambda_pde=lambda_pde, chunk_S=chunk_S, prec=None, lambda_gp=lambda_gp,
-                                          gp_eps=gp_eps)
-    num = _Num(prec)
     gT = np.zeros(np.asarray(pT).size, F64)
     gD = np.zeros(np.asarray(pD).size, F64)
     sum_DF = 0.0
     sum_r2 = 0.0
     P_gp = 0.0
     n_gp = min(S, B)
-    DR, hsR = mlp_forward(pD, dshape, real, keep=True, prec=num)
-    gD += mlp_backward(pD, dshape, hsR, np.full(B, -w / B, F64), prec=num)
+    DR, hsR = mlp_forward(pD, dshape, real, keep=True)
+    gD += mlp_backward(pD, dshape, hsR, np.full(B, -w / B, F64))
     sum_DR = DR.sum()
     for s0 in range(0, S, chunk_S):
         sl = slice(s0, min(S, s0 + chunk_S))
@@ -826,24 +727,24 @@ def train_step_group_trunk(gshape, dshape, d, pT, pD, z, xc, xsY, xsU, f, real,
         # trunk at the Y sensors (Y head) and at the u sensors (u head)
         XY, ZY = sensor_rows(xsY, zc)
         XU, ZU = sensor_rows(xsU, zc)
-        fY_s = trunk_forward(pT, gshape, d, XY, ZY, 0, keep=True, prec=num)
-        fU_s = trunk_forward(pT, gshape, d, XU, ZU, 0, keep=True, prec=num)
+        fY_s = trunk_forward(pT, gshape, d, XY, ZY, 0, keep=True)
+        fU_s = trunk_forward(pT, gshape, d, XU, ZU, 0, keep=True)
         F = np.concatenate([fY_s["Y"].reshape(Sc, -1), fU_s["u"].reshape(Sc, -1)], axis=1)
         # trunk at the collocation points: jets of both heads
         XC, ZC = colloc_rows(xc[sl], zc)
-        jc = trunk_forward(pT, gshape, d, XC, ZC, 2, keep=True, prec=num)
+        jc = trunk_forward(pT, gshape, d, XC, ZC, 2, keep=True)
         fc = f[sl].reshape(-1)
         r = darcy_residual(jc["Y"], jc["dY"], jc["du"], jc["ddu"], fc)
         sum_r2 += float((r * r).sum())
-        DF, hsF = mlp_forward(pD, dshape, F, keep=True, prec=num)
+        DF, hsF = mlp_forward(pD, dshape, F, keep=True)
         sum_DF += float(DF.sum())
-        gDc, gF = mlp_backward(pD, dshape, hsF, np.full(Sc, w / S, F64), want_input_grad=True, prec=num)
+        gDc, gF = mlp_backward(pD, dshape, hsF, np.full(Sc, w / S, F64), want_input_grad=True)
         gD += gDc
         if lambda_gp != 0.0:
             b1 = min(n_gp, s0 + Sc)
             if b1 > s0:
                 Pc, gPc = gradient_penalty(pD, dshape, F[:b1 - s0], real[s0:b1], np.asarray(gp_eps, F64)[s0:b1],
-                                           lambda_gp, w=w, n_total=n_gp, prec=num)
+                                           lambda_gp, w=w, n_total=n_gp)
                 P_gp += Pc
                 gD += gPc
         gF = -gF
@@ -853,16 +754,16 @@ def train_step_group_trunk(gshape, dshape, d, pT, pD, z, xc, xsY, xsU, f, real,
         g_Ydy = np.stack([-q * eY * jc["du"][i] for i in range(d)])
         g_Udy = np.stack([-q * eY * jc["dY"][i] for i in range(d)])
         g_Uddy = np.stack([-q * eY for _ in range(d)])
-        gT += trunk_backward(pT, gshape, d, XY, ZY, fY_s, gY=gF[:, :nY].reshape(-1), prec=num)
-        gT += trunk_backward(pT, gshape, d, XU, ZU, fU_s, gu=gF[:, nY:].reshape(-1), prec=num)
-        gT += trunk_backward(pT, gshape, d, XC, ZC, jc, gY=g_Yval, gdY=g_Ydy, gdu=g_Udy, gddu=g_Uddy, prec=num)
+        gT += trunk_backward(pT, gshape, d, XY, ZY, fY_s, gY=gF[:, :nY].reshape(-1))
+        gT += trunk_backward(pT, gshape, d, XU, ZU, fU_s, gu=gF[:, nY:].reshape(-1))
+        gT += trunk_backward(pT, gshape, d, XC, ZC, jc, gY=g_Yval, gdY=g_Ydy, gdu=g_Udy, gddu=g_Uddy)
     L_D = w * (sum_DF / S - sum_DR / B) + P_gp
     L_adv = -w * sum_DF / S
     L_pde = w * lambda_pde * sum_r2 / (S * P)
     return dict(L_D=L_D, L_adv=L_adv, L_pde=L_pde, gT=gT, gD=gD, P_gp=P_gp)
 
 
-def train_step_trunk(wl, inp, real, lambda_pde=None, chunk_S=None, prec=None, lambda_gp=0.0, gp_eps=None):
+def train_step_trunk(wl, inp, real, lambda_pde=None, chunk_S=None, lambda_gp=0.0, gp_eps=None):
     """All groups of a trunk workload (inp.pT holds the trunk weights).
     Returns loss [G, 3], gT [G, nT], gD [G, nD], P_gp [G] (gp_eps is
     [G, min(S, B_r)] when lambda_gp > 0)."""
@@ -876,7 +777,7 @@ def train_step_trunk(wl, inp, real, lambda_pde=None, chunk_S=None, prec=None, la
         f = inp.f[g] if inp.f is not None else np.full((S, P), inp.f_const)
         outs.append(train_step_group_trunk(gshape, dshape, wl.d, inp.pT[g], inp.pD[g], inp.z[g], inp.xc[g],
                                            inp.xsY[g], inp.xsU[g], f, real[g], w=float(inp.w_group[g]),
-                                           lambda_pde=lam, chunk_S=chunk_S, prec=prec, lambda_gp=lambda_gp,
+                                           lambda_pde=lam, chunk_S=chunk_S, lambda_gp=lambda_gp,
                                            gp_eps=None if gp_eps is None else gp_eps[g]))
     return dict(loss=np.array([[o["L_D"], o["L_adv"], o["L_pde"]] for o in outs]),
                 gT=np.stack([o["gT"] for o in outs]),
@@ -892,7 +793,7 @@ def real_snapshots_trunk(wl, inp):
 
 
 def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, idxU, idxF, real, w,
-                    lambda_pde=0.0, chunk_S=None, prec=None, trunk=False, lambda_gp=0.0, gp_eps=None):
+                    lambda_pde=0.0, chunk_S=None, trunk=False, lambda_gp=0.0, gp_eps=None):
     """Domain decomposition (Sec. III.B.1): one generator pair, one critic per
     subdomain of every level.  Critic k sees the paper's snapshot of its
     subdomain: [Y at Y sensors idxY[k] | u at u sensors idxU[k] | the
@@ -916,12 +817,6 @@ def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, id
     S, P = xc.shape[0], xc.shape[1]
     D = len(pDs)
     chunk_S = S if not chunk_S else chunk_S
-    if prec == "fp32":
-        with _working_type(np.float32):
-            return train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, idxU, idxF, real, w,
-                                   lambda_pde=lambda_pde, chunk_S=chunk_S, prec=None, trunk=trunk,
-                                   lambda_gp=lambda_gp, gp_eps=gp_eps)
-    num = _Num(prec)
     gY = np.zeros(np.asarray(pY).size, F64)
     gU = np.zeros(0 if trunk else np.asarray(pU).size, F64)
     gD = np.zeros((D, np.asarray(pDs[0]).size), F64)
@@ -932,8 +827,8 @@ def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, id
     n_gp = min(S, np.asarray(real[0]).shape[0])
     for k in range(D):
         Rk = np.asarray(real[k], F64)
-        DR, hsR = mlp_forward(pDs[k], dshape, Rk, keep=True, prec=num)
-        gD[k] += mlp_backward(pDs[k], dshape, hsR, np.full(Rk.shape[0], -w[k] / Rk.shape[0], F64), prec=num)
+        DR, hsR = mlp_forward(pDs[k], dshape, Rk, keep=True)
+        gD[k] += mlp_backward(pDs[k], dshape, hsR, np.full(Rk.shape[0], -w[k] / Rk.shape[0], F64))
         sum_DR[k] = DR.sum()
     B = np.asarray(real[0]).shape[0]
     nYs, nUs = np.asarray(xsY).shape[0], np.asarray(xsU).shape[0]
@@ -945,20 +840,20 @@ def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, id
         XU, ZU = sensor_rows(xsU, zc)
         XC, ZC = colloc_rows(xc[sl], zc)
         if trunk:
-            fY_s = trunk_forward(pY, gshape, d, XY, ZY, 0, keep=True, prec=num)
-            fU_s = trunk_forward(pY, gshape, d, XU, ZU, 0, keep=True, prec=num)
+            fY_s = trunk_forward(pY, gshape, d, XY, ZY, 0, keep=True)
+            fU_s = trunk_forward(pY, gshape, d, XU, ZU, 0, keep=True)
             Ys = fY_s["Y"].reshape(Sc, nYs)
             Us = fU_s["u"].reshape(Sc, nUs)
-            jc = trunk_forward(pY, gshape, d, XC, ZC, 2, keep=True, prec=num)
+            jc = trunk_forward(pY, gshape, d, XC, ZC, 2, keep=True)
             jY = dict(y=jc["Y"], dy=jc["dY"])
             jU = dict(y=jc["u"], dy=jc["du"], ddy=jc["ddu"])
         else:
-            fY_s = gen_forward(pY, gshape, d, XY, ZY, 0, keep=True, prec=num)
-            fU_s = gen_forward(pU, gshape, d, XU, ZU, 0, keep=True, prec=num)
+            fY_s = gen_forward(pY, gshape, d, XY, ZY, 0, keep=True)
+            fU_s = gen_forward(pU, gshape, d, XU, ZU, 0, keep=True)
             Ys = fY_s["y"].reshape(Sc, nYs)
             Us = fU_s["y"].reshape(Sc, nUs)
-            jY = gen_forward(pY, gshape, d, XC, ZC, 1, keep=True, prec=num)
-            jU = gen_forward(pU, gshape, d, XC, ZC, 2, keep=True, prec=num)
+            jY = gen_forward(pY, gshape, d, XC, ZC, 1, keep=True)
+            jU = gen_forward(pU, gshape, d, XC, ZC, 2, keep=True)
         fc = f[sl].reshape(-1)
         r = darcy_residual(jY["y"], jY["dy"], jU["dy"], jU["ddy"], fc)
         sum_r2 += float((r * r).sum())
@@ -969,16 +864,16 @@ def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, id
         for k in range(D):
             iY, iU, iF = np.asarray(idxY[k]), np.asarray(idxU[k]), np.asarray(idxF[k])
             F = np.concatenate([Ys[:, iY], Us[:, iU], Nf[:, iF], xc[sl][:, iF, :].reshape(Sc, -1)], axis=1)
-            DF, hsF = mlp_forward(pDs[k], dshape, F, keep=True, prec=num)
+            DF, hsF = mlp_forward(pDs[k], dshape, F, keep=True)
             sum_DF[k] += float(DF.sum())
-            gDc, gF = mlp_backward(pDs[k], dshape, hsF, np.full(Sc, w[k] / S, F64), want_input_grad=True, prec=num)
+            gDc, gF = mlp_backward(pDs[k], dshape, hsF, np.full(Sc, w[k] / S, F64), want_input_grad=True)
             gD[k] += gDc
             if lambda_gp != 0.0:
                 b1 = min(n_gp, s0 + Sc)
                 if b1 > s0:
                     Pc, gPc = gradient_penalty(pDs[k], dshape, F[:b1 - s0], np.asarray(real[k], F64)[s0:b1],
                                                np.asarray(gp_eps, F64)[k, s0:b1], lambda_gp, w=w[k],
-                                               n_total=n_gp, prec=num)
+                                               n_total=n_gp)
                     P_gp[k] += Pc
                     gD[k] += gPc
             gF = -gF                                      # L_adv = -w mean D(F)
@@ -995,14 +890,14 @@ def train_step_hier(gshape, dshape, d, pY, pU, pDs, z, xc, xsY, xsU, f, idxY, id
         g_Udy = np.stack([-q * eY * jY["dy"][i] for i in range(d)])
         g_Uddy = np.stack([-q * eY for _ in range(d)])
         if trunk:
-            gY += trunk_backward(pY, gshape, d, XY, ZY, fY_s, gY=gYs.reshape(-1), prec=num)
-            gY += trunk_backward(pY, gshape, d, XU, ZU, fU_s, gu=gUs.reshape(-1), prec=num)
-            gY += trunk_backward(pY, gshape, d, XC, ZC, jc, gY=g_Yval, gdY=g_Ydy, gdu=g_Udy, gddu=g_Uddy, prec=num)
+            gY += trunk_backward(pY, gshape, d, XY, ZY, fY_s, gY=gYs.reshape(-1))
+            gY += trunk_backward(pY, gshape, d, XU, ZU, fU_s, gu=gUs.reshape(-1))
+            gY += trunk_backward(pY, gshape, d, XC, ZC, jc, gY=g_Yval, gdY=g_Ydy, gdu=g_Udy, gddu=g_Uddy)
         else:
-            gY += gen_backward(pY, gshape, d, XY, ZY, fY_s, gYs.reshape(-1), prec=num)
-            gU += gen_backward(pU, gshape, d, XU, ZU, fU_s, gUs.reshape(-1), prec=num)
-            gY += gen_backward(pY, gshape, d, XC, ZC, jY, g_Yval, g_Ydy, prec=num)
-            gU += gen_backward(pU, gshape, d, XC, ZC, jU, np.zeros_like(r), g_Udy, g_Uddy, prec=num)
+            gY += gen_backward(pY, gshape, d, XY, ZY, fY_s, gYs.reshape(-1))
+            gU += gen_backward(pU, gshape, d, XU, ZU, fU_s, gUs.reshape(-1))
+            gY += gen_backward(pY, gshape, d, XC, ZC, jY, g_Yval, g_Ydy)
+            gU += gen_backward(pU, gshape, d, XC, ZC, jU, np.zeros_like(r), g_Udy, g_Uddy)
     w = np.asarray(w, F64)
     return dict(L_D=w * (sum_DF / S - sum_DR / B) + P_gp, L_adv=-w * sum_DF / S,
                 L_pde=lambda_pde * sum_r2 / (S * P), gY=gY, gU=gU, gD=gD, P_gp=P_gp)
