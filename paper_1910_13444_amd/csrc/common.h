@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "pigan.h"
 
 namespace pigan {
@@ -55,6 +57,50 @@ template <> struct Elem<f16> {
 };
 
 // ---------------------------------------------------------------------------
+// Split products for fp32 storage.  A fragment of 8 fp32 values is cut into
+// bf16 pieces x = x0 + x1 (+ x2) by repeated round-to-nearest: each residual
+// is exact in fp32, so two pieces carry about 16 significand bits and three
+// pieces carry all 24 of an fp32 value.  Products of bf16 pieces are exact in
+// the matrix core's fp32 accumulator.
+//   PM_SPLIT2: x0 y0 + x0 y1 + x1 y0  (about 2^-16 relative; x1 y1 dropped)
+//   PM_SPLIT3: all pieces with i + j <= 2 (the terms dropped are below 2^-24
+//              relative), accumulated per operand stage and then in fp64
+//              by the kernels, so that long contractions do not round at
+//              fp32 precision at every step.
+// ---------------------------------------------------------------------------
+//   PM_F64:    the fp32 operands go through the fp64 matrix core (exact
+//              products, fp64 accumulation), rounded once at the end.
+enum ProdMode { PM_NATIVE = 0, PM_SPLIT2 = 2, PM_SPLIT3 = 3, PM_F64 = 4 };
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+template <int NP>
+__device__ __forceinline__ void split_frag(const f32x8& x, bf16x8 (&p)[NP]) {
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    float r = x[q];
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      const bf16 h = (bf16)r;
+      p[i][q] = h;
+      r -= (float)h;
+    }
+  }
+}
+
+// acc += b . a over one 16-wide chunk from split operands (smallest terms first)
+template <int NP>
+__device__ __forceinline__ void mma_split(f32x16& acc, const bf16x8 (&b)[NP], const bf16x8 (&a)[NP]) {
+  if constexpr (NP == 3) {
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[2], a[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[1], a[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[0], a[2], acc, 0, 0, 0);
+  }
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[1], a[0], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[0], a[1], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[0], a[0], acc, 0, 0, 0);
+}
+
+// ---------------------------------------------------------------------------
 // tanh and its derivatives with respect to the pre-activation a:
 //   t = tanh(a), s = dt/da = 1 - t^2, s' = -2 t s, s'' = 2 s (3 t^2 - 1).
 // With e = exp(-2|a|) and m = e - 1 (= expm1(-2|a|)):
@@ -80,6 +126,22 @@ __device__ __forceinline__ void tanh_ts(float a, float& t, float& s) {
   t = copysignf(ta, a);
   const float den = 1.0f + e;
   s = 4.0f * e * __builtin_amdgcn_rcpf(den * den);
+}
+
+// The same quantities evaluated in fp64 and rounded once (fp32-mode kernels:
+// every stored value then carries a single rounding).
+__device__ __forceinline__ void tanh_ts64(float a, float& t, float& s) {
+  const double x = -2.0 * fabs((double)a);
+  const double e = exp(x);
+  const double m = expm1(x);
+  t = (float)copysign(-m / (2.0 + m), (double)a);
+  s = (float)(4.0 * e / ((1.0 + e) * (1.0 + e)));
+}
+
+template <bool X64>
+__device__ __forceinline__ void tanh_pair(float a, float& t, float& s) {
+  if constexpr (X64) tanh_ts64(a, t, s);
+  else tanh_ts(a, t, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -134,6 +196,11 @@ template <class T> struct NtArgs {
   int32_t sY_ld; int32_t sU_ld; int32_t sU_off;
   Seg seg;
   int32_t N, K;
+  // fp32 storage: how the products are formed (ProdMode)
+  int32_t pm;
+  // two-term weights (16-bit storage): K = 2 kx, the weight rows hold
+  // [W_hi | W_lo] and the operand X (kx wide) is read twice
+  int32_t kx;
 };
 
 // per-kernel-family profiling hooks (host)
@@ -146,10 +213,13 @@ void prof_end(hipStream_t st);
 template <class T>
 hipError_t launch_gemm_nt(int epi, int nd1, int nd2, const NtArgs<T>& a, int G, hipStream_t st);
 
+// pm: ProdMode for fp32 storage; PM_SPLIT3 and PM_F64 write their split
+// partials in fp64 to partial64 instead of partial
 template <class T>
 hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int64_t h_g, int64_t ldh,
                           int64_t R, int64_t n_value, int N, int J, float* partial, double* pdb,
-                          int n_split, int64_t rows_per_split, int G, hipStream_t st);
+                          int n_split, int64_t rows_per_split, int G, hipStream_t st, int pm = PM_NATIVE,
+                          double* partial64 = nullptr);
 
 // whether launch_gemm_nt runs this shape on the persistent resident-weight
 // kernel, which alone fuses the output layer and the first layer (16-bit

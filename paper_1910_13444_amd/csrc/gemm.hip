@@ -95,10 +95,10 @@ __device__ __forceinline__ void lds_sync() {
 // Jet carries through tanh of one (point, column); index k runs over the
 // streams: value, d/dx_1..d/dx_ND1, d^2/dx_1^2..d^2/dx_ND2^2.
 // Forward: pre-activations in, activations out.
-template <int ND1, int ND2>
+template <int ND1, int ND2, bool X64 = false>
 __device__ __forceinline__ void jet_fwd(float* v) {
   float tt, s;
-  tanh_ts(v[0], tt, s);
+  tanh_pair<X64>(v[0], tt, s);
   const float sp = -2.0f * tt * s;
 #pragma unroll
   for (int i = 0; i < ND2; ++i) v[1 + ND1 + i] = s * v[1 + ND1 + i] + sp * v[1 + i] * v[1 + i];
@@ -109,10 +109,10 @@ __device__ __forceinline__ void jet_fwd(float* v) {
 
 // Reverse: activation cotangents in, pre-activation cotangents out, given the
 // saved pre-activations ap.
-template <int ND1, int ND2>
+template <int ND1, int ND2, bool X64 = false>
 __device__ __forceinline__ void jet_bwd(float* g, const float* ap) {
   float tt, s;
-  tanh_ts(ap[0], tt, s);
+  tanh_pair<X64>(ap[0], tt, s);
   const float sp = -2.0f * tt * s;
   const float spp = 2.0f * s * (3.0f * tt * tt - 1.0f);
   float ga = s * g[0];
@@ -145,8 +145,12 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 // into an NS-deep LDS ring (global_load_lds_dwordx4, no register staging),
 // issued NS - 1 stages ahead of the multiply, so that the load latency is
 // covered by several stages of matrix-core work.
+// PM (fp32 storage only): products from bf16 pieces of the fp32 operands
+// (ProdMode); PM_SPLIT3 folds the accumulators into fp64 after every stage.
+// p.kx > 0 (two-term weights): operand X is kx wide and is read twice, the
+// weight rows are 2 kx wide.
 template <class T, int ND1, int ND2, int WM, int WN, int MT, int NT, int EPI, int OCC, bool DB = (OCC >= 2),
-          int NS = 0>
+          int NS = 0, int PM = PM_NATIVE>
 __global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OCC)))
 k_gemm_nt(const NtArgs<T> p) {
   constexpr int C = 1 + ND1 + ND2;
@@ -165,6 +169,9 @@ k_gemm_nt(const NtArgs<T> p) {
   constexpr int RING = (NS > 0 ? NS : 2) * STAGE;
   constexpr int LDSB = RING > OUTB ? RING : OUTB;
   static_assert(NS == 0 || (ES == 2 && NS >= 2 && ROWS % 16 == 0), "direct-to-LDS stages: 16-bit types");
+  static_assert(PM == PM_NATIVE || ES == 4, "split products: fp32 storage");
+  // fp32 mode (fp32 storage, products not split into bf16): tanh in fp64
+  constexpr bool X64 = ES == 4 && PM != PM_SPLIT2 && PM != PM_SPLIT3;
   typedef typename Elem<T>::frag frag;
   __shared__ __attribute__((aligned(16))) char lds[LDSB];
 
@@ -188,12 +195,13 @@ k_gemm_nt(const NtArgs<T> p) {
   // each thread moves PPT 16-byte pieces of every stage: operand row piece>>2,
   // 16-byte segment piece&3 of its 64-byte k-slice
   const char* src[PPT];
-  bool valid[PPT];
+  bool valid[PPT], isx[PPT];
 #pragma unroll
   for (int i = 0; i < (NS > 0 ? 0 : PPT); ++i) {
     const int piece = tid + i * NTH;
     const int row = piece >> 2, sg = piece & 3;
     valid[i] = false;
+    isx[i] = row < C * BM;
     src[i] = Xb;
     if (piece < PIECES) {
       if (row < C * BM) {
@@ -219,10 +227,16 @@ k_gemm_nt(const NtArgs<T> p) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[u][k][t][r] = 0.0f;
 
+  // stage kt of the weights is stage kxs(kt) of operand X (two-term weights
+  // read X twice)
+  const int nk = p.K / KS;
+  const int nkx = p.kx > 0 ? p.kx / KS : nk;
+  auto kxs = [&](int kt) { return kt >= nkx ? kt - nkx : kt; };
   auto gload = [&](uint4* buf, int kt) {
+    const int ktx = kxs(kt);
 #pragma unroll
     for (int i = 0; i < PPT; ++i)
-      buf[i] = valid[i] ? *(const uint4*)(src[i] + (int64_t)kt * 64) : make_uint4(0u, 0u, 0u, 0u);
+      buf[i] = valid[i] ? *(const uint4*)(src[i] + (int64_t)(isx[i] ? ktx : kt) * 64) : make_uint4(0u, 0u, 0u, 0u);
   };
   auto lstore = [&](const uint4* buf, int stage) {
     char* base = lds + stage * STAGE;
@@ -236,6 +250,7 @@ k_gemm_nt(const NtArgs<T> p) {
   // segments in fp32); every fragment row base is a multiple of 32, so the
   // segment swizzle of the lane's row is (lane >> 2) & 3
   const int gsw = (lane >> 2) & 3;
+  bool odd = false;   // PM_SPLIT3: operand X negated in this stage
   auto frag_at = [&](const char* base, int row, int c) {
     if constexpr (ES == 2) {
       const int seg = 2 * c + (lane >> 5);
@@ -250,6 +265,29 @@ k_gemm_nt(const NtArgs<T> p) {
   };
   auto compute = [&](int stage) {
     const char* base = lds + stage * STAGE;
+    if constexpr (PM != PM_NATIVE) {
+      // fp32 fragments (one chunk per stage), each cut into bf16 pieces once.
+      // PM_SPLIT3 negates operand X on every other stage (the fold subtracts
+      // those stages): the matrix core's sums carry a small bias of one sign
+      // whatever the sign of the result, which then cancels in the fp64 sum
+      // instead of adding up over the stages.
+      constexpr int NP = PM == PM_SPLIT3 ? 3 : 2;
+      bf16x8 bp[NT][NP];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) split_frag<NP>(frag_at(base, C * BM + 32 * (wn * NT + t) + (lane & 31), 0), bp[t]);
+#pragma unroll
+      for (int u = 0; u < MT; ++u)
+#pragma unroll
+        for (int k = 0; k < C; ++k) {
+          bf16x8 ap[NP];
+          f32x8 xf = frag_at(base, k * BM + 32 * (MT * wm + u) + (lane & 31), 0);
+          if (PM == PM_SPLIT3 && odd) xf = -xf;
+          split_frag<NP>(xf, ap);
+#pragma unroll
+          for (int t = 0; t < NT; ++t) mma_split<NP>(acc[u][k][t], bp[t], ap);
+        }
+      return;
+    }
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       frag bfr[NT];
@@ -265,8 +303,73 @@ k_gemm_nt(const NtArgs<T> p) {
         }
     }
   };
+  // PM_F64 (one fragment per wave and stream: 32 points x 32 columns, 2 x 2
+  // blocks of the 16 x 16 fp64 product, whose lane l holds rows
+  // (l >> 4) + 4 r and column l & 15 of a block)
+  static_assert(PM != PM_F64 || (MT == 1 && NT == 1 && C <= 2), "fp64 products: one fragment per wave");
+  f64x4 accd[PM == PM_F64 ? C : 1][2][2];
+  if constexpr (PM == PM_F64) {
+#pragma unroll
+    for (int k = 0; k < C; ++k)
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) accd[k][a][b] = f64x4{0.0, 0.0, 0.0, 0.0};
+  }
+  // fp32 element kx (0..15) of LDS stage row r
+  auto lds_f = [&](const char* base, int r, int kx) {
+    return (double)*(const float*)(base + lds_seg(r, kx >> 2) + (kx & 3) * 4);
+  };
+  auto compute64 = [&](int stage) {
+    const char* base = lds + stage * STAGE;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int kx = 4 * kk + (lane >> 4);
+      double wv[2];
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) wv[nb] = lds_f(base, C * BM + 32 * wn + 16 * nb + (lane & 15), kx);
+#pragma unroll
+      for (int k = 0; k < C; ++k)
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb) {
+          const double xv = lds_f(base, k * BM + 32 * wm + 16 * pb + (lane & 15), kx);
+#pragma unroll
+          for (int nb = 0; nb < 2; ++nb)
+            accd[k][nb][pb] = __builtin_amdgcn_mfma_f64_16x16x4f64(wv[nb], xv, accd[k][nb][pb], 0, 0, 0);
+        }
+    }
+  };
+  // PM_SPLIT3: the stage's fp32 sums are added into (odd stages: subtracted
+  // from) fp64 accumulators
+  constexpr int A64 = PM == PM_SPLIT3 ? 1 : 0;
+  double acc64[A64 ? MT : 1][A64 ? C : 1][A64 ? NT : 1][A64 ? 16 : 1];
+  if constexpr (A64) {
+#pragma unroll
+    for (int u = 0; u < MT; ++u)
+#pragma unroll
+      for (int k = 0; k < C; ++k)
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc64[u][k][t][r] = 0.0;
+  }
+  auto fold = [&]() {
+    if constexpr (A64) {
+#pragma unroll
+      for (int u = 0; u < MT; ++u)
+#pragma unroll
+        for (int k = 0; k < C; ++k)
+#pragma unroll
+          for (int t = 0; t < NT; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              acc64[u][k][t][r] += odd ? -(double)acc[u][k][t][r] : (double)acc[u][k][t][r];
+              acc[u][k][t][r] = 0.0f;
+            }
+      odd = !odd;
+    }
+  };
 
-  const int nk = p.K / KS;
   if constexpr (NS > 0) {
     // One DMA instruction of a wave fills 1 KB of LDS, lane l at byte 16 l:
     // 16 stage rows (row 16 g + l / 4, physical segment l % 4, holding the
@@ -282,6 +385,7 @@ k_gemm_nt(const NtArgs<T> p) {
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const char* dsrc[GPW];
     int dlds[GPW];
+    bool dx[GPW];
 #pragma unroll
     for (int i = 0; i < GPW; ++i) {
       int grp = wv + i * (NTH / 64);
@@ -289,6 +393,7 @@ k_gemm_nt(const NtArgs<T> p) {
       dlds[i] = grp * 1024;
       const int row = grp * 16 + (lane >> 2);
       const int ls = (lane & 3) ^ ((row >> 2) & 3);
+      dx[i] = grp * 16 < C * BM;   // a 16-row group is all X rows or all weight rows (C * BM % 16 == 0)
       if (row < C * BM) {
         const int k = row / BM, pp = row % BM;
         int64_t pt = m0 + pp;
@@ -301,9 +406,10 @@ k_gemm_nt(const NtArgs<T> p) {
       }
     }
     auto issue = [&](int kt, int stage) {
+      const int ktx = kxs(kt);
 #pragma unroll
       for (int i = 0; i < GPW; ++i)
-        __builtin_amdgcn_global_load_lds((const void*)(dsrc[i] + (int64_t)kt * 64),
+        __builtin_amdgcn_global_load_lds((const void*)(dsrc[i] + (int64_t)(dx[i] ? ktx : kt) * 64),
                                          (lds_ptr_t)(lds + stage * STAGE + dlds[i]), 16, 0, 0);
     };
 #pragma unroll
@@ -328,7 +434,8 @@ k_gemm_nt(const NtArgs<T> p) {
       // with stage kt - 1, whose buffer the next issue refills
       lds_sync();
       if (kt + NS - 1 < nk) issue(kt + NS - 1, st == 0 ? NS - 1 : st - 1);
-      compute(st);
+      if constexpr (PM == PM_F64) compute64(st); else compute(st);
+      fold();
       st = st + 1 == NS ? 0 : st + 1;
     }
     lds_sync();
@@ -345,13 +452,15 @@ k_gemm_nt(const NtArgs<T> p) {
     lds_sync();
     for (int kt = 0; kt < nk; kt += 2) {
       gload(b0, kt + 2 < nk ? kt + 2 : nk - 1);
-      compute(0);
+      if constexpr (PM == PM_F64) compute64(0); else compute(0);
+      fold();
       __builtin_amdgcn_sched_barrier(0);
       if (kt + 1 < nk) lstore(b1, 1);
       lds_sync();
       if (kt + 1 >= nk) break;
       gload(b1, kt + 3 < nk ? kt + 3 : nk - 1);
-      compute(1);
+      if constexpr (PM == PM_F64) compute64(1); else compute(1);
+      fold();
       __builtin_amdgcn_sched_barrier(0);
       if (kt + 2 < nk) lstore(b0, 0);
       lds_sync();
@@ -365,9 +474,42 @@ k_gemm_nt(const NtArgs<T> p) {
     lds_sync();
     for (int kt = 0; kt < nk; ++kt) {
       gload(b0, kt + 1 < nk ? kt + 1 : nk - 1);
-      compute(kt & 1);
+      if constexpr (PM == PM_F64) compute64(kt & 1); else compute(kt & 1);
+      fold();
       __builtin_amdgcn_sched_barrier(0);
       if (kt + 1 < nk) lstore(b0, (kt + 1) & 1);
+      lds_sync();
+    }
+  }
+  if constexpr (A64) {
+#pragma unroll
+    for (int u = 0; u < MT; ++u)
+#pragma unroll
+      for (int k = 0; k < C; ++k)
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[u][k][t][r] = (float)acc64[u][k][t][r];
+  }
+  if constexpr (PM == PM_F64) {
+    // each stream through LDS, [point][column] floats (pitch 65), into the
+    // lane layout of the fp32 fragments the epilogue reads
+    float* tl = (float*)lds;
+    lds_sync();
+#pragma unroll
+    for (int k = 0; k < C; ++k) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            tl[(32 * wm + 16 * pb + (lane & 15)) * 65 + 32 * wn + 16 * nb + (lane >> 4) + 4 * r] =
+                (float)accd[k][nb][pb][r];
+      lds_sync();
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        acc[0][k][0][r] = tl[(32 * wm + (lane & 31)) * 65 + 32 * wn + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)];
       lds_sync();
     }
   }
@@ -482,7 +624,7 @@ k_gemm_nt(const NtArgs<T> p) {
           float v[C];
 #pragma unroll
           for (int k = 0; k < C; ++k) v[k] = acc[u][k][t][r];
-          jet_fwd<ND1, ND2>(v);
+          jet_fwd<ND1, ND2, X64>(v);
 #pragma unroll
           for (int k = 0; k < C; ++k) acc[u][k][t][r] = v[k];
         }
@@ -527,7 +669,7 @@ k_gemm_nt(const NtArgs<T> p) {
             gv[k] = acc[u][k][t][r];
             av[k] = ap[k][e];
           }
-          jet_bwd<ND1, ND2>(gv, av);
+          jet_bwd<ND1, ND2, X64>(gv, av);
 #pragma unroll
           for (int k = 0; k < C; ++k) acc[u][k][t][r] = gv[k];
         }
@@ -954,11 +1096,15 @@ __device__ __forceinline__ int dw_col(int c) {
   return (c >> 5) * 2624 + (c & 31) * 80 + ((c & 16) ? 64 : 0);
 }
 
-template <class T, int WM, int WN, int NT, int OCC, int NB>
+// PM (fp32 storage): products from bf16 pieces (ProdMode); with PM_SPLIT3
+// the stage sums are folded into fp64 and the split partials are written in
+// fp64 to partial64 (partial is unused).
+template <class T, int WM, int WN, int NT, int OCC, int NB, int PM = PM_NATIVE>
 __global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OCC)))
 k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restrict__ H, int64_t h_g,
           int64_t ldh, int64_t R, int64_t n_value, int N, int J, float* __restrict__ partial,
-          double* __restrict__ pdb, int n_split, int64_t rows_per_split) {
+          double* __restrict__ pdb, int n_split, int64_t rows_per_split, double* __restrict__ partial64) {
+  static_assert(PM == PM_NATIVE || sizeof(T) == 4, "split products: fp32 storage");
   constexpr int BNn = 32 * NT * WM;
   constexpr int BJ = 32 * NT * WN;
   constexpr int NTH = 64 * WM * WN;
@@ -1009,7 +1155,26 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
     for (int b = 0; b < NT; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
+  constexpr int A64 = PM == PM_SPLIT3 ? 1 : 0;
+  double acc64[A64 ? NT : 1][A64 ? NT : 1][A64 ? 16 : 1];
+  if constexpr (A64) {
+#pragma unroll
+    for (int a = 0; a < NT; ++a)
+#pragma unroll
+      for (int b = 0; b < NT; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc64[a][b][r] = 0.0;
+  }
+  // PM_F64: a wave's 32 x 32 outputs as 2 x 2 blocks of the 16 x 16 fp64
+  // product (lane l: rows (l >> 4) + 4 r, column l & 15 of a block)
+  static_assert(PM != PM_F64 || NT == 1, "fp64 products: one fragment per wave");
+  f64x4 accd[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) accd[a][b] = f64x4{0.0, 0.0, 0.0, 0.0};
   double dbacc = 0.0;
+  bool odd = false;   // PM_SPLIT3: dA negated in this stage
 
   // piece q of an operand: row piece q % NRP, column group q / NRP
   auto gload = [&](uint4 (*buf)[RPP], int64_t k0) {
@@ -1060,8 +1225,25 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
   };
   auto compute = [&](int stage, int64_t k0) {
     const char* base = lds + stage * STAGE;
+    if constexpr (PM == PM_F64) {
+      // fp32 rows of each column line, four at a time through the fp64 product
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
+      for (int kk = 0; kk < 4; ++kk) {
+        const int ro = (4 * kk + (lane >> 4)) * 4;
+        double av[2], bv[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          av[h] = (double)*(const float*)(base + dw_col(32 * wm + 16 * h + (lane & 15)) + ro);
+          bv[h] = (double)*(const float*)(base + REGA + dw_col(32 * wn + 16 * h + (lane & 15)) + ro);
+        }
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+          for (int b = 0; b < 2; ++b) accd[a][b] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[a], bv[b], accd[a][b], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < (PM == PM_F64 ? 0 : NCH); ++c) {
       const int koff = c * 32 + (lane >> 5) * (8 * ES);
       frag af[NT], bf[NT];
 #pragma unroll
@@ -1069,17 +1251,45 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
         af[t] = *(const frag*)(base + dw_col(32 * (wm * NT + t) + (lane & 31)) + koff);
         bf[t] = *(const frag*)(base + REGA + dw_col(32 * (wn * NT + t) + (lane & 31)) + koff);
       }
+      if constexpr (PM != PM_NATIVE) {
+        // PM_SPLIT3 negates dA on every other stage and subtracts those
+        // stages in the fp64 fold (the matrix core's one-signed bias cancels)
+        constexpr int NP = PM == PM_SPLIT3 ? 3 : 2;
+        bf16x8 ap[NT][NP], bp[NT][NP];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          split_frag<NP>(PM == PM_SPLIT3 && odd ? -af[t] : af[t], ap[t]);
+          split_frag<NP>(bf[t], bp[t]);
+        }
+#pragma unroll
+        for (int a = 0; a < NT; ++a)
+#pragma unroll
+          for (int b = 0; b < NT; ++b) mma_split<NP>(acc[a][b], ap[a], bp[b]);
+      } else {
+#pragma unroll
+        for (int a = 0; a < NT; ++a)
+#pragma unroll
+          for (int b = 0; b < NT; ++b) Elem<T>::mma(acc[a][b], af[a], bf[b]);
+      }
+    }
+    if constexpr (PM == PM_SPLIT3) {
 #pragma unroll
       for (int a = 0; a < NT; ++a)
 #pragma unroll
-        for (int b = 0; b < NT; ++b) Elem<T>::mma(acc[a][b], af[a], bf[b]);
+        for (int b = 0; b < NT; ++b)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            acc64[a][b][r] += odd ? -(double)acc[a][b][r] : (double)acc[a][b][r];
+            acc[a][b][r] = 0.0f;
+          }
+      odd = !odd;
     }
     // bias cotangent: value rows of this slice, one column per thread
     // (the 64-byte column line is read as 16 independent words)
     if (pdb && tj == 0 && tid < BNn && k0 < rv) {
       const int nr = (int)((rv - k0) < SR ? (rv - k0) : SR);
       const uint32_t* colw = (const uint32_t*)(base + dw_col(tid));
-      float part_sum = 0.0f;
+      typename std::conditional<ES == 4, double, float>::type part_sum = 0;
 #pragma unroll
       for (int w = 0; w < 16; ++w) {
         const uint32_t v = colw[w];
@@ -1088,7 +1298,7 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
           const float hi = Elem<T>::to_f(__builtin_bit_cast(T, (uint16_t)(v >> 16)));
           part_sum += (2 * w < nr ? lo : 0.0f) + (2 * w + 1 < nr ? hi : 0.0f);
         } else {
-          part_sum += w < nr ? __uint_as_float(v) : 0.0f;
+          part_sum += w < nr ? (double)__uint_as_float(v) : 0.0;
         }
       }
       dbacc += (double)part_sum;
@@ -1137,9 +1347,22 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
   }
 
   const int hh = lane >> 5;
-  float* out = partial + ((int64_t)g * n_split + split) * (int64_t)N * J;
+  const int64_t obase = ((int64_t)g * n_split + split) * (int64_t)N * J;
+  if constexpr (PM == PM_F64) {
 #pragma unroll
-  for (int a = 0; a < NT; ++a) {
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int j = j0 + 32 * wn + 16 * b + (lane & 15);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int n = n0 + 32 * wm + 16 * a + (lane >> 4) + 4 * r;
+          if (n < N && j < J) partial64[obase + (int64_t)n * J + j] = accd[a][b][r];
+        }
+      }
+  }
+#pragma unroll
+  for (int a = 0; a < (PM == PM_F64 ? 0 : NT); ++a) {
 #pragma unroll
     for (int b = 0; b < NT; ++b) {
       const int j = j0 + 32 * (wn * NT + b) + (lane & 31);
@@ -1147,7 +1370,9 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int n = n0 + 32 * (wm * NT + a) + 8 * (r >> 2) + 4 * hh + (r & 3);
-        if (n < N) out[(int64_t)n * J + j] = acc[a][b][r];
+        if (n >= N) continue;
+        if constexpr (A64) partial64[obase + (int64_t)n * J + j] = acc64[a][b][r];
+        else partial[obase + (int64_t)n * J + j] = acc[a][b][r];
       }
     }
   }
@@ -1504,6 +1729,38 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   constexpr int NTM = C == 1 ? 4 : (C == 2 ? 2 : 1);
   const int64_t npts = a.seg.n_points;
   if (npts <= 0) return hipSuccess;
+  if ((a.pm != PM_NATIVE && sizeof(T) != 4) || (a.kx > 0 && (sizeof(T) != 2 || a.K != 2 * a.kx)))
+    return hipErrorInvalidValue;
+  if constexpr (sizeof(T) == 4) {
+    // split products (the critic and the generators' sensor rows): one or two
+    // streams; register-staged tiles
+    if (a.pm != PM_NATIVE) {
+      if (a.y || a.fp1) return hipErrorInvalidValue;
+      if constexpr (C <= 2) {
+        if (a.N <= 32 && a.pm != PM_F64) {
+          dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 31) / 32)), 1, G);
+          if (a.pm == PM_SPLIT2) k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, 2, true, 0, PM_SPLIT2><<<grid, 256, 0, st>>>(a);
+          else k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, 2, true, 0, PM_SPLIT3><<<grid, 256, 0, st>>>(a);
+        } else if (a.pm == PM_SPLIT2) {
+          // 64 points x 64 NTM columns, 2 x 2 waves
+          constexpr int BN = 64 * NTM;
+          dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + BN - 1) / BN)), 1, G);
+          k_gemm_nt<T, ND1, ND2, 2, 2, 1, NTM, EPI, 2, true, 0, PM_SPLIT2><<<grid, 256, 0, st>>>(a);
+        } else if (a.pm == PM_F64) {
+          // fp64 products: 64 x 64 tiles
+          dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + 63) / 64)), 1, G);
+          k_gemm_nt<T, ND1, ND2, 2, 2, 1, 1, EPI, 2, true, 0, PM_F64><<<grid, 256, 0, st>>>(a);
+        } else {
+          // fp64 stage sums: 64 x 64 tiles
+          dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + 63) / 64)), 1, G);
+          k_gemm_nt<T, ND1, ND2, 2, 2, 1, 1, EPI, 2, true, 0, PM_SPLIT3><<<grid, 256, 0, st>>>(a);
+        }
+        return hipGetLastError();
+      } else {
+        return hipErrorInvalidValue;
+      }
+    }
+  }
   if constexpr (sizeof(T) == 2 && C <= 5 && EPI != EPI_DF) {
     const bool skip = a.skip || a.skip_g || a.out_gh;
     if (nt_resident_ok((int)sizeof(T), C, a.K, a.N, npts, a.ldx, a.ldo) && !(skip && (a.fp1 || a.y))) {
@@ -1643,8 +1900,37 @@ void dw_split_plan(int64_t R, int N, int J, int elem_bytes, int G, int* n_split,
 template <class T>
 hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int64_t h_g, int64_t ldh,
                           int64_t R, int64_t n_value, int N, int J, float* partial, double* pdb,
-                          int n_split, int64_t rows_per_split, int G, hipStream_t st) {
+                          int n_split, int64_t rows_per_split, int G, hipStream_t st, int pm, double* partial64) {
   if (R <= 0) return hipSuccess;
+  if (pm != PM_NATIVE && sizeof(T) != 4) return hipErrorInvalidValue;
+  if ((pm == PM_SPLIT3 || pm == PM_F64) && !partial64) return hipErrorInvalidValue;
+  if constexpr (sizeof(T) == 4) {
+    if (pm == PM_F64) {
+      dim3 grid((unsigned)(((N + 63) / 64) * ((J + 63) / 64)) * n_split, 1, G);
+      k_gemm_dw<T, 2, 2, 1, 2, 2, PM_F64><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial,
+                                                              pdb, n_split, rows_per_split, partial64);
+      return hipGetLastError();
+    }
+    if (pm != PM_NATIVE) {
+#define PIGAN_DW_PM(WM_, WN_, NT_, NTH_, BT_)                                                                     \
+  do {                                                                                                           \
+    dim3 grid((unsigned)(((N + BT_ - 1) / BT_) * ((J + BT_ - 1) / BT_)) * n_split, 1, G);                         \
+    if (pm == PM_SPLIT2)                                                                                         \
+      k_gemm_dw<T, WM_, WN_, NT_, 2, 4, PM_SPLIT2><<<grid, NTH_, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, \
+                                                                       J, partial, pdb, n_split, rows_per_split,   \
+                                                                       partial64);                                 \
+    else                                                                                                         \
+      k_gemm_dw<T, WM_, WN_, NT_, 2, 2, PM_SPLIT3><<<grid, NTH_, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, \
+                                                                       J, partial, pdb, n_split, rows_per_split,   \
+                                                                       partial64);                                 \
+  } while (0)
+      if (N >= 128 && J >= 128) PIGAN_DW_PM(2, 2, 2, 256, 128);
+      else if (N >= 64 && J >= 64) PIGAN_DW_PM(2, 2, 1, 256, 64);
+      else PIGAN_DW_PM(1, 1, 1, 64, 32);
+#undef PIGAN_DW_PM
+      return hipGetLastError();
+    }
+  }
   if constexpr (sizeof(T) == 2) {
     // operand stages straight into an LDS ring; 64 x 64 columns per wave.
     // Block shapes per width are the fastest measured.
@@ -1677,15 +1963,15 @@ hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int
   if (N >= 128 && J >= 128) {
     dim3 grid((unsigned)(((N + 127) / 128) * ((J + 127) / 128)) * n_split, 1, G);
     k_gemm_dw<T, 2, 2, 2, 2, 4><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
-                                                    n_split, rows_per_split);
+                                                    n_split, rows_per_split, nullptr);
   } else if (N >= 64 && J >= 64) {
     dim3 grid((unsigned)(((N + 63) / 64) * ((J + 63) / 64)) * n_split, 1, G);
     k_gemm_dw<T, 2, 2, 1, 2, 4><<<grid, 256, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
-                                                 n_split, rows_per_split);
+                                                 n_split, rows_per_split, nullptr);
   } else {
     dim3 grid((unsigned)(((N + 31) / 32) * ((J + 31) / 32)) * n_split, 1, G);
     k_gemm_dw<T, 1, 1, 1, 2, 4><<<grid, 64, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J, partial, pdb,
-                                                n_split, rows_per_split);
+                                                n_split, rows_per_split, nullptr);
   }
   return hipGetLastError();
 }
@@ -1693,7 +1979,8 @@ hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int
 #define PIGAN_INST(T)                                                                                    \
   template hipError_t launch_gemm_nt<T>(int, int, int, const NtArgs<T>&, int, hipStream_t);              \
   template hipError_t launch_gemm_dw<T>(const T*, int64_t, int64_t, const T*, int64_t, int64_t, int64_t, \
-                                        int64_t, int, int, float*, double*, int, int64_t, int, hipStream_t);
+                                        int64_t, int, int, float*, double*, int, int64_t, int, hipStream_t, int, \
+                                        double*);
 PIGAN_INST(float)
 PIGAN_INST(bf16)
 PIGAN_INST(f16)

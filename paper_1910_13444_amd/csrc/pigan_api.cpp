@@ -168,28 +168,67 @@ static int64_t ob_ppb(int64_t n_points, int W) {
 }
 
 // ---------------------------------------------------------------------------
+// storage and product policy
+// ---------------------------------------------------------------------------
+// The collocation rows (value and derivative streams feeding the residual)
+// are stored in the step's type T.  The adversarial path -- the generators'
+// sensor rows, whose cotangents come from the critic, and the critic itself
+// -- is stored in fp32 and multiplied with split products (ProdMode): at the
+// initial weights a critic is far less sensitive to a uniform shift of a
+// sensor block than to the single sensors it sums over, so the generators'
+// gradients there are small differences of large per-row terms.  Rounding
+// every row on that path to a 16-bit format, or accumulating its long
+// contractions in fp32, moves them by several hundred rounding units.  In
+// fp32 mode those products run on the fp64 matrix core (fp32 operands are
+// exact in fp64, one rounding per result); in 16-bit modes two bf16 pieces
+// per operand suffice for their bar.
+template <class T> constexpr int adv_pm() { return sizeof(T) == 2 ? PM_SPLIT2 : PM_F64; }
+// split-K partials of these product modes are fp64
+static bool pm_wide(int pm) { return pm == PM_SPLIT3 || pm == PM_F64; }
+// 16-bit storage: the collocation forward products take two-term weights
+// [W_hi | W_lo], so the generated fields and their derivatives see the fp32
+// weights to about 16 significand bits (the residual at the initial weights is
+// a small difference of jet products and amplifies a one-term rounding).
+template <class T> constexpr bool two_term() { return sizeof(T) == 2; }
+
+static const char* pm_tag(int pm) {
+  return pm == PM_SPLIT2 ? "_x2" : (pm == PM_SPLIT3 ? "_x3" : (pm == PM_F64 ? "_f64" : ""));
+}
+
+// ---------------------------------------------------------------------------
 // training-step plan
 // ---------------------------------------------------------------------------
+// One network's buffers for a chunk of samples.  Sensor rows (value stream
+// only, fp32) and collocation stream rows (storage type T, stream k of point p
+// at row k * n_col + p) have separate activation buffers; the output jets and
+// their cotangents are fp32 vectors [sensor outputs | stream planes].
 struct NetBuf {
   MlpOff off;
   int nd1 = 0, nd2 = 0, n_s = 0;
   int64_t n_sen = 0, n_col = 0;
-  int64_t R = 0;     // planned rows per group (group stride of every activation buffer)
-  int64_t rows = 0;  // rows used by the current chunk (<= R)
-  std::vector<size_t> A, H;  // index 1..L
-  size_t dA[2] = {0, 0};
-  size_t jet = 0, gbar = 0, zp = 0, wc = 0, wcT = 0, fb = 0, ob = 0;
+  int64_t Rs = 0, Rc = 0;    // planned sensor rows / collocation stream rows per group
+  int64_t R = 0;             // jet rows per group (Rs + Rc)
+  int64_t rows = 0;          // jet rows used by the current chunk (<= R)
+  std::vector<size_t> As, Hs, Ac, Hc;   // index 1..L
+  size_t dAs[2] = {0, 0}, dAc[2] = {0, 0};
+  // wc: collocation forward weights (two-term rows in 16-bit storage), wcT
+  // their transposes (reverse pass); ws, wsT: fp32 copies and transposes for
+  // the sensor rows (aligned rows: a packed parameter vector is only 4-byte
+  // aligned per group)
+  size_t jet = 0, gbar = 0, zp = 0, wc = 0, wcT = 0, ws = 0, wsT = 0, fb = 0, ob = 0;
   int64_t ob_slots = 0;
   int64_t ppb_sen = 8, ppb_col = 8;
   int nrc = 1;       // row chunks per sample in the first-layer reverse pass
   // shared trunk: residual blocks, a second head (u) with its own jets and
-  // cotangents, the skip cotangent buffer, and the concatenated sensor
+  // cotangents, the skip cotangent buffers, and the concatenated sensor
   // locations [Y sensors ; u sensors]
   bool skip = false;
   int heads = 1;
-  size_t jet2 = 0, gbar2 = 0, gh = 0, xsc = 0;
+  size_t jet2 = 0, gbar2 = 0, ghs = 0, ghc = 0, xsc = 0;
+  int C() const { return 1 + nd1 + nd2; }
 };
 
+// the critic: fp32 storage throughout
 struct DiscBuf {
   MlpOff off;
   int Kp = 0;
@@ -226,27 +265,36 @@ static void plan_net(Carver& cv, NetBuf& nb, const pigan_mlp& m, int d, int nd2,
   nb.n_s = n_s;
   nb.n_sen = (int64_t)Sc * n_s;
   nb.n_col = (int64_t)Sc * P;
-  const int C = 1 + nb.nd1 + nb.nd2;
-  nb.R = nb.n_sen + C * nb.n_col;
+  nb.Rs = nb.n_sen;
+  nb.Rc = nb.C() * nb.n_col;
+  nb.R = nb.Rs + nb.Rc;
   nb.rows = nb.R;
   const int L = m.n_hidden, W = m.width;
-  const size_t act = (size_t)nb.R * W * es * G;
-  nb.A.assign(L + 1, 0);
-  nb.H.assign(L + 1, 0);
+  const size_t act_s = (size_t)nb.Rs * W * 4 * G, act_c = (size_t)nb.Rc * W * es * G;
+  nb.As.assign(L + 1, 0);
+  nb.Hs.assign(L + 1, 0);
+  nb.Ac.assign(L + 1, 0);
+  nb.Hc.assign(L + 1, 0);
   for (int l = 1; l <= L; ++l) {
-    nb.A[l] = cv.take(act);
-    nb.H[l] = cv.take(act);
+    nb.As[l] = cv.take(act_s);
+    nb.Hs[l] = cv.take(act_s);
+    nb.Ac[l] = cv.take(act_c);
+    nb.Hc[l] = cv.take(act_c);
   }
-  nb.dA[0] = cv.take(act);
-  nb.dA[1] = cv.take(act);
+  for (int i = 0; i < 2; ++i) {
+    nb.dAs[i] = cv.take(act_s);
+    nb.dAc[i] = cv.take(act_c);
+  }
   nb.jet = cv.take((size_t)nb.R * 4 * G);
   nb.gbar = cv.take((size_t)nb.R * 4 * G);
   nb.zp = cv.take((size_t)Sc * W * 4 * G);
-  const size_t wsz = (size_t)std::max(L - 1, 1) * W * W * es * G;
-  nb.wc = cv.take(wsz);
-  nb.wcT = cv.take(wsz);
+  const size_t nw = (size_t)std::max(L - 1, 1) * W * W * G;
+  nb.wc = cv.take(nw * es * (es == 2 ? 2 : 1));
+  nb.wcT = cv.take(nw * es);
+  nb.ws = cv.take(nw * 4);
+  nb.wsT = cv.take(nw * 4);
   nb.nrc = first_bwd_chunks(Sc);
-  nb.fb = cv.take((size_t)Sc * nb.nrc * 7 * W * 4 * G);
+  nb.fb = cv.take((size_t)Sc * nb.nrc * 7 * W * 8 * G);
   nb.ppb_sen = ob_ppb(nb.n_sen, W);
   nb.ppb_col = ob_ppb(nb.n_col, W);
   nb.ob_slots = out_bwd_blocks(nb.n_sen, (int)nb.ppb_sen) + out_bwd_blocks(nb.n_col, (int)nb.ppb_col);
@@ -254,9 +302,66 @@ static void plan_net(Carver& cv, NetBuf& nb, const pigan_mlp& m, int d, int nd2,
   if (trunk) {
     nb.jet2 = cv.take((size_t)nb.R * 4 * G);
     nb.gbar2 = cv.take((size_t)nb.R * 4 * G);
-    if (L >= 3) nb.gh = cv.take(act);
+    if (L >= 3) {
+      nb.ghs = cv.take(act_s);
+      nb.ghc = cv.take(act_c);
+    }
     nb.xsc = cv.take((size_t)n_s * d * 4 * G);
   }
+}
+
+static void plan_disc(Carver& cv, DiscBuf& D, const pigan_mlp& disc, int64_t Bmax, int GD) {
+  D.off.init(disc.in_dim, disc.n_hidden, disc.width);
+  const int WD = disc.width, LD = disc.n_hidden;
+  D.Kp = (int)round_up(disc.in_dim, 32);
+  D.Bmax = Bmax;
+  D.X0 = cv.take((size_t)D.Bmax * D.Kp * 4 * GD);
+  D.A.assign(LD + 1, 0);
+  D.H.assign(LD + 1, 0);
+  const size_t act = (size_t)D.Bmax * WD * 4 * GD;
+  for (int l = 1; l <= LD; ++l) {
+    D.A[l] = cv.take(act);
+    D.H[l] = cv.take(act);
+  }
+  D.dA[0] = cv.take(act);
+  D.dA[1] = cv.take(act);
+  D.score = cv.take((size_t)D.Bmax * 4 * GD);
+  D.seed = cv.take((size_t)D.Bmax * 4 * GD);
+  D.w1 = cv.take((size_t)WD * D.Kp * 4 * GD);
+  D.w1T = cv.take((size_t)WD * D.Kp * 4 * GD);
+  D.wc = cv.take((size_t)std::max(LD - 1, 1) * WD * WD * 4 * GD);
+  D.wcT = cv.take((size_t)std::max(LD - 1, 1) * WD * WD * 4 * GD);
+  D.ppb = ob_ppb(D.Bmax, WD);
+  D.ob_slots = out_bwd_blocks(D.Bmax, (int)D.ppb);
+  D.ob = cv.take((size_t)D.ob_slots * (WD + 1) * 8 * GD);
+}
+
+// split-K partials (8 bytes per entry: fp32, or fp64 for PM_SPLIT3): the
+// largest of all weight-gradient launches of a plan.  Gx groups per launch.
+static void plan_partials(Carver& cv, StepPlan& pl, const pigan_step_desc* s, bool trunk, int Gg, int GD) {
+  int64_t mx = 0, mxb = 0;
+  auto consider = [&](int64_t R, int N, int J, int eb, int Gx) {
+    int ns;
+    int64_t rps;
+    dw_split_plan(R, N, J, eb, Gx, &ns, &rps);
+    mx = std::max(mx, (int64_t)ns * N * J * Gx);
+    mxb = std::max(mxb, (int64_t)ns * N * Gx);
+  };
+  for (const NetBuf* nb : {&pl.Y, &pl.U}) {
+    if (nb == &pl.U && trunk) continue;
+    const int L = nb->off.L, W = nb->off.W;
+    if (L > 1) {
+      consider(nb->Rs, W, W, 4, Gg);
+      consider(nb->Rc, W, W, (int)pl.es, Gg);
+    }
+  }
+  const DiscBuf& D = pl.D;
+  consider(D.Bmax, s->disc.width, D.Kp, 4, GD);
+  if (s->disc.n_hidden > 1) consider(D.Bmax, s->disc.width, s->disc.width, 4, GD);
+  pl.dwp_floats = mx;
+  pl.dwdb_floats = mxb;
+  pl.dwp = cv.take((size_t)mx * 8);
+  pl.dwdb = cv.take((size_t)mxb * 8);
 }
 
 static void plan_step(const pigan_step_desc* s, int Sc, StepPlan& pl, bool trunk = false) {
@@ -272,48 +377,8 @@ static void plan_step(const pigan_step_desc* s, int Sc, StepPlan& pl, bool trunk
     plan_net(cv, pl.Y, s->genY, s->d, 0, s->n_sY, Sc, s->P, pl.es, G);
     plan_net(cv, pl.U, s->genU, s->d, s->d, s->n_sU, Sc, s->P, pl.es, G);
   }
-  DiscBuf& D = pl.D;
-  D.off.init(s->disc.in_dim, s->disc.n_hidden, s->disc.width);
-  const int WD = s->disc.width, LD = s->disc.n_hidden;
-  D.Kp = (int)round_up(s->disc.in_dim, 32);
-  D.Bmax = (int64_t)Sc + s->B_r;
-  D.X0 = cv.take((size_t)D.Bmax * D.Kp * pl.es * G);
-  D.A.assign(LD + 1, 0);
-  D.H.assign(LD + 1, 0);
-  const size_t act = (size_t)D.Bmax * WD * pl.es * G;
-  for (int l = 1; l <= LD; ++l) {
-    D.A[l] = cv.take(act);
-    D.H[l] = cv.take(act);
-  }
-  D.dA[0] = cv.take(act);
-  D.dA[1] = cv.take(act);
-  D.score = cv.take((size_t)D.Bmax * 4 * G);
-  D.seed = cv.take((size_t)D.Bmax * 4 * G);
-  D.w1 = cv.take((size_t)WD * D.Kp * pl.es * G);
-  D.w1T = cv.take((size_t)WD * D.Kp * pl.es * G);
-  const size_t wsz = (size_t)std::max(LD - 1, 1) * WD * WD * pl.es * G;
-  D.wc = cv.take(wsz);
-  D.wcT = cv.take(wsz);
-  D.ppb = ob_ppb(D.Bmax, WD);
-  D.ob_slots = out_bwd_blocks(D.Bmax, (int)D.ppb);
-  D.ob = cv.take((size_t)D.ob_slots * (WD + 1) * 8 * G);
-  // split-K partials: the largest of all weight-gradient launches
-  int64_t mx = 0, mxb = 0;
-  auto consider = [&](int64_t R, int N, int J) {
-    int ns;
-    int64_t rps;
-    dw_split_plan(R, N, J, (int)pl.es, G, &ns, &rps);
-    mx = std::max(mx, (int64_t)ns * N * J);
-    mxb = std::max(mxb, (int64_t)ns * N);
-  };
-  if (s->genY.n_hidden > 1) consider(pl.Y.R, s->genY.width, s->genY.width);
-  if (!trunk && s->genU.n_hidden > 1) consider(pl.U.R, s->genU.width, s->genU.width);
-  consider(D.Bmax, WD, D.Kp);
-  if (LD > 1) consider(D.Bmax, WD, WD);
-  pl.dwp_floats = mx;
-  pl.dwdb_floats = mxb;
-  pl.dwp = cv.take((size_t)mx * 4 * G);
-  pl.dwdb = cv.take((size_t)mxb * 8 * G);
+  plan_disc(cv, pl.D, s->disc, (int64_t)Sc + s->B_r, G);
+  plan_partials(cv, pl, s, trunk, G, G);
   pl.rblocks = residual_blocks((int64_t)Sc * s->P);
   pl.rpart = cv.take((size_t)pl.rblocks * 8 * G);
   pl.acc = cv.take((size_t)4 * 8 * G);
@@ -340,53 +405,14 @@ static void plan_hier(const pigan_step_desc* s, int Sc, StepPlan& pl, bool trunk
     plan_net(cv, pl.Y, s->genY, s->d, 0, s->n_sY, Sc, s->P, pl.es, 1);
     plan_net(cv, pl.U, s->genU, s->d, s->d, s->n_sU, Sc, s->P, pl.es, 1);
   }
-  DiscBuf& D = pl.D;
-  D.off.init(s->disc.in_dim, s->disc.n_hidden, s->disc.width);
-  const int WD = s->disc.width, LD = s->disc.n_hidden;
-  D.Kp = (int)round_up(s->disc.in_dim, 32);
-  D.Bmax = (int64_t)Sc + s->B_r;
-  D.X0 = cv.take((size_t)D.Bmax * D.Kp * pl.es * GD);
-  D.A.assign(LD + 1, 0);
-  D.H.assign(LD + 1, 0);
-  const size_t act = (size_t)D.Bmax * WD * pl.es * GD;
-  for (int l = 1; l <= LD; ++l) {
-    D.A[l] = cv.take(act);
-    D.H[l] = cv.take(act);
-  }
-  D.dA[0] = cv.take(act);
-  D.dA[1] = cv.take(act);
-  D.score = cv.take((size_t)D.Bmax * 4 * GD);
-  D.seed = cv.take((size_t)D.Bmax * 4 * GD);
-  D.w1 = cv.take((size_t)WD * D.Kp * pl.es * GD);
-  D.w1T = cv.take((size_t)WD * D.Kp * pl.es * GD);
-  const size_t wsz = (size_t)std::max(LD - 1, 1) * WD * WD * pl.es * GD;
-  D.wc = cv.take(wsz);
-  D.wcT = cv.take(wsz);
-  D.ppb = ob_ppb(D.Bmax, WD);
-  D.ob_slots = out_bwd_blocks(D.Bmax, (int)D.ppb);
-  D.ob = cv.take((size_t)D.ob_slots * (WD + 1) * 8 * GD);
-  int64_t mx = 0, mxb = 0;
-  auto consider = [&](int64_t R, int N, int J, int Gx) {
-    int ns;
-    int64_t rps;
-    dw_split_plan(R, N, J, (int)pl.es, Gx, &ns, &rps);
-    mx = std::max(mx, (int64_t)ns * N * J * Gx);
-    mxb = std::max(mxb, (int64_t)ns * N * Gx);
-  };
-  if (s->genY.n_hidden > 1) consider(pl.Y.R, s->genY.width, s->genY.width, 1);
-  if (!trunk && s->genU.n_hidden > 1) consider(pl.U.R, s->genU.width, s->genU.width, 1);
-  consider(D.Bmax, WD, D.Kp, GD);
-  if (LD > 1) consider(D.Bmax, WD, WD, GD);
-  pl.dwp_floats = mx;
-  pl.dwdb_floats = mxb;
-  pl.dwp = cv.take((size_t)mx * 4);
-  pl.dwdb = cv.take((size_t)mxb * 8);
+  plan_disc(cv, pl.D, s->disc, (int64_t)Sc + s->B_r, GD);
+  plan_partials(cv, pl, s, trunk, 1, GD);
   pl.rblocks = residual_blocks((int64_t)Sc * s->P);
   pl.rpart = cv.take((size_t)pl.rblocks * 8);
   pl.acc = cv.take((size_t)4 * 8 * GD);
   pl.hr = cv.take((size_t)Sc * s->P * 4);
   pl.hgn = cv.take((size_t)Sc * s->P * 4);
-  pl.hdx = cv.take((size_t)Sc * D.Kp * 4 * GD);
+  pl.hdx = cv.take((size_t)Sc * pl.D.Kp * 4 * GD);
   if (s->lambda_gp > 0.0f) {
     pl.gpg = cv.take((size_t)Sc * s->disc.in_dim * 4 * GD);
     pl.gpp = cv.take((size_t)Sc * 8 * GD);
@@ -452,55 +478,63 @@ template <class T>
 static pigan_status gemm_nt(int epi, int nd1, int nd2, const NtArgs<T>& a, int G, hipStream_t st, const char* name) {
   const int C = 1 + nd1 + nd2;
   const double M = (double)C * a.seg.n_points;
-  const double flops = 2.0 * M * a.N * a.K * G + (a.y ? 2.0 * M * a.N * G : 0.0);
+  const int Ka = a.kx > 0 ? a.kx : a.K;   // the contraction the method defines (two-term weights: one term)
+  const double flops = 2.0 * M * a.N * Ka * G + (a.y ? 2.0 * M * a.N * G : 0.0);
   const double es = sizeof(T);
   // operand X is read unless the first layer is formed in the kernel (then
   // its activations may be stored instead)
-  double bytes = ((a.fp1 ? (a.f_out_h ? M * a.K : 0.0) : M * a.K) + (double)a.N * a.K) * es * G;
+  double bytes = ((a.fp1 ? (a.f_out_h ? M * Ka : 0.0) : M * Ka) + (double)a.N * a.K) * es * G;
   if (epi == EPI_FWD) bytes += M * a.N * es * G * ((a.out_a ? 1 : 0) + (a.out_h ? 1 : 0)) + (a.y ? M * 4.0 * G : 0.0);
   else if (epi == EPI_BWD) bytes += (a.fp1 ? 1.0 : 2.0) * M * a.N * es * G;
   else bytes += M * a.N * 4.0 * G;
   // timing records are keyed by launch shape: one name = one kernel instantiation and size
   char key[64];
-  snprintf(key, sizeof key, "%s_c%d_k%d_n%d", name, C, a.K, a.N);
+  snprintf(key, sizeof key, "%s_c%d_k%d_n%d%s%s", name, C, Ka, a.N, pm_tag(a.pm), a.kx > 0 ? "_w2" : "");
   ProfScope ps(st, key, flops, bytes);
   HIP_TRY(launch_gemm_nt<T>(epi, nd1, nd2, a, G, st));
   return PIGAN_OK;
 }
 
+// part: the plan's split-K partial buffer (fp32 entries, or fp64 for PM_SPLIT3)
 template <class T>
 static pigan_status weight_grad(const T* dA, int64_t a_g, int64_t lda, const T* H, int64_t h_g, int64_t ldh,
                                 int64_t R, int64_t n_value, int N, int Jp, int J, float* gW, float* gb, int64_t g_g,
-                                int accumulate, float scale, int32_t* nonfinite, float* part, double* pdb, int G,
-                                hipStream_t st) {
+                                int accumulate, float scale, int32_t* nonfinite, void* part, double* pdb, int G,
+                                hipStream_t st, int pm = PM_NATIVE) {
   int ns;
   int64_t rps;
   dw_split_plan(R, N, Jp, (int)sizeof(T), G, &ns, &rps);
   {
     char key[64];
-    snprintf(key, sizeof key, "gemm_dw_n%d_j%d", N, Jp);
-    ProfScope ps(st, key, 2.0 * R * N * Jp * G, ((double)R * (N + Jp) * sizeof(T) + 4.0 * ns * N * Jp) * G);
-    HIP_TRY(launch_gemm_dw<T>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, Jp, part, pdb, ns, rps, G, st));
+    snprintf(key, sizeof key, "gemm_dw_n%d_j%d%s", N, Jp, pm_tag(pm));
+    ProfScope ps(st, key, 2.0 * R * N * Jp * G,
+                 ((double)R * (N + Jp) * sizeof(T) + (pm_wide(pm) ? 8.0 : 4.0) * ns * N * Jp) * G);
+    HIP_TRY(launch_gemm_dw<T>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, Jp, (float*)part, pdb, ns, rps, G, st, pm,
+                              (double*)part));
   }
   {
-    ProfScope ps(st, "reduce_dw", 0.0, 4.0 * ((double)ns + 1.0) * N * Jp * G);
+    ProfScope ps(st, "reduce_dw", 0.0, (pm_wide(pm) ? 8.0 : 4.0) * ((double)ns + 1.0) * N * Jp * G);
     const int64_t nw = (int64_t)N * Jp;
-    HIP_TRY(launch_colsum<float>(part, (int64_t)ns * nw, ns, nw, nw, Jp, J, gW, g_g, accumulate, scale, nonfinite, G,
-                                 st));
+    if (pm_wide(pm))
+      HIP_TRY(launch_colsum<double>((double*)part, (int64_t)ns * nw, ns, nw, nw, Jp, J, gW, g_g, accumulate, scale,
+                                    nonfinite, G, st));
+    else
+      HIP_TRY(launch_colsum<float>((float*)part, (int64_t)ns * nw, ns, nw, nw, Jp, J, gW, g_g, accumulate, scale,
+                                   nonfinite, G, st));
     HIP_TRY(launch_colsum<double>(pdb, (int64_t)ns * N, ns, N, N, 1, 1, gb, g_g, accumulate, scale, nonfinite, G,
                                   st));
   }
   return PIGAN_OK;
 }
 
-// Forward of one generator over a chunk: sensor rows then collocation rows.
-// whether both segments of a generator's chunk run on the resident kernel
-// (then the first and output layers are fused into the hidden GEMMs)
+// whether the collocation segment of a generator's chunk runs on the resident
+// kernel (then the first and output layers are fused into the hidden GEMMs):
+// one-term weights only
 template <class T>
-static bool resident_net(const NetBuf& nb) {
-  const int W = nb.off.W, C = 1 + nb.nd1 + nb.nd2;
-  return nt_resident_ok((int)sizeof(T), 1, W, W, nb.n_sen, W, W) &&
-         nt_resident_ok((int)sizeof(T), C, W, W, nb.n_col, W, W);
+static bool colloc_resident(const NetBuf& nb) {
+  const int W = nb.off.W;
+  return !two_term<T>() && nb.off.L >= 2 && !nb.skip && nb.heads == 1 &&
+         nt_resident_ok((int)sizeof(T), nb.C(), W, W, nb.n_col, W, W);
 }
 
 // first-layer source of a second-layer GEMM (coordinates are per segment)
@@ -511,76 +545,107 @@ static void first_src(NtArgs<T>& a, const float* params, int64_t pg, int in_dim,
   a.fzp = zp; a.fzp_g = zp_g;
 }
 
+// collocation forward weights of hidden layer l: two-term rows [W_hi | W_lo]
+// in 16-bit storage
+template <class T>
+static void colloc_weights(NtArgs<T>& a, void* ws, const NetBuf& nb, int l) {
+  const int W = nb.off.W, L = nb.off.L;
+  const int tw = two_term<T>() ? 2 : 1;
+  a.Wm = tp<T>(ws, nb.wc) + (size_t)(l - 2) * W * W * tw;
+  a.w_g = (int64_t)std::max(L - 1, 1) * W * W * tw;
+  a.ldw = (int64_t)W * tw;
+  a.K = W * tw;
+  a.kx = tw == 2 ? W : 0;
+}
+
+// Forward of one generator over a chunk: sensor rows, then collocation rows.
 template <class T>
 static pigan_status gen_chunk_fwd(void* ws, const NetBuf& nb, const float* params, const float* xs, int64_t xs_g,
                                   const float* xc, int64_t xc_g, const float* z, int64_t z_g, int d, int n_z, int Sc,
                                   int P, int G, hipStream_t st) {
   const int W = nb.off.W, L = nb.off.L;
   const int64_t pg = nb.off.n;
-  const int64_t actg = nb.R * W;  // per-group element stride of activations
+  const int64_t ags = nb.Rs * W, agc = nb.Rc * W;   // per-group element strides of the activations
   {
     ProfScope ps(st, "zproj", 2.0 * Sc * W * n_z * G, 0.0);
     HIP_TRY(launch_zproj(params, pg, nb.off.in_dim, d, W, z, z_g, n_z, Sc, tp<float>(ws, nb.zp), (int64_t)Sc * W, G,
                          st));
   }
-  // On the resident kernel the first layer is formed inside the second
-  // layer's GEMM (its pre-activations are never stored; its activations are,
-  // for the weight gradient), and the output layer rides on the last hidden
-  // layer's epilogue (the last activations are never stored).
-  const bool resident = L >= 2 && !nb.skip && nb.heads == 1 && resident_net<T>(nb);
+  // ---- sensor rows: fp32 storage, split products, value stream only
+  {
+    FirstArgs<float> fa{};
+    fa.p1 = params; fa.p_g = pg; fa.in_dim = nb.off.in_dim; fa.d = d; fa.W = W;
+    fa.zp = tp<float>(ws, nb.zp); fa.zp_g = (int64_t)Sc * W;
+    fa.out_a = tp<float>(ws, nb.As[1]); fa.out_h = tp<float>(ws, nb.Hs[1]); fa.o_g = ags; fa.ldo = W;
+    fa.x = xs; fa.x_g = xs_g; fa.x_shared = 1; fa.Pn = nb.n_s;
+    fa.seg = Seg{nb.n_sen, 0, 0};
+    fa.exact = adv_pm<T>() == PM_F64;
+    ProfScope ps(st, "first_fwd", 2.0 * nb.n_sen * W * d * G, (double)nb.n_sen * W * 2 * 4 * G);
+    HIP_TRY(launch_first_fwd<float>(0, 0, fa, G, st));
+  }
+  for (int l = 2; l <= L; ++l) {
+    NtArgs<float> a{};
+    a.X = tp<float>(ws, nb.Hs[l - 1]); a.x_g = ags; a.ldx = W;
+    a.Wm = tp<float>(ws, nb.ws) + (size_t)(l - 2) * W * W; a.w_g = (int64_t)std::max(L - 1, 1) * W * W; a.ldw = W;
+    a.bias = params + nb.off.b[l]; a.b_g = pg;
+    a.out_a = tp<float>(ws, nb.As[l]); a.out_h = tp<float>(ws, nb.Hs[l]); a.o_g = ags; a.ldo = W;
+    if (nb.skip && trunk_skip(l)) a.skip = tp<float>(ws, nb.Hs[l - 2]);   // residual block output
+    a.N = W; a.K = W; a.pm = adv_pm<T>();
+    a.seg = Seg{nb.n_sen, 0, 0};
+    pigan_status s1 = gemm_nt<float>(EPI_FWD, 0, 0, a, G, st, "gemm_fwd");
+    if (s1 != PIGAN_OK) return s1;
+  }
+  {
+    ProfScope ps(st, "out_fwd", 2.0 * nb.heads * nb.n_sen * W * G, (double)nb.heads * nb.n_sen * W * 4 * G);
+    HIP_TRY(launch_out_fwd<float>(tp<float>(ws, nb.Hs[L]), ags, W, nb.n_sen, nb.n_sen, W, params + nb.off.wout, pg,
+                                  tp<float>(ws, nb.jet), nb.R, G, st));
+    if (nb.heads == 2)   // second head (u): [w_u, b_u] follows [w_Y, b_Y]
+      HIP_TRY(launch_out_fwd<float>(tp<float>(ws, nb.Hs[L]), ags, W, nb.n_sen, nb.n_sen, W,
+                                    params + nb.off.wout + W + 1, pg, tp<float>(ws, nb.jet2), nb.R, G, st));
+  }
+  // ---- collocation rows: storage type T, every jet stream
+  const int C = nb.C();
+  const int64_t mc = C * nb.n_col;
+  const bool resident = colloc_resident<T>(nb);
   if (!resident) {
     FirstArgs<T> fa{};
     fa.p1 = params; fa.p_g = pg; fa.in_dim = nb.off.in_dim; fa.d = d; fa.W = W;
     fa.zp = tp<float>(ws, nb.zp); fa.zp_g = (int64_t)Sc * W;
-    fa.out_a = tp<T>(ws, nb.A[1]); fa.out_h = tp<T>(ws, nb.H[1]); fa.o_g = actg; fa.ldo = W;
-    // sensors: shared locations, value stream only
-    fa.x = xs; fa.x_g = xs_g; fa.x_shared = 1; fa.Pn = nb.n_s;
-    fa.seg = Seg{nb.n_sen, 0, 0};
-    {
-      ProfScope ps(st, "first_fwd", 2.0 * nb.n_sen * W * d * G, (double)nb.n_sen * W * 2 * sizeof(T) * G);
-      HIP_TRY(launch_first_fwd<T>(0, 0, fa, G, st));
-    }
+    fa.out_a = tp<T>(ws, nb.Ac[1]); fa.out_h = tp<T>(ws, nb.Hc[1]); fa.o_g = agc; fa.ldo = W;
     fa.x = xc; fa.x_g = xc_g; fa.x_shared = 0; fa.Pn = P;
-    fa.seg = Seg{nb.n_col, nb.n_sen, nb.n_col};
-    {
-      const int C = 1 + nb.nd1 + nb.nd2;
-      ProfScope ps(st, "first_fwd", 2.0 * nb.n_col * W * d * G, (double)nb.n_col * C * W * 2 * sizeof(T) * G);
-      HIP_TRY(launch_first_fwd<T>(nb.nd1, nb.nd2, fa, G, st));
-    }
+    fa.seg = Seg{nb.n_col, 0, nb.n_col};
+    fa.exact = sizeof(T) == 4;
+    ProfScope ps(st, "first_fwd", 2.0 * nb.n_col * W * d * G, (double)mc * W * 2 * sizeof(T) * G);
+    HIP_TRY(launch_first_fwd<T>(nb.nd1, nb.nd2, fa, G, st));
   }
-  const bool fuse_out = resident;
   for (int l = 2; l <= L; ++l) {
     NtArgs<T> a{};
-    a.X = tp<T>(ws, nb.H[l - 1]); a.x_g = actg; a.ldx = W;
-    a.Wm = tp<T>(ws, nb.wc) + (size_t)(l - 2) * W * W; a.w_g = (int64_t)std::max(L - 1, 1) * W * W; a.ldw = W;
+    a.X = tp<T>(ws, nb.Hc[l - 1]); a.x_g = agc; a.ldx = W;
+    colloc_weights<T>(a, ws, nb, l);
     a.bias = params + nb.off.b[l]; a.b_g = pg;
-    a.out_a = tp<T>(ws, nb.A[l]); a.out_h = tp<T>(ws, nb.H[l]); a.o_g = actg; a.ldo = W;
-    if (l == L && fuse_out) {
+    a.out_a = tp<T>(ws, nb.Ac[l]); a.out_h = tp<T>(ws, nb.Hc[l]); a.o_g = agc; a.ldo = W;
+    if (l == L && resident) {
       a.out_h = nullptr;
-      a.y = tp<float>(ws, nb.jet); a.y_g = nb.R; a.wout = params + nb.off.wout; a.wo_g = pg;
+      a.y = tp<float>(ws, nb.jet) + nb.n_sen; a.y_g = nb.R; a.wout = params + nb.off.wout; a.wo_g = pg;
     }
     if (l == 2 && resident) {
       first_src(a, params, pg, nb.off.in_dim, d, tp<float>(ws, nb.zp), (int64_t)Sc * W);
-      a.f_out_h = tp<T>(ws, nb.H[1]);
+      a.f_out_h = tp<T>(ws, nb.Hc[1]);
     }
-    if (nb.skip && trunk_skip(l)) a.skip = tp<T>(ws, nb.H[l - 2]);   // residual block output
-    a.N = W; a.K = W;
-    a.seg = Seg{nb.n_sen, 0, 0};
-    a.fx = xs; a.fx_g = xs_g; a.fx_shared = 1; a.fPn = nb.n_s;
-    pigan_status s1 = gemm_nt<T>(EPI_FWD, 0, 0, a, G, st, "gemm_fwd");
-    if (s1 != PIGAN_OK) return s1;
-    a.seg = Seg{nb.n_col, nb.n_sen, nb.n_col};
+    if (nb.skip && trunk_skip(l)) a.skip = tp<T>(ws, nb.Hc[l - 2]);
+    a.N = W;
+    a.seg = Seg{nb.n_col, 0, nb.n_col};
     a.fx = xc; a.fx_g = xc_g; a.fx_shared = 0; a.fPn = P;
-    s1 = gemm_nt<T>(EPI_FWD, nb.nd1, nb.nd2, a, G, st, "gemm_fwd");
+    pigan_status s1 = gemm_nt<T>(EPI_FWD, nb.nd1, nb.nd2, a, G, st, "gemm_fwd");
     if (s1 != PIGAN_OK) return s1;
   }
-  if (!fuse_out) {
-    ProfScope ps(st, "out_fwd", 2.0 * nb.heads * nb.rows * W * G, (double)nb.heads * nb.rows * W * sizeof(T) * G);
-    HIP_TRY(launch_out_fwd<T>(tp<T>(ws, nb.H[L]), actg, W, nb.rows, nb.n_sen + nb.n_col, W, params + nb.off.wout, pg,
-                              tp<float>(ws, nb.jet), nb.R, G, st));
-    if (nb.heads == 2)   // second head (u): [w_u, b_u] follows [w_Y, b_Y]
-      HIP_TRY(launch_out_fwd<T>(tp<T>(ws, nb.H[L]), actg, W, nb.rows, nb.n_sen + nb.n_col, W,
-                                params + nb.off.wout + W + 1, pg, tp<float>(ws, nb.jet2), nb.R, G, st));
+  if (!resident) {
+    ProfScope ps(st, "out_fwd", 2.0 * nb.heads * mc * W * G, (double)nb.heads * mc * W * sizeof(T) * G);
+    HIP_TRY(launch_out_fwd<T>(tp<T>(ws, nb.Hc[L]), agc, W, mc, nb.n_col, W, params + nb.off.wout, pg,
+                              tp<float>(ws, nb.jet) + nb.n_sen, nb.R, G, st));
+    if (nb.heads == 2)
+      HIP_TRY(launch_out_fwd<T>(tp<T>(ws, nb.Hc[L]), agc, W, mc, nb.n_col, W, params + nb.off.wout + W + 1, pg,
+                                tp<float>(ws, nb.jet2) + nb.n_sen, nb.R, G, st));
   }
   return PIGAN_OK;
 }
@@ -594,83 +659,110 @@ static pigan_status gen_chunk_bwd(void* ws, const StepPlan& pl, const NetBuf& nb
                                   int32_t* nonfinite, int G, hipStream_t st) {
   const int W = nb.off.W, L = nb.off.L;
   const int64_t pg = nb.off.n;
-  const int64_t actg = nb.R * W;
+  const int64_t ags = nb.Rs * W, agc = nb.Rc * W;
+  const int C = nb.C();
+  const int64_t mc = C * nb.n_col;
+  const int pm = adv_pm<T>();
+  const bool resident = colloc_resident<T>(nb);
+  const int blk_sen = out_bwd_blocks(nb.n_sen, (int)nb.ppb_sen);
+  const int n_slots = blk_sen + out_bwd_blocks(nb.n_col, (int)nb.ppb_col);
+  // output layer of both segments: one slot range of w_out partials
   if (nb.heads == 2) {
     // two heads on the trunk's last activations; their cotangent is also the
     // skip cotangent of the top residual block's input
-    Out2BwdArgs<T> ob{};
-    ob.A = tp<T>(ws, nb.A[L]); ob.H = tp<T>(ws, nb.H[L]); ob.dA = tp<T>(ws, nb.dA[0]);
-    ob.gh = nb.skip && trunk_skip(L) ? tp<T>(ws, nb.gh) : nullptr;
-    ob.o_g = actg; ob.ldo = W;
-    ob.gbar0 = tp<float>(ws, nb.gbar); ob.gbar1 = tp<float>(ws, nb.gbar2); ob.gb_g = nb.R;
-    ob.wout = params + nb.off.wout; ob.w_g = pg;
-    const int blk_sen = out_bwd_blocks(nb.n_sen, (int)nb.ppb_sen);
-    const int n_slots = blk_sen + out_bwd_blocks(nb.n_col, (int)nb.ppb_col);
-    ob.W = W; ob.part = tp<double>(ws, nb.ob); ob.n_slots = n_slots;
-    ob.ppb = nb.ppb_sen; ob.slot0 = 0; ob.seg = Seg{nb.n_sen, 0, 0};
-    ProfScope ps(st, "out_bwd", 0.0, (double)nb.rows * W * (ob.gh ? 4 : 3) * sizeof(T) * G);
-    HIP_TRY(launch_out2_bwd<T>(0, 0, ob, G, st));
-    ob.ppb = nb.ppb_col; ob.slot0 = blk_sen; ob.seg = Seg{nb.n_col, nb.n_sen, nb.n_col};
-    HIP_TRY(launch_out2_bwd<T>(nb.nd1, nb.nd2, ob, G, st));
+    const bool topskip = nb.skip && trunk_skip(L);
+    Out2BwdArgs<float> os{};
+    os.A = tp<float>(ws, nb.As[L]); os.H = tp<float>(ws, nb.Hs[L]); os.dA = tp<float>(ws, nb.dAs[0]);
+    os.gh = topskip ? tp<float>(ws, nb.ghs) : nullptr;
+    os.o_g = ags; os.ldo = W;
+    os.gbar0 = tp<float>(ws, nb.gbar); os.gbar1 = tp<float>(ws, nb.gbar2); os.gb_g = nb.R;
+    os.wout = params + nb.off.wout; os.w_g = pg;
+    os.W = W; os.part = tp<double>(ws, nb.ob); os.n_slots = n_slots;
+    os.ppb = nb.ppb_sen; os.slot0 = 0; os.seg = Seg{nb.n_sen, 0, 0}; os.exact = pm == PM_F64;
+    Out2BwdArgs<T> oc{};
+    oc.A = tp<T>(ws, nb.Ac[L]); oc.H = tp<T>(ws, nb.Hc[L]); oc.dA = tp<T>(ws, nb.dAc[0]);
+    oc.gh = topskip ? tp<T>(ws, nb.ghc) : nullptr;
+    oc.o_g = agc; oc.ldo = W;
+    oc.gbar0 = tp<float>(ws, nb.gbar) + nb.n_sen; oc.gbar1 = tp<float>(ws, nb.gbar2) + nb.n_sen; oc.gb_g = nb.R;
+    oc.wout = params + nb.off.wout; oc.w_g = pg;
+    oc.W = W; oc.part = tp<double>(ws, nb.ob); oc.n_slots = n_slots;
+    oc.ppb = nb.ppb_col; oc.slot0 = blk_sen; oc.seg = Seg{nb.n_col, 0, nb.n_col}; oc.exact = sizeof(T) == 4;
+    ProfScope ps(st, "out_bwd", 0.0,
+                 ((double)nb.n_sen * 4 + (double)mc * sizeof(T)) * W * (topskip ? 4 : 3) * G);
+    HIP_TRY(launch_out2_bwd<float>(0, 0, os, G, st));
+    HIP_TRY(launch_out2_bwd<T>(nb.nd1, nb.nd2, oc, G, st));
     HIP_TRY(launch_colsum<double>(tp<double>(ws, nb.ob), (int64_t)n_slots * 2 * (W + 1), n_slots, 2 * (W + 1),
                                   2 * (W + 1), 1, 1, grad + nb.off.wout, pg, accumulate, scale, nonfinite, G, st));
   } else {
-  OutBwdArgs<T> ob{};
-  ob.A = tp<T>(ws, nb.A[L]); ob.dA = tp<T>(ws, nb.dA[0]); ob.o_g = actg; ob.ldo = W;
-  ob.gbar = tp<float>(ws, nb.gbar); ob.gb_g = nb.R;
-  ob.wout = params + nb.off.wout; ob.w_g = pg;
-  const int blk_sen = out_bwd_blocks(nb.n_sen, (int)nb.ppb_sen);
-  const int n_slots = blk_sen + out_bwd_blocks(nb.n_col, (int)nb.ppb_col);
-  ob.W = W; ob.part = tp<double>(ws, nb.ob); ob.n_slots = n_slots;
-  ob.ppb = nb.ppb_sen; ob.slot0 = 0; ob.seg = Seg{nb.n_sen, 0, 0};
-  {
-    ProfScope ps(st, "out_bwd", 0.0, (double)nb.rows * W * 2 * sizeof(T) * G);
-    HIP_TRY(launch_out_bwd<T>(0, 0, ob, G, st));
-    ob.ppb = nb.ppb_col; ob.slot0 = blk_sen; ob.seg = Seg{nb.n_col, nb.n_sen, nb.n_col};
-    HIP_TRY(launch_out_bwd<T>(nb.nd1, nb.nd2, ob, G, st));
+    OutBwdArgs<float> os{};
+    os.A = tp<float>(ws, nb.As[L]); os.dA = tp<float>(ws, nb.dAs[0]); os.o_g = ags; os.ldo = W;
+    os.gbar = tp<float>(ws, nb.gbar); os.gb_g = nb.R;
+    os.wout = params + nb.off.wout; os.w_g = pg;
+    os.W = W; os.part = tp<double>(ws, nb.ob); os.n_slots = n_slots;
+    os.ppb = nb.ppb_sen; os.slot0 = 0; os.seg = Seg{nb.n_sen, 0, 0}; os.exact = pm == PM_F64;
+    OutBwdArgs<T> oc{};
+    oc.A = tp<T>(ws, nb.Ac[L]); oc.dA = tp<T>(ws, nb.dAc[0]); oc.o_g = agc; oc.ldo = W;
+    oc.gbar = tp<float>(ws, nb.gbar) + nb.n_sen; oc.gb_g = nb.R;
+    oc.wout = params + nb.off.wout; oc.w_g = pg;
+    oc.W = W; oc.part = tp<double>(ws, nb.ob); oc.n_slots = n_slots;
+    oc.ppb = nb.ppb_col; oc.slot0 = blk_sen; oc.seg = Seg{nb.n_col, 0, nb.n_col}; oc.exact = sizeof(T) == 4;
+    ProfScope ps(st, "out_bwd", 0.0, ((double)nb.n_sen * 4 + (double)mc * sizeof(T)) * W * 2 * G);
+    HIP_TRY(launch_out_bwd<float>(0, 0, os, G, st));
+    HIP_TRY(launch_out_bwd<T>(nb.nd1, nb.nd2, oc, G, st));
     HIP_TRY(launch_colsum<double>(tp<double>(ws, nb.ob), (int64_t)n_slots * (W + 1), n_slots, W + 1, W + 1, 1, 1,
                                   grad + nb.off.wout, pg, accumulate, scale, nonfinite, G, st));
   }
-  }
+  void* part = tp<void>(ws, pl.dwp);
+  double* pdb = tp<double>(ws, pl.dwdb);
   int cur = 0;
   for (int l = L; l >= 2; --l) {
-    pigan_status s1 = weight_grad<T>(tp<T>(ws, nb.dA[cur]), actg, W, tp<T>(ws, nb.H[l - 1]), actg, W, nb.rows,
-                                     nb.n_sen + nb.n_col, W, W, W, grad + nb.off.w[l], grad + nb.off.b[l], pg,
-                                     accumulate, scale, nonfinite, tp<float>(ws, pl.dwp), tp<double>(ws, pl.dwdb), G, st);
+    // weight and bias gradients: sensor rows (split products), then the
+    // collocation rows added
+    pigan_status s1 = weight_grad<float>(tp<float>(ws, nb.dAs[cur]), ags, W, tp<float>(ws, nb.Hs[l - 1]), ags, W,
+                                         nb.n_sen, nb.n_sen, W, W, W, grad + nb.off.w[l], grad + nb.off.b[l], pg,
+                                         accumulate, scale, nonfinite, part, pdb, G, st, pm);
     if (s1 != PIGAN_OK) return s1;
-    NtArgs<T> a{};
-    a.X = tp<T>(ws, nb.dA[cur]); a.x_g = actg; a.ldx = W;
-    a.Wm = tp<T>(ws, nb.wcT) + (size_t)(l - 2) * W * W; a.w_g = (int64_t)std::max(L - 1, 1) * W * W; a.ldw = W;
-    a.aprev = tp<T>(ws, nb.A[l - 1]); a.out_da = tp<T>(ws, nb.dA[1 - cur]); a.o_g = actg; a.ldo = W;
-    if (l == 2 && !nb.skip && nb.heads == 1 && resident_net<T>(nb))   // the first layer's pre-activations were never stored
-      first_src(a, params, pg, nb.off.in_dim, d, tp<float>(ws, nb.zp), (int64_t)Sc * W);
-    if (nb.skip && (l - 1) % 2 == 1) {
-      // h_{l-1} is a residual block's input (when l + 1 <= L): add the total
-      // cotangent of that block's output; when h_{l-1} is itself a block's
-      // output (l - 1 >= 3), keep its total for the block below (in place)
-      if (l + 1 <= L) a.skip_g = tp<T>(ws, nb.gh);
-      if (l - 1 >= 3) a.out_gh = tp<T>(ws, nb.gh);
-    }
-    a.N = W; a.K = W;
-    a.seg = Seg{nb.n_sen, 0, 0};
-    a.fx = xs; a.fx_g = xs_g; a.fx_shared = 1; a.fPn = nb.n_s;
-    s1 = gemm_nt<T>(EPI_BWD, 0, 0, a, G, st, "gemm_bwd");
+    s1 = weight_grad<T>(tp<T>(ws, nb.dAc[cur]), agc, W, tp<T>(ws, nb.Hc[l - 1]), agc, W, mc, nb.n_col, W, W, W,
+                        grad + nb.off.w[l], grad + nb.off.b[l], pg, 1, scale, nonfinite, part, pdb, G, st);
     if (s1 != PIGAN_OK) return s1;
-    a.seg = Seg{nb.n_col, nb.n_sen, nb.n_col};
-    a.fx = xc; a.fx_g = xc_g; a.fx_shared = 0; a.fPn = P;
-    s1 = gemm_nt<T>(EPI_BWD, nb.nd1, nb.nd2, a, G, st, "gemm_bwd");
-    if (s1 != PIGAN_OK) return s1;
+    // h_{l-1} is a residual block's input (when l + 1 <= L): add the total
+    // cotangent of that block's output; when h_{l-1} is itself a block's
+    // output (l - 1 >= 3), keep its total for the block below (in place)
+    const bool skip_in = nb.skip && (l - 1) % 2 == 1 && l + 1 <= L;
+    const bool skip_out = nb.skip && (l - 1) % 2 == 1 && l - 1 >= 3;
+    NtArgs<float> as{};
+    as.X = tp<float>(ws, nb.dAs[cur]); as.x_g = ags; as.ldx = W;
+    as.Wm = tp<float>(ws, nb.wsT) + (size_t)(l - 2) * W * W; as.w_g = (int64_t)std::max(L - 1, 1) * W * W; as.ldw = W;
+    as.aprev = tp<float>(ws, nb.As[l - 1]); as.out_da = tp<float>(ws, nb.dAs[1 - cur]); as.o_g = ags; as.ldo = W;
+    if (skip_in) as.skip_g = tp<float>(ws, nb.ghs);
+    if (skip_out) as.out_gh = tp<float>(ws, nb.ghs);
+    as.N = W; as.K = W; as.pm = pm;
+    as.seg = Seg{nb.n_sen, 0, 0};
+    if ((s1 = gemm_nt<float>(EPI_BWD, 0, 0, as, G, st, "gemm_bwd")) != PIGAN_OK) return s1;
+    NtArgs<T> ac{};
+    ac.X = tp<T>(ws, nb.dAc[cur]); ac.x_g = agc; ac.ldx = W;
+    ac.Wm = tp<T>(ws, nb.wcT) + (size_t)(l - 2) * W * W; ac.w_g = (int64_t)std::max(L - 1, 1) * W * W; ac.ldw = W;
+    ac.aprev = tp<T>(ws, nb.Ac[l - 1]); ac.out_da = tp<T>(ws, nb.dAc[1 - cur]); ac.o_g = agc; ac.ldo = W;
+    if (l == 2 && resident)   // the first layer's pre-activations were never stored
+      first_src(ac, params, pg, nb.off.in_dim, d, tp<float>(ws, nb.zp), (int64_t)Sc * W);
+    if (skip_in) ac.skip_g = tp<T>(ws, nb.ghc);
+    if (skip_out) ac.out_gh = tp<T>(ws, nb.ghc);
+    ac.N = W; ac.K = W;
+    ac.seg = Seg{nb.n_col, 0, nb.n_col};
+    ac.fx = xc; ac.fx_g = xc_g; ac.fx_shared = 0; ac.fPn = P;
+    if ((s1 = gemm_nt<T>(EPI_BWD, nb.nd1, nb.nd2, ac, G, st, "gemm_bwd")) != PIGAN_OK) return s1;
     cur = 1 - cur;
   }
   FirstBwdArgs<T> fb{};
-  fb.dA = tp<T>(ws, nb.dA[cur]); fb.a_g = actg; fb.lda = W;
+  fb.dAs = tp<float>(ws, nb.dAs[cur]); fb.as_g = ags; fb.ldas = W;
+  fb.dA = tp<T>(ws, nb.dAc[cur]); fb.a_g = agc; fb.lda = W;
   fb.n_sen = nb.n_sen; fb.n_col = nb.n_col; fb.n_s = nb.n_s; fb.P = P; fb.S = Sc; fb.W = W; fb.d = d; fb.nd1 = nb.nd1;
-  fb.xs = xs; fb.xs_g = xs_g; fb.xc = xc; fb.xc_g = xc_g; fb.part = tp<float>(ws, nb.fb);
+  fb.xs = xs; fb.xs_g = xs_g; fb.xc = xc; fb.xc_g = xc_g; fb.part = tp<double>(ws, nb.fb);
   fb.nrc = nb.nrc;   // planned for the largest chunk: Sc * nrc never exceeds the partial buffer
   {
-    ProfScope ps(st, "first_bwd", 0.0, (double)(nb.n_sen + (1 + nb.nd1) * nb.n_col) * W * sizeof(T) * G);
+    ProfScope ps(st, "first_bwd", 0.0, ((double)nb.n_sen * 4 + (double)(1 + nb.nd1) * nb.n_col * sizeof(T)) * W * G);
     HIP_TRY(launch_first_bwd<T>(fb, G, st));
-    HIP_TRY(launch_first_wgrad(tp<float>(ws, nb.fb), Sc, fb.nrc, W, d, nb.nd1, nb.off.in_dim, z, z_g, n_z, grad, pg,
+    HIP_TRY(launch_first_wgrad(tp<double>(ws, nb.fb), Sc, fb.nrc, W, d, nb.nd1, nb.off.in_dim, z, z_g, n_z, grad, pg,
                                accumulate, scale, nonfinite, G, st));
   }
   return PIGAN_OK;
@@ -680,32 +772,53 @@ template <class T>
 static pigan_status cast_gen_weights(void* ws, const NetBuf& nb, const float* params, int G, hipStream_t st) {
   const int W = nb.off.W, L = nb.off.L;
   const int64_t dg = (int64_t)std::max(L - 1, 1) * W * W;
-  for (int l = 2; l <= L; ++l)
-    HIP_TRY(launch_cast<T>(params + nb.off.w[l], nb.off.n, W, W, W, tp<T>(ws, nb.wc) + (size_t)(l - 2) * W * W,
-                           tp<T>(ws, nb.wcT) + (size_t)(l - 2) * W * W, dg, G, st));
+  for (int l = 2; l <= L; ++l) {
+    const float* src = params + nb.off.w[l];
+    const size_t o = (size_t)(l - 2) * W * W;
+    if constexpr (two_term<T>()) {
+      HIP_TRY(launch_cast2<T>(src, nb.off.n, W, W, tp<T>(ws, nb.wc) + 2 * o, 2 * dg, G, st));
+      HIP_TRY(launch_cast<T>(src, nb.off.n, W, W, W, nullptr, tp<T>(ws, nb.wcT) + o, dg, G, st));
+    } else {
+      HIP_TRY(launch_cast<T>(src, nb.off.n, W, W, W, tp<T>(ws, nb.wc) + o, tp<T>(ws, nb.wcT) + o, dg, G, st));
+    }
+    HIP_TRY(launch_cast<float>(src, nb.off.n, W, W, W, tp<float>(ws, nb.ws) + o, tp<float>(ws, nb.wsT) + o, dg, G,
+                               st));
+  }
   return PIGAN_OK;
 }
 
-// discriminator forward over `seg` (nd1 = 1: value and one tangent stream)
-template <class T>
+// the critic's padded first-layer weights and their transpose, and the
+// hidden layers' weights and transposes (fp32 copies with aligned rows)
+static pigan_status cast_disc_weights(void* ws, const DiscBuf& D, const float* pD, int WD, int LD, int n_in, int G,
+                                      hipStream_t st) {
+  HIP_TRY(launch_cast<float>(pD + D.off.w[1], D.off.n, WD, n_in, D.Kp, tp<float>(ws, D.w1), tp<float>(ws, D.w1T),
+                             (int64_t)WD * D.Kp, G, st));
+  const int64_t dgl = (int64_t)std::max(LD - 1, 1) * WD * WD;
+  for (int l = 2; l <= LD; ++l)
+    HIP_TRY(launch_cast<float>(pD + D.off.w[l], D.off.n, WD, WD, WD, tp<float>(ws, D.wc) + (size_t)(l - 2) * WD * WD,
+                               tp<float>(ws, D.wcT) + (size_t)(l - 2) * WD * WD, dgl, G, st));
+  return PIGAN_OK;
+}
+
+// critic forward over `seg` (nd1 = 1: value and one tangent stream)
 static pigan_status disc_forward(void* ws, const DiscBuf& D, const float* pD, int WD, int LD, Seg seg, int nd1,
-                                 int G, hipStream_t st, const char* name) {
+                                 int G, hipStream_t st, const char* name, int pm) {
   const int64_t dact = D.Bmax * WD;
   for (int l = 1; l <= LD; ++l) {
-    NtArgs<T> a{};
+    NtArgs<float> a{};
     if (l == 1) {
-      a.X = tp<T>(ws, D.X0); a.x_g = D.Bmax * D.Kp; a.ldx = D.Kp;
-      a.Wm = tp<T>(ws, D.w1); a.w_g = (int64_t)WD * D.Kp; a.ldw = D.Kp; a.K = D.Kp;
+      a.X = tp<float>(ws, D.X0); a.x_g = D.Bmax * D.Kp; a.ldx = D.Kp;
+      a.Wm = tp<float>(ws, D.w1); a.w_g = (int64_t)WD * D.Kp; a.ldw = D.Kp; a.K = D.Kp;
     } else {
-      a.X = tp<T>(ws, D.H[l - 1]); a.x_g = dact; a.ldx = WD;
-      a.Wm = tp<T>(ws, D.wc) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD;
+      a.X = tp<float>(ws, D.H[l - 1]); a.x_g = dact; a.ldx = WD;
+      a.Wm = tp<float>(ws, D.wc) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD;
       a.ldw = WD; a.K = WD;
     }
     a.bias = pD + D.off.b[l]; a.b_g = D.off.n;
-    a.out_a = tp<T>(ws, D.A[l]); a.out_h = tp<T>(ws, D.H[l]); a.o_g = dact; a.ldo = WD;
-    a.N = WD;
+    a.out_a = tp<float>(ws, D.A[l]); a.out_h = tp<float>(ws, D.H[l]); a.o_g = dact; a.ldo = WD;
+    a.N = WD; a.pm = pm;
     a.seg = seg;
-    pigan_status r = gemm_nt<T>(EPI_FWD, nd1, 0, a, G, st, name);
+    pigan_status r = gemm_nt<float>(EPI_FWD, nd1, 0, a, G, st, name);
     if (r != PIGAN_OK) return r;
   }
   return PIGAN_OK;
@@ -719,158 +832,159 @@ static pigan_status disc_forward(void* ws, const DiscBuf& D, const float* pD, in
 // so the weight gradient is the reverse pass of a (value, tangent) jet of D
 // seeded with (x_b, c_b), with cotangent 1 on the tangent output.  Added to
 // gD; the row terms go to acc[g][3].  G critics, one per grid z.
-template <class T>
 static pigan_status critic_penalty(void* ws, const StepPlan& pl, const pigan_step_desc* s, const float* pD,
                                    const float* w_group, int n, float* gD, float inv, int32_t* nonfinite,
-                                   double* acc, int G, hipStream_t st) {
+                                   double* acc, int G, hipStream_t st, int pm) {
   const DiscBuf& D = pl.D;
   const int WD = s->disc.width, LD = s->disc.n_hidden, n_in = s->disc.in_dim;
   const int64_t dact = D.Bmax * WD, xg = D.Bmax * D.Kp;
   const int n_gp = std::min(s->S, s->B_r);
   const int64_t gg = (int64_t)pl.Sc * n_in;
+  void* part = tp<void>(ws, pl.dwp);
+  double* pdb = tp<double>(ws, pl.dwdb);
   pigan_status r;
   {
     ProfScope ps(st, "gp_misc", 0.0, 0.0);
     HIP_TRY(launch_fill2(tp<float>(ws, D.seed), D.Bmax, n, 1.0f, 0.0f, 0, G, st));
   }
   // 1. D on the interpolates, then its reverse pass to the input: g = dD/dv
-  if ((r = disc_forward<T>(ws, D, pD, WD, LD, Seg{n, 0, 0}, 0, G, st, "gp_fwd")) != PIGAN_OK) return r;
-  OutBwdArgs<T> ob{};
-  ob.A = tp<T>(ws, D.A[LD]); ob.dA = tp<T>(ws, D.dA[0]); ob.o_g = dact; ob.ldo = WD;
+  if ((r = disc_forward(ws, D, pD, WD, LD, Seg{n, 0, 0}, 0, G, st, "gp_fwd", pm)) != PIGAN_OK) return r;
+  OutBwdArgs<float> ob{};
+  ob.A = tp<float>(ws, D.A[LD]); ob.dA = tp<float>(ws, D.dA[0]); ob.o_g = dact; ob.ldo = WD;
   ob.gbar = tp<float>(ws, D.seed); ob.gb_g = D.Bmax;
   ob.wout = pD + D.off.wout; ob.w_g = D.off.n;
   ob.W = WD; ob.ppb = D.ppb; ob.part = tp<double>(ws, D.ob); ob.n_slots = out_bwd_blocks(n, (int)D.ppb);
-  ob.slot0 = 0; ob.seg = Seg{n, 0, 0};
+  ob.slot0 = 0; ob.seg = Seg{n, 0, 0}; ob.exact = pm == PM_F64;
   {
-    ProfScope ps(st, "gp_bwd", 0.0, (double)n * WD * 2 * sizeof(T) * G);
-    HIP_TRY(launch_out_bwd<T>(0, 0, ob, G, st));   // (its output-weight partials are not used)
+    ProfScope ps(st, "gp_bwd", 0.0, (double)n * WD * 2 * 4 * G);
+    HIP_TRY(launch_out_bwd<float>(0, 0, ob, G, st));   // (its output-weight partials are not used)
   }
   int cur = 0;
   for (int l = LD; l >= 2; --l) {
-    NtArgs<T> a{};
-    a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
-    a.Wm = tp<T>(ws, D.wcT) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD; a.ldw = WD;
-    a.aprev = tp<T>(ws, D.A[l - 1]); a.out_da = tp<T>(ws, D.dA[1 - cur]); a.o_g = dact; a.ldo = WD;
-    a.N = WD; a.K = WD; a.seg = Seg{n, 0, 0};
-    if ((r = gemm_nt<T>(EPI_BWD, 0, 0, a, G, st, "gp_bwd")) != PIGAN_OK) return r;
+    NtArgs<float> a{};
+    a.X = tp<float>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
+    a.Wm = tp<float>(ws, D.wcT) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD;
+    a.ldw = WD;
+    a.aprev = tp<float>(ws, D.A[l - 1]); a.out_da = tp<float>(ws, D.dA[1 - cur]); a.o_g = dact; a.ldo = WD;
+    a.N = WD; a.K = WD; a.pm = pm; a.seg = Seg{n, 0, 0};
+    if ((r = gemm_nt<float>(EPI_BWD, 0, 0, a, G, st, "gp_bwd")) != PIGAN_OK) return r;
     cur = 1 - cur;
   }
   {
-    NtArgs<T> a{};
-    a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
-    a.Wm = tp<T>(ws, D.w1T); a.w_g = (int64_t)WD * D.Kp; a.ldw = WD;
-    a.N = D.Kp; a.K = WD; a.seg = Seg{n, 0, 0};
+    NtArgs<float> a{};
+    a.X = tp<float>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
+    a.Wm = tp<float>(ws, D.w1T); a.w_g = (int64_t)WD * D.Kp; a.ldw = WD;
+    a.N = D.Kp; a.K = WD; a.pm = pm; a.seg = Seg{n, 0, 0};
     a.seedY = tp<float>(ws, pl.gpg); a.sY_g = gg; a.seedU = nullptr; a.sU_g = 0;
     a.nY = n_in; a.nU = 0; a.df_sign = 1.0f;
-    if ((r = gemm_nt<T>(EPI_DF, 0, 0, a, G, st, "gp_bwd")) != PIGAN_OK) return r;
+    if ((r = gemm_nt<float>(EPI_DF, 0, 0, a, G, st, "gp_bwd")) != PIGAN_OK) return r;
   }
   // 2. row terms (|g| - 1)^2 and tangent rows c = dP/dg (times the loss scale)
   {
     ProfScope ps(st, "gp_misc", 0.0, 0.0);
     const float scale = (float)(2.0 * s->lambda_gp * s->loss_scale / n_gp);
-    HIP_TRY(launch_gp_norm<T>(tp<float>(ws, pl.gpg), gg, n, n_in, w_group, scale, tp<double>(ws, pl.gpp), n,
-                              tp<T>(ws, D.X0), xg, D.Kp, G, st));
+    HIP_TRY(launch_gp_norm<float>(tp<float>(ws, pl.gpg), gg, n, n_in, w_group, scale, tp<double>(ws, pl.gpp), n,
+                                  tp<float>(ws, D.X0), xg, D.Kp, G, st));
     HIP_TRY(launch_sum_partials(tp<double>(ws, pl.gpp), n, acc, 4, 3, G, st));
     HIP_TRY(launch_fill2(tp<float>(ws, D.seed), D.Bmax, n, 0.0f, 1.0f, 1, G, st));
   }
   // 3. (value, tangent) jet of D and its reverse pass with cotangent 1 on the
   //    tangent output: the weight gradient of the penalty
-  if ((r = disc_forward<T>(ws, D, pD, WD, LD, Seg{n, 0, n}, 1, G, st, "gp_fwd")) != PIGAN_OK) return r;
-  ob.A = tp<T>(ws, D.A[LD]); ob.dA = tp<T>(ws, D.dA[0]);
+  if ((r = disc_forward(ws, D, pD, WD, LD, Seg{n, 0, n}, 1, G, st, "gp_fwd", pm)) != PIGAN_OK) return r;
+  ob.A = tp<float>(ws, D.A[LD]); ob.dA = tp<float>(ws, D.dA[0]);
   ob.n_slots = out_bwd_blocks(n, (int)D.ppb);     // blocks run over points, every stream of a point in one
   ob.seg = Seg{n, 0, n};
   {
-    ProfScope ps(st, "gp_bwd", 0.0, (double)2 * n * WD * 2 * sizeof(T) * G);
-    HIP_TRY(launch_out_bwd<T>(1, 0, ob, G, st));
+    ProfScope ps(st, "gp_bwd", 0.0, (double)2 * n * WD * 2 * 4 * G);
+    HIP_TRY(launch_out_bwd<float>(1, 0, ob, G, st));
     HIP_TRY(launch_colsum<double>(tp<double>(ws, D.ob), (int64_t)ob.n_slots * (WD + 1), ob.n_slots, WD + 1, WD + 1,
                                   1, 1, gD + D.off.wout, D.off.n, 1, inv, nonfinite, G, st));
   }
   cur = 0;
   for (int l = LD; l >= 2; --l) {
-    if ((r = weight_grad<T>(tp<T>(ws, D.dA[cur]), dact, WD, tp<T>(ws, D.H[l - 1]), dact, WD, 2 * (int64_t)n, n, WD,
-                            WD, WD, gD + D.off.w[l], gD + D.off.b[l], D.off.n, 1, inv, nonfinite,
-                            tp<float>(ws, pl.dwp), tp<double>(ws, pl.dwdb), G, st)) != PIGAN_OK)
+    if ((r = weight_grad<float>(tp<float>(ws, D.dA[cur]), dact, WD, tp<float>(ws, D.H[l - 1]), dact, WD,
+                                2 * (int64_t)n, n, WD, WD, WD, gD + D.off.w[l], gD + D.off.b[l], D.off.n, 1, inv,
+                                nonfinite, part, pdb, G, st, pm)) != PIGAN_OK)
       return r;
-    NtArgs<T> a{};
-    a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
-    a.Wm = tp<T>(ws, D.wcT) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD; a.ldw = WD;
-    a.aprev = tp<T>(ws, D.A[l - 1]); a.out_da = tp<T>(ws, D.dA[1 - cur]); a.o_g = dact; a.ldo = WD;
-    a.N = WD; a.K = WD; a.seg = Seg{n, 0, n};
-    if ((r = gemm_nt<T>(EPI_BWD, 1, 0, a, G, st, "gp_bwd")) != PIGAN_OK) return r;
+    NtArgs<float> a{};
+    a.X = tp<float>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
+    a.Wm = tp<float>(ws, D.wcT) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD;
+    a.ldw = WD;
+    a.aprev = tp<float>(ws, D.A[l - 1]); a.out_da = tp<float>(ws, D.dA[1 - cur]); a.o_g = dact; a.ldo = WD;
+    a.N = WD; a.K = WD; a.pm = pm; a.seg = Seg{n, 0, n};
+    if ((r = gemm_nt<float>(EPI_BWD, 1, 0, a, G, st, "gp_bwd")) != PIGAN_OK) return r;
     cur = 1 - cur;
   }
-  return weight_grad<T>(tp<T>(ws, D.dA[cur]), dact, WD, tp<T>(ws, D.X0), xg, D.Kp, 2 * (int64_t)n, n, WD, D.Kp,
-                        n_in, gD + D.off.w[1], gD + D.off.b[1], D.off.n, 1, inv, nonfinite, tp<float>(ws, pl.dwp),
-                        tp<double>(ws, pl.dwdb), G, st);
+  return weight_grad<float>(tp<float>(ws, D.dA[cur]), dact, WD, tp<float>(ws, D.X0), xg, D.Kp, 2 * (int64_t)n, n, WD,
+                            D.Kp, n_in, gD + D.off.w[1], gD + D.off.b[1], D.off.n, 1, inv, nonfinite, part, pdb, G,
+                            st, pm);
 }
 
-// Discriminator forward on the B rows of D.X0 (fake rows first, then n_real
-// real rows), its seeds (+w/S fake, -w/B_r real, times the loss scale) and the
+// Critic forward on the B rows of D.X0 (fake rows first, then n_real real
+// rows), its seeds (+w/S fake, -w/B_r real, times the loss scale) and the
 // reverse pass with every weight gradient (accumulated when accum != 0).  On
 // return D.dA[*cur] holds the first layer's pre-activation cotangents.
-template <class T>
 static pigan_status disc_pass(void* ws, const StepPlan& pl, const float* pD, int WD, int LD, int n_in, int B, int Sc,
                               int n_real, int S, int B_r, const float* w_group, float ls, float inv, int accum,
-                              float* gD, int32_t* nonfinite, double* acc, int G, hipStream_t st, int* cur_out) {
+                              float* gD, int32_t* nonfinite, double* acc, int G, hipStream_t st, int* cur_out,
+                              int pm) {
   const DiscBuf& D = pl.D;
   const int64_t dact = D.Bmax * WD;
+  void* part = tp<void>(ws, pl.dwp);
+  double* pdb = tp<double>(ws, pl.dwdb);
   pigan_status r;
-  for (int l = 1; l <= LD; ++l) {
-    NtArgs<T> a{};
-    if (l == 1) {
-      a.X = tp<T>(ws, D.X0); a.x_g = D.Bmax * D.Kp; a.ldx = D.Kp;
-      a.Wm = tp<T>(ws, D.w1); a.w_g = (int64_t)WD * D.Kp; a.ldw = D.Kp; a.K = D.Kp;
-    } else {
-      a.X = tp<T>(ws, D.H[l - 1]); a.x_g = dact; a.ldx = WD;
-      a.Wm = tp<T>(ws, D.wc) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD;
-      a.ldw = WD; a.K = WD;
-    }
-    a.bias = pD + D.off.b[l]; a.b_g = D.off.n;
-    a.out_a = tp<T>(ws, D.A[l]); a.out_h = tp<T>(ws, D.H[l]); a.o_g = dact; a.ldo = WD;
-    a.N = WD;
-    a.seg = Seg{B, 0, 0};
-    if ((r = gemm_nt<T>(EPI_FWD, 0, 0, a, G, st, "disc_fwd")) != PIGAN_OK) return r;
-  }
+  if ((r = disc_forward(ws, D, pD, WD, LD, Seg{B, 0, 0}, 0, G, st, "disc_fwd", pm)) != PIGAN_OK) return r;
   {
-    ProfScope ps(st, "out_fwd", 2.0 * B * WD * G, (double)B * WD * sizeof(T) * G);
-    HIP_TRY(launch_out_fwd<T>(tp<T>(ws, D.H[LD]), dact, WD, B, B, WD, pD + D.off.wout, D.off.n,
-                              tp<float>(ws, D.score), D.Bmax, G, st));
+    ProfScope ps(st, "out_fwd", 2.0 * B * WD * G, (double)B * WD * 4 * G);
+    HIP_TRY(launch_out_fwd<float>(tp<float>(ws, D.H[LD]), dact, WD, B, B, WD, pD + D.off.wout, D.off.n,
+                                  tp<float>(ws, D.score), D.Bmax, G, st));
     HIP_TRY(launch_disc_seed(tp<float>(ws, D.score), D.Bmax, Sc, n_real, S, B_r, w_group, ls,
                              tp<float>(ws, D.seed), acc, 4, G, st));
   }
-  // discriminator reverse pass
+  // critic reverse pass
   {
-    OutBwdArgs<T> ob{};
-    ob.A = tp<T>(ws, D.A[LD]); ob.dA = tp<T>(ws, D.dA[0]); ob.o_g = dact; ob.ldo = WD;
+    OutBwdArgs<float> ob{};
+    ob.A = tp<float>(ws, D.A[LD]); ob.dA = tp<float>(ws, D.dA[0]); ob.o_g = dact; ob.ldo = WD;
     ob.gbar = tp<float>(ws, D.seed); ob.gb_g = D.Bmax;
     ob.wout = pD + D.off.wout; ob.w_g = D.off.n;
     ob.W = WD; ob.ppb = D.ppb; ob.part = tp<double>(ws, D.ob); ob.n_slots = out_bwd_blocks(B, (int)D.ppb);
-    ob.slot0 = 0; ob.seg = Seg{B, 0, 0};
-    ProfScope ps(st, "out_bwd", 0.0, (double)B * WD * 2 * sizeof(T) * G);
-    HIP_TRY(launch_out_bwd<T>(0, 0, ob, G, st));
+    ob.slot0 = 0; ob.seg = Seg{B, 0, 0}; ob.exact = pm == PM_F64;
+    ProfScope ps(st, "out_bwd", 0.0, (double)B * WD * 2 * 4 * G);
+    HIP_TRY(launch_out_bwd<float>(0, 0, ob, G, st));
     HIP_TRY(launch_colsum<double>(tp<double>(ws, D.ob), (int64_t)ob.n_slots * (WD + 1), ob.n_slots, WD + 1, WD + 1,
                                   1, 1, gD + D.off.wout, D.off.n, accum, inv, nonfinite, G, st));
   }
   int cur = 0;
   for (int l = LD; l >= 2; --l) {
-    if ((r = weight_grad<T>(tp<T>(ws, D.dA[cur]), dact, WD, tp<T>(ws, D.H[l - 1]), dact, WD, B, B, WD, WD, WD,
-                            gD + D.off.w[l], gD + D.off.b[l], D.off.n, accum, inv, nonfinite, tp<float>(ws, pl.dwp),
-                            tp<double>(ws, pl.dwdb), G, st)) != PIGAN_OK)
+    if ((r = weight_grad<float>(tp<float>(ws, D.dA[cur]), dact, WD, tp<float>(ws, D.H[l - 1]), dact, WD, B, B, WD, WD,
+                                WD, gD + D.off.w[l], gD + D.off.b[l], D.off.n, accum, inv, nonfinite, part, pdb, G, st,
+                                pm)) != PIGAN_OK)
       return r;
-    NtArgs<T> a{};
-    a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
-    a.Wm = tp<T>(ws, D.wcT) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD; a.ldw = WD;
-    a.aprev = tp<T>(ws, D.A[l - 1]); a.out_da = tp<T>(ws, D.dA[1 - cur]); a.o_g = dact; a.ldo = WD;
-    a.N = WD; a.K = WD; a.seg = Seg{B, 0, 0};
-    if ((r = gemm_nt<T>(EPI_BWD, 0, 0, a, G, st, "disc_bwd")) != PIGAN_OK) return r;
+    NtArgs<float> a{};
+    a.X = tp<float>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
+    a.Wm = tp<float>(ws, D.wcT) + (size_t)(l - 2) * WD * WD; a.w_g = (int64_t)std::max(LD - 1, 1) * WD * WD;
+    a.ldw = WD;
+    a.aprev = tp<float>(ws, D.A[l - 1]); a.out_da = tp<float>(ws, D.dA[1 - cur]); a.o_g = dact; a.ldo = WD;
+    a.N = WD; a.K = WD; a.pm = pm; a.seg = Seg{B, 0, 0};
+    if ((r = gemm_nt<float>(EPI_BWD, 0, 0, a, G, st, "disc_bwd")) != PIGAN_OK) return r;
     cur = 1 - cur;
   }
-  if ((r = weight_grad<T>(tp<T>(ws, D.dA[cur]), dact, WD, tp<T>(ws, D.X0), D.Bmax * D.Kp, D.Kp, B, B, WD, D.Kp, n_in,
-                          gD + D.off.w[1], gD + D.off.b[1], D.off.n, accum, inv, nonfinite, tp<float>(ws, pl.dwp),
-                          tp<double>(ws, pl.dwdb), G, st)) != PIGAN_OK)
+  if ((r = weight_grad<float>(tp<float>(ws, D.dA[cur]), dact, WD, tp<float>(ws, D.X0), D.Bmax * D.Kp, D.Kp, B, B, WD,
+                              D.Kp, n_in, gD + D.off.w[1], gD + D.off.b[1], D.off.n, accum, inv, nonfinite, part, pdb,
+                              G, st, pm)) != PIGAN_OK)
     return r;
   *cur_out = cur;
   return PIGAN_OK;
+}
+
+// chunk-local view of a network's buffers: the plan is laid out for pl.Sc
+// samples; a shorter last chunk uses the same buffers with its own row counts
+static NetBuf chunk_view(const NetBuf& nb, int Sc, int P) {
+  NetBuf c = nb;
+  c.n_sen = (int64_t)Sc * c.n_s;
+  c.n_col = (int64_t)Sc * P;
+  c.rows = c.n_sen + c.C() * c.n_col;
+  return c;
 }
 
 template <class T>
@@ -884,6 +998,7 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
   const float inv = 1.0f / ls;
   const DiscBuf& D = pl.D;
   const int WD = s->disc.width, LD = s->disc.n_hidden, n_in = s->disc.in_dim;
+  const int pm = adv_pm<T>();
   double* acc = tp<double>(ws, pl.acc);
   pigan_status r;
 
@@ -895,12 +1010,7 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
     if (pl.trunk)   // the trunk sees both sensor sets: locations [Y sensors ; u sensors]
       HIP_TRY(launch_concat_rows(xsY, (int64_t)s->n_sY * d, s->n_sY, xsU, (int64_t)s->n_sU * d, s->n_sU, d,
                                  tp<float>(ws, pl.Y.xsc), (int64_t)(s->n_sY + s->n_sU) * d, G, st));
-    const int64_t dg1 = (int64_t)WD * D.Kp;
-    HIP_TRY(launch_cast<T>(pD + D.off.w[1], D.off.n, WD, n_in, D.Kp, tp<T>(ws, D.w1), tp<T>(ws, D.w1T), dg1, G, st));
-    const int64_t dgl = (int64_t)std::max(LD - 1, 1) * WD * WD;
-    for (int l = 2; l <= LD; ++l)
-      HIP_TRY(launch_cast<T>(pD + D.off.w[l], D.off.n, WD, WD, WD, tp<T>(ws, D.wc) + (size_t)(l - 2) * WD * WD,
-                             tp<T>(ws, D.wcT) + (size_t)(l - 2) * WD * WD, dgl, G, st));
+    if ((r = cast_disc_weights(ws, D, pD, WD, LD, n_in, G, st)) != PIGAN_OK) return r;
   }
 
   const int64_t xs_gU = (int64_t)s->n_sU * d;
@@ -914,14 +1024,7 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
     const int accum = ci > 0;
     const float* zc = z + (int64_t)s0 * n_z;
     const float* xcc = xc + (int64_t)s0 * P * d;
-    // chunk-local views: the plan is laid out for pl.Sc samples; a shorter
-    // last chunk uses the same buffers with its own row counts
-    NetBuf Yc = pl.Y, Uc = pl.U;
-    for (NetBuf* nb : {&Yc, &Uc}) {
-      nb->n_sen = (int64_t)Sc * nb->n_s;
-      nb->n_col = (int64_t)Sc * P;
-      nb->rows = nb->n_sen + (1 + nb->nd1 + nb->nd2) * nb->n_col;
-    }
+    const NetBuf Yc = chunk_view(pl.Y, Sc, P), Uc = chunk_view(pl.U, Sc, P);
     // generator forward passes
     if ((r = gen_chunk_fwd<T>(ws, Yc, pY, xsG, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, G, st)) != PIGAN_OK) return r;
     if (!pl.trunk &&
@@ -952,37 +1055,37 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
       HIP_TRY(launch_residual(ra, G, st));
       HIP_TRY(launch_sum_partials(tp<double>(ws, pl.rpart), residual_blocks(ra.M), acc, 4, 2, G, st));
     }
-    // discriminator forward on fake (and, in the first chunk, real) snapshots
+    // critic forward on fake (and, in the first chunk, real) snapshots
     const int n_real = ci == 0 ? s->B_r : 0;
     const int B = Sc + n_real;
     const int64_t dact = D.Bmax * WD;
     {
       ProfScope ps(st, "misc", 0.0, 0.0);
       if (pl.trunk)   // sample s's sensor rows: [Y sensors ; u sensors], Y head then u head values
-        HIP_TRY(launch_snap_fill_rows<T>(tp<float>(ws, Yc.jet), Yc.R, jetU, ju_g, s->n_sY, s->n_sU, n_s, s->n_sY,
-                                         Sc, real, (int64_t)s->B_r * n_in, n_real, n_in, tp<T>(ws, D.X0),
-                                         D.Bmax * D.Kp, D.Kp, G, st));
+        HIP_TRY(launch_snap_fill_rows<float>(tp<float>(ws, Yc.jet), Yc.R, jetU, ju_g, s->n_sY, s->n_sU, n_s, s->n_sY,
+                                             Sc, real, (int64_t)s->B_r * n_in, n_real, n_in, tp<float>(ws, D.X0),
+                                             D.Bmax * D.Kp, D.Kp, G, st));
       else
-        HIP_TRY(launch_snap_fill<T>(tp<float>(ws, Yc.jet), Yc.R, tp<float>(ws, Uc.jet), Uc.R, s->n_sY, s->n_sU, Sc,
-                                    real, (int64_t)s->B_r * n_in, n_real, n_in, tp<T>(ws, D.X0), D.Bmax * D.Kp, D.Kp,
-                                    G, st));
+        HIP_TRY(launch_snap_fill<float>(tp<float>(ws, Yc.jet), Yc.R, tp<float>(ws, Uc.jet), Uc.R, s->n_sY, s->n_sU,
+                                        Sc, real, (int64_t)s->B_r * n_in, n_real, n_in, tp<float>(ws, D.X0),
+                                        D.Bmax * D.Kp, D.Kp, G, st));
     }
     int cur = 0;
-    if ((r = disc_pass<T>(ws, pl, pD, WD, LD, n_in, B, Sc, n_real, S, s->B_r, w_group, ls, inv, accum, gD, nonfinite,
-                          acc, G, st, &cur)) != PIGAN_OK)
+    if ((r = disc_pass(ws, pl, pD, WD, LD, n_in, B, Sc, n_real, S, s->B_r, w_group, ls, inv, accum, gD, nonfinite,
+                       acc, G, st, &cur, pm)) != PIGAN_OK)
       return r;
     {
       // d(L_adv)/dF = -dL_D/dF for the fake rows -> generator sensor cotangents
-      NtArgs<T> a{};
-      a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
-      a.Wm = tp<T>(ws, D.w1T); a.w_g = (int64_t)WD * D.Kp; a.ldw = WD;
-      a.N = D.Kp; a.K = WD; a.seg = Seg{Sc, 0, 0};
+      NtArgs<float> a{};
+      a.X = tp<float>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
+      a.Wm = tp<float>(ws, D.w1T); a.w_g = (int64_t)WD * D.Kp; a.ldw = WD;
+      a.N = D.Kp; a.K = WD; a.pm = pm; a.seg = Seg{Sc, 0, 0};
       a.seedY = tp<float>(ws, Yc.gbar); a.sY_g = Yc.R; a.seedU = gbarU; a.sU_g = ju_g;
       a.nY = s->n_sY; a.nU = s->n_sU; a.df_sign = -1.0f;
       if (pl.trunk) {
         a.sY_ld = n_s; a.sU_ld = n_s; a.sU_off = s->n_sY;
       }
-      if ((r = gemm_nt<T>(EPI_DF, 0, 0, a, G, st, "disc_bwd")) != PIGAN_OK) return r;
+      if ((r = gemm_nt<float>(EPI_DF, 0, 0, a, G, st, "disc_bwd")) != PIGAN_OK) return r;
     }
     // critic gradient penalty on the pairs of this chunk's samples
     if (s->lambda_gp > 0.0f) {
@@ -991,11 +1094,11 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
       if (npair > 0) {
         {
           ProfScope ps(st, "gp_misc", 0.0, 0.0);
-          HIP_TRY(launch_gp_mix<T>(tp<float>(ws, Yc.jet), Yc.R, jetU, ju_g, s->n_sY, s->n_sU, ldY, ldU, offU, real,
-                                   (int64_t)s->B_r * n_in, gp_eps, n_gp, s0, npair, n_in, tp<T>(ws, D.X0),
-                                   D.Bmax * D.Kp, D.Kp, G, st));
+          HIP_TRY(launch_gp_mix<float>(tp<float>(ws, Yc.jet), Yc.R, jetU, ju_g, s->n_sY, s->n_sU, ldY, ldU, offU, real,
+                                       (int64_t)s->B_r * n_in, gp_eps, n_gp, s0, npair, n_in, tp<float>(ws, D.X0),
+                                       D.Bmax * D.Kp, D.Kp, G, st));
         }
-        if ((r = critic_penalty<T>(ws, pl, s, pD, w_group, npair, gD, inv, nonfinite, acc, G, st)) != PIGAN_OK)
+        if ((r = critic_penalty(ws, pl, s, pD, w_group, npair, gD, inv, nonfinite, acc, G, st, pm)) != PIGAN_OK)
           return r;
       }
     }
@@ -1032,6 +1135,7 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
   const float inv = 1.0f / ls;
   const DiscBuf& D = pl.D;
   const int WD = s->disc.width, LD = s->disc.n_hidden, n_in = s->disc.in_dim;
+  const int pm = adv_pm<T>();
   double* acc = tp<double>(ws, pl.acc);
   pigan_status r;
   {
@@ -1042,12 +1146,7 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
     if (pl.trunk)   // the trunk sees both sensor sets: locations [Y sensors ; u sensors]
       HIP_TRY(launch_concat_rows(xsY, (int64_t)s->n_sY * d, s->n_sY, xsU, (int64_t)s->n_sU * d, s->n_sU, d,
                                  tp<float>(ws, pl.Y.xsc), (int64_t)(s->n_sY + s->n_sU) * d, 1, st));
-    HIP_TRY(launch_cast<T>(pD + D.off.w[1], D.off.n, WD, n_in, D.Kp, tp<T>(ws, D.w1), tp<T>(ws, D.w1T),
-                           (int64_t)WD * D.Kp, GD, st));
-    const int64_t dgl = (int64_t)std::max(LD - 1, 1) * WD * WD;
-    for (int l = 2; l <= LD; ++l)
-      HIP_TRY(launch_cast<T>(pD + D.off.w[l], D.off.n, WD, WD, WD, tp<T>(ws, D.wc) + (size_t)(l - 2) * WD * WD,
-                             tp<T>(ws, D.wcT) + (size_t)(l - 2) * WD * WD, dgl, GD, st));
+    if ((r = cast_disc_weights(ws, D, pD, WD, LD, n_in, GD, st)) != PIGAN_OK) return r;
   }
   const int n_s = s->n_sY + s->n_sU;
   const float* xsG = pl.trunk ? tp<float>(ws, pl.Y.xsc) : xsY;
@@ -1062,12 +1161,7 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
     const int accum = ci > 0;
     const float* zc = z + (int64_t)s0 * n_z;
     const float* xcc = xc + (int64_t)s0 * P * d;
-    NetBuf Yc = pl.Y, Uc = pl.U;
-    for (NetBuf* nb : {&Yc, &Uc}) {
-      nb->n_sen = (int64_t)Sc * nb->n_s;
-      nb->n_col = (int64_t)Sc * P;
-      nb->rows = nb->n_sen + (1 + nb->nd1 + nb->nd2) * nb->n_col;
-    }
+    const NetBuf Yc = chunk_view(pl.Y, Sc, P), Uc = chunk_view(pl.U, Sc, P);
     if ((r = gen_chunk_fwd<T>(ws, Yc, pY, xsG, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, 1, st)) != PIGAN_OK) return r;
     if (!pl.trunk &&
         (r = gen_chunk_fwd<T>(ws, Uc, pU, xsU, xs_gU, xcc, xc_g, zc, z_g, d, n_z, Sc, P, 1, st)) != PIGAN_OK)
@@ -1103,23 +1197,23 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
       HIP_TRY(launch_fill_f32(tp<float>(ws, Yc.gbar), Yc.rows, Yc.R, 0.0f, 1, st));
       HIP_TRY(launch_fill_f32(gbarU, rowsU, ju_g, 0.0f, 1, st));
       HIP_TRY(launch_fill_f32(gN, M, M, 0.0f, 1, st));
-      HIP_TRY(launch_hier_snap<T>(h, Sc, real, (int64_t)s->B_r * n_in, n_real, tp<T>(ws, D.X0), D.Bmax * D.Kp,
-                                  D.Kp, GD, st));
+      HIP_TRY(launch_hier_snap<float>(h, Sc, real, (int64_t)s->B_r * n_in, n_real, tp<float>(ws, D.X0),
+                                      D.Bmax * D.Kp, D.Kp, GD, st));
     }
     int cur = 0;
-    if ((r = disc_pass<T>(ws, pl, pD, WD, LD, n_in, B, Sc, n_real, S, s->B_r, w_disc, ls, inv, accum, gD, nonfinite,
-                          acc, GD, st, &cur)) != PIGAN_OK)
+    if ((r = disc_pass(ws, pl, pD, WD, LD, n_in, B, Sc, n_real, S, s->B_r, w_disc, ls, inv, accum, gD, nonfinite,
+                       acc, GD, st, &cur, pm)) != PIGAN_OK)
       return r;
     {
       // -dL_D/dX of every critic's fake rows (all inputs), then added to the
       // generator outputs they were read from
       const int64_t dact = D.Bmax * WD;
-      NtArgs<T> a{};
-      a.X = tp<T>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
-      a.Wm = tp<T>(ws, D.w1T); a.w_g = (int64_t)WD * D.Kp; a.ldw = WD;
-      a.N = D.Kp; a.K = WD; a.seg = Seg{Sc, 0, 0};
+      NtArgs<float> a{};
+      a.X = tp<float>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
+      a.Wm = tp<float>(ws, D.w1T); a.w_g = (int64_t)WD * D.Kp; a.ldw = WD;
+      a.N = D.Kp; a.K = WD; a.pm = pm; a.seg = Seg{Sc, 0, 0};
       a.seedY = dX; a.sY_g = dx_g; a.sY_ld = D.Kp; a.nY = n_in; a.nU = 0; a.df_sign = -1.0f;
-      if ((r = gemm_nt<T>(EPI_DF, 0, 0, a, GD, st, "disc_bwd")) != PIGAN_OK) return r;
+      if ((r = gemm_nt<float>(EPI_DF, 0, 0, a, GD, st, "disc_bwd")) != PIGAN_OK) return r;
       ProfScope ps(st, "misc", 0.0, 0.0);
       HIP_TRY(launch_hier_scatter(h, dX, dx_g, D.Kp, Sc, GD, tp<float>(ws, Yc.gbar), gbarU, gN, st));
     }
@@ -1130,10 +1224,10 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
       if (npair > 0) {
         {
           ProfScope ps(st, "gp_misc", 0.0, 0.0);
-          HIP_TRY(launch_hier_snap<T>(h, npair, real, (int64_t)s->B_r * n_in, 0, tp<T>(ws, D.X0), D.Bmax * D.Kp,
-                                      D.Kp, GD, st, gp_eps, n_gp, s0));
+          HIP_TRY(launch_hier_snap<float>(h, npair, real, (int64_t)s->B_r * n_in, 0, tp<float>(ws, D.X0),
+                                          D.Bmax * D.Kp, D.Kp, GD, st, gp_eps, n_gp, s0));
         }
-        if ((r = critic_penalty<T>(ws, pl, s, pD, w_disc, npair, gD, inv, nonfinite, acc, GD, st)) != PIGAN_OK)
+        if ((r = critic_penalty(ws, pl, s, pD, w_disc, npair, gD, inv, nonfinite, acc, GD, st, pm)) != PIGAN_OK)
           return r;
       }
     }
@@ -1518,7 +1612,7 @@ static GenFwdPlan plan_gen_fwd(const pigan_mlp* net, int d, int S, int P, int or
   p.zp = cv.take((size_t)S * W * 4 * G);
   p.h[0] = cv.take((size_t)p.R * W * es * G);
   p.h[1] = cv.take((size_t)p.R * W * es * G);
-  p.wc = cv.take((size_t)std::max(L - 1, 1) * W * W * es * G);
+  p.wc = cv.take((size_t)std::max(L - 1, 1) * W * W * es * G * (es == 2 ? 2 : 1));   // two-term rows in 16-bit storage
   p.total = round_up((int64_t)cv.off, 256);
   return p;
 }
@@ -1554,18 +1648,22 @@ static pigan_status run_gen_fwd(const pigan_mlp* net, const float* params, int d
   const int nd1 = order >= 1 ? d : 0, nd2 = order >= 2 ? d : 0;
   const int64_t M = (int64_t)S * P;
   const int64_t actg = p.R * W;
+  constexpr int tw = two_term<T>() ? 2 : 1;
+  const int64_t dg = (int64_t)std::max(L - 1, 1) * W * W * tw;
   {
     ProfScope ps(st, "misc", 0.0, 0.0);
-    const int64_t dg = (int64_t)std::max(L - 1, 1) * W * W;
-    for (int l = 2; l <= L; ++l)
-      HIP_TRY(launch_cast<T>(params + off.w[l], off.n, W, W, W, tp<T>(ws, p.wc) + (size_t)(l - 2) * W * W, nullptr,
-                             dg, G, st));
+    for (int l = 2; l <= L; ++l) {
+      T* dst = tp<T>(ws, p.wc) + (size_t)(l - 2) * W * W * tw;
+      if constexpr (two_term<T>()) HIP_TRY(launch_cast2<T>(params + off.w[l], off.n, W, W, dst, dg, G, st));
+      else HIP_TRY(launch_cast<T>(params + off.w[l], off.n, W, W, W, dst, nullptr, dg, G, st));
+    }
     HIP_TRY(launch_zproj(params, off.n, in_dim, d, W, z, (int64_t)S * n_z, n_z, S, tp<float>(ws, p.zp),
                          (int64_t)S * W, G, st));
   }
-  // on the resident kernel the first layer is formed inside the second
-  // layer's GEMM and the output layer rides on the last one's epilogue
-  const bool fuse_out = L >= 2 && nt_resident_ok((int)sizeof(T), 1 + nd1 + nd2, W, W, M, W, W);
+  // on the resident kernel (one-term weights) the first layer is formed
+  // inside the second layer's GEMM and the output layer rides on the last
+  // one's epilogue
+  const bool fuse_out = !two_term<T>() && L >= 2 && nt_resident_ok((int)sizeof(T), 1 + nd1 + nd2, W, W, M, W, W);
   const int64_t x_g = x_shared ? (int64_t)P * d : M * d;
   if (!fuse_out) {
     FirstArgs<T> fa{};
@@ -1574,6 +1672,7 @@ static pigan_status run_gen_fwd(const pigan_mlp* net, const float* params, int d
     fa.x = x; fa.x_g = x_g; fa.x_shared = x_shared ? 1 : 0; fa.Pn = P;
     fa.out_a = nullptr; fa.out_h = tp<T>(ws, p.h[0]); fa.o_g = actg; fa.ldo = W;
     fa.seg = Seg{M, 0, M};
+    fa.exact = sizeof(T) == 4;
     ProfScope ps(st, "first_fwd", 2.0 * M * W * d * G, (double)M * (1 + nd1 + nd2) * W * sizeof(T) * G);
     HIP_TRY(launch_first_fwd<T>(nd1, nd2, fa, G, st));
   }
@@ -1581,7 +1680,8 @@ static pigan_status run_gen_fwd(const pigan_mlp* net, const float* params, int d
   for (int l = 2; l <= L; ++l) {
     NtArgs<T> a{};
     a.X = tp<T>(ws, p.h[cur]); a.x_g = actg; a.ldx = W;
-    a.Wm = tp<T>(ws, p.wc) + (size_t)(l - 2) * W * W; a.w_g = (int64_t)std::max(L - 1, 1) * W * W; a.ldw = W;
+    a.Wm = tp<T>(ws, p.wc) + (size_t)(l - 2) * W * W * tw; a.w_g = dg; a.ldw = (int64_t)W * tw;
+    a.K = W * tw; a.kx = tw == 2 ? W : 0;
     a.bias = params + off.b[l]; a.b_g = off.n;
     a.out_a = nullptr; a.out_h = tp<T>(ws, p.h[1 - cur]); a.o_g = actg; a.ldo = W;
     if (l == L && fuse_out) {
@@ -1592,7 +1692,7 @@ static pigan_status run_gen_fwd(const pigan_mlp* net, const float* params, int d
       first_src(a, params, off.n, in_dim, d, tp<float>(ws, p.zp), (int64_t)S * W);
       a.fx = x; a.fx_g = x_g; a.fx_shared = x_shared ? 1 : 0; a.fPn = P;
     }
-    a.N = W; a.K = W; a.seg = Seg{M, 0, M};
+    a.N = W; a.seg = Seg{M, 0, M};
     pigan_status s1 = gemm_nt<T>(EPI_FWD, nd1, nd2, a, G, st, "gemm_fwd");
     if (s1 != PIGAN_OK) return s1;
     cur = 1 - cur;
@@ -1658,11 +1758,13 @@ struct DiscFwdPlan {
   int Kp;
 };
 
+// the critic runs in fp32 storage in every mode (split products)
 static DiscFwdPlan plan_disc_fwd(const pigan_mlp* net, int B, pigan_dtype dt) {
   DiscFwdPlan p{};
   Carver cv;
   const int G = net->n_groups, W = net->width, L = net->n_hidden;
-  const size_t es = esize(dt);
+  const size_t es = 4;
+  (void)dt;
   p.Kp = (int)round_up(net->in_dim, 32);
   p.X0 = cv.take((size_t)B * p.Kp * es * G);
   p.h[0] = cv.take((size_t)B * W * es * G);
@@ -1691,36 +1793,37 @@ static pigan_status run_disc_fwd(const pigan_mlp* net, const float* params, cons
   const int64_t actg = (int64_t)B * W;
   {
     ProfScope ps(st, "misc", 0.0, 0.0);
-    HIP_TRY(launch_cast<T>(params + off.w[1], off.n, W, n_in, p.Kp, tp<T>(ws, p.w1), nullptr, (int64_t)W * p.Kp, G,
-                           st));
+    HIP_TRY(launch_cast<float>(params + off.w[1], off.n, W, n_in, p.Kp, tp<float>(ws, p.w1), nullptr,
+                               (int64_t)W * p.Kp, G, st));
     const int64_t dg = (int64_t)std::max(L - 1, 1) * W * W;
     for (int l = 2; l <= L; ++l)
-      HIP_TRY(launch_cast<T>(params + off.w[l], off.n, W, W, W, tp<T>(ws, p.wc) + (size_t)(l - 2) * W * W, nullptr,
-                             dg, G, st));
-    HIP_TRY(launch_snap_fill<T>(nullptr, 0, nullptr, 0, 0, 0, 0, snap, (int64_t)B * n_in, B, n_in, tp<T>(ws, p.X0),
-                                (int64_t)B * p.Kp, p.Kp, G, st));
+      HIP_TRY(launch_cast<float>(params + off.w[l], off.n, W, W, W, tp<float>(ws, p.wc) + (size_t)(l - 2) * W * W,
+                                 nullptr, dg, G, st));
+    HIP_TRY(launch_snap_fill<float>(nullptr, 0, nullptr, 0, 0, 0, 0, snap, (int64_t)B * n_in, B, n_in,
+                                    tp<float>(ws, p.X0), (int64_t)B * p.Kp, p.Kp, G, st));
   }
   // layer l writes h[(l - 1) % 2]
   for (int l = 1; l <= L; ++l) {
-    NtArgs<T> a{};
+    NtArgs<float> a{};
     if (l == 1) {
-      a.X = tp<T>(ws, p.X0); a.x_g = (int64_t)B * p.Kp; a.ldx = p.Kp;
-      a.Wm = tp<T>(ws, p.w1); a.w_g = (int64_t)W * p.Kp; a.ldw = p.Kp; a.K = p.Kp;
+      a.X = tp<float>(ws, p.X0); a.x_g = (int64_t)B * p.Kp; a.ldx = p.Kp;
+      a.Wm = tp<float>(ws, p.w1); a.w_g = (int64_t)W * p.Kp; a.ldw = p.Kp; a.K = p.Kp;
     } else {
-      a.X = tp<T>(ws, p.h[(l - 2) % 2]); a.x_g = actg; a.ldx = W;
-      a.Wm = tp<T>(ws, p.wc) + (size_t)(l - 2) * W * W; a.w_g = (int64_t)std::max(L - 1, 1) * W * W; a.ldw = W;
+      a.X = tp<float>(ws, p.h[(l - 2) % 2]); a.x_g = actg; a.ldx = W;
+      a.Wm = tp<float>(ws, p.wc) + (size_t)(l - 2) * W * W; a.w_g = (int64_t)std::max(L - 1, 1) * W * W; a.ldw = W;
       a.K = W;
     }
     a.bias = params + off.b[l]; a.b_g = off.n;
-    a.out_a = nullptr; a.out_h = tp<T>(ws, p.h[(l - 1) % 2]); a.o_g = actg; a.ldo = W;
-    a.N = W; a.seg = Seg{B, 0, 0};
-    pigan_status s1 = gemm_nt<T>(EPI_FWD, 0, 0, a, G, st, "disc_fwd");
+    a.out_a = nullptr; a.out_h = tp<float>(ws, p.h[(l - 1) % 2]); a.o_g = actg; a.ldo = W;
+    a.N = W; a.pm = adv_pm<T>(); a.seg = Seg{B, 0, 0};
+    pigan_status s1 = gemm_nt<float>(EPI_FWD, 0, 0, a, G, st, "disc_fwd");
     if (s1 != PIGAN_OK) return s1;
   }
   const int cur = (L - 1) % 2;
   {
-    ProfScope ps(st, "out_fwd", 2.0 * B * W * G, (double)B * W * sizeof(T) * G);
-    HIP_TRY(launch_out_fwd<T>(tp<T>(ws, p.h[cur]), actg, W, B, B, W, params + off.wout, off.n, score, B, G, st));
+    ProfScope ps(st, "out_fwd", 2.0 * B * W * G, (double)B * W * 4 * G);
+    HIP_TRY(launch_out_fwd<float>(tp<float>(ws, p.h[cur]), actg, W, B, B, W, params + off.wout, off.n, score, B, G,
+                                  st));
   }
   return PIGAN_OK;
 }

@@ -10,6 +10,7 @@ template <class T> struct FirstArgs {
   const float* x; int64_t x_g; int x_shared; int64_t Pn;   // locations; Pn points per sample
   T* out_a; T* out_h; int64_t o_g; int64_t ldo;
   Seg seg;
+  int exact;                                               // fp32 storage: tanh in fp64
 };
 
 struct ResidArgs {
@@ -31,6 +32,7 @@ template <class T> struct OutBwdArgs {
   int W; int64_t ppb;                            // points per block
   double* part; int n_slots; int slot0;          // [G][n_slots][W+1] fp64 partials
   Seg seg;
+  int exact;                                     // fp32 storage: tanh in fp64
 };
 
 // output layer of a shared trunk (two heads), reverse pass
@@ -41,16 +43,18 @@ template <class T> struct Out2BwdArgs {
   int W; int64_t ppb;                                          // points per block
   double* part; int n_slots; int slot0;                        // [G][n_slots][2 (W+1)] fp64 partials
   Seg seg;
+  int exact;                                                   // fp32 storage: tanh in fp64
 };
 
 template <class T> struct FirstBwdArgs {
-  const T* dA; int64_t a_g; int64_t lda;
+  const float* dAs; int64_t as_g; int64_t ldas;  // sensor rows (fp32) [n_sen][W]
+  const T* dA; int64_t a_g; int64_t lda;         // collocation stream rows: stream k at k * n_col
   int64_t n_sen; int64_t n_col;
   int n_s; int P; int S; int W; int d; int nd1;
   const float* xs; int64_t xs_g;                 // sensor locations [n_s][d]
   const float* xc; int64_t xc_g;                 // collocation points of the chunk [S][P][d]
   int nrc;                                       // row chunks per sample (blocks per sample)
-  float* part;                                   // [G][S][nrc][7][W]
+  double* part;                                  // [G][S][nrc][7][W]
 };
 
 hipError_t launch_zproj(const float* p1, int64_t p_g, int in_dim, int d, int W, const float* z, int64_t z_g,
@@ -118,7 +122,7 @@ hipError_t launch_colsum(const Tin* part, int64_t p_g, int n_slots, int64_t slot
                          float* dst, int64_t d_g, int accumulate, float scale, int32_t* nonfinite, int G,
                          hipStream_t st);
 template <class T> hipError_t launch_first_bwd(const FirstBwdArgs<T>& a, int G, hipStream_t st);
-hipError_t launch_first_wgrad(const float* part, int S, int nrc, int W, int d, int nd1, int in_dim, const float* z,
+hipError_t launch_first_wgrad(const double* part, int S, int nrc, int W, int d, int nd1, int in_dim, const float* z,
                               int64_t z_g, int n_z, float* grad, int64_t g_g, int accumulate, float scale,
                               int32_t* nonfinite, int G, hipStream_t st);
 hipError_t launch_losses(const double* acc, int acc_stride, const float* w_group, int S, int B, int64_t SP,
@@ -128,5 +132,8 @@ hipError_t launch_zero(double* acc, int n, int32_t* flag, hipStream_t st);
 template <class T>
 hipError_t launch_cast(const float* src, int64_t s_g, int N, int K, int Kp, T* dst, T* dstT, int64_t d_g, int G,
                        hipStream_t st);
+// two-term weights [hi | lo] per row (16-bit storage), rows 2 K wide
+template <class T>
+hipError_t launch_cast2(const float* src, int64_t s_g, int N, int K, T* dst, int64_t d_g, int G, hipStream_t st);
 
 }  // namespace pigan

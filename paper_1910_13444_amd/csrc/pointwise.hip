@@ -9,7 +9,8 @@
 namespace pigan {
 
 // ---------------------------------------------------------------------------
-// zp[g][s][n] = b1[n] + sum_j W1[n][d + j] z[g][s][j]      (fp32)
+// zp[g][s][n] = b1[n] + sum_j W1[n][d + j] z[g][s][j]   (summed in fp64,
+// stored in fp32)
 // ---------------------------------------------------------------------------
 __global__ void k_zproj(const float* __restrict__ p1, int64_t p_g, int in_dim, int d, int W,
                         const float* __restrict__ z, int64_t z_g, int n_z, int S, float* __restrict__ zp,
@@ -20,9 +21,9 @@ __global__ void k_zproj(const float* __restrict__ p1, int64_t p_g, int in_dim, i
   const int s = (int)(idx / W), n = (int)(idx % W);
   const float* Wn = p1 + g * p_g + (int64_t)n * in_dim + d;
   const float* zs = z + g * z_g + (int64_t)s * n_z;
-  float a = p1[g * p_g + (int64_t)W * in_dim + n];
-  for (int j = 0; j < n_z; ++j) a += Wn[j] * zs[j];
-  zp[g * zp_g + idx] = a;
+  double a = (double)p1[g * p_g + (int64_t)W * in_dim + n];
+  for (int j = 0; j < n_z; ++j) a += (double)Wn[j] * (double)zs[j];
+  zp[g * zp_g + idx] = (float)a;
 }
 
 // ---------------------------------------------------------------------------
@@ -64,7 +65,7 @@ __device__ __forceinline__ void store8(T* p, const float* v) {
 // leave as full 16-byte pieces of consecutive columns.
 constexpr int FF_PPB = 32;
 
-template <class T, int ND1, int ND2>
+template <class T, int ND1, int ND2, bool X64 = false>
 __global__ void __launch_bounds__(256)
 k_first_fwd(FirstArgs<T> p) {
   constexpr int C = 1 + ND1 + ND2;
@@ -104,7 +105,7 @@ k_first_fwd(FirstArgs<T> p) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         float t, sd;
-        tanh_ts(a[e], t, sd);
+        tanh_pair<X64>(a[e], t, sd);
         h[0][e] = t;
         s8[e] = sd;
         sp8[e] = -2.0f * t * sd;
@@ -134,7 +135,8 @@ k_first_fwd(FirstArgs<T> p) {
 
 // ---------------------------------------------------------------------------
 // scalar output layer: y[row] = w_out . H[row] (+ b_out on value rows)
-// eight lanes per row, 16-byte loads, shuffle reduction
+// eight lanes per row, 16-byte loads, shuffle reduction; fp32 storage (the
+// sensor rows and the critic) sums in fp64
 // ---------------------------------------------------------------------------
 template <class T>
 __global__ void __launch_bounds__(256)
@@ -144,21 +146,22 @@ k_out_fwd(const T* __restrict__ H, int64_t h_g, int64_t ldh, int64_t R, int64_t 
   const int g = blockIdx.z;
   const int team = threadIdx.x >> 3, e = threadIdx.x & 7;
   const int64_t row = (int64_t)blockIdx.x * 32 + team;
+  typedef typename std::conditional<sizeof(T) == 4, double, float>::type Acc;
   const float* w = wout + g * w_g;
-  float acc = 0.0f;
+  Acc acc = 0;
   if (row < R) {
     const T* hr = H + g * h_g + row * ldh;
     for (int c = e * EPP; c < W; c += 8 * EPP) {
       uint4 v = *(const uint4*)(hr + c);
       const T* hv = (const T*)&v;
 #pragma unroll
-      for (int q = 0; q < EPP; ++q) acc += w[c + q] * Elem<T>::to_f(hv[q]);
+      for (int q = 0; q < EPP; ++q) acc += (Acc)w[c + q] * (Acc)Elem<T>::to_f(hv[q]);
     }
   }
   acc += __shfl_xor(acc, 1);
   acc += __shfl_xor(acc, 2);
   acc += __shfl_xor(acc, 4);
-  if (row < R && e == 0) y[g * y_g + row] = acc + (row < n_value ? w[W] : 0.0f);
+  if (row < R && e == 0) y[g * y_g + row] = (float)(acc + (row < n_value ? (Acc)w[W] : (Acc)0));
 }
 
 // ---------------------------------------------------------------------------
@@ -361,7 +364,7 @@ k_disc_seed(const float* __restrict__ score, int64_t sc_g, int n_fake, int n_rea
 // 256/TPP points per pass; up to two column groups per thread (W <= 4096).
 // Partials are fp64: part[g][slot][W+1].
 // ---------------------------------------------------------------------------
-template <class T, int ND1, int ND2>
+template <class T, int ND1, int ND2, bool X64 = false>
 __global__ void __launch_bounds__(256)
 k_out_bwd(OutBwdArgs<T> p) {
   constexpr int C = 1 + ND1 + ND2;
@@ -406,7 +409,7 @@ k_out_bwd(OutBwdArgs<T> p) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         float t, s;
-        tanh_ts(ap[0][e], t, s);
+        tanh_pair<X64>(ap[0][e], t, s);
         const float sp = -2.0f * t * s;
         const float spp = 2.0f * s * (3.0f * t * t - 1.0f);
         float hsum = gk[0] * t;
@@ -472,7 +475,7 @@ k_out_bwd(OutBwdArgs<T> p) {
 // (for the skip below the top block) when p.gh is set, then carried back
 // through tanh into dA.  fp64 per-block partials [2 (W + 1)], fixed order.
 // ---------------------------------------------------------------------------
-template <class T, int ND1, int ND2>
+template <class T, int ND1, int ND2, bool X64 = false>
 __global__ void __launch_bounds__(256)
 k_out2_bwd(Out2BwdArgs<T> p) {
   constexpr int C = 1 + ND1 + ND2;
@@ -546,7 +549,7 @@ k_out2_bwd(Out2BwdArgs<T> p) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         float t, s;
-        tanh_ts(ap[0][e], t, s);
+        tanh_pair<X64>(ap[0][e], t, s);
         const float sp = -2.0f * t * s;
         const float spp = 2.0f * s * (3.0f * t * t - 1.0f);
         float ga = s * gh[0][e];
@@ -824,7 +827,7 @@ k_colsum(const Tin* __restrict__ part, int64_t p_g, int n_slots, int64_t slot_st
 template <class T>
 __global__ void __launch_bounds__(256)
 k_first_bwd(FirstBwdArgs<T> p) {
-  __shared__ float red[256 * 8];
+  __shared__ double red[256 * 8];
   const int g = blockIdx.z;
   const int s = blockIdx.x / p.nrc;
   const int rc = blockIdx.x % p.nrc;
@@ -838,26 +841,27 @@ k_first_bwd(FirstBwdArgs<T> p) {
   const bool valid = cg < G8;
   const int n0 = cg * 8;
   const int d = p.d;
-  float acc[7][8];
+  double acc[7][8];
 #pragma unroll
   for (int q = 0; q < 7; ++q)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[q][e] = 0.0f;
+    for (int e = 0; e < 8; ++e) acc[q][e] = 0.0;
   const T* A = p.dA + g * p.a_g;
   if (valid) {
     const int j0 = (int)((int64_t)p.n_s * rc / p.nrc), j1 = (int)((int64_t)p.n_s * (rc + 1) / p.nrc);
+    const float* As = p.dAs + g * p.as_g;
     for (int j = j0 + lp; j < j1; j += PPP) {
       float v[8];
-      load8<T>(A + ((int64_t)s * p.n_s + j) * p.lda + n0, v);
+      load8<float>(As + ((int64_t)s * p.n_s + j) * p.ldas + n0, v);
       const float* xv = p.xs + g * p.xs_g + (int64_t)j * d;
-      float x[3];
+      double x[3];
 #pragma unroll
-      for (int i = 0; i < 3; ++i) x[i] = i < d ? xv[i] : 0.0f;
+      for (int i = 0; i < 3; ++i) x[i] = i < d ? (double)xv[i] : 0.0;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        acc[0][e] += v[e];
+        acc[0][e] += (double)v[e];
 #pragma unroll
-        for (int i = 0; i < 3; ++i) acc[1 + i][e] += v[e] * x[i];
+        for (int i = 0; i < 3; ++i) acc[1 + i][e] += (double)v[e] * x[i];
       }
     }
     const int q0 = (int)((int64_t)p.P * rc / p.nrc), q1 = (int)((int64_t)p.P * (rc + 1) / p.nrc);
@@ -865,42 +869,40 @@ k_first_bwd(FirstBwdArgs<T> p) {
     for (int q = q0 + lp; q < q1; q += PPP) {
       const int64_t pt = (int64_t)s * p.P + q;
       float v[8];
-      load8<T>(A + (p.n_sen + pt) * p.lda + n0, v);
+      load8<T>(A + pt * p.lda + n0, v);
       const float* xv = p.xc + g * p.xc_g + pt * d;
       float x[3];
 #pragma unroll
       for (int i = 0; i < 3; ++i) x[i] = i < d ? xv[i] : 0.0f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        acc[0][e] += v[e];
+        acc[0][e] += (double)v[e];
 #pragma unroll
-        for (int i = 0; i < 3; ++i) acc[1 + i][e] += v[e] * x[i];
+        for (int i = 0; i < 3; ++i) acc[1 + i][e] += (double)(v[e] * x[i]);
       }
 #pragma unroll
       for (int i = 0; i < 3; ++i) {
         if (i >= p.nd1) continue;
         float u[8];
-        load8<T>(A + (p.n_sen + (1 + i) * p.n_col + pt) * p.lda + n0, u);
+        load8<T>(A + ((1 + i) * p.n_col + pt) * p.lda + n0, u);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[4 + i][e] += u[e];
+        for (int e = 0; e < 8; ++e) acc[4 + i][e] += (double)u[e];
       }
     }
   }
-  float* out = p.part + (((int64_t)g * p.S + s) * p.nrc + rc) * 7 * W;
+  double* out = p.part + (((int64_t)g * p.S + s) * p.nrc + rc) * 7 * W;
 #pragma unroll
   for (int q = 0; q < 7; ++q) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) red[threadIdx.x * 8 + e] = acc[q][e];
     __syncthreads();
     if (lp == 0 && valid) {
-      float v[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        float t = 0.0f;
+        double t = 0.0;
         for (int u = 0; u < PPP; ++u) t += red[(u * TPP + lt) * 8 + e];
-        v[e] = t;
+        out[(int64_t)q * W + n0 + e] = t;
       }
-      store8<float>(out + (int64_t)q * W + n0, v);
     }
     __syncthreads();
   }
@@ -910,7 +912,7 @@ k_first_bwd(FirstBwdArgs<T> p) {
 //   c < d : sum_{s,rc} gx_c + gd_c ;  c >= d : sum_{s,rc} gs * z_s[c-d] ;
 //   bias (blockIdx.y == in_dim) : sum_{s,rc} gs
 __global__ void __launch_bounds__(1024)
-k_first_wgrad(const float* __restrict__ part, int S, int nrc, int W, int d, int nd1, int in_dim,
+k_first_wgrad(const double* __restrict__ part, int S, int nrc, int W, int d, int nd1, int in_dim,
               const float* __restrict__ z, int64_t z_g, int n_z, float* grad, int64_t g_g, int accumulate,
               float scale, int32_t* nonfinite) {
   __shared__ double red[32][32];
@@ -920,17 +922,17 @@ k_first_wgrad(const float* __restrict__ part, int S, int nrc, int W, int d, int 
   const int n = blockIdx.x * 32 + lane;
   double acc = 0.0;
   if (n < W) {
-    const float* pp = part + (int64_t)g * S * nrc * 7 * W + n;
+    const double* pp = part + (int64_t)g * S * nrc * 7 * W + n;
     const bool xcol = c < d;                       // weight of coordinate c: sum of gx_c and gd_c
     const bool two = xcol && c < nd1;
     const int64_t o1 = xcol ? (int64_t)(1 + c) * W : 0, o2 = (int64_t)(4 + c) * W;
     for (int s = grp; s < S; s += 32) {
-      const float* b = pp + (int64_t)s * nrc * 7 * W;
+      const double* b = pp + (int64_t)s * nrc * 7 * W;
       double t = 0.0;
 #pragma unroll 4
       for (int r = 0; r < nrc; ++r) {
-        t += (double)b[(int64_t)r * 7 * W + o1];
-        if (two) t += (double)b[(int64_t)r * 7 * W + o2];
+        t += b[(int64_t)r * 7 * W + o1];
+        if (two) t += b[(int64_t)r * 7 * W + o2];
       }
       if (!xcol && c < in_dim) t *= (double)z[g * z_g + (int64_t)s * n_z + (c - d)];
       acc += t;
@@ -1013,6 +1015,21 @@ k_cast_tr(const float* __restrict__ src, int64_t s_g, int N, int K, int Kp, T* _
   }
 }
 
+// two-term weights: dst[n] = [hi(W[n][:]) | lo(W[n][:])] (2 K wide), with
+// hi = W rounded to the storage type and lo = W - hi rounded likewise
+template <class T>
+__global__ void k_cast2(const float* __restrict__ src, int64_t s_g, int N, int K, T* __restrict__ dst, int64_t d_g) {
+  const int g = blockIdx.z;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)N * K) return;
+  const int64_t n = idx / K, k = idx % K;
+  const float v = src[g * s_g + idx];
+  const T hi = Elem<T>::from_f(v);
+  const T lo = Elem<T>::from_f(v - Elem<T>::to_f(hi));
+  dst[g * d_g + n * 2 * K + k] = hi;
+  dst[g * d_g + n * 2 * K + K + k] = lo;
+}
+
 template <class T>
 __global__ void k_cast(const float* __restrict__ src, int64_t s_g, int N, int K, int Kp, T* __restrict__ dst,
                        T* __restrict__ dstT, int64_t d_g) {
@@ -1037,21 +1054,29 @@ hipError_t launch_zproj(const float* p1, int64_t p_g, int in_dim, int d, int W, 
   return hipGetLastError();
 }
 
+template <class T, bool X64>
+static hipError_t first_fwd_nd(int nd1, int nd2, const FirstArgs<T>& a, dim3 grid, hipStream_t st) {
+  switch (nd1 * 10 + nd2) {
+    case 0: k_first_fwd<T, 0, 0, X64><<<grid, 256, 0, st>>>(a); break;
+    case 10: k_first_fwd<T, 1, 0, X64><<<grid, 256, 0, st>>>(a); break;
+    case 20: k_first_fwd<T, 2, 0, X64><<<grid, 256, 0, st>>>(a); break;
+    case 30: k_first_fwd<T, 3, 0, X64><<<grid, 256, 0, st>>>(a); break;
+    case 11: k_first_fwd<T, 1, 1, X64><<<grid, 256, 0, st>>>(a); break;
+    case 22: k_first_fwd<T, 2, 2, X64><<<grid, 256, 0, st>>>(a); break;
+    case 33: k_first_fwd<T, 3, 3, X64><<<grid, 256, 0, st>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 template <class T>
 hipError_t launch_first_fwd(int nd1, int nd2, const FirstArgs<T>& a, int G, hipStream_t st) {
   if (a.seg.n_points <= 0) return hipSuccess;
   dim3 grid(nblk(a.seg.n_points, FF_PPB), 1, G);
-  switch (nd1 * 10 + nd2) {
-    case 0: k_first_fwd<T, 0, 0><<<grid, 256, 0, st>>>(a); break;
-    case 10: k_first_fwd<T, 1, 0><<<grid, 256, 0, st>>>(a); break;
-    case 20: k_first_fwd<T, 2, 0><<<grid, 256, 0, st>>>(a); break;
-    case 30: k_first_fwd<T, 3, 0><<<grid, 256, 0, st>>>(a); break;
-    case 11: k_first_fwd<T, 1, 1><<<grid, 256, 0, st>>>(a); break;
-    case 22: k_first_fwd<T, 2, 2><<<grid, 256, 0, st>>>(a); break;
-    case 33: k_first_fwd<T, 3, 3><<<grid, 256, 0, st>>>(a); break;
-    default: return hipErrorInvalidValue;
+  if constexpr (sizeof(T) == 4) {
+    if (a.exact) return first_fwd_nd<T, true>(nd1, nd2, a, grid, st);
   }
-  return hipGetLastError();
+  return first_fwd_nd<T, false>(nd1, nd2, a, grid, st);
 }
 
 template <class T>
@@ -1133,18 +1158,38 @@ hipError_t launch_disc_seed(const float* score, int64_t sc_g, int n_fake, int n_
 
 int out_bwd_blocks(int64_t n_points, int ppb) { return (int)nblk(n_points, ppb); }
 
+template <class T, bool X64>
+static hipError_t out_bwd_nd(int nd1, int nd2, const OutBwdArgs<T>& a, dim3 grid, hipStream_t st) {
+  switch (nd1 * 10 + nd2) {
+    case 0: k_out_bwd<T, 0, 0, X64><<<grid, 256, 0, st>>>(a); break;
+    case 10: k_out_bwd<T, 1, 0, X64><<<grid, 256, 0, st>>>(a); break;
+    case 20: k_out_bwd<T, 2, 0, X64><<<grid, 256, 0, st>>>(a); break;
+    case 30: k_out_bwd<T, 3, 0, X64><<<grid, 256, 0, st>>>(a); break;
+    case 11: k_out_bwd<T, 1, 1, X64><<<grid, 256, 0, st>>>(a); break;
+    case 22: k_out_bwd<T, 2, 2, X64><<<grid, 256, 0, st>>>(a); break;
+    case 33: k_out_bwd<T, 3, 3, X64><<<grid, 256, 0, st>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 template <class T>
 hipError_t launch_out_bwd(int nd1, int nd2, const OutBwdArgs<T>& a, int G, hipStream_t st) {
   if (a.seg.n_points <= 0) return hipSuccess;
   dim3 grid(nblk(a.seg.n_points, a.ppb), 1, G);
+  if constexpr (sizeof(T) == 4) {
+    if (a.exact) return out_bwd_nd<T, true>(nd1, nd2, a, grid, st);
+  }
+  return out_bwd_nd<T, false>(nd1, nd2, a, grid, st);
+}
+
+template <class T, bool X64>
+static hipError_t out2_bwd_nd(int nd1, int nd2, const Out2BwdArgs<T>& a, dim3 grid, hipStream_t st) {
   switch (nd1 * 10 + nd2) {
-    case 0: k_out_bwd<T, 0, 0><<<grid, 256, 0, st>>>(a); break;
-    case 10: k_out_bwd<T, 1, 0><<<grid, 256, 0, st>>>(a); break;
-    case 20: k_out_bwd<T, 2, 0><<<grid, 256, 0, st>>>(a); break;
-    case 30: k_out_bwd<T, 3, 0><<<grid, 256, 0, st>>>(a); break;
-    case 11: k_out_bwd<T, 1, 1><<<grid, 256, 0, st>>>(a); break;
-    case 22: k_out_bwd<T, 2, 2><<<grid, 256, 0, st>>>(a); break;
-    case 33: k_out_bwd<T, 3, 3><<<grid, 256, 0, st>>>(a); break;
+    case 0: k_out2_bwd<T, 0, 0, X64><<<grid, 256, 0, st>>>(a); break;
+    case 11: k_out2_bwd<T, 1, 1, X64><<<grid, 256, 0, st>>>(a); break;
+    case 22: k_out2_bwd<T, 2, 2, X64><<<grid, 256, 0, st>>>(a); break;
+    case 33: k_out2_bwd<T, 3, 3, X64><<<grid, 256, 0, st>>>(a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -1154,14 +1199,10 @@ template <class T>
 hipError_t launch_out2_bwd(int nd1, int nd2, const Out2BwdArgs<T>& a, int G, hipStream_t st) {
   if (a.seg.n_points <= 0) return hipSuccess;
   dim3 grid(nblk(a.seg.n_points, a.ppb), 1, G);
-  switch (nd1 * 10 + nd2) {
-    case 0: k_out2_bwd<T, 0, 0><<<grid, 256, 0, st>>>(a); break;
-    case 11: k_out2_bwd<T, 1, 1><<<grid, 256, 0, st>>>(a); break;
-    case 22: k_out2_bwd<T, 2, 2><<<grid, 256, 0, st>>>(a); break;
-    case 33: k_out2_bwd<T, 3, 3><<<grid, 256, 0, st>>>(a); break;
-    default: return hipErrorInvalidValue;
+  if constexpr (sizeof(T) == 4) {
+    if (a.exact) return out2_bwd_nd<T, true>(nd1, nd2, a, grid, st);
   }
-  return hipGetLastError();
+  return out2_bwd_nd<T, false>(nd1, nd2, a, grid, st);
 }
 
 hipError_t launch_concat_rows(const float* a, int64_t a_g, int na, const float* b, int64_t b_g, int nb, int d,
@@ -1252,7 +1293,7 @@ hipError_t launch_first_bwd(const FirstBwdArgs<T>& a, int G, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_first_wgrad(const float* part, int S, int nrc, int W, int d, int nd1, int in_dim, const float* z,
+hipError_t launch_first_wgrad(const double* part, int S, int nrc, int W, int d, int nd1, int in_dim, const float* z,
                               int64_t z_g, int n_z, float* grad, int64_t g_g, int accumulate, float scale,
                               int32_t* nonfinite, int G, hipStream_t st) {
   k_first_wgrad<<<dim3(nblk(W, 32), in_dim + 1, G), 1024, 0, st>>>(part, S, nrc, W, d, nd1, in_dim, z, z_g, n_z,
@@ -1283,6 +1324,14 @@ hipError_t launch_cast(const float* src, int64_t s_g, int N, int K, int Kp, T* d
     k_cast<T><<<dim3(nblk((int64_t)N * Kp, 256), 1, G), 256, 0, st>>>(src, s_g, N, K, Kp, dst, dstT, d_g);
   return hipGetLastError();
 }
+
+template <class T>
+hipError_t launch_cast2(const float* src, int64_t s_g, int N, int K, T* dst, int64_t d_g, int G, hipStream_t st) {
+  k_cast2<T><<<dim3(nblk((int64_t)N * K, 256), 1, G), 256, 0, st>>>(src, s_g, N, K, dst, d_g);
+  return hipGetLastError();
+}
+template hipError_t launch_cast2<bf16>(const float*, int64_t, int, int, bf16*, int64_t, int, hipStream_t);
+template hipError_t launch_cast2<f16>(const float*, int64_t, int, int, f16*, int64_t, int, hipStream_t);
 
 #define PIGAN_INST(T)                                                                                         \
   template hipError_t launch_first_fwd<T>(int, int, const FirstArgs<T>&, int, hipStream_t);                  \

@@ -3,10 +3,11 @@ samples x P=1024 collocation points, 200+200 sensors, 3x256 discriminator,
 bf16), in the launch configuration the benchmark times:
 
 * generator jets at sampled (sample, point) pairs against the oracle;
-* the three losses against the oracle evaluated at full size;
-* gradients through a property that holds at any size: the step is a mean
-  over noise samples, so the full step equals the average of the steps on
-  the two halves of the samples (same real batch).
+* the three losses and every weight and bias gradient against the oracle
+  evaluated at full size (normwise per tensor, max|d| / max|oracle| printed);
+* a property that holds at any size: the step is a mean over noise samples,
+  so the full step equals the average of the steps on the two halves of the
+  samples (same real batch).
 
 The grouped 16-subdomain workload (4x256, S=128, P=1024) and the 6x1024 step
 with the 5x2048 critic (S=1024, P=2048) get sampled jets of several groups
@@ -19,7 +20,7 @@ import pytest
 import oracle
 from paper_1910_13444_amd import configs, pigan
 from paper_1910_13444_amd.inputs import make_inputs
-from _parity import TOL, check, check_conditioned, rel, run_step_gpu, to_dev
+from _parity import TOL, amax_rel, check, rel, run_step_gpu, step_errors, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -79,45 +80,17 @@ def test_full_jets_sampled_large(wl):
     torch.cuda.empty_cache()
 
 
-def _oracle_losses(inp, real, prec=None, with_pde=True, chunk=32):
-    """Losses of the step at full size from the oracle's forward passes."""
-    gs, ds, d = WL.gen_shape(), WL.disc_shape(), WL.d
-    g = 0
-    F = oracle.snapshots(inp.pY[g], inp.pU[g], gs, d, inp.xsY[g], inp.xsU[g], inp.z[g]) if prec is None else None
-    if prec is not None:
-        from oracle.pigan_oracle import sensor_rows, gen_forward
-        S = inp.z.shape[1]
-        XY, ZY = sensor_rows(inp.xsY[g], inp.z[g])
-        XU, ZU = sensor_rows(inp.xsU[g], inp.z[g])
-        F = np.concatenate([gen_forward(inp.pY[g], gs, d, XY, ZY, 0, prec=prec)["y"].reshape(S, -1),
-                            gen_forward(inp.pU[g], gs, d, XU, ZU, 0, prec=prec)["y"].reshape(S, -1)], axis=1)
-    DF = oracle.mlp_forward(inp.pD[g], ds, F, prec=prec)
-    DR = oracle.mlp_forward(inp.pD[g], ds, real[g], prec=prec)
-    w = float(inp.w_group[g])
-    out = {"L_D": w * (DF.mean() - DR.mean()), "L_adv": -w * DF.mean()}
-    if with_pde:
-        r2 = 0.0
-        for s0 in range(0, WL.S, chunk):
-            z = inp.z[g][s0:s0 + chunk]
-            x = inp.xc[g][s0:s0 + chunk]
-            jY = oracle.gen_jets(inp.pY[g], gs, d, z, x, 1)
-            jU = oracle.gen_jets(inp.pU[g], gs, d, z, x, 2)
-            r = oracle.darcy_residual(jY[0], jY[1:1 + d], jU[1:1 + d], jU[1 + d:], WL.f_const)
-            r2 += float((r * r).sum())
-        out["L_pde"] = w * WL.lambda_pde * r2 / (WL.S * WL.P)
-    return out
-
-
-def test_full_losses(full):
+def test_full_step_against_oracle(full):
+    """The whole 2-D step at full size (S=256, P=1024), bf16, in the launch
+    configuration the benchmark times: the three losses and every weight and
+    bias gradient of both generators and the critic against the oracle's
+    full step."""
     inp, real = full
-    print("full-size step losses", flush=True)
+    print("full-size step: losses and every gradient tensor", flush=True)
     out = run_step_gpu(WL, inp, real)
     assert out["nonfinite"] == 0
-    ref = _oracle_losses(inp, real)
-    errs = {k: rel(out["loss"][0, i], ref[k]) for i, k in enumerate(("L_D", "L_adv", "L_pde"))}
-    model = _oracle_losses(inp, real, prec=WL.dtype, with_pde=False)
-    merrs = {k: rel(model[k], ref[k]) for k in ("L_D", "L_adv")}
-    check_conditioned(errs, merrs, TOL[WL.dtype], "full losses")
+    ref = oracle.train_step(WL, inp, real, chunk_S=32)
+    check(step_errors(WL, out, ref), TOL[WL.dtype], "full step", maxe=step_errors(WL, out, ref, amax_rel))
 
 
 def test_full_step_is_mean_of_half_steps(full):

@@ -2,12 +2,9 @@
 same seeded inputs.
 
 Metric: normwise relative error per tensor (every jet component, the residual
-r and r + f separately, every layer's weight and bias gradient, each loss).
-Bar: 1e-5 in fp32 mode, 2e-2 in bf16/fp16 mode.  For training-step outputs the
-bar of a tensor is raised to 3x the error of the oracle's precision model
-(the same definitions with the library's storage format and fp32 products)
-when that model itself misses the bar: such tensors are sums of nearly
-cancelling terms, so any evaluation in that format carries that error."""
+r and r + f separately, every layer's weight and bias gradient, each loss),
+with max|d| / max|oracle| printed beside it.  Bar: 1e-5 in fp32 mode, 2e-2 in
+bf16/fp16 mode, for every tensor."""
 import sys
 
 import numpy as np
@@ -16,7 +13,7 @@ import pytest
 import oracle
 from paper_1910_13444_amd import configs, pigan
 from paper_1910_13444_amd.inputs import glorot_mlp, make_inputs
-from _parity import TOL, check, check_conditioned, rel, run_step_gpu, step_errors, to_dev
+from _parity import TOL, amax_rel, check, rel, run_step_gpu, step_errors, to_dev
 from _tiny import TINY1, TINY2, TINY3
 
 pytestmark = pytest.mark.gpu
@@ -59,6 +56,43 @@ def test_gen_forward(dtype, d, order, x_shared, L, W, S, P):
         ref = oracle.gen_jets(p[g], shape, d, z[g], x[g], order)
         errs = {f"g{g}.c{k}": rel(jet[g, k], ref[k]) for k in range(ref.shape[0])}
         check(errs, TOL[dtype], "gen_forward")
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_gen_forward_saturated(dtype):
+    """Every hidden unit saturated: biases of magnitude 5 to 10 put |a| in
+    about [4, 11], where 1 - tanh^2 computed from tanh in fp32 loses most of
+    its digits (s = 4.5e-7 at |a| = 8 next to an fp32 spacing of 6e-8 near 1)
+    while the jets are built from s alone.  The oracle's fp64 1 - tanh^2
+    keeps about 1e-6 relative accuracy up to |a| = 12."""
+    _say(f"gen_forward saturated units dtype={dtype}")
+    import torch
+    from oracle.pigan_oracle import unpack
+    rng = np.random.default_rng(77)
+    d, n_z, L, W, S, P = 2, 5, 3, 128, 3, 200
+    shape = (d + n_z, L, W)
+    p = glorot_mlp(rng, *shape)
+    off = 0
+    fan = d + n_z
+    for _ in range(L):                       # biases +-[5, 10]
+        off += W * fan
+        p[off:off + W] = rng.choice([-1.0, 1.0], W) * rng.uniform(5.0, 10.0, W)
+        off += W
+        fan = W
+    p = p[None]
+    z = rng.standard_normal((1, S, n_z)).astype(np.float32)
+    x = rng.random((1, S, P, d)).astype(np.float32)
+    layers, _, _ = unpack(p[0], *shape)
+    a1 = x[0].reshape(-1, d) @ layers[0][0][:, :d].T.astype(np.float64) + \
+        np.repeat(z[0], P, 0) @ layers[0][0][:, d:].T.astype(np.float64) + layers[0][1]
+    assert np.abs(a1).min() > 3.5 and np.abs(a1).max() < 12.0
+    jet = pigan.gen_forward(to_dev(p), shape, d, to_dev(z), to_dev(x), 2, dtype=dtype)
+    torch.cuda.synchronize()
+    jet = jet.cpu().numpy()[0]
+    ref = oracle.gen_jets(p[0], shape, d, z[0], x[0], 2)
+    assert np.abs(ref[1:]).max() < 1e-2 * np.abs(ref[0]).max()   # the derivative jets are small: s is tiny
+    check({f"c{k}": rel(jet[k], ref[k]) for k in range(ref.shape[0])}, TOL[dtype], "gen_forward saturated",
+          maxe={f"c{k}": amax_rel(jet[k], ref[k]) for k in range(ref.shape[0])})
 
 
 def test_pde_residual():
@@ -110,11 +144,11 @@ STEP_CASES = {
     "c2_S3_fp32": (configs.C2.with_(S=3, P=333, B_r=4, dtype="fp32"), dict(f_array=True)),
     "c4_groups_S2_bf16": (configs.C4.with_(S=2, P=96, B_r=2), {}),
     "c3_S2_bf16": (configs.C3.with_(S=2, P=256, B_r=2), {}),
-    "c5_S1_bf16": (configs.C5.with_(S=1, P=128, B_r=1), {}),
+    "c5_S2_bf16": (configs.C5.with_(S=2, P=128, B_r=2), {}),
     "c2_S3_ragged_bf16_f": (configs.C2.with_(S=3, P=1000, B_r=3), dict(f_array=True)),
     "c3_S2_fp32": (configs.C3.with_(S=2, P=256, B_r=2, dtype="fp32"), {}),
     "c4_groups_S2_fp32": (configs.C4.with_(S=2, P=96, B_r=2, dtype="fp32"), {}),
-    "c5_S1_fp32": (configs.C5.with_(S=1, P=128, B_r=1, dtype="fp32"), {}),
+    "c5_S2_fp32": (configs.C5.with_(S=2, P=128, B_r=2, dtype="fp32"), {}),
 }
 
 
@@ -133,13 +167,7 @@ def _step_case(wl, inp, key, label, **kw):
     real, ref = _oracle_step(wl, inp, key)
     out = run_step_gpu(wl, inp, real, **kw)
     assert out["nonfinite"] == 0
-    errs = step_errors(wl, out, ref)
-    tol = TOL[wl.dtype]
-    if max(errs.values()) <= tol:
-        check(errs, tol, label)
-        return
-    model = oracle.train_step(wl, inp, real, prec=wl.dtype)
-    check_conditioned(errs, step_errors(wl, model, ref), tol, label)
+    check(step_errors(wl, out, ref), TOL[wl.dtype], label, maxe=step_errors(wl, out, ref, amax_rel))
 
 
 @pytest.mark.parametrize("case", list(STEP_CASES))
@@ -151,7 +179,7 @@ def test_train_step(case):
 
 
 def test_train_step_fp16_loss_scale():
-    wl = configs.C5H.with_(S=1, P=128, B_r=1)
+    wl = configs.C5H.with_(S=2, P=128, B_r=2)
     _say("train_step fp16 C5-shaped with loss scale 1024")
     inp = make_inputs(wl)
     _step_case(wl, inp, (wl.seed, wl.S, wl.P, wl.G, "{}"), "c5_fp16", loss_scale=1024.0)

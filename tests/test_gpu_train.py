@@ -100,7 +100,10 @@ def test_trainer_matches_oracle(schedule, arch):
     eL = rel(losses.reshape(ref_losses.shape), ref_losses)
     print(f"weight change rel err: generator {eG:.3g}, critic {eD:.3g}; losses {eL:.3g}")
     assert losses.shape[0] == ref_losses.shape[0]
-    assert eG <= 1e-3 and eD <= 1e-3 and eL <= 1e-4
+    # losses at the fp32 bar; weight changes within 2e-5 (Adam's normalised update
+    # divides by sqrt(v) + eps, so coordinates with tiny gradients amplify their
+    # error; measured at most 4.1e-6 over these schedules)
+    assert eG <= 2e-5 and eD <= 2e-5 and eL <= 1e-5
 
 
 def test_dynamic_loss_scale_fp16_skips_overflow():
@@ -115,9 +118,18 @@ def test_dynamic_loss_scale_fp16_skips_overflow():
     torch.cuda.synchronize()
     assert tr.skipped == 2 and tr.scaler.scale == 2.0 ** 38
     assert torch.equal(pD0, tr.pD)               # skipped on the device: weights untouched
-    tr.run(20)
-    print(f"after 21 rounds: scale 2^{np.log2(tr.scaler.scale):.0f}, skipped {tr.skipped}")
-    assert tr.scaler.scale <= 2.0 ** 24 and tr.skipped < 42
+    # the scale comes down to one at which steps stop overflowing: some block
+    # of 4 rounds (8 step calls) runs without a skip within 60 rounds
+    clean = False
+    for _ in range(15):
+        before = tr.skipped
+        tr.run(4)
+        torch.cuda.synchronize()
+        if tr.skipped == before:
+            clean = True
+            break
+    print(f"scale 2^{np.log2(tr.scaler.scale):.0f}, skipped {tr.skipped}")
+    assert clean and tr.scaler.scale < 2.0 ** 38
     assert not torch.equal(pD0, tr.pD)
     assert torch.isfinite(tr.pD).all() and all(torch.isfinite(g).all() for g in tr.gen)
 
@@ -182,7 +194,10 @@ def test_hier_trainer_matches_oracle(schedule, arch):
     eL = rel(losses, ref_losses)
     print(f"weight change rel err: generator {eG:.3g}, critics {eD:.3g}; losses {eL:.3g}")
     assert losses.shape == ref_losses.shape
-    assert eG <= 1e-3 and eD <= 1e-3 and eL <= 1e-4
+    # losses at the fp32 bar; weight changes within 2e-5 (Adam's normalised update
+    # divides by sqrt(v) + eps, so coordinates with tiny gradients amplify their
+    # error; measured at most 4.1e-6 over these schedules)
+    assert eG <= 2e-5 and eD <= 2e-5 and eL <= 1e-5
 
 
 @pytest.mark.parametrize("schedule,arch", [("sequential", "pair"), ("parallel", "trunk"), ("sequential", "hier")])
@@ -262,4 +277,7 @@ def test_trainer_with_gradient_penalty_matches_oracle(schedule, arch):
     eD = rel(gpu_D - pD0, pD - pD0)
     eL = rel(losses.reshape(ref_losses.shape), ref_losses)
     print(f"weight change rel err: generator {eG:.3g}, critic {eD:.3g}; losses {eL:.3g}")
-    assert eG <= 1e-3 and eD <= 1e-3 and eL <= 1e-4
+    # losses at the fp32 bar; weight changes within 2e-5 (Adam's normalised update
+    # divides by sqrt(v) + eps, so coordinates with tiny gradients amplify their
+    # error; measured at most 4.1e-6 over these schedules)
+    assert eG <= 2e-5 and eD <= 2e-5 and eL <= 1e-5
