@@ -30,9 +30,17 @@
  *    and groups are stacked contiguously: params[g * n_params + i].
  *  - Generator input order is [x_1..x_d, z_1..z_nz] (in_dim = d + n_z).
  *  - The arithmetic type (pigan_dtype) selects the storage and matrix-core
- *    operand type of the hidden layers; accumulation, the first generator
- *    layer, tanh and its derivatives, the residual, losses and gradients are
- *    always fp32.
+ *    operand type of the generators' hidden layers at the collocation points
+ *    (the residual's jets); in bf16/fp16 their forward products take the
+ *    fp32 weights as two terms, hi + lo in that type.  The adversarial path --
+ *    the generators at the sensors and the discriminator -- is stored in fp32
+ *    in every mode, with products from two bf16 pieces per fp32 operand in
+ *    bf16/fp16 modes and from the fp64 matrix core in fp32 mode (there tanh
+ *    and its derivatives are evaluated in fp64).  At the initial weights the
+ *    critic responds far less to a uniform shift of a sensor block than to
+ *    single sensors, so the sensor-row gradients are small differences of
+ *    large terms and need the extra precision.  Accumulation, the first
+ *    generator layer, the residual, losses and gradients are fp32 or wider.
  *  - Results are deterministic run to run (fixed-order reductions, no float
  *    atomics).
  */
@@ -55,7 +63,7 @@ typedef enum {
 } pigan_status;
 
 typedef enum {
-  PIGAN_FP32 = 0,        /* fp32 storage, fp32 matrix cores */
+  PIGAN_FP32 = 0,        /* fp32 storage, fp32 matrix cores (fp64 on the adversarial path) */
   PIGAN_BF16 = 1,        /* bf16 storage (round-to-nearest-even), fp32 accumulate */
   PIGAN_FP16 = 2         /* fp16 storage (round-to-nearest-even), fp32 accumulate */
 } pigan_dtype;

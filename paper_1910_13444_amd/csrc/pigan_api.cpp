@@ -181,7 +181,8 @@ static int64_t ob_ppb(int64_t n_points, int W) {
 // contractions in fp32, moves them by several hundred rounding units.  In
 // fp32 mode those products run on the fp64 matrix core (fp32 operands are
 // exact in fp64, one rounding per result); in 16-bit modes two bf16 pieces
-// per operand suffice for their bar.
+// per operand (about 16 significand bits each, three products) keep those
+// gradients well inside the accuracy of the 16-bit collocation rows.
 template <class T> constexpr int adv_pm() { return sizeof(T) == 2 ? PM_SPLIT2 : PM_F64; }
 // split-K partials of these product modes are fp64
 static bool pm_wide(int pm) { return pm == PM_SPLIT3 || pm == PM_F64; }
