@@ -18,7 +18,9 @@
  *  - Every pointer argument is a DEVICE pointer owned by the caller unless
  *    stated otherwise.  The library never allocates device memory, never frees
  *    caller memory and keeps no state between calls besides a thread-local
- *    error string (and, when enabled, the profiling record).
+ *    error string (and, when enabled, the profiling record).  The one
+ *    exception is pigan_train_step_grads_noalloc, which works in a fixed
+ *    device array of the library instead of a caller workspace.
  *  - `stream` is a hipStream_t (NULL = the default stream).  Calls enqueue work
  *    on it and return; outputs are valid after the caller synchronises it.
  *  - Argument checks run on the host before anything is enqueued; a non-OK
@@ -190,6 +192,30 @@ pigan_status pigan_train_step_grads(const pigan_step_desc* s, const float* pY, c
                                     float f_const, const float* real, const float* w_group,
                                     float* gY, float* gU, float* gD, float* loss,
                                     int32_t* nonfinite, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * pigan_train_step_grads_noalloc — for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same step, the same kernels and the same results as
+ * pigan_train_step_grads, with its workspace in a fixed array of the library
+ * (PIGAN_NOALLOC_SCRATCH_BYTES per device, held from the first call on a
+ * device until the process ends) instead of a caller buffer.  It allocates
+ * nothing itself.
+ *   Returns PIGAN_EWORKSPACE, and launches nothing, when the step needs more
+ *   than PIGAN_NOALLOC_SCRATCH_BYTES (pigan_workspace_bytes of the same
+ *   descriptor; a smaller chunk_S lowers it).  lambda_gp must be 0.
+ *   Every call on one device shares that device's array: calls whose work
+ *   overlaps on a device (other streams, other host threads) race; serialise
+ *   them.  The step initialises every workspace byte it reads, so no clearing
+ *   is needed between calls.
+ */
+#define PIGAN_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+pigan_status pigan_train_step_grads_noalloc(const pigan_step_desc* s, const float* pY, const float* pU,
+                                            const float* pD, const float* z, const float* xc,
+                                            const float* xsY, const float* xsU, const float* f,
+                                            float f_const, const float* real, const float* w_group,
+                                            float* gY, float* gU, float* gD, float* loss,
+                                            int32_t* nonfinite, void* stream);
 
 /*
  * pigan_train_step_grads plus the critic's gradient penalty, the member of the

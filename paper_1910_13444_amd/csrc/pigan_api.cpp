@@ -1584,6 +1584,56 @@ pigan_status pigan_train_step_grads(const pigan_step_desc* s, const float* pY, c
                           nullptr, nonfinite, ws, ws_bytes, stream, false);
 }
 
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// no-allocation entry point: the workspace is a file-scope device array.  In
+// host code `scratch` names a host-side stand-in, so its device address is
+// taken once per device with hipGetSymbolAddress (that device current) and
+// only that address is ever passed to kernels.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) char scratch[PIGAN_NOALLOC_SCRATCH_BYTES];
+static std::mutex g_scratch_m;
+static void* g_scratch_dev[64];
+
+static pigan_status scratch_address(void** out) {
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) return fail(PIGAN_EDEVICE, "device index %d out of range", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_m);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p || (uintptr_t)p % 256) return fail(PIGAN_EDEVICE, "scratch array address %p is not usable", p);
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return PIGAN_OK;
+}
+
+extern "C" {
+
+pigan_status pigan_train_step_grads_noalloc(const pigan_step_desc* s, const float* pY, const float* pU,
+                                            const float* pD, const float* z, const float* xc, const float* xsY,
+                                            const float* xsU, const float* f, float f_const, const float* real,
+                                            const float* w_group, float* gY, float* gU, float* gD, float* loss,
+                                            int32_t* nonfinite, void* stream) {
+  g_err.clear();
+  pigan_status st = check_step(s, false, "pigan_train_step_grads_noalloc");
+  if (st != PIGAN_OK) return st;
+  StepPlan pl;
+  plan_step(s, choose_chunk(s), pl);
+  if (pl.total > PIGAN_NOALLOC_SCRATCH_BYTES)
+    return fail(PIGAN_EWORKSPACE,
+                "the step needs %zu bytes of workspace; the no-allocation entry point holds %zu (set chunk_S lower "
+                "or use pigan_train_step_grads)",
+                pl.total, (size_t)PIGAN_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((st = scratch_address(&ws)) != PIGAN_OK) return st;
+  return train_step_entry(s, pY, pU, pD, z, xc, xsY, xsU, f, f_const, real, w_group, nullptr, gY, gU, gD, loss,
+                          nullptr, nonfinite, ws, pl.total, stream, false);
+}
+
 pigan_status pigan_train_step_grads_gp(const pigan_step_desc* s, const float* pY, const float* pU, const float* pD,
                                        const float* z, const float* xc, const float* xsY, const float* xsU,
                                        const float* f, float f_const, const float* real, const float* w_group,

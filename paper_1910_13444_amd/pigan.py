@@ -98,6 +98,7 @@ def lib():
         "pigan_workspace_bytes": (sz, [P]),
         "pigan_train_step_grads": (i32, [P, P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, sz, P]),
         "pigan_train_step_grads_gp": (i32, [P, P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, P, P, sz, P]),
+        "pigan_train_step_grads_noalloc": (i32, [P, P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P]),
         "pigan_adam_update": (i32, [i64, P, P, P, P, f32, f32, f32, f32, i32, P, P]),
         "pigan_hier_workspace_bytes": (sz, [P]),
         "pigan_hier_step_grads": (i32, [P, P, P, P, P, P, P, P, P, f32, P, P, P, P, P, P, P, P, P, P, P, sz, P]),
@@ -249,10 +250,13 @@ class StepOut:
 
 
 class TrainStep:
-    """Holds the workspace and output buffers of repeated training steps."""
+    """Holds the workspace and output buffers of repeated training steps.
+    noalloc=True calls pigan_train_step_grads_noalloc instead: no workspace
+    is allocated, the library's fixed device array serves as workspace."""
 
-    def __init__(self, desc: StepDesc, device="cuda"):
+    def __init__(self, desc: StepDesc, device="cuda", noalloc: bool = False):
         self.desc = desc
+        self.noalloc = noalloc
         self.device = torch.device(device)
         G = desc.genY.n_groups
         self.nY = n_params(desc.genY.in_dim, desc.genY.n_hidden, desc.genY.width)
@@ -262,7 +266,7 @@ class TrainStep:
         if need == 0:
             _check(lib().pigan_train_step_grads(C.byref(desc), *([None] * 8), 0.0, *([None] * 8), 0, None))
         self.ws_bytes = need
-        self.ws = _workspace(need, self.device)
+        self.ws = None if noalloc else _workspace(need, self.device)
         f32 = dict(dtype=torch.float32, device=self.device)
         self.out = StepOut(torch.empty((G, self.nY), **f32), torch.empty((G, self.nU), **f32),
                            torch.empty((G, self.nD), **f32), torch.empty((G, 3), **f32),
@@ -283,7 +287,10 @@ class TrainStep:
         outs = [_ptr(o.gY, "gY"), _ptr(o.gU, "gU"), _ptr(o.gD, "gD"), _ptr(o.loss, "loss")]
         tail = [_ptr(o.nonfinite, "nonfinite", 1, dtype=torch.int32), _ptr(self.ws, "ws", dtype=torch.uint8),
                 self.ws_bytes, _stream()]
-        if d.lambda_gp != 0.0:
+        if self.noalloc:
+            st = lib().pigan_train_step_grads_noalloc(*args, *outs, _ptr(o.nonfinite, "nonfinite", 1,
+                                                                         dtype=torch.int32), _stream())
+        elif d.lambda_gp != 0.0:
             eps = _ptr(gp_eps, "gp_eps", G * min(S, d.B_r))
             st = lib().pigan_train_step_grads_gp(*args, eps, *outs, _ptr(o.gp, "gp", G), *tail)
         else:
