@@ -69,6 +69,9 @@ typedef enum {
   PIGAN_BF16 = 1,        /* bf16 storage (round-to-nearest-even), fp32 accumulate */
   PIGAN_FP16 = 2         /* fp16 storage (round-to-nearest-even), fp32 accumulate */
 } pigan_dtype;
+/* Descriptor fields and arguments that carry a pigan_dtype are int32_t, so
+ * that any value a caller passes is well defined and rejected (EINVAL) when it
+ * is none of the above. */
 
 /* Shape of one tanh MLP: n_hidden tanh layers of `width` units on `in_dim`
  * inputs, then a linear scalar output.  `n_groups` independent copies
@@ -102,10 +105,10 @@ int64_t pigan_mlp_n_params(const pigan_mlp* net);
  *            256-byte aligned.
  */
 size_t pigan_gen_forward_workspace(const pigan_mlp* net, int32_t d, int32_t S, int32_t P,
-                                   int32_t order, pigan_dtype dt);
+                                   int32_t order, int32_t dt);
 pigan_status pigan_gen_forward(const pigan_mlp* net, const float* params, int32_t d,
                                const float* z, const float* x, int32_t x_shared,
-                               int32_t S, int32_t P, int32_t order, pigan_dtype dt,
+                               int32_t S, int32_t P, int32_t order, int32_t dt,
                                float* jet, void* ws, size_t ws_bytes, void* stream);
 
 /*
@@ -134,9 +137,9 @@ pigan_status pigan_pde_residual(int32_t d, int32_t G, int64_t M, const float* je
  *   snap  : [G, B, in_dim] fp32 snapshots.
  *   score : [G, B] fp32 output.
  */
-size_t pigan_disc_forward_workspace(const pigan_mlp* net, int32_t B, pigan_dtype dt);
+size_t pigan_disc_forward_workspace(const pigan_mlp* net, int32_t B, int32_t dt);
 pigan_status pigan_disc_forward(const pigan_mlp* net, const float* params, const float* snap,
-                                int32_t B, pigan_dtype dt, float* score, void* ws,
+                                int32_t B, int32_t dt, float* score, void* ws,
                                 size_t ws_bytes, void* stream);
 
 /*
@@ -164,7 +167,7 @@ typedef struct {
   int32_t n_sY, n_sU;          /* Y and u sensors per group (>= 1 each) */
   int32_t B_r;                 /* real snapshots per group */
   int32_t chunk_S;             /* samples per chunk, 0 = automatic */
-  pigan_dtype dt;
+  int32_t dt;            /* a pigan_dtype value */
   float lambda_pde;            /* weight of the residual penalty (>= 0) */
   float lambda_gp;             /* critic gradient-penalty weight (>= 0); must be 0 for
                                   pigan_train_step_grads (ENOTSUP otherwise), any value for
@@ -262,7 +265,7 @@ typedef struct {
                                   disc in_dim = n_sY + n_sU */
   int32_t d, n_z, S, P;        /* as pigan_step_desc */
   int32_t n_sY, n_sU, B_r, chunk_S;
-  pigan_dtype dt;
+  int32_t dt;            /* a pigan_dtype value */
   float lambda_pde;            /* weight of the residual penalty (>= 0) */
   float loss_scale;            /* static loss scale (> 0; 1 unless fp16) */
   float lambda_gp;             /* critic gradient penalty weight: 0 for pigan_trunk_step_grads,
@@ -331,7 +334,7 @@ typedef struct {
   int32_t d, n_z, S, P;
   int32_t n_sY, n_sU, B_r, chunk_S;
   int32_t mY, mU, nF;          /* inputs of every critic: Y sensors, u sensors, free sensors */
-  pigan_dtype dt;
+  int32_t dt;            /* a pigan_dtype value */
   float lambda_pde;            /* >= 0 */
   float loss_scale;            /* > 0 */
   float lambda_gp;             /* critic gradient penalty weight: 0 for pigan_hier_step_grads,
@@ -401,7 +404,7 @@ typedef struct {
   int32_t d, n_z, S, P;
   int32_t n_sY, n_sU, B_r, chunk_S;
   int32_t mY, mU, nF;
-  pigan_dtype dt;
+  int32_t dt;            /* a pigan_dtype value */
   float lambda_pde;            /* >= 0 */
   float loss_scale;            /* > 0 */
   float lambda_gp;             /* critic gradient penalty weight: 0 for

@@ -99,7 +99,7 @@ struct Carver {
   }
 };
 
-static size_t esize(pigan_dtype dt) { return dt == PIGAN_FP32 ? 4 : 2; }
+static size_t esize(int32_t dt) { return dt == PIGAN_FP32 ? 4 : 2; }
 
 struct MlpOff {  // offsets (in floats) of one group's packed parameters
   int in_dim, L, W;
@@ -146,7 +146,7 @@ static pigan_status check_mlp(const pigan_mlp* m, const char* what) {
   return PIGAN_OK;
 }
 
-static pigan_status check_dtype(pigan_dtype dt) {
+static pigan_status check_dtype(int32_t dt) {
   if (dt != PIGAN_FP32 && dt != PIGAN_BF16 && dt != PIGAN_FP16) return fail(PIGAN_EINVAL, "unknown dtype %d", (int)dt);
   return PIGAN_OK;
 }
@@ -1653,7 +1653,7 @@ struct GenFwdPlan {
   int64_t R;
 };
 
-static GenFwdPlan plan_gen_fwd(const pigan_mlp* net, int d, int S, int P, int order, pigan_dtype dt) {
+static GenFwdPlan plan_gen_fwd(const pigan_mlp* net, int d, int S, int P, int order, int32_t dt) {
   GenFwdPlan p{};
   Carver cv;
   const int G = net->n_groups, W = net->width, L = net->n_hidden;
@@ -1668,7 +1668,7 @@ static GenFwdPlan plan_gen_fwd(const pigan_mlp* net, int d, int S, int P, int or
   return p;
 }
 
-static pigan_status check_gen_fwd(const pigan_mlp* net, int d, int S, int P, int order, pigan_dtype dt) {
+static pigan_status check_gen_fwd(const pigan_mlp* net, int d, int S, int P, int order, int32_t dt) {
   pigan_status st = check_mlp(net, "generator");
   if (st != PIGAN_OK) return st;
   if ((st = check_dtype(dt)) != PIGAN_OK) return st;
@@ -1682,7 +1682,7 @@ static pigan_status check_gen_fwd(const pigan_mlp* net, int d, int S, int P, int
 extern "C" {
 
 size_t pigan_gen_forward_workspace(const pigan_mlp* net, int32_t d, int32_t S, int32_t P, int32_t order,
-                                   pigan_dtype dt) {
+                                   int32_t dt) {
   if (check_gen_fwd(net, d, S, P, order, dt) != PIGAN_OK) return 0;
   return plan_gen_fwd(net, d, S, P, order, dt).total;
 }
@@ -1758,7 +1758,7 @@ static pigan_status run_gen_fwd(const pigan_mlp* net, const float* params, int d
 extern "C" {
 
 pigan_status pigan_gen_forward(const pigan_mlp* net, const float* params, int32_t d, const float* z, const float* x,
-                               int32_t x_shared, int32_t S, int32_t P, int32_t order, pigan_dtype dt, float* jet,
+                               int32_t x_shared, int32_t S, int32_t P, int32_t order, int32_t dt, float* jet,
                                void* ws, size_t ws_bytes, void* stream) {
   g_err.clear();
   pigan_status st = check_gen_fwd(net, d, S, P, order, dt);
@@ -1810,7 +1810,7 @@ struct DiscFwdPlan {
 };
 
 // the critic runs in fp32 storage in every mode (split products)
-static DiscFwdPlan plan_disc_fwd(const pigan_mlp* net, int B, pigan_dtype dt) {
+static DiscFwdPlan plan_disc_fwd(const pigan_mlp* net, int B, int32_t dt) {
   DiscFwdPlan p{};
   Carver cv;
   const int G = net->n_groups, W = net->width, L = net->n_hidden;
@@ -1828,7 +1828,7 @@ static DiscFwdPlan plan_disc_fwd(const pigan_mlp* net, int B, pigan_dtype dt) {
 
 extern "C" {
 
-size_t pigan_disc_forward_workspace(const pigan_mlp* net, int32_t B, pigan_dtype dt) {
+size_t pigan_disc_forward_workspace(const pigan_mlp* net, int32_t B, int32_t dt) {
   if (check_mlp(net, "disc") != PIGAN_OK || check_dtype(dt) != PIGAN_OK || B < 1) return 0;
   return plan_disc_fwd(net, B, dt).total;
 }
@@ -1882,7 +1882,7 @@ static pigan_status run_disc_fwd(const pigan_mlp* net, const float* params, cons
 extern "C" {
 
 pigan_status pigan_disc_forward(const pigan_mlp* net, const float* params, const float* snap, int32_t B,
-                                pigan_dtype dt, float* score, void* ws, size_t ws_bytes, void* stream) {
+                                int32_t dt, float* score, void* ws, size_t ws_bytes, void* stream) {
   g_err.clear();
   pigan_status st = check_mlp(net, "disc");
   if (st != PIGAN_OK) return st;

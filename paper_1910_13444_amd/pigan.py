@@ -18,7 +18,9 @@ import torch
 from .configs import Workload, n_params
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libpigan.so")
+# PIGAN_LIBRARY selects another build of the same sources (the host-sanitized
+# one of the CPU argument-check tests)
+LIB_PATH = os.environ.get("PIGAN_LIBRARY") or os.path.join(_HERE, "libpigan.so")
 HEADER = os.path.join(os.path.dirname(_HERE), "include", "pigan.h")
 
 OK, EINVAL, ENOTSUP, EWORKSPACE, EDEVICE = 0, 1, 2, 3, 4
