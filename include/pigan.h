@@ -167,12 +167,16 @@ typedef struct {
   int32_t n_sY, n_sU;          /* Y and u sensors per group (>= 1 each) */
   int32_t B_r;                 /* real snapshots per group */
   int32_t chunk_S;             /* samples per chunk, 0 = automatic */
-  int32_t dt;            /* a pigan_dtype value */
+  int32_t dt;                  /* a pigan_dtype value */
   float lambda_pde;            /* weight of the residual penalty (>= 0) */
   float lambda_gp;             /* critic gradient-penalty weight (>= 0); must be 0 for
                                   pigan_train_step_grads (ENOTSUP otherwise), any value for
                                   pigan_train_step_grads_gp */
   float loss_scale;            /* static loss scale (> 0; 1 unless fp16) */
+  int32_t critic_only;         /* 0: every gradient; 1: the critic's update only -- gD and the
+                                  losses as in the full step, the generators' reverse pass
+                                  skipped and their gradient outputs neither written nor
+                                  required (may be NULL) */
 } pigan_step_desc;
 
 size_t pigan_workspace_bytes(const pigan_step_desc* s);
@@ -265,11 +269,15 @@ typedef struct {
                                   disc in_dim = n_sY + n_sU */
   int32_t d, n_z, S, P;        /* as pigan_step_desc */
   int32_t n_sY, n_sU, B_r, chunk_S;
-  int32_t dt;            /* a pigan_dtype value */
+  int32_t dt;                  /* a pigan_dtype value */
   float lambda_pde;            /* weight of the residual penalty (>= 0) */
   float loss_scale;            /* static loss scale (> 0; 1 unless fp16) */
   float lambda_gp;             /* critic gradient penalty weight: 0 for pigan_trunk_step_grads,
                                   >= 0 for pigan_trunk_step_grads_gp */
+  int32_t critic_only;         /* 0: every gradient; 1: the critic's update only -- gD and the
+                                  losses as in the full step, the generators' reverse pass
+                                  skipped and their gradient outputs neither written nor
+                                  required (may be NULL) */
 } pigan_trunk_desc;
 
 /* Workspace bytes for pigan_trunk_step_grads(_gp) (0 if the descriptor is invalid;
@@ -334,11 +342,15 @@ typedef struct {
   int32_t d, n_z, S, P;
   int32_t n_sY, n_sU, B_r, chunk_S;
   int32_t mY, mU, nF;          /* inputs of every critic: Y sensors, u sensors, free sensors */
-  int32_t dt;            /* a pigan_dtype value */
+  int32_t dt;                  /* a pigan_dtype value */
   float lambda_pde;            /* >= 0 */
   float loss_scale;            /* > 0 */
   float lambda_gp;             /* critic gradient penalty weight: 0 for pigan_hier_step_grads,
                                   >= 0 for pigan_hier_step_grads_gp */
+  int32_t critic_only;         /* 0: every gradient; 1: the critic's update only -- gD and the
+                                  losses as in the full step, the generators' reverse pass
+                                  skipped and their gradient outputs neither written nor
+                                  required (may be NULL) */
 } pigan_hier_desc;
 
 /* Workspace bytes for pigan_hier_step_grads(_gp) (0 if the descriptor is invalid;
@@ -404,11 +416,15 @@ typedef struct {
   int32_t d, n_z, S, P;
   int32_t n_sY, n_sU, B_r, chunk_S;
   int32_t mY, mU, nF;
-  int32_t dt;            /* a pigan_dtype value */
+  int32_t dt;                  /* a pigan_dtype value */
   float lambda_pde;            /* >= 0 */
   float loss_scale;            /* > 0 */
   float lambda_gp;             /* critic gradient penalty weight: 0 for
                                   pigan_hier_trunk_step_grads, >= 0 for its _gp form */
+  int32_t critic_only;         /* 0: every gradient; 1: the critic's update only -- gD and the
+                                  losses as in the full step, the generators' reverse pass
+                                  skipped and their gradient outputs neither written nor
+                                  required (may be NULL) */
 } pigan_hier_trunk_desc;
 
 /* Workspace bytes for pigan_hier_trunk_step_grads(_gp) (0 if the descriptor is

@@ -467,6 +467,8 @@ static pigan_status check_step(const pigan_step_desc* s, bool gp_entry = false,
     return fail(PIGAN_ENOTSUP, "lambda_gp != 0 needs the per-pair mixing weights: use %s", gp_name);
   if (!(s->loss_scale > 0.0f) || !__builtin_isfinite(s->loss_scale))
     return fail(PIGAN_EINVAL, "loss_scale must be finite and > 0");
+  if (s->critic_only != 0 && s->critic_only != 1)
+    return fail(PIGAN_EINVAL, "critic_only=%d must be 0 or 1", s->critic_only);
   return PIGAN_OK;
 }
 
@@ -1075,7 +1077,7 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
     if ((r = disc_pass(ws, pl, pD, WD, LD, n_in, B, Sc, n_real, S, s->B_r, w_group, ls, inv, accum, gD, nonfinite,
                        acc, G, st, &cur, pm)) != PIGAN_OK)
       return r;
-    {
+    if (!s->critic_only) {
       // d(L_adv)/dF = -dL_D/dF for the fake rows -> generator sensor cotangents
       NtArgs<float> a{};
       a.X = tp<float>(ws, D.dA[cur]); a.x_g = dact; a.ldx = WD;
@@ -1103,7 +1105,8 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
           return r;
       }
     }
-    // generator reverse passes
+    // generator reverse passes (not in a critic-only step)
+    if (s->critic_only) continue;
     if ((r = gen_chunk_bwd<T>(ws, pl, Yc, pY, xsG, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, gY, accum, inv, nonfinite,
                               G, st)) != PIGAN_OK)
       return r;
@@ -1205,7 +1208,7 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
     if ((r = disc_pass(ws, pl, pD, WD, LD, n_in, B, Sc, n_real, S, s->B_r, w_disc, ls, inv, accum, gD, nonfinite,
                        acc, GD, st, &cur, pm)) != PIGAN_OK)
       return r;
-    {
+    if (!s->critic_only) {
       // -dL_D/dX of every critic's fake rows (all inputs), then added to the
       // generator outputs they were read from
       const int64_t dact = D.Bmax * WD;
@@ -1232,6 +1235,7 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
           return r;
       }
     }
+    if (s->critic_only) continue;   // no generator reverse pass
     {
       // jet cotangents from the penalty and the critics' source cotangents
       ProfScope ps(st, "residual", 0.0, (double)M * (3 * d + 2) * 4.0 * 2);
@@ -1291,7 +1295,9 @@ static pigan_status train_step_entry(const pigan_step_desc* s, const float* pY, 
   g_err.clear();
   pigan_status st = check_step(s, gp_entry);
   if (st != PIGAN_OK) return st;
-  if (!pY || !pU || !pD || !z || !xc || !xsY || !xsU || !real || !gY || !gU || !gD || !loss || !nonfinite)
+  const bool gen_out = !s->critic_only;   // the generators' gradients are outputs
+  if (!pY || !pU || !pD || !z || !xc || !xsY || !xsU || !real || (gen_out && (!gY || !gU)) || !gD || !loss ||
+      !nonfinite)
     return fail(PIGAN_EINVAL, "null input or output pointer");
   if (s->lambda_gp > 0.0f && !gp_eps) return fail(PIGAN_EINVAL, "lambda_gp > 0 needs gp_eps");
   if (!__builtin_isfinite(f_const)) return fail(PIGAN_EINVAL, "f_const must be finite");
@@ -1347,11 +1353,13 @@ static pigan_status check_hier(const pigan_hier_desc* h, pigan_step_desc* out, b
     return fail(PIGAN_EINVAL, "lambda_gp must be finite and >= 0");
   if (!gp_entry && h->lambda_gp != 0.0f)
     return fail(PIGAN_ENOTSUP, "lambda_gp != 0 needs the per-pair mixing weights: use %s", gp_name);
+  if (h->critic_only != 0 && h->critic_only != 1)
+    return fail(PIGAN_EINVAL, "critic_only=%d must be 0 or 1", h->critic_only);
   pigan_step_desc s{};
   s.genY = h->genY; s.genU = h->genU; s.disc = h->disc;
   s.d = h->d; s.n_z = h->n_z; s.S = h->S; s.P = h->P; s.n_sY = h->n_sY; s.n_sU = h->n_sU; s.B_r = h->B_r;
   s.chunk_S = h->chunk_S; s.dt = h->dt; s.lambda_pde = h->lambda_pde; s.lambda_gp = h->lambda_gp;
-  s.loss_scale = h->loss_scale;
+  s.loss_scale = h->loss_scale; s.critic_only = h->critic_only;
   *out = s;
   return PIGAN_OK;
 }
@@ -1363,7 +1371,7 @@ static pigan_step_desc trunk_as_step(const pigan_trunk_desc* t) {
   s.genY = t->trunk; s.genU = t->trunk; s.disc = t->disc;
   s.d = t->d; s.n_z = t->n_z; s.S = t->S; s.P = t->P; s.n_sY = t->n_sY; s.n_sU = t->n_sU; s.B_r = t->B_r;
   s.chunk_S = t->chunk_S; s.dt = t->dt; s.lambda_pde = t->lambda_pde; s.lambda_gp = t->lambda_gp;
-  s.loss_scale = t->loss_scale;
+  s.loss_scale = t->loss_scale; s.critic_only = t->critic_only;
   return s;
 }
 
@@ -1374,7 +1382,7 @@ static pigan_hier_desc hier_trunk_as_hier(const pigan_hier_trunk_desc* t) {
   h.genY = t->trunk; h.genU = t->trunk; h.disc = t->disc;
   h.d = t->d; h.n_z = t->n_z; h.S = t->S; h.P = t->P; h.n_sY = t->n_sY; h.n_sU = t->n_sU; h.B_r = t->B_r;
   h.chunk_S = t->chunk_S; h.mY = t->mY; h.mU = t->mU; h.nF = t->nF; h.dt = t->dt; h.lambda_pde = t->lambda_pde;
-  h.loss_scale = t->loss_scale; h.lambda_gp = t->lambda_gp;
+  h.loss_scale = t->loss_scale; h.lambda_gp = t->lambda_gp; h.critic_only = t->critic_only;
   return h;
 }
 
@@ -1391,8 +1399,9 @@ static pigan_status hier_entry(const pigan_hier_desc* h, bool trunk, bool gp_ent
   pigan_step_desc s;
   pigan_status st = check_hier(h, &s, gp_entry, gp_name);
   if (st != PIGAN_OK) return st;
-  if (!pY || (!trunk && (!pU || !gU)) || !pD || !z || !xc || !xsY || !xsU || !real || !w_disc || !gY || !gD ||
-      !loss || !nonfinite)
+  const bool gen_out = !s.critic_only;   // the generators' gradients are outputs
+  if (!pY || (!trunk && (!pU || (gen_out && !gU))) || !pD || !z || !xc || !xsY || !xsU || !real || !w_disc ||
+      (gen_out && !gY) || !gD || !loss || !nonfinite)
     return fail(PIGAN_EINVAL, "null input or output pointer");
   if ((h->mY > 0 && !idxY) || (h->mU > 0 && !idxU) || (h->nF > 0 && !idxF))
     return fail(PIGAN_EINVAL, "null sensor index list");
@@ -1535,7 +1544,7 @@ static pigan_status trunk_step_entry(const pigan_trunk_desc* t, const float* pT,
   const pigan_step_desc s = trunk_as_step(t);
   pigan_status st = check_step(&s, gp_entry, "pigan_trunk_step_grads_gp");
   if (st != PIGAN_OK) return st;
-  if (!pT || !pD || !z || !xc || !xsY || !xsU || !real || !gT || !gD || !loss || !nonfinite)
+  if (!pT || !pD || !z || !xc || !xsY || !xsU || !real || (!s.critic_only && !gT) || !gD || !loss || !nonfinite)
     return fail(PIGAN_EINVAL, "null input or output pointer");
   if (s.lambda_gp > 0.0f && !gp_eps) return fail(PIGAN_EINVAL, "lambda_gp > 0 needs gp_eps");
   if (!__builtin_isfinite(f_const)) return fail(PIGAN_EINVAL, "f_const must be finite");

@@ -43,7 +43,7 @@ class StepDesc(C.Structure):
                 ("d", C.c_int32), ("n_z", C.c_int32), ("S", C.c_int32), ("P", C.c_int32),
                 ("n_sY", C.c_int32), ("n_sU", C.c_int32), ("B_r", C.c_int32), ("chunk_S", C.c_int32),
                 ("dt", C.c_int32), ("lambda_pde", C.c_float), ("lambda_gp", C.c_float),
-                ("loss_scale", C.c_float)]
+                ("loss_scale", C.c_float), ("critic_only", C.c_int32)]
 
 
 class TrunkDesc(C.Structure):
@@ -51,7 +51,7 @@ class TrunkDesc(C.Structure):
                 ("d", C.c_int32), ("n_z", C.c_int32), ("S", C.c_int32), ("P", C.c_int32),
                 ("n_sY", C.c_int32), ("n_sU", C.c_int32), ("B_r", C.c_int32), ("chunk_S", C.c_int32),
                 ("dt", C.c_int32), ("lambda_pde", C.c_float), ("loss_scale", C.c_float),
-                ("lambda_gp", C.c_float)]
+                ("lambda_gp", C.c_float), ("critic_only", C.c_int32)]
 
 
 class HierDesc(C.Structure):
@@ -60,7 +60,7 @@ class HierDesc(C.Structure):
                 ("n_sY", C.c_int32), ("n_sU", C.c_int32), ("B_r", C.c_int32), ("chunk_S", C.c_int32),
                 ("mY", C.c_int32), ("mU", C.c_int32), ("nF", C.c_int32),
                 ("dt", C.c_int32), ("lambda_pde", C.c_float), ("loss_scale", C.c_float),
-                ("lambda_gp", C.c_float)]
+                ("lambda_gp", C.c_float), ("critic_only", C.c_int32)]
 
 
 class HierTrunkDesc(C.Structure):
@@ -69,7 +69,7 @@ class HierTrunkDesc(C.Structure):
                 ("n_sY", C.c_int32), ("n_sU", C.c_int32), ("B_r", C.c_int32), ("chunk_S", C.c_int32),
                 ("mY", C.c_int32), ("mU", C.c_int32), ("nF", C.c_int32),
                 ("dt", C.c_int32), ("lambda_pde", C.c_float), ("loss_scale", C.c_float),
-                ("lambda_gp", C.c_float)]
+                ("lambda_gp", C.c_float), ("critic_only", C.c_int32)]
 
 
 class KernelStat(C.Structure):

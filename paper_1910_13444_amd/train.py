@@ -164,9 +164,12 @@ class Trainer:
             return self.gp_eps_fn(self.calls)
         return torch.rand(self.gp_shape, generator=self.gp_gen, device=self.pD.device, dtype=torch.float32)
 
-    def _call(self, gen, pD):
+    def _call(self, gen, pD, critic_only=False):
+        """One step call; critic_only skips the generators' reverse pass (their
+        gradients are then not computed: grads_g holds stale buffers)."""
         if self.scaler is not None:
             self.desc.loss_scale = self.scaler.scale
+        self.desc.critic_only = int(critic_only)
         i = self.inp
         eps = self._gp_eps()
         self.calls += 1
@@ -207,7 +210,7 @@ class Trainer:
         cfg = self.cfg
         if cfg.schedule == "sequential":
             for _ in range(cfg.n_critic):
-                o, _, sk = self._call(self.gen, self.pD)
+                o, _, sk = self._call(self.gen, self.pD, critic_only=True)
                 self._update_d(o.gD, o.nonfinite, sk)
             o, grads_g, sk = self._call(self.gen, self.pD)
             self._update_g(grads_g, o.nonfinite, sk)
@@ -215,7 +218,7 @@ class Trainer:
             for _ in range(cfg.steps_per_exchange):
                 o, grads_g, sk = self._call(self.gen, self.pD_copy)
                 self._update_g(grads_g, o.nonfinite, sk)
-                o, _, sk = self._call(self.gen_copy, self.pD)
+                o, _, sk = self._call(self.gen_copy, self.pD, critic_only=True)
                 self._update_d(o.gD, o.nonfinite, sk)
             for c, g in zip(self.gen_copy, self.gen):
                 c.copy_(g)

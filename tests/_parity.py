@@ -69,7 +69,7 @@ def to_dev(a, dev="cuda"):
 
 
 def run_step_gpu(wl, inp, real, chunk_S=0, dtype=None, loss_scale=1.0, lambda_pde=None, lambda_gp=0.0,
-                 gp_eps=None):
+                 gp_eps=None, critic_only=False):
     """One training step through pigan_train_step_grads (or, with lambda_gp,
     pigan_train_step_grads_gp); returns numpy outputs."""
     import torch
@@ -77,6 +77,7 @@ def run_step_gpu(wl, inp, real, chunk_S=0, dtype=None, loss_scale=1.0, lambda_pd
     S = inp.z.shape[1]
     desc = pigan.step_desc(wl, S=S, B_r=real.shape[1], chunk_S=chunk_S, dtype=dtype, loss_scale=loss_scale,
                            lambda_pde=lambda_pde, lambda_gp=lambda_gp)
+    desc.critic_only = int(critic_only)
     step = pigan.TrainStep(desc)
     o = step(to_dev(inp.pY), to_dev(inp.pU), to_dev(inp.pD), to_dev(inp.z), to_dev(inp.xc), to_dev(inp.xsY),
              to_dev(inp.xsU), to_dev(real), f=None if inp.f is None else to_dev(inp.f), f_const=inp.f_const,
@@ -110,13 +111,15 @@ def trunk_slices(in_dim, L, W):
     return out
 
 
-def run_trunk_gpu(wl, inp, real, chunk_S=0, dtype=None, loss_scale=1.0, lambda_gp=0.0, gp_eps=None):
+def run_trunk_gpu(wl, inp, real, chunk_S=0, dtype=None, loss_scale=1.0, lambda_gp=0.0, gp_eps=None,
+                  critic_only=False):
     """One training step through pigan_trunk_step_grads (or, with lambda_gp >
     0, pigan_trunk_step_grads_gp); returns numpy outputs."""
     import torch
     from paper_1910_13444_amd import pigan
     desc = pigan.trunk_desc(wl, S=inp.z.shape[1], B_r=real.shape[1], chunk_S=chunk_S, dtype=dtype,
                             loss_scale=loss_scale, lambda_gp=lambda_gp)
+    desc.critic_only = int(critic_only)
     step = pigan.TrunkStep(desc)
     o = step(to_dev(inp.pT), to_dev(inp.pD), to_dev(inp.z), to_dev(inp.xc), to_dev(inp.xsY), to_dev(inp.xsU),
              to_dev(real), f=None if inp.f is None else to_dev(inp.f), f_const=inp.f_const,
@@ -143,7 +146,7 @@ def trunk_errors(wl, out, ref, metric=rel):
 
 
 def run_hier_gpu(wl, hi, real, lam=0.0, chunk_S=0, dtype=None, idx=None, f=None, f_const=0.0, lambda_gp=0.0,
-                 gp_eps=None):
+                 gp_eps=None, critic_only=False):
     """One domain-decomposition step through pigan_hier_step_grads (or, with
     lambda_gp > 0, pigan_hier_step_grads_gp: then the result has P_gp)."""
     import torch
@@ -152,6 +155,7 @@ def run_hier_gpu(wl, hi, real, lam=0.0, chunk_S=0, dtype=None, idx=None, f=None,
     iY, iU, iF = idx if idx is not None else (h.idxY, h.idxU, h.idxF)
     desc = pigan.hier_desc(wl, h.D, iY.shape[1], iU.shape[1], iF.shape[1], S=b.z.shape[1], B_r=real.shape[1],
                            chunk_S=chunk_S, dtype=dtype, lambda_pde=lam, lambda_gp=lambda_gp)
+    desc.critic_only = int(critic_only)
     step = pigan.HierStep(desc)
 
     def ti(a):
@@ -167,7 +171,8 @@ def run_hier_gpu(wl, hi, real, lam=0.0, chunk_S=0, dtype=None, idx=None, f=None,
     return out
 
 
-def run_hier_trunk_gpu(wl, hi, real, lam=0.0, chunk_S=0, dtype=None, f_const=0.0, lambda_gp=0.0, gp_eps=None):
+def run_hier_trunk_gpu(wl, hi, real, lam=0.0, chunk_S=0, dtype=None, f_const=0.0, lambda_gp=0.0, gp_eps=None,
+                       critic_only=False):
     """One domain-decomposition step with the shared trunk
     (pigan_hier_trunk_step_grads, or its _gp form when lambda_gp > 0)."""
     import torch
@@ -176,6 +181,7 @@ def run_hier_trunk_gpu(wl, hi, real, lam=0.0, chunk_S=0, dtype=None, f_const=0.0
     desc = pigan.hier_trunk_desc(wl, h.D, h.idxY.shape[1], h.idxU.shape[1], h.idxF.shape[1], S=b.z.shape[1],
                                  B_r=real.shape[1], chunk_S=chunk_S, dtype=dtype, lambda_pde=lam,
                                  lambda_gp=lambda_gp)
+    desc.critic_only = int(critic_only)
     step = pigan.HierTrunkStep(desc)
 
     def ti(a):

@@ -40,7 +40,7 @@ def _step(desc, ws_bytes, ptr=FAKE, f=None, wg=None):
     ("d", 0, pigan.EINVAL), ("d", 4, pigan.EINVAL), ("n_z", 0, pigan.EINVAL), ("S", 0, pigan.EINVAL),
     ("P", -1, pigan.EINVAL), ("n_sY", 0, pigan.EINVAL), ("B_r", 0, pigan.EINVAL), ("chunk_S", -2, pigan.EINVAL),
     ("lambda_gp", -0.5, pigan.EINVAL), ("loss_scale", 0.0, pigan.EINVAL), ("lambda_pde", -1.0, pigan.EINVAL),
-    ("dt", 7, pigan.EINVAL),
+    ("dt", 7, pigan.EINVAL), ("critic_only", 2, pigan.EINVAL), ("critic_only", -1, pigan.EINVAL),
 ])
 def test_step_rejects_bad_descriptor(field, value, status):
     d = pigan.step_desc(configs.C1)
@@ -154,7 +154,8 @@ def _trunk_step(desc, ws_bytes, ptr=FAKE, ws=FAKE):
 
 
 @pytest.mark.parametrize("field,value", [("d", 0), ("n_z", 0), ("S", 0), ("P", 0), ("n_sU", 0), ("B_r", 0),
-                                         ("chunk_S", -1), ("loss_scale", -1.0), ("lambda_pde", -2.0), ("dt", 9)])
+                                         ("chunk_S", -1), ("loss_scale", -1.0), ("lambda_pde", -2.0), ("dt", 9),
+                                         ("critic_only", 3)])
 def test_trunk_step_rejects_bad_descriptor(field, value):
     d = pigan.trunk_desc(configs.T5)
     setattr(d, field, value)
@@ -207,7 +208,7 @@ def test_hier_step_validation():
     assert _hier(d, need, idx=None) == pigan.EINVAL
     assert _hier(d, need - 1) == pigan.EWORKSPACE
     assert _hier(d, need, ws=C.c_void_p(4096 + 32)) == pigan.EINVAL
-    for field, value in (("mY", -1), ("nF", -3), ("B_r", 0), ("lambda_pde", -1.0), ("d", 5)):
+    for field, value in (("mY", -1), ("nF", -3), ("B_r", 0), ("lambda_pde", -1.0), ("d", 5), ("critic_only", 2)):
         e = pigan.hier_desc(wl, 21, 16, 16, 16)
         setattr(e, field, value)
         assert _hier(e, 1 << 40) == pigan.EINVAL, field
@@ -293,3 +294,18 @@ def test_hier_gradient_penalty_validation():
             e = mk(wl, 21, 16, 16, 16, lambda_gp=bad)
             assert int(ws_fn(C.byref(e))) == 0
             assert gp_fn(C.byref(e), *head[1:], FAKE, *outs, FAKE, FAKE, FAKE, 1 << 40, None) == pigan.EINVAL
+
+
+def test_critic_only_step_needs_no_generator_gradients():
+    """critic_only = 1: the generators' gradient outputs may be NULL; the
+    full step still requires them."""
+    L = pigan.lib()
+    d = pigan.step_desc(configs.C1)
+    need = pigan.workspace_bytes(d)
+
+    def call(desc, gY):
+        return L.pigan_train_step_grads(C.byref(desc), *([FAKE] * 7), None, 0.0, FAKE, None, gY, gY, FAKE, FAKE,
+                                        FAKE, FAKE, need - 1, None)
+    assert call(d, None) == pigan.EINVAL
+    d.critic_only = 1
+    assert call(d, None) == pigan.EWORKSPACE       # past the pointer checks; stops at the workspace size
