@@ -103,29 +103,26 @@ __device__ __forceinline__ void mma_split(f32x16& acc, const bf16x8 (&b)[NP], co
 // ---------------------------------------------------------------------------
 // tanh and its derivatives with respect to the pre-activation a:
 //   t = tanh(a), s = dt/da = 1 - t^2, s' = -2 t s, s'' = 2 s (3 t^2 - 1).
-// With e = exp(-2|a|) and m = e - 1 (= expm1(-2|a|)):
-//   |t| = -m / (2 + m),  s = 4 e / (1 + e)^2.
+// With e = exp(-2|a|):  |t| = (1 - e) / (1 + e),  s = 4 e / (1 + e)^2.
 // s is formed from e directly, so it keeps full relative accuracy for
-// saturated units where 1 - t^2 would cancel; for |a| < 1/8 the factor m is
-// taken from its Taylor series (8 terms, truncation below 1e-9 relative) so
-// that t keeps full relative accuracy near zero.
+// saturated units where 1 - t^2 would cancel.  e comes from the hardware
+// base-2 exponential (about 1e-6 relative for |a| <= 10, the rounding of the
+// scaled argument included).  For |a| < 1/8, where 1 - e would cancel, t is
+// the odd Taylor series a - a^3/3 + 2a^5/15 - 17a^7/315 + 62a^9/2835
+// (truncation below 2e-10 relative there).
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void tanh_ts(float a, float& t, float& s) {
-  const float x = -2.0f * fabsf(a);
-  const float e = expf(x);
-  // expm1(x) = x (1 + x/2 (1 + x/3 (1 + x/4 (... (1 + x/8)))))
-  float p = 1.0f + x * (1.0f / 8.0f);
-  p = 1.0f + x * (1.0f / 7.0f) * p;
-  p = 1.0f + x * (1.0f / 6.0f) * p;
-  p = 1.0f + x * (1.0f / 5.0f) * p;
-  p = 1.0f + x * (1.0f / 4.0f) * p;
-  p = 1.0f + x * (1.0f / 3.0f) * p;
-  p = 1.0f + x * 0.5f * p;
-  const float m = (x > -0.25f) ? x * p : e - 1.0f;
-  const float ta = -m * __builtin_amdgcn_rcpf(2.0f + m);
-  t = copysignf(ta, a);
-  const float den = 1.0f + e;
-  s = 4.0f * e * __builtin_amdgcn_rcpf(den * den);
+  const float ax = fabsf(a);
+  const float e = __builtin_amdgcn_exp2f(ax * -2.8853900817779268f);   // -2 / ln 2
+  const float r = __builtin_amdgcn_rcpf(1.0f + e);
+  const float a2 = a * a;
+  float q = 62.0f / 2835.0f;
+  q = q * a2 - 17.0f / 315.0f;
+  q = q * a2 + 2.0f / 15.0f;
+  q = q * a2 - 1.0f / 3.0f;
+  const float small = a + (a * a2) * q;
+  t = ax < 0.125f ? small : copysignf((1.0f - e) * r, a);
+  s = (4.0f * e) * (r * r);
 }
 
 // The same quantities evaluated in fp64 and rounded once (fp32-mode kernels:

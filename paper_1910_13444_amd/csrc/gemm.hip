@@ -238,12 +238,31 @@ k_gemm_nt(const NtArgs<T> p) {
     for (int i = 0; i < PPT; ++i)
       buf[i] = valid[i] ? *(const uint4*)(src[i] + (int64_t)(isx[i] ? ktx : kt) * 64) : make_uint4(0u, 0u, 0u, 0u);
   };
+  // PM_SPLIT2: each fp32 value is cut into its two bf16 pieces once, as the
+  // stage is stored: a 64-byte stage row (16 k) then holds the high pieces
+  // in segments 0-1 and the low pieces in segments 2-3, i.e. the layout of a
+  // 16-bit stage whose first 16-wide chunk is the high part and second the
+  // low part
   auto lstore = [&](const uint4* buf, int stage) {
     char* base = lds + stage * STAGE;
 #pragma unroll
     for (int i = 0; i < PPT; ++i) {
       const int piece = tid + i * NTH;
-      if (piece < PIECES) *(uint4*)(base + lds_seg(piece >> 2, piece & 3)) = buf[i];
+      if (piece >= PIECES) continue;
+      const int row = piece >> 2, sg = piece & 3;
+      if constexpr (PM == PM_SPLIT2) {
+        const float* v = (const float*)&buf[i];
+        bf16 hi[4], lo[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          hi[e] = (bf16)v[e];
+          lo[e] = (bf16)(v[e] - (float)hi[e]);
+        }
+        *(uint2*)(base + lds_seg(row, sg >> 1) + (sg & 1) * 8) = __builtin_bit_cast(uint2, hi);
+        *(uint2*)(base + lds_seg(row, 2 + (sg >> 1)) + (sg & 1) * 8) = __builtin_bit_cast(uint2, lo);
+      } else {
+        *(uint4*)(base + lds_seg(row, sg)) = buf[i];
+      }
     }
   };
   // a fragment: 8 consecutive k of one row (16 bytes in 16-bit types, two
@@ -263,11 +282,33 @@ k_gemm_nt(const NtArgs<T> p) {
       return __builtin_bit_cast(frag, w);
     }
   };
+  // the high (c = 0) or low (c = 1) bf16 pieces of a PM_SPLIT2 fragment
+  auto piece_at = [&](const char* base, int row, int c) {
+    return *(const bf16x8*)(base + row * LDS_PITCH + (((2 * c + (lane >> 5)) ^ gsw) << 4));
+  };
   auto compute = [&](int stage) {
     const char* base = lds + stage * STAGE;
+    if constexpr (PM == PM_SPLIT2) {
+      bf16x8 bp[NT][2];
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) bp[t][c] = piece_at(base, C * BM + 32 * (wn * NT + t) + (lane & 31), c);
+#pragma unroll
+      for (int u = 0; u < MT; ++u)
+#pragma unroll
+        for (int k = 0; k < C; ++k) {
+          bf16x8 ap[2];
+#pragma unroll
+          for (int c = 0; c < 2; ++c) ap[c] = piece_at(base, k * BM + 32 * (MT * wm + u) + (lane & 31), c);
+#pragma unroll
+          for (int t = 0; t < NT; ++t) mma_split<2>(acc[u][k][t], bp[t], ap);
+        }
+      return;
+    }
     if constexpr (PM != PM_NATIVE) {
-      // fp32 fragments (one chunk per stage), each cut into bf16 pieces once.
-      // PM_SPLIT3 negates operand X on every other stage (the fold subtracts
+      // PM_SPLIT3: fp32 fragments (one chunk per stage), each cut into bf16
+      // pieces as it is read.  PM_SPLIT3 negates operand X on every other stage (the fold subtracts
       // those stages): the matrix core's sums carry a small bias of one sign
       // whatever the sign of the result, which then cancels in the fp64 sum
       // instead of adding up over the stages.
@@ -1111,7 +1152,11 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
   constexpr int ES = (int)sizeof(T);
   constexpr int SR = 64 / ES;               // rows per stage
   constexpr int EPP = 16 / ES;              // elements per 16-byte load
-  constexpr int RPP = ES == 2 ? 2 : 1;      // rows per piece (packed 4-byte LDS writes)
+  // PM_SPLIT2: every fp32 value is cut into its two bf16 pieces once, as the
+  // stage is stored; a 64-byte column line (16 rows) then holds the 16 high
+  // pieces followed by the 16 low pieces
+  constexpr bool SPL = PM == PM_SPLIT2;
+  constexpr int RPP = (ES == 2 || SPL) ? 2 : 1;   // rows per piece (packed 4-byte LDS writes)
   constexpr int NRP = SR / RPP;             // row pieces per stage (16)
   constexpr int NCH = 64 / (16 * ES);
   constexpr int PA = NRP * (BNn / EPP);
@@ -1209,7 +1254,21 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
       char* base = lds + stage * STAGE + (isA ? 0 : REGA);
       const uint32_t m0k = (k0 + rp * RPP < r1) ? 0xffffffffu : 0u;            // row validity masks
       const uint32_t m1k = (k0 + rp * RPP + RPP - 1 < r1) ? 0xffffffffu : 0u;
-      if (ES == 2) {
+      if constexpr (SPL) {
+        // rows 2 rp and 2 rp + 1: one word of high pieces, one of low pieces
+        const float* x0 = (const float*)&buf[i][0];
+        const float* x1 = (const float*)&buf[i][RPP - 1];
+#pragma unroll
+        for (int e = 0; e < EPP; ++e) {
+          const bf16 h0 = (bf16)x0[e], h1 = (bf16)x1[e];
+          const bf16 l0 = (bf16)(x0[e] - (float)h0), l1 = (bf16)(x1[e] - (float)h1);
+          char* line = base + dw_col(cg * EPP + e) + rp * 4;
+          *(uint32_t*)line = ((uint32_t)__builtin_bit_cast(uint16_t, h0) & m0k & 0xffffu) |
+                             (((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16) & m1k);
+          *(uint32_t*)(line + 32) = ((uint32_t)__builtin_bit_cast(uint16_t, l0) & m0k & 0xffffu) |
+                                    (((uint32_t)__builtin_bit_cast(uint16_t, l1) << 16) & m1k);
+        }
+      } else if (ES == 2) {
         const uint16_t* lo = (const uint16_t*)&buf[i][0];
         const uint16_t* hi = (const uint16_t*)&buf[i][RPP - 1];
 #pragma unroll
@@ -1242,8 +1301,24 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
           for (int b = 0; b < 2; ++b) accd[a][b] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[a], bv[b], accd[a][b], 0, 0, 0);
       }
     }
+    if constexpr (SPL) {
+      // high pieces at byte 0 of a column line, low pieces at byte 32
+      const int koff = (lane >> 5) * 16;
+      bf16x8 ap[NT][2], bp[NT][2];
 #pragma unroll
-    for (int c = 0; c < (PM == PM_F64 ? 0 : NCH); ++c) {
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          ap[t][c] = *(const bf16x8*)(base + dw_col(32 * (wm * NT + t) + (lane & 31)) + 32 * c + koff);
+          bp[t][c] = *(const bf16x8*)(base + REGA + dw_col(32 * (wn * NT + t) + (lane & 31)) + 32 * c + koff);
+        }
+#pragma unroll
+      for (int a = 0; a < NT; ++a)
+#pragma unroll
+        for (int b = 0; b < NT; ++b) mma_split<2>(acc[a][b], ap[a], bp[b]);
+    }
+#pragma unroll
+    for (int c = 0; c < (PM == PM_F64 || SPL ? 0 : NCH); ++c) {
       const int koff = c * 32 + (lane >> 5) * (8 * ES);
       frag af[NT], bf[NT];
 #pragma unroll
@@ -1293,7 +1368,17 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
 #pragma unroll
       for (int w = 0; w < 16; ++w) {
         const uint32_t v = colw[w];
-        if constexpr (ES == 2) {
+        if constexpr (SPL) {
+          // words 0-7: high pieces of rows 2w, 2w + 1; words 8-15: low pieces
+          if (w < 8) {
+            const uint32_t l = colw[w + 8];
+            const double r0 = (double)(float)__builtin_bit_cast(bf16, (uint16_t)(v & 0xffffu)) +
+                              (double)(float)__builtin_bit_cast(bf16, (uint16_t)(l & 0xffffu));
+            const double r1 = (double)(float)__builtin_bit_cast(bf16, (uint16_t)(v >> 16)) +
+                              (double)(float)__builtin_bit_cast(bf16, (uint16_t)(l >> 16));
+            part_sum += (2 * w < nr ? r0 : 0.0) + (2 * w + 1 < nr ? r1 : 0.0);
+          }
+        } else if constexpr (ES == 2) {
           const float lo = Elem<T>::to_f(__builtin_bit_cast(T, (uint16_t)(v & 0xffffu)));
           const float hi = Elem<T>::to_f(__builtin_bit_cast(T, (uint16_t)(v >> 16)));
           part_sum += (2 * w < nr ? lo : 0.0f) + (2 * w + 1 < nr ? hi : 0.0f);
