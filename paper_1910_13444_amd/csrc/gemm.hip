@@ -1826,6 +1826,11 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
           dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 31) / 32)), 1, G);
           if (a.pm == PM_SPLIT2) k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, 2, true, 0, PM_SPLIT2><<<grid, 256, 0, st>>>(a);
           else k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, 2, true, 0, PM_SPLIT3><<<grid, 256, 0, st>>>(a);
+        } else if (a.pm == PM_SPLIT2 && C == 1 && a.N >= 256 && npts >= 16384) {
+          // 128 points x 256 columns, 2 x 4 waves of 2 x 2 fragments (the
+          // fastest measured for the sensor rows at K = N = 1024)
+          dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 255) / 256)), 1, G);
+          k_gemm_nt<T, ND1, ND2, 2, 4, 2, 2, EPI, 1, true, 0, PM_SPLIT2><<<grid, 512, 0, st>>>(a);
         } else if (a.pm == PM_SPLIT2) {
           // 64 points x 64 NTM columns, 2 x 2 waves
           constexpr int BN = 64 * NTM;
@@ -2009,7 +2014,13 @@ hipError_t launch_gemm_dw(const T* dA, int64_t a_g, int64_t lda, const T* H, int
                                                                        J, partial, pdb, n_split, rows_per_split,   \
                                                                        partial64);                                 \
   } while (0)
-      if (N >= 128 && J >= 128) PIGAN_DW_PM(2, 2, 2, 256, 128);
+      if (N >= 256 && J >= 256 && pm == PM_SPLIT2) {
+        // 256 x 256, 16 waves of 64 x 64 (the fastest measured at 1024 x 1024)
+        dim3 grid((unsigned)(((N + 255) / 256) * ((J + 255) / 256)) * n_split, 1, G);
+        k_gemm_dw<T, 4, 4, 2, 1, 2, PM_SPLIT2><<<grid, 1024, 0, st>>>(dA, a_g, lda, H, h_g, ldh, R, n_value, N, J,
+                                                                     partial, pdb, n_split, rows_per_split,
+                                                                     partial64);
+      } else if (N >= 128 && J >= 128) PIGAN_DW_PM(2, 2, 2, 256, 128);
       else if (N >= 64 && J >= 64) PIGAN_DW_PM(2, 2, 1, 256, 64);
       else PIGAN_DW_PM(1, 1, 1, 64, 32);
 #undef PIGAN_DW_PM
