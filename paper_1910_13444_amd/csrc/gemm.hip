@@ -1827,10 +1827,10 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
           if (a.pm == PM_SPLIT2) k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, 2, true, 0, PM_SPLIT2><<<grid, 256, 0, st>>>(a);
           else k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, 2, true, 0, PM_SPLIT3><<<grid, 256, 0, st>>>(a);
         } else if (a.pm == PM_SPLIT2 && C == 1 && a.N >= 256 && npts >= 16384) {
-          // 128 points x 256 columns, 2 x 4 waves of 2 x 2 fragments (the
+          // 128 points x 256 columns, 4 x 4 waves of 1 x 2 fragments (the
           // fastest measured for the sensor rows at K = N = 1024)
           dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 255) / 256)), 1, G);
-          k_gemm_nt<T, ND1, ND2, 2, 4, 2, 2, EPI, 1, true, 0, PM_SPLIT2><<<grid, 512, 0, st>>>(a);
+          k_gemm_nt<T, ND1, ND2, 4, 4, 1, 2, EPI, 1, true, 0, PM_SPLIT2><<<grid, 1024, 0, st>>>(a);
         } else if (a.pm == PM_SPLIT2) {
           // 64 points x 64 NTM columns, 2 x 2 waves
           constexpr int BN = 64 * NTM;
@@ -1906,11 +1906,12 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
       }
     } else if constexpr (C == 5 && EPI == EPI_BWD) {
       if (deep) {
-        // eight waves (1 x 8), 32 points x 256 columns, 4-stage ring: each
+        // eight waves (1 x 8), 32 points x 256 columns, 3-stage ring: each
         // activation row tile is read by half as many column tiles as with
-        // 64 x 128 (6-12 % faster at K = 512 and 1024)
+        // 64 x 128 (6-12 % faster at K = 512 and 1024; 3 stages 6 % faster
+        // than 4)
         dim3 grid((unsigned)(((npts + 31) / 32) * ((a.N + 255) / 256)), 1, G);
-        k_gemm_nt<T, ND1, ND2, 1, 8, 1, 1, EPI, 2, true, 4><<<grid, 512, 0, st>>>(a);
+        k_gemm_nt<T, ND1, ND2, 1, 8, 1, 1, EPI, 2, true, 3><<<grid, 512, 0, st>>>(a);
       } else {
         // eight waves (2 x 4), 64 points x 128 columns, 3-stage ring
         dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + 127) / 128)), 1, G);
@@ -1925,9 +1926,10 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
           return hipGetLastError();
         }
       }
-      // eight waves (2 x 4), 64 points x 256 columns, 4-stage ring
+      // eight waves (2 x 4), 64 points x 256 columns, 3-stage ring (6-11 %
+      // faster than 4 stages at K = 1024, two-term forward and reverse)
       dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + 255) / 256)), 1, G);
-      k_gemm_nt<T, ND1, ND2, 2, 4, 1, 2, EPI, 1, false, 4><<<grid, 512, 0, st>>>(a);
+      k_gemm_nt<T, ND1, ND2, 2, 4, 1, 2, EPI, 1, false, 3><<<grid, 512, 0, st>>>(a);
     }
   } else {
     constexpr int BN = 64 * NTM;
