@@ -150,7 +150,7 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 // p.kx > 0 (two-term weights): operand X is kx wide and is read twice, the
 // weight rows are 2 kx wide.
 template <class T, int ND1, int ND2, int WM, int WN, int MT, int NT, int EPI, int OCC, bool DB = (OCC >= 2),
-          int NS = 0, int PM = PM_NATIVE>
+          int NS = 0, int PM = PM_NATIVE, int NB = 2>
 __global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OCC)))
 k_gemm_nt(const NtArgs<T> p) {
   constexpr int C = 1 + ND1 + ND2;
@@ -480,6 +480,31 @@ k_gemm_nt(const NtArgs<T> p) {
       st = st + 1 == NS ? 0 : st + 1;
     }
     lds_sync();
+  } else if constexpr (DB && NB > 2) {
+    // two LDS stages and a ring of NB register buffers: buffer b holds the
+    // stages kt = b (mod NB), so the global loads of stage kt + NB are issued
+    // while stage kt is multiplied.  Loads are unconditional (stage index
+    // clamped), so the compiler's waits are static counts.
+    uint4 bufs[NB][PPT];
+    const int last = nk - 1;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) gload(bufs[b], b < last ? b : last);
+    lstore(bufs[0], 0);
+    gload(bufs[0], NB < last ? NB : last);
+    lds_sync();
+    for (int k0 = 0; k0 < nk; k0 += NB) {
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const int kt = k0 + u;
+        if (kt >= nk) break;
+        if constexpr (PM == PM_F64) compute64(kt & 1); else compute(kt & 1);
+        fold();
+        __builtin_amdgcn_sched_barrier(0);
+        if (kt + 1 < nk) lstore(bufs[(u + 1) % NB], (kt + 1) & 1);
+        gload(bufs[(u + 1) % NB], kt + 1 + NB < last ? kt + 1 + NB : last);
+        lds_sync();
+      }
+    }
   } else if constexpr (DB) {
     // two LDS stages, two register buffers: the global loads of stage kt+2
     // are issued before stage kt is multiplied; one barrier per stage
@@ -1390,7 +1415,7 @@ k_gemm_dw(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __restric
     }
   };
 
-  if constexpr (OCC >= 2) {
+  if constexpr (OCC >= 2 || NB > 2) {
     // two LDS stages and a ring of NB register buffers: buffer b holds the
     // stages s = b (mod NB), so NB stages of loads are in flight while one is
     // multiplied.  Loads are unconditional (stage index clamped, rows past
@@ -1827,10 +1852,14 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
           if (a.pm == PM_SPLIT2) k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, 2, true, 0, PM_SPLIT2><<<grid, 256, 0, st>>>(a);
           else k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, 2, true, 0, PM_SPLIT3><<<grid, 256, 0, st>>>(a);
         } else if (a.pm == PM_SPLIT2 && C == 1 && a.N >= 256 && npts >= 16384) {
-          // 128 points x 256 columns, 4 x 4 waves of 1 x 2 fragments (the
-          // fastest measured for the sensor rows at K = N = 1024)
+          // 128 points x 256 columns, 4 x 4 waves of 1 x 2 fragments, a ring
+          // of 3 (forward) or 4 (reverse) register stages (the fastest
+          // measured for the sensor rows at K = N = 1024)
           dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 255) / 256)), 1, G);
-          k_gemm_nt<T, ND1, ND2, 4, 4, 1, 2, EPI, 1, true, 0, PM_SPLIT2><<<grid, 1024, 0, st>>>(a);
+          if constexpr (EPI == EPI_FWD)
+            k_gemm_nt<T, ND1, ND2, 4, 4, 1, 2, EPI, 1, true, 0, PM_SPLIT2, 3><<<grid, 1024, 0, st>>>(a);
+          else
+            k_gemm_nt<T, ND1, ND2, 4, 4, 1, 2, EPI, 1, true, 0, PM_SPLIT2, 4><<<grid, 1024, 0, st>>>(a);
         } else if (a.pm == PM_SPLIT2) {
           // 64 points x 64 NTM columns, 2 x 2 waves
           constexpr int BN = 64 * NTM;
