@@ -716,15 +716,34 @@ k_gemm_nt(const NtArgs<T> p) {
     const int64_t pt = m0 + mloc(u);
     const bool pvalid = pt < npts;
 #pragma unroll
-    for (int t = 0; t < NT; ++t)
+    for (int t = 0; t < NT; ++t) {
+      // the saved pre-activations of all four column groups of this fragment,
+      // issued together (one memory latency per fragment, not per group)
+      typedef typename std::conditional<ES == 2, uint2, float4>::type raw_t;
+      raw_t raw[4][C];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int nb = n0 + ncol(t, q);
+#pragma unroll
+        for (int k = 0; k < C; ++k) {
+          if (pvalid && nb < p.N)
+            raw[q][k] = *(const raw_t*)(p.aprev + g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + nb);
+          else
+            raw[q][k] = raw_t{};
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
         float ap[C][4];
 #pragma unroll
         for (int k = 0; k < C; ++k) {
-          if (pvalid && nb < p.N) load4<T>(p.aprev + g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + nb, ap[k]);
-          else ap[k][0] = ap[k][1] = ap[k][2] = ap[k][3] = 0.0f;
+          if constexpr (ES == 2) {
+            const T* ev = (const T*)&raw[q][k];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) ap[k][e] = Elem<T>::to_f(ev[e]);
+          } else {
+            ap[k][0] = raw[q][k].x; ap[k][1] = raw[q][k].y; ap[k][2] = raw[q][k].z; ap[k][3] = raw[q][k].w;
+          }
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -739,8 +758,9 @@ k_gemm_nt(const NtArgs<T> p) {
 #pragma unroll
           for (int k = 0; k < C; ++k) acc[u][k][t][r] = gv[k];
         }
-        __builtin_amdgcn_sched_barrier(0);
       }
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
 #pragma unroll
   for (int k = 0; k < C; ++k) stage_out(k, p.out_da);
