@@ -784,12 +784,16 @@ k_gemm_nt(const NtArgs<T> p) {
 template <int C, bool SKIP>
 constexpr int wr_blocks_per_cu() { return SKIP && C >= 5 ? 1 : 2; }
 
-template <class T, int ND1, int ND2, int EPI, bool FIRST, bool SKIP = false>
+// TWO: two-term weight rows [W_hi | W_lo] (forward, K = 2 x 128): W_hi is the
+// LDS-resident tile, each wave keeps its columns' W_lo fragments in registers
+// for the whole launch.
+template <class T, int ND1, int ND2, int EPI, bool FIRST, bool SKIP = false, bool TWO = false>
 __global__ void __launch_bounds__(256)
 __attribute__((amdgpu_waves_per_eu(wr_blocks_per_cu<1 + ND1 + ND2, SKIP>())))
 k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
   static_assert(sizeof(T) == 2, "16-bit storage only");
   static_assert(!(SKIP && FIRST), "residual blocks never start at the first layer");
+  static_assert(!TWO || EPI == EPI_FWD, "two-term weights: forward products only");
   constexpr int C = 1 + ND1 + ND2;
   constexpr int BM = 32, BN = 128, NTH = 256, ES = 2;
   constexpr int RB = 256;                          // bytes of one operand row (K = 128)
@@ -826,6 +830,13 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
     for (int i = 0; i < WP; ++i) wb[i] = *(const u32x4*)(Wb + (int64_t)(tid / SEGS + RPP * i) * p.ldw * ES + sg * 16);
 #pragma unroll
     for (int i = 0; i < WP; ++i) *(u32x4*)(wl + (tid / SEGS + RPP * i) * PITCH + sg * 16) = wb[i];
+  }
+  // the low terms of the wave's 32 weight rows, one fragment per 16-wide k chunk
+  frag wlo[TWO ? RB / 32 : 1];
+  if constexpr (TWO) {
+    const char* wrow = Wb + (int64_t)(32 * wave + (lane & 31)) * p.ldw * ES + RB;
+#pragma unroll
+    for (int c = 0; c < RB / 32; ++c) wlo[c] = *(const frag*)(wrow + c * 32 + hh * 16);
   }
 
   // first layer formed in the kernel: W1[n][0..d-1] for every unit n
@@ -1035,6 +1046,7 @@ k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
 #pragma unroll
       for (int k = 0; k < C; ++k) {
         const frag afr = *(const frag*)(xl + (k * BM + (lane & 31)) * PITCH + koff);
+        if constexpr (TWO) Elem<T>::mma(acc[k], wlo[c], afr);
         Elem<T>::mma(acc[k], bfr, afr);            // rows: columns n; cols: points
       }
     }
@@ -1902,7 +1914,9 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   }
   if constexpr (sizeof(T) == 2 && C <= 5 && EPI != EPI_DF) {
     const bool skip = a.skip || a.skip_g || a.out_gh;
-    if (nt_resident_ok((int)sizeof(T), C, a.K, a.N, npts, a.ldx, a.ldo) && !(skip && (a.fp1 || a.y))) {
+    const bool two = a.kx > 0;   // two-term weight rows: the operand is kx wide
+    if (nt_resident_ok((int)sizeof(T), C, two ? a.kx : a.K, a.N, npts, a.ldx, a.ldo) &&
+        !(skip && (a.fp1 || a.y)) && (!two || (EPI == EPI_FWD && a.K == 2 * a.kx))) {
       // persistent weight-resident kernel: two blocks per CU in total (one
       // for the five-stream skip variant)
       const int64_t ntiles = (npts + 31) / 32;
@@ -1912,6 +1926,14 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
       if (nb < 1) nb = 1;
       if (nb > ntiles) nb = ntiles;
       dim3 grid((unsigned)nb, 1, G);
+      if constexpr (EPI == EPI_FWD) {
+        if (two) {
+          if (a.fp1) k_gemm_nt_wr<T, ND1, ND2, EPI, true, false, true><<<grid, 256, 0, st>>>(a, ntiles);
+          else if (skip) k_gemm_nt_wr<T, ND1, ND2, EPI, false, true, true><<<grid, 256, 0, st>>>(a, ntiles);
+          else k_gemm_nt_wr<T, ND1, ND2, EPI, false, false, true><<<grid, 256, 0, st>>>(a, ntiles);
+          return hipGetLastError();
+        }
+      }
       if (a.fp1) k_gemm_nt_wr<T, ND1, ND2, EPI, true><<<grid, 256, 0, st>>>(a, ntiles);
       else if (skip) k_gemm_nt_wr<T, ND1, ND2, EPI, false, true><<<grid, 256, 0, st>>>(a, ntiles);
       else k_gemm_nt_wr<T, ND1, ND2, EPI, false><<<grid, 256, 0, st>>>(a, ntiles);

@@ -531,12 +531,11 @@ static pigan_status weight_grad(const T* dA, int64_t a_g, int64_t lda, const T* 
 }
 
 // whether the collocation segment of a generator's chunk runs on the resident
-// kernel (then the first and output layers are fused into the hidden GEMMs):
-// one-term weights only
+// kernel (then the first and output layers are fused into the hidden GEMMs)
 template <class T>
 static bool colloc_resident(const NetBuf& nb) {
   const int W = nb.off.W;
-  return !two_term<T>() && nb.off.L >= 2 && !nb.skip && nb.heads == 1 &&
+  return nb.off.L >= 2 && !nb.skip && nb.heads == 1 &&
          nt_resident_ok((int)sizeof(T), nb.C(), W, W, nb.n_col, W, W);
 }
 
@@ -1720,10 +1719,9 @@ static pigan_status run_gen_fwd(const pigan_mlp* net, const float* params, int d
     HIP_TRY(launch_zproj(params, off.n, in_dim, d, W, z, (int64_t)S * n_z, n_z, S, tp<float>(ws, p.zp),
                          (int64_t)S * W, G, st));
   }
-  // on the resident kernel (one-term weights) the first layer is formed
-  // inside the second layer's GEMM and the output layer rides on the last
-  // one's epilogue
-  const bool fuse_out = !two_term<T>() && L >= 2 && nt_resident_ok((int)sizeof(T), 1 + nd1 + nd2, W, W, M, W, W);
+  // on the resident kernel the first layer is formed inside the second
+  // layer's GEMM and the output layer rides on the last one's epilogue
+  const bool fuse_out = L >= 2 && nt_resident_ok((int)sizeof(T), 1 + nd1 + nd2, W, W, M, W, W);
   const int64_t x_g = x_shared ? (int64_t)P * d : M * d;
   if (!fuse_out) {
     FirstArgs<T> fa{};
