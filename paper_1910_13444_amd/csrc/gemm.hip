@@ -781,15 +781,15 @@ k_gemm_nt(const NtArgs<T> p) {
 // ---------------------------------------------------------------------------
 // one block per CU (and the whole register file) for the skip variant of
 // five streams, whose skip rows do not fit beside the prefetch otherwise
-template <int C, bool SKIP>
-constexpr int wr_blocks_per_cu() { return SKIP && C >= 5 ? 1 : 2; }
+template <int C, bool SKIP, bool TWO = false>
+constexpr int wr_blocks_per_cu() { return (SKIP || TWO) && C >= 5 ? 1 : 2; }
 
 // TWO: two-term weight rows [W_hi | W_lo] (forward, K = 2 x 128): W_hi is the
 // LDS-resident tile, each wave keeps its columns' W_lo fragments in registers
 // for the whole launch.
 template <class T, int ND1, int ND2, int EPI, bool FIRST, bool SKIP = false, bool TWO = false>
 __global__ void __launch_bounds__(256)
-__attribute__((amdgpu_waves_per_eu(wr_blocks_per_cu<1 + ND1 + ND2, SKIP>())))
+__attribute__((amdgpu_waves_per_eu(wr_blocks_per_cu<1 + ND1 + ND2, SKIP, TWO>())))
 k_gemm_nt_wr(const NtArgs<T> p, int64_t ntiles) {
   static_assert(sizeof(T) == 2, "16-bit storage only");
   static_assert(!(SKIP && FIRST), "residual blocks never start at the first layer");
@@ -1922,7 +1922,7 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
       const int64_t ntiles = (npts + 31) / 32;
       // one-stream launches (sensor rows: few tiles, small blocks) take three
       // blocks per CU
-      int64_t nb = (skip ? wr_blocks_per_cu<C, true>() : (C == 1 ? 3 : 2)) * (int64_t)cu_count() / G;
+      int64_t nb = (skip || (two && C >= 5) ? wr_blocks_per_cu<C, true>() : (C == 1 ? 3 : 2)) * (int64_t)cu_count() / G;
       if (nb < 1) nb = 1;
       if (nb > ntiles) nb = ntiles;
       dim3 grid((unsigned)nb, 1, G);
