@@ -1892,6 +1892,10 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
             k_gemm_nt<T, ND1, ND2, 4, 4, 1, 2, EPI, 1, true, 0, PM_SPLIT2, 3><<<grid, 1024, 0, st>>>(a);
           else
             k_gemm_nt<T, ND1, ND2, 4, 4, 1, 2, EPI, 1, true, 0, PM_SPLIT2, 4><<<grid, 1024, 0, st>>>(a);
+        } else if (a.pm == PM_SPLIT2 && C == 1 && a.N <= 128) {
+          // 64 points x 128 columns, 2 x 2 waves (no idle column half at N = 128)
+          dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + 127) / 128)), 1, G);
+          k_gemm_nt<T, ND1, ND2, 2, 2, 1, 2, EPI, 2, true, 0, PM_SPLIT2><<<grid, 256, 0, st>>>(a);
         } else if (a.pm == PM_SPLIT2) {
           // 64 points x 64 NTM columns, 2 x 2 waves
           constexpr int BN = 64 * NTM;
