@@ -173,10 +173,11 @@ typedef struct {
                                   pigan_train_step_grads (ENOTSUP otherwise), any value for
                                   pigan_train_step_grads_gp */
   float loss_scale;            /* static loss scale (> 0; 1 unless fp16) */
-  int32_t critic_only;         /* 0: every gradient; 1: the critic's update only -- gD and the
-                                  losses as in the full step, the generators' reverse pass
-                                  skipped and their gradient outputs neither written nor
-                                  required (may be NULL) */
+  int32_t critic_only;         /* 0: every gradient; 1: the critic's update only -- gD, L_D
+                                  and L_adv as in the full step; the generators run at the
+                                  sensors only (no collocation rows, no residual: L_pde is
+                                  reported as 0) and have no reverse pass; their gradient
+                                  outputs are neither written nor required (may be NULL) */
 } pigan_step_desc;
 
 size_t pigan_workspace_bytes(const pigan_step_desc* s);
@@ -274,10 +275,11 @@ typedef struct {
   float loss_scale;            /* static loss scale (> 0; 1 unless fp16) */
   float lambda_gp;             /* critic gradient penalty weight: 0 for pigan_trunk_step_grads,
                                   >= 0 for pigan_trunk_step_grads_gp */
-  int32_t critic_only;         /* 0: every gradient; 1: the critic's update only -- gD and the
-                                  losses as in the full step, the generators' reverse pass
-                                  skipped and their gradient outputs neither written nor
-                                  required (may be NULL) */
+  int32_t critic_only;         /* 0: every gradient; 1: the critic's update only -- gD, L_D
+                                  and L_adv as in the full step; the generators run at the
+                                  sensors only (no collocation rows, no residual: L_pde is
+                                  reported as 0) and have no reverse pass; their gradient
+                                  outputs are neither written nor required (may be NULL) */
 } pigan_trunk_desc;
 
 /* Workspace bytes for pigan_trunk_step_grads(_gp) (0 if the descriptor is invalid;
@@ -348,9 +350,10 @@ typedef struct {
   float lambda_gp;             /* critic gradient penalty weight: 0 for pigan_hier_step_grads,
                                   >= 0 for pigan_hier_step_grads_gp */
   int32_t critic_only;         /* 0: every gradient; 1: the critic's update only -- gD and the
-                                  losses as in the full step, the generators' reverse pass
-                                  skipped and their gradient outputs neither written nor
-                                  required (may be NULL) */
+                                  losses as in the full step (the critics read the generated
+                                  source, so the residual is still evaluated), no reverse pass
+                                  of the generator; its gradient outputs are neither written
+                                  nor required (may be NULL) */
 } pigan_hier_desc;
 
 /* Workspace bytes for pigan_hier_step_grads(_gp) (0 if the descriptor is invalid;
@@ -422,9 +425,10 @@ typedef struct {
   float lambda_gp;             /* critic gradient penalty weight: 0 for
                                   pigan_hier_trunk_step_grads, >= 0 for its _gp form */
   int32_t critic_only;         /* 0: every gradient; 1: the critic's update only -- gD and the
-                                  losses as in the full step, the generators' reverse pass
-                                  skipped and their gradient outputs neither written nor
-                                  required (may be NULL) */
+                                  losses as in the full step (the critics read the generated
+                                  source, so the residual is still evaluated), no reverse pass
+                                  of the generator; its gradient outputs are neither written
+                                  nor required (may be NULL) */
 } pigan_hier_trunk_desc;
 
 /* Workspace bytes for pigan_hier_trunk_step_grads(_gp) (0 if the descriptor is

@@ -560,11 +560,12 @@ static void colloc_weights(NtArgs<T>& a, void* ws, const NetBuf& nb, int l) {
   a.kx = tw == 2 ? W : 0;
 }
 
-// Forward of one generator over a chunk: sensor rows, then collocation rows.
+// Forward of one generator over a chunk: sensor rows, then (unless colloc is
+// false: a critic-only step of the paired or trunk generators) collocation rows.
 template <class T>
 static pigan_status gen_chunk_fwd(void* ws, const NetBuf& nb, const float* params, const float* xs, int64_t xs_g,
                                   const float* xc, int64_t xc_g, const float* z, int64_t z_g, int d, int n_z, int Sc,
-                                  int P, int G, hipStream_t st) {
+                                  int P, int G, hipStream_t st, bool colloc = true) {
   const int W = nb.off.W, L = nb.off.L;
   const int64_t pg = nb.off.n;
   const int64_t ags = nb.Rs * W, agc = nb.Rc * W;   // per-group element strides of the activations
@@ -605,6 +606,7 @@ static pigan_status gen_chunk_fwd(void* ws, const NetBuf& nb, const float* param
       HIP_TRY(launch_out_fwd<float>(tp<float>(ws, nb.Hs[L]), ags, W, nb.n_sen, nb.n_sen, W,
                                     params + nb.off.wout + W + 1, pg, tp<float>(ws, nb.jet2), nb.R, G, st));
   }
+  if (!colloc) return PIGAN_OK;
   // ---- collocation rows: storage type T, every jet stream
   const int C = nb.C();
   const int64_t mc = C * nb.n_col;
@@ -1027,10 +1029,13 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
     const float* zc = z + (int64_t)s0 * n_z;
     const float* xcc = xc + (int64_t)s0 * P * d;
     const NetBuf Yc = chunk_view(pl.Y, Sc, P), Uc = chunk_view(pl.U, Sc, P);
-    // generator forward passes
-    if ((r = gen_chunk_fwd<T>(ws, Yc, pY, xsG, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, G, st)) != PIGAN_OK) return r;
+    // generator forward passes (a critic-only step needs the sensor rows only:
+    // the residual penalty is a generator term)
+    const bool colloc = !s->critic_only;
+    if ((r = gen_chunk_fwd<T>(ws, Yc, pY, xsG, xs_gY, xcc, xc_g, zc, z_g, d, n_z, Sc, P, G, st, colloc)) != PIGAN_OK)
+      return r;
     if (!pl.trunk &&
-        (r = gen_chunk_fwd<T>(ws, Uc, pU, xsU, xs_gU, xcc, xc_g, zc, z_g, d, n_z, Sc, P, G, st)) != PIGAN_OK)
+        (r = gen_chunk_fwd<T>(ws, Uc, pU, xsU, xs_gU, xcc, xc_g, zc, z_g, d, n_z, Sc, P, G, st, colloc)) != PIGAN_OK)
       return r;
     // the trunk's head cotangents: the residual and the critic fill only
     // their own rows and streams (Y: value and first derivatives at the
@@ -1044,7 +1049,7 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
       HIP_TRY(launch_fill_f32(gbarU, Yc.rows, Yc.R, 0.0f, G, st));
     }
     // residual and its cotangents
-    {
+    if (colloc) {
       ResidArgs ra{};
       ra.jY = tp<float>(ws, Yc.jet); ra.jy_g = Yc.R; ra.offY = Yc.n_sen;
       ra.jU = jetU; ra.ju_g = ju_g; ra.offU = pl.trunk ? Yc.n_sen : Uc.n_sen;

@@ -165,8 +165,10 @@ class Trainer:
         return torch.rand(self.gp_shape, generator=self.gp_gen, device=self.pD.device, dtype=torch.float32)
 
     def _call(self, gen, pD, critic_only=False):
-        """One step call; critic_only skips the generators' reverse pass (their
-        gradients are then not computed: grads_g holds stale buffers)."""
+        """One step call.  critic_only skips the generators' reverse pass (their
+        gradients are then not computed: grads_g holds stale buffers) and, for
+        the paired and trunk steps, their collocation rows and the residual
+        (the call's L_pde is recorded as 0)."""
         if self.scaler is not None:
             self.desc.loss_scale = self.scaler.scale
         self.desc.critic_only = int(critic_only)
