@@ -193,30 +193,25 @@ k_gemm_nt(const NtArgs<T> p) {
   const char* Wb = (const char*)(p.Wm + g * p.w_g);
 
   // each thread moves PPT 16-byte pieces of every stage: operand row piece>>2,
-  // 16-byte segment piece&3 of its 64-byte k-slice.  Every load is
-  // unconditional, so that the compiler can count the loads in flight and
-  // wait only for the stage it stores (a load under a condition makes it
-  // wait for all of them): points past the segment end and columns past N
-  // read a clamped (valid) row, whose products are never stored, and
-  // threads without a piece read the operand's first segment and drop it.
+  // 16-byte segment piece&3 of its 64-byte k-slice
   const char* src[PPT];
-  bool isx[PPT];
+  bool valid[PPT], isx[PPT];
 #pragma unroll
   for (int i = 0; i < (NS > 0 ? 0 : PPT); ++i) {
     const int piece = tid + i * NTH;
     const int row = piece >> 2, sg = piece & 3;
-    isx[i] = true;
+    valid[i] = false;
+    isx[i] = row < C * BM;
     src[i] = Xb;
     if (piece < PIECES) {
       if (row < C * BM) {
         const int k = row / BM, pp = row % BM;
-        int64_t pt = m0 + pp;
-        if (pt > npts - 1) pt = npts - 1;
+        const int64_t pt = m0 + pp;
+        valid[i] = pt < npts;
         src[i] = Xb + (p.seg.row0 + k * p.seg.plane + pt) * p.ldx * (int64_t)ES + sg * 16;
       } else {
-        int n = n0 + row - C * BM;
-        if (n > p.N - 1) n = p.N - 1;
-        isx[i] = false;
+        const int n = n0 + row - C * BM;
+        valid[i] = n < p.N;
         src[i] = Wb + (int64_t)n * p.ldw * (int64_t)ES + sg * 16;
       }
     }
@@ -241,7 +236,7 @@ k_gemm_nt(const NtArgs<T> p) {
     const int ktx = kxs(kt);
 #pragma unroll
     for (int i = 0; i < PPT; ++i)
-      buf[i] = *(const uint4*)(src[i] + (int64_t)(isx[i] ? ktx : kt) * 64);
+      buf[i] = valid[i] ? *(const uint4*)(src[i] + (int64_t)(isx[i] ? ktx : kt) * 64) : make_uint4(0u, 0u, 0u, 0u);
   };
   // PM_SPLIT2: each fp32 value is cut into its two bf16 pieces once, as the
   // stage is stored: a 64-byte stage row (16 k) then holds the high pieces
