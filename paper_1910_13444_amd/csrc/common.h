@@ -120,8 +120,13 @@ __device__ __forceinline__ void tanh_ts(float a, float& t, float& s) {
   q = q * a2 - 17.0f / 315.0f;
   q = q * a2 + 2.0f / 15.0f;
   q = q * a2 - 1.0f / 3.0f;
-  const float small = a + (a * a2) * q;
-  t = ax < 0.125f ? small : copysignf((1.0f - e) * r, a);
+  float small = a + (a * a2) * q;
+  float big = copysignf((1.0f - e) * r, a);
+  // both branches are evaluated (a few FMAs) and selected per lane: left as a
+  // conditional, the compiler forms divergent branches around each element,
+  // which serialises the epilogues' independent tanh evaluations
+  asm("" : "+v"(small), "+v"(big));
+  t = ax < 0.125f ? small : big;
   s = (4.0f * e) * (r * r);
 }
 

@@ -193,25 +193,35 @@ k_gemm_nt(const NtArgs<T> p) {
   const char* Wb = (const char*)(p.Wm + g * p.w_g);
 
   // each thread moves PPT 16-byte pieces of every stage: operand row piece>>2,
-  // 16-byte segment piece&3 of its 64-byte k-slice
+  // 16-byte segment piece&3 of its 64-byte k-slice.  The register ring
+  // (NB > 2) loads unconditionally, so that the compiler can count the loads
+  // in flight and wait only for the stage it stores (a load under a condition
+  // makes it wait for all of them): points past the segment end and columns
+  // past N read a clamped (valid) row, whose products are never stored, and
+  // threads without a piece re-read the operand's first segment and drop it.
+  // (Elsewhere the loads stay conditional: unconditional ones there moved the
+  // staging registers of many kernels to scratch memory.)
+  constexpr bool UNCOND = DB && NB > 2;
   const char* src[PPT];
   bool valid[PPT], isx[PPT];
 #pragma unroll
   for (int i = 0; i < (NS > 0 ? 0 : PPT); ++i) {
     const int piece = tid + i * NTH;
     const int row = piece >> 2, sg = piece & 3;
-    valid[i] = false;
-    isx[i] = row < C * BM;
+    valid[i] = UNCOND;
+    isx[i] = row < C * BM || piece >= PIECES;   // a dropped re-read stays inside X's first row
     src[i] = Xb;
     if (piece < PIECES) {
       if (row < C * BM) {
         const int k = row / BM, pp = row % BM;
-        const int64_t pt = m0 + pp;
-        valid[i] = pt < npts;
+        int64_t pt = m0 + pp;
+        valid[i] = UNCOND || pt < npts;
+        if (UNCOND && pt > npts - 1) pt = npts - 1;
         src[i] = Xb + (p.seg.row0 + k * p.seg.plane + pt) * p.ldx * (int64_t)ES + sg * 16;
       } else {
-        const int n = n0 + row - C * BM;
-        valid[i] = n < p.N;
+        int n = n0 + row - C * BM;
+        valid[i] = UNCOND || n < p.N;
+        if (UNCOND && n > p.N - 1) n = p.N - 1;
         src[i] = Wb + (int64_t)n * p.ldw * (int64_t)ES + sg * 16;
       }
     }
@@ -236,7 +246,8 @@ k_gemm_nt(const NtArgs<T> p) {
     const int ktx = kxs(kt);
 #pragma unroll
     for (int i = 0; i < PPT; ++i)
-      buf[i] = valid[i] ? *(const uint4*)(src[i] + (int64_t)(isx[i] ? ktx : kt) * 64) : make_uint4(0u, 0u, 0u, 0u);
+      buf[i] = (UNCOND || valid[i]) ? *(const uint4*)(src[i] + (int64_t)(isx[i] ? ktx : kt) * 64)
+                                    : make_uint4(0u, 0u, 0u, 0u);
   };
   // PM_SPLIT2: each fp32 value is cut into its two bf16 pieces once, as the
   // stage is stored: a 64-byte stage row (16 k) then holds the high pieces
@@ -713,8 +724,11 @@ k_gemm_nt(const NtArgs<T> p) {
   // pre-activation a_k of the layer below
 #pragma unroll
   for (int u = 0; u < MT; ++u) {
-    const int64_t pt = m0 + mloc(u);
-    const bool pvalid = pt < npts;
+    // points past the segment end and columns past N read a clamped (valid)
+    // element: their results are never stored, and unconditional loads keep
+    // the loads of a fragment together, without a branch around each
+    int64_t pt = m0 + mloc(u);
+    if (pt > npts - 1) pt = npts - 1;
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       // the saved pre-activations of all four column groups of this fragment,
@@ -723,14 +737,11 @@ k_gemm_nt(const NtArgs<T> p) {
       raw_t raw[4][C];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int nb = n0 + ncol(t, q);
+        int nb = n0 + ncol(t, q);
+        if (nb >= p.N) nb = 0;
 #pragma unroll
-        for (int k = 0; k < C; ++k) {
-          if (pvalid && nb < p.N)
-            raw[q][k] = *(const raw_t*)(p.aprev + g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + nb);
-          else
-            raw[q][k] = raw_t{};
-        }
+        for (int k = 0; k < C; ++k)
+          raw[q][k] = *(const raw_t*)(p.aprev + g * p.o_g + (p.seg.row0 + k * p.seg.plane + pt) * p.ldo + nb);
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
