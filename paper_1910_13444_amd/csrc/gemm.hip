@@ -1962,7 +1962,7 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
   if (a.N <= 32) {
     dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 31) / 32)), 1, G);
     k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, (C >= 4 ? 1 : 2)><<<grid, 256, 0, st>>>(a);
-  } else if (wide_ok<T, C>() && a.K >= 256 && a.N >= 256 && !(C == 3 && EPI == EPI_BWD && a.K < 512)) {
+  } else if (wide_ok<T, C>() && a.K >= 256 && a.N >= 256) {
     // wide layers: operand stages loaded straight into an LDS ring several
     // stages ahead, larger wave tiles (fewer LDS fragment reads per MFMA) and
     // fewer L2 re-reads of each activation tile.  Tile shapes are the
@@ -1990,19 +1990,23 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
         dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 127) / 128)), 1, G);
         k_gemm_nt<T, ND1, ND2, 2, 2, 2, 2, EPI, 2, true, 3><<<grid, 256, 0, st>>>(a);
       }
-    } else if constexpr (C == 5 && EPI == EPI_BWD) {
-      if (deep) {
-        // eight waves (1 x 8), 32 points x 256 columns, 3-stage ring: each
-        // activation row tile is read by half as many column tiles as with
-        // 64 x 128 (6-12 % faster at K = 512 and 1024; 3 stages 6 % faster
-        // than 4)
-        dim3 grid((unsigned)(((npts + 31) / 32) * ((a.N + 255) / 256)), 1, G);
-        k_gemm_nt<T, ND1, ND2, 1, 8, 1, 1, EPI, 2, true, 3><<<grid, 512, 0, st>>>(a);
-      } else {
-        // eight waves (2 x 4), 64 points x 128 columns, 3-stage ring
-        dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + 127) / 128)), 1, G);
-        k_gemm_nt<T, ND1, ND2, 2, 4, 1, 1, EPI, 2, true, 3><<<grid, 512, 0, st>>>(a);
+    } else if constexpr ((C == 5 || C == 3) && EPI == EPI_BWD) {
+      if constexpr (C == 3) {
+        if (deep) {
+          // eight waves (2 x 4), 64 points x 256 columns, 3-stage ring
+          dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + 255) / 256)), 1, G);
+          k_gemm_nt<T, ND1, ND2, 2, 4, 1, 2, EPI, 1, false, 3><<<grid, 512, 0, st>>>(a);
+          return hipGetLastError();
+        }
       }
+      // four waves (1 x 4), 32 points x 128 columns, 3-stage ring: two blocks
+      // per CU, so that one block's epilogue (the jet carry, VALU work a third
+      // to three quarters as long as its products) runs beside the other's
+      // products (five streams: 8-10 % faster than eight waves of 32 x 256 or
+      // 64 x 128 at K = 1024 and 256; three streams at K = 256: 15 % faster
+      // than the register-staged 64 x 128 tile)
+      dim3 grid((unsigned)(((npts + 31) / 32) * ((a.N + 127) / 128)), 1, G);
+      k_gemm_nt<T, ND1, ND2, 1, 4, 1, 1, EPI, 2, true, 3><<<grid, 256, 0, st>>>(a);
     } else {
       if constexpr (C == 3 && EPI == EPI_FWD) {
         if (!deep) {
