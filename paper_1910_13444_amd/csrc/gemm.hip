@@ -249,11 +249,12 @@ k_gemm_nt(const NtArgs<T> p) {
       buf[i] = (UNCOND || valid[i]) ? *(const uint4*)(src[i] + (int64_t)(isx[i] ? ktx : kt) * 64)
                                     : make_uint4(0u, 0u, 0u, 0u);
   };
-  // PM_SPLIT2: each fp32 value is cut into its two bf16 pieces once, as the
-  // stage is stored: a 64-byte stage row (16 k) then holds the high pieces
-  // in segments 0-1 and the low pieces in segments 2-3, i.e. the layout of a
-  // 16-bit stage whose first 16-wide chunk is the high part and second the
-  // low part
+  // PM_SPLIT2: each fp32 value of operand X is cut into its two bf16 pieces
+  // once, as the stage is stored: a 64-byte stage row (16 k) then holds the
+  // high pieces in segments 0-1 and the low pieces in segments 2-3, i.e. the
+  // layout of a 16-bit stage whose first 16-wide chunk is the high part and
+  // second the low part.  The weight rows arrive in that layout already (the
+  // weight copies are split once per step), and are stored as loaded.
   auto lstore = [&](const uint4* buf, int stage) {
     char* base = lds + stage * STAGE;
 #pragma unroll
@@ -261,7 +262,7 @@ k_gemm_nt(const NtArgs<T> p) {
       const int piece = tid + i * NTH;
       if (piece >= PIECES) continue;
       const int row = piece >> 2, sg = piece & 3;
-      if constexpr (PM == PM_SPLIT2) {
+      if (PM == PM_SPLIT2 && row < C * BM) {
         const float* v = (const float*)&buf[i];
         bf16 hi[4], lo[4];
 #pragma unroll

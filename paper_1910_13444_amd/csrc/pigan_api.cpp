@@ -785,22 +785,31 @@ static pigan_status cast_gen_weights(void* ws, const NetBuf& nb, const float* pa
     } else {
       HIP_TRY(launch_cast<T>(src, nb.off.n, W, W, W, tp<T>(ws, nb.wc) + o, tp<T>(ws, nb.wcT) + o, dg, G, st));
     }
-    HIP_TRY(launch_cast<float>(src, nb.off.n, W, W, W, tp<float>(ws, nb.ws) + o, tp<float>(ws, nb.wsT) + o, dg, G,
+    // the sensor rows' copies: pre-split for the split products
+    if constexpr (adv_pm<T>() == PM_SPLIT2)
+      HIP_TRY(launch_cast_pair(src, nb.off.n, W, W, W, tp<float>(ws, nb.ws) + o, tp<float>(ws, nb.wsT) + o, dg, G,
                                st));
+    else
+      HIP_TRY(launch_cast<float>(src, nb.off.n, W, W, W, tp<float>(ws, nb.ws) + o, tp<float>(ws, nb.wsT) + o, dg, G,
+                                 st));
   }
   return PIGAN_OK;
 }
 
 // the critic's padded first-layer weights and their transpose, and the
-// hidden layers' weights and transposes (fp32 copies with aligned rows)
+// hidden layers' weights and transposes (fp32 copies with aligned rows;
+// pair: pre-split for the split products)
 static pigan_status cast_disc_weights(void* ws, const DiscBuf& D, const float* pD, int WD, int LD, int n_in, int G,
-                                      hipStream_t st) {
-  HIP_TRY(launch_cast<float>(pD + D.off.w[1], D.off.n, WD, n_in, D.Kp, tp<float>(ws, D.w1), tp<float>(ws, D.w1T),
-                             (int64_t)WD * D.Kp, G, st));
+                                      hipStream_t st, bool pair) {
+  auto cast = [&](const float* src, int N, int K, int Kp, float* dst, float* dstT, int64_t d_g) {
+    return pair ? launch_cast_pair(src, D.off.n, N, K, Kp, dst, dstT, d_g, G, st)
+                : launch_cast<float>(src, D.off.n, N, K, Kp, dst, dstT, d_g, G, st);
+  };
+  HIP_TRY(cast(pD + D.off.w[1], WD, n_in, D.Kp, tp<float>(ws, D.w1), tp<float>(ws, D.w1T), (int64_t)WD * D.Kp));
   const int64_t dgl = (int64_t)std::max(LD - 1, 1) * WD * WD;
   for (int l = 2; l <= LD; ++l)
-    HIP_TRY(launch_cast<float>(pD + D.off.w[l], D.off.n, WD, WD, WD, tp<float>(ws, D.wc) + (size_t)(l - 2) * WD * WD,
-                               tp<float>(ws, D.wcT) + (size_t)(l - 2) * WD * WD, dgl, G, st));
+    HIP_TRY(cast(pD + D.off.w[l], WD, WD, WD, tp<float>(ws, D.wc) + (size_t)(l - 2) * WD * WD,
+                 tp<float>(ws, D.wcT) + (size_t)(l - 2) * WD * WD, dgl));
   return PIGAN_OK;
 }
 
@@ -1014,7 +1023,7 @@ static pigan_status run_step(const pigan_step_desc* s, const StepPlan& pl, const
     if (pl.trunk)   // the trunk sees both sensor sets: locations [Y sensors ; u sensors]
       HIP_TRY(launch_concat_rows(xsY, (int64_t)s->n_sY * d, s->n_sY, xsU, (int64_t)s->n_sU * d, s->n_sU, d,
                                  tp<float>(ws, pl.Y.xsc), (int64_t)(s->n_sY + s->n_sU) * d, G, st));
-    if ((r = cast_disc_weights(ws, D, pD, WD, LD, n_in, G, st)) != PIGAN_OK) return r;
+    if ((r = cast_disc_weights(ws, D, pD, WD, LD, n_in, G, st, adv_pm<T>() == PM_SPLIT2)) != PIGAN_OK) return r;
   }
 
   const int64_t xs_gU = (int64_t)s->n_sU * d;
@@ -1154,7 +1163,7 @@ static pigan_status run_hier(const pigan_step_desc* s, const StepPlan& pl, const
     if (pl.trunk)   // the trunk sees both sensor sets: locations [Y sensors ; u sensors]
       HIP_TRY(launch_concat_rows(xsY, (int64_t)s->n_sY * d, s->n_sY, xsU, (int64_t)s->n_sU * d, s->n_sU, d,
                                  tp<float>(ws, pl.Y.xsc), (int64_t)(s->n_sY + s->n_sU) * d, 1, st));
-    if ((r = cast_disc_weights(ws, D, pD, WD, LD, n_in, GD, st)) != PIGAN_OK) return r;
+    if ((r = cast_disc_weights(ws, D, pD, WD, LD, n_in, GD, st, adv_pm<T>() == PM_SPLIT2)) != PIGAN_OK) return r;
   }
   const int n_s = s->n_sY + s->n_sU;
   const float* xsG = pl.trunk ? tp<float>(ws, pl.Y.xsc) : xsY;
@@ -1856,12 +1865,15 @@ static pigan_status run_disc_fwd(const pigan_mlp* net, const float* params, cons
   const int64_t actg = (int64_t)B * W;
   {
     ProfScope ps(st, "misc", 0.0, 0.0);
-    HIP_TRY(launch_cast<float>(params + off.w[1], off.n, W, n_in, p.Kp, tp<float>(ws, p.w1), nullptr,
-                               (int64_t)W * p.Kp, G, st));
+    // weight copies (pre-split for the split products)
+    auto cast = [&](const float* src, int N, int K, int Kp, float* dst, int64_t d_g) {
+      return adv_pm<T>() == PM_SPLIT2 ? launch_cast_pair(src, off.n, N, K, Kp, dst, nullptr, d_g, G, st)
+                                      : launch_cast<float>(src, off.n, N, K, Kp, dst, nullptr, d_g, G, st);
+    };
+    HIP_TRY(cast(params + off.w[1], W, n_in, p.Kp, tp<float>(ws, p.w1), (int64_t)W * p.Kp));
     const int64_t dg = (int64_t)std::max(L - 1, 1) * W * W;
     for (int l = 2; l <= L; ++l)
-      HIP_TRY(launch_cast<float>(params + off.w[l], off.n, W, W, W, tp<float>(ws, p.wc) + (size_t)(l - 2) * W * W,
-                                 nullptr, dg, G, st));
+      HIP_TRY(cast(params + off.w[l], W, W, W, tp<float>(ws, p.wc) + (size_t)(l - 2) * W * W, dg));
     HIP_TRY(launch_snap_fill<float>(nullptr, 0, nullptr, 0, 0, 0, 0, snap, (int64_t)B * n_in, B, n_in,
                                     tp<float>(ws, p.X0), (int64_t)B * p.Kp, p.Kp, G, st));
   }

@@ -132,6 +132,9 @@ hipError_t launch_zero(double* acc, int n, int32_t* flag, hipStream_t st);
 template <class T>
 hipError_t launch_cast(const float* src, int64_t s_g, int N, int K, int Kp, T* dst, T* dstT, int64_t d_g, int G,
                        hipStream_t st);
+// split-product weight copies (pair-blocked bf16 pieces in fp32-pitch rows)
+hipError_t launch_cast_pair(const float* src, int64_t s_g, int N, int K, int Kp, float* dst, float* dstT, int64_t d_g,
+                            int G, hipStream_t st);
 // two-term weights [hi | lo] per row (16-bit storage), rows 2 K wide
 template <class T>
 hipError_t launch_cast2(const float* src, int64_t s_g, int N, int K, T* dst, int64_t d_g, int G, hipStream_t st);

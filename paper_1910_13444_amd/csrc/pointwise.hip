@@ -1015,6 +1015,46 @@ k_cast_tr(const float* __restrict__ src, int64_t s_g, int N, int K, int Kp, T* _
   }
 }
 
+// split-product weight copies: fp32 src [N][K] -> dst [N][Kp] and dstT
+// [Kp][N] with every 16-element block of a row stored as its 16 high bf16
+// pieces followed by its 16 low pieces (hi = RNE(w), lo = RNE(w - hi)): the
+// rows keep the fp32 byte pitch, and a 64-byte k-slice of a row is exactly
+// the split layout the split-product GEMM stages in LDS (padding: zeros)
+__device__ __forceinline__ void pair_put(bf16* row, int k, float v) {
+  const bf16 hi = (bf16)v;
+  const bf16 lo = (bf16)(v - (float)hi);
+  row[32 * (k >> 4) + (k & 15)] = hi;
+  row[32 * (k >> 4) + 16 + (k & 15)] = lo;
+}
+
+__global__ void __launch_bounds__(256)
+k_cast_pair(const float* __restrict__ src, int64_t s_g, int N, int K, int Kp, float* __restrict__ dst,
+            float* __restrict__ dstT, int64_t d_g) {
+  __shared__ float tile[32][33];
+  const int g = blockIdx.z;
+  const int k0 = blockIdx.x * 32, n0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  bf16* d = dst ? (bf16*)(dst + g * d_g) : nullptr;
+  bf16* dT = dstT ? (bf16*)(dstT + g * d_g) : nullptr;
+#pragma unroll
+  for (int r = ty; r < 32; r += 8) {
+    const int n = n0 + r, k = k0 + tx;
+    float v = 0.0f;
+    if (n < N && k < Kp) {
+      v = k < K ? src[g * s_g + (int64_t)n * K + k] : 0.0f;
+      if (dst) pair_put(d + (int64_t)n * 2 * Kp, k, v);
+    }
+    tile[r][tx] = v;
+  }
+  if (!dstT) return;
+  __syncthreads();
+#pragma unroll
+  for (int r = ty; r < 32; r += 8) {
+    const int k = k0 + r, n = n0 + tx;
+    if (k < Kp && n < N) pair_put(dT + (int64_t)k * 2 * N, n, tile[tx][r]);
+  }
+}
+
 // two-term weights: dst[n] = [hi(W[n][:]) | lo(W[n][:])] (2 K wide), with
 // hi = W rounded to the storage type and lo = W - hi rounded likewise
 template <class T>
@@ -1322,6 +1362,14 @@ hipError_t launch_cast(const float* src, int64_t s_g, int N, int K, int Kp, T* d
                                                                                                 dst, dstT, d_g);
   else
     k_cast<T><<<dim3(nblk((int64_t)N * Kp, 256), 1, G), 256, 0, st>>>(src, s_g, N, K, Kp, dst, dstT, d_g);
+  return hipGetLastError();
+}
+
+hipError_t launch_cast_pair(const float* src, int64_t s_g, int N, int K, int Kp, float* dst, float* dstT, int64_t d_g,
+                            int G, hipStream_t st) {
+  if (Kp % 16 != 0 || (dstT && N % 16 != 0)) return hipErrorInvalidValue;   // whole 16-element blocks per row
+  k_cast_pair<<<dim3((unsigned)((Kp + 31) / 32), (unsigned)((N + 31) / 32), G), 256, 0, st>>>(src, s_g, N, K, Kp, dst,
+                                                                                            dstT, d_g);
   return hipGetLastError();
 }
 
