@@ -1897,17 +1897,18 @@ hipError_t nt_dispatch_tile(const NtArgs<T>& a, int G, hipStream_t st) {
           else k_gemm_nt<T, ND1, ND2, 4, 1, 1, 1, EPI, 2, true, 0, PM_SPLIT3><<<grid, 256, 0, st>>>(a);
         } else if (a.pm == PM_SPLIT2 && C == 1 && a.N >= 256 && npts >= 16384) {
           // 128 points x 256 columns, 4 x 4 waves of 1 x 2 fragments, a ring
-          // of 3 (forward) or 4 (reverse) register stages (the fastest
-          // measured for the sensor rows at K = N = 1024)
-          dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 255) / 256)), 1, G);
-          if constexpr (EPI == EPI_FWD)
+          // of 3 register stages (the fastest measured for the sensor rows
+          // at K = N = 1024)
+          if constexpr (C == 1) {
+            dim3 grid((unsigned)(((npts + 127) / 128) * ((a.N + 255) / 256)), 1, G);
             k_gemm_nt<T, ND1, ND2, 4, 4, 1, 2, EPI, 1, true, 0, PM_SPLIT2, 3><<<grid, 1024, 0, st>>>(a);
-          else
-            k_gemm_nt<T, ND1, ND2, 4, 4, 1, 2, EPI, 1, true, 0, PM_SPLIT2, 4><<<grid, 1024, 0, st>>>(a);
+          }
         } else if (a.pm == PM_SPLIT2 && C == 1 && a.N <= 128) {
           // 64 points x 128 columns, 2 x 2 waves (no idle column half at N = 128)
-          dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + 127) / 128)), 1, G);
-          k_gemm_nt<T, ND1, ND2, 2, 2, 1, 2, EPI, 2, true, 0, PM_SPLIT2><<<grid, 256, 0, st>>>(a);
+          if constexpr (C == 1) {
+            dim3 grid((unsigned)(((npts + 63) / 64) * ((a.N + 127) / 128)), 1, G);
+            k_gemm_nt<T, ND1, ND2, 2, 2, 1, 2, EPI, 2, true, 0, PM_SPLIT2><<<grid, 256, 0, st>>>(a);
+          }
         } else if (a.pm == PM_SPLIT2) {
           // 64 points x 64 NTM columns, 2 x 2 waves
           constexpr int BN = 64 * NTM;
