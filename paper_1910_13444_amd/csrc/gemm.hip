@@ -666,7 +666,9 @@ k_gemm_nt(const NtArgs<T> p) {
         }
     lds_sync();
 #pragma unroll
-    for (int i = tid; i < CHUNKS; i += NTH) {
+    for (int it = 0; it < (CHUNKS + NTH - 1) / NTH; ++it) {
+      const int i = tid + it * NTH;
+      if (CHUNKS % NTH != 0 && i >= CHUNKS) break;
       const int row = i / CPR, ch = i % CPR;
       const int64_t ptr = m0 + row;
       const int n = n0 + ch * (16 / ES);
@@ -686,8 +688,9 @@ k_gemm_nt(const NtArgs<T> p) {
       for (int t = 0; t < NT; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
+          // columns past N take the last bias (their results are never stored)
           const int n = n0 + ncol(t, r >> 2) + (r & 3);
-          if (p.bias && n < p.N) acc[u][0][t][r] += p.bias[g * p.b_g + n];
+          if (p.bias) acc[u][0][t][r] += p.bias[g * p.b_g + (n < p.N ? n : p.N - 1)];
         }
     if (p.out_a) {
 #pragma unroll
