@@ -1562,6 +1562,29 @@ __device__ __forceinline__ u32x2 lds_read_tr(const char* p) {
   }
 }
 
+// The same transposing read issued as an instruction the compiler does not
+// model.  Stages filled by LDS DMA (global_load_lds) are guarded by explicit
+// vmcnt waits and barriers; with the intrinsic, the compiler cannot tell the
+// DMA targets apart from the stage being read and drains every DMA in flight
+// (vmcnt(0)) before each stage's reads, which leaves nothing prefetched.  The
+// caller waits for these reads itself (lgkm_wait below).
+__device__ __forceinline__ u32x2 lds_read_tr_raw(const char* p) {
+  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+  u32x2 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(a));
+  return r;
+}
+
+// s_waitcnt lgkmcnt(N) that the values read before it flow through, so no
+// use of them is scheduled ahead of the wait
+template <int N, int K>
+__device__ __forceinline__ void lgkm_wait(u32x4 (&v)[K]) {
+  static_assert(N >= 0 && N <= 15, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+#pragma unroll
+  for (int i = 0; i < K; ++i) asm volatile("" : "+v"(v[i]));
+}
+
 __host__ __device__ constexpr int dw_tr_pitch(int row_bytes) {
   // smallest pitch >= row_bytes (multiple of 64 bytes) with pitch/4 = 16 or 48 mod 64
   return (row_bytes / 4) % 64 == 16 || (row_bytes / 4) % 64 == 48 ? row_bytes
@@ -1689,6 +1712,73 @@ k_gemm_dw_tr(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __rest
     const u32x4 w = {lo.x, lo.y, hi.x, hi.y};
     return __builtin_bit_cast(frag, w);
   };
+  // DMA stages: raw transposing reads of the fragments.  Four-wave blocks
+  // read both 16-row chunks up front and start the first chunk's products
+  // once its reads have landed; larger blocks (which would lose occupancy to
+  // the extra registers) read one chunk at a time.
+  auto frag_raw = [&](const char* region, int pitch, int c, int colblk) {
+    const int byte = (colblk + 16 * (grp & 1) + 4 * qq4) * 2;
+    const char* p0 = region + (c * 16 + kb + rr) * pitch + (((byte >> 4) ^ (4 * rr)) << 4) + (byte & 15);
+    const u32x2 lo = lds_read_tr_raw(p0);
+    const u32x2 hi = lds_read_tr_raw(p0 + 4 * pitch);
+    return u32x4{lo.x, lo.y, hi.x, hi.y};
+  };
+  auto compute_dma = [&](int stage, int64_t k0) {
+    static_assert(SR == 32, "two 16-row chunks per stage");
+    const char* base = lds + stage * DSTAGE;
+    const char* bbase = base + SR * RBA;
+    constexpr bool AHEAD = NTH <= 256;
+    u32x4 w[2][2 * NT];   // chunk c: A fragments 0..NT-1, then B fragments
+    auto read_chunk = [&](int c) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        w[c][t] = frag_raw(base, RBA, c, 32 * (wm * NT + t));
+        w[c][NT + t] = frag_raw(bbase, RBB, c, 32 * (wn * NT + t));
+      }
+    };
+    read_chunk(0);
+    if constexpr (AHEAD) read_chunk(1);
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      if (c == 1 && !AHEAD) read_chunk(1);
+      if (c == 0 && AHEAD) lgkm_wait<4 * NT>(w[0]);   // the second chunk's 4 NT reads may still be in flight
+      else lgkm_wait<0>(w[c]);
+      frag af[NT], bf[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        af[t] = __builtin_bit_cast(frag, w[c][t]);
+        bf[t] = __builtin_bit_cast(frag, w[c][NT + t]);
+      }
+      // the stages hold clamped copies of the last row past R: their dA
+      // elements (rows k0 + 16 c + kb + e of this lane) contribute zero
+      if (k0 + SR > r1) {
+        const int64_t rw0 = k0 + c * 16 + kb;
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (rw0 + e >= r1) af[t][e] = Elem<T>::from_f(0.0f);
+      }
+#pragma unroll
+      for (int a = 0; a < NT; ++a)
+#pragma unroll
+        for (int b = 0; b < NT; ++b) Elem<T>::mma(acc[a][b], af[a], bf[b]);
+      if (want_db && k0 + c * 16 < rv) {
+        const int64_t rw0 = k0 + c * 16 + kb;
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) dbp[t] += rw0 + e < rv ? Elem<T>::to_f(af[t][e]) : 0.0f;
+      }
+    }
+    if (want_db) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        dbacc[t] += (double)dbp[t];
+        dbp[t] = 0.0f;
+      }
+    }
+  };
   auto compute = [&](int stage, int64_t k0) {
     const char* base = lds + stage * (NS > 0 ? DSTAGE : STAGE);
     const char* bbase = base + (NS > 0 ? SR * RBA : REGA);
@@ -1727,10 +1817,11 @@ k_gemm_dw_tr(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __rest
     // operand (RB = its row bytes), lane l at byte 16 l (physical segment
     // l % (RB / 16) of its row, holding the logical segment of that index
     // ^ 4 (row & 3)).  A stage is GA such groups of A rows and GB of B rows,
-    // dealt to the waves round-robin.  A stage that reaches past row R (the
-    // last one, at most) is loaded through registers instead, with the rows
-    // past R zeroed; its loads wait for every earlier one, so the immediate
-    // vmcnt counts below stay conservative.
+    // dealt to the waves round-robin.  Rows past R (in the last stage, at
+    // most) load a clamped row; compute() zeroes their dA elements.  Every
+    // stage is a DMA stage, so the waits below are the only ones on the
+    // ring (a register-loaded stage made the compiler drain every load in
+    // flight before each stage's LDS reads).
     constexpr int GA = SR * RBA / 1024, GB = SR * RBB / 1024;
     constexpr int NG = GA + GB;
     constexpr int NW = NTH / 64;
@@ -1751,27 +1842,19 @@ k_gemm_dw_tr(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __rest
       int col = (isA ? n0 : j0) + sg * 8;
       const int lim = isA ? N : J;
       if (col >= lim) col = lim - 8;
-      dsrc[i] = (isA ? A : B) + (int64_t)row * (isA ? lda : ldh) + col;
+      dsrc[i] = (isA ? A : B) + col;
       dld[i] = isA ? lda : ldh;
       drow[i] = row;
     }
     auto issue = [&](int sc, int buf) {
       const int64_t k0 = krow(sc);
       char* dst = lds + buf * DSTAGE;
-      if (k0 + SR <= r1) {
 #pragma unroll
-        for (int i = 0; i < GPW; ++i)
-          __builtin_amdgcn_global_load_lds((const void*)(dsrc[i] + k0 * dld[i]),
-                                           (lds_ptr_t)(dst + (wv + i * NW) * 1024), 16, 0, 0);
-      } else {
-        u32x4 v[GPW];
-#pragma unroll
-        for (int i = 0; i < GPW; ++i) {
-          const bool ok = k0 + drow[i] < r1;
-          v[i] = ok ? *(const u32x4*)(dsrc[i] + k0 * dld[i]) : u32x4{0u, 0u, 0u, 0u};
-        }
-#pragma unroll
-        for (int i = 0; i < GPW; ++i) *(u32x4*)(dst + (wv + i * NW) * 1024 + lane * 16) = v[i];
+      for (int i = 0; i < GPW; ++i) {
+        int64_t gr = k0 + drow[i];
+        if (gr > r1 - 1) gr = r1 - 1;
+        __builtin_amdgcn_global_load_lds((const void*)(dsrc[i] + gr * dld[i]),
+                                         (lds_ptr_t)(dst + (wv + i * NW) * 1024), 16, 0, 0);
       }
     };
 #pragma unroll
@@ -1792,7 +1875,7 @@ k_gemm_dw_tr(const T* __restrict__ dA, int64_t a_g, int64_t lda, const T* __rest
       }
       lds_sync();
       if (sc + NS - 1 < nst) issue(sc + NS - 1, stg == 0 ? NS - 1 : stg - 1);
-      compute(stg, krow(sc));
+      compute_dma(stg, krow(sc));
       stg = stg + 1 == NS ? 0 : stg + 1;
     }
   } else {
