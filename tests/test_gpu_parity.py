@@ -145,6 +145,11 @@ STEP_CASES = {
     "c4_groups_S2_bf16": (configs.C4.with_(S=2, P=96, B_r=2), {}),
     "c3_S2_bf16": (configs.C3.with_(S=2, P=256, B_r=2), {}),
     "c5_S2_bf16": (configs.C5.with_(S=2, P=128, B_r=2), {}),
+    # ragged collocation rows (R not a multiple of the 32-row weight-gradient
+    # stage, points not a multiple of the 32-point reverse tile) at widths
+    # 512 and 256, whose weight gradients take the 256 x 256 and 128 x 256 tiles
+    "c3_S2_ragged_bf16": (configs.C3.with_(S=2, P=250, B_r=2), {}),
+    "c4_groups_S2_ragged_bf16": (configs.C4.with_(S=2, P=100, B_r=2), {}),
     "c2_S3_ragged_bf16_f": (configs.C2.with_(S=3, P=1000, B_r=3), dict(f_array=True)),
     "c3_S2_fp32": (configs.C3.with_(S=2, P=256, B_r=2, dtype="fp32"), {}),
     "c4_groups_S2_fp32": (configs.C4.with_(S=2, P=96, B_r=2, dtype="fp32"), {}),
