@@ -504,9 +504,13 @@ k_gemm_nt(const NtArgs<T> p) {
     lstore(bufs[0], 0);
     gload(bufs[0], NB < last ? NB : last);
     lds_sync();
-    for (int k0 = 0; k0 < nk; k0 += NB) {
+    // UR rounds of the ring per loop pass: the compiler drains every load in
+    // flight once per pass (its wait analysis does not carry the ring across
+    // the back edge), so longer passes drain less often
+    constexpr int UR = 4;
+    for (int k0 = 0; k0 < nk; k0 += NB * UR) {
 #pragma unroll
-      for (int u = 0; u < NB; ++u) {
+      for (int u = 0; u < NB * UR; ++u) {
         const int kt = k0 + u;
         if (kt >= nk) break;
         if constexpr (PM == PM_F64) compute64(kt & 1); else compute(kt & 1);
